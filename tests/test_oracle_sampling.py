@@ -1,0 +1,149 @@
+"""Oracle pins for minimal variance sampling (Sec. 2.4, Eq. 9; Sec. 3.4,
+Alg. 7) and for the exact integer gradient sums.  CPU only."""
+from fractions import Fraction
+import math
+
+import numpy as np
+import pytest
+
+
+def phi(keys, T):
+    """sum_i min(1, a_i / T), exactly."""
+    return sum(Fraction(1) if a >= T else Fraction(int(a), T) for a in keys)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_threshold_is_least_T_with_expected_count_at_most_K(orc, seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 9))
+    keys = rng.integers(0, 40, n).astype(np.int64)
+    if seed % 3 == 0:
+        keys[: n // 2] = 0
+    K = int(rng.integers(1, n + 1))
+    T = orc.mvs_threshold(keys, K)
+    # brute force over every candidate T with exact rationals
+    brute = next(t for t in range(1, 10**6) if phi(keys, t) <= K)
+    assert T == brute
+
+
+def test_threshold_minimality_at_scale(orc):
+    rng = np.random.default_rng(1)
+    keys = (rng.exponential(size=2000) * 2**30).astype(np.int64)
+    K = 200
+    T = orc.mvs_threshold(keys, K)
+    assert phi(keys, T) <= K < phi(keys, T - 1)
+
+
+def test_all_zero_keys_give_empty_sample(orc):
+    keys = np.zeros(10, np.int64)
+    T = orc.mvs_threshold(keys, 3)
+    assert T == 1
+    assert not orc.mvs_select(keys, T, 0, 0).any()
+
+
+def test_equal_keys_reduce_to_uniform_sampling(orc):
+    # with every a_i equal, p_i = a/T* = K/n: plain uniform subsampling (SGB)
+    n, K = 1000, 100
+    keys = np.full(n, 12345, np.int64)
+    T = orc.mvs_threshold(keys, K)
+    assert phi(keys, T) == K
+    assert Fraction(12345, T) == Fraction(K, n)
+
+
+def test_selection_uses_philox_first_word(orc):
+    rng = np.random.default_rng(2)
+    keys = rng.integers(0, 1000, 500).astype(np.int64)
+    T, seed, it, off = 700, 17, 3, 1000
+    keep = orc.mvs_select(keys, T, seed, it, off)
+    for i in range(500):
+        row = off + i
+        U = int(np.random.Philox(counter=np.array([row - 1, it, 0, 0], np.uint64),
+                                 key=np.array([seed, 0], np.uint64)).random_raw(1)[0])
+        want = keys[i] >= T or U * T < int(keys[i]) * 2**64
+        assert keep[i] == want
+
+
+def test_inverse_probability_weights_are_unbiased(orc):
+    # E[keep_i * w_i] = P(U*T < a*2^64) * T/a = ceil(a*2^64/T)/2^64 * T/a ~ 1
+    rng = np.random.default_rng(3)
+    gp = np.stack([rng.normal(size=3000), rng.uniform(0.05, 0.25, 3000)], 1).astype(np.float32)
+    keys, _ = orc.mvs_keys(gp, 1.0)
+    K = orc.mvs_target(0.1, len(keys))
+    T = orc.mvs_threshold(keys, K)
+    exp_g = exp_h = Fraction(0)
+    for a, (g, h) in zip(keys.tolist(), gp.tolist()):
+        if a == 0:
+            continue
+        p = Fraction(1) if a >= T else Fraction(-(-a * 2**64 // T), 2**64)
+        w = orc.mvs_weight(a, T)
+        exp_g += p * Fraction(w) * Fraction(g)
+        exp_h += p * Fraction(w) * Fraction(h)
+    tot_g = sum(Fraction(g) for g in gp[:, 0].tolist() if True)
+    tot_h = sum(Fraction(h) for h in gp[:, 1].tolist())
+    assert abs(float(exp_g - tot_g)) <= 1e-12 * float(np.abs(gp[:, 0]).sum())
+    assert abs(float(exp_h - tot_h)) <= 1e-12 * float(gp[:, 1].sum())
+    # the expected sample size is K
+    assert abs(float(sum(Fraction(1) if a >= T else Fraction(-(-a * 2**64 // T), 2**64)
+                         for a in keys.tolist())) - K) < 1.0
+
+
+def test_monte_carlo_over_seeds(orc):
+    rng = np.random.default_rng(4)
+    n = 400
+    gp = np.stack([rng.normal(size=n), np.full(n, 0.25)], 1).astype(np.float32)
+    keys, _ = orc.mvs_keys(gp, 1.0)
+    K = orc.mvs_target(0.2, n)
+    T = orc.mvs_threshold(keys, K)
+    w = np.array([orc.mvs_weight(a, T) if a else 0.0 for a in keys])
+    totals, counts = [], []
+    for s in range(2000):
+        keep = orc.mvs_select(keys, T, s, 0)
+        totals.append(float((gp[keep, 0].astype(np.float64) * w[keep]).sum()))
+        counts.append(int(keep.sum()))
+    totals = np.array(totals)
+    true = float(gp[:, 0].astype(np.float64).sum())
+    se = totals.std() / math.sqrt(len(totals))
+    assert abs(totals.mean() - true) < 4 * se + 1e-9
+    assert abs(np.mean(counts) - K) < 4 * np.std(counts) / math.sqrt(len(counts)) + 1e-9
+
+
+def test_keys_scale_and_zero_gradient_rows(orc):
+    gp = np.array([[0.0, 0.0], [3.0, 4.0], [-1.5, 2.0]], np.float32)
+    keys, e = orc.mvs_keys(gp, 1.0)
+    # r = (0, 5, 2.5); max 5 < 2^3, L = ceil(log2 3) = 2, e = 62 - 3 - 2
+    assert e == 57
+    assert keys.tolist() == [0, 5 * 2**57, int(2.5 * 2**57)]
+
+
+def test_mvs_lambda_enters_keys(orc):
+    gp = np.array([[3.0, 2.0], [0.0, 1.0]], np.float32)
+    k1, e1 = orc.mvs_keys(gp, 0.0)
+    k4, e4 = orc.mvs_keys(gp, 4.0)
+    # lambda=0: r=(3,0); lambda=4: r=(5,2)
+    assert k1[1] == 0 and k1[0] == 3 * 2**e1
+    assert k4.tolist() == [5 * 2**e4, 2 * 2**e4]
+
+
+def test_fixed_point_bounds_and_error(orc):
+    rng = np.random.default_rng(6)
+    for R in [1, 2, 3, 1000, 4097]:
+        gw = np.stack([rng.normal(size=R) * 1e3, rng.uniform(0, 1, R)], 1)
+        q, eg, eh = orc.fixed_point(gw)
+        L = math.ceil(math.log2(R)) if R > 1 else 0
+        assert np.abs(q[:, 0]).max() <= 2 ** (62 - L)
+        assert np.abs(q[:, 1]).max() <= 2 ** (62 - L)
+        # any subset sum stays below 2^62
+        assert abs(int(q[:, 0].astype(object).sum())) < 2**62
+        assert int(q[:, 1].astype(object).sum()) < 2**62
+        # |G_fx - G_exact| <= R * 2^-(e+1)
+        G_fx = Fraction(int(q[:, 0].astype(object).sum()), 2**eg) if eg >= 0 else None
+        G_ex = sum(Fraction(x) for x in gw[:, 0].tolist())
+        assert abs(G_fx - G_ex) <= Fraction(R, 2 ** (eg + 1))
+        # the exponent is maximal: doubling it would overflow the bound
+        M = np.abs(gw[:, 0]).max()
+        assert M * 2.0 ** (eg + 1) >= 2 ** (62 - L)
+
+
+def test_fixed_point_zero_input(orc):
+    q, eg, eh = orc.fixed_point(np.zeros((4, 2)))
+    assert (q == 0).all() and eg == 60 and eh == 60
