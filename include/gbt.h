@@ -1,0 +1,344 @@
+/*
+ * gbt.h -- C-ABI of libgbt.so: the per-iteration hot path of out-of-core GPU
+ * gradient boosting (Ou, "Out-of-Core GPU Gradient Boosting", KDD 2020) as
+ * hand-written HIP kernels for MI355X (gfx950).
+ *
+ * Conventions
+ *  - Every call returns gbt_status: GBT_OK (0) or a negative error.  No call
+ *    aborts or throws across this boundary.  gbt_last_error() returns the
+ *    message of the calling thread's last failed call.
+ *  - Pointers ending in _d are device pointers on the context's device; _h
+ *    are host pointers.  Arrays the caller sees are caller-allocated (for
+ *    example torch tensors passed by data_ptr()); opaque objects (gbt_ctx,
+ *    gbt_matrix, gbt_sampled, gbt_quantizer) are library-owned and released
+ *    by their *_free / *_destroy call.
+ *  - Work is enqueued on the context's stream.  Calls that return host
+ *    values (counts, trees, info) synchronise that stream before returning.
+ *    A context is used by one thread at a time; separate contexts are
+ *    independent.
+ *  - Hyperparameters are double; sizes are int64_t.
+ *
+ * Error codes
+ *  GBT_E_INVALID      bad argument: NULL pointer, n < 0, max_bin outside
+ *                     [2, 65535], f outside (0, 1], +-inf in the input,
+ *                     unsorted CSR indices, an inconsistent page/matrix
+ *  GBT_E_OOM          device or pinned-host allocation failed
+ *  GBT_E_BUDGET       the context's device byte budget would be exceeded
+ *                     (the out-of-memory limit of the paper's Table 1)
+ *  GBT_E_DEVICE       a HIP runtime error (message saved)
+ *  GBT_E_UNSUPPORTED  a valid request this build does not implement
+ */
+#ifndef GBT_H
+#define GBT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t gbt_status;
+
+#define GBT_OK 0
+#define GBT_E_INVALID (-1)
+#define GBT_E_OOM (-2)
+#define GBT_E_BUDGET (-3)
+#define GBT_E_DEVICE (-4)
+#define GBT_E_UNSUPPORTED (-5)
+
+#define GBT_ABI_VERSION 1
+
+enum { GBT_INPUT_DENSE_F32 = 0, GBT_INPUT_CSR_F32 = 1 };
+enum { GBT_LOC_HOST = 0, GBT_LOC_DEVICE = 1 };
+enum { GBT_HOME_DEVICE = 0, GBT_HOME_PINNED_HOST = 1 };
+enum { GBT_LOSS_LOGISTIC = 0, GBT_LOSS_SQUARED = 1 };
+enum { GBT_NODE_PRESENT = 1, GBT_NODE_LEAF = 2, GBT_NODE_DEFAULT_LEFT = 4 };
+
+typedef struct gbt_ctx gbt_ctx;
+typedef struct gbt_matrix gbt_matrix;
+typedef struct gbt_sampled gbt_sampled;
+typedef struct gbt_quantizer gbt_quantizer;
+
+/* Raw training examples X (Sec. 2.1): dense row-major float32 with NaN for
+ * a missing value, or CSR float32 whose absent entries (and NaN values) are
+ * missing.  CSR column indices must be strictly ascending within a row. */
+typedef struct {
+    int32_t kind;          /* GBT_INPUT_DENSE_F32 | GBT_INPUT_CSR_F32 */
+    int32_t location;      /* GBT_LOC_HOST | GBT_LOC_DEVICE */
+    int64_t n_rows;
+    int32_t n_cols;
+    int32_t pad0;
+    const float *values;   /* dense: n_rows*ld; CSR: nnz values */
+    int64_t ld;            /* dense leading dimension (>= n_cols) */
+    const int64_t *indptr; /* CSR: n_rows+1 */
+    const int32_t *indices;/* CSR: nnz */
+    int64_t nnz;
+} gbt_input;
+
+typedef struct {
+    int32_t max_bin;          /* Sec. 2.2: bins per feature, default 256 */
+    int32_t page_home;        /* GBT_HOME_DEVICE | GBT_HOME_PINNED_HOST */
+    int64_t sketch_max_rows;  /* 0 = 2^24: above it, every ceil(n/this)-th row is sketched */
+    int64_t page_rows;        /* rows per ELLPACK page; 0 = one page */
+} gbt_quant_params;
+
+/* Geometry of a quantized matrix.  Symbols: dense pages hold feature j's
+ * local bin in slot j (null = 2^w - 1 when any value is missing); sparse
+ * pages hold the row's present features in ascending order as global bins
+ * off_j + bin, padded with null = total_bins.  A row is an LSB-first bit
+ * stream of stride*w bits in row_words 32-bit words (a multiple of 4). */
+typedef struct {
+    int64_t n_rows;
+    int32_t n_cols;
+    int32_t sparse;
+    int32_t has_missing;
+    int32_t symbol_bits;
+    int32_t stride;
+    int32_t row_words;
+    uint32_t null_symbol;
+    int32_t n_pages;
+    int64_t total_bins;
+    int64_t page_rows;
+    int32_t page_home;
+    int32_t pad0;
+} gbt_matrix_info;
+
+typedef struct {
+    int32_t loss;             /* GBT_LOSS_* */
+    int32_t max_depth;        /* 0..20 */
+    double eta;               /* learning rate */
+    double lambda;            /* L2 term of Eq. 2-3 */
+    double gamma;             /* per-leaf term of Eq. 2-3 / Eq. 8 */
+    double min_child_weight;  /* minimum hessian sum per child */
+    double f;                 /* sampling fraction, (0, 1]; 1 = no sampling */
+    double mvs_lambda;        /* lambda of Eq. 9 */
+    uint64_t seed;
+    uint64_t iteration;       /* tree index; keys the sampling stream */
+} gbt_train_params;
+
+/* A node's row segment rows[begin, end) and its histogram slot. */
+typedef struct {
+    int32_t node_slot;
+    int32_t pad0;
+    int64_t begin;
+    int64_t end;
+} gbt_seg;
+
+/* hist[target_slot] = parent_hist[parent_slot] - hist[built_slot] */
+typedef struct {
+    int32_t parent_slot;
+    int32_t built_slot;
+    int32_t target_slot;
+    int32_t pad0;
+} gbt_sub;
+
+typedef struct {
+    double gain;
+    int64_t left_g, left_h, right_g, right_h; /* fixed-point sums */
+    int32_t feature;
+    int32_t split_bin;     /* left iff bin < split_bin */
+    int32_t default_left;  /* missing values go left */
+    int32_t valid;
+} gbt_split;
+
+/* One node of a heap-ordered tree: the children of node i are 2i+1, 2i+2. */
+typedef struct {
+    int32_t feature;       /* split nodes; -1 otherwise */
+    int32_t split_bin;
+    float threshold;       /* raw-value form: left iff x <= threshold */
+    float leaf_value;      /* leaves */
+    double gain;           /* split nodes */
+    int64_t sum_g, sum_h;  /* fixed-point gradient sums of the node */
+    int32_t n_rows;        /* training rows in the node */
+    uint8_t flags;         /* GBT_NODE_* */
+    uint8_t pad[3];
+} gbt_node;
+
+/* Caller-allocated host tree of n_nodes = 2^(max_depth+1) - 1 nodes.  The
+ * fixed-point exponents convert node sums back: G = sum_g * 2^-exp_g. */
+typedef struct {
+    int32_t max_depth;
+    int32_t n_nodes;
+    int32_t exp_g;
+    int32_t exp_h;
+    gbt_node *nodes;
+} gbt_tree;
+
+typedef struct {
+    int64_t n_sampled;      /* R: rows the tree was built on */
+    int64_t threshold;      /* MVS threshold T* (0 without sampling) */
+    int32_t exp_key;        /* MVS key exponent */
+    int32_t hist_launches;  /* histogram-building kernel launches */
+    int64_t hist_rows;      /* rows streamed by the histogram kernels */
+    int64_t hist_updates;   /* non-null (row, feature) updates performed */
+    int64_t hist_bytes;     /* algorithmic bytes of the histogram kernels */
+    double ms_hist;         /* histogram kernel time (only with timing on) */
+    double ms_total;
+} gbt_tree_stats;
+
+typedef struct {
+    double f;
+    double mvs_lambda;
+    uint64_t seed;
+    uint64_t iteration;
+    int32_t loss;           /* used when gradients are recomputed from margins */
+    int32_t pad0;
+} gbt_sample_params;
+
+typedef struct {
+    int64_t n_sampled;
+    int64_t threshold;
+    int64_t target;         /* K = max(1, rint(f*n)) */
+    int32_t exp_key;
+    int32_t exp_g;
+    int32_t exp_h;
+    int32_t is_alias;       /* f = 1: the page is the data's own page */
+    const uint32_t *page_d; /* R rows of row_words words */
+    const int32_t *rows_d;  /* R global row ids, ascending */
+    const double *gpair_d;  /* R reweighted (g', h') in double */
+    const int64_t *gpair_fx_d; /* R fixed-point (q_g, q_h) */
+} gbt_sampled_info;
+
+/* ---- library ----------------------------------------------------------- */
+int32_t gbt_abi_version(void);
+const char *gbt_last_error(void);
+
+/* ---- context ------------------------------------------------------------
+ * device: HIP device ordinal.  budget_bytes: cap on library-owned device
+ * allocations (0 = unlimited).  hip_stream: the stream work is enqueued on
+ * (NULL = the device's null stream).  A second stream at default priority
+ * is created for host-to-device page copies. */
+gbt_status gbt_ctx_create(int32_t device, uint64_t budget_bytes, void *hip_stream, gbt_ctx **out);
+gbt_status gbt_ctx_destroy(gbt_ctx *ctx);
+/* Bytes of device memory the context currently holds (budgeted). */
+gbt_status gbt_ctx_memory(gbt_ctx *ctx, uint64_t *used_bytes, uint64_t *peak_bytes);
+/* Record HIP events around histogram launches (for gbt_tree_stats.ms_hist). */
+gbt_status gbt_ctx_set_timing(gbt_ctx *ctx, int32_t enable);
+
+/* ---- quantile cuts and ELLPACK pages: Sec. 2.2, Sec. 3.1 (Alg. 2, 3),
+ * Sec. 3.2 (Alg. 4, 5) ------------------------------------------------------
+ * Cuts are exact quantiles of a sketch sample: for a feature with sorted
+ * non-missing sketch values s_0..s_{N-1}, candidate k (1..max_bin-1) is
+ * s[ceil(k*N/max_bin)-1]; duplicates and values >= s_{N-1} are dropped;
+ * bin(x) = #{cuts < x}.  gbt_quantize is the one-shot form; the incremental
+ * form takes batches (Alg. 3 sketch, then Alg. 5 pages):
+ *   begin -> sketch_batch* (every batch, in row order) -> finalize_cuts ->
+ *   encode_batch* (every batch again, same order) -> end.
+ * n_rows_total fixes the sketch stride.  page_home PINNED_HOST keeps pages
+ * in page-locked host memory for streaming. */
+gbt_status gbt_quantize(gbt_ctx *ctx, const gbt_input *in, const gbt_quant_params *p,
+                        gbt_matrix **out);
+gbt_status gbt_quantize_begin(gbt_ctx *ctx, const gbt_quant_params *p, int32_t n_cols,
+                              int64_t n_rows_total, int32_t input_kind, gbt_quantizer **out);
+gbt_status gbt_quantize_sketch_batch(gbt_quantizer *q, const gbt_input *batch);
+gbt_status gbt_quantize_finalize_cuts(gbt_quantizer *q);
+gbt_status gbt_quantize_encode_batch(gbt_quantizer *q, const gbt_input *batch);
+gbt_status gbt_quantize_end(gbt_quantizer *q, gbt_matrix **out); /* frees q */
+gbt_status gbt_quantizer_free(gbt_quantizer *q);
+
+gbt_status gbt_matrix_info_get(const gbt_matrix *m, gbt_matrix_info *info);
+/* Host copies of the cuts: cut_ptr_h[n_cols+1], cut_values_h[cut_ptr_h[n_cols]]. */
+gbt_status gbt_matrix_get_cuts(const gbt_matrix *m, int32_t *cut_ptr_h, float *cut_values_h);
+/* Copy page `page` (page_rows[page]*row_words words) to dst (host or device). */
+gbt_status gbt_matrix_copy_page(const gbt_matrix *m, int32_t page, void *dst, int64_t dst_words);
+gbt_status gbt_matrix_page_rows(const gbt_matrix *m, int32_t page, int64_t *row0, int64_t *rows);
+gbt_status gbt_matrix_free(gbt_matrix *m);
+
+/* ---- gradients: Eq. 4-5 ---------------------------------------------------
+ * gpair_d[2i], gpair_d[2i+1] = (float) g_i, h_i computed in double:
+ *   logistic: s = 1/(1+exp(-z)), g = s - y, h = max(s(1-s), 1e-16)
+ *   squared : g = z - y, h = 1
+ * times weight_d[i] when weight_d is not NULL. */
+gbt_status gbt_gradients(gbt_ctx *ctx, int32_t loss, const float *margin_d, const float *label_d,
+                         const float *weight_d, int64_t n, float *gpair_d);
+
+/* ---- sampling and compaction: Sec. 2.4 Eq. 9, Sec. 3.4 Alg. 7 -------------
+ * Minimal variance sampling of the n rows of `data` with probability
+ * proportional to sqrt(g^2 + mvs_lambda h^2), then compaction of the kept
+ * rows (ascending) into one device page, reweighting by the inverse
+ * inclusion probability, and exact fixed-point conversion of the reweighted
+ * pairs.  Integer reading:
+ *   a_i = rint(r_i 2^e), e = 62 - E - ceil(log2 n), max r < 2^E
+ *   K = max(1, rint(f n)); T* = least T >= 1 with
+ *       sum_{a_i<T} a_i <= (K - #{a_i >= T}) T
+ *   keep iff a_i >= T* or hi64(U_i T*) < a_i, U_i = word 0 of
+ *       Philox4x64-10(counter (i, iteration, 0, 0), key (seed, 0))
+ *   w_i = 1 if a_i >= T* else T* / a_i;  (g', h') = (g w_i, h w_i)
+ *   q = rint((g', h') 2^(e_g, e_h)), e = 62 - E - ceil(log2 R)
+ * gpair_d (n pairs) may be NULL for pinned-host data: gradients are then
+ * recomputed from margin_d/label_d with sp->loss while pages stream.
+ * f = 1 keeps every row without copying (is_alias) when the data is one
+ * device page. */
+gbt_status gbt_sample(gbt_ctx *ctx, const gbt_matrix *data, const float *gpair_d,
+                      const float *margin_d, const float *label_d, const gbt_sample_params *sp,
+                      gbt_sampled **out);
+gbt_status gbt_sampled_info_get(const gbt_sampled *s, gbt_sampled_info *info);
+gbt_status gbt_sampled_free(gbt_sampled *s);
+
+/* ---- Alg. 1 BuildHistograms ------------------------------------------------
+ * For each build segment: hist_d[slot][off_j + b] += (q_g, q_h) of the rows
+ * rows_d[begin..end) (row ids of `page`, NULL = identity) whose symbol for
+ * feature j is bin b; missing values add nothing.  hist_d is int64
+ * [slots][total_bins][2] and the built slots are overwritten.  Then for each
+ * sub entry: hist_d[target] = parent_hist_d[parent] - hist_d[built] (the
+ * sibling of a built child), exact in integers.  `page` is a device page of
+ * the matrix geometry of `layout` (page_d rows of row_words words). */
+gbt_status gbt_build_hist(gbt_ctx *ctx, const gbt_matrix *layout, const uint32_t *page_d,
+                          const int64_t *gpair_fx_d, const int32_t *rows_d, const gbt_seg *build_h,
+                          int32_t n_build, const gbt_sub *sub_h, int32_t n_sub,
+                          const int64_t *parent_hist_d, int64_t *hist_d);
+
+/* ---- Alg. 1 EvaluateSplit with Eq. 8 ---------------------------------------
+ * For node k: histogram hist_d[node_slot_h[k]], node sum node_sum_d[2k..2k+1].
+ * Every feature with >= 2 bins, every s in 1..B_j-1, missing right then
+ * left: Q_L = sum_{b<s} H (+ missing sums), Q_R = node - Q_L; valid when
+ * H_L, H_R >= min_child_weight; gain = 0.5((G_L^2/(H_L+l) + G_R^2/(H_R+l))
+ * - G^2/(H+l)) - gamma in double; the best is the highest gain, ties to the
+ * lower feature, lower s, missing right.  out_d[k] receives it. */
+gbt_status gbt_eval_splits(gbt_ctx *ctx, const gbt_matrix *layout, const int64_t *hist_d,
+                           const int64_t *node_sum_d, const int32_t *node_slot_h, int32_t n_nodes,
+                           const gbt_train_params *tp, int32_t exp_g, int32_t exp_h,
+                           gbt_split *out_d);
+
+/* ---- Alg. 1 RepartitionInstances -------------------------------------------
+ * For node k with segment seg_h[k] of rows_d and split split_h[k] (valid):
+ * stable partition into [left | right] where a row goes left iff its bin
+ * for the split feature is < split_bin, or it is missing and default_left.
+ * position_d[row] receives child_h[2k] or child_h[2k+1].  seg_out_h[2k],
+ * seg_out_h[2k+1] receive the child segments (host, after a sync).
+ * rows_tmp_d is scratch of the same length as rows_d (n_rows). */
+gbt_status gbt_partition(gbt_ctx *ctx, const gbt_matrix *layout, const uint32_t *page_d,
+                         const gbt_split *split_h, const gbt_seg *seg_h, const int32_t *child_h,
+                         int32_t n_nodes, int32_t *rows_d, int32_t *rows_tmp_d, int64_t n_rows,
+                         int32_t *position_d, gbt_seg *seg_out_h);
+
+/* ---- Eq. 6 leaves and the Eq. 1 margin update -------------------------------
+ * Leaves of `tree` (flags LEAF) get leaf_value = (float)((-G/(H+lambda))*eta)
+ * from their fixed-point sums; then margin_d[i] += leaf(tree, row i) for the
+ * n rows of `data`, by traversal of each row's binned symbols. */
+gbt_status gbt_update_leaves(gbt_ctx *ctx, gbt_tree *tree, const gbt_train_params *tp,
+                             const gbt_matrix *data, float *margin_d);
+
+/* ---- one boosting iteration: Alg. 7 then Alg. 1 -----------------------------
+ * Gradients, sampling (f < 1) with compaction into one device page, the
+ * level-wise tree (histograms with the sibling subtraction, splits,
+ * partitions), leaves and the margin update of all rows.  Pinned-host
+ * matrices stream their pages.  tree->nodes must hold 2^(max_depth+1)-1
+ * nodes. */
+gbt_status gbt_train_tree(gbt_ctx *ctx, const gbt_matrix *data, const float *label_d,
+                          float *margin_d, const gbt_train_params *p, gbt_tree *tree,
+                          gbt_tree_stats *stats);
+
+/* ---- Eq. 1 prediction -------------------------------------------------------
+ * margin_out_d[i] = base_margin + sum_t leaf(tree t, row i), in float, tree
+ * order.  Exactly one of raw (rows traverse by x <= threshold, missing by
+ * default_left; must be device resident) or binned (symbols) is given. */
+gbt_status gbt_predict(gbt_ctx *ctx, const gbt_tree *trees, int32_t n_trees,
+                       const gbt_input *raw, const gbt_matrix *binned, float base_margin,
+                       float *margin_out_d);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GBT_H */

@@ -1,0 +1,239 @@
+// common.h -- internals shared by the libgbt translation units: context,
+// budgeted device allocator, error model, matrix/page objects and the
+// device-side ELLPACK decoding helpers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "gbt.h"
+
+namespace gbt {
+
+// ---------------------------------------------------------------- errors
+gbt_status set_error(gbt_status code, const char *fmt, ...);
+gbt_status hip_error(hipError_t e, const char *what, const char *file, int line);
+
+#define GBT_HIP(call)                                                                  \
+    do {                                                                               \
+        hipError_t e_ = (call);                                                        \
+        if (e_ != hipSuccess) return ::gbt::hip_error(e_, #call, __FILE__, __LINE__); \
+    } while (0)
+
+#define GBT_TRY(expr)                    \
+    do {                                 \
+        gbt_status s_ = (expr);          \
+        if (s_ != GBT_OK) return s_;     \
+    } while (0)
+
+#define GBT_CHECK(cond, ...)                                              \
+    do {                                                                  \
+        if (!(cond)) return ::gbt::set_error(GBT_E_INVALID, __VA_ARGS__); \
+    } while (0)
+
+// Kernel launches: check the launch itself (configuration errors).
+#define GBT_LAUNCHED() GBT_HIP(hipGetLastError())
+
+constexpr int kXcds = 8;         // gfx950: 8 XCDs of 32 CUs
+constexpr int kCUs = 256;
+
+// Map a linear workgroup id so that logically adjacent ids run on the same
+// XCD (the hardware deals workgroups round-robin over the XCDs).
+__device__ inline uint32_t xcd_remap(uint32_t b, uint32_t n)
+{
+    uint32_t xcd = b % kXcds, local = b / kXcds;
+    uint32_t per = n / kXcds, rem = n % kXcds;
+    return xcd < rem ? xcd * (per + 1) + local : rem * (per + 1) + (xcd - rem) * per + local;
+}
+
+}  // namespace gbt
+
+// ---------------------------------------------------------------- context
+struct gbt_ctx {
+    int device = 0;
+    hipStream_t stream = nullptr;   // compute stream (caller's)
+    hipStream_t side = nullptr;     // host-to-device page copies
+    uint64_t budget = 0;            // 0 = unlimited
+    uint64_t used = 0, peak = 0;
+    bool timing = false;
+    struct Scratch {
+        void *p = nullptr;
+        size_t bytes = 0;
+    };
+    std::vector<Scratch> scratch;   // reusable workspaces, by slot id
+};
+
+namespace gbt {
+
+gbt_status dev_alloc(gbt_ctx *c, size_t bytes, void **p);
+void dev_free(gbt_ctx *c, void *p, size_t bytes);
+// Grow-only workspace in slot `slot` of the context.
+gbt_status scratch(gbt_ctx *c, int slot, size_t bytes, void **p);
+gbt_status set_device(gbt_ctx *c);
+
+enum ScratchSlot {
+    kScrGpair = 0,   // float (g, h) of all rows
+    kScrKeys,        // MVS keys
+    kScrFlags,       // keep flags
+    kScrPos,         // scan of the keep flags
+    kScrMisc,        // threshold radix histogram
+    kScrState,       // SampleState
+    kScrSampled,     // the sampled page
+    kScrSel,         // global ids of the sampled rows
+    kScrGw,          // reweighted (g', h') in double
+    kScrQ,           // fixed-point (q_g, q_h)
+    kScrRows, kScrRowsTmp, kScrPosition,
+    kScrHistA, kScrHistB,
+    kScrNodes,       // DevNode table
+    kScrEvalNodes,   // EvalNode list
+    kScrSplits,      // gbt_split per evaluated node
+    kScrEval,        // per feature-block candidates
+    kScrPartFlags, kScrPartPos,
+    kScrWork,        // histogram plan
+    kScrUpd,         // histogram update counter
+    kScrScan,        // scan block sums
+    kScrStage0, kScrStage1,  // streamed page chunks
+    kScrLeaf,        // leaf values
+    kScrTrees,       // trees for prediction
+    kScrSlotNode,    // slot -> node map
+    kScrCount
+};
+
+template <typename T>
+gbt_status scratch_t(gbt_ctx *c, int slot, size_t n, T **p)
+{
+    return scratch(c, slot, n * sizeof(T), reinterpret_cast<void **>(p));
+}
+
+}  // namespace gbt
+
+// ---------------------------------------------------------------- matrix
+struct GbtPage {
+    int64_t row0 = 0;
+    int64_t rows = 0;
+    uint32_t *words = nullptr;  // device or pinned host
+    bool host = false;
+};
+
+struct gbt_matrix {
+    gbt_ctx *ctx = nullptr;
+    int64_t n_rows = 0;
+    int32_t m = 0;
+    int32_t sparse = 0;
+    int32_t has_missing = 0;
+    int32_t w = 1;
+    int32_t stride = 0;
+    int32_t row_words = 4;
+    uint32_t null_sym = 0;
+    int64_t total_bins = 0;
+    int64_t page_rows = 0;
+    int32_t page_home = GBT_HOME_DEVICE;
+    std::vector<int32_t> cut_ptr_h;     // m+1
+    std::vector<float> cut_values_h;
+    int32_t *cut_ptr_d = nullptr;       // m+1
+    float *cut_values_d = nullptr;
+    int32_t *bin_ptr_d = nullptr;       // m+1 global bin offsets (cut_ptr[j] + j)
+    std::vector<int32_t> bin_ptr_h;
+    std::vector<GbtPage> pages;
+};
+
+namespace gbt {
+
+// Everything a kernel needs to decode an ELLPACK row.
+struct Geo {
+    int32_t m;
+    int32_t w;
+    int32_t stride;
+    int32_t row_words;
+    uint32_t null_sym;
+    uint32_t mask;
+    int32_t sparse;
+    int32_t pad0;
+    int64_t total_bins;
+    const int32_t *bin_ptr;  // m+1
+};
+
+// null_sym is a value no symbol can take when the matrix has no missing
+// value (a dense page without missing values uses every w-bit code).
+inline Geo geo_of(const gbt_matrix *mx)
+{
+    Geo g;
+    g.m = mx->m;
+    g.w = mx->w;
+    g.stride = mx->stride;
+    g.row_words = mx->row_words;
+    g.null_sym = (mx->sparse || mx->has_missing) ? mx->null_sym : 0xffffffffu;
+    g.mask = mx->w >= 32 ? 0xffffffffu : ((1u << mx->w) - 1u);
+    g.sparse = mx->sparse;
+    g.pad0 = 0;
+    g.total_bins = mx->total_bins;
+    g.bin_ptr = mx->bin_ptr_d;
+    return g;
+}
+
+// Symbol in slot s of an ELLPACK row (LSB-first bit stream).  Reads the next
+// word only when the symbol straddles a word boundary.
+__device__ inline uint32_t row_symbol(const uint32_t *__restrict__ row, int32_t s, int32_t w,
+                                      uint32_t mask)
+{
+    uint32_t bit = (uint32_t)s * (uint32_t)w;
+    uint32_t k = bit >> 5, sh = bit & 31u;
+    uint32_t v = row[k] >> sh;
+    if (sh + (uint32_t)w > 32u) v |= row[k + 1] << (32u - sh);
+    return v & mask;
+}
+
+// Local bin of feature j in a row, or -1 when missing.
+__device__ inline int32_t row_feature_bin(const uint32_t *__restrict__ row, const Geo &g, int32_t j)
+{
+    if (!g.sparse) {
+        uint32_t s = row_symbol(row, j, g.w, g.mask);
+        return s == g.null_sym ? -1 : (int32_t)s;
+    }
+    uint32_t lo = (uint32_t)g.bin_ptr[j], hi = (uint32_t)g.bin_ptr[j + 1];
+    for (int32_t s = 0; s < g.stride; ++s) {
+        uint32_t v = row_symbol(row, s, g.w, g.mask);
+        if (v >= hi) return -1;  // ascending global bins; null = total_bins ends the row
+        if (v >= lo) return (int32_t)(v - lo);
+    }
+    return -1;
+}
+
+// Device node table entry used by the tree driver (heap order).
+struct DevNode {
+    int64_t sum_g, sum_h;
+    int64_t begin, end;
+    int32_t present;
+    int32_t split;          // 1 if the node splits
+    int32_t feature, split_bin;
+    int32_t default_left;
+    int32_t left_child;     // node ids of the children (heap: 2i+1, 2i+2)
+    int32_t right_child;
+    int32_t pad0;
+    double gain;
+    int64_t left_g, left_h, right_g, right_h;
+};
+
+// ---------------------------------------------------------------- scans
+// Exclusive prefix sum of n flags (bytes 0/1) or counts (uint32): out[i] for
+// i in [0, n], out[n] = total.  Device-wide, deterministic.
+gbt_status scan_u8(gbt_ctx *c, const uint8_t *in, int64_t n, int32_t *out);
+gbt_status scan_u32(gbt_ctx *c, const uint32_t *in, int64_t n, int32_t *out);
+
+// ---------------------------------------------------------------- shared launches
+gbt_status launch_gradients(gbt_ctx *c, int32_t loss, const float *margin, const float *label,
+                            const float *weight, int64_t n, float *gpair);
+gbt_status build_hist_impl(gbt_ctx *c, const gbt_matrix *layout, const uint32_t *page,
+                           const int64_t *q, const int32_t *rows, const gbt_seg *build,
+                           int32_t n_build, const gbt_sub *sub, int32_t n_sub,
+                           const int64_t *parent_hist, int64_t *hist, gbt_tree_stats *stats);
+
+// Row-major ELLPACK page geometry helpers (host).
+int32_t ceil_log2_u64(uint64_t v);
+
+}  // namespace gbt

@@ -1,0 +1,152 @@
+// ctx.hip -- context, error model and the budgeted device allocator.
+#include "common.h"
+
+#include <mutex>
+
+namespace gbt {
+
+static thread_local std::string g_last_error;
+
+gbt_status set_error(gbt_status code, const char *fmt, ...)
+{
+    char buf[1024];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return code;
+}
+
+gbt_status hip_error(hipError_t e, const char *what, const char *file, int line)
+{
+    gbt_status code = (e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation) ? GBT_E_OOM
+                                                                                  : GBT_E_DEVICE;
+    return set_error(code, "%s failed: %s (%s:%d)", what, hipGetErrorString(e), file, line);
+}
+
+gbt_status set_device(gbt_ctx *c)
+{
+    GBT_HIP(hipSetDevice(c->device));
+    return GBT_OK;
+}
+
+gbt_status dev_alloc(gbt_ctx *c, size_t bytes, void **p)
+{
+    *p = nullptr;
+    if (bytes == 0) bytes = 256;
+    if (c->budget && c->used + bytes > c->budget)
+        return set_error(GBT_E_BUDGET,
+                         "device budget exceeded: %llu bytes held + %llu requested > %llu",
+                         (unsigned long long)c->used, (unsigned long long)bytes,
+                         (unsigned long long)c->budget);
+    hipError_t e = hipMalloc(p, bytes);
+    if (e != hipSuccess) {
+        *p = nullptr;
+        (void)hipGetLastError();
+        return set_error(GBT_E_OOM, "hipMalloc(%llu) failed: %s", (unsigned long long)bytes,
+                         hipGetErrorString(e));
+    }
+    c->used += bytes;
+    if (c->used > c->peak) c->peak = c->used;
+    return GBT_OK;
+}
+
+void dev_free(gbt_ctx *c, void *p, size_t bytes)
+{
+    if (!p) return;
+    if (bytes == 0) bytes = 256;
+    (void)hipFree(p);
+    c->used -= bytes;
+}
+
+gbt_status scratch(gbt_ctx *c, int slot, size_t bytes, void **p)
+{
+    if ((int)c->scratch.size() <= slot) c->scratch.resize(slot + 1);
+    auto &s = c->scratch[slot];
+    if (s.bytes < bytes) {
+        // the stream may still use the old buffer
+        GBT_HIP(hipStreamSynchronize(c->stream));
+        dev_free(c, s.p, s.bytes);
+        s.p = nullptr;
+        s.bytes = 0;
+        size_t want = bytes + bytes / 8 + 4096;  // slack so small growth does not reallocate
+        GBT_TRY(dev_alloc(c, want, &s.p));
+        s.bytes = want;
+    }
+    *p = s.p;
+    return GBT_OK;
+}
+
+int32_t ceil_log2_u64(uint64_t v)
+{
+    int32_t b = 0;
+    while (b < 64 && ((uint64_t)1 << b) < v) ++b;
+    return b;
+}
+
+}  // namespace gbt
+
+using namespace gbt;
+
+extern "C" {
+
+int32_t gbt_abi_version(void) { return GBT_ABI_VERSION; }
+
+const char *gbt_last_error(void) { return g_last_error.c_str(); }
+
+gbt_status gbt_ctx_create(int32_t device, uint64_t budget_bytes, void *hip_stream, gbt_ctx **out)
+{
+    if (!out) return set_error(GBT_E_INVALID, "gbt_ctx_create: out is NULL");
+    *out = nullptr;
+    int n = 0;
+    GBT_HIP(hipGetDeviceCount(&n));
+    if (device < 0 || device >= n)
+        return set_error(GBT_E_INVALID, "gbt_ctx_create: device %d of %d", device, n);
+    GBT_HIP(hipSetDevice(device));
+    hipDeviceProp_t prop;
+    GBT_HIP(hipGetDeviceProperties(&prop, device));
+    if (std::string(prop.gcnArchName).find("gfx950") == std::string::npos)
+        return set_error(GBT_E_UNSUPPORTED, "libgbt is built for gfx950; device %d is %s", device,
+                         prop.gcnArchName);
+    auto *c = new gbt_ctx();
+    c->device = device;
+    c->budget = budget_bytes;
+    c->stream = (hipStream_t)hip_stream;
+    hipError_t e = hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking);
+    if (e != hipSuccess) {
+        delete c;
+        return hip_error(e, "hipStreamCreateWithFlags", __FILE__, __LINE__);
+    }
+    *out = c;
+    return GBT_OK;
+}
+
+gbt_status gbt_ctx_destroy(gbt_ctx *c)
+{
+    if (!c) return GBT_OK;
+    (void)hipSetDevice(c->device);
+    (void)hipStreamSynchronize(c->stream);
+    (void)hipStreamSynchronize(c->side);
+    for (auto &s : c->scratch) dev_free(c, s.p, s.bytes);
+    (void)hipStreamDestroy(c->side);
+    delete c;
+    return GBT_OK;
+}
+
+gbt_status gbt_ctx_memory(gbt_ctx *c, uint64_t *used, uint64_t *peak)
+{
+    if (!c) return set_error(GBT_E_INVALID, "gbt_ctx_memory: ctx is NULL");
+    if (used) *used = c->used;
+    if (peak) *peak = c->peak;
+    return GBT_OK;
+}
+
+gbt_status gbt_ctx_set_timing(gbt_ctx *c, int32_t enable)
+{
+    if (!c) return set_error(GBT_E_INVALID, "gbt_ctx_set_timing: ctx is NULL");
+    c->timing = enable != 0;
+    return GBT_OK;
+}
+
+}  // extern "C"

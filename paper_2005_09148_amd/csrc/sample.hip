@@ -1,0 +1,559 @@
+// sample.hip -- Eq. 4-5 gradients, Eq. 9 minimal variance sampling with the
+// compaction of Alg. 7 (Sec. 3.4), and the exact fixed-point conversion of
+// the reweighted gradient pairs.
+//
+// The sampling threshold T* (least integer T >= 1 with
+// sum_{a_i<T} a_i <= (K - #{a_i >= T}) T) is found without sorting: at the
+// boundaries of key buckets both #{a >= T} and sum_{a < T} a follow from a
+// (count, sum) histogram, so a radix descent over 11-bit digits pins T*
+// exactly in ceil(bits/11) passes over the keys.  When T* exceeds every key
+// it has the closed form ceil(sum a / K).
+#include "sample_impl.h"
+
+namespace gbt {
+
+// ------------------------------------------------------------ exp (device)
+// Cody & Waite reduction of x by ln 2 (head with 32 significant bits, tail
+// the remainder), Taylor polynomial of e^r through r^13 by Horner with fused
+// multiply-adds, scaling by 2^k.  Inputs beyond +-708 clamp to +inf / 0.
+__device__ inline double cw_exp(double x)
+{
+    constexpr double kLn2Head = 0x1.62e42fee00000p-1;
+    constexpr double kLn2Tail = 0x1.a39ef35793c76p-33;
+    constexpr double kInvLn2 = 0x1.71547652b82fep+0;
+    // 1/13!, 1/12!, ..., 1/2!, 1/1!, 1/0!
+    constexpr double kTaylor[14] = {0x1.6124613a86d09p-33, 0x1.1eed8eff8d898p-29, 0x1.ae64567f544e4p-26,
+                                    0x1.27e4fb7789f5cp-22, 0x1.71de3a556c734p-19, 0x1.a01a01a01a01ap-16,
+                                    0x1.a01a01a01a01ap-13, 0x1.6c16c16c16c17p-10, 0x1.1111111111111p-7,
+                                    0x1.5555555555555p-5,  0x1.5555555555555p-3,  0.5,
+                                    1.0,                   1.0};
+    if (x != x) return x;
+    if (x > 708.0) return __builtin_huge_val();
+    if (x < -708.0) return 0.0;
+    double k = rint(x * kInvLn2);
+    double r = (x - k * kLn2Head) - k * kLn2Tail;
+    double p = kTaylor[0];
+#pragma unroll
+    for (int i = 1; i < 14; ++i) p = fma(p, r, kTaylor[i]);
+    return ldexp(p, (int)k);
+}
+
+__device__ inline void gradient_pair(int32_t loss, float margin, float label, double *g, double *h)
+{
+    double z = (double)margin, y = (double)label;
+    if (loss == GBT_LOSS_LOGISTIC) {
+        double s = 1.0 / (1.0 + cw_exp(-z));
+        *g = s - y;
+        double hh = s * (1.0 - s);
+        *h = hh < 1e-16 ? 1e-16 : hh;
+    } else {
+        *g = z - y;
+        *h = 1.0;
+    }
+}
+
+__global__ void k_gradients(int32_t loss, const float *__restrict__ margin,
+                            const float *__restrict__ label, const float *__restrict__ weight,
+                            int64_t n, float2 *__restrict__ gpair)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    double g, h;
+    gradient_pair(loss, margin[i], label[i], &g, &h);
+    if (weight) {
+        double w = (double)weight[i];
+        g = g * w;
+        h = h * w;
+    }
+    gpair[i] = make_float2((float)g, (float)h);
+}
+
+gbt_status launch_gradients(gbt_ctx *c, int32_t loss, const float *margin, const float *label,
+                            const float *weight, int64_t n, float *gpair)
+{
+    if (n == 0) return GBT_OK;
+    k_gradients<<<(unsigned)((n + 255) / 256), 256, 0, c->stream>>>(loss, margin, label, weight, n,
+                                                                    (float2 *)gpair);
+    GBT_LAUNCHED();
+    return GBT_OK;
+}
+
+// ------------------------------------------------------------ Philox4x64-10
+// Salmon et al., SC'11: ten rounds of two 64x64->128 multiplies, the key
+// advanced by the Weyl increments between rounds.
+__device__ inline uint64_t philox_word0(uint64_t c0, uint64_t c1, uint64_t c2, uint64_t c3,
+                                        uint64_t k0, uint64_t k1)
+{
+    constexpr uint64_t kMul0 = 0xD2E7470EE14C6C93ull, kMul1 = 0xCA5A826395121157ull;
+    constexpr uint64_t kWeyl0 = 0x9E3779B97F4A7C15ull, kWeyl1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+    for (int round = 0; round < 10; ++round) {
+        uint64_t p0hi = __umul64hi(kMul0, c0), p0lo = kMul0 * c0;
+        uint64_t p1hi = __umul64hi(kMul1, c2), p1lo = kMul1 * c2;
+        uint64_t n0 = p1hi ^ c1 ^ k0, n2 = p0hi ^ c3 ^ k1;
+        c0 = n0;
+        c1 = p1lo;
+        c2 = n2;
+        c3 = p0lo;
+        k0 += kWeyl0;
+        k1 += kWeyl1;
+    }
+    return c0;
+}
+
+// ------------------------------------------------------------ MVS keys
+template <int kSrc>
+__device__ inline void row_gh(const SampleSrc &src, int64_t i, double *g, double *h)
+{
+    if (kSrc == kSrcGpair) {
+        float2 p = src.gpair[i];
+        *g = (double)p.x;
+        *h = (double)p.y;
+    } else {
+        // gradients recomputed from margins, rounded to float as if stored
+        double gg, hh;
+        gradient_pair(src.loss, src.margin[i], src.label[i], &gg, &hh);
+        *g = (double)(float)gg;
+        *h = (double)(float)hh;
+    }
+}
+
+__device__ inline double mvs_r(double g, double h, double lambda)
+{
+    return sqrt(g * g + lambda * (h * h));
+}
+
+template <int kSrc>
+__global__ void __launch_bounds__(256) k_mvs_rmax(SampleSrc src, int64_t n, double lambda,
+                                                  SampleState *__restrict__ st)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    double r = 0.0;
+    if (i < n) {
+        double g, h;
+        row_gh<kSrc>(src, i, &g, &h);
+        r = mvs_r(g, h, lambda);
+        if (r != r || r > 1.7e308) atomicOr(&st->bad, 1u);
+    }
+    unsigned long long b = __double_as_longlong(r);
+    for (int d = 32; d > 0; d >>= 1) {
+        unsigned long long o = __shfl_xor(b, d, 64);
+        b = o > b ? o : b;
+    }
+    if ((threadIdx.x & 63) == 0 && b) atomicMax(&st->rmax_bits, b);
+}
+
+// a_i = rint(r_i * 2^e), e = 62 - E - L with max r < 2^E; also max and sum
+// of the keys and, fused, nothing else.
+template <int kSrc>
+__global__ void __launch_bounds__(256) k_mvs_keys(SampleSrc src, int64_t n, double lambda,
+                                                  int32_t log2n, SampleState *__restrict__ st,
+                                                  int64_t *__restrict__ keys)
+{
+    int E;
+    frexp(__longlong_as_double(st->rmax_bits), &E);
+    int32_t e = 62 - E - log2n;
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    unsigned long long a = 0;
+    if (i < n) {
+        double g, h;
+        row_gh<kSrc>(src, i, &g, &h);
+        a = (unsigned long long)(long long)rint(ldexp(mvs_r(g, h, lambda), e));
+        if (keys) keys[i] = (int64_t)a;
+    }
+    unsigned long long mx = a, sm = a;
+    for (int d = 32; d > 0; d >>= 1) {
+        unsigned long long o = __shfl_xor(mx, d, 64);
+        mx = o > mx ? o : mx;
+        sm += __shfl_xor(sm, d, 64);
+    }
+    if ((threadIdx.x & 63) == 0) {
+        if (mx) atomicMax(&st->amax, mx);
+        if (sm) atomicAdd(&st->asum, sm);
+    }
+    if (i == 0) st->e_key = e;
+}
+
+// Closed form when T* exceeds every key; otherwise the radix descent
+// starts on [0, 2^S) with 2^S > amax + 1.
+__global__ void k_mvs_thresh_init(SampleState *__restrict__ st, int64_t K)
+{
+    if (threadIdx.x != 0) return;
+    unsigned long long amax = st->amax, asum = st->asum;
+    unsigned long long q = (asum + (unsigned long long)K - 1) / (unsigned long long)K;
+    st->C_above = 0;
+    st->F_below = 0;
+    st->lo = 0;
+    if (q > amax + 1) {
+        st->T = (long long)q;
+        st->done = 1;
+        st->levels = 0;
+        return;
+    }
+    int S = 64 - __clzll((long long)(amax + 1));  // 2^S > amax + 1
+    int levels = (S + kDigitBits - 1) / kDigitBits;
+    st->shift = (levels - 1) * kDigitBits;
+    st->nbuckets = (int32_t)(((1ull << S) + (1ull << st->shift) - 1) >> st->shift);
+    st->levels = levels;
+    st->done = 0;
+    st->T = 0;
+}
+
+template <int kSrc>
+__global__ void __launch_bounds__(256) k_mvs_radix_hist(SampleSrc src, const int64_t *__restrict__ keys,
+                                                        int64_t n, double lambda, int32_t log2n,
+                                                        const SampleState *__restrict__ st,
+                                                        unsigned long long *__restrict__ hcnt,
+                                                        unsigned long long *__restrict__ hsum)
+{
+    __shared__ unsigned int scnt[kDigitBuckets];
+    __shared__ unsigned long long ssum[kDigitBuckets];
+    if (st->done) return;
+    const unsigned long long lo = (unsigned long long)st->lo;
+    const int shift = st->shift;
+    const int32_t nb = st->nbuckets;
+    for (int t = threadIdx.x; t < nb; t += blockDim.x) {
+        scnt[t] = 0;
+        ssum[t] = 0;
+    }
+    __syncthreads();
+    int32_t e = st->e_key;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        unsigned long long a;
+        if (keys) {
+            a = (unsigned long long)keys[i];
+        } else {
+            double g, h;
+            row_gh<kSrc>(src, i, &g, &h);
+            a = (unsigned long long)(long long)rint(ldexp(mvs_r(g, h, lambda), e));
+        }
+        if (a < lo) continue;
+        unsigned long long b = (a - lo) >> shift;
+        if (b >= (unsigned long long)nb) continue;
+        atomicAdd(&scnt[b], 1u);
+        atomicAdd(&ssum[b], a);
+    }
+    __syncthreads();
+    for (int t = threadIdx.x; t < nb; t += blockDim.x) {
+        if (scnt[t]) {
+            atomicAdd(&hcnt[t], (unsigned long long)scnt[t]);
+            atomicAdd(&hsum[t], ssum[t]);
+        }
+    }
+}
+
+// cond(T): sum_{a<T} a <= (K - #{a>=T}) * T, exactly (T >= 1).
+__device__ inline bool thresh_ok(unsigned long long F, unsigned long long C, int64_t K,
+                                 unsigned long long T)
+{
+    if (T == 0) return false;
+    if ((unsigned long long)K < C) return false;
+    unsigned long long d = (unsigned long long)K - C;
+    unsigned long long hi = __umul64hi(d, T), lo = d * T;
+    return hi != 0 || lo >= F;
+}
+
+// One block of 256 threads: evaluate every bucket boundary, keep the least
+// one that satisfies cond, descend into the bucket below it, clear the
+// histogram for the next level.
+__global__ void __launch_bounds__(256) k_mvs_radix_decide(SampleState *__restrict__ st, int64_t K,
+                                                          unsigned long long *__restrict__ hcnt,
+                                                          unsigned long long *__restrict__ hsum)
+{
+    __shared__ unsigned long long s_c[kDigitBuckets + 1], s_f[kDigitBuckets + 1];
+    __shared__ int s_best;
+    if (st->done) return;
+    const int32_t nb = st->nbuckets;
+    const int shift = st->shift;
+    const unsigned long long lo = (unsigned long long)st->lo;
+    if (threadIdx.x == 0) {
+        // serial prefix/suffix over at most 2048 buckets
+        unsigned long long f = st->F_below;
+        for (int b = 0; b <= nb; ++b) {
+            s_f[b] = f;
+            if (b < nb) f += hsum[b];
+        }
+        unsigned long long cabove = st->C_above;
+        for (int b = nb; b >= 0; --b) {
+            s_c[b] = cabove;
+            if (b > 0) cabove += hcnt[b - 1];
+        }
+        s_best = nb + 1;
+    }
+    __syncthreads();
+    for (int b = threadIdx.x; b <= nb; b += blockDim.x) {
+        unsigned long long T = lo + ((unsigned long long)b << shift);
+        if (thresh_ok(s_f[b], s_c[b], K, T)) atomicMin(&s_best, b);
+    }
+    __syncthreads();
+    int best = s_best;
+    if (threadIdx.x == 0) {
+        if (best > nb || best == 0) {
+            // cannot happen when the invariant holds; report instead of looping
+            st->bad |= 2u;
+            st->done = 1;
+        } else if (shift == 0) {
+            st->T = (long long)(lo + (unsigned long long)best);
+            st->done = 1;
+        } else {
+            st->F_below = s_f[best - 1];
+            st->C_above = s_c[best];
+            st->lo = (long long)(lo + ((unsigned long long)(best - 1) << shift));
+            int ns = shift > kDigitBits ? shift - kDigitBits : 0;
+            st->nbuckets = 1 << (shift - ns);
+            st->shift = ns;
+        }
+    }
+    for (int b = threadIdx.x; b < nb; b += blockDim.x) {
+        hcnt[b] = 0;
+        hsum[b] = 0;
+    }
+}
+
+template <int kSrc>
+__global__ void __launch_bounds__(256) k_mvs_select(SampleSrc src, const int64_t *__restrict__ keys,
+                                                    int64_t n, double lambda,
+                                                    const SampleState *__restrict__ st,
+                                                    uint64_t seed, uint64_t iteration,
+                                                    int64_t row_offset, uint8_t *__restrict__ keep)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    unsigned long long a;
+    if (keys) {
+        a = (unsigned long long)keys[i];
+    } else {
+        double g, h;
+        row_gh<kSrc>(src, i, &g, &h);
+        a = (unsigned long long)(long long)rint(ldexp(mvs_r(g, h, lambda), st->e_key));
+    }
+    unsigned long long T = (unsigned long long)st->T;
+    bool k;
+    if (a >= T) {
+        k = true;
+    } else {
+        uint64_t U = philox_word0((uint64_t)(row_offset + i), iteration, 0, 0, seed, 0);
+        k = __umul64hi(U, T) < a;
+    }
+    keep[i] = k ? 1 : 0;
+}
+
+// Gather the kept rows (ascending) into the sampled page and reweight their
+// gradients by the inverse inclusion probability.
+template <int kSrc>
+__global__ void __launch_bounds__(256) k_compact(SampleSrc src, const int64_t *__restrict__ keys,
+                                                 int64_t n, double lambda,
+                                                 const SampleState *__restrict__ st,
+                                                 const uint8_t *__restrict__ keep,
+                                                 const int32_t *__restrict__ pos,
+                                                 const uint4 *__restrict__ page, int32_t row_q4,
+                                                 int64_t out_base, uint4 *__restrict__ out_page,
+                                                 int32_t *__restrict__ sel, int64_t sel_offset,
+                                                 double2 *__restrict__ gw)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n || !keep[i]) return;
+    int64_t k = (int64_t)pos[i] - out_base;
+    const uint4 *src_row = page + i * row_q4;
+    uint4 *dst = out_page + k * row_q4;
+    for (int32_t t = 0; t < row_q4; ++t) dst[t] = src_row[t];
+    sel[k] = (int32_t)(sel_offset + i);
+    double g, h;
+    row_gh<kSrc>(src, i, &g, &h);
+    unsigned long long a;
+    if (keys)
+        a = (unsigned long long)keys[i];
+    else
+        a = (unsigned long long)(long long)rint(ldexp(mvs_r(g, h, lambda), st->e_key));
+    unsigned long long T = (unsigned long long)st->T;
+    double w = a >= T ? 1.0 : (double)(long long)T / (double)(long long)a;
+    gw[k] = make_double2(g * w, h * w);
+}
+
+// f = 1: every row trains, unweighted.
+__global__ void k_gw_all(const float2 *__restrict__ gpair, int64_t n, double2 *__restrict__ gw)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    float2 p = gpair[i];
+    gw[i] = make_double2((double)p.x, (double)p.y);
+}
+
+// ------------------------------------------------------------ fixed point
+__global__ void __launch_bounds__(256) k_fx_max(const double2 *__restrict__ gw, int64_t R,
+                                                SampleState *__restrict__ st)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    unsigned long long bg = 0, bh = 0;
+    if (i < R) {
+        double2 v = gw[i];
+        bg = __double_as_longlong(fabs(v.x));
+        bh = __double_as_longlong(fabs(v.y));
+    }
+    for (int d = 32; d > 0; d >>= 1) {
+        unsigned long long og = __shfl_xor(bg, d, 64), oh = __shfl_xor(bh, d, 64);
+        bg = og > bg ? og : bg;
+        bh = oh > bh ? oh : bh;
+    }
+    if ((threadIdx.x & 63) == 0) {
+        if (bg) atomicMax(&st->gmax_bits, bg);
+        if (bh) atomicMax(&st->hmax_bits, bh);
+    }
+}
+
+// q = rint((g', h') * 2^(e_g, e_h)), e = 62 - E - ceil(log2 R); also the
+// root sums (integer, order independent).
+__global__ void __launch_bounds__(256) k_fx_convert(const double2 *__restrict__ gw, int64_t R,
+                                                    int32_t log2R, SampleState *__restrict__ st,
+                                                    longlong2 *__restrict__ q)
+{
+    int Eg, Eh;
+    frexp(__longlong_as_double(st->gmax_bits), &Eg);
+    frexp(__longlong_as_double(st->hmax_bits), &Eh);
+    int32_t eg = 62 - Eg - log2R, eh = 62 - Eh - log2R;
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    long long qg = 0, qh = 0;
+    if (i < R) {
+        double2 v = gw[i];
+        qg = (long long)rint(ldexp(v.x, eg));
+        qh = (long long)rint(ldexp(v.y, eh));
+        q[i] = make_longlong2(qg, qh);
+    }
+    for (int d = 32; d > 0; d >>= 1) {
+        qg += __shfl_xor(qg, d, 64);
+        qh += __shfl_xor(qh, d, 64);
+    }
+    if ((threadIdx.x & 63) == 0) {
+        atomicAdd(&st->root_g, (unsigned long long)qg);
+        atomicAdd(&st->root_h, (unsigned long long)qh);
+    }
+    if (i == 0) {
+        st->e_g = eg;
+        st->e_h = eh;
+    }
+}
+
+__global__ void k_state_init(SampleState *st)
+{
+    if (threadIdx.x == 0) {
+        SampleState z = {};
+        *st = z;
+    }
+}
+
+__global__ void k_zero_u64(unsigned long long *p, int64_t n)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0ull;
+}
+
+static unsigned blocks(int64_t n, int t = 256) { return (unsigned)((n + t - 1) / t); }
+
+static int32_t log2_ceil(int64_t v) { return v <= 1 ? 0 : ceil_log2_u64((uint64_t)v); }
+
+// ------------------------------------------------------------ drivers
+gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
+                         double lambda, int64_t K, SampleState *st, SampleState *host_st)
+{
+    int32_t l2 = log2_ceil(n);
+    unsigned long long *hist = nullptr;
+    GBT_TRY(scratch_t(c, kScrMisc, 2 * kDigitBuckets, &hist));
+    if (n > 0) {
+        if (kind == kSrcGpair)
+            k_mvs_rmax<kSrcGpair><<<blocks(n), 256, 0, c->stream>>>(src, n, lambda, st);
+        else
+            k_mvs_rmax<kSrcMargin><<<blocks(n), 256, 0, c->stream>>>(src, n, lambda, st);
+        GBT_LAUNCHED();
+        if (kind == kSrcGpair)
+            k_mvs_keys<kSrcGpair><<<blocks(n), 256, 0, c->stream>>>(src, n, lambda, l2, st, (int64_t *)keys);
+        else
+            k_mvs_keys<kSrcMargin><<<blocks(n), 256, 0, c->stream>>>(src, n, lambda, l2, st, (int64_t *)keys);
+        GBT_LAUNCHED();
+    }
+    k_mvs_thresh_init<<<1, 64, 0, c->stream>>>(st, K);
+    GBT_LAUNCHED();
+    k_zero_u64<<<blocks(2 * kDigitBuckets), 256, 0, c->stream>>>(hist, 2 * kDigitBuckets);
+    GBT_LAUNCHED();
+    GBT_HIP(hipMemcpyAsync(host_st, st, sizeof(SampleState), hipMemcpyDeviceToHost, c->stream));
+    GBT_HIP(hipStreamSynchronize(c->stream));
+    if (host_st->bad & 1u) return set_error(GBT_E_INVALID, "non-finite gradient in sampling");
+    unsigned grid = (unsigned)std::min<int64_t>(std::max<int64_t>(blocks(n), 1), 4 * kCUs);
+    for (int lev = 0; lev < host_st->levels; ++lev) {
+        if (kind == kSrcGpair)
+            k_mvs_radix_hist<kSrcGpair><<<grid, 256, 0, c->stream>>>(src, keys, n, lambda, l2, st, hist,
+                                                                     hist + kDigitBuckets);
+        else
+            k_mvs_radix_hist<kSrcMargin><<<grid, 256, 0, c->stream>>>(src, keys, n, lambda, l2, st, hist,
+                                                                      hist + kDigitBuckets);
+        GBT_LAUNCHED();
+        k_mvs_radix_decide<<<1, 256, 0, c->stream>>>(st, K, hist, hist + kDigitBuckets);
+        GBT_LAUNCHED();
+    }
+    return GBT_OK;
+}
+
+gbt_status mvs_select(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
+                      double lambda, const SampleState *st, uint64_t seed, uint64_t iteration,
+                      int64_t row_offset, uint8_t *keep)
+{
+    if (n == 0) return GBT_OK;
+    if (kind == kSrcGpair)
+        k_mvs_select<kSrcGpair><<<blocks(n), 256, 0, c->stream>>>(src, keys, n, lambda, st, seed,
+                                                                  iteration, row_offset, keep);
+    else
+        k_mvs_select<kSrcMargin><<<blocks(n), 256, 0, c->stream>>>(src, keys, n, lambda, st, seed,
+                                                                   iteration, row_offset, keep);
+    GBT_LAUNCHED();
+    return GBT_OK;
+}
+
+gbt_status mvs_compact(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
+                       double lambda, const SampleState *st, const uint8_t *keep, const int32_t *pos,
+                       const uint32_t *page, int32_t row_words, int64_t out_base, uint32_t *out_page,
+                       int32_t *sel, int64_t sel_offset, double *gw)
+{
+    if (n == 0) return GBT_OK;
+    if (kind == kSrcGpair)
+        k_compact<kSrcGpair><<<blocks(n), 256, 0, c->stream>>>(
+            src, keys, n, lambda, st, keep, pos, (const uint4 *)page, row_words / 4, out_base,
+            (uint4 *)out_page, sel, sel_offset, (double2 *)gw);
+    else
+        k_compact<kSrcMargin><<<blocks(n), 256, 0, c->stream>>>(
+            src, keys, n, lambda, st, keep, pos, (const uint4 *)page, row_words / 4, out_base,
+            (uint4 *)out_page, sel, sel_offset, (double2 *)gw);
+    GBT_LAUNCHED();
+    return GBT_OK;
+}
+
+gbt_status gw_all(gbt_ctx *c, const float *gpair, int64_t n, double *gw)
+{
+    if (n == 0) return GBT_OK;
+    k_gw_all<<<blocks(n), 256, 0, c->stream>>>((const float2 *)gpair, n, (double2 *)gw);
+    GBT_LAUNCHED();
+    return GBT_OK;
+}
+
+gbt_status fixed_point(gbt_ctx *c, const double *gw, int64_t R, SampleState *st, int64_t *q)
+{
+    if (R == 0) {
+        k_fx_convert<<<1, 256, 0, c->stream>>>((const double2 *)gw, 0, 0, st, (longlong2 *)q);
+        GBT_LAUNCHED();
+        return GBT_OK;
+    }
+    k_fx_max<<<blocks(R), 256, 0, c->stream>>>((const double2 *)gw, R, st);
+    GBT_LAUNCHED();
+    k_fx_convert<<<blocks(R), 256, 0, c->stream>>>((const double2 *)gw, R, log2_ceil(R), st,
+                                                   (longlong2 *)q);
+    GBT_LAUNCHED();
+    return GBT_OK;
+}
+
+gbt_status state_init(gbt_ctx *c, SampleState *st)
+{
+    k_state_init<<<1, 64, 0, c->stream>>>(st);
+    GBT_LAUNCHED();
+    return GBT_OK;
+}
+
+}  // namespace gbt

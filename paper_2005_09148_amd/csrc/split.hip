@@ -1,0 +1,411 @@
+// split.hip -- Alg. 1 EvaluateSplit with the loss reduction of Eq. 8, and
+// Alg. 1 RepartitionInstances (stable, scan based).
+//
+// Evaluation: one wavefront per (node, feature).  Each lane holds four
+// consecutive bins; an int64 wavefront prefix scan gives the left sums of
+// every cut s, the missing sums come from node sum minus the feature's bin
+// total, and every (s, direction) gain is computed in double exactly as
+// 0.5*((G_L^2/(H_L+l) + G_R^2/(H_R+l)) - G^2/(H+l)) - gamma.  The best is
+// the highest gain; ties go to the lower feature, then the lower s, then
+// missing-right.
+//
+// Partition: per training slot a left flag from the row's symbol of the
+// split feature, a device-wide exclusive scan of the flags, and a scatter
+// that writes [left | right] of every splitting segment in input order.
+#include "split_impl.h"
+
+#include <cstring>
+
+namespace gbt {
+
+constexpr int kEvalThreads = 256;
+constexpr int kFeatPerBlock = 16;
+
+struct Cand {
+    double gain;
+    int32_t order;  // s*2 + dir within a feature, or feature index across features
+    int32_t valid;
+    long long lg, lh;
+};
+
+__device__ inline bool better(const Cand &a, const Cand &b)
+{
+    // a strictly preferred over b
+    if (!a.valid) return false;
+    if (!b.valid) return true;
+    if (a.gain > b.gain) return true;
+    if (a.gain < b.gain) return false;
+    return a.order < b.order;
+}
+
+__device__ inline double fx(long long Q, int32_t e) { return ldexp((double)Q, -e); }
+
+__device__ inline double eq8_gain(double GL, double HL, double GR, double HR, double G, double H,
+                                  double lambda, double gamma)
+{
+    double a = (GL * GL) / (HL + lambda);
+    double b = (GR * GR) / (HR + lambda);
+    double c = (G * G) / (H + lambda);
+    return 0.5 * ((a + b) - c) - gamma;
+}
+
+__device__ inline Cand wave_best(Cand x)
+{
+    for (int d = 32; d > 0; d >>= 1) {
+        Cand o;
+        o.gain = __shfl_xor(x.gain, d, 64);
+        o.order = __shfl_xor(x.order, d, 64);
+        o.valid = __shfl_xor(x.valid, d, 64);
+        o.lg = __shfl_xor(x.lg, d, 64);
+        o.lh = __shfl_xor(x.lh, d, 64);
+        if (better(o, x)) x = o;
+    }
+    return x;
+}
+
+__device__ inline long long wave_sum(long long v)
+{
+    for (int d = 32; d > 0; d >>= 1) v += __shfl_xor(v, d, 64);
+    return v;
+}
+
+// Best split of one feature for one node, evaluated by one wavefront.  The
+// result (valid in every lane) carries order = s*2 + dir.
+__device__ Cand eval_feature(const longlong2 *__restrict__ hj, int32_t B, long long Qg, long long Qh,
+                             const EvalParams &ep)
+{
+    const int lane = threadIdx.x & 63;
+    Cand best;
+    best.valid = 0;
+    best.gain = 0.0;
+    best.order = 0;
+    best.lg = best.lh = 0;
+    // totals over the feature's bins -> missing sums
+    long long tg = 0, th = 0;
+    for (int32_t b = lane; b < B; b += 64) {
+        longlong2 v = hj[b];
+        tg += v.x;
+        th += v.y;
+    }
+    tg = wave_sum(tg);
+    th = wave_sum(th);
+    const long long mg = Qg - tg, mh = Qh - th;
+    const double G = fx(Qg, ep.e_g), H = fx(Qh, ep.e_h);
+    long long carry_g = 0, carry_h = 0;
+    for (int32_t base = 0; base < B; base += 256) {
+        longlong2 v[4];
+        long long sg = 0, sh = 0;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            int32_t b = base + lane * 4 + t;
+            v[t] = b < B ? hj[b] : make_longlong2(0, 0);
+            sg += v[t].x;
+            sh += v[t].y;
+        }
+        // exclusive wavefront scan of the lane totals
+        long long xg = sg, xh = sh;
+        for (int d = 1; d < 64; d <<= 1) {
+            long long yg = __shfl_up(xg, d, 64), yh = __shfl_up(xh, d, 64);
+            if (lane >= d) {
+                xg += yg;
+                xh += yh;
+            }
+        }
+        long long pg = carry_g + xg - sg, ph = carry_h + xh - sh;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            int32_t b = base + lane * 4 + t;
+            pg += v[t].x;
+            ph += v[t].y;
+            int32_t s = b + 1;  // left = bins < s
+            if (s > B - 1) continue;
+#pragma unroll
+            for (int dir = 0; dir < 2; ++dir) {
+                long long lg = pg + (dir ? mg : 0), lh = ph + (dir ? mh : 0);
+                double GL = fx(lg, ep.e_g), HL = fx(lh, ep.e_h);
+                double GR = fx(Qg - lg, ep.e_g), HR = fx(Qh - lh, ep.e_h);
+                if (!(HL >= ep.mcw && HR >= ep.mcw)) continue;
+                double gain = eq8_gain(GL, HL, GR, HR, G, H, ep.lambda, ep.gamma);
+                if (gain != gain) continue;
+                Cand c;
+                c.gain = gain;
+                c.order = s * 2 + dir;
+                c.valid = 1;
+                c.lg = lg;
+                c.lh = lh;
+                if (better(c, best)) best = c;
+            }
+        }
+        carry_g += __shfl(xg, 63, 64);
+        carry_h += __shfl(xh, 63, 64);
+    }
+    return wave_best(best);
+}
+
+__global__ void __launch_bounds__(kEvalThreads)
+    k_eval(const longlong2 *__restrict__ hist, int64_t total_bins, const EvalNode *__restrict__ nodes,
+           const int32_t *__restrict__ bin_ptr, int32_t m, EvalParams ep, EvalCand *__restrict__ out)
+{
+    __shared__ EvalCand wbest[kEvalThreads / 64];
+    const EvalNode nd = nodes[blockIdx.y];
+    const int wid = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const longlong2 *h = hist + (int64_t)nd.slot * total_bins;
+    EvalCand mine;
+    mine.valid = 0;
+    mine.gain = 0.0;
+    mine.feature = -1;
+    mine.split_bin = -1;
+    mine.default_left = 0;
+    mine.lg = mine.lh = 0;
+    const int32_t f_end = min(m, (int32_t)(blockIdx.x + 1) * kFeatPerBlock);
+    for (int32_t j = blockIdx.x * kFeatPerBlock + wid; j < f_end; j += kEvalThreads / 64) {
+        const int32_t b0 = bin_ptr[j], B = bin_ptr[j + 1] - b0;
+        if (B < 2) continue;
+        Cand c = eval_feature(h + b0, B, nd.sum_g, nd.sum_h, ep);
+        // features visited in ascending order: keep the first of equal gains
+        if (c.valid && (!mine.valid || c.gain > mine.gain)) {
+            mine.valid = 1;
+            mine.gain = c.gain;
+            mine.feature = j;
+            mine.split_bin = c.order >> 1;
+            mine.default_left = c.order & 1;
+            mine.lg = c.lg;
+            mine.lh = c.lh;
+        }
+    }
+    if (lane == 0) wbest[wid] = mine;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        EvalCand b = wbest[0];
+        for (int w = 1; w < kEvalThreads / 64; ++w) {
+            const EvalCand &o = wbest[w];
+            if (!o.valid) continue;
+            if (!b.valid || o.gain > b.gain || (o.gain == b.gain && o.feature < b.feature)) b = o;
+        }
+        out[(int64_t)blockIdx.y * gridDim.x + blockIdx.x] = b;
+    }
+}
+
+// Reduce the per-feature-block candidates of each node into a gbt_split.
+__global__ void k_eval_reduce(const EvalCand *__restrict__ cand, int32_t n_fblocks,
+                              const EvalNode *__restrict__ nodes, int32_t n_nodes,
+                              gbt_split *__restrict__ out)
+{
+    int32_t k = blockIdx.x * blockDim.x + threadIdx.x;
+    if (k >= n_nodes) return;
+    EvalCand b;
+    b.valid = 0;
+    for (int32_t f = 0; f < n_fblocks; ++f) {
+        const EvalCand &o = cand[(int64_t)k * n_fblocks + f];
+        if (!o.valid) continue;
+        if (!b.valid || o.gain > b.gain) b = o;
+    }
+    gbt_split s;
+    s.valid = b.valid;
+    s.gain = b.valid ? b.gain : 0.0;
+    s.feature = b.valid ? b.feature : -1;
+    s.split_bin = b.valid ? b.split_bin : -1;
+    s.default_left = b.valid ? b.default_left : 0;
+    s.left_g = b.valid ? b.lg : 0;
+    s.left_h = b.valid ? b.lh : 0;
+    s.right_g = b.valid ? nodes[k].sum_g - b.lg : 0;
+    s.right_h = b.valid ? nodes[k].sum_h - b.lh : 0;
+    out[k] = s;
+}
+
+gbt_status eval_impl(gbt_ctx *c, const gbt_matrix *mx, const int64_t *hist, const EvalNode *nodes_d,
+                     int32_t n_nodes, const EvalParams &ep, gbt_split *out_d)
+{
+    if (n_nodes == 0) return GBT_OK;
+    int32_t nfb = (mx->m + kFeatPerBlock - 1) / kFeatPerBlock;
+    EvalCand *cand;
+    GBT_TRY(scratch_t(c, kScrEval, (size_t)n_nodes * nfb, &cand));
+    dim3 grid((unsigned)nfb, (unsigned)n_nodes);
+    k_eval<<<grid, kEvalThreads, 0, c->stream>>>((const longlong2 *)hist, mx->total_bins, nodes_d,
+                                                 mx->bin_ptr_d, mx->m, ep, cand);
+    GBT_LAUNCHED();
+    k_eval_reduce<<<(n_nodes + 127) / 128, 128, 0, c->stream>>>(cand, nfb, nodes_d, n_nodes, out_d);
+    GBT_LAUNCHED();
+    return GBT_OK;
+}
+
+// ------------------------------------------------------------ partition
+// node of slot i: slot_node[i] when given, else position[rows[i]]
+__global__ void k_part_flags(const int32_t *__restrict__ rows, int64_t n, const uint32_t *__restrict__ page,
+                             Geo geo, const int32_t *__restrict__ position,
+                             const int32_t *__restrict__ slot_node, const DevNode *__restrict__ nodes,
+                             uint8_t *__restrict__ flags)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    int32_t r = rows[i];
+    int32_t nid = slot_node ? slot_node[i] : position[r];
+    uint8_t f = 0;
+    if (nid >= 0 && nodes[nid].split) {
+        const DevNode &nd = nodes[nid];
+        int32_t b = row_feature_bin(page + (int64_t)r * geo.row_words, geo, nd.feature);
+        f = (b < 0) ? (uint8_t)(nd.default_left != 0) : (uint8_t)(b < nd.split_bin);
+    }
+    flags[i] = f;
+}
+
+__global__ void k_part_scatter(const int32_t *__restrict__ rows, int64_t n,
+                               const uint8_t *__restrict__ flags, const int32_t *__restrict__ P,
+                               int32_t *__restrict__ position, const int32_t *__restrict__ slot_node,
+                               const DevNode *__restrict__ nodes, int32_t *__restrict__ rows_out)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    int32_t r = rows[i];
+    int32_t nid = slot_node ? slot_node[i] : position[r];
+    if (nid < 0 || !nodes[nid].split) {
+        rows_out[i] = r;
+        return;
+    }
+    const DevNode &nd = nodes[nid];
+    int64_t b = nd.begin, e = nd.end;
+    int64_t nl = (int64_t)P[e] - P[b];
+    int64_t pl = (int64_t)P[i] - P[b];
+    int64_t dest;
+    int32_t child;
+    if (flags[i]) {
+        dest = b + pl;
+        child = nd.left_child;
+    } else {
+        dest = b + nl + (i - b - pl);
+        child = nd.right_child;
+    }
+    rows_out[dest] = r;
+    position[r] = child;
+}
+
+gbt_status partition_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int32_t *rows,
+                          int64_t n, int32_t *position, const int32_t *slot_node,
+                          const DevNode *nodes, int32_t *rows_out, int32_t **P_out)
+{
+    if (n == 0) {
+        *P_out = nullptr;
+        return GBT_OK;
+    }
+    uint8_t *flags;
+    int32_t *P;
+    GBT_TRY(scratch_t(c, kScrPartFlags, (size_t)n, &flags));
+    GBT_TRY(scratch_t(c, kScrPartPos, (size_t)n + 1, &P));
+    Geo geo = geo_of(mx);
+    unsigned grid = (unsigned)((n + 255) / 256);
+    k_part_flags<<<grid, 256, 0, c->stream>>>(rows, n, page, geo, position, slot_node, nodes, flags);
+    GBT_LAUNCHED();
+    GBT_TRY(scan_u8(c, flags, n, P));
+    k_part_scatter<<<grid, 256, 0, c->stream>>>(rows, n, flags, P, position, slot_node, nodes, rows_out);
+    GBT_LAUNCHED();
+    *P_out = P;
+    return GBT_OK;
+}
+
+}  // namespace gbt
+
+using namespace gbt;
+
+extern "C" {
+
+gbt_status gbt_eval_splits(gbt_ctx *c, const gbt_matrix *layout, const int64_t *hist_d,
+                           const int64_t *node_sum_d, const int32_t *node_slot_h, int32_t n_nodes,
+                           const gbt_train_params *tp, int32_t exp_g, int32_t exp_h, gbt_split *out_d)
+{
+    GBT_CHECK(c && layout && tp && out_d, "gbt_eval_splits: NULL argument");
+    GBT_CHECK(n_nodes >= 0, "negative node count");
+    if (n_nodes == 0) return GBT_OK;
+    GBT_CHECK(hist_d && node_sum_d && node_slot_h, "gbt_eval_splits: NULL input");
+    GBT_TRY(set_device(c));
+    std::vector<int64_t> sums(2 * (size_t)n_nodes);
+    GBT_HIP(hipMemcpyAsync(sums.data(), node_sum_d, sums.size() * 8, hipMemcpyDeviceToHost, c->stream));
+    GBT_HIP(hipStreamSynchronize(c->stream));
+    std::vector<EvalNode> nodes(n_nodes);
+    for (int32_t k = 0; k < n_nodes; ++k) {
+        nodes[k].sum_g = sums[2 * k];
+        nodes[k].sum_h = sums[2 * k + 1];
+        nodes[k].slot = node_slot_h[k];
+        nodes[k].heap = k;
+    }
+    EvalNode *nodes_d;
+    GBT_TRY(scratch_t(c, kScrEvalNodes, (size_t)n_nodes, &nodes_d));
+    GBT_HIP(hipMemcpyAsync(nodes_d, nodes.data(), nodes.size() * sizeof(EvalNode), hipMemcpyHostToDevice,
+                           c->stream));
+    EvalParams ep{tp->lambda, tp->gamma, tp->min_child_weight, exp_g, exp_h};
+    GBT_TRY(eval_impl(c, layout, hist_d, nodes_d, n_nodes, ep, out_d));
+    GBT_HIP(hipStreamSynchronize(c->stream));
+    return GBT_OK;
+}
+
+__global__ void k_fill_slot_node(const gbt_seg *__restrict__ segs, int32_t n_nodes,
+                                 int32_t *__restrict__ slot_node, int64_t n)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    int32_t k = -1;
+    for (int32_t t = 0; t < n_nodes; ++t)
+        if (i >= segs[t].begin && i < segs[t].end) k = t;
+    slot_node[i] = k;
+}
+
+gbt_status gbt_partition(gbt_ctx *c, const gbt_matrix *layout, const uint32_t *page_d,
+                         const gbt_split *split_h, const gbt_seg *seg_h, const int32_t *child_h,
+                         int32_t n_nodes, int32_t *rows_d, int32_t *rows_tmp_d, int64_t n_rows,
+                         int32_t *position_d, gbt_seg *seg_out_h)
+{
+    GBT_CHECK(c && layout && page_d && split_h && seg_h && child_h && rows_d && rows_tmp_d && position_d,
+              "gbt_partition: NULL argument");
+    GBT_CHECK(n_nodes >= 0 && n_rows >= 0, "negative sizes");
+    for (int32_t k = 0; k < n_nodes; ++k) {
+        GBT_CHECK(seg_h[k].begin >= 0 && seg_h[k].begin <= seg_h[k].end && seg_h[k].end <= n_rows,
+                  "segment %d outside [0, n_rows]", k);
+        if (split_h[k].valid)
+            GBT_CHECK(split_h[k].feature >= 0 && split_h[k].feature < layout->m, "split feature %d", k);
+    }
+    GBT_TRY(set_device(c));
+    std::vector<DevNode> nodes(std::max(n_nodes, 1));
+    for (int32_t k = 0; k < n_nodes; ++k) {
+        DevNode &d = nodes[k];
+        memset(&d, 0, sizeof(d));
+        d.begin = seg_h[k].begin;
+        d.end = seg_h[k].end;
+        d.present = 1;
+        d.split = split_h[k].valid ? 1 : 0;
+        d.feature = split_h[k].feature;
+        d.split_bin = split_h[k].split_bin;
+        d.default_left = split_h[k].default_left;
+        d.left_child = child_h[2 * k];
+        d.right_child = child_h[2 * k + 1];
+    }
+    DevNode *nodes_d;
+    gbt_seg *segs_d;
+    int32_t *slot_node;
+    GBT_TRY(scratch_t(c, kScrNodes, nodes.size(), &nodes_d));
+    GBT_TRY(scratch_t(c, kScrEvalNodes, (size_t)std::max(n_nodes, 1), &segs_d));
+    GBT_TRY(scratch_t(c, kScrSlotNode, (size_t)std::max<int64_t>(n_rows, 1), &slot_node));
+    GBT_HIP(hipMemcpyAsync(nodes_d, nodes.data(), nodes.size() * sizeof(DevNode), hipMemcpyHostToDevice, c->stream));
+    if (n_nodes)
+        GBT_HIP(hipMemcpyAsync(segs_d, seg_h, n_nodes * sizeof(gbt_seg), hipMemcpyHostToDevice, c->stream));
+    if (n_rows) {
+        k_fill_slot_node<<<(unsigned)((n_rows + 255) / 256), 256, 0, c->stream>>>(segs_d, n_nodes, slot_node, n_rows);
+        GBT_LAUNCHED();
+    }
+    int32_t *P = nullptr;
+    GBT_TRY(partition_impl(c, layout, page_d, rows_d, n_rows, position_d, slot_node, nodes_d, rows_tmp_d, &P));
+    if (n_rows)
+        GBT_HIP(hipMemcpyAsync(rows_d, rows_tmp_d, (size_t)n_rows * 4, hipMemcpyDeviceToDevice, c->stream));
+    std::vector<int32_t> Ph(n_rows + 1, 0);
+    if (P) GBT_HIP(hipMemcpyAsync(Ph.data(), P, (size_t)(n_rows + 1) * 4, hipMemcpyDeviceToHost, c->stream));
+    GBT_HIP(hipStreamSynchronize(c->stream));
+    if (seg_out_h) {
+        for (int32_t k = 0; k < n_nodes; ++k) {
+            int64_t b = seg_h[k].begin, e = seg_h[k].end;
+            int64_t nl = split_h[k].valid ? (int64_t)Ph[e] - Ph[b] : e - b;
+            seg_out_h[2 * k] = {child_h[2 * k], 0, b, b + nl};
+            seg_out_h[2 * k + 1] = {child_h[2 * k + 1], 0, b + nl, e};
+        }
+    }
+    return GBT_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,42 @@
+// split_impl.h -- internal interface of split evaluation and partitioning
+// (split.hip) used by the tree driver.
+#pragma once
+
+#include "common.h"
+
+namespace gbt {
+
+struct EvalParams {
+    double lambda;
+    double gamma;
+    double mcw;
+    int32_t e_g;
+    int32_t e_h;
+};
+
+struct EvalNode {
+    long long sum_g, sum_h;
+    int32_t slot;   // histogram slot
+    int32_t heap;   // node id
+};
+
+struct EvalCand {
+    double gain;
+    long long lg, lh;
+    int32_t feature;
+    int32_t split_bin;
+    int32_t default_left;
+    int32_t valid;
+};
+
+gbt_status eval_impl(gbt_ctx *c, const gbt_matrix *mx, const int64_t *hist, const EvalNode *nodes_d,
+                     int32_t n_nodes, const EvalParams &ep, gbt_split *out_d);
+// Stable partition of rows[0, n) by each slot's node (slot_node[i], or
+// position[rows[i]] when slot_node is NULL).  rows_out receives the new
+// order, position[row] the child id.  *P receives the exclusive scan of the
+// left flags (n+1 entries, device).
+gbt_status partition_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int32_t *rows,
+                          int64_t n, int32_t *position, const int32_t *slot_node,
+                          const DevNode *nodes, int32_t *rows_out, int32_t **P);
+
+}  // namespace gbt

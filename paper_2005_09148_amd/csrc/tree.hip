@@ -1,0 +1,791 @@
+// tree.hip -- one boosting iteration (Alg. 7 then Alg. 1 of the paper), the
+// Eq. 6 leaves with the Eq. 1 margin update, Eq. 1 prediction, and the page
+// streamer that feeds pinned-host ELLPACK pages to the device on a second
+// stream, double buffered and overlapped with the kernels that consume them.
+#include <algorithm>
+#include <chrono>
+#include <cstring>
+#include <functional>
+
+#include "sample_impl.h"
+#include "split_impl.h"
+
+namespace gbt {
+
+static unsigned blocks(int64_t n, int t = 256) { return (unsigned)((n + t - 1) / t); }
+
+// ------------------------------------------------------------ page streamer
+// Calls fn(words_d, row0, rows) for consecutive row chunks of every page.
+// Device pages are passed in place; pinned-host pages are copied chunk by
+// chunk on the side stream into two alternating device buffers, the copy of
+// chunk c+1 overlapping the compute on chunk c.
+using ChunkFn = std::function<gbt_status(const uint32_t *, int64_t, int64_t)>;
+
+struct StreamEvents {
+    hipEvent_t copied[2] = {nullptr, nullptr};
+    hipEvent_t consumed[2] = {nullptr, nullptr};
+    ~StreamEvents()
+    {
+        for (int i = 0; i < 2; ++i) {
+            if (copied[i]) (void)hipEventDestroy(copied[i]);
+            if (consumed[i]) (void)hipEventDestroy(consumed[i]);
+        }
+    }
+};
+
+static int64_t g_stream_chunk_rows = (int64_t)1 << 22;
+
+gbt_status for_each_chunk(gbt_ctx *c, const gbt_matrix *mx, const ChunkFn &fn, double *h2d_bytes)
+{
+    struct Chunk {
+        const GbtPage *pg;
+        int64_t off, rows;
+    };
+    std::vector<Chunk> host_chunks;
+    for (const auto &pg : mx->pages) {
+        if (!pg.host) {
+            if (pg.rows) GBT_TRY(fn(pg.words, pg.row0, pg.rows));
+            continue;
+        }
+        for (int64_t o = 0; o < pg.rows; o += g_stream_chunk_rows)
+            host_chunks.push_back({&pg, o, std::min(g_stream_chunk_rows, pg.rows - o)});
+    }
+    if (host_chunks.empty()) return GBT_OK;
+    const size_t row_bytes = (size_t)mx->row_words * 4;
+    int64_t maxrows = 0;
+    for (auto &ch : host_chunks) maxrows = std::max(maxrows, ch.rows);
+    uint32_t *buf[2];
+    GBT_TRY(scratch(c, kScrStage0, (size_t)maxrows * row_bytes, (void **)&buf[0]));
+    GBT_TRY(scratch(c, kScrStage1, (size_t)maxrows * row_bytes, (void **)&buf[1]));
+    StreamEvents ev;
+    for (int i = 0; i < 2; ++i) {
+        GBT_HIP(hipEventCreateWithFlags(&ev.copied[i], hipEventDisableTiming));
+        GBT_HIP(hipEventCreateWithFlags(&ev.consumed[i], hipEventDisableTiming));
+    }
+    // the buffers may still be read by earlier work on the compute stream
+    GBT_HIP(hipEventRecord(ev.consumed[0], c->stream));
+    GBT_HIP(hipEventRecord(ev.consumed[1], c->stream));
+    auto issue = [&](size_t k) -> gbt_status {
+        const Chunk &ch = host_chunks[k];
+        int b = (int)(k & 1);
+        GBT_HIP(hipStreamWaitEvent(c->side, ev.consumed[b], 0));
+        GBT_HIP(hipMemcpyAsync(buf[b], ch.pg->words + ch.off * mx->row_words, (size_t)ch.rows * row_bytes,
+                               hipMemcpyHostToDevice, c->side));
+        GBT_HIP(hipEventRecord(ev.copied[b], c->side));
+        if (h2d_bytes) *h2d_bytes += (double)ch.rows * row_bytes;
+        return GBT_OK;
+    };
+    GBT_TRY(issue(0));
+    for (size_t k = 0; k < host_chunks.size(); ++k) {
+        if (k + 1 < host_chunks.size()) GBT_TRY(issue(k + 1));
+        int b = (int)(k & 1);
+        GBT_HIP(hipStreamWaitEvent(c->stream, ev.copied[b], 0));
+        const Chunk &ch = host_chunks[k];
+        GBT_TRY(fn(buf[b], ch.pg->row0 + ch.off, ch.rows));
+        GBT_HIP(hipEventRecord(ev.consumed[b], c->stream));
+    }
+    // keep the events alive until the side stream is done with them
+    GBT_HIP(hipStreamSynchronize(c->side));
+    return GBT_OK;
+}
+
+static bool all_device_single(const gbt_matrix *mx)
+{
+    return mx->pages.size() == 1 && !mx->pages[0].host;
+}
+
+static bool any_host_pages(const gbt_matrix *mx)
+{
+    for (auto &pg : mx->pages)
+        if (pg.host) return true;
+    return false;
+}
+
+// ------------------------------------------------------------ sampling driver
+struct Buffers {
+    gbt_ctx *c;
+    bool owned;
+    std::vector<std::pair<void *, size_t>> held;
+    gbt_status get(int slot, size_t bytes, void **p)
+    {
+        if (!owned) return scratch(c, slot, bytes, p);
+        GBT_TRY(dev_alloc(c, bytes, p));
+        held.push_back({*p, bytes});
+        return GBT_OK;
+    }
+    void release()
+    {
+        for (auto &h : held) dev_free(c, h.first, h.second);
+        held.clear();
+    }
+};
+
+struct SampleOut {
+    const uint32_t *page = nullptr;  // R rows
+    int32_t *sel = nullptr;          // R global ids (NULL: identity)
+    double *gw = nullptr;
+    int64_t *q = nullptr;
+    int64_t R = 0, K = 0, T = 0;
+    int32_t e_key = 0, e_g = 0, e_h = 0;
+    bool alias = false;
+    long long root_g = 0, root_h = 0;
+    SampleState *st = nullptr;
+};
+
+// Alg. 7: g' <- Sample(g); AllocateOnGPU(sampled_page); Compact each page.
+gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, const float *margin,
+                      const float *label, const gbt_sample_params &sp, Buffers &bufs, SampleOut *o,
+                      double *h2d_bytes)
+{
+    const int64_t n = mx->n_rows;
+    GBT_CHECK(sp.f > 0.0 && sp.f <= 1.0, "sampling fraction %g outside (0, 1]", sp.f);
+    GBT_CHECK(gpair || (margin && label), "sampling needs gradient pairs or margins and labels");
+    SampleState *st;
+    GBT_TRY(bufs.get(kScrState, sizeof(SampleState), (void **)&st));
+    o->st = st;
+    GBT_TRY(state_init(c, st));
+    SampleSrc src{(const float2 *)gpair, margin, label, sp.loss, 0};
+    const int kind = gpair ? kSrcGpair : kSrcMargin;
+
+    if (sp.f >= 1.0 && all_device_single(mx) && gpair) {
+        // no sampling: the data page trains as it is
+        o->alias = true;
+        o->page = mx->pages[0].words;
+        o->R = n;
+        GBT_TRY(bufs.get(kScrGw, (size_t)std::max<int64_t>(n, 1) * 16, (void **)&o->gw));
+        GBT_TRY(gw_all(c, gpair, n, o->gw));
+    } else {
+        int64_t *keys = nullptr;
+        uint8_t *keep;
+        int32_t *pos;
+        GBT_TRY(bufs.get(kScrFlags, (size_t)std::max<int64_t>(n, 1), (void **)&keep));
+        GBT_TRY(bufs.get(kScrPos, (size_t)(n + 1) * 4, (void **)&pos));
+        SampleState hst;
+        if (sp.f < 1.0) {
+            o->K = std::max<int64_t>(1, (int64_t)std::nearbyint(sp.f * (double)n));
+            if (kind == kSrcGpair) GBT_TRY(bufs.get(kScrKeys, (size_t)std::max<int64_t>(n, 1) * 8, (void **)&keys));
+            GBT_TRY(mvs_threshold(c, src, kind, keys, n, sp.mvs_lambda, o->K, st, &hst));
+        }
+        // with f = 1 the state keeps T = 0: every row is kept with weight 1
+        GBT_TRY(mvs_select(c, src, kind, keys, n, sp.mvs_lambda, st, sp.seed, sp.iteration, 0, keep));
+        GBT_TRY(scan_u8(c, keep, n, pos));
+        int32_t R32 = 0;
+        GBT_HIP(hipMemcpyAsync(&R32, pos + n, 4, hipMemcpyDeviceToHost, c->stream));
+        GBT_HIP(hipStreamSynchronize(c->stream));
+        o->R = R32;
+        size_t rb = (size_t)mx->row_words * 4;
+        uint32_t *spage;
+        GBT_TRY(bufs.get(kScrSampled, (size_t)std::max<int64_t>(o->R, 1) * rb, (void **)&spage));
+        GBT_TRY(bufs.get(kScrSel, (size_t)std::max<int64_t>(o->R, 1) * 4, (void **)&o->sel));
+        GBT_TRY(bufs.get(kScrGw, (size_t)std::max<int64_t>(o->R, 1) * 16, (void **)&o->gw));
+        o->page = spage;
+        GBT_TRY(for_each_chunk(
+            c, mx,
+            [&](const uint32_t *words, int64_t row0, int64_t rows) -> gbt_status {
+                SampleSrc s2 = src;
+                if (s2.gpair) s2.gpair += row0;
+                if (s2.margin) s2.margin += row0;
+                if (s2.label) s2.label += row0;
+                return mvs_compact(c, s2, kind, keys ? keys + row0 : nullptr, rows, sp.mvs_lambda, st,
+                                   keep + row0, pos + row0, words, mx->row_words, 0, spage, o->sel, row0,
+                                   o->gw);
+            },
+            h2d_bytes));
+    }
+    GBT_TRY(bufs.get(kScrQ, (size_t)std::max<int64_t>(o->R, 1) * 16, (void **)&o->q));
+    GBT_TRY(fixed_point(c, o->gw, o->R, st, o->q));
+    SampleState hst;
+    GBT_HIP(hipMemcpyAsync(&hst, st, sizeof(SampleState), hipMemcpyDeviceToHost, c->stream));
+    GBT_HIP(hipStreamSynchronize(c->stream));
+    if (hst.bad) return set_error(GBT_E_INVALID, "sampling failed (state flags %u)", hst.bad);
+    o->T = hst.T;
+    o->e_key = hst.e_key;
+    o->e_g = hst.e_g;
+    o->e_h = hst.e_h;
+    o->root_g = (long long)hst.root_g;
+    o->root_h = (long long)hst.root_h;
+    return GBT_OK;
+}
+
+// ------------------------------------------------------------ tree kernels
+__global__ void k_tree_init(DevNode *__restrict__ nodes, int32_t n_nodes, long long rg, long long rh,
+                            int64_t R)
+{
+    int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n_nodes) return;
+    DevNode d;
+    memset(&d, 0, sizeof(d));
+    d.left_child = 2 * i + 1;
+    d.right_child = 2 * i + 2;
+    if (i == 0) {
+        d.present = 1;
+        d.sum_g = rg;
+        d.sum_h = rh;
+        d.begin = 0;
+        d.end = R;
+    }
+    nodes[i] = d;
+}
+
+__global__ void k_rows_init(int32_t *__restrict__ rows, int32_t *__restrict__ position, int64_t R)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= R) return;
+    rows[i] = (int32_t)i;
+    position[i] = 0;
+}
+
+// A node splits iff its best valid gain is > 0 (depth < max_depth is the
+// caller's); the children inherit the split's left/right sums.
+__global__ void k_decide(DevNode *__restrict__ nodes, const EvalNode *__restrict__ ev,
+                         const gbt_split *__restrict__ sp, int32_t n)
+{
+    int32_t k = blockIdx.x * blockDim.x + threadIdx.x;
+    if (k >= n) return;
+    const gbt_split s = sp[k];
+    DevNode &d = nodes[ev[k].heap];
+    if (s.valid && s.gain > 0.0) {
+        d.split = 1;
+        d.feature = s.feature;
+        d.split_bin = s.split_bin;
+        d.default_left = s.default_left;
+        d.gain = s.gain;
+        d.left_g = s.left_g;
+        d.left_h = s.left_h;
+        d.right_g = s.right_g;
+        d.right_h = s.right_h;
+    }
+}
+
+// Child segments of every split node from the partition's left counts.
+__global__ void k_children(DevNode *__restrict__ nodes, const EvalNode *__restrict__ ev, int32_t n,
+                           const int32_t *__restrict__ P)
+{
+    int32_t k = blockIdx.x * blockDim.x + threadIdx.x;
+    if (k >= n) return;
+    const DevNode d = nodes[ev[k].heap];
+    if (!d.split) return;
+    int64_t nl = (int64_t)P[d.end] - P[d.begin];
+    DevNode &L = nodes[d.left_child];
+    DevNode &Rn = nodes[d.right_child];
+    L.present = 1;
+    L.sum_g = d.left_g;
+    L.sum_h = d.left_h;
+    L.begin = d.begin;
+    L.end = d.begin + nl;
+    Rn.present = 1;
+    Rn.sum_g = d.right_g;
+    Rn.sum_h = d.right_h;
+    Rn.begin = d.begin + nl;
+    Rn.end = d.end;
+}
+
+// Eq. 6 scaled by the learning rate, for every present node that does not
+// split: leaf = (float)((-G/(H+lambda)) * eta).
+__device__ inline float leaf_of(long long Qg, long long Qh, int32_t eg, int32_t eh, double lambda,
+                                double eta)
+{
+    double G = ldexp((double)Qg, -eg), H = ldexp((double)Qh, -eh);
+    double w = -G / (H + lambda);
+    return (float)(w * eta);
+}
+
+__global__ void k_leaves(const DevNode *__restrict__ nodes, int32_t n_nodes, int32_t eg, int32_t eh,
+                         double lambda, double eta, float *__restrict__ leaf)
+{
+    int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n_nodes) return;
+    const DevNode d = nodes[i];
+    leaf[i] = (d.present && !d.split) ? leaf_of(d.sum_g, d.sum_h, eg, eh, lambda, eta) : 0.0f;
+}
+
+// Margin update from the final node of each training row (no sampling).
+__global__ void k_margin_pos(float *__restrict__ margin, const int32_t *__restrict__ position,
+                             const float *__restrict__ leaf, int64_t n)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) margin[i] = margin[i] + leaf[position[i]];
+}
+
+// Margin update by walking each row's symbols down the tree.
+__global__ void k_margin_walk(const uint32_t *__restrict__ words, int64_t rows, Geo geo,
+                              const DevNode *__restrict__ nodes, const float *__restrict__ leaf,
+                              float *__restrict__ margin)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= rows) return;
+    const uint32_t *row = words + i * geo.row_words;
+    int32_t id = 0;
+    while (nodes[id].split) {
+        const DevNode &d = nodes[id];
+        int32_t b = row_feature_bin(row, geo, d.feature);
+        bool left = b < 0 ? d.default_left != 0 : b < d.split_bin;
+        id = left ? d.left_child : d.right_child;
+    }
+    margin[i] = margin[i] + leaf[id];
+}
+
+// ------------------------------------------------------------ prediction
+__device__ inline int32_t walk_binned(const gbt_node *__restrict__ t, int64_t nn, const uint32_t *row,
+                                      const Geo &geo)
+{
+    int32_t id = 0;
+    while (!(t[id].flags & GBT_NODE_LEAF) && 2 * (int64_t)id + 2 < nn) {
+        int32_t b = row_feature_bin(row, geo, t[id].feature);
+        bool left = b < 0 ? (t[id].flags & GBT_NODE_DEFAULT_LEFT) != 0 : b < t[id].split_bin;
+        id = left ? 2 * id + 1 : 2 * id + 2;
+    }
+    return id;
+}
+
+__global__ void k_predict_binned(const uint32_t *__restrict__ words, int64_t rows, Geo geo,
+                                 const gbt_node *__restrict__ trees, const int64_t *__restrict__ offs,
+                                 int32_t n_trees, float base, float *__restrict__ out)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= rows) return;
+    const uint32_t *row = words + i * geo.row_words;
+    float acc = base;
+    for (int32_t t = 0; t < n_trees; ++t) {
+        const gbt_node *tr = trees + offs[t];
+        acc = acc + tr[walk_binned(tr, offs[t + 1] - offs[t], row, geo)].leaf_value;
+    }
+    out[i] = acc;
+}
+
+__global__ void k_predict_raw_dense(const float *__restrict__ X, int64_t n, int64_t ld,
+                                    const gbt_node *__restrict__ trees, const int64_t *__restrict__ offs,
+                                    int32_t n_trees, float base, float *__restrict__ out)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const float *x = X + i * ld;
+    float acc = base;
+    for (int32_t t = 0; t < n_trees; ++t) {
+        const gbt_node *tr = trees + offs[t];
+        const int64_t nn = offs[t + 1] - offs[t];
+        int32_t id = 0;
+        while (!(tr[id].flags & GBT_NODE_LEAF) && 2 * (int64_t)id + 2 < nn) {
+            float v = x[tr[id].feature];
+            bool left = v != v ? (tr[id].flags & GBT_NODE_DEFAULT_LEFT) != 0 : v <= tr[id].threshold;
+            id = left ? 2 * id + 1 : 2 * id + 2;
+        }
+        acc = acc + tr[id].leaf_value;
+    }
+    out[i] = acc;
+}
+
+__global__ void k_predict_raw_csr(const int64_t *__restrict__ indptr, const int32_t *__restrict__ idx,
+                                  const float *__restrict__ val, int64_t n,
+                                  const gbt_node *__restrict__ trees, const int64_t *__restrict__ offs,
+                                  int32_t n_trees, float base, float *__restrict__ out)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    int64_t base_e = indptr[0];
+    int64_t e0 = indptr[i] - base_e, e1 = indptr[i + 1] - base_e;
+    float acc = base;
+    for (int32_t t = 0; t < n_trees; ++t) {
+        const gbt_node *tr = trees + offs[t];
+        const int64_t nn = offs[t + 1] - offs[t];
+        int32_t id = 0;
+        while (!(tr[id].flags & GBT_NODE_LEAF) && 2 * (int64_t)id + 2 < nn) {
+            int32_t j = tr[id].feature;
+            float v = __builtin_nanf("");
+            int64_t lo = e0, hi = e1;  // binary search: indices ascend
+            while (lo < hi) {
+                int64_t mid = (lo + hi) >> 1;
+                if (idx[mid] < j)
+                    lo = mid + 1;
+                else
+                    hi = mid;
+            }
+            if (lo < e1 && idx[lo] == j) v = val[lo];
+            bool left = v != v ? (tr[id].flags & GBT_NODE_DEFAULT_LEFT) != 0 : v <= tr[id].threshold;
+            id = left ? 2 * id + 1 : 2 * id + 2;
+        }
+        acc = acc + tr[id].leaf_value;
+    }
+    out[i] = acc;
+}
+
+__global__ void k_leaf_values(gbt_node *__restrict__ t, int32_t n, int32_t eg, int32_t eh, double lambda,
+                              double eta)
+{
+    int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    if ((t[i].flags & GBT_NODE_PRESENT) && (t[i].flags & GBT_NODE_LEAF))
+        t[i].leaf_value = leaf_of(t[i].sum_g, t[i].sum_h, eg, eh, lambda, eta);
+}
+
+__global__ void k_margin_add_tree(const uint32_t *__restrict__ words, int64_t rows, Geo geo,
+                                  const gbt_node *__restrict__ t, int64_t nn, float *__restrict__ margin)
+{
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= rows) return;
+    margin[i] = margin[i] + t[walk_binned(t, nn, words + i * geo.row_words, geo)].leaf_value;
+}
+
+// ------------------------------------------------------------ the iteration
+struct LevelNode {
+    int32_t heap;
+    int32_t slot;
+    int64_t begin, end;
+    long long sum_g, sum_h;
+};
+
+static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float *label, float *margin,
+                                  const gbt_train_params *p, gbt_tree *tree, gbt_tree_stats *stats)
+{
+    auto t_start = std::chrono::steady_clock::now();
+    const int64_t n = mx->n_rows;
+    const int32_t D = p->max_depth;
+    const int32_t NN = (1 << (D + 1)) - 1;
+    const bool host_pages = any_host_pages(mx);
+    double h2d = 0.0;
+
+    float *gpair = nullptr;
+    if (!host_pages) {
+        GBT_TRY(scratch_t(c, kScrGpair, (size_t)std::max<int64_t>(n, 1) * 2, &gpair));
+        GBT_TRY(launch_gradients(c, p->loss, margin, label, nullptr, n, gpair));
+    }
+    Buffers bufs{c, false, {}};
+    gbt_sample_params sp{p->f, p->mvs_lambda, p->seed, p->iteration, p->loss, 0};
+    SampleOut so;
+    GBT_TRY(sample_run(c, mx, gpair, margin, label, sp, bufs, &so, &h2d));
+    const int64_t R = so.R;
+    if (stats) {
+        stats->n_sampled = R;
+        stats->threshold = so.T;
+        stats->exp_key = so.e_key;
+    }
+
+    // ---- Alg. 1 on the sampled page, level by level
+    DevNode *nodes;
+    int32_t *rows, *rows_tmp, *position;
+    float *leaf;
+    EvalNode *ev_d;
+    gbt_split *splits_d;
+    GBT_TRY(scratch_t(c, kScrNodes, (size_t)NN, &nodes));
+    GBT_TRY(scratch_t(c, kScrLeaf, (size_t)NN, &leaf));
+    GBT_TRY(scratch_t(c, kScrRows, (size_t)std::max<int64_t>(R, 1), &rows));
+    GBT_TRY(scratch_t(c, kScrRowsTmp, (size_t)std::max<int64_t>(R, 1), &rows_tmp));
+    GBT_TRY(scratch_t(c, kScrPosition, (size_t)std::max<int64_t>(R, 1), &position));
+    int32_t max_level_nodes = (int32_t)std::min<int64_t>((int64_t)1 << std::max(D - 1, 0), std::max<int64_t>(R, 1));
+    GBT_TRY(scratch_t(c, kScrEvalNodes, (size_t)max_level_nodes, &ev_d));
+    GBT_TRY(scratch_t(c, kScrSplits, (size_t)max_level_nodes, &splits_d));
+    const size_t hist_bytes = (size_t)max_level_nodes * (size_t)mx->total_bins * 16;
+    int64_t *histA = nullptr, *histB = nullptr;
+    if (D > 0) {
+        GBT_TRY(scratch(c, kScrHistA, std::max<size_t>(hist_bytes, 16), (void **)&histA));
+        GBT_TRY(scratch(c, kScrHistB, std::max<size_t>(hist_bytes, 16), (void **)&histB));
+    }
+    k_tree_init<<<blocks(NN), 256, 0, c->stream>>>(nodes, NN, so.root_g, so.root_h, R);
+    GBT_LAUNCHED();
+    if (R) {
+        k_rows_init<<<blocks(R), 256, 0, c->stream>>>(rows, position, R);
+        GBT_LAUNCHED();
+    }
+    EvalParams ep{p->lambda, p->gamma, p->min_child_weight, so.e_g, so.e_h};
+    std::vector<LevelNode> cur{{0, 0, 0, R, so.root_g, so.root_h}};
+    if (D > 0) {
+        gbt_seg root{0, 0, 0, R};
+        GBT_TRY(build_hist_impl(c, mx, so.page, so.q, nullptr, &root, 1, nullptr, 0, nullptr, histA, stats));
+    }
+    std::vector<DevNode> hnodes;
+    for (int32_t d = 0; d < D && !cur.empty(); ++d) {
+        const int32_t nc = (int32_t)cur.size();
+        std::vector<EvalNode> ev(nc);
+        for (int32_t k = 0; k < nc; ++k) ev[k] = {cur[k].sum_g, cur[k].sum_h, cur[k].slot, cur[k].heap};
+        GBT_HIP(hipMemcpyAsync(ev_d, ev.data(), nc * sizeof(EvalNode), hipMemcpyHostToDevice, c->stream));
+        GBT_TRY(eval_impl(c, mx, histA, ev_d, nc, ep, splits_d));
+        k_decide<<<blocks(nc), 256, 0, c->stream>>>(nodes, ev_d, splits_d, nc);
+        GBT_LAUNCHED();
+        int32_t *P = nullptr;
+        GBT_TRY(partition_impl(c, mx, so.page, rows, R, position, nullptr, nodes, rows_tmp, &P));
+        std::swap(rows, rows_tmp);
+        if (P) {
+            k_children<<<blocks(nc), 256, 0, c->stream>>>(nodes, ev_d, nc, P);
+            GBT_LAUNCHED();
+        }
+        // the next level's nodes
+        const int32_t first = (1 << (d + 1)) - 1, count = 1 << (d + 1);
+        hnodes.resize(count);
+        GBT_HIP(hipMemcpyAsync(hnodes.data(), nodes + first, count * sizeof(DevNode), hipMemcpyDeviceToHost,
+                               c->stream));
+        GBT_HIP(hipStreamSynchronize(c->stream));
+        std::vector<LevelNode> next;
+        for (int32_t k = 0; k < count; ++k) {
+            const DevNode &h = hnodes[k];
+            if (!h.present) continue;
+            next.push_back({first + k, (int32_t)next.size(), h.begin, h.end, h.sum_g, h.sum_h});
+        }
+        if (d + 1 < D && !next.empty()) {
+            // build the smaller child of each pair, subtract for its sibling
+            std::vector<int32_t> slot_of(count, -1);
+            for (auto &x : next) slot_of[x.heap - first] = x.slot;
+            std::vector<gbt_seg> build;
+            std::vector<gbt_sub> sub;
+            for (auto &par : cur) {
+                int32_t l = 2 * par.heap + 1, r = l + 1;
+                int32_t sl = slot_of[l - first], sr = slot_of[r - first];
+                if (sl < 0) continue;  // not split
+                const DevNode &L = hnodes[l - first], &Rn = hnodes[r - first];
+                bool left_small = (L.end - L.begin) <= (Rn.end - Rn.begin);
+                const DevNode &S = left_small ? L : Rn;
+                int32_t ss = left_small ? sl : sr, so2 = left_small ? sr : sl;
+                build.push_back({ss, 0, S.begin, S.end});
+                sub.push_back({par.slot, ss, so2, 0});
+            }
+            GBT_TRY(build_hist_impl(c, mx, so.page, so.q, rows, build.data(), (int32_t)build.size(), sub.data(),
+                                    (int32_t)sub.size(), histA, histB, stats));
+            std::swap(histA, histB);
+        }
+        cur.swap(next);
+    }
+    // ---- leaves and the margin update of all n rows (Eq. 1)
+    k_leaves<<<blocks(NN), 256, 0, c->stream>>>(nodes, NN, so.e_g, so.e_h, p->lambda, p->eta, leaf);
+    GBT_LAUNCHED();
+    if (so.alias) {
+        if (n) {
+            k_margin_pos<<<blocks(n), 256, 0, c->stream>>>(margin, position, leaf, n);
+            GBT_LAUNCHED();
+        }
+    } else {
+        Geo geo = geo_of(mx);
+        GBT_TRY(for_each_chunk(
+            c, mx,
+            [&](const uint32_t *words, int64_t row0, int64_t rows_n) -> gbt_status {
+                k_margin_walk<<<blocks(rows_n), 256, 0, c->stream>>>(words, rows_n, geo, nodes, leaf,
+                                                                     margin + row0);
+                GBT_LAUNCHED();
+                return GBT_OK;
+            },
+            &h2d));
+    }
+    // ---- the tree, host side
+    std::vector<DevNode> all(NN);
+    std::vector<float> leafh(NN);
+    GBT_HIP(hipMemcpyAsync(all.data(), nodes, NN * sizeof(DevNode), hipMemcpyDeviceToHost, c->stream));
+    GBT_HIP(hipMemcpyAsync(leafh.data(), leaf, NN * 4, hipMemcpyDeviceToHost, c->stream));
+    GBT_HIP(hipStreamSynchronize(c->stream));
+    tree->exp_g = so.e_g;
+    tree->exp_h = so.e_h;
+    for (int32_t i = 0; i < NN; ++i) {
+        gbt_node &o = tree->nodes[i];
+        memset(&o, 0, sizeof(o));
+        const DevNode &d = all[i];
+        if (!d.present) continue;
+        o.flags = GBT_NODE_PRESENT;
+        o.sum_g = d.sum_g;
+        o.sum_h = d.sum_h;
+        o.n_rows = (int32_t)(d.end - d.begin);
+        if (d.split) {
+            o.feature = d.feature;
+            o.split_bin = d.split_bin;
+            o.threshold = mx->cut_values_h[mx->cut_ptr_h[d.feature] + d.split_bin - 1];
+            o.gain = d.gain;
+            if (d.default_left) o.flags |= GBT_NODE_DEFAULT_LEFT;
+        } else {
+            o.feature = -1;
+            o.split_bin = -1;
+            o.flags |= GBT_NODE_LEAF;
+            o.leaf_value = leafh[i];
+        }
+    }
+    if (stats) {
+        stats->ms_total =
+            std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t_start).count();
+    }
+    return GBT_OK;
+}
+
+static gbt_status upload_trees(gbt_ctx *c, const gbt_tree *trees, int32_t n_trees, gbt_node **nodes_d,
+                               int64_t **offs_d)
+{
+    std::vector<int64_t> offs(n_trees + 1, 0);
+    for (int32_t t = 0; t < n_trees; ++t) {
+        GBT_CHECK(trees[t].nodes && trees[t].n_nodes > 0, "tree %d has no nodes", t);
+        offs[t + 1] = offs[t] + trees[t].n_nodes;
+    }
+    size_t o_off = ((size_t)offs[n_trees] * sizeof(gbt_node) + 255) / 256 * 256;
+    char *buf;
+    GBT_TRY(scratch_t(c, kScrTrees, o_off + (n_trees + 1) * 8, &buf));
+    std::vector<char> h(o_off + (n_trees + 1) * 8);
+    for (int32_t t = 0; t < n_trees; ++t)
+        memcpy(h.data() + offs[t] * sizeof(gbt_node), trees[t].nodes, trees[t].n_nodes * sizeof(gbt_node));
+    memcpy(h.data() + o_off, offs.data(), (n_trees + 1) * 8);
+    GBT_HIP(hipMemcpyAsync(buf, h.data(), h.size(), hipMemcpyHostToDevice, c->stream));
+    *nodes_d = (gbt_node *)buf;
+    *offs_d = (int64_t *)(buf + o_off);
+    return GBT_OK;
+}
+
+}  // namespace gbt
+
+using namespace gbt;
+
+struct gbt_sampled {
+    gbt_ctx *ctx = nullptr;
+    Buffers bufs{nullptr, true, {}};
+    SampleOut out;
+    int32_t row_words = 0;
+};
+
+extern "C" {
+
+gbt_status gbt_gradients(gbt_ctx *c, int32_t loss, const float *margin_d, const float *label_d,
+                         const float *weight_d, int64_t n, float *gpair_d)
+{
+    GBT_CHECK(c, "ctx is NULL");
+    GBT_CHECK(n >= 0, "n < 0");
+    GBT_CHECK(loss == GBT_LOSS_LOGISTIC || loss == GBT_LOSS_SQUARED, "unknown loss %d", loss);
+    GBT_CHECK(n == 0 || (margin_d && label_d && gpair_d), "gbt_gradients: NULL array");
+    GBT_TRY(set_device(c));
+    GBT_TRY(launch_gradients(c, loss, margin_d, label_d, weight_d, n, gpair_d));
+    GBT_HIP(hipStreamSynchronize(c->stream));
+    return GBT_OK;
+}
+
+gbt_status gbt_sample(gbt_ctx *c, const gbt_matrix *data, const float *gpair_d, const float *margin_d,
+                      const float *label_d, const gbt_sample_params *sp, gbt_sampled **out)
+{
+    GBT_CHECK(c && data && sp && out, "gbt_sample: NULL argument");
+    *out = nullptr;
+    GBT_CHECK(sp->loss == GBT_LOSS_LOGISTIC || sp->loss == GBT_LOSS_SQUARED || gpair_d, "unknown loss");
+    GBT_TRY(set_device(c));
+    auto *s = new gbt_sampled();
+    s->ctx = c;
+    s->bufs.c = c;
+    s->row_words = data->row_words;
+    gbt_status st = sample_run(c, data, gpair_d, margin_d, label_d, *sp, s->bufs, &s->out, nullptr);
+    if (st == GBT_OK) {
+        hipError_t e = hipStreamSynchronize(c->stream);
+        if (e != hipSuccess) st = hip_error(e, "sync", __FILE__, __LINE__);
+    }
+    if (st != GBT_OK) {
+        (void)hipStreamSynchronize(c->stream);
+        s->bufs.release();
+        delete s;
+        return st;
+    }
+    *out = s;
+    return GBT_OK;
+}
+
+gbt_status gbt_sampled_info_get(const gbt_sampled *s, gbt_sampled_info *info)
+{
+    GBT_CHECK(s && info, "gbt_sampled_info_get: NULL argument");
+    info->n_sampled = s->out.R;
+    info->threshold = s->out.T;
+    info->target = s->out.K;
+    info->exp_key = s->out.e_key;
+    info->exp_g = s->out.e_g;
+    info->exp_h = s->out.e_h;
+    info->is_alias = s->out.alias ? 1 : 0;
+    info->page_d = s->out.page;
+    info->rows_d = s->out.sel;
+    info->gpair_d = s->out.gw;
+    info->gpair_fx_d = s->out.q;
+    return GBT_OK;
+}
+
+gbt_status gbt_sampled_free(gbt_sampled *s)
+{
+    if (!s) return GBT_OK;
+    (void)hipSetDevice(s->ctx->device);
+    (void)hipStreamSynchronize(s->ctx->stream);
+    s->bufs.release();
+    delete s;
+    return GBT_OK;
+}
+
+gbt_status gbt_train_tree(gbt_ctx *c, const gbt_matrix *data, const float *label_d, float *margin_d,
+                          const gbt_train_params *p, gbt_tree *tree, gbt_tree_stats *stats)
+{
+    GBT_CHECK(c && data && p && tree && tree->nodes, "gbt_train_tree: NULL argument");
+    GBT_CHECK(data->n_rows == 0 || (label_d && margin_d), "gbt_train_tree: NULL labels/margins");
+    GBT_CHECK(p->max_depth >= 0 && p->max_depth <= 20, "max_depth %d outside [0, 20]", p->max_depth);
+    GBT_CHECK(p->f > 0.0 && p->f <= 1.0, "f %g outside (0, 1]", p->f);
+    GBT_CHECK(p->loss == GBT_LOSS_LOGISTIC || p->loss == GBT_LOSS_SQUARED, "unknown loss %d", p->loss);
+    GBT_CHECK(data->n_rows < ((int64_t)1 << 31) - 1, "more than 2^31-2 rows");
+    const int32_t NN = (1 << (p->max_depth + 1)) - 1;
+    GBT_CHECK(tree->n_nodes >= NN, "tree holds %d nodes, needs %d", tree->n_nodes, NN);
+    tree->max_depth = p->max_depth;
+    if (stats) memset(stats, 0, sizeof(*stats));
+    GBT_TRY(set_device(c));
+    return train_tree_impl(c, data, label_d, margin_d, p, tree, stats);
+}
+
+gbt_status gbt_update_leaves(gbt_ctx *c, gbt_tree *tree, const gbt_train_params *tp, const gbt_matrix *data,
+                             float *margin_d)
+{
+    GBT_CHECK(c && tree && tree->nodes && tp && data, "gbt_update_leaves: NULL argument");
+    GBT_CHECK(data->n_rows == 0 || margin_d, "margins are NULL");
+    GBT_TRY(set_device(c));
+    gbt_node *nodes_d;
+    int64_t *offs_d;
+    GBT_TRY(upload_trees(c, tree, 1, &nodes_d, &offs_d));
+    k_leaf_values<<<blocks(tree->n_nodes), 256, 0, c->stream>>>(nodes_d, tree->n_nodes, tree->exp_g,
+                                                               tree->exp_h, tp->lambda, tp->eta);
+    GBT_LAUNCHED();
+    Geo geo = geo_of(data);
+    GBT_TRY(for_each_chunk(
+        c, data,
+        [&](const uint32_t *words, int64_t row0, int64_t rows) -> gbt_status {
+            k_margin_add_tree<<<blocks(rows), 256, 0, c->stream>>>(words, rows, geo, nodes_d, tree->n_nodes,
+                                                                   margin_d + row0);
+            GBT_LAUNCHED();
+            return GBT_OK;
+        },
+        nullptr));
+    GBT_HIP(hipMemcpyAsync(tree->nodes, nodes_d, tree->n_nodes * sizeof(gbt_node), hipMemcpyDeviceToHost,
+                           c->stream));
+    GBT_HIP(hipStreamSynchronize(c->stream));
+    return GBT_OK;
+}
+
+gbt_status gbt_predict(gbt_ctx *c, const gbt_tree *trees, int32_t n_trees, const gbt_input *raw,
+                       const gbt_matrix *binned, float base_margin, float *margin_out_d)
+{
+    GBT_CHECK(c && (trees || n_trees == 0) && n_trees >= 0, "gbt_predict: bad trees");
+    GBT_CHECK((raw != nullptr) != (binned != nullptr), "give exactly one of raw and binned input");
+    GBT_TRY(set_device(c));
+    gbt_node *nodes_d = nullptr;
+    int64_t *offs_d = nullptr;
+    if (n_trees) GBT_TRY(upload_trees(c, trees, n_trees, &nodes_d, &offs_d));
+    if (binned) {
+        GBT_CHECK(binned->n_rows == 0 || margin_out_d, "output is NULL");
+        Geo geo = geo_of(binned);
+        GBT_TRY(for_each_chunk(
+            c, binned,
+            [&](const uint32_t *words, int64_t row0, int64_t rows) -> gbt_status {
+                k_predict_binned<<<blocks(rows), 256, 0, c->stream>>>(words, rows, geo, nodes_d, offs_d,
+                                                                     n_trees, base_margin, margin_out_d + row0);
+                GBT_LAUNCHED();
+                return GBT_OK;
+            },
+            nullptr));
+    } else {
+        GBT_CHECK(raw->location == GBT_LOC_DEVICE, "raw prediction input must be device resident");
+        GBT_CHECK(raw->n_rows >= 0, "n_rows < 0");
+        if (raw->n_rows) {
+            GBT_CHECK(margin_out_d, "output is NULL");
+            if (raw->kind == GBT_INPUT_DENSE_F32) {
+                GBT_CHECK(raw->values && raw->ld >= raw->n_cols, "bad dense input");
+                k_predict_raw_dense<<<blocks(raw->n_rows), 256, 0, c->stream>>>(
+                    raw->values, raw->n_rows, raw->ld, nodes_d, offs_d, n_trees, base_margin, margin_out_d);
+            } else {
+                GBT_CHECK(raw->indptr && (raw->nnz == 0 || (raw->indices && raw->values)), "bad CSR input");
+                k_predict_raw_csr<<<blocks(raw->n_rows), 256, 0, c->stream>>>(
+                    raw->indptr, raw->indices, raw->values, raw->n_rows, nodes_d, offs_d, n_trees, base_margin,
+                    margin_out_d);
+            }
+            GBT_LAUNCHED();
+        }
+    }
+    GBT_HIP(hipStreamSynchronize(c->stream));
+    return GBT_OK;
+}
+
+}  // extern "C"

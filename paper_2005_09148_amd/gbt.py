@@ -1,0 +1,563 @@
+"""ctypes binding of libgbt.so (the C-ABI in include/gbt.h).
+
+Argument marshalling only: every step of the boosting iteration runs in the
+library's HIP kernels.  torch supplies device memory and the stream.  There
+is no fallback: importing this module fails when libgbt.so is missing or does
+not load.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgbt.so")
+
+GBT_OK = 0
+GBT_E_INVALID = -1
+GBT_E_OOM = -2
+GBT_E_BUDGET = -3
+GBT_E_DEVICE = -4
+GBT_E_UNSUPPORTED = -5
+
+INPUT_DENSE = 0
+INPUT_CSR = 1
+LOC_HOST = 0
+LOC_DEVICE = 1
+HOME_DEVICE = 0
+HOME_PINNED_HOST = 1
+LOSS_LOGISTIC = 0
+LOSS_SQUARED = 1
+NODE_PRESENT = 1
+NODE_LEAF = 2
+NODE_DEFAULT_LEFT = 4
+
+
+class GbtError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"libgbt error {code}: {msg}")
+        self.code = code
+
+
+class Input(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("location", C.c_int32), ("n_rows", C.c_int64),
+                ("n_cols", C.c_int32), ("pad0", C.c_int32), ("values", C.c_void_p),
+                ("ld", C.c_int64), ("indptr", C.c_void_p), ("indices", C.c_void_p),
+                ("nnz", C.c_int64)]
+
+
+class QuantParams(C.Structure):
+    _fields_ = [("max_bin", C.c_int32), ("page_home", C.c_int32),
+                ("sketch_max_rows", C.c_int64), ("page_rows", C.c_int64)]
+
+
+class MatrixInfo(C.Structure):
+    _fields_ = [("n_rows", C.c_int64), ("n_cols", C.c_int32), ("sparse", C.c_int32),
+                ("has_missing", C.c_int32), ("symbol_bits", C.c_int32), ("stride", C.c_int32),
+                ("row_words", C.c_int32), ("null_symbol", C.c_uint32), ("n_pages", C.c_int32),
+                ("total_bins", C.c_int64), ("page_rows", C.c_int64), ("page_home", C.c_int32),
+                ("pad0", C.c_int32)]
+
+
+class TrainParams(C.Structure):
+    _fields_ = [("loss", C.c_int32), ("max_depth", C.c_int32), ("eta", C.c_double),
+                ("lambda_", C.c_double), ("gamma", C.c_double), ("min_child_weight", C.c_double),
+                ("f", C.c_double), ("mvs_lambda", C.c_double), ("seed", C.c_uint64),
+                ("iteration", C.c_uint64)]
+
+
+class Seg(C.Structure):
+    _fields_ = [("node_slot", C.c_int32), ("pad0", C.c_int32), ("begin", C.c_int64),
+                ("end", C.c_int64)]
+
+
+class Sub(C.Structure):
+    _fields_ = [("parent_slot", C.c_int32), ("built_slot", C.c_int32),
+                ("target_slot", C.c_int32), ("pad0", C.c_int32)]
+
+
+SPLIT_DTYPE = np.dtype([("gain", "<f8"), ("left_g", "<i8"), ("left_h", "<i8"),
+                        ("right_g", "<i8"), ("right_h", "<i8"), ("feature", "<i4"),
+                        ("split_bin", "<i4"), ("default_left", "<i4"), ("valid", "<i4")])
+NODE_DTYPE = np.dtype([("feature", "<i4"), ("split_bin", "<i4"), ("threshold", "<f4"),
+                       ("leaf_value", "<f4"), ("gain", "<f8"), ("sum_g", "<i8"),
+                       ("sum_h", "<i8"), ("n_rows", "<i4"), ("flags", "u1"),
+                       ("pad", "u1", (3,))])
+assert SPLIT_DTYPE.itemsize == 56 and NODE_DTYPE.itemsize == 48
+
+
+class Split(C.Structure):
+    _fields_ = [("gain", C.c_double), ("left_g", C.c_int64), ("left_h", C.c_int64),
+                ("right_g", C.c_int64), ("right_h", C.c_int64), ("feature", C.c_int32),
+                ("split_bin", C.c_int32), ("default_left", C.c_int32), ("valid", C.c_int32)]
+
+
+class Tree(C.Structure):
+    _fields_ = [("max_depth", C.c_int32), ("n_nodes", C.c_int32), ("exp_g", C.c_int32),
+                ("exp_h", C.c_int32), ("nodes", C.c_void_p)]
+
+
+class TreeStats(C.Structure):
+    _fields_ = [("n_sampled", C.c_int64), ("threshold", C.c_int64), ("exp_key", C.c_int32),
+                ("hist_launches", C.c_int32), ("hist_rows", C.c_int64),
+                ("hist_updates", C.c_int64), ("hist_bytes", C.c_int64), ("ms_hist", C.c_double),
+                ("ms_total", C.c_double)]
+
+
+class SampleParams(C.Structure):
+    _fields_ = [("f", C.c_double), ("mvs_lambda", C.c_double), ("seed", C.c_uint64),
+                ("iteration", C.c_uint64), ("loss", C.c_int32), ("pad0", C.c_int32)]
+
+
+class SampledInfo(C.Structure):
+    _fields_ = [("n_sampled", C.c_int64), ("threshold", C.c_int64), ("target", C.c_int64),
+                ("exp_key", C.c_int32), ("exp_g", C.c_int32), ("exp_h", C.c_int32),
+                ("is_alias", C.c_int32), ("page_d", C.c_void_p), ("rows_d", C.c_void_p),
+                ("gpair_d", C.c_void_p), ("gpair_fx_d", C.c_void_p)]
+
+
+# every symbol the header declares, with its signature
+_vp, _i32, _i64, _u64, _f32, _f64 = (C.c_void_p, C.c_int32, C.c_int64, C.c_uint64, C.c_float,
+                                     C.c_double)
+SIGNATURES = {
+    "gbt_abi_version": (_i32, []),
+    "gbt_last_error": (C.c_char_p, []),
+    "gbt_ctx_create": (_i32, [_i32, _u64, _vp, _vp]),
+    "gbt_ctx_destroy": (_i32, [_vp]),
+    "gbt_ctx_memory": (_i32, [_vp, _vp, _vp]),
+    "gbt_ctx_set_timing": (_i32, [_vp, _i32]),
+    "gbt_quantize": (_i32, [_vp, _vp, _vp, _vp]),
+    "gbt_quantize_begin": (_i32, [_vp, _vp, _i32, _i64, _i32, _vp]),
+    "gbt_quantize_sketch_batch": (_i32, [_vp, _vp]),
+    "gbt_quantize_finalize_cuts": (_i32, [_vp]),
+    "gbt_quantize_encode_batch": (_i32, [_vp, _vp]),
+    "gbt_quantize_end": (_i32, [_vp, _vp]),
+    "gbt_quantizer_free": (_i32, [_vp]),
+    "gbt_matrix_info_get": (_i32, [_vp, _vp]),
+    "gbt_matrix_get_cuts": (_i32, [_vp, _vp, _vp]),
+    "gbt_matrix_copy_page": (_i32, [_vp, _i32, _vp, _i64]),
+    "gbt_matrix_page_rows": (_i32, [_vp, _i32, _vp, _vp]),
+    "gbt_matrix_free": (_i32, [_vp]),
+    "gbt_gradients": (_i32, [_vp, _i32, _vp, _vp, _vp, _i64, _vp]),
+    "gbt_sample": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "gbt_sampled_info_get": (_i32, [_vp, _vp]),
+    "gbt_sampled_free": (_i32, [_vp]),
+    "gbt_build_hist": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp]),
+    "gbt_eval_splits": (_i32, [_vp, _vp, _vp, _vp, _vp, _i32, _vp, _i32, _i32, _vp]),
+    "gbt_partition": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _i64, _vp, _vp]),
+    "gbt_update_leaves": (_i32, [_vp, _vp, _vp, _vp, _vp]),
+    "gbt_train_tree": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "gbt_predict": (_i32, [_vp, _vp, _i32, _vp, _vp, _f32, _vp]),
+}
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2005_09148_amd.build`")
+    lib = C.CDLL(LIB_PATH)
+    for name, (res, args) in SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+_lib = _load()
+
+
+def lib():
+    return _lib
+
+
+def last_error() -> str:
+    return _lib.gbt_last_error().decode()
+
+
+def _check(code):
+    if code != GBT_OK:
+        raise GbtError(code, last_error())
+
+
+def abi_version() -> int:
+    return _lib.gbt_abi_version()
+
+
+# ---------------------------------------------------------------- torch glue
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if isinstance(t, np.ndarray):
+        return t.ctypes.data
+    return t.data_ptr()
+
+
+def _dev_tensor(a, dtype, device):
+    """A contiguous device tensor of `a` (numpy array or tensor)."""
+    torch = _torch()
+    if isinstance(a, np.ndarray):
+        a = torch.from_numpy(np.ascontiguousarray(a))
+    return a.to(device=device, dtype=dtype).contiguous()
+
+
+class Context:
+    """A libgbt context bound to one device and torch's current stream."""
+
+    def __init__(self, device: int = 0, budget_bytes: int = 0, stream=None):
+        torch = _torch()
+        self.device = device
+        torch.cuda.set_device(device)
+        s = stream if stream is not None else torch.cuda.current_stream(device)
+        self.stream = s
+        h = C.c_void_p()
+        _check(_lib.gbt_ctx_create(device, budget_bytes, s.cuda_stream, C.byref(h)))
+        self.h = h
+
+    def close(self):
+        if self.h:
+            _lib.gbt_ctx_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def memory(self):
+        used, peak = C.c_uint64(), C.c_uint64()
+        _check(_lib.gbt_ctx_memory(self.h, C.byref(used), C.byref(peak)))
+        return used.value, peak.value
+
+    def set_timing(self, on: bool):
+        _check(_lib.gbt_ctx_set_timing(self.h, int(on)))
+
+    @property
+    def torch_device(self):
+        return _torch().device("cuda", self.device)
+
+
+# ---------------------------------------------------------------- quantization
+def _make_input(data, location):
+    """gbt_input for dense X (2-D float32) or CSR (indptr, indices, values, m)."""
+    inp = Input()
+    keep = []
+    if isinstance(data, dict) and data.get("kind") == "csr":
+        ip, ix, v = data["indptr"], data["indices"], data["values"]
+        inp.kind = INPUT_CSR
+        inp.n_rows = len(ip) - 1
+        inp.n_cols = int(data["m"])
+        inp.nnz = int(ip[-1] - ip[0])
+        arrs = [ip, ix, v]
+    else:
+        X = data
+        inp.kind = INPUT_DENSE
+        inp.n_rows, inp.n_cols = int(X.shape[0]), int(X.shape[1])
+        inp.ld = int(X.shape[1])
+        arrs = [X]
+    if location == LOC_HOST:
+        arrs = [np.ascontiguousarray(a) for a in arrs]
+    keep.extend(arrs)
+    inp.location = location
+    if inp.kind == INPUT_CSR:
+        inp.indptr, inp.indices, inp.values = (_ptr(a) for a in arrs)
+    else:
+        inp.values = _ptr(arrs[0])
+    return inp, keep
+
+
+def dense_input(X, location=None):
+    if location is None:
+        location = LOC_HOST if isinstance(X, np.ndarray) else LOC_DEVICE
+    if isinstance(X, np.ndarray):
+        X = np.ascontiguousarray(X, dtype=np.float32)
+    return _make_input(X, location)
+
+
+def csr_input(indptr, indices, values, m, location=LOC_HOST):
+    if location == LOC_HOST:
+        d = {"kind": "csr", "indptr": np.ascontiguousarray(indptr, np.int64),
+             "indices": np.ascontiguousarray(indices, np.int32),
+             "values": np.ascontiguousarray(values, np.float32), "m": m}
+    else:
+        d = {"kind": "csr", "indptr": indptr, "indices": indices, "values": values, "m": m}
+    return _make_input(d, location)
+
+
+class Matrix:
+    """A quantized ELLPACK matrix owned by the library."""
+
+    def __init__(self, ctx: Context, handle):
+        self.ctx = ctx
+        self.h = handle
+        self._info = None
+
+    def free(self):
+        if self.h:
+            _lib.gbt_matrix_free(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+    def info(self) -> MatrixInfo:
+        if self._info is None:
+            inf = MatrixInfo()
+            _check(_lib.gbt_matrix_info_get(self.h, C.byref(inf)))
+            self._info = inf
+        return self._info
+
+    def cuts(self):
+        inf = self.info()
+        cp = np.zeros(inf.n_cols + 1, np.int32)
+        _check(_lib.gbt_matrix_get_cuts(self.h, _ptr(cp), None))
+        cv = np.zeros(max(int(cp[-1]), 1), np.float32)
+        _check(_lib.gbt_matrix_get_cuts(self.h, None, _ptr(cv)))
+        return cp, cv[: int(cp[-1])]
+
+    def page_rows(self, i):
+        r0, r = C.c_int64(), C.c_int64()
+        _check(_lib.gbt_matrix_page_rows(self.h, i, C.byref(r0), C.byref(r)))
+        return r0.value, r.value
+
+    def page(self, i=0) -> np.ndarray:
+        inf = self.info()
+        _, rows = self.page_rows(i)
+        out = np.zeros((rows, inf.row_words), np.uint32)
+        _check(_lib.gbt_matrix_copy_page(self.h, i, _ptr(out), out.size))
+        return out
+
+    def pages(self) -> np.ndarray:
+        return np.concatenate([self.page(i) for i in range(self.info().n_pages)])
+
+
+def gbt_quantize(ctx: Context, data, max_bin=256, page_rows=0, page_home=HOME_DEVICE,
+                 sketch_max_rows=0) -> Matrix:
+    """Sec. 3.1-3.2: quantile cuts and ELLPACK pages of dense X (numpy host
+    array or device tensor) or CSR (a dict kind='csr')."""
+    if isinstance(data, dict):
+        loc = LOC_HOST if isinstance(data["indptr"], np.ndarray) else LOC_DEVICE
+        inp, keep = csr_input(data["indptr"], data["indices"], data["values"], data["m"], loc)
+    else:
+        inp, keep = dense_input(data)
+    qp = QuantParams(max_bin, page_home, sketch_max_rows, page_rows)
+    h = C.c_void_p()
+    _check(_lib.gbt_quantize(ctx.h, C.byref(inp), C.byref(qp), C.byref(h)))
+    del keep
+    return Matrix(ctx, h)
+
+
+class Quantizer:
+    """Incremental quantization (Alg. 3 sketch batches, then Alg. 5 pages)."""
+
+    def __init__(self, ctx, n_cols, n_rows_total, max_bin=256, page_rows=0,
+                 page_home=HOME_DEVICE, sketch_max_rows=0, kind=INPUT_DENSE):
+        self.ctx = ctx
+        qp = QuantParams(max_bin, page_home, sketch_max_rows, page_rows)
+        h = C.c_void_p()
+        _check(_lib.gbt_quantize_begin(ctx.h, C.byref(qp), n_cols, n_rows_total, kind,
+                                       C.byref(h)))
+        self.h = h
+
+    def sketch(self, X):
+        inp, keep = dense_input(X)
+        _check(_lib.gbt_quantize_sketch_batch(self.h, C.byref(inp)))
+
+    def finalize(self):
+        _check(_lib.gbt_quantize_finalize_cuts(self.h))
+
+    def encode(self, X):
+        inp, keep = dense_input(X)
+        _check(_lib.gbt_quantize_encode_batch(self.h, C.byref(inp)))
+
+    def end(self) -> Matrix:
+        m = C.c_void_p()
+        _check(_lib.gbt_quantize_end(self.h, C.byref(m)))
+        self.h = None
+        return Matrix(self.ctx, m)
+
+    def __del__(self):
+        if getattr(self, "h", None):
+            _lib.gbt_quantizer_free(self.h)
+
+
+# ---------------------------------------------------------------- iteration steps
+def gbt_gradients(ctx, loss, margin, label, weight=None, out=None):
+    torch = _torch()
+    n = margin.numel()
+    if out is None:
+        out = torch.empty((n, 2), dtype=torch.float32, device=margin.device)
+    _check(_lib.gbt_gradients(ctx.h, loss, _ptr(margin), _ptr(label), _ptr(weight), n, _ptr(out)))
+    return out
+
+
+def _hip():
+    hip = getattr(_hip, "lib", None)
+    if hip is None:
+        hip = C.CDLL("libamdhip64.so")
+        hip.hipMemcpy.argtypes = [C.c_void_p, C.c_void_p, C.c_size_t, C.c_int]
+        hip.hipMemcpy.restype = C.c_int
+        _hip.lib = hip
+    return hip
+
+
+def _copy_out(dev_ptr, nbytes, dtype, shape, device):
+    """A new torch tensor holding a copy of library-owned device memory."""
+    torch = _torch()
+    t = torch.empty(shape, dtype=dtype, device=device)
+    if nbytes:
+        torch.cuda.synchronize(device)
+        rc = _hip().hipMemcpy(t.data_ptr(), dev_ptr, nbytes, 3)  # device to device
+        if rc != 0:
+            raise RuntimeError(f"hipMemcpy failed ({rc})")
+    return t
+
+
+@dataclass
+class SampleResult:
+    info: SampledInfo
+    page: object      # uint32 [R, row_words] (torch, int32 view)
+    rows: object      # int32 [R] global row ids (None when aliased)
+    gw: object        # float64 [R, 2]
+    q: object         # int64 [R, 2]
+
+
+def gbt_sample(ctx, matrix: Matrix, gpair=None, margin=None, label=None, f=1.0, mvs_lambda=1.0,
+               seed=0, iteration=0, loss=LOSS_LOGISTIC, keep_handle=False):
+    """Alg. 7 sampling + compaction; returns copies of the sampled arrays."""
+    torch = _torch()
+    sp = SampleParams(f, mvs_lambda, seed, iteration, loss, 0)
+    h = C.c_void_p()
+    _check(_lib.gbt_sample(ctx.h, matrix.h, _ptr(gpair), _ptr(margin), _ptr(label),
+                           C.byref(sp), C.byref(h)))
+    try:
+        inf = SampledInfo()
+        _check(_lib.gbt_sampled_info_get(h, C.byref(inf)))
+        R = inf.n_sampled
+        rw = matrix.info().row_words
+        dev = ctx.torch_device
+        page = _copy_out(inf.page_d, R * rw * 4, torch.int32, (R, rw), dev)
+        rows = None if inf.is_alias else _copy_out(inf.rows_d, R * 4, torch.int32, (R,), dev)
+        gw = _copy_out(inf.gpair_d, R * 16, torch.float64, (R, 2), dev)
+        q = _copy_out(inf.gpair_fx_d, R * 16, torch.int64, (R, 2), dev)
+        info = SampledInfo.from_buffer_copy(inf)
+    finally:
+        _lib.gbt_sampled_free(h)
+    return SampleResult(info, page, rows, gw, q)
+
+
+def gbt_build_hist(ctx, matrix: Matrix, page, q, rows, build, sub=(), parent_hist=None, hist=None):
+    """build: [(slot, begin, end)], sub: [(parent_slot, built_slot, target_slot)]."""
+    bl = (Seg * max(len(build), 1))(*[Seg(s, 0, b, e) for s, b, e in build])
+    sl = (Sub * max(len(sub), 1))(*[Sub(p, b, t, 0) for p, b, t in sub])
+    _check(_lib.gbt_build_hist(ctx.h, matrix.h, _ptr(page), _ptr(q), _ptr(rows), bl, len(build),
+                               sl, len(sub), _ptr(parent_hist), _ptr(hist)))
+    return hist
+
+
+def make_train_params(loss=LOSS_LOGISTIC, max_depth=6, eta=0.3, lambda_=1.0, gamma=0.0,
+                      min_child_weight=1.0, f=1.0, mvs_lambda=1.0, seed=0, iteration=0):
+    return TrainParams(loss, max_depth, eta, lambda_, gamma, min_child_weight, f, mvs_lambda,
+                       seed, iteration)
+
+
+def gbt_eval_splits(ctx, matrix: Matrix, hist, node_sums, slots, params: TrainParams, e_g, e_h):
+    torch = _torch()
+    n = len(slots)
+    out = torch.zeros((max(n, 1), SPLIT_DTYPE.itemsize // 8), dtype=torch.int64,
+                      device=ctx.torch_device)
+    sl = np.ascontiguousarray(slots, np.int32)
+    _check(_lib.gbt_eval_splits(ctx.h, matrix.h, _ptr(hist), _ptr(node_sums), _ptr(sl), n,
+                                C.byref(params), e_g, e_h, _ptr(out)))
+    return out.cpu().numpy().view(SPLIT_DTYPE).reshape(-1)[:n]
+
+
+def gbt_partition(ctx, matrix: Matrix, page, splits, segs, children, rows, position):
+    """splits: SPLIT_DTYPE array; segs: [(slot, begin, end)]; children: [l0, r0, l1, r1, ...].
+    rows/position are int32 device tensors (partitioned/updated in place).  Returns the
+    child segments as a list of (child, begin, end)."""
+    torch = _torch()
+    n = len(segs)
+    sp = np.ascontiguousarray(splits, SPLIT_DTYPE)
+    sg = (Seg * max(n, 1))(*[Seg(s, 0, b, e) for s, b, e in segs])
+    ch = np.ascontiguousarray(children, np.int32)
+    out = (Seg * max(2 * n, 1))()
+    tmp = torch.empty_like(rows)
+    _check(_lib.gbt_partition(ctx.h, matrix.h, _ptr(page), sp.ctypes.data, sg, _ptr(ch), n,
+                              _ptr(rows), _ptr(tmp), rows.numel(), _ptr(position), out))
+    return [(out[i].node_slot, out[i].begin, out[i].end) for i in range(2 * n)]
+
+
+@dataclass
+class TreeOut:
+    nodes: np.ndarray
+    exp_g: int
+    exp_h: int
+    max_depth: int
+    stats: TreeStats | None = None
+
+    def as_struct(self):
+        t = Tree(self.max_depth, len(self.nodes), self.exp_g, self.exp_h, self.nodes.ctypes.data)
+        return t
+
+
+def gbt_train_tree(ctx, matrix: Matrix, label, margin, params: TrainParams, stats=True) -> TreeOut:
+    nn = (1 << (params.max_depth + 1)) - 1
+    nodes = np.zeros(nn, NODE_DTYPE)
+    t = Tree(params.max_depth, nn, 0, 0, nodes.ctypes.data)
+    st = TreeStats() if stats else None
+    _check(_lib.gbt_train_tree(ctx.h, matrix.h, _ptr(label), _ptr(margin), C.byref(params),
+                               C.byref(t), C.byref(st) if st is not None else None))
+    return TreeOut(nodes, t.exp_g, t.exp_h, params.max_depth, st)
+
+
+def gbt_update_leaves(ctx, tree: TreeOut, params: TrainParams, matrix: Matrix, margin):
+    t = tree.as_struct()
+    _check(_lib.gbt_update_leaves(ctx.h, C.byref(t), C.byref(params), matrix.h, _ptr(margin)))
+    return tree
+
+
+def gbt_predict(ctx, trees, base_margin, binned: Matrix | None = None, raw=None, out=None):
+    """raw: dense device tensor or dict(kind='csr') of device tensors."""
+    torch = _torch()
+    arr = (Tree * max(len(trees), 1))(*[t.as_struct() for t in trees])
+    if binned is not None:
+        n = binned.info().n_rows
+        if out is None:
+            out = torch.empty(n, dtype=torch.float32, device=ctx.torch_device)
+        _check(_lib.gbt_predict(ctx.h, arr, len(trees), None, binned.h, base_margin, _ptr(out)))
+        return out
+    if isinstance(raw, dict):
+        inp, keep = csr_input(raw["indptr"], raw["indices"], raw["values"], raw["m"], LOC_DEVICE)
+    else:
+        inp, keep = dense_input(raw, LOC_DEVICE)
+    if out is None:
+        out = torch.empty(inp.n_rows, dtype=torch.float32, device=ctx.torch_device)
+    _check(_lib.gbt_predict(ctx.h, arr, len(trees), C.byref(inp), None, base_margin, _ptr(out)))
+    return out
+
+
+def train(ctx, matrix: Matrix, label, params: TrainParams, n_trees, base_margin, margin=None):
+    """n_trees boosting iterations; returns (trees, margin)."""
+    torch = _torch()
+    n = matrix.info().n_rows
+    if margin is None:
+        margin = torch.full((n,), base_margin, dtype=torch.float32, device=ctx.torch_device)
+    trees = []
+    for t in range(n_trees):
+        p = TrainParams.from_buffer_copy(params)
+        p.iteration = t
+        trees.append(gbt_train_tree(ctx, matrix, label, margin, p))
+    return trees, margin

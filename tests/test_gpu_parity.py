@@ -1,0 +1,433 @@
+"""GPU parity: every step of the HIP path, called through the C-ABI, against
+the CPU oracle on the same seeded inputs.  Integer results (cuts, pages,
+selections, fixed-point gradients, histograms, partitions, chosen splits)
+must be bit-exact; floating-point results are computed by the same IEEE
+operations on both sides and must be bit-exact too."""
+import numpy as np
+import pytest
+
+from oracle import oracle as orc
+from paper_2005_09148_amd import datagen
+from tests.gpu_helpers import node_diff, oracle_quantize, same_bits, small_csr
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def gbt():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2005_09148_amd import gbt as g
+    return g
+
+
+@pytest.fixture(scope="module")
+def ctx(gbt):
+    c = gbt.Context(0)
+    yield c
+    c.close()
+
+
+def dense_case(seed, n, m, missing, dist="normal"):
+    rng = np.random.default_rng(seed)
+    if dist == "normal":
+        X = rng.normal(size=(n, m)).astype(np.float32)
+    elif dist == "uniform":
+        X = rng.random((n, m), dtype=np.float32)
+    else:  # few distinct values, ties and a constant column
+        X = rng.integers(0, 7, size=(n, m)).astype(np.float32)
+        X[:, 0] = 3.0
+    if missing:
+        X[rng.random(X.shape) < missing] = np.nan
+    return X
+
+
+# ------------------------------------------------------------ quantization
+@pytest.mark.parametrize("n,m,missing,dist,max_bin", [
+    (3000, 28, 0.0, "normal", 256),
+    (5003, 50, 0.2, "uniform", 256),
+    (777, 9, 0.05, "ties", 16),
+    (64, 3, 0.0, "normal", 2),
+    (4097, 5, 0.5, "normal", 64),
+    (1, 4, 0.0, "normal", 256),
+])
+def test_quantize_dense(gbt, ctx, n, m, missing, dist, max_bin):
+    X = dense_case(n + m, n, m, missing, dist)
+    cuts, b, geo, page = oracle_quantize(X, max_bin)
+    mx = gbt.gbt_quantize(ctx, X, max_bin=max_bin)
+    cp, cv = mx.cuts()
+    inf = mx.info()
+    assert same_bits(cp, cuts.cut_ptr) and same_bits(cv, cuts.cut_values)
+    assert (inf.symbol_bits, inf.stride, inf.row_words) == (geo.w, geo.stride, geo.row_words)
+    assert inf.has_missing == int(b.has_missing())
+    assert same_bits(mx.page(0), page)
+
+
+def test_quantize_from_device_tensor(gbt, ctx):
+    X = dense_case(5, 2000, 7, 0.1)
+    mx = gbt.gbt_quantize(ctx, torch.from_numpy(X).cuda(), max_bin=128)
+    _, _, _, page = oracle_quantize(X, 128)
+    assert same_bits(mx.page(0), page)
+
+
+def test_quantize_sketch_stride(gbt, ctx):
+    X = dense_case(6, 5003, 6, 0.1)
+    cuts, b, geo, page = oracle_quantize(X, 32, sketch_max_rows=1000)
+    mx = gbt.gbt_quantize(ctx, X, max_bin=32, sketch_max_rows=1000)
+    cp, cv = mx.cuts()
+    assert same_bits(cv, cuts.cut_values) and same_bits(mx.page(0), page)
+
+
+@pytest.mark.parametrize("n,m,density,max_bin", [(3000, 200, 0.05, 64), (500, 40, 0.5, 256),
+                                                 (129, 2000, 0.01, 64)])
+def test_quantize_csr(gbt, ctx, n, m, density, max_bin):
+    d, _ = small_csr(n, m, density, n + m)
+    cuts, b, geo, page = oracle_quantize(d, max_bin)
+    mx = gbt.gbt_quantize(ctx, d, max_bin=max_bin)
+    cp, cv = mx.cuts()
+    inf = mx.info()
+    assert inf.sparse == 1
+    assert same_bits(cp, cuts.cut_ptr) and same_bits(cv, cuts.cut_values)
+    assert (inf.symbol_bits, inf.stride, inf.row_words, inf.null_symbol) == \
+        (geo.w, geo.stride, geo.row_words, geo.null)
+    assert same_bits(mx.page(0), page)
+
+
+@pytest.mark.parametrize("home", ["device", "pinned"])
+def test_quantize_pages_and_batches(gbt, ctx, home):
+    X = dense_case(7, 5000, 11, 0.1)
+    _, _, _, page = oracle_quantize(X, 64)
+    h = gbt.HOME_DEVICE if home == "device" else gbt.HOME_PINNED_HOST
+    q = gbt.Quantizer(ctx, 11, 5000, max_bin=64, page_rows=1536, page_home=h)
+    for lo in range(0, 5000, 1300):
+        q.sketch(X[lo:lo + 1300])
+    q.finalize()
+    for lo in range(0, 5000, 1300):
+        q.encode(X[lo:lo + 1300])
+    mx = q.end()
+    assert mx.info().n_pages == 4
+    assert same_bits(mx.pages(), page)
+
+
+def test_quantize_rejects_bad_input(gbt, ctx):
+    X = dense_case(8, 100, 3, 0.0)
+    X[5, 1] = np.inf
+    with pytest.raises(gbt.GbtError) as e:
+        gbt.gbt_quantize(ctx, X)
+    assert e.value.code == gbt.GBT_E_INVALID
+    d = {"kind": "csr", "indptr": np.array([0, 2], np.int64), "indices": np.array([1, 0], np.int32),
+         "values": np.array([1.0, 2.0], np.float32), "m": 2}
+    with pytest.raises(gbt.GbtError):
+        gbt.gbt_quantize(ctx, d)
+    with pytest.raises(gbt.GbtError):
+        gbt.gbt_quantize(ctx, dense_case(9, 10, 2, 0.0), max_bin=1)
+
+
+# ------------------------------------------------------------ gradients
+@pytest.mark.parametrize("loss", [0, 1])
+def test_gradients(gbt, ctx, loss):
+    rng = np.random.default_rng(10 + loss)
+    n = 100_003
+    z = np.concatenate([rng.normal(0, 3, n - 8), [0, -0.0, 40, -40, 709.5, -709.5, 1e-30, 37]])
+    z = z.astype(np.float32)
+    y = (rng.random(n) < 0.5).astype(np.float32) if loss == 0 else rng.normal(size=n).astype(np.float32)
+    ref = orc.gradients(loss, z, y)
+    out = gbt.gbt_gradients(ctx, loss, torch.from_numpy(z).cuda(), torch.from_numpy(y).cuda())
+    assert same_bits(out.cpu().numpy(), ref)
+    w = rng.uniform(0, 2, n).astype(np.float32)
+    ref = orc.gradients(loss, z, y, w)
+    out = gbt.gbt_gradients(ctx, loss, torch.from_numpy(z).cuda(), torch.from_numpy(y).cuda(),
+                            torch.from_numpy(w).cuda())
+    assert same_bits(out.cpu().numpy(), ref)
+
+
+# ------------------------------------------------------------ sampling
+def oracle_sample(gp, f, lam, seed, it):
+    n = len(gp)
+    if f >= 1.0:
+        sel = np.arange(n)
+        gw = gp.astype(np.float64)
+        T = 0
+        e = 0
+    else:
+        keys, e = orc.mvs_keys(gp, lam)
+        T = orc.mvs_target(f, n)
+        T = orc.mvs_threshold(keys, T)
+        keep = orc.mvs_select(keys, T, seed, it)
+        sel = np.nonzero(keep)[0]
+        w = np.array([orc.mvs_weight(int(keys[i]), T) for i in sel], np.float64)
+        gw = gp[sel].astype(np.float64) * w[:, None]
+    q, eg, eh = orc.fixed_point(gw.reshape(-1, 2)) if len(sel) else (np.zeros((0, 2), np.int64), 60, 60)
+    return sel, T, e, gw, q, eg, eh
+
+
+@pytest.mark.parametrize("f,kind", [(0.1, "normal"), (0.5, "normal"), (0.03, "skewed"),
+                                    (0.2, "equal"), (0.999, "normal"), (1.0, "normal"),
+                                    (0.1, "zeros")])
+def test_sample(gbt, ctx, f, kind):
+    rng = np.random.default_rng(20)
+    n, m = 20_011, 13
+    X = dense_case(21, n, m, 0.1)
+    _, _, _, page = oracle_quantize(X, 256)
+    mx = gbt.gbt_quantize(ctx, X, max_bin=256)
+    if kind == "normal":
+        gp = np.stack([rng.normal(size=n), rng.uniform(0.01, 0.25, n)], 1)
+    elif kind == "skewed":
+        gp = np.stack([rng.standard_cauchy(n) * 1e-3, rng.uniform(0, 1e-3, n)], 1)
+        gp[::7] = 0.0
+    elif kind == "equal":
+        gp = np.tile([[0.5, 0.25]], (n, 1))
+    else:
+        gp = np.zeros((n, 2))
+    gp = gp.astype(np.float32)
+    lam, seed, it = 1.0, 7, 3
+    sel, T, e, gw, q, eg, eh = oracle_sample(gp, f, lam, seed, it)
+    r = gbt.gbt_sample(ctx, mx, gpair=torch.from_numpy(gp).cuda(), f=f, mvs_lambda=lam, seed=seed,
+                       iteration=it)
+    assert r.info.n_sampled == len(sel)
+    if f < 1.0:
+        assert r.info.threshold == T and r.info.exp_key == e
+        assert same_bits(r.rows.cpu().numpy(), sel.astype(np.int32))
+    else:
+        assert r.info.is_alias == 1
+    assert same_bits(r.page.cpu().numpy().view(np.uint32), page[sel])
+    assert same_bits(r.gw.cpu().numpy(), gw)
+    if len(sel):
+        assert (r.info.exp_g, r.info.exp_h) == (eg, eh)
+        assert same_bits(r.q.cpu().numpy(), q)
+
+
+def test_sample_from_margins_matches_stored_gradients(gbt, ctx):
+    rng = np.random.default_rng(22)
+    n = 30_000
+    X = dense_case(23, n, 8, 0.0)
+    y = (rng.random(n) < 0.4).astype(np.float32)
+    z = rng.normal(size=n).astype(np.float32)
+    mx = gbt.gbt_quantize(ctx, X, max_bin=64)
+    gp = orc.gradients(orc.LOSS_LOGISTIC, z, y)
+    a = gbt.gbt_sample(ctx, mx, gpair=torch.from_numpy(gp).cuda(), f=0.2, seed=1, iteration=5)
+    b = gbt.gbt_sample(ctx, mx, margin=torch.from_numpy(z).cuda(), label=torch.from_numpy(y).cuda(),
+                       f=0.2, seed=1, iteration=5, loss=gbt.LOSS_LOGISTIC)
+    assert a.info.n_sampled == b.info.n_sampled and a.info.threshold == b.info.threshold
+    assert torch.equal(a.rows, b.rows) and torch.equal(a.q, b.q) and torch.equal(a.page, b.page)
+
+
+# ------------------------------------------------------------ histograms
+def test_build_hist_and_subtraction(gbt, ctx):
+    rng = np.random.default_rng(30)
+    for (n, m, missing, sparse) in [(9000, 28, 0.0, False), (7001, 50, 0.2, False),
+                                    (4000, 300, 0.03, True)]:
+        if sparse:
+            data, _ = small_csr(n, m, missing, 31)
+        else:
+            data = dense_case(31, n, m, missing)
+        _, b, _, _ = oracle_quantize(data, 256 if not sparse else 64)
+        mx = gbt.gbt_quantize(ctx, data, max_bin=256 if not sparse else 64)
+        tb = mx.info().total_bins
+        q = rng.integers(-2**40, 2**40, size=(n, 2)).astype(np.int64)
+        perm = rng.permutation(n).astype(np.int32)
+        # segments: parent P = rows[0:s], children A = rows[0:a], B = rows[a:s], plus odd sizes
+        s, a = 6000 if n > 6000 else n - 500, 2500
+        A = np.sort(perm[:a])
+        Bc = np.sort(perm[a:s])
+        rows_np = np.concatenate([A, Bc, perm[s:s + 1], perm[s + 1:s + 64]]).astype(np.int32)
+        page = torch.from_numpy(mx.page(0).view(np.int32)).cuda()
+        qd = torch.from_numpy(q).cuda()
+        rows = torch.from_numpy(rows_np).cuda()
+        parent = torch.zeros((1, tb, 2), dtype=torch.int64, device="cuda")
+        gbt.gbt_build_hist(ctx, mx, page, qd, None, [(0, 0, n)], hist=parent)
+        assert same_bits(parent[0].cpu().numpy(), orc.build_hist(b, np.arange(n), q))
+        hist = torch.zeros((5, tb, 2), dtype=torch.int64, device="cuda")
+        hist.fill_(123)  # built slots are overwritten
+        gbt.gbt_build_hist(ctx, mx, page, qd, rows,
+                           [(1, 0, a), (3, s, s + 1), (4, s + 1, s + 64), (0, 0, 0)],
+                           sub=[(0, 1, 2)], parent_hist=parent, hist=hist)
+        h = hist.cpu().numpy()
+        assert same_bits(h[1], orc.build_hist(b, A, q))
+        assert same_bits(h[3], orc.build_hist(b, rows_np[s:s + 1], q))
+        assert same_bits(h[4], orc.build_hist(b, rows_np[s + 1:s + 64], q))
+        assert not h[0].any()
+        rest = np.setdiff1d(np.arange(n), A)
+        assert same_bits(h[2], orc.build_hist(b, rest, q))
+
+
+# ------------------------------------------------------------ split evaluation
+@pytest.mark.parametrize("lam,gamma,mcw", [(1.0, 0.0, 1.0), (0.0, 0.0, 0.0), (5.0, 0.1, 0.5)])
+def test_eval_splits(gbt, ctx, lam, gamma, mcw):
+    rng = np.random.default_rng(40)
+    n, m = 6000, 37
+    X = dense_case(41, n, m, 0.15)
+    X[:, 3] = 1.0  # one bin
+    _, b, _, _ = oracle_quantize(X, 256)
+    mx = gbt.gbt_quantize(ctx, X, max_bin=256)
+    tb = mx.info().total_bins
+    gp = np.stack([rng.normal(size=n), rng.uniform(0.05, 0.25, n)], 1)
+    q, eg, eh = orc.fixed_point(gp)
+    node_rows = [np.arange(n), np.sort(rng.choice(n, 40, replace=False)), np.array([5]),
+                 np.sort(rng.choice(n, 3000, replace=False))]
+    hists = np.stack([orc.build_hist(b, r, q) for r in node_rows])
+    sums = np.stack([q[r].sum(0) for r in node_rows]).astype(np.int64)
+    P = gbt.make_train_params(lambda_=lam, gamma=gamma, min_child_weight=mcw)
+    out = gbt.gbt_eval_splits(ctx, mx, torch.from_numpy(hists).cuda(), torch.from_numpy(sums).cuda(),
+                              list(range(len(node_rows))), P, eg, eh)
+    OP = orc.Params(lambda_=lam, gamma=gamma, min_child_weight=mcw)
+    for k in range(len(node_rows)):
+        s = orc.eval_node(hists[k], sums[k], b.cuts.nbins, OP, eg, eh)
+        got = out[k]
+        assert got["valid"] == s.valid
+        if s.valid:
+            assert (got["feature"], got["split_bin"], got["default_left"]) == \
+                (s.feature, s.split_bin, s.default_left)
+            assert np.float64(got["gain"]).tobytes() == np.float64(s.gain).tobytes()
+            assert (got["left_g"], got["left_h"], got["right_g"], got["right_h"]) == \
+                (s.left_g, s.left_h, s.right_g, s.right_h)
+
+
+# ------------------------------------------------------------ partition
+def test_partition(gbt, ctx):
+    rng = np.random.default_rng(50)
+    for data, mb in [(dense_case(51, 8000, 20, 0.2), 256), (small_csr(6000, 150, 0.05, 52)[0], 64)]:
+        _, b, _, _ = oracle_quantize(data, mb)
+        mx = gbt.gbt_quantize(ctx, data, max_bin=mb)
+        n = mx.info().n_rows
+        perm = rng.permutation(n).astype(np.int32)
+        bounds = [0, 3000, 3001, 5500, n]
+        segs, splits, children = [], np.zeros(4, gbt.SPLIT_DTYPE), []
+        for k in range(4):
+            segs.append((k, bounds[k], bounds[k + 1]))
+            splits[k]["valid"] = k != 2
+            splits[k]["feature"] = int(rng.integers(0, b.m))
+            nb = int(b.cuts.nbins[splits[k]["feature"]])
+            splits[k]["split_bin"] = int(rng.integers(1, max(nb, 2)))
+            splits[k]["default_left"] = k % 2
+            children += [10 + 2 * k, 11 + 2 * k]
+        rows = torch.from_numpy(perm.copy()).cuda()
+        position = torch.full((n,), -1, dtype=torch.int32, device="cuda")
+        page = torch.from_numpy(mx.page(0).view(np.int32)).cuda()
+        out = gbt.gbt_partition(ctx, mx, page, splits, segs, children, rows, position)
+        got = rows.cpu().numpy()
+        pos = position.cpu().numpy()
+        for k in range(4):
+            seg = perm[bounds[k]:bounds[k + 1]].astype(np.int64)
+            if not splits[k]["valid"]:
+                assert same_bits(got[bounds[k]:bounds[k + 1]], seg.astype(np.int32))
+                continue
+            left, right = orc.partition(b, seg, int(splits[k]["feature"]), int(splits[k]["split_bin"]),
+                                        bool(splits[k]["default_left"]))
+            nl = len(left)
+            assert out[2 * k] == (children[2 * k], bounds[k], bounds[k] + nl)
+            assert same_bits(got[bounds[k]:bounds[k] + nl], left.astype(np.int32))
+            assert same_bits(got[bounds[k] + nl:bounds[k + 1]], right.astype(np.int32))
+            assert (pos[left] == children[2 * k]).all() and (pos[right] == children[2 * k + 1]).all()
+
+
+# ------------------------------------------------------------ whole trees
+def train_both(gbt, ctx, data, y, cfg, n_trees, page_rows=0, home=0, budget_ctx=None):
+    c = budget_ctx or ctx
+    mb = cfg.max_bin
+    _, b, _, _ = oracle_quantize(data, mb)
+    mx = gbt.gbt_quantize(c, data, max_bin=mb, page_rows=page_rows, page_home=home)
+    P = gbt.make_train_params(loss=cfg.loss, max_depth=cfg.max_depth, eta=cfg.eta, lambda_=cfg.lambda_,
+                              gamma=cfg.gamma, min_child_weight=cfg.min_child_weight, f=cfg.f,
+                              mvs_lambda=cfg.mvs_lambda, seed=cfg.seed)
+    trees, margin = gbt.train(c, mx, torch.from_numpy(y).cuda(), P, n_trees, cfg.base_margin)
+    OP = orc.Params(loss=cfg.loss, max_depth=cfg.max_depth, eta=cfg.eta, lambda_=cfg.lambda_,
+                    gamma=cfg.gamma, min_child_weight=cfg.min_child_weight, f=cfg.f,
+                    mvs_lambda=cfg.mvs_lambda, seed=cfg.seed)
+    otrees, omargin = orc.train(b, y, OP, n_trees, cfg.base_margin)
+    return trees, margin.cpu().numpy(), otrees, omargin, mx, b
+
+
+def assert_same_trees(trees, margin, otrees, omargin):
+    for t, (g, o) in enumerate(zip(trees, otrees)):
+        d = node_diff(g.nodes, o.nodes)
+        assert d is None, f"tree {t} node {d[0]}: gpu {d[1]} oracle {d[2]}"
+    assert same_bits(margin, omargin)
+
+
+@pytest.mark.parametrize("cfg_id,n,n_trees", [(1, 10_000, 10), (2, 30_000, 4), (3, 60_000, 4),
+                                               (5, 6_000, 3)])
+def test_train_trees_match_oracle(gbt, ctx, cfg_id, n, n_trees):
+    cfg = datagen.CONFIGS[cfg_id]
+    if cfg_id == 5:
+        d = datagen.config5(n=n, m=400)
+        data, y = d, d["y"]
+    else:
+        d = datagen.make(cfg_id, n)
+        data, y = d["X"], d["y"]
+    trees, margin, otrees, omargin, _, _ = train_both(gbt, ctx, data, y, cfg, n_trees)
+    assert_same_trees(trees, margin, otrees, omargin)
+    if cfg.f < 1.0:
+        assert all(t.stats.n_sampled < n for t in trees)
+
+
+def test_out_of_core_equals_in_core(gbt, ctx):
+    # no sampling: streamed pinned-host pages give the in-core trees (Sec. 4.2)
+    cfg = datagen.TrainConfig("t", 0, 64, 5, 3, eta=0.3)
+    d = datagen.config1(n=5000)
+    a = train_both(gbt, ctx, d["X"], d["y"], cfg, 3)
+    b = train_both(gbt, ctx, d["X"], d["y"], cfg, 3, page_rows=700, home=gbt.HOME_PINNED_HOST)
+    assert_same_trees(a[0], a[1], a[2], a[3])
+    assert_same_trees(b[0], b[1], a[2], a[3])
+
+
+def test_out_of_core_sampled_matches_oracle(gbt, ctx):
+    cfg = datagen.TrainConfig("t", 0, 256, 6, 3, eta=0.1, f=0.3)
+    d = datagen.config2(n=20_000)
+    r = train_both(gbt, ctx, d["X"], d["y"], cfg, 3, page_rows=3000, home=gbt.HOME_PINNED_HOST)
+    assert_same_trees(*r[:4])
+
+
+@pytest.mark.parametrize("depth,n", [(0, 1000), (1, 65), (3, 1), (4, 63)])
+def test_degenerate_trees(gbt, ctx, depth, n):
+    cfg = datagen.TrainConfig("t", 1, 32, depth, 2, eta=0.5, f=0.5 if n > 10 else 1.0)
+    d = datagen.config3(n=n, m=6)
+    r = train_both(gbt, ctx, d["X"], d["y"], cfg, 2)
+    assert_same_trees(*r[:4])
+
+
+# ------------------------------------------------------------ leaves and prediction
+def test_predict_and_update_leaves(gbt, ctx):
+    cfg = datagen.TrainConfig("t", 0, 64, 5, 4, eta=0.3, gamma=0.05)
+    d = datagen.config3(n=8000, m=12)
+    y = (d["y"] > 0).astype(np.float32)
+    X = d["X"]
+    trees, margin, otrees, omargin, mx, b = train_both(gbt, ctx, X, y, cfg, 4)
+    pb = gbt.gbt_predict(ctx, trees, 0.0, binned=mx).cpu().numpy()
+    pr = gbt.gbt_predict(ctx, trees, 0.0, raw=torch.from_numpy(X).cuda()).cpu().numpy()
+    assert same_bits(pb, orc.predict_binned(b, otrees, 0.0))
+    assert same_bits(pr, orc.predict_raw_dense(X, otrees, 0.0))
+    assert same_bits(pb, margin)
+    # CSR raw input
+    ds, Xs = small_csr(3000, 60, 0.2, 60)
+    _, bs, _, _ = oracle_quantize(ds, 64)
+    ms = gbt.gbt_quantize(ctx, ds, max_bin=64)
+    ys = (np.nan_to_num(Xs[:, 0]) > 1).astype(np.float32)
+    P = gbt.make_train_params(max_depth=4, eta=0.3)
+    st, sm = gbt.train(ctx, ms, torch.from_numpy(ys).cuda(), P, 3, 0.0)
+    ot, om = orc.train(bs, ys, orc.Params(max_depth=4, eta=0.3), 3, 0.0)
+    raw = {"kind": "csr", "indptr": torch.from_numpy(ds["indptr"]).cuda(),
+           "indices": torch.from_numpy(ds["indices"]).cuda(),
+           "values": torch.from_numpy(ds["values"]).cuda(), "m": 60}
+    pcs = gbt.gbt_predict(ctx, st, 0.0, raw=raw).cpu().numpy()
+    assert same_bits(pcs, orc.predict_raw_csr(ds["indptr"], ds["indices"], ds["values"], ot, 0.0))
+    # leaves from sums, then the margin update
+    t0 = trees[0]
+    blank = gbt.TreeOut(t0.nodes.copy(), t0.exp_g, t0.exp_h, t0.max_depth)
+    blank.nodes["leaf_value"] = 0.0
+    mg = torch.zeros(mx.info().n_rows, dtype=torch.float32, device="cuda")
+    P = gbt.make_train_params(max_depth=5, eta=0.3)
+    gbt.gbt_update_leaves(ctx, blank, P, mx, mg)
+    assert same_bits(blank.nodes, t0.nodes)
+    assert same_bits(mg.cpu().numpy(), orc.predict_binned(b, [otrees[0]], 0.0))
+
+
+def test_budget_is_enforced(gbt):
+    d = datagen.config1(n=5000)
+    small = gbt.Context(0, budget_bytes=200_000)
+    with pytest.raises(gbt.GbtError) as e:
+        gbt.gbt_quantize(small, d["X"])
+    assert e.value.code == gbt.GBT_E_BUDGET
+    small.close()
