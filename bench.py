@@ -1,0 +1,198 @@
+#!/usr/bin/env python
+"""Benchmark of the per-iteration hot path on one MI355X.
+
+A step is one boosting iteration (one tree) of the sampled-regression
+workload: 10,000,000 rows x 50 uniform features with 20% missing values,
+squared error, max_bin 256, depth 8, minimal variance sampling with f = 0.1
+in front of the tree.  The quantized ELLPACK page, labels and margins are
+resident in HBM before the timed region.  Each step runs gradients, MVS
+sampling and compaction into one device page, the fixed-point conversion,
+the level-wise tree (histograms with the sibling subtraction, split search,
+partitions), the leaves and the margin update of all 10M rows.
+
+Prints one JSON line: value = histogram row-feature updates performed per
+second of step time (G/s); ms_per_step is seconds per tree x 1000; roofline
+is that of the histogram kernel (algorithmic bytes / its HIP-event time);
+cpu_baseline times the CPU oracle on the first two trees of the same
+workload on the host (single-threaded) and reports the same unit.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "histogram row-feature updates/sec (G/s), sec/tree, achieved HBM GB/s on 1 MI355X"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--rows", type=int, default=None, help="override the row count (testing)")
+    ap.add_argument("--f", type=float, default=None, help="override the sampling fraction")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-trees", type=int, default=2)
+    return ap.parse_args()
+
+
+def oracle_updates(b, res, depth):
+    """Histogram updates the oracle performs for one tree: every evaluated node
+    (depth < max_depth) sums every non-missing symbol of each of its rows."""
+    from oracle import oracle as orc
+    rows = res.sel
+    nodes = res.nodes
+    nonnull = (b.dense[rows] != orc.MISSING).sum(1).astype(np.int64)
+    node = np.zeros(len(rows), np.int64)
+    levels = np.zeros(len(rows), np.int64)
+    active = np.ones(len(rows), bool)
+    for d in range(depth):
+        levels += active
+        idx = np.nonzero(active)[0]
+        nd = nodes[node[idx]]
+        leaf = (nd["flags"] & orc.NODE_LEAF) != 0
+        act_idx = idx[~leaf]
+        feat = nd["feature"][~leaf]
+        sb = nd["split_bin"][~leaf]
+        dl = (nd["flags"][~leaf] & orc.NODE_DEFAULT_LEFT) != 0
+        binv = b.dense[rows[act_idx], feat]
+        miss = binv == orc.MISSING
+        left = np.where(miss, dl, binv < sb)
+        node[act_idx] = np.where(left, 2 * node[act_idx] + 1, 2 * node[act_idx] + 2)
+        active[:] = False
+        active[act_idx] = True
+    return int((nonnull * levels).sum())
+
+
+def cpu_baseline(X, y, cfg, n_trees, gpu_trees):
+    """Times the oracle on the first n_trees iterations of the same workload."""
+    from oracle import oracle as orc
+    print("[bench] cpu baseline: oracle cuts and bins", file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    cuts = orc.sketch_cuts_dense(X, cfg.max_bin)
+    b = orc.bin_dense(X, cuts)
+    prep = time.perf_counter() - t0
+    P = orc.Params(loss=cfg.loss, max_depth=cfg.max_depth, eta=cfg.eta, lambda_=cfg.lambda_,
+                   gamma=cfg.gamma, min_child_weight=cfg.min_child_weight, f=cfg.f,
+                   mvs_lambda=cfg.mvs_lambda, seed=cfg.seed)
+    margin = np.full(len(y), cfg.base_margin, np.float32)
+    secs, updates, same = 0.0, 0, True
+    for t in range(n_trees):
+        t1 = time.perf_counter()
+        res = orc.train_tree(b, y, margin, P, iteration=t, want_detail=True)
+        secs += time.perf_counter() - t1
+        updates += oracle_updates(b, res, cfg.max_depth)
+        print(f"[bench] oracle tree {t}: {time.perf_counter() - t1:.1f} s", file=sys.stderr, flush=True)
+        if t < len(gpu_trees):
+            same &= res.nodes.tobytes() == gpu_trees[t].tobytes()
+    return {
+        "value": round(updates / secs / 1e9, 4),
+        "unit": "G updates/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"first {n_trees} trees of the same {len(y):,}-row workload (oracle cuts and "
+                  f"bins prepared untimed in {prep:.0f} s); {secs / n_trees:.2f} s/tree",
+        "sec_per_tree": round(secs / n_trees, 3),
+        "trees_identical_to_gpu": bool(same),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the hot path here runs on a single MI355X "
+              "(no multi-GPU path is built); run it with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2005_09148_amd import datagen, gbt
+
+    cfg = datagen.CONFIGS[3]
+    if args.f is not None:
+        cfg.f = args.f
+    n = args.rows or datagen.FULL_ROWS[3]
+    t = time.perf_counter()
+    data = datagen.config3(n)
+    X, y = data["X"], data["y"]
+    print(f"[bench] generated {n:,} x {X.shape[1]} rows in {time.perf_counter() - t:.1f} s",
+          file=sys.stderr, flush=True)
+
+    ctx = gbt.Context(0)
+    t = time.perf_counter()
+    mx = gbt.gbt_quantize(ctx, X, max_bin=cfg.max_bin)
+    info = mx.info()
+    print(f"[bench] quantized in {time.perf_counter() - t:.2f} s: w={info.symbol_bits} "
+          f"row_words={info.row_words} total_bins={info.total_bins}", file=sys.stderr, flush=True)
+    label = torch.from_numpy(y).cuda()
+    margin = torch.full((n,), cfg.base_margin, dtype=torch.float32, device="cuda")
+    P = gbt.make_train_params(loss=cfg.loss, max_depth=cfg.max_depth, eta=cfg.eta,
+                              lambda_=cfg.lambda_, gamma=cfg.gamma,
+                              min_child_weight=cfg.min_child_weight, f=cfg.f,
+                              mvs_lambda=cfg.mvs_lambda, seed=cfg.seed)
+    ctx.set_timing(True)
+    first_trees = []
+    for w in range(args.warmup):
+        P.iteration = w
+        tr = gbt.gbt_train_tree(ctx, mx, label, margin, P)
+        first_trees.append(tr.nodes.copy())
+    torch.cuda.synchronize()
+    stats = []
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        P.iteration = args.warmup + k
+        tr = gbt.gbt_train_tree(ctx, mx, label, margin, P)
+        stats.append(tr.stats)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    print(f"[bench] {args.steps} trees in {dt:.3f} s", file=sys.stderr, flush=True)
+
+    upd = sum(s.hist_updates for s in stats)
+    hbytes = sum(s.hist_bytes for s in stats)
+    hms = sum(s.ms_hist for s in stats)
+    launches = sum(s.hist_launches for s in stats)
+    phases = {k: round(sum(getattr(s, "ms_" + k) for s in stats) / args.steps, 4)
+              for k in ("sample", "hist", "hist_aux", "split", "margin", "total")}
+    achieved = hbytes / (hms * 1e-3) / 1e9 if hms > 0 else 0.0
+    line = {
+        "metric": METRIC,
+        "value": round(upd / dt / 1e9, 4),
+        "unit": "G updates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(dt * 1e3 / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic",
+        "config": {"workload": f"sampled regression {n:,} x 50, 20% missing, squared error, "
+                               f"max_bin 256, depth 8, MVS f={cfg.f}",
+                   "rows": n, "features": 50, "max_bin": cfg.max_bin, "max_depth": cfg.max_depth,
+                   "f": cfg.f},
+        "sec_per_tree": round(dt / args.steps, 6),
+        "rows_sampled_per_tree": round(sum(s.n_sampled for s in stats) / args.steps),
+        "hist_updates_per_tree": upd // args.steps,
+        "phase_ms_per_tree": phases,
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "k_hist_lds", "launches": launches,
+                     "avg_launch_us": round(hms * 1e3 / max(launches, 1), 2),
+                     "algorithmic_bytes_per_launch": hbytes // max(launches, 1)},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(X, y, cfg, args.cpu_trees, first_trees)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

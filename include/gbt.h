@@ -172,8 +172,14 @@ typedef struct {
     int64_t hist_rows;      /* rows streamed by the histogram kernels */
     int64_t hist_updates;   /* non-null (row, feature) updates performed */
     int64_t hist_bytes;     /* algorithmic bytes of the histogram kernels */
-    double ms_hist;         /* histogram kernel time (only with timing on) */
-    double ms_total;
+    /* kernel time per phase, from HIP events on the context stream (timing on) */
+    double ms_hist;         /* histogram-building kernel */
+    double ms_hist_aux;     /* histogram zeroing and sibling subtraction */
+    double ms_sample;       /* gradients, sampling, compaction, fixed point */
+    double ms_split;        /* split evaluation and partitioning */
+    double ms_margin;       /* leaves and the margin update */
+    double ms_total;        /* wall time of the call */
+    double h2d_bytes;       /* bytes streamed from pinned-host pages */
 } gbt_tree_stats;
 
 typedef struct {
@@ -212,7 +218,7 @@ gbt_status gbt_ctx_create(int32_t device, uint64_t budget_bytes, void *hip_strea
 gbt_status gbt_ctx_destroy(gbt_ctx *ctx);
 /* Bytes of device memory the context currently holds (budgeted). */
 gbt_status gbt_ctx_memory(gbt_ctx *ctx, uint64_t *used_bytes, uint64_t *peak_bytes);
-/* Record HIP events around histogram launches (for gbt_tree_stats.ms_hist). */
+/* Record HIP events around the kernels of each phase (gbt_tree_stats.ms_*). */
 gbt_status gbt_ctx_set_timing(gbt_ctx *ctx, int32_t enable);
 
 /* ---- quantile cuts and ELLPACK pages: Sec. 2.2, Sec. 3.1 (Alg. 2, 3),

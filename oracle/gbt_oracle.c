@@ -307,12 +307,19 @@ int orc_sketch_cuts_csr(const int64_t *indptr, const int32_t *indices, const flo
     return ORC_OK;
 }
 
-/* bin(x) = #{cuts < x}, by a plain linear count (the cut lists are short). */
+/* bin(x) = #{cuts < x}: the cuts ascend, so this is the first index whose
+ * cut is not below x (bisection). */
 static int32_t lookup_bin(const float *cuts, int32_t nc, float x)
 {
-    int32_t b = 0;
-    while (b < nc && cuts[b] < x) ++b;
-    return b;
+    int32_t lo = 0, hi = nc;
+    while (lo < hi) {
+        int32_t mid = lo + (hi - lo) / 2;
+        if (cuts[mid] < x)
+            lo = mid + 1;
+        else
+            hi = mid;
+    }
+    return lo;
 }
 
 /* Dense raw -> dense bins (ORC_MISSING for NaN). */

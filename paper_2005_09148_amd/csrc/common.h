@@ -61,6 +61,13 @@ struct gbt_ctx {
     uint64_t budget = 0;            // 0 = unlimited
     uint64_t used = 0, peak = 0;
     bool timing = false;
+    struct Mark {
+        int a, b;    // indices into events
+        int phase;
+    };
+    std::vector<hipEvent_t> events;  // pool, reused
+    int events_used = 0;
+    std::vector<Mark> marks;
     struct Scratch {
         void *p = nullptr;
         size_t bytes = 0;
@@ -69,6 +76,13 @@ struct gbt_ctx {
 };
 
 namespace gbt {
+
+// Phase timing: events recorded on the context stream around kernel
+// groups, read once after the stream has drained.
+enum Phase { kPhSample = 0, kPhHist, kPhHistAux, kPhSplit, kPhMargin, kPhCount };
+int timer_begin(gbt_ctx *c, int phase);   // -1 when timing is off
+void timer_end(gbt_ctx *c, int mark);
+void timer_collect(gbt_ctx *c, double *ms_per_phase);  // adds, then resets
 
 gbt_status dev_alloc(gbt_ctx *c, size_t bytes, void **p);
 void dev_free(gbt_ctx *c, void *p, size_t bytes);
@@ -101,6 +115,7 @@ enum ScratchSlot {
     kScrLeaf,        // leaf values
     kScrTrees,       // trees for prediction
     kScrSlotNode,    // slot -> node map
+    kScrPartials,    // per-chunk partial histograms
     kScrCount
 };
 

@@ -78,6 +78,46 @@ gbt_status scratch(gbt_ctx *c, int slot, size_t bytes, void **p)
     return GBT_OK;
 }
 
+static int next_event(gbt_ctx *c)
+{
+    if (c->events_used == (int)c->events.size()) {
+        hipEvent_t e;
+        if (hipEventCreate(&e) != hipSuccess) return -1;
+        c->events.push_back(e);
+    }
+    return c->events_used++;
+}
+
+int timer_begin(gbt_ctx *c, int phase)
+{
+    if (!c->timing) return -1;
+    int a = next_event(c), b = next_event(c);
+    if (a < 0 || b < 0) return -1;
+    (void)hipEventRecord(c->events[a], c->stream);
+    c->marks.push_back({a, b, phase});
+    return (int)c->marks.size() - 1;
+}
+
+void timer_end(gbt_ctx *c, int mark)
+{
+    if (mark < 0) return;
+    (void)hipEventRecord(c->events[c->marks[mark].b], c->stream);
+}
+
+void timer_collect(gbt_ctx *c, double *ms)
+{
+    if (!c->marks.empty()) {
+        (void)hipStreamSynchronize(c->stream);
+        for (auto &mk : c->marks) {
+            float t = 0.f;
+            if (hipEventElapsedTime(&t, c->events[mk.a], c->events[mk.b]) == hipSuccess && ms)
+                ms[mk.phase] += t;
+        }
+    }
+    c->marks.clear();
+    c->events_used = 0;
+}
+
 int32_t ceil_log2_u64(uint64_t v)
 {
     int32_t b = 0;
@@ -129,6 +169,7 @@ gbt_status gbt_ctx_destroy(gbt_ctx *c)
     (void)hipStreamSynchronize(c->stream);
     (void)hipStreamSynchronize(c->side);
     for (auto &s : c->scratch) dev_free(c, s.p, s.bytes);
+    for (auto e : c->events) (void)hipEventDestroy(e);
     (void)hipStreamDestroy(c->side);
     delete c;
     return GBT_OK;

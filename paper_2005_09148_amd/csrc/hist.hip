@@ -1,14 +1,16 @@
 // hist.hip -- Alg. 1 BuildHistograms on bit-packed ELLPACK rows.
 //
-// Each workgroup owns one (row chunk of one node, feature group) pair.  A
-// feature group is a contiguous feature range whose bins fit the LDS
-// budget; its int64 fixed-point (g, h) histogram lives in LDS while the
-// chunk's rows stream through (one row per lane, the group's words decoded
-// by a running bit buffer), then it is merged into the node's global
-// histogram with one 64-bit atomic per non-zero bin.  Work items are mapped
-// so that the groups of one chunk run on the same XCD and share its L2 for
-// the gradient pairs and row ids.  The sibling of a built child is the
-// parent minus the built child, an exact integer subtraction.
+// Work is split two ways.  Bins: the features are cut into contiguous groups
+// whose int64 (g, h) bins fit the LDS budget, with about equal bin counts.
+// Rows: each built node's row segment is cut into chunks.  One workgroup owns
+// one (chunk, group) pair: it accumulates the chunk's rows into its LDS
+// histogram with 64-bit LDS atomics (one row per lane, the group's words
+// decoded by a running bit buffer) and writes the result, with plain
+// coalesced stores, as a partial histogram of that chunk.  A second kernel
+// sums each node's partials into its histogram and, in the same pass, forms
+// the sibling as parent minus the built child (exact integer arithmetic).
+// Work items are mapped so the groups of one chunk run on the same XCD and
+// share its L2 for the gradient pairs and row ids.
 #include "common.h"
 
 #include <algorithm>
@@ -16,12 +18,12 @@
 
 namespace gbt {
 
-constexpr int kHistThreads = 256;
+constexpr int kHistThreads = 512;
 constexpr int kLdsBins = 4096;  // 64 KiB of int64 (g, h) per workgroup
 
 struct HistWork {
-    int64_t begin, end;
-    int32_t slot;
+    int64_t begin, end;  // rows[begin, end) of one node
+    int32_t part;        // partial histogram this chunk writes
     int32_t pad0;
 };
 
@@ -30,67 +32,104 @@ struct HistGroup {
     int32_t b0, b1;  // global bins [b0, b1)
     int32_t w0;      // dense: word holding the first bit of feature f0
     int32_t skip;    // dense: bit offset of feature f0 in that word
+    int32_t nw;      // dense: words spanned by the group's symbols
+    int32_t pad0;
 };
 
-template <bool kSparse, bool kRows>
+// A dense group spans at most this many words of a row and this many features.
+constexpr int kGroupWords = 8;
+constexpr int kMaxGroupFeat = 32;
+
+// One built node: its partials [part0, part0 + nparts) sum into hist[slot];
+// when sub_target >= 0, hist[sub_target] = parent[sub_parent] - that sum.
+struct HistReduce {
+    int32_t slot;
+    int32_t part0;
+    int32_t nparts;
+    int32_t sub_parent;
+    int32_t sub_target;
+    int32_t pad0;
+};
+
+// Zero the LDS histogram (sg | sh, nb bins each).
+__device__ inline void lds_zero(unsigned long long *lds, int32_t nb)
+{
+    for (int t = threadIdx.x; t < 2 * nb; t += kHistThreads) lds[t] = 0ull;
+    __syncthreads();
+}
+
+// Write the LDS histogram as the chunk's partial and count the updates.
+__device__ inline void lds_flush(const unsigned long long *sg, const unsigned long long *sh,
+                                 int32_t nb, longlong2 *__restrict__ dst, unsigned int cnt,
+                                 unsigned long long *__restrict__ n_updates)
+{
+    __syncthreads();
+    for (int t = threadIdx.x; t < nb; t += kHistThreads)
+        dst[t] = make_longlong2((long long)sg[t], (long long)sh[t]);
+    if (n_updates) {
+        for (int d = 32; d > 0; d >>= 1) cnt += __shfl_xor(cnt, d, 64);
+        if ((threadIdx.x & 63) == 0 && cnt) atomicAdd(n_updates, (unsigned long long)cnt);
+    }
+}
+
+// Dense rows: slot j holds feature j.  The group's bin offsets live in scalar
+// registers; each lane fetches the next row's pair and words while it
+// decodes the current row from a register queue (constant indices only).
+template <bool kRows>
 __global__ void __launch_bounds__(kHistThreads)
-    k_hist_lds(const uint32_t *__restrict__ page, int32_t row_words, int32_t w, uint32_t mask,
-               uint32_t null_sym, int32_t stride, const longlong2 *__restrict__ q,
-               const int32_t *__restrict__ rows, const HistWork *__restrict__ work,
-               const HistGroup *__restrict__ groups, int32_t n_groups,
-               const int32_t *__restrict__ bin_ptr, int64_t total_bins,
-               unsigned long long *__restrict__ hist, unsigned long long *__restrict__ n_updates)
+    k_hist_dense(const uint32_t *__restrict__ page, int32_t row_words, int32_t w, uint32_t mask,
+                 uint32_t null_sym, const longlong2 *__restrict__ q, const int32_t *__restrict__ rows,
+                 const HistWork *__restrict__ work, const HistGroup *__restrict__ groups,
+                 int32_t n_groups, const int32_t *__restrict__ bin_ptr, int64_t total_bins,
+                 longlong2 *__restrict__ partials, unsigned long long *__restrict__ n_updates)
 {
     extern __shared__ unsigned long long lds[];
     const uint32_t L = xcd_remap(blockIdx.x, gridDim.x);
     const HistWork wk = work[L / n_groups];
     const HistGroup gr = groups[L % n_groups];
-    const int32_t nb = gr.b1 - gr.b0;
+    const int32_t nb = gr.b1 - gr.b0, nf = gr.f1 - gr.f0;
     unsigned long long *sg = lds, *sh = lds + nb;
-    for (int t = threadIdx.x; t < nb; t += kHistThreads) {
-        sg[t] = 0ull;
-        sh[t] = 0ull;
-    }
-    __syncthreads();
+    int32_t off[kMaxGroupFeat];
+#pragma unroll
+    for (int u = 0; u < kMaxGroupFeat; ++u) off[u] = u < nf ? bin_ptr[gr.f0 + u] - gr.b0 : 0;
+    lds_zero(lds, nb);
+
     unsigned int cnt = 0;
-    for (int64_t i = wk.begin + threadIdx.x; i < wk.end; i += kHistThreads) {
-        const int64_t r = kRows ? (int64_t)rows[i] : i;
-        const longlong2 qq = q[r];
-        const unsigned long long qg = (unsigned long long)qq.x, qh = (unsigned long long)qq.y;
-        const uint32_t *p = page + r * row_words;
-        if (!kSparse) {
-            p += gr.w0;
-            uint64_t buf = (uint64_t)(*p++) >> gr.skip;
-            int32_t nbits = 32 - gr.skip;
-            for (int32_t f = gr.f0; f < gr.f1; ++f) {
+    int64_t i = wk.begin + threadIdx.x;
+    longlong2 qn = make_longlong2(0, 0);
+    uint32_t wn[kGroupWords];
+    auto fetch = [&](int64_t ii) {
+        const int64_t r = kRows ? (int64_t)rows[ii] : ii;
+        qn = q[r];
+        const uint32_t *p = page + r * row_words + gr.w0;
+#pragma unroll
+        for (int k = 0; k < kGroupWords; ++k) wn[k] = k < gr.nw ? p[k] : 0u;
+    };
+    if (i < wk.end) fetch(i);
+    for (; i < wk.end; i += kHistThreads) {
+        const unsigned long long qg = (unsigned long long)qn.x, qh = (unsigned long long)qn.y;
+        uint32_t wq[kGroupWords];
+#pragma unroll
+        for (int k = 0; k < kGroupWords; ++k) wq[k] = wn[k];
+        if (i + kHistThreads < wk.end) fetch(i + kHistThreads);
+        uint64_t buf = (uint64_t)wq[0] >> gr.skip;
+        int32_t nbits = 32 - gr.skip;
+#pragma unroll
+        for (int k = 0; k + 1 < kGroupWords; ++k) wq[k] = wq[k + 1];
+#pragma unroll
+        for (int u = 0; u < kMaxGroupFeat; ++u) {
+            if (u < nf) {
                 if (nbits < w) {
-                    buf |= (uint64_t)(*p++) << nbits;
+                    buf |= (uint64_t)wq[0] << nbits;
                     nbits += 32;
+#pragma unroll
+                    for (int k = 0; k + 1 < kGroupWords; ++k) wq[k] = wq[k + 1];
                 }
                 const uint32_t sym = (uint32_t)buf & mask;
                 buf >>= w;
                 nbits -= w;
                 if (sym != null_sym) {
-                    const int32_t idx = bin_ptr[f] - gr.b0 + (int32_t)sym;
-                    atomicAdd(&sg[idx], qg);
-                    atomicAdd(&sh[idx], qh);
-                    ++cnt;
-                }
-            }
-        } else {
-            uint64_t buf = (uint64_t)(*p++);
-            int32_t nbits = 32;
-            for (int32_t s = 0; s < stride; ++s) {
-                if (nbits < w) {
-                    buf |= (uint64_t)(*p++) << nbits;
-                    nbits += 32;
-                }
-                const uint32_t sym = (uint32_t)buf & mask;
-                buf >>= w;
-                nbits -= w;
-                if (sym >= (uint32_t)gr.b1) break;  // ascending; padding is the largest symbol
-                if (sym >= (uint32_t)gr.b0) {
-                    const int32_t idx = (int32_t)sym - gr.b0;
+                    const int32_t idx = off[u] + (int32_t)sym;
                     atomicAdd(&sg[idx], qg);
                     atomicAdd(&sh[idx], qh);
                     ++cnt;
@@ -98,53 +137,94 @@ __global__ void __launch_bounds__(kHistThreads)
             }
         }
     }
-    __syncthreads();
-    unsigned long long *dst = hist + ((int64_t)wk.slot * total_bins + gr.b0) * 2;
-    for (int t = threadIdx.x; t < nb; t += kHistThreads) {
-        const unsigned long long g = sg[t], h = sh[t];
-        if (g) atomicAdd(&dst[2 * t], g);
-        if (h) atomicAdd(&dst[2 * t + 1], h);
-    }
-    if (n_updates) {
-        for (int d = 32; d > 0; d >>= 1) cnt += __shfl_xor(cnt, d, 64);
-        if ((threadIdx.x & 63) == 0 && cnt) atomicAdd(n_updates, (unsigned long long)cnt);
-    }
+    lds_flush(sg, sh, nb, partials + (int64_t)wk.part * total_bins + gr.b0, cnt, n_updates);
 }
 
-__global__ void k_hist_zero(unsigned long long *__restrict__ hist, const int32_t *__restrict__ slots,
-                            int64_t total_bins)
+// Sparse rows: the row's present features in ascending order as global
+// bins, null padded; the group keeps the symbols in its bin range.
+template <bool kRows>
+__global__ void __launch_bounds__(kHistThreads)
+    k_hist_sparse(const uint32_t *__restrict__ page, int32_t row_words, int32_t w, uint32_t mask,
+                  int32_t stride, const longlong2 *__restrict__ q, const int32_t *__restrict__ rows,
+                  const HistWork *__restrict__ work, const HistGroup *__restrict__ groups,
+                  int32_t n_groups, int64_t total_bins, longlong2 *__restrict__ partials,
+                  unsigned long long *__restrict__ n_updates)
 {
-    const int64_t per = total_bins * 2;
-    unsigned long long *h = hist + (int64_t)slots[blockIdx.y] * per;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < per;
-         i += (int64_t)gridDim.x * blockDim.x)
-        h[i] = 0ull;
+    extern __shared__ unsigned long long lds[];
+    const uint32_t L = xcd_remap(blockIdx.x, gridDim.x);
+    const HistWork wk = work[L / n_groups];
+    const HistGroup gr = groups[L % n_groups];
+    const int32_t nb = gr.b1 - gr.b0;
+    unsigned long long *sg = lds, *sh = lds + nb;
+    lds_zero(lds, nb);
+    unsigned int cnt = 0;
+    for (int64_t i = wk.begin + threadIdx.x; i < wk.end; i += kHistThreads) {
+        const int64_t r = kRows ? (int64_t)rows[i] : i;
+        const longlong2 qq = q[r];
+        const unsigned long long qg = (unsigned long long)qq.x, qh = (unsigned long long)qq.y;
+        const uint32_t *p = page + r * row_words;
+        uint64_t buf = (uint64_t)(*p++);
+        int32_t nbits = 32;
+        for (int32_t s = 0; s < stride; ++s) {
+            if (nbits < w) {
+                buf |= (uint64_t)(*p++) << nbits;
+                nbits += 32;
+            }
+            const uint32_t sym = (uint32_t)buf & mask;
+            buf >>= w;
+            nbits -= w;
+            if (sym >= (uint32_t)gr.b1) break;  // ascending; padding is the largest symbol
+            if (sym >= (uint32_t)gr.b0) {
+                const int32_t idx = (int32_t)sym - gr.b0;
+                atomicAdd(&sg[idx], qg);
+                atomicAdd(&sh[idx], qh);
+                ++cnt;
+            }
+        }
+    }
+    lds_flush(sg, sh, nb, partials + (int64_t)wk.part * total_bins + gr.b0, cnt, n_updates);
 }
 
-__global__ void k_hist_sub(const longlong2 *__restrict__ parent, longlong2 *__restrict__ hist,
-                           const gbt_sub *__restrict__ subs, int64_t total_bins)
+__global__ void k_hist_reduce(const longlong2 *__restrict__ partials, const HistReduce *__restrict__ red,
+                              const longlong2 *__restrict__ parent, longlong2 *__restrict__ hist,
+                              int64_t total_bins)
 {
-    const gbt_sub s = subs[blockIdx.y];
-    const longlong2 *p = parent + (int64_t)s.parent_slot * total_bins;
-    const longlong2 *b = hist + (int64_t)s.built_slot * total_bins;
-    longlong2 *t = hist + (int64_t)s.target_slot * total_bins;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total_bins;
-         i += (int64_t)gridDim.x * blockDim.x) {
-        longlong2 a = p[i], c = b[i];
-        t[i] = make_longlong2(a.x - c.x, a.y - c.y);
+    const HistReduce rd = red[blockIdx.y];
+    for (int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; b < total_bins;
+         b += (int64_t)gridDim.x * blockDim.x) {
+        long long g = 0, h = 0;
+        for (int32_t k = 0; k < rd.nparts; ++k) {
+            longlong2 v = partials[(int64_t)(rd.part0 + k) * total_bins + b];
+            g += v.x;
+            h += v.y;
+        }
+        hist[(int64_t)rd.slot * total_bins + b] = make_longlong2(g, h);
+        if (rd.sub_target >= 0) {
+            longlong2 pv = parent[(int64_t)rd.sub_parent * total_bins + b];
+            hist[(int64_t)rd.sub_target * total_bins + b] = make_longlong2(pv.x - g, pv.y - h);
+        }
     }
 }
 
-// Feature groups whose bins fit kLdsBins (a single wider feature gets a group
-// of its own and the global-memory kernel).
+// Feature groups with at most kLdsBins bins each and about equal bin counts;
+// a dense group's symbols also span at most kGroupWords words.
 static void make_groups(const gbt_matrix *mx, std::vector<HistGroup> *out, bool *fits)
 {
     out->clear();
     *fits = true;
+    const int64_t tb = mx->total_bins;
+    const int64_t G = std::max<int64_t>(1, (tb + kLdsBins - 1) / kLdsBins);
+    const int64_t target = (tb + G - 1) / G;
+    auto span_words = [&](int32_t f0, int32_t f1) {
+        int64_t b0 = (int64_t)f0 * mx->w, b1 = (int64_t)f1 * mx->w;
+        return (int32_t)((b1 + 31) / 32 - b0 / 32);
+    };
     int32_t f0 = 0;
     while (f0 < mx->m) {
         int32_t f1 = f0 + 1;
-        while (f1 < mx->m && mx->bin_ptr_h[f1 + 1] - mx->bin_ptr_h[f0] <= kLdsBins) ++f1;
+        while (f1 < mx->m && mx->bin_ptr_h[f1 + 1] - mx->bin_ptr_h[f0] <= target &&
+               (mx->sparse || (span_words(f0, f1 + 1) <= kGroupWords && f1 + 1 - f0 <= kMaxGroupFeat)))
+            ++f1;
         HistGroup g;
         g.f0 = f0;
         g.f1 = f1;
@@ -153,7 +233,10 @@ static void make_groups(const gbt_matrix *mx, std::vector<HistGroup> *out, bool 
         int64_t bit = (int64_t)f0 * mx->w;
         g.w0 = (int32_t)(bit >> 5);
         g.skip = (int32_t)(bit & 31);
+        g.nw = span_words(f0, f1);
+        g.pad0 = 0;
         if (g.b1 - g.b0 > kLdsBins) *fits = false;
+        if (!mx->sparse && g.nw > kGroupWords) *fits = false;
         out->push_back(g);
         f0 = f1;
     }
@@ -165,114 +248,115 @@ gbt_status build_hist_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *pag
                            int64_t *hist, gbt_tree_stats *stats)
 {
     const int64_t tb = mx->total_bins;
-    if (tb == 0 || (n_build == 0 && n_sub == 0)) return GBT_OK;
+    if (tb == 0 || n_build == 0) {
+        GBT_CHECK(n_sub == 0, "a subtraction needs its built sibling in the same call");
+        return GBT_OK;
+    }
     std::vector<HistGroup> groups;
     bool fits;
     make_groups(mx, &groups, &fits);
     if (!fits)
-        return set_error(GBT_E_UNSUPPORTED, "a feature has more than %d bins", kLdsBins);
+        return set_error(GBT_E_UNSUPPORTED, "a feature has more than %d bins or %d words of symbols",
+                         kLdsBins, kGroupWords);
     const int32_t G = (int32_t)groups.size();
 
     int64_t total_rows = 0;
     for (int32_t k = 0; k < n_build; ++k) total_rows += std::max<int64_t>(0, build[k].end - build[k].begin);
-    // chunk so the grid is a few waves of workgroups per CU
-    const int64_t target_wg = 8 * kCUs;
+    // chunks: about two workgroups per CU over all groups, at least 2048 rows each
+    const int64_t target_wg = 2 * kCUs;
     int64_t chunk = (total_rows * G + target_wg - 1) / target_wg;
-    chunk = std::min<int64_t>(std::max<int64_t>(chunk, 2048), 1 << 20);
+    chunk = std::max<int64_t>(chunk, 2048);
     std::vector<HistWork> work;
-    std::vector<int32_t> slots;
+    std::vector<HistReduce> red;
+    int32_t nparts = 0;
     for (int32_t k = 0; k < n_build; ++k) {
-        slots.push_back(build[k].node_slot);
-        for (int64_t b = build[k].begin; b < build[k].end; b += chunk)
-            work.push_back({b, std::min(build[k].end, b + chunk), build[k].node_slot, 0});
+        HistReduce rd{build[k].node_slot, nparts, 0, -1, -1, 0};
+        for (int64_t b = build[k].begin; b < build[k].end; b += chunk) {
+            work.push_back({b, std::min(build[k].end, b + chunk), nparts, 0});
+            ++nparts;
+            ++rd.nparts;
+        }
+        red.push_back(rd);
+    }
+    for (int32_t s = 0; s < n_sub; ++s) {
+        int32_t k = 0;
+        while (k < n_build && build[k].node_slot != sub[s].built_slot) ++k;
+        GBT_CHECK(k < n_build, "subtraction %d names slot %d, which is not built", s, sub[s].built_slot);
+        GBT_CHECK(red[k].sub_target < 0, "slot %d is the built child of two subtractions", sub[s].built_slot);
+        red[k].sub_parent = sub[s].parent_slot;
+        red[k].sub_target = sub[s].target_slot;
     }
 
-    // upload the plan: groups | work | slots | subs
+    // upload the plan: groups | work | reduce items
     size_t o_w = ((size_t)G * sizeof(HistGroup) + 255) / 256 * 256;
-    size_t o_s = o_w + (work.size() * sizeof(HistWork) + 255) / 256 * 256;
-    size_t o_u = o_s + (slots.size() * 4 + 255) / 256 * 256;
-    size_t bytes = o_u + (size_t)n_sub * sizeof(gbt_sub) + 256;
+    size_t o_r = o_w + (std::max<size_t>(work.size(), 1) * sizeof(HistWork) + 255) / 256 * 256;
+    size_t bytes = o_r + red.size() * sizeof(HistReduce) + 256;
     char *plan;
     GBT_TRY(scratch_t(c, kScrWork, bytes, &plan));
     std::vector<char> h(bytes);
     memcpy(h.data(), groups.data(), G * sizeof(HistGroup));
     if (!work.empty()) memcpy(h.data() + o_w, work.data(), work.size() * sizeof(HistWork));
-    if (!slots.empty()) memcpy(h.data() + o_s, slots.data(), slots.size() * 4);
-    if (n_sub) memcpy(h.data() + o_u, sub, (size_t)n_sub * sizeof(gbt_sub));
+    memcpy(h.data() + o_r, red.data(), red.size() * sizeof(HistReduce));
     GBT_HIP(hipMemcpyAsync(plan, h.data(), bytes, hipMemcpyHostToDevice, c->stream));
     const HistGroup *groups_d = (const HistGroup *)plan;
     const HistWork *work_d = (const HistWork *)(plan + o_w);
-    const int32_t *slots_d = (const int32_t *)(plan + o_s);
-    const gbt_sub *subs_d = (const gbt_sub *)(plan + o_u);
+    const HistReduce *red_d = (const HistReduce *)(plan + o_r);
 
+    longlong2 *partials = nullptr;
+    GBT_TRY(scratch(c, kScrPartials, (size_t)std::max(nparts, 1) * tb * 16, (void **)&partials));
+
+    // the tree driver zeroes this counter per tree and reads it once
     unsigned long long *upd = nullptr;
     if (stats) GBT_TRY(scratch_t(c, kScrUpd, 1, &upd));
 
-    if (n_build) {
-        dim3 zg((unsigned)std::min<int64_t>((tb * 2 + 255) / 256, 1024), (unsigned)n_build);
-        k_hist_zero<<<zg, 256, 0, c->stream>>>((unsigned long long *)hist, slots_d, tb);
-        GBT_LAUNCHED();
-    }
     if (!work.empty()) {
-        if (stats) {
-            unsigned long long zero = 0;
-            GBT_HIP(hipMemcpyAsync(upd, &zero, 8, hipMemcpyHostToDevice, c->stream));
-        }
         int32_t maxnb = 0;
         for (auto &g : groups) maxnb = std::max(maxnb, g.b1 - g.b0);
         size_t lds = (size_t)maxnb * 16;
         uint32_t null_sym = (mx->sparse || mx->has_missing) ? mx->null_sym : 0xffffffffu;
         uint32_t mask = mx->w >= 32 ? 0xffffffffu : ((1u << mx->w) - 1u);
         unsigned grid = (unsigned)(work.size() * (size_t)G);
-        hipEvent_t e0 = nullptr, e1 = nullptr;
-        if (c->timing && stats) {
-            GBT_HIP(hipEventCreate(&e0));
-            GBT_HIP(hipEventCreate(&e1));
-            GBT_HIP(hipEventRecord(e0, c->stream));
-        }
-#define GBT_HIST_LAUNCH(SP, RW)                                                                    \
-    k_hist_lds<SP, RW><<<grid, kHistThreads, lds, c->stream>>>(                                     \
-        page, mx->row_words, mx->w, mask, null_sym, mx->stride, (const longlong2 *)q, rows, work_d, \
-        groups_d, G, mx->bin_ptr_d, tb, (unsigned long long *)hist, upd)
+        const int mark = timer_begin(c, kPhHist);
+#define GBT_HIST_DENSE(RW)                                                                        \
+    k_hist_dense<RW><<<grid, kHistThreads, lds, c->stream>>>(page, mx->row_words, mx->w, mask, null_sym, \
+                                                             (const longlong2 *)q, rows, work_d,       \
+                                                             groups_d, G, mx->bin_ptr_d, tb, partials, upd)
+#define GBT_HIST_SPARSE(RW)                                                                       \
+    k_hist_sparse<RW><<<grid, kHistThreads, lds, c->stream>>>(page, mx->row_words, mx->w, mask,     \
+                                                              mx->stride, (const longlong2 *)q, rows, \
+                                                              work_d, groups_d, G, tb, partials, upd)
         if (mx->sparse) {
             if (rows)
-                GBT_HIST_LAUNCH(true, true);
+                GBT_HIST_SPARSE(true);
             else
-                GBT_HIST_LAUNCH(true, false);
+                GBT_HIST_SPARSE(false);
         } else {
             if (rows)
-                GBT_HIST_LAUNCH(false, true);
+                GBT_HIST_DENSE(true);
             else
-                GBT_HIST_LAUNCH(false, false);
+                GBT_HIST_DENSE(false);
         }
-#undef GBT_HIST_LAUNCH
+#undef GBT_HIST_DENSE
+#undef GBT_HIST_SPARSE
         GBT_LAUNCHED();
-        if (e0) {
-            GBT_HIP(hipEventRecord(e1, c->stream));
-            GBT_HIP(hipEventSynchronize(e1));
-            float ms = 0.f;
-            GBT_HIP(hipEventElapsedTime(&ms, e0, e1));
-            stats->ms_hist += ms;
-            (void)hipEventDestroy(e0);
-            (void)hipEventDestroy(e1);
-        }
+        timer_end(c, mark);
         if (stats) {
-            unsigned long long u = 0;
-            GBT_HIP(hipMemcpyAsync(&u, upd, 8, hipMemcpyDeviceToHost, c->stream));
-            GBT_HIP(hipStreamSynchronize(c->stream));
+            // algorithmic bytes: the packed symbols of each row, its 16-byte
+            // fixed-point pair, its 4-byte row id (when indirect), and one
+            // write of every chunk's partial histogram
             int64_t wbytes = 4 * (((int64_t)mx->stride * mx->w + 31) / 32);
             stats->hist_launches += 1;
             stats->hist_rows += total_rows;
-            stats->hist_updates += (int64_t)u;
-            stats->hist_bytes += total_rows * (wbytes + 16 + (rows ? 4 : 0)) + (int64_t)n_build * tb * 16;
+            stats->hist_bytes += total_rows * (wbytes + 16 + (rows ? 4 : 0)) + (int64_t)nparts * tb * 16;
         }
     }
-    if (n_sub) {
-        GBT_CHECK(parent_hist, "subtraction needs the parent histograms");
-        dim3 sg((unsigned)std::min<int64_t>((tb + 255) / 256, 1024), (unsigned)n_sub);
-        k_hist_sub<<<sg, 256, 0, c->stream>>>((const longlong2 *)parent_hist, (longlong2 *)hist, subs_d, tb);
-        GBT_LAUNCHED();
-    }
+    const int aux = timer_begin(c, kPhHistAux);
+    GBT_CHECK(n_sub == 0 || parent_hist, "subtraction needs the parent histograms");
+    dim3 rg((unsigned)std::min<int64_t>((tb + 255) / 256, 256), (unsigned)red.size());
+    k_hist_reduce<<<rg, 256, 0, c->stream>>>(partials, red_d, (const longlong2 *)parent_hist,
+                                             (longlong2 *)hist, tb);
+    GBT_LAUNCHED();
+    timer_end(c, aux);
     return GBT_OK;
 }
 

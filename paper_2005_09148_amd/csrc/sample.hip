@@ -101,6 +101,33 @@ __device__ inline uint64_t philox_word0(uint64_t c0, uint64_t c1, uint64_t c2, u
     return c0;
 }
 
+// ------------------------------------------------------------ block reductions
+// 256-thread blocks: wavefront butterfly, then the four wave results in LDS.
+__device__ inline unsigned long long block_max_u64(unsigned long long v, unsigned long long *lds4)
+{
+    for (int d = 32; d > 0; d >>= 1) {
+        unsigned long long o = __shfl_xor(v, d, 64);
+        v = o > v ? o : v;
+    }
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) lds4[threadIdx.x >> 6] = v;
+    __syncthreads();
+    unsigned long long r = lds4[0];
+    for (int w = 1; w < 4; ++w) r = lds4[w] > r ? lds4[w] : r;
+    return r;
+}
+
+__device__ inline unsigned long long block_sum_u64(unsigned long long v, unsigned long long *lds4)
+{
+    for (int d = 32; d > 0; d >>= 1) v += __shfl_xor(v, d, 64);
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) lds4[threadIdx.x >> 6] = v;
+    __syncthreads();
+    return lds4[0] + lds4[1] + lds4[2] + lds4[3];
+}
+
+constexpr int kReduceGrid = 2048;  // blocks of the grid-stride reductions
+
 // ------------------------------------------------------------ MVS keys
 template <int kSrc>
 __device__ inline void row_gh(const SampleSrc &src, int64_t i, double *g, double *h)
@@ -127,20 +154,21 @@ template <int kSrc>
 __global__ void __launch_bounds__(256) k_mvs_rmax(SampleSrc src, int64_t n, double lambda,
                                                   SampleState *__restrict__ st)
 {
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    double r = 0.0;
-    if (i < n) {
+    __shared__ unsigned long long lds4[4];
+    unsigned long long b = 0;
+    bool bad = false;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
         double g, h;
         row_gh<kSrc>(src, i, &g, &h);
-        r = mvs_r(g, h, lambda);
-        if (r != r || r > 1.7e308) atomicOr(&st->bad, 1u);
+        double r = mvs_r(g, h, lambda);
+        bad |= (r != r || r > 1.7e308);
+        unsigned long long rb = __double_as_longlong(r);  // r >= 0: bit order = value order
+        b = rb > b ? rb : b;
     }
-    unsigned long long b = __double_as_longlong(r);
-    for (int d = 32; d > 0; d >>= 1) {
-        unsigned long long o = __shfl_xor(b, d, 64);
-        b = o > b ? o : b;
-    }
-    if ((threadIdx.x & 63) == 0 && b) atomicMax(&st->rmax_bits, b);
+    if (bad) atomicOr(&st->bad, 1u);
+    b = block_max_u64(b, lds4);
+    if (threadIdx.x == 0 && b) atomicMax(&st->rmax_bits, b);
 }
 
 // a_i = rint(r_i * 2^e), e = 62 - E - L with max r < 2^E; also max and sum
@@ -150,28 +178,27 @@ __global__ void __launch_bounds__(256) k_mvs_keys(SampleSrc src, int64_t n, doub
                                                   int32_t log2n, SampleState *__restrict__ st,
                                                   int64_t *__restrict__ keys)
 {
+    __shared__ unsigned long long lds4[4];
     int E;
     frexp(__longlong_as_double(st->rmax_bits), &E);
-    int32_t e = 62 - E - log2n;
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    unsigned long long a = 0;
-    if (i < n) {
+    const int32_t e = 62 - E - log2n;
+    unsigned long long mx = 0, sm = 0;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
         double g, h;
         row_gh<kSrc>(src, i, &g, &h);
-        a = (unsigned long long)(long long)rint(ldexp(mvs_r(g, h, lambda), e));
+        unsigned long long a = (unsigned long long)(long long)rint(ldexp(mvs_r(g, h, lambda), e));
         if (keys) keys[i] = (int64_t)a;
+        mx = a > mx ? a : mx;
+        sm += a;
     }
-    unsigned long long mx = a, sm = a;
-    for (int d = 32; d > 0; d >>= 1) {
-        unsigned long long o = __shfl_xor(mx, d, 64);
-        mx = o > mx ? o : mx;
-        sm += __shfl_xor(sm, d, 64);
-    }
-    if ((threadIdx.x & 63) == 0) {
+    mx = block_max_u64(mx, lds4);
+    sm = block_sum_u64(sm, lds4);
+    if (threadIdx.x == 0) {
         if (mx) atomicMax(&st->amax, mx);
         if (sm) atomicAdd(&st->asum, sm);
+        if (blockIdx.x == 0) st->e_key = e;
     }
-    if (i == 0) st->e_key = e;
 }
 
 // Closed form when T* exceeds every key; otherwise the radix descent
@@ -384,19 +411,18 @@ __global__ void k_gw_all(const float2 *__restrict__ gpair, int64_t n, double2 *_
 __global__ void __launch_bounds__(256) k_fx_max(const double2 *__restrict__ gw, int64_t R,
                                                 SampleState *__restrict__ st)
 {
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    __shared__ unsigned long long lds4[4];
     unsigned long long bg = 0, bh = 0;
-    if (i < R) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < R;
+         i += (int64_t)gridDim.x * blockDim.x) {
         double2 v = gw[i];
-        bg = __double_as_longlong(fabs(v.x));
-        bh = __double_as_longlong(fabs(v.y));
+        unsigned long long a = __double_as_longlong(fabs(v.x)), b = __double_as_longlong(fabs(v.y));
+        bg = a > bg ? a : bg;
+        bh = b > bh ? b : bh;
     }
-    for (int d = 32; d > 0; d >>= 1) {
-        unsigned long long og = __shfl_xor(bg, d, 64), oh = __shfl_xor(bh, d, 64);
-        bg = og > bg ? og : bg;
-        bh = oh > bh ? oh : bh;
-    }
-    if ((threadIdx.x & 63) == 0) {
+    bg = block_max_u64(bg, lds4);
+    bh = block_max_u64(bh, lds4);
+    if (threadIdx.x == 0) {
         if (bg) atomicMax(&st->gmax_bits, bg);
         if (bh) atomicMax(&st->hmax_bits, bh);
     }
@@ -408,29 +434,29 @@ __global__ void __launch_bounds__(256) k_fx_convert(const double2 *__restrict__ 
                                                     int32_t log2R, SampleState *__restrict__ st,
                                                     longlong2 *__restrict__ q)
 {
+    __shared__ unsigned long long lds4[4];
     int Eg, Eh;
     frexp(__longlong_as_double(st->gmax_bits), &Eg);
     frexp(__longlong_as_double(st->hmax_bits), &Eh);
-    int32_t eg = 62 - Eg - log2R, eh = 62 - Eh - log2R;
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    long long qg = 0, qh = 0;
-    if (i < R) {
+    const int32_t eg = 62 - Eg - log2R, eh = 62 - Eh - log2R;
+    unsigned long long sg = 0, sh = 0;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < R;
+         i += (int64_t)gridDim.x * blockDim.x) {
         double2 v = gw[i];
-        qg = (long long)rint(ldexp(v.x, eg));
-        qh = (long long)rint(ldexp(v.y, eh));
+        long long qg = (long long)rint(ldexp(v.x, eg)), qh = (long long)rint(ldexp(v.y, eh));
         q[i] = make_longlong2(qg, qh);
+        sg += (unsigned long long)qg;
+        sh += (unsigned long long)qh;
     }
-    for (int d = 32; d > 0; d >>= 1) {
-        qg += __shfl_xor(qg, d, 64);
-        qh += __shfl_xor(qh, d, 64);
-    }
-    if ((threadIdx.x & 63) == 0) {
-        atomicAdd(&st->root_g, (unsigned long long)qg);
-        atomicAdd(&st->root_h, (unsigned long long)qh);
-    }
-    if (i == 0) {
-        st->e_g = eg;
-        st->e_h = eh;
+    sg = block_sum_u64(sg, lds4);
+    sh = block_sum_u64(sh, lds4);
+    if (threadIdx.x == 0) {
+        if (sg) atomicAdd(&st->root_g, sg);
+        if (sh) atomicAdd(&st->root_h, sh);
+        if (blockIdx.x == 0) {
+            st->e_g = eg;
+            st->e_h = eh;
+        }
     }
 }
 
@@ -450,6 +476,8 @@ __global__ void k_zero_u64(unsigned long long *p, int64_t n)
 
 static unsigned blocks(int64_t n, int t = 256) { return (unsigned)((n + t - 1) / t); }
 
+static unsigned rblocks(int64_t n) { return std::max(1u, std::min(blocks(n), (unsigned)kReduceGrid)); }
+
 static int32_t log2_ceil(int64_t v) { return v <= 1 ? 0 : ceil_log2_u64((uint64_t)v); }
 
 // ------------------------------------------------------------ drivers
@@ -461,14 +489,14 @@ gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64
     GBT_TRY(scratch_t(c, kScrMisc, 2 * kDigitBuckets, &hist));
     if (n > 0) {
         if (kind == kSrcGpair)
-            k_mvs_rmax<kSrcGpair><<<blocks(n), 256, 0, c->stream>>>(src, n, lambda, st);
+            k_mvs_rmax<kSrcGpair><<<rblocks(n), 256, 0, c->stream>>>(src, n, lambda, st);
         else
-            k_mvs_rmax<kSrcMargin><<<blocks(n), 256, 0, c->stream>>>(src, n, lambda, st);
+            k_mvs_rmax<kSrcMargin><<<rblocks(n), 256, 0, c->stream>>>(src, n, lambda, st);
         GBT_LAUNCHED();
         if (kind == kSrcGpair)
-            k_mvs_keys<kSrcGpair><<<blocks(n), 256, 0, c->stream>>>(src, n, lambda, l2, st, (int64_t *)keys);
+            k_mvs_keys<kSrcGpair><<<rblocks(n), 256, 0, c->stream>>>(src, n, lambda, l2, st, (int64_t *)keys);
         else
-            k_mvs_keys<kSrcMargin><<<blocks(n), 256, 0, c->stream>>>(src, n, lambda, l2, st, (int64_t *)keys);
+            k_mvs_keys<kSrcMargin><<<rblocks(n), 256, 0, c->stream>>>(src, n, lambda, l2, st, (int64_t *)keys);
         GBT_LAUNCHED();
     }
     k_mvs_thresh_init<<<1, 64, 0, c->stream>>>(st, K);
@@ -478,7 +506,7 @@ gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64
     GBT_HIP(hipMemcpyAsync(host_st, st, sizeof(SampleState), hipMemcpyDeviceToHost, c->stream));
     GBT_HIP(hipStreamSynchronize(c->stream));
     if (host_st->bad & 1u) return set_error(GBT_E_INVALID, "non-finite gradient in sampling");
-    unsigned grid = (unsigned)std::min<int64_t>(std::max<int64_t>(blocks(n), 1), 4 * kCUs);
+    unsigned grid = (unsigned)std::min<int64_t>(std::max<int64_t>(blocks(n), 1), 2 * kCUs);
     for (int lev = 0; lev < host_st->levels; ++lev) {
         if (kind == kSrcGpair)
             k_mvs_radix_hist<kSrcGpair><<<grid, 256, 0, c->stream>>>(src, keys, n, lambda, l2, st, hist,
@@ -541,9 +569,9 @@ gbt_status fixed_point(gbt_ctx *c, const double *gw, int64_t R, SampleState *st,
         GBT_LAUNCHED();
         return GBT_OK;
     }
-    k_fx_max<<<blocks(R), 256, 0, c->stream>>>((const double2 *)gw, R, st);
+    k_fx_max<<<rblocks(R), 256, 0, c->stream>>>((const double2 *)gw, R, st);
     GBT_LAUNCHED();
-    k_fx_convert<<<blocks(R), 256, 0, c->stream>>>((const double2 *)gw, R, log2_ceil(R), st,
+    k_fx_convert<<<rblocks(R), 256, 0, c->stream>>>((const double2 *)gw, R, log2_ceil(R), st,
                                                    (longlong2 *)q);
     GBT_LAUNCHED();
     return GBT_OK;

@@ -208,6 +208,11 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
 }
 
 // ------------------------------------------------------------ tree kernels
+__global__ void k_zero_counter(unsigned long long *p)
+{
+    if (threadIdx.x == 0) *p = 0ull;
+}
+
 __global__ void k_tree_init(DevNode *__restrict__ nodes, int32_t n_nodes, long long rg, long long rh,
                             int64_t R)
 {
@@ -307,14 +312,45 @@ __global__ void k_margin_pos(float *__restrict__ margin, const int32_t *__restri
     if (i < n) margin[i] = margin[i] + leaf[position[i]];
 }
 
-// Margin update by walking each row's symbols down the tree.
-__global__ void k_margin_walk(const uint32_t *__restrict__ words, int64_t rows, Geo geo,
-                              const DevNode *__restrict__ nodes, const float *__restrict__ leaf,
-                              float *__restrict__ margin)
+// Row staging for the tree walks: the block's 256 consecutive rows are read
+// with coalesced 16-byte loads into LDS (row stride padded to an odd word
+// count against bank conflicts); each lane then walks its row from LDS.
+constexpr int kWalkThreads = 256;
+constexpr int kWalkMaxWords = 60;  // rows up to this many words are staged
+
+template <bool kStage>
+__device__ inline const uint32_t *stage_row(const uint32_t *__restrict__ words, int64_t rows,
+                                            int32_t row_words, uint32_t *lds)
 {
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t r0 = (int64_t)blockIdx.x * kWalkThreads;
+    if (!kStage) return words + (r0 + threadIdx.x) * row_words;
+    const int32_t ps = row_words + 1;
+    const int32_t q4 = row_words / 4;
+    const int32_t nr = (int32_t)min((int64_t)kWalkThreads, rows - r0);
+    const uint4 *src = (const uint4 *)(words + r0 * row_words);
+    for (int32_t t = threadIdx.x; t < nr * q4; t += kWalkThreads) {
+        uint4 v = src[t];
+        uint32_t *d = lds + (t / q4) * ps + (t % q4) * 4;
+        d[0] = v.x;
+        d[1] = v.y;
+        d[2] = v.z;
+        d[3] = v.w;
+    }
+    __syncthreads();
+    return lds + threadIdx.x * ps;
+}
+
+// Margin update by walking each row's symbols down the tree.
+template <bool kStage>
+__global__ void __launch_bounds__(kWalkThreads)
+    k_margin_walk(const uint32_t *__restrict__ words, int64_t rows, Geo geo,
+                  const DevNode *__restrict__ nodes, const float *__restrict__ leaf,
+                  float *__restrict__ margin)
+{
+    extern __shared__ uint32_t walk_lds[];
+    const uint32_t *row = stage_row<kStage>(words, rows, geo.row_words, walk_lds);
+    int64_t i = (int64_t)blockIdx.x * kWalkThreads + threadIdx.x;
     if (i >= rows) return;
-    const uint32_t *row = words + i * geo.row_words;
     int32_t id = 0;
     while (nodes[id].split) {
         const DevNode &d = nodes[id];
@@ -338,13 +374,16 @@ __device__ inline int32_t walk_binned(const gbt_node *__restrict__ t, int64_t nn
     return id;
 }
 
-__global__ void k_predict_binned(const uint32_t *__restrict__ words, int64_t rows, Geo geo,
-                                 const gbt_node *__restrict__ trees, const int64_t *__restrict__ offs,
-                                 int32_t n_trees, float base, float *__restrict__ out)
+template <bool kStage>
+__global__ void __launch_bounds__(kWalkThreads)
+    k_predict_binned(const uint32_t *__restrict__ words, int64_t rows, Geo geo,
+                     const gbt_node *__restrict__ trees, const int64_t *__restrict__ offs,
+                     int32_t n_trees, float base, float *__restrict__ out)
 {
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    extern __shared__ uint32_t walk_lds[];
+    const uint32_t *row = stage_row<kStage>(words, rows, geo.row_words, walk_lds);
+    int64_t i = (int64_t)blockIdx.x * kWalkThreads + threadIdx.x;
     if (i >= rows) return;
-    const uint32_t *row = words + i * geo.row_words;
     float acc = base;
     for (int32_t t = 0; t < n_trees; ++t) {
         const gbt_node *tr = trees + offs[t];
@@ -418,13 +457,19 @@ __global__ void k_leaf_values(gbt_node *__restrict__ t, int32_t n, int32_t eg, i
         t[i].leaf_value = leaf_of(t[i].sum_g, t[i].sum_h, eg, eh, lambda, eta);
 }
 
-__global__ void k_margin_add_tree(const uint32_t *__restrict__ words, int64_t rows, Geo geo,
-                                  const gbt_node *__restrict__ t, int64_t nn, float *__restrict__ margin)
+template <bool kStage>
+__global__ void __launch_bounds__(kWalkThreads)
+    k_margin_add_tree(const uint32_t *__restrict__ words, int64_t rows, Geo geo,
+                      const gbt_node *__restrict__ t, int64_t nn, float *__restrict__ margin)
 {
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    extern __shared__ uint32_t walk_lds[];
+    const uint32_t *row = stage_row<kStage>(words, rows, geo.row_words, walk_lds);
+    int64_t i = (int64_t)blockIdx.x * kWalkThreads + threadIdx.x;
     if (i >= rows) return;
-    margin[i] = margin[i] + t[walk_binned(t, nn, words + i * geo.row_words, geo)].leaf_value;
+    margin[i] = margin[i] + t[walk_binned(t, nn, row, geo)].leaf_value;
 }
+
+static size_t walk_lds_bytes(const Geo &g) { return (size_t)kWalkThreads * (g.row_words + 1) * 4; }
 
 // ------------------------------------------------------------ the iteration
 struct LevelNode {
@@ -444,6 +489,15 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     const bool host_pages = any_host_pages(mx);
     double h2d = 0.0;
 
+    unsigned long long *upd = nullptr;
+    if (stats) {
+        GBT_TRY(scratch_t(c, kScrUpd, 1, &upd));
+        k_zero_counter<<<1, 64, 0, c->stream>>>(upd);
+        GBT_LAUNCHED();
+    }
+    c->marks.clear();
+    c->events_used = 0;
+    int mark = timer_begin(c, kPhSample);
     float *gpair = nullptr;
     if (!host_pages) {
         GBT_TRY(scratch_t(c, kScrGpair, (size_t)std::max<int64_t>(n, 1) * 2, &gpair));
@@ -453,6 +507,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     gbt_sample_params sp{p->f, p->mvs_lambda, p->seed, p->iteration, p->loss, 0};
     SampleOut so;
     GBT_TRY(sample_run(c, mx, gpair, margin, label, sp, bufs, &so, &h2d));
+    timer_end(c, mark);
     const int64_t R = so.R;
     if (stats) {
         stats->n_sampled = R;
@@ -498,6 +553,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         std::vector<EvalNode> ev(nc);
         for (int32_t k = 0; k < nc; ++k) ev[k] = {cur[k].sum_g, cur[k].sum_h, cur[k].slot, cur[k].heap};
         GBT_HIP(hipMemcpyAsync(ev_d, ev.data(), nc * sizeof(EvalNode), hipMemcpyHostToDevice, c->stream));
+        mark = timer_begin(c, kPhSplit);
         GBT_TRY(eval_impl(c, mx, histA, ev_d, nc, ep, splits_d));
         k_decide<<<blocks(nc), 256, 0, c->stream>>>(nodes, ev_d, splits_d, nc);
         GBT_LAUNCHED();
@@ -508,6 +564,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
             k_children<<<blocks(nc), 256, 0, c->stream>>>(nodes, ev_d, nc, P);
             GBT_LAUNCHED();
         }
+        timer_end(c, mark);
         // the next level's nodes
         const int32_t first = (1 << (d + 1)) - 1, count = 1 << (d + 1);
         hnodes.resize(count);
@@ -544,6 +601,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         cur.swap(next);
     }
     // ---- leaves and the margin update of all n rows (Eq. 1)
+    mark = timer_begin(c, kPhMargin);
     k_leaves<<<blocks(NN), 256, 0, c->stream>>>(nodes, NN, so.e_g, so.e_h, p->lambda, p->eta, leaf);
     GBT_LAUNCHED();
     if (so.alias) {
@@ -556,13 +614,18 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         GBT_TRY(for_each_chunk(
             c, mx,
             [&](const uint32_t *words, int64_t row0, int64_t rows_n) -> gbt_status {
-                k_margin_walk<<<blocks(rows_n), 256, 0, c->stream>>>(words, rows_n, geo, nodes, leaf,
-                                                                     margin + row0);
+                if (geo.row_words <= kWalkMaxWords)
+                    k_margin_walk<true><<<blocks(rows_n), kWalkThreads, walk_lds_bytes(geo), c->stream>>>(
+                        words, rows_n, geo, nodes, leaf, margin + row0);
+                else
+                    k_margin_walk<false><<<blocks(rows_n), kWalkThreads, 0, c->stream>>>(
+                        words, rows_n, geo, nodes, leaf, margin + row0);
                 GBT_LAUNCHED();
                 return GBT_OK;
             },
             &h2d));
     }
+    timer_end(c, mark);
     // ---- the tree, host side
     std::vector<DevNode> all(NN);
     std::vector<float> leafh(NN);
@@ -593,7 +656,19 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
             o.leaf_value = leafh[i];
         }
     }
+    double ms[kPhCount] = {0.0};
+    timer_collect(c, ms);
     if (stats) {
+        unsigned long long u = 0;
+        GBT_HIP(hipMemcpyAsync(&u, upd, 8, hipMemcpyDeviceToHost, c->stream));
+        GBT_HIP(hipStreamSynchronize(c->stream));
+        stats->hist_updates = (int64_t)u;
+        stats->ms_sample = ms[kPhSample];
+        stats->ms_hist = ms[kPhHist];
+        stats->ms_hist_aux = ms[kPhHistAux];
+        stats->ms_split = ms[kPhSplit];
+        stats->ms_margin = ms[kPhMargin];
+        stats->h2d_bytes = h2d;
         stats->ms_total =
             std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t_start).count();
     }
@@ -733,8 +808,12 @@ gbt_status gbt_update_leaves(gbt_ctx *c, gbt_tree *tree, const gbt_train_params 
     GBT_TRY(for_each_chunk(
         c, data,
         [&](const uint32_t *words, int64_t row0, int64_t rows) -> gbt_status {
-            k_margin_add_tree<<<blocks(rows), 256, 0, c->stream>>>(words, rows, geo, nodes_d, tree->n_nodes,
-                                                                   margin_d + row0);
+            if (geo.row_words <= kWalkMaxWords)
+                k_margin_add_tree<true><<<blocks(rows), kWalkThreads, walk_lds_bytes(geo), c->stream>>>(
+                    words, rows, geo, nodes_d, tree->n_nodes, margin_d + row0);
+            else
+                k_margin_add_tree<false><<<blocks(rows), kWalkThreads, 0, c->stream>>>(
+                    words, rows, geo, nodes_d, tree->n_nodes, margin_d + row0);
             GBT_LAUNCHED();
             return GBT_OK;
         },
@@ -760,8 +839,12 @@ gbt_status gbt_predict(gbt_ctx *c, const gbt_tree *trees, int32_t n_trees, const
         GBT_TRY(for_each_chunk(
             c, binned,
             [&](const uint32_t *words, int64_t row0, int64_t rows) -> gbt_status {
-                k_predict_binned<<<blocks(rows), 256, 0, c->stream>>>(words, rows, geo, nodes_d, offs_d,
-                                                                     n_trees, base_margin, margin_out_d + row0);
+                if (geo.row_words <= kWalkMaxWords)
+                    k_predict_binned<true><<<blocks(rows), kWalkThreads, walk_lds_bytes(geo), c->stream>>>(
+                        words, rows, geo, nodes_d, offs_d, n_trees, base_margin, margin_out_d + row0);
+                else
+                    k_predict_binned<false><<<blocks(rows), kWalkThreads, 0, c->stream>>>(
+                        words, rows, geo, nodes_d, offs_d, n_trees, base_margin, margin_out_d + row0);
                 GBT_LAUNCHED();
                 return GBT_OK;
             },

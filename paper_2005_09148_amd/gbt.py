@@ -104,7 +104,8 @@ class TreeStats(C.Structure):
     _fields_ = [("n_sampled", C.c_int64), ("threshold", C.c_int64), ("exp_key", C.c_int32),
                 ("hist_launches", C.c_int32), ("hist_rows", C.c_int64),
                 ("hist_updates", C.c_int64), ("hist_bytes", C.c_int64), ("ms_hist", C.c_double),
-                ("ms_total", C.c_double)]
+                ("ms_hist_aux", C.c_double), ("ms_sample", C.c_double), ("ms_split", C.c_double),
+                ("ms_margin", C.c_double), ("ms_total", C.c_double), ("h2d_bytes", C.c_double)]
 
 
 class SampleParams(C.Structure):
