@@ -218,8 +218,9 @@ gbt_status gbt_ctx_create(int32_t device, uint64_t budget_bytes, void *hip_strea
 gbt_status gbt_ctx_destroy(gbt_ctx *ctx);
 /* Bytes of device memory the context currently holds (budgeted). */
 gbt_status gbt_ctx_memory(gbt_ctx *ctx, uint64_t *used_bytes, uint64_t *peak_bytes);
-/* Record HIP events around the kernels of each phase (gbt_tree_stats.ms_*). */
-gbt_status gbt_ctx_set_timing(gbt_ctx *ctx, int32_t enable);
+/* HIP events on the context stream (gbt_tree_stats.ms_*): 0 off, 1 around
+ * the histogram-building kernel only, 2 around every phase. */
+gbt_status gbt_ctx_set_timing(gbt_ctx *ctx, int32_t level);
 
 /* ---- quantile cuts and ELLPACK pages: Sec. 2.2, Sec. 3.1 (Alg. 2, 3),
  * Sec. 3.2 (Alg. 4, 5) ------------------------------------------------------

@@ -40,6 +40,7 @@ gbt_status hip_error(hipError_t e, const char *what, const char *file, int line)
 #define GBT_LAUNCHED() GBT_HIP(hipGetLastError())
 
 constexpr int kXcds = 8;         // gfx950: 8 XCDs of 32 CUs
+constexpr int kUpdCounters = 16; // spread copies of the histogram update counter
 constexpr int kCUs = 256;
 
 // Map a linear workgroup id so that logically adjacent ids run on the same
@@ -60,7 +61,7 @@ struct gbt_ctx {
     hipStream_t side = nullptr;     // host-to-device page copies
     uint64_t budget = 0;            // 0 = unlimited
     uint64_t used = 0, peak = 0;
-    bool timing = false;
+    int timing = 0;  // 0 off, 1 histogram kernel only, 2 every phase
     struct Mark {
         int a, b;    // indices into events
         int phase;
@@ -116,6 +117,9 @@ enum ScratchSlot {
     kScrTrees,       // trees for prediction
     kScrSlotNode,    // slot -> node map
     kScrPartials,    // per-chunk partial histograms
+    kScrCompact,     // compact tree for the row walk
+    kScrPlan,        // device-side level plans (lists, work items, counts)
+    kScrPartialsDev, // partial histograms of the device-planned levels
     kScrCount
 };
 
@@ -239,6 +243,12 @@ struct DevNode {
 // i in [0, n], out[n] = total.  Device-wide, deterministic.
 gbt_status scan_u8(gbt_ctx *c, const uint8_t *in, int64_t n, int32_t *out);
 gbt_status scan_u32(gbt_ctx *c, const uint32_t *in, int64_t n, int32_t *out);
+// Exclusive sums of the per-tile counts of n flags (tiles of 4096);
+// tile_off[ceil(n/4096)] = total.
+gbt_status scan_tiles_u8(gbt_ctx *c, const uint8_t *in, int64_t n, int32_t *tile_off);
+// The scan given the per-tile counts of its first pass (tile_cnt is
+// overwritten with the tile offsets).
+gbt_status scan_u8_from_tiles(gbt_ctx *c, const uint8_t *in, int64_t n, int32_t *tile_cnt, int32_t *out);
 
 // ---------------------------------------------------------------- shared launches
 gbt_status launch_gradients(gbt_ctx *c, int32_t loss, const float *margin, const float *label,

@@ -90,7 +90,7 @@ static int next_event(gbt_ctx *c)
 
 int timer_begin(gbt_ctx *c, int phase)
 {
-    if (!c->timing) return -1;
+    if (c->timing == 0 || (c->timing == 1 && phase != kPhHist)) return -1;
     int a = next_event(c), b = next_event(c);
     if (a < 0 || b < 0) return -1;
     (void)hipEventRecord(c->events[a], c->stream);
@@ -186,7 +186,7 @@ gbt_status gbt_ctx_memory(gbt_ctx *c, uint64_t *used, uint64_t *peak)
 gbt_status gbt_ctx_set_timing(gbt_ctx *c, int32_t enable)
 {
     if (!c) return set_error(GBT_E_INVALID, "gbt_ctx_set_timing: ctx is NULL");
-    c->timing = enable != 0;
+    c->timing = enable < 0 ? 0 : (enable > 2 ? 2 : enable);
     return GBT_OK;
 }
 

@@ -11,7 +11,7 @@
 // the sibling as parent minus the built child (exact integer arithmetic).
 // Work items are mapped so the groups of one chunk run on the same XCD and
 // share its L2 for the gradient pairs and row ids.
-#include "common.h"
+#include "hist_impl.h"
 
 #include <algorithm>
 #include <cstring>
@@ -21,35 +21,9 @@ namespace gbt {
 constexpr int kHistThreads = 512;
 constexpr int kLdsBins = 4096;  // 64 KiB of int64 (g, h) per workgroup
 
-struct HistWork {
-    int64_t begin, end;  // rows[begin, end) of one node
-    int32_t part;        // partial histogram this chunk writes
-    int32_t pad0;
-};
-
-struct HistGroup {
-    int32_t f0, f1;  // features [f0, f1)
-    int32_t b0, b1;  // global bins [b0, b1)
-    int32_t w0;      // dense: word holding the first bit of feature f0
-    int32_t skip;    // dense: bit offset of feature f0 in that word
-    int32_t nw;      // dense: words spanned by the group's symbols
-    int32_t pad0;
-};
-
 // A dense group spans at most this many words of a row and this many features.
 constexpr int kGroupWords = 8;
 constexpr int kMaxGroupFeat = 32;
-
-// One built node: its partials [part0, part0 + nparts) sum into hist[slot];
-// when sub_target >= 0, hist[sub_target] = parent[sub_parent] - that sum.
-struct HistReduce {
-    int32_t slot;
-    int32_t part0;
-    int32_t nparts;
-    int32_t sub_parent;
-    int32_t sub_target;
-    int32_t pad0;
-};
 
 // Zero the LDS histogram (sg | sh, nb bins each).
 __device__ inline void lds_zero(unsigned long long *lds, int32_t nb)
@@ -67,8 +41,16 @@ __device__ inline void lds_flush(const unsigned long long *sg, const unsigned lo
     for (int t = threadIdx.x; t < nb; t += kHistThreads)
         dst[t] = make_longlong2((long long)sg[t], (long long)sh[t]);
     if (n_updates) {
+        // one atomic per block, spread over kUpdCounters addresses
+        __shared__ unsigned int red[kHistThreads / 64];
         for (int d = 32; d > 0; d >>= 1) cnt += __shfl_xor(cnt, d, 64);
-        if ((threadIdx.x & 63) == 0 && cnt) atomicAdd(n_updates, (unsigned long long)cnt);
+        if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = cnt;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            unsigned long long t = 0;
+            for (int w = 0; w < kHistThreads / 64; ++w) t += red[w];
+            if (t) atomicAdd(&n_updates[blockIdx.x % kUpdCounters], t);
+        }
     }
 }
 
@@ -80,11 +62,14 @@ __global__ void __launch_bounds__(kHistThreads)
     k_hist_dense(const uint32_t *__restrict__ page, int32_t row_words, int32_t w, uint32_t mask,
                  uint32_t null_sym, const longlong2 *__restrict__ q, const int32_t *__restrict__ rows,
                  const HistWork *__restrict__ work, const HistGroup *__restrict__ groups,
-                 int32_t n_groups, const int32_t *__restrict__ bin_ptr, int64_t total_bins,
-                 longlong2 *__restrict__ partials, unsigned long long *__restrict__ n_updates)
+                 int32_t n_groups, const int32_t *__restrict__ n_work_d, const int32_t *__restrict__ bin_ptr,
+                 int64_t total_bins, longlong2 *__restrict__ partials,
+                 unsigned long long *__restrict__ n_updates)
 {
     extern __shared__ unsigned long long lds[];
-    const uint32_t L = xcd_remap(blockIdx.x, gridDim.x);
+    const uint32_t active = n_work_d ? (uint32_t)(*n_work_d * n_groups) : gridDim.x;
+    if (blockIdx.x >= active) return;
+    const uint32_t L = xcd_remap(blockIdx.x, active);
     const HistWork wk = work[L / n_groups];
     const HistGroup gr = groups[L % n_groups];
     const int32_t nb = gr.b1 - gr.b0, nf = gr.f1 - gr.f0;
@@ -147,11 +132,13 @@ __global__ void __launch_bounds__(kHistThreads)
     k_hist_sparse(const uint32_t *__restrict__ page, int32_t row_words, int32_t w, uint32_t mask,
                   int32_t stride, const longlong2 *__restrict__ q, const int32_t *__restrict__ rows,
                   const HistWork *__restrict__ work, const HistGroup *__restrict__ groups,
-                  int32_t n_groups, int64_t total_bins, longlong2 *__restrict__ partials,
-                  unsigned long long *__restrict__ n_updates)
+                  int32_t n_groups, const int32_t *__restrict__ n_work_d, int64_t total_bins,
+                  longlong2 *__restrict__ partials, unsigned long long *__restrict__ n_updates)
 {
     extern __shared__ unsigned long long lds[];
-    const uint32_t L = xcd_remap(blockIdx.x, gridDim.x);
+    const uint32_t active = n_work_d ? (uint32_t)(*n_work_d * n_groups) : gridDim.x;
+    if (blockIdx.x >= active) return;
+    const uint32_t L = xcd_remap(blockIdx.x, active);
     const HistWork wk = work[L / n_groups];
     const HistGroup gr = groups[L % n_groups];
     const int32_t nb = gr.b1 - gr.b0;
@@ -186,9 +173,10 @@ __global__ void __launch_bounds__(kHistThreads)
 }
 
 __global__ void k_hist_reduce(const longlong2 *__restrict__ partials, const HistReduce *__restrict__ red,
-                              const longlong2 *__restrict__ parent, longlong2 *__restrict__ hist,
-                              int64_t total_bins)
+                              const int32_t *__restrict__ n_red_d, const longlong2 *__restrict__ parent,
+                              longlong2 *__restrict__ hist, int64_t total_bins)
 {
+    if (n_red_d && (int32_t)blockIdx.y >= *n_red_d) return;
     const HistReduce rd = red[blockIdx.y];
     for (int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; b < total_bins;
          b += (int64_t)gridDim.x * blockDim.x) {
@@ -208,10 +196,10 @@ __global__ void k_hist_reduce(const longlong2 *__restrict__ partials, const Hist
 
 // Feature groups with at most kLdsBins bins each and about equal bin counts;
 // a dense group's symbols also span at most kGroupWords words.
-static void make_groups(const gbt_matrix *mx, std::vector<HistGroup> *out, bool *fits)
+bool hist_groups(const gbt_matrix *mx, std::vector<HistGroup> *out)
 {
     out->clear();
-    *fits = true;
+    bool fits = true;
     const int64_t tb = mx->total_bins;
     const int64_t G = std::max<int64_t>(1, (tb + kLdsBins - 1) / kLdsBins);
     const int64_t target = (tb + G - 1) / G;
@@ -235,11 +223,12 @@ static void make_groups(const gbt_matrix *mx, std::vector<HistGroup> *out, bool 
         g.skip = (int32_t)(bit & 31);
         g.nw = span_words(f0, f1);
         g.pad0 = 0;
-        if (g.b1 - g.b0 > kLdsBins) *fits = false;
-        if (!mx->sparse && g.nw > kGroupWords) *fits = false;
+        if (g.b1 - g.b0 > kLdsBins) fits = false;
+        if (!mx->sparse && g.nw > kGroupWords) fits = false;
         out->push_back(g);
         f0 = f1;
     }
+    return fits;
 }
 
 gbt_status build_hist_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int64_t *q,
@@ -253,8 +242,7 @@ gbt_status build_hist_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *pag
         return GBT_OK;
     }
     std::vector<HistGroup> groups;
-    bool fits;
-    make_groups(mx, &groups, &fits);
+    const bool fits = hist_groups(mx, &groups);
     if (!fits)
         return set_error(GBT_E_UNSUPPORTED, "a feature has more than %d bins or %d words of symbols",
                          kLdsBins, kGroupWords);
@@ -305,26 +293,50 @@ gbt_status build_hist_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *pag
     longlong2 *partials = nullptr;
     GBT_TRY(scratch(c, kScrPartials, (size_t)std::max(nparts, 1) * tb * 16, (void **)&partials));
 
-    // the tree driver zeroes this counter per tree and reads it once
+    // the tree driver zeroes these counters per tree and reads them once
     unsigned long long *upd = nullptr;
-    if (stats) GBT_TRY(scratch_t(c, kScrUpd, 1, &upd));
+    if (stats) GBT_TRY(scratch_t(c, kScrUpd, kUpdCounters, &upd));
 
-    if (!work.empty()) {
-        int32_t maxnb = 0;
-        for (auto &g : groups) maxnb = std::max(maxnb, g.b1 - g.b0);
-        size_t lds = (size_t)maxnb * 16;
+    HistLaunch hl{groups_d, G, 0, work_d, nullptr, (int32_t)work.size(), red_d, nullptr, (int32_t)red.size(),
+                  (int64_t *)partials};
+    for (auto &g : groups) hl.max_groups_bins = std::max(hl.max_groups_bins, g.b1 - g.b0);
+    GBT_CHECK(n_sub == 0 || parent_hist, "subtraction needs the parent histograms");
+    GBT_TRY(hist_launch_device(c, mx, page, q, rows, hl, parent_hist, hist, upd));
+    if (stats && !work.empty()) {
+        // algorithmic bytes: the packed symbols of each row, its 16-byte
+        // fixed-point pair, its 4-byte row id (when indirect), and one write
+        // of every chunk's partial histogram
+        int64_t wbytes = 4 * (((int64_t)mx->stride * mx->w + 31) / 32);
+        stats->hist_launches += 1;
+        stats->hist_rows += total_rows;
+        stats->hist_bytes += total_rows * (wbytes + 16 + (rows ? 4 : 0)) + (int64_t)nparts * tb * 16;
+    }
+    return GBT_OK;
+}
+
+gbt_status hist_launch_device(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int64_t *q,
+                              const int32_t *rows, const HistLaunch &hl, const int64_t *parent_hist,
+                              int64_t *hist, unsigned long long *upd)
+{
+    const int64_t tb = mx->total_bins;
+    const int32_t G = hl.n_groups;
+    longlong2 *partials = (longlong2 *)hl.partials;
+    if (hl.max_work > 0) {
+        size_t lds = (size_t)hl.max_groups_bins * 16;
         uint32_t null_sym = (mx->sparse || mx->has_missing) ? mx->null_sym : 0xffffffffu;
         uint32_t mask = mx->w >= 32 ? 0xffffffffu : ((1u << mx->w) - 1u);
-        unsigned grid = (unsigned)(work.size() * (size_t)G);
+        unsigned grid = (unsigned)((size_t)hl.max_work * (size_t)G);
         const int mark = timer_begin(c, kPhHist);
-#define GBT_HIST_DENSE(RW)                                                                        \
-    k_hist_dense<RW><<<grid, kHistThreads, lds, c->stream>>>(page, mx->row_words, mx->w, mask, null_sym, \
-                                                             (const longlong2 *)q, rows, work_d,       \
-                                                             groups_d, G, mx->bin_ptr_d, tb, partials, upd)
-#define GBT_HIST_SPARSE(RW)                                                                       \
-    k_hist_sparse<RW><<<grid, kHistThreads, lds, c->stream>>>(page, mx->row_words, mx->w, mask,     \
-                                                              mx->stride, (const longlong2 *)q, rows, \
-                                                              work_d, groups_d, G, tb, partials, upd)
+#define GBT_HIST_DENSE(RW)                                                                          \
+    k_hist_dense<RW><<<grid, kHistThreads, lds, c->stream>>>(page, mx->row_words, mx->w, mask, null_sym,   \
+                                                             (const longlong2 *)q, rows, hl.work,        \
+                                                             hl.groups, G, hl.n_work_d, mx->bin_ptr_d, tb, \
+                                                             partials, upd)
+#define GBT_HIST_SPARSE(RW)                                                                        \
+    k_hist_sparse<RW><<<grid, kHistThreads, lds, c->stream>>>(page, mx->row_words, mx->w, mask,      \
+                                                              mx->stride, (const longlong2 *)q, rows,  \
+                                                              hl.work, hl.groups, G, hl.n_work_d, tb,  \
+                                                              partials, upd)
         if (mx->sparse) {
             if (rows)
                 GBT_HIST_SPARSE(true);
@@ -340,23 +352,15 @@ gbt_status build_hist_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *pag
 #undef GBT_HIST_SPARSE
         GBT_LAUNCHED();
         timer_end(c, mark);
-        if (stats) {
-            // algorithmic bytes: the packed symbols of each row, its 16-byte
-            // fixed-point pair, its 4-byte row id (when indirect), and one
-            // write of every chunk's partial histogram
-            int64_t wbytes = 4 * (((int64_t)mx->stride * mx->w + 31) / 32);
-            stats->hist_launches += 1;
-            stats->hist_rows += total_rows;
-            stats->hist_bytes += total_rows * (wbytes + 16 + (rows ? 4 : 0)) + (int64_t)nparts * tb * 16;
-        }
     }
-    const int aux = timer_begin(c, kPhHistAux);
-    GBT_CHECK(n_sub == 0 || parent_hist, "subtraction needs the parent histograms");
-    dim3 rg((unsigned)std::min<int64_t>((tb + 255) / 256, 256), (unsigned)red.size());
-    k_hist_reduce<<<rg, 256, 0, c->stream>>>(partials, red_d, (const longlong2 *)parent_hist,
-                                             (longlong2 *)hist, tb);
-    GBT_LAUNCHED();
-    timer_end(c, aux);
+    if (hl.max_red > 0) {
+        const int aux = timer_begin(c, kPhHistAux);
+        dim3 rg((unsigned)std::min<int64_t>((tb + 255) / 256, 256), (unsigned)hl.max_red);
+        k_hist_reduce<<<rg, 256, 0, c->stream>>>(partials, hl.red, hl.n_red_d, (const longlong2 *)parent_hist,
+                                                 (longlong2 *)hist, tb);
+        GBT_LAUNCHED();
+        timer_end(c, aux);
+    }
     return GBT_OK;
 }
 

@@ -1,0 +1,59 @@
+// hist_impl.h -- internal interface of the histogram kernels (hist.hip) used
+// by the tree driver, which plans the levels below the root on the device.
+#pragma once
+
+#include <vector>
+
+#include "common.h"
+
+namespace gbt {
+
+struct HistWork {
+    int64_t begin, end;  // rows[begin, end) of one node
+    int32_t part;        // partial histogram this chunk writes
+    int32_t pad0;
+};
+
+struct HistGroup {
+    int32_t f0, f1;  // features [f0, f1)
+    int32_t b0, b1;  // global bins [b0, b1)
+    int32_t w0;      // dense: word holding the first bit of feature f0
+    int32_t skip;    // dense: bit offset of feature f0 in that word
+    int32_t nw;      // dense: words spanned by the group's symbols
+    int32_t pad0;
+};
+
+// One built node: its partials [part0, part0 + nparts) sum into hist[slot];
+// when sub_target >= 0, hist[sub_target] = parent[sub_parent] - that sum.
+struct HistReduce {
+    int32_t slot;
+    int32_t part0;
+    int32_t nparts;
+    int32_t sub_parent;
+    int32_t sub_target;
+    int32_t pad0;
+};
+
+// Feature groups of the histogram kernels; false when a feature does not fit.
+bool hist_groups(const gbt_matrix *mx, std::vector<HistGroup> *out);
+
+// A histogram pass whose work lists live on the device.  Counts are read
+// from device memory (n_work_d, n_red_d); the grids are sized by the maxima.
+struct HistLaunch {
+    const HistGroup *groups;
+    int32_t n_groups;
+    int32_t max_groups_bins;  // largest group, in bins
+    const HistWork *work;
+    const int32_t *n_work_d;
+    int32_t max_work;
+    const HistReduce *red;
+    const int32_t *n_red_d;
+    int32_t max_red;
+    int64_t *partials;
+};
+
+gbt_status hist_launch_device(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int64_t *q,
+                              const int32_t *rows, const HistLaunch &hl, const int64_t *parent_hist,
+                              int64_t *hist, unsigned long long *n_updates);
+
+}  // namespace gbt

@@ -68,6 +68,13 @@ __global__ void k_gradients(int32_t loss, const float *__restrict__ margin,
     gpair[i] = make_float2((float)g, (float)h);
 }
 
+// Gradients of all rows and the maximum of r over them, as the keys define it
+// (from the float-rounded pair).
+__global__ void __launch_bounds__(256) k_gradients_rmax(int32_t loss, const float *__restrict__ margin,
+                                                        const float *__restrict__ label, int64_t n,
+                                                        float2 *__restrict__ gpair, double lambda,
+                                                        SampleState *__restrict__ st);
+
 gbt_status launch_gradients(gbt_ctx *c, int32_t loss, const float *margin, const float *label,
                             const float *weight, int64_t n, float *gpair)
 {
@@ -168,7 +175,7 @@ __global__ void __launch_bounds__(256) k_mvs_rmax(SampleSrc src, int64_t n, doub
     }
     if (bad) atomicOr(&st->bad, 1u);
     b = block_max_u64(b, lds4);
-    if (threadIdx.x == 0 && b) atomicMax(&st->rmax_bits, b);
+    if (threadIdx.x == 0 && b) atomicMax(&st->rmax[blockIdx.x % kSpread], b);
 }
 
 // a_i = rint(r_i * 2^e), e = 62 - E - L with max r < 2^E; also max and sum
@@ -180,7 +187,7 @@ __global__ void __launch_bounds__(256) k_mvs_keys(SampleSrc src, int64_t n, doub
 {
     __shared__ unsigned long long lds4[4];
     int E;
-    frexp(__longlong_as_double(st->rmax_bits), &E);
+    frexp(__longlong_as_double(fold_max(st->rmax)), &E);
     const int32_t e = 62 - E - log2n;
     unsigned long long mx = 0, sm = 0;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
@@ -195,8 +202,8 @@ __global__ void __launch_bounds__(256) k_mvs_keys(SampleSrc src, int64_t n, doub
     mx = block_max_u64(mx, lds4);
     sm = block_sum_u64(sm, lds4);
     if (threadIdx.x == 0) {
-        if (mx) atomicMax(&st->amax, mx);
-        if (sm) atomicAdd(&st->asum, sm);
+        if (mx) atomicMax(&st->amax[blockIdx.x % kSpread], mx);
+        if (sm) atomicAdd(&st->asum[blockIdx.x % kSpread], sm);
         if (blockIdx.x == 0) st->e_key = e;
     }
 }
@@ -206,7 +213,7 @@ __global__ void __launch_bounds__(256) k_mvs_keys(SampleSrc src, int64_t n, doub
 __global__ void k_mvs_thresh_init(SampleState *__restrict__ st, int64_t K)
 {
     if (threadIdx.x != 0) return;
-    unsigned long long amax = st->amax, asum = st->asum;
+    unsigned long long amax = fold_max(st->amax), asum = fold_sum(st->asum);
     unsigned long long q = (asum + (unsigned long long)K - 1) / (unsigned long long)K;
     st->C_above = 0;
     st->F_below = 0;
@@ -366,38 +373,6 @@ __global__ void __launch_bounds__(256) k_mvs_select(SampleSrc src, const int64_t
     keep[i] = k ? 1 : 0;
 }
 
-// Gather the kept rows (ascending) into the sampled page and reweight their
-// gradients by the inverse inclusion probability.
-template <int kSrc>
-__global__ void __launch_bounds__(256) k_compact(SampleSrc src, const int64_t *__restrict__ keys,
-                                                 int64_t n, double lambda,
-                                                 const SampleState *__restrict__ st,
-                                                 const uint8_t *__restrict__ keep,
-                                                 const int32_t *__restrict__ pos,
-                                                 const uint4 *__restrict__ page, int32_t row_q4,
-                                                 int64_t out_base, uint4 *__restrict__ out_page,
-                                                 int32_t *__restrict__ sel, int64_t sel_offset,
-                                                 double2 *__restrict__ gw)
-{
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n || !keep[i]) return;
-    int64_t k = (int64_t)pos[i] - out_base;
-    const uint4 *src_row = page + i * row_q4;
-    uint4 *dst = out_page + k * row_q4;
-    for (int32_t t = 0; t < row_q4; ++t) dst[t] = src_row[t];
-    sel[k] = (int32_t)(sel_offset + i);
-    double g, h;
-    row_gh<kSrc>(src, i, &g, &h);
-    unsigned long long a;
-    if (keys)
-        a = (unsigned long long)keys[i];
-    else
-        a = (unsigned long long)(long long)rint(ldexp(mvs_r(g, h, lambda), st->e_key));
-    unsigned long long T = (unsigned long long)st->T;
-    double w = a >= T ? 1.0 : (double)(long long)T / (double)(long long)a;
-    gw[k] = make_double2(g * w, h * w);
-}
-
 // f = 1: every row trains, unweighted.
 __global__ void k_gw_all(const float2 *__restrict__ gpair, int64_t n, double2 *__restrict__ gw)
 {
@@ -405,6 +380,100 @@ __global__ void k_gw_all(const float2 *__restrict__ gpair, int64_t n, double2 *_
     if (i >= n) return;
     float2 p = gpair[i];
     gw[i] = make_double2((double)p.x, (double)p.y);
+}
+
+// Compaction of one range of rows, tile by tile: the block rescans its tile's
+// keep flags (exclusive, from the tile offset), gathers each kept row of the
+// range into the sampled page, records its global id and its reweighted
+// pair, and folds the maxima of |g'| and |h'|.
+template <int kSrc>
+__global__ void __launch_bounds__(256)
+    k_compact_tiles(SampleSrc src, int64_t n, double lambda, SampleState *__restrict__ st,
+                    const uint8_t *__restrict__ keep, const int32_t *__restrict__ tile_off,
+                    int64_t tile0, int64_t row_lo, int64_t row_hi, const uint4 *__restrict__ words,
+                    int32_t row_q4, uint4 *__restrict__ out_page, int32_t *__restrict__ sel,
+                    double2 *__restrict__ gw)
+{
+    __shared__ int32_t lds4[4];
+    __shared__ unsigned long long red4[4];
+    const int64_t tile = tile0 + blockIdx.x;
+    const int64_t base = tile * kCompactTile + (int64_t)threadIdx.x * 16;
+    uint32_t bits = 0;
+    if (base + 16 <= n) {
+        uint4 v = *(const uint4 *)(keep + base);
+        uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int k = 0; k < 16; ++k) bits |= ((wv[k >> 2] >> (8 * (k & 3))) & 1u) << k;
+    } else {
+        for (int k = 0; k < 16; ++k)
+            if (base + k < n && keep[base + k]) bits |= 1u << k;
+    }
+    // exclusive scan of the per-thread counts across the block
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    const int32_t cnt = __popc(bits);
+    int32_t x = cnt;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        int32_t y = __shfl_up(x, d, 64);
+        if (lane >= d) x += y;
+    }
+    if (lane == 63) lds4[wid] = x;
+    __syncthreads();
+    int32_t run = tile_off[tile] + x - cnt;
+    for (int w = 0; w < wid; ++w) run += lds4[w];
+    const unsigned long long T = (unsigned long long)st->T;
+    const int32_t e = st->e_key;
+    unsigned long long mg = 0, mh = 0;
+    while (bits) {
+        const int k = __ffs(bits) - 1;
+        bits &= bits - 1;
+        const int64_t i = base + k;
+        const int32_t pos = run++;
+        if (i < row_lo || i >= row_hi) continue;
+        const uint4 *src_row = words + (i - row_lo) * row_q4;
+        uint4 *dst = out_page + (int64_t)pos * row_q4;
+        for (int32_t t = 0; t < row_q4; ++t) dst[t] = src_row[t];
+        sel[pos] = (int32_t)i;
+        double g, h;
+        row_gh<kSrc>(src, i, &g, &h);
+        unsigned long long a = (unsigned long long)(long long)rint(ldexp(mvs_r(g, h, lambda), e));
+        double w = a >= T ? 1.0 : (double)(long long)T / (double)(long long)a;
+        double2 v = make_double2(g * w, h * w);
+        gw[pos] = v;
+        unsigned long long bg = __double_as_longlong(fabs(v.x)), bh = __double_as_longlong(fabs(v.y));
+        mg = bg > mg ? bg : mg;
+        mh = bh > mh ? bh : mh;
+    }
+    mg = block_max_u64(mg, red4);
+    mh = block_max_u64(mh, red4);
+    if (threadIdx.x == 0) {
+        if (mg) atomicMax(&st->gmax[blockIdx.x % kSpread], mg);
+        if (mh) atomicMax(&st->hmax[blockIdx.x % kSpread], mh);
+    }
+}
+
+__global__ void __launch_bounds__(256) k_gradients_rmax(int32_t loss, const float *__restrict__ margin,
+                                                        const float *__restrict__ label, int64_t n,
+                                                        float2 *__restrict__ gpair, double lambda,
+                                                        SampleState *__restrict__ st)
+{
+    __shared__ unsigned long long lds4[4];
+    unsigned long long b = 0;
+    bool bad = false;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        double g, h;
+        gradient_pair(loss, margin[i], label[i], &g, &h);
+        float2 p = make_float2((float)g, (float)h);
+        gpair[i] = p;
+        double r = mvs_r((double)p.x, (double)p.y, lambda);
+        bad |= (r != r || r > 1.7e308);
+        unsigned long long rb = __double_as_longlong(r);
+        b = rb > b ? rb : b;
+    }
+    if (bad) atomicOr(&st->bad, 1u);
+    b = block_max_u64(b, lds4);
+    if (threadIdx.x == 0 && b) atomicMax(&st->rmax[blockIdx.x % kSpread], b);
 }
 
 // ------------------------------------------------------------ fixed point
@@ -423,8 +492,8 @@ __global__ void __launch_bounds__(256) k_fx_max(const double2 *__restrict__ gw, 
     bg = block_max_u64(bg, lds4);
     bh = block_max_u64(bh, lds4);
     if (threadIdx.x == 0) {
-        if (bg) atomicMax(&st->gmax_bits, bg);
-        if (bh) atomicMax(&st->hmax_bits, bh);
+        if (bg) atomicMax(&st->gmax[blockIdx.x % kSpread], bg);
+        if (bh) atomicMax(&st->hmax[blockIdx.x % kSpread], bh);
     }
 }
 
@@ -436,8 +505,8 @@ __global__ void __launch_bounds__(256) k_fx_convert(const double2 *__restrict__ 
 {
     __shared__ unsigned long long lds4[4];
     int Eg, Eh;
-    frexp(__longlong_as_double(st->gmax_bits), &Eg);
-    frexp(__longlong_as_double(st->hmax_bits), &Eh);
+    frexp(__longlong_as_double(fold_max(st->gmax)), &Eg);
+    frexp(__longlong_as_double(fold_max(st->hmax)), &Eh);
     const int32_t eg = 62 - Eg - log2R, eh = 62 - Eh - log2R;
     unsigned long long sg = 0, sh = 0;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < R;
@@ -451,8 +520,8 @@ __global__ void __launch_bounds__(256) k_fx_convert(const double2 *__restrict__ 
     sg = block_sum_u64(sg, lds4);
     sh = block_sum_u64(sh, lds4);
     if (threadIdx.x == 0) {
-        if (sg) atomicAdd(&st->root_g, sg);
-        if (sh) atomicAdd(&st->root_h, sh);
+        if (sg) atomicAdd(&st->root_g[blockIdx.x % kSpread], sg);
+        if (sh) atomicAdd(&st->root_h[blockIdx.x % kSpread], sh);
         if (blockIdx.x == 0) {
             st->e_g = eg;
             st->e_h = eh;
@@ -482,13 +551,15 @@ static int32_t log2_ceil(int64_t v) { return v <= 1 ? 0 : ceil_log2_u64((uint64_
 
 // ------------------------------------------------------------ drivers
 gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
-                         double lambda, int64_t K, SampleState *st, SampleState *host_st)
+                         double lambda, int64_t K, SampleState *st, SampleState *host_st, bool rmax_done)
 {
     int32_t l2 = log2_ceil(n);
     unsigned long long *hist = nullptr;
     GBT_TRY(scratch_t(c, kScrMisc, 2 * kDigitBuckets, &hist));
     if (n > 0) {
-        if (kind == kSrcGpair)
+        if (rmax_done)
+            ;
+        else if (kind == kSrcGpair)
             k_mvs_rmax<kSrcGpair><<<rblocks(n), 256, 0, c->stream>>>(src, n, lambda, st);
         else
             k_mvs_rmax<kSrcMargin><<<rblocks(n), 256, 0, c->stream>>>(src, n, lambda, st);
@@ -503,11 +574,13 @@ gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64
     GBT_LAUNCHED();
     k_zero_u64<<<blocks(2 * kDigitBuckets), 256, 0, c->stream>>>(hist, 2 * kDigitBuckets);
     GBT_LAUNCHED();
-    GBT_HIP(hipMemcpyAsync(host_st, st, sizeof(SampleState), hipMemcpyDeviceToHost, c->stream));
-    GBT_HIP(hipStreamSynchronize(c->stream));
-    if (host_st->bad & 1u) return set_error(GBT_E_INVALID, "non-finite gradient in sampling");
+    // Every key is at most 2^(62 - ceil(log2 n)), so the descent needs at
+    // most ceil((63 - ceil(log2 n)) / 11) levels; levels past the answer (or
+    // past the closed form) return at once.
+    (void)host_st;
+    const int levels = std::max(1, (63 - l2 + kDigitBits - 1) / kDigitBits);
     unsigned grid = (unsigned)std::min<int64_t>(std::max<int64_t>(blocks(n), 1), 2 * kCUs);
-    for (int lev = 0; lev < host_st->levels; ++lev) {
+    for (int lev = 0; lev < levels; ++lev) {
         if (kind == kSrcGpair)
             k_mvs_radix_hist<kSrcGpair><<<grid, 256, 0, c->stream>>>(src, keys, n, lambda, l2, st, hist,
                                                                      hist + kDigitBuckets);
@@ -536,24 +609,6 @@ gbt_status mvs_select(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t 
     return GBT_OK;
 }
 
-gbt_status mvs_compact(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
-                       double lambda, const SampleState *st, const uint8_t *keep, const int32_t *pos,
-                       const uint32_t *page, int32_t row_words, int64_t out_base, uint32_t *out_page,
-                       int32_t *sel, int64_t sel_offset, double *gw)
-{
-    if (n == 0) return GBT_OK;
-    if (kind == kSrcGpair)
-        k_compact<kSrcGpair><<<blocks(n), 256, 0, c->stream>>>(
-            src, keys, n, lambda, st, keep, pos, (const uint4 *)page, row_words / 4, out_base,
-            (uint4 *)out_page, sel, sel_offset, (double2 *)gw);
-    else
-        k_compact<kSrcMargin><<<blocks(n), 256, 0, c->stream>>>(
-            src, keys, n, lambda, st, keep, pos, (const uint4 *)page, row_words / 4, out_base,
-            (uint4 *)out_page, sel, sel_offset, (double2 *)gw);
-    GBT_LAUNCHED();
-    return GBT_OK;
-}
-
 gbt_status gw_all(gbt_ctx *c, const float *gpair, int64_t n, double *gw)
 {
     if (n == 0) return GBT_OK;
@@ -562,15 +617,51 @@ gbt_status gw_all(gbt_ctx *c, const float *gpair, int64_t n, double *gw)
     return GBT_OK;
 }
 
-gbt_status fixed_point(gbt_ctx *c, const double *gw, int64_t R, SampleState *st, int64_t *q)
+gbt_status gradients_rmax(gbt_ctx *c, int32_t loss, const float *margin, const float *label, int64_t n,
+                          float *gpair, double lambda, SampleState *st)
+{
+    if (n == 0) return GBT_OK;
+    k_gradients_rmax<<<rblocks(n), 256, 0, c->stream>>>(loss, margin, label, n, (float2 *)gpair, lambda, st);
+    GBT_LAUNCHED();
+    return GBT_OK;
+}
+
+gbt_status keep_tile_offsets(gbt_ctx *c, const uint8_t *keep, int64_t n, int32_t *tile_off)
+{
+    return scan_tiles_u8(c, keep, n, tile_off);
+}
+
+gbt_status mvs_compact_tiles(gbt_ctx *c, const SampleSrc &src, int kind, int64_t n, double lambda,
+                             SampleState *st, const uint8_t *keep, const int32_t *tile_off,
+                             int64_t row_lo, int64_t row_hi, const uint32_t *words, int32_t row_words,
+                             uint32_t *out_page, int32_t *sel, double *gw)
+{
+    if (row_hi <= row_lo) return GBT_OK;
+    const int64_t t0 = row_lo / kCompactTile, t1 = (row_hi - 1) / kCompactTile + 1;
+    const unsigned grid = (unsigned)(t1 - t0);
+    if (kind == kSrcGpair)
+        k_compact_tiles<kSrcGpair><<<grid, 256, 0, c->stream>>>(
+            src, n, lambda, st, keep, tile_off, t0, row_lo, row_hi, (const uint4 *)words, row_words / 4,
+            (uint4 *)out_page, sel, (double2 *)gw);
+    else
+        k_compact_tiles<kSrcMargin><<<grid, 256, 0, c->stream>>>(
+            src, n, lambda, st, keep, tile_off, t0, row_lo, row_hi, (const uint4 *)words, row_words / 4,
+            (uint4 *)out_page, sel, (double2 *)gw);
+    GBT_LAUNCHED();
+    return GBT_OK;
+}
+
+gbt_status fixed_point(gbt_ctx *c, const double *gw, int64_t R, SampleState *st, int64_t *q, bool fx_max_done)
 {
     if (R == 0) {
         k_fx_convert<<<1, 256, 0, c->stream>>>((const double2 *)gw, 0, 0, st, (longlong2 *)q);
         GBT_LAUNCHED();
         return GBT_OK;
     }
-    k_fx_max<<<rblocks(R), 256, 0, c->stream>>>((const double2 *)gw, R, st);
-    GBT_LAUNCHED();
+    if (!fx_max_done) {
+        k_fx_max<<<rblocks(R), 256, 0, c->stream>>>((const double2 *)gw, R, st);
+        GBT_LAUNCHED();
+    }
     k_fx_convert<<<rblocks(R), 256, 0, c->stream>>>((const double2 *)gw, R, log2_ceil(R), st,
                                                    (longlong2 *)q);
     GBT_LAUNCHED();

@@ -23,17 +23,24 @@ struct SampleSrc {
     int32_t pad0;
 };
 
+// Reductions over all rows land in kSpread copies (block b uses copy
+// b % kSpread) so that same-address atomics do not serialize; readers fold
+// the copies.
+constexpr int kSpread = 16;
+
 // Device-side state of one sampling + fixed-point pass.
 struct SampleState {
-    unsigned long long rmax_bits;  // max r (double bits; r >= 0)
-    unsigned long long amax;       // max key
-    unsigned long long asum;       // sum of keys (< 2^62)
+    unsigned long long rmax[kSpread];    // max r (double bits; r >= 0)
+    unsigned long long amax[kSpread];    // max key
+    unsigned long long asum[kSpread];    // sum of keys (< 2^62 in total)
+    unsigned long long gmax[kSpread];    // max |g'| (double bits)
+    unsigned long long hmax[kSpread];    // max |h'| (double bits)
+    unsigned long long root_g[kSpread];  // fixed-point sums of all training rows
+    unsigned long long root_h[kSpread];
     unsigned long long C_above;    // radix descent: #keys >= upper end of the range
     unsigned long long F_below;    // radix descent: sum of keys below the range
     long long lo;                  // radix descent: range start
     long long T;                   // the threshold T*
-    unsigned long long gmax_bits, hmax_bits;
-    unsigned long long root_g, root_h;  // fixed-point sums of all training rows
     int32_t e_key;
     int32_t e_g, e_h;
     int32_t shift;
@@ -43,18 +50,44 @@ struct SampleState {
     unsigned int bad;
 };
 
+__host__ __device__ inline unsigned long long fold_max(const unsigned long long *a)
+{
+    unsigned long long m = 0;
+    for (int i = 0; i < kSpread; ++i) m = a[i] > m ? a[i] : m;
+    return m;
+}
+
+__host__ __device__ inline unsigned long long fold_sum(const unsigned long long *a)
+{
+    unsigned long long m = 0;
+    for (int i = 0; i < kSpread; ++i) m += a[i];
+    return m;
+}
+
 gbt_status state_init(gbt_ctx *c, SampleState *st);
 // keys may be NULL (recomputed on every pass).  Leaves T* in st (device).
 gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
-                         double lambda, int64_t K, SampleState *st, SampleState *host_st);
+                         double lambda, int64_t K, SampleState *st, SampleState *host_st,
+                         bool rmax_done = false);
 gbt_status mvs_select(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
                       double lambda, const SampleState *st, uint64_t seed, uint64_t iteration,
                       int64_t row_offset, uint8_t *keep);
-gbt_status mvs_compact(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
-                       double lambda, const SampleState *st, const uint8_t *keep, const int32_t *pos,
-                       const uint32_t *page, int32_t row_words, int64_t out_base, uint32_t *out_page,
-                       int32_t *sel, int64_t sel_offset, double *gw);
 gbt_status gw_all(gbt_ctx *c, const float *gpair, int64_t n, double *gw);
-gbt_status fixed_point(gbt_ctx *c, const double *gw, int64_t R, SampleState *st, int64_t *q);
+// fx_max_done: the maxima of |g'| and |h'| are already in st (fused upstream)
+gbt_status fixed_point(gbt_ctx *c, const double *gw, int64_t R, SampleState *st, int64_t *q,
+                       bool fx_max_done = false);
+// Gradients of all rows and, fused, the maximum of r = sqrt(g^2 + lambda h^2).
+gbt_status gradients_rmax(gbt_ctx *c, int32_t loss, const float *margin, const float *label, int64_t n,
+                          float *gpair, double lambda, SampleState *st);
+// Exclusive per-tile offsets (tiles of kCompactTile flags) and the total.
+constexpr int kCompactTile = 4096;
+gbt_status keep_tile_offsets(gbt_ctx *c, const uint8_t *keep, int64_t n, int32_t *tile_off);
+// Compaction of the kept rows among global rows [row_lo, row_hi) whose page
+// words start at `words`; positions come from the tile offsets; also folds
+// the maxima of |g'| and |h'| into st.
+gbt_status mvs_compact_tiles(gbt_ctx *c, const SampleSrc &src, int kind, int64_t n, double lambda,
+                             SampleState *st, const uint8_t *keep, const int32_t *tile_off,
+                             int64_t row_lo, int64_t row_hi, const uint32_t *words, int32_t row_words,
+                             uint32_t *out_page, int32_t *sel, double *gw);
 
 }  // namespace gbt

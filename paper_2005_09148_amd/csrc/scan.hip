@@ -125,6 +125,32 @@ static gbt_status scan_impl(gbt_ctx *c, const T *in, int64_t n, int32_t *out)
     return GBT_OK;
 }
 
+gbt_status scan_tiles_u8(gbt_ctx *c, const uint8_t *in, int64_t n, int32_t *tile_off)
+{
+    if (n < 0 || n >= ((int64_t)1 << 31) - 1)
+        return set_error(GBT_E_UNSUPPORTED, "scan of %lld items (limit 2^31-2)", (long long)n);
+    int64_t nb = (n + kScanTile - 1) / kScanTile;
+    if (nb > 0) {
+        k_scan_reduce<uint8_t><<<(unsigned)nb, kScanThreads, 0, c->stream>>>(in, n, tile_off);
+        GBT_LAUNCHED();
+    }
+    k_scan_spine<<<1, 1024, 0, c->stream>>>(tile_off, nb, tile_off + nb);
+    GBT_LAUNCHED();
+    return GBT_OK;
+}
+
+gbt_status scan_u8_from_tiles(gbt_ctx *c, const uint8_t *in, int64_t n, int32_t *tile_cnt, int32_t *out)
+{
+    int64_t nb = (n + kScanTile - 1) / kScanTile;
+    k_scan_spine<<<1, 1024, 0, c->stream>>>(tile_cnt, nb, out + n);
+    GBT_LAUNCHED();
+    if (nb > 0) {
+        k_scan_down<uint8_t><<<(unsigned)nb, kScanThreads, 0, c->stream>>>(in, n, tile_cnt, out);
+        GBT_LAUNCHED();
+    }
+    return GBT_OK;
+}
+
 gbt_status scan_u8(gbt_ctx *c, const uint8_t *in, int64_t n, int32_t *out)
 {
     return scan_impl<uint8_t>(c, in, n, out);

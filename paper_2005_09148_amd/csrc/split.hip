@@ -19,7 +19,7 @@
 namespace gbt {
 
 constexpr int kEvalThreads = 256;
-constexpr int kFeatPerBlock = 16;
+constexpr int kFeatPerBlock = 4;
 
 struct Cand {
     double gain;
@@ -144,9 +144,11 @@ __device__ Cand eval_feature(const longlong2 *__restrict__ hj, int32_t B, long l
 
 __global__ void __launch_bounds__(kEvalThreads)
     k_eval(const longlong2 *__restrict__ hist, int64_t total_bins, const EvalNode *__restrict__ nodes,
-           const int32_t *__restrict__ bin_ptr, int32_t m, EvalParams ep, EvalCand *__restrict__ out)
+           const int32_t *__restrict__ n_nodes_d, const int32_t *__restrict__ bin_ptr, int32_t m,
+           EvalParams ep, EvalCand *__restrict__ out)
 {
     __shared__ EvalCand wbest[kEvalThreads / 64];
+    if (n_nodes_d && (int32_t)blockIdx.y >= *n_nodes_d) return;
     const EvalNode nd = nodes[blockIdx.y];
     const int wid = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const longlong2 *h = hist + (int64_t)nd.slot * total_bins;
@@ -187,12 +189,16 @@ __global__ void __launch_bounds__(kEvalThreads)
 }
 
 // Reduce the per-feature-block candidates of each node into a gbt_split.
+// With `decide` given, a node whose best valid gain is > 0 is also marked
+// as split in the tree driver's node table (depth < max_depth is the
+// caller's).
 __global__ void k_eval_reduce(const EvalCand *__restrict__ cand, int32_t n_fblocks,
                               const EvalNode *__restrict__ nodes, int32_t n_nodes,
-                              gbt_split *__restrict__ out)
+                              const int32_t *__restrict__ n_nodes_d, gbt_split *__restrict__ out,
+                              DevNode *__restrict__ decide)
 {
     int32_t k = blockIdx.x * blockDim.x + threadIdx.x;
-    if (k >= n_nodes) return;
+    if (k >= n_nodes || (n_nodes_d && k >= *n_nodes_d)) return;
     EvalCand b;
     b.valid = 0;
     for (int32_t f = 0; f < n_fblocks; ++f) {
@@ -211,44 +217,40 @@ __global__ void k_eval_reduce(const EvalCand *__restrict__ cand, int32_t n_fbloc
     s.right_g = b.valid ? nodes[k].sum_g - b.lg : 0;
     s.right_h = b.valid ? nodes[k].sum_h - b.lh : 0;
     out[k] = s;
+    if (decide && s.valid && s.gain > 0.0) {
+        DevNode &d = decide[nodes[k].heap];
+        d.split = 1;
+        d.feature = s.feature;
+        d.split_bin = s.split_bin;
+        d.default_left = s.default_left;
+        d.gain = s.gain;
+        d.left_g = s.left_g;
+        d.left_h = s.left_h;
+        d.right_g = s.right_g;
+        d.right_h = s.right_h;
+    }
 }
 
 gbt_status eval_impl(gbt_ctx *c, const gbt_matrix *mx, const int64_t *hist, const EvalNode *nodes_d,
-                     int32_t n_nodes, const EvalParams &ep, gbt_split *out_d)
+                     int32_t n_nodes, const EvalParams &ep, gbt_split *out_d, const int32_t *n_nodes_d,
+                     DevNode *decide)
 {
     if (n_nodes == 0) return GBT_OK;
     int32_t nfb = (mx->m + kFeatPerBlock - 1) / kFeatPerBlock;
     EvalCand *cand;
     GBT_TRY(scratch_t(c, kScrEval, (size_t)n_nodes * nfb, &cand));
     dim3 grid((unsigned)nfb, (unsigned)n_nodes);
-    k_eval<<<grid, kEvalThreads, 0, c->stream>>>((const longlong2 *)hist, mx->total_bins, nodes_d,
+    k_eval<<<grid, kEvalThreads, 0, c->stream>>>((const longlong2 *)hist, mx->total_bins, nodes_d, n_nodes_d,
                                                  mx->bin_ptr_d, mx->m, ep, cand);
     GBT_LAUNCHED();
-    k_eval_reduce<<<(n_nodes + 127) / 128, 128, 0, c->stream>>>(cand, nfb, nodes_d, n_nodes, out_d);
+    k_eval_reduce<<<(n_nodes + 127) / 128, 128, 0, c->stream>>>(cand, nfb, nodes_d, n_nodes, n_nodes_d, out_d,
+                                                                decide);
     GBT_LAUNCHED();
     return GBT_OK;
 }
 
 // ------------------------------------------------------------ partition
 // node of slot i: slot_node[i] when given, else position[rows[i]]
-__global__ void k_part_flags(const int32_t *__restrict__ rows, int64_t n, const uint32_t *__restrict__ page,
-                             Geo geo, const int32_t *__restrict__ position,
-                             const int32_t *__restrict__ slot_node, const DevNode *__restrict__ nodes,
-                             uint8_t *__restrict__ flags)
-{
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n) return;
-    int32_t r = rows[i];
-    int32_t nid = slot_node ? slot_node[i] : position[r];
-    uint8_t f = 0;
-    if (nid >= 0 && nodes[nid].split) {
-        const DevNode &nd = nodes[nid];
-        int32_t b = row_feature_bin(page + (int64_t)r * geo.row_words, geo, nd.feature);
-        f = (b < 0) ? (uint8_t)(nd.default_left != 0) : (uint8_t)(b < nd.split_bin);
-    }
-    flags[i] = f;
-}
-
 __global__ void k_part_scatter(const int32_t *__restrict__ rows, int64_t n,
                                const uint8_t *__restrict__ flags, const int32_t *__restrict__ P,
                                int32_t *__restrict__ position, const int32_t *__restrict__ slot_node,
@@ -279,6 +281,37 @@ __global__ void k_part_scatter(const int32_t *__restrict__ rows, int64_t n,
     position[r] = child;
 }
 
+// Left flags of 16 consecutive slots per thread and the count of each tile
+// of 4096 slots (the first pass of the scan).
+__global__ void __launch_bounds__(256)
+    k_part_flags_tiles(const int32_t *__restrict__ rows, int64_t n, const uint32_t *__restrict__ page, Geo geo,
+                       const int32_t *__restrict__ position, const int32_t *__restrict__ slot_node,
+                       const DevNode *__restrict__ nodes, uint8_t *__restrict__ flags,
+                       int32_t *__restrict__ tile_cnt)
+{
+    __shared__ int32_t red[4];
+    const int64_t base = (int64_t)blockIdx.x * 4096 + (int64_t)threadIdx.x * 16;
+    int32_t cnt = 0;
+    for (int k = 0; k < 16; ++k) {
+        const int64_t i = base + k;
+        if (i >= n) break;
+        const int32_t r = rows[i];
+        const int32_t nid = slot_node ? slot_node[i] : position[r];
+        uint8_t f = 0;
+        if (nid >= 0 && nodes[nid].split) {
+            const DevNode &nd = nodes[nid];
+            const int32_t b = row_feature_bin(page + (int64_t)r * geo.row_words, geo, nd.feature);
+            f = (b < 0) ? (uint8_t)(nd.default_left != 0) : (uint8_t)(b < nd.split_bin);
+        }
+        flags[i] = f;
+        cnt += f;
+    }
+    for (int d = 32; d > 0; d >>= 1) cnt += __shfl_xor(cnt, d, 64);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = cnt;
+    __syncthreads();
+    if (threadIdx.x == 0) tile_cnt[blockIdx.x] = red[0] + red[1] + red[2] + red[3];
+}
+
 gbt_status partition_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int32_t *rows,
                           int64_t n, int32_t *position, const int32_t *slot_node,
                           const DevNode *nodes, int32_t *rows_out, int32_t **P_out)
@@ -293,9 +326,13 @@ gbt_status partition_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page
     GBT_TRY(scratch_t(c, kScrPartPos, (size_t)n + 1, &P));
     Geo geo = geo_of(mx);
     unsigned grid = (unsigned)((n + 255) / 256);
-    k_part_flags<<<grid, 256, 0, c->stream>>>(rows, n, page, geo, position, slot_node, nodes, flags);
+    const int64_t tiles = (n + 4095) / 4096;
+    int32_t *tile_off;
+    GBT_TRY(scratch_t(c, kScrScan, (size_t)tiles + 1, &tile_off));
+    k_part_flags_tiles<<<(unsigned)tiles, 256, 0, c->stream>>>(rows, n, page, geo, position, slot_node, nodes,
+                                                               flags, tile_off);
     GBT_LAUNCHED();
-    GBT_TRY(scan_u8(c, flags, n, P));
+    GBT_TRY(scan_u8_from_tiles(c, flags, n, tile_off, P));
     k_part_scatter<<<grid, 256, 0, c->stream>>>(rows, n, flags, P, position, slot_node, nodes, rows_out);
     GBT_LAUNCHED();
     *P_out = P;

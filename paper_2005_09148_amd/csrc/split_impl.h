@@ -29,8 +29,11 @@ struct EvalCand {
     int32_t valid;
 };
 
+// n_nodes sizes the grid; when n_nodes_d is given the live count is read
+// from device memory (at most n_nodes).
 gbt_status eval_impl(gbt_ctx *c, const gbt_matrix *mx, const int64_t *hist, const EvalNode *nodes_d,
-                     int32_t n_nodes, const EvalParams &ep, gbt_split *out_d);
+                     int32_t n_nodes, const EvalParams &ep, gbt_split *out_d,
+                     const int32_t *n_nodes_d = nullptr, DevNode *decide = nullptr);
 // Stable partition of rows[0, n) by each slot's node (slot_node[i], or
 // position[rows[i]] when slot_node is NULL).  rows_out receives the new
 // order, position[row] the child id.  *P receives the exclusive scan of the

@@ -8,6 +8,7 @@
 #include <functional>
 
 #include "sample_impl.h"
+#include "hist_impl.h"
 #include "split_impl.h"
 
 namespace gbt {
@@ -133,19 +134,24 @@ struct SampleOut {
 };
 
 // Alg. 7: g' <- Sample(g); AllocateOnGPU(sampled_page); Compact each page.
+// st_ready: the caller has initialized st and folded the maximum of r into
+// it while computing the gradients.
 gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, const float *margin,
                       const float *label, const gbt_sample_params &sp, Buffers &bufs, SampleOut *o,
-                      double *h2d_bytes)
+                      double *h2d_bytes, SampleState *st_ready = nullptr)
 {
     const int64_t n = mx->n_rows;
     GBT_CHECK(sp.f > 0.0 && sp.f <= 1.0, "sampling fraction %g outside (0, 1]", sp.f);
     GBT_CHECK(gpair || (margin && label), "sampling needs gradient pairs or margins and labels");
-    SampleState *st;
-    GBT_TRY(bufs.get(kScrState, sizeof(SampleState), (void **)&st));
+    SampleState *st = st_ready;
+    if (!st) {
+        GBT_TRY(bufs.get(kScrState, sizeof(SampleState), (void **)&st));
+        GBT_TRY(state_init(c, st));
+    }
     o->st = st;
-    GBT_TRY(state_init(c, st));
     SampleSrc src{(const float2 *)gpair, margin, label, sp.loss, 0};
     const int kind = gpair ? kSrcGpair : kSrcMargin;
+    bool fx_max_done = false;
 
     if (sp.f >= 1.0 && all_device_single(mx) && gpair) {
         // no sampling: the data page trains as it is
@@ -155,22 +161,21 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
         GBT_TRY(bufs.get(kScrGw, (size_t)std::max<int64_t>(n, 1) * 16, (void **)&o->gw));
         GBT_TRY(gw_all(c, gpair, n, o->gw));
     } else {
-        int64_t *keys = nullptr;
         uint8_t *keep;
-        int32_t *pos;
-        GBT_TRY(bufs.get(kScrFlags, (size_t)std::max<int64_t>(n, 1), (void **)&keep));
-        GBT_TRY(bufs.get(kScrPos, (size_t)(n + 1) * 4, (void **)&pos));
+        int32_t *tile_off;
+        const int64_t ntiles = (n + kCompactTile - 1) / kCompactTile;
+        GBT_TRY(bufs.get(kScrFlags, (size_t)std::max<int64_t>(n, 16) + 16, (void **)&keep));
+        GBT_TRY(bufs.get(kScrPos, (size_t)(ntiles + 1) * 4, (void **)&tile_off));
         SampleState hst;
         if (sp.f < 1.0) {
             o->K = std::max<int64_t>(1, (int64_t)std::nearbyint(sp.f * (double)n));
-            if (kind == kSrcGpair) GBT_TRY(bufs.get(kScrKeys, (size_t)std::max<int64_t>(n, 1) * 8, (void **)&keys));
-            GBT_TRY(mvs_threshold(c, src, kind, keys, n, sp.mvs_lambda, o->K, st, &hst));
+            GBT_TRY(mvs_threshold(c, src, kind, nullptr, n, sp.mvs_lambda, o->K, st, &hst, st_ready != nullptr));
         }
         // with f = 1 the state keeps T = 0: every row is kept with weight 1
-        GBT_TRY(mvs_select(c, src, kind, keys, n, sp.mvs_lambda, st, sp.seed, sp.iteration, 0, keep));
-        GBT_TRY(scan_u8(c, keep, n, pos));
+        GBT_TRY(mvs_select(c, src, kind, nullptr, n, sp.mvs_lambda, st, sp.seed, sp.iteration, 0, keep));
+        GBT_TRY(keep_tile_offsets(c, keep, n, tile_off));
         int32_t R32 = 0;
-        GBT_HIP(hipMemcpyAsync(&R32, pos + n, 4, hipMemcpyDeviceToHost, c->stream));
+        GBT_HIP(hipMemcpyAsync(&R32, tile_off + ntiles, 4, hipMemcpyDeviceToHost, c->stream));
         GBT_HIP(hipStreamSynchronize(c->stream));
         o->R = R32;
         size_t rb = (size_t)mx->row_words * 4;
@@ -182,18 +187,14 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
         GBT_TRY(for_each_chunk(
             c, mx,
             [&](const uint32_t *words, int64_t row0, int64_t rows) -> gbt_status {
-                SampleSrc s2 = src;
-                if (s2.gpair) s2.gpair += row0;
-                if (s2.margin) s2.margin += row0;
-                if (s2.label) s2.label += row0;
-                return mvs_compact(c, s2, kind, keys ? keys + row0 : nullptr, rows, sp.mvs_lambda, st,
-                                   keep + row0, pos + row0, words, mx->row_words, 0, spage, o->sel, row0,
-                                   o->gw);
+                return mvs_compact_tiles(c, src, kind, n, sp.mvs_lambda, st, keep, tile_off, row0, row0 + rows,
+                                         words, mx->row_words, spage, o->sel, o->gw);
             },
             h2d_bytes));
+        fx_max_done = true;
     }
     GBT_TRY(bufs.get(kScrQ, (size_t)std::max<int64_t>(o->R, 1) * 16, (void **)&o->q));
-    GBT_TRY(fixed_point(c, o->gw, o->R, st, o->q));
+    GBT_TRY(fixed_point(c, o->gw, o->R, st, o->q, fx_max_done));
     SampleState hst;
     GBT_HIP(hipMemcpyAsync(&hst, st, sizeof(SampleState), hipMemcpyDeviceToHost, c->stream));
     GBT_HIP(hipStreamSynchronize(c->stream));
@@ -202,15 +203,15 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
     o->e_key = hst.e_key;
     o->e_g = hst.e_g;
     o->e_h = hst.e_h;
-    o->root_g = (long long)hst.root_g;
-    o->root_h = (long long)hst.root_h;
+    o->root_g = (long long)fold_sum(hst.root_g);
+    o->root_h = (long long)fold_sum(hst.root_h);
     return GBT_OK;
 }
 
 // ------------------------------------------------------------ tree kernels
 __global__ void k_zero_counter(unsigned long long *p)
 {
-    if (threadIdx.x == 0) *p = 0ull;
+    if (threadIdx.x < kUpdCounters) p[threadIdx.x] = 0ull;
 }
 
 __global__ void k_tree_init(DevNode *__restrict__ nodes, int32_t n_nodes, long long rg, long long rh,
@@ -240,49 +241,108 @@ __global__ void k_rows_init(int32_t *__restrict__ rows, int32_t *__restrict__ po
     position[i] = 0;
 }
 
-// A node splits iff its best valid gain is > 0 (depth < max_depth is the
-// caller's); the children inherit the split's left/right sums.
-__global__ void k_decide(DevNode *__restrict__ nodes, const EvalNode *__restrict__ ev,
-                         const gbt_split *__restrict__ sp, int32_t n)
+// Exclusive scan across a 1024-thread block; *total receives the sum.
+__device__ inline int32_t scan1024(int32_t v, int32_t *lds16, int32_t *total)
 {
-    int32_t k = blockIdx.x * blockDim.x + threadIdx.x;
-    if (k >= n) return;
-    const gbt_split s = sp[k];
-    DevNode &d = nodes[ev[k].heap];
-    if (s.valid && s.gain > 0.0) {
-        d.split = 1;
-        d.feature = s.feature;
-        d.split_bin = s.split_bin;
-        d.default_left = s.default_left;
-        d.gain = s.gain;
-        d.left_g = s.left_g;
-        d.left_h = s.left_h;
-        d.right_g = s.right_g;
-        d.right_h = s.right_h;
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    int32_t x = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        int32_t y = __shfl_up(x, d, 64);
+        if (lane >= d) x += y;
     }
+    __syncthreads();
+    if (lane == 63) lds16[wid] = x;
+    __syncthreads();
+    int32_t off = 0, tot = 0;
+    for (int w = 0; w < 16; ++w) {
+        if (w < wid) off += lds16[w];
+        tot += lds16[w];
+    }
+    *total = tot;
+    return x - v + off;
 }
 
-// Child segments of every split node from the partition's left counts.
-__global__ void k_children(DevNode *__restrict__ nodes, const EvalNode *__restrict__ ev, int32_t n,
-                           const int32_t *__restrict__ P)
+// After a level's partition (one block of 1024 threads): the child segments
+// of every split node from the partition's left counts P, then, when `plan`
+// is set, the plan of the next level: the list of present children in heap
+// order with their histogram slots, and for each split parent the smaller
+// child to build (chunked into work items) with the larger one as parent
+// minus it.
+__global__ void __launch_bounds__(1024)
+    k_plan_level(const EvalNode *__restrict__ cur, const int32_t *__restrict__ n_cur_d,
+                 DevNode *__restrict__ nodes, const int32_t *__restrict__ P, int32_t plan, int64_t chunk,
+                 EvalNode *__restrict__ next, int32_t *__restrict__ n_next_d, HistWork *__restrict__ work,
+                 int32_t *__restrict__ n_work_d, HistReduce *__restrict__ red, int32_t *__restrict__ n_red_d,
+                 unsigned long long *__restrict__ stat)
 {
-    int32_t k = blockIdx.x * blockDim.x + threadIdx.x;
-    if (k >= n) return;
-    const DevNode d = nodes[ev[k].heap];
-    if (!d.split) return;
-    int64_t nl = (int64_t)P[d.end] - P[d.begin];
-    DevNode &L = nodes[d.left_child];
-    DevNode &Rn = nodes[d.right_child];
-    L.present = 1;
-    L.sum_g = d.left_g;
-    L.sum_h = d.left_h;
-    L.begin = d.begin;
-    L.end = d.begin + nl;
-    Rn.present = 1;
-    Rn.sum_g = d.right_g;
-    Rn.sum_h = d.right_h;
-    Rn.begin = d.begin + nl;
-    Rn.end = d.end;
+    __shared__ int32_t lds16[16];
+    const int32_t n_cur = *n_cur_d;
+    for (int32_t t = threadIdx.x; t < n_cur; t += 1024) {
+        const DevNode d = nodes[cur[t].heap];
+        if (!d.split) continue;
+        const int64_t nl = (int64_t)P[d.end] - P[d.begin];
+        DevNode &L = nodes[d.left_child];
+        DevNode &Rn = nodes[d.right_child];
+        L.present = 1;
+        L.sum_g = d.left_g;
+        L.sum_h = d.left_h;
+        L.begin = d.begin;
+        L.end = d.begin + nl;
+        Rn.present = 1;
+        Rn.sum_g = d.right_g;
+        Rn.sum_h = d.right_h;
+        Rn.begin = d.begin + nl;
+        Rn.end = d.end;
+    }
+    if (!plan) return;
+    __threadfence_block();
+    __syncthreads();
+    int32_t c_build = 0, c_part = 0;
+    unsigned long long rows_built = 0;
+    for (int32_t base = 0; base < n_cur; base += 1024) {
+        const int32_t t = base + (int32_t)threadIdx.x;
+        bool split = false;
+        int32_t p = 0, nchunks = 0;
+        int64_t nl = 0, nr = 0;
+        if (t < n_cur) {
+            p = cur[t].heap;
+            split = nodes[p].split != 0;
+            if (split) {
+                nl = nodes[2 * p + 1].end - nodes[2 * p + 1].begin;
+                nr = nodes[2 * p + 2].end - nodes[2 * p + 2].begin;
+                int64_t ns = nl <= nr ? nl : nr;
+                nchunks = (int32_t)(ns > 0 ? (ns + chunk - 1) / chunk : 1);
+                rows_built += (unsigned long long)ns;
+            }
+        }
+        int32_t tot_b, tot_p;
+        const int32_t kb = scan1024(split ? 1 : 0, lds16, &tot_b) + c_build;
+        const int32_t kp = scan1024(nchunks, lds16, &tot_p) + c_part;
+        if (split) {
+            const int32_t sl = 2 * kb, sr = sl + 1;  // the children of split parents, in heap order
+            const DevNode &L = nodes[2 * p + 1], &Rn = nodes[2 * p + 2];
+            next[sl] = {L.sum_g, L.sum_h, sl, 2 * p + 1};
+            next[sr] = {Rn.sum_g, Rn.sum_h, sr, 2 * p + 2};
+            const bool left_small = nl <= nr;
+            const DevNode &S = left_small ? L : Rn;
+            red[kb] = {left_small ? sl : sr, kp, nchunks, cur[t].slot, left_small ? sr : sl, 0};
+            for (int32_t j = 0; j < nchunks; ++j) {
+                int64_t b = S.begin + (int64_t)j * chunk;
+                work[kp + j] = {b, b + chunk < S.end ? b + chunk : S.end, kp + j, 0};
+            }
+        }
+        c_build += tot_b;
+        c_part += tot_p;
+    }
+    for (int d = 32; d > 0; d >>= 1) rows_built += __shfl_xor(rows_built, d, 64);
+    if ((threadIdx.x & 63) == 0 && rows_built) atomicAdd(&stat[0], rows_built);
+    if (threadIdx.x == 0) {
+        *n_next_d = 2 * c_build;
+        *n_red_d = c_build;
+        *n_work_d = c_part;
+        atomicAdd(&stat[1], (unsigned long long)c_part);
+    }
 }
 
 // Eq. 6 scaled by the learning rate, for every present node that does not
@@ -295,13 +355,18 @@ __device__ inline float leaf_of(long long Qg, long long Qh, int32_t eg, int32_t 
     return (float)(w * eta);
 }
 
+// Leaf values, and the compact form of the tree used by the row walk:
+// {feature, split_bin << 2 | default_left << 1 | splits} per node.
 __global__ void k_leaves(const DevNode *__restrict__ nodes, int32_t n_nodes, int32_t eg, int32_t eh,
-                         double lambda, double eta, float *__restrict__ leaf)
+                         double lambda, double eta, float *__restrict__ leaf, uint2 *__restrict__ compact)
 {
     int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n_nodes) return;
     const DevNode d = nodes[i];
     leaf[i] = (d.present && !d.split) ? leaf_of(d.sum_g, d.sum_h, eg, eh, lambda, eta) : 0.0f;
+    compact[i] = d.split ? make_uint2((uint32_t)d.feature, ((uint32_t)d.split_bin << 2) |
+                                                               ((d.default_left ? 1u : 0u) << 1) | 1u)
+                         : make_uint2(0u, 0u);
 }
 
 // Margin update from the final node of each training row (no sampling).
@@ -359,6 +424,57 @@ __global__ void __launch_bounds__(kWalkThreads)
         id = left ? d.left_child : d.right_child;
     }
     margin[i] = margin[i] + leaf[id];
+}
+
+// Margin update of every row by walking the tree held in LDS.  The grid is
+// a few blocks per CU; each block loads the compact tree once, then loops
+// over tiles of 256 rows staged through LDS with coalesced loads.
+constexpr int kWalkTileRows = 256;
+constexpr int kWalkLdsNodes = 4095;  // trees up to depth 11 are held in LDS
+
+__global__ void __launch_bounds__(kWalkTileRows)
+    k_margin_walk_lds(const uint32_t *__restrict__ words, int64_t rows, Geo geo,
+                      const uint2 *__restrict__ compact, const float *__restrict__ leaf, int32_t nn,
+                      float *__restrict__ margin)
+{
+    extern __shared__ uint32_t walk_lds[];
+    uint2 *tn = (uint2 *)walk_lds;
+    float *tl = (float *)(tn + nn);
+    uint32_t *rb = (uint32_t *)(tl + nn);
+    for (int32_t t = threadIdx.x; t < nn; t += kWalkTileRows) {
+        tn[t] = compact[t];
+        tl[t] = leaf[t];
+    }
+    const int32_t ps = geo.row_words + 1, q4 = geo.row_words / 4;
+    const int64_t n_tiles = (rows + kWalkTileRows - 1) / kWalkTileRows;
+    for (int64_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
+        const int64_t r0 = tile * kWalkTileRows;
+        const int32_t nr = (int32_t)min((int64_t)kWalkTileRows, rows - r0);
+        const uint4 *src = (const uint4 *)(words + r0 * geo.row_words);
+        __syncthreads();  // the previous tile's rows are consumed
+        for (int32_t t = threadIdx.x; t < nr * q4; t += kWalkTileRows) {
+            uint4 v = src[t];
+            uint32_t *d = rb + (t / q4) * ps + (t % q4) * 4;
+            d[0] = v.x;
+            d[1] = v.y;
+            d[2] = v.z;
+            d[3] = v.w;
+        }
+        __syncthreads();
+        if ((int32_t)threadIdx.x < nr) {
+            const uint32_t *row = rb + threadIdx.x * ps;
+            int32_t id = 0;
+            uint2 nd = tn[0];
+            while (nd.y & 1u) {
+                int32_t b = row_feature_bin(row, geo, (int32_t)nd.x);
+                bool left = b < 0 ? ((nd.y >> 1) & 1u) != 0 : b < (int32_t)(nd.y >> 2);
+                id = 2 * id + (left ? 1 : 2);
+                nd = tn[id];
+            }
+            const int64_t i = r0 + threadIdx.x;
+            margin[i] = margin[i] + tl[id];
+        }
+    }
 }
 
 // ------------------------------------------------------------ prediction
@@ -472,12 +588,6 @@ __global__ void __launch_bounds__(kWalkThreads)
 static size_t walk_lds_bytes(const Geo &g) { return (size_t)kWalkThreads * (g.row_words + 1) * 4; }
 
 // ------------------------------------------------------------ the iteration
-struct LevelNode {
-    int32_t heap;
-    int32_t slot;
-    int64_t begin, end;
-    long long sum_g, sum_h;
-};
 
 static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float *label, float *margin,
                                   const gbt_train_params *p, gbt_tree *tree, gbt_tree_stats *stats)
@@ -491,7 +601,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
 
     unsigned long long *upd = nullptr;
     if (stats) {
-        GBT_TRY(scratch_t(c, kScrUpd, 1, &upd));
+        GBT_TRY(scratch_t(c, kScrUpd, kUpdCounters, &upd));
         k_zero_counter<<<1, 64, 0, c->stream>>>(upd);
         GBT_LAUNCHED();
     }
@@ -499,14 +609,22 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     c->events_used = 0;
     int mark = timer_begin(c, kPhSample);
     float *gpair = nullptr;
+    SampleState *st_ready = nullptr;
     if (!host_pages) {
         GBT_TRY(scratch_t(c, kScrGpair, (size_t)std::max<int64_t>(n, 1) * 2, &gpair));
-        GBT_TRY(launch_gradients(c, p->loss, margin, label, nullptr, n, gpair));
+        if (p->f < 1.0) {
+            // the gradient pass also folds the maximum of r for the sampling keys
+            GBT_TRY(scratch_t(c, kScrState, 1, &st_ready));
+            GBT_TRY(state_init(c, st_ready));
+            GBT_TRY(gradients_rmax(c, p->loss, margin, label, n, gpair, p->mvs_lambda, st_ready));
+        } else {
+            GBT_TRY(launch_gradients(c, p->loss, margin, label, nullptr, n, gpair));
+        }
     }
     Buffers bufs{c, false, {}};
     gbt_sample_params sp{p->f, p->mvs_lambda, p->seed, p->iteration, p->loss, 0};
     SampleOut so;
-    GBT_TRY(sample_run(c, mx, gpair, margin, label, sp, bufs, &so, &h2d));
+    GBT_TRY(sample_run(c, mx, gpair, margin, label, sp, bufs, &so, &h2d, st_ready));
     timer_end(c, mark);
     const int64_t R = so.R;
     if (stats) {
@@ -515,19 +633,19 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         stats->exp_key = so.e_key;
     }
 
-    // ---- Alg. 1 on the sampled page, level by level
+    // ---- Alg. 1 on the sampled page, level by level.  Levels below the root
+    // are planned on the device: no host round trip inside the tree.
     DevNode *nodes;
     int32_t *rows, *rows_tmp, *position;
     float *leaf;
-    EvalNode *ev_d;
     gbt_split *splits_d;
     GBT_TRY(scratch_t(c, kScrNodes, (size_t)NN, &nodes));
     GBT_TRY(scratch_t(c, kScrLeaf, (size_t)NN, &leaf));
     GBT_TRY(scratch_t(c, kScrRows, (size_t)std::max<int64_t>(R, 1), &rows));
     GBT_TRY(scratch_t(c, kScrRowsTmp, (size_t)std::max<int64_t>(R, 1), &rows_tmp));
     GBT_TRY(scratch_t(c, kScrPosition, (size_t)std::max<int64_t>(R, 1), &position));
-    int32_t max_level_nodes = (int32_t)std::min<int64_t>((int64_t)1 << std::max(D - 1, 0), std::max<int64_t>(R, 1));
-    GBT_TRY(scratch_t(c, kScrEvalNodes, (size_t)max_level_nodes, &ev_d));
+    const int32_t max_level_nodes =
+        (int32_t)std::min<int64_t>((int64_t)1 << std::max(D - 1, 0), std::max<int64_t>(R, 1));
     GBT_TRY(scratch_t(c, kScrSplits, (size_t)max_level_nodes, &splits_d));
     const size_t hist_bytes = (size_t)max_level_nodes * (size_t)mx->total_bins * 16;
     int64_t *histA = nullptr, *histB = nullptr;
@@ -535,6 +653,40 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         GBT_TRY(scratch(c, kScrHistA, std::max<size_t>(hist_bytes, 16), (void **)&histA));
         GBT_TRY(scratch(c, kScrHistB, std::max<size_t>(hist_bytes, 16), (void **)&histB));
     }
+    // plan buffers: two level lists, their counts, work items, reduce items, stats
+    std::vector<HistGroup> groups;
+    if (!hist_groups(mx, &groups))
+        return set_error(GBT_E_UNSUPPORTED, "a feature has too many bins or symbol words for LDS");
+    const int32_t G = (int32_t)groups.size();
+    const int64_t chunk = std::max<int64_t>(2048, ((R / 2) * G + 2 * kCUs - 1) / (2 * kCUs));
+    const int32_t max_work = (int32_t)((R / 2) / chunk + max_level_nodes + 1);
+    auto al = [](size_t b) { return (b + 255) / 256 * 256; };
+    const size_t o_ev1 = al((size_t)max_level_nodes * sizeof(EvalNode));
+    const size_t o_cnt = o_ev1 + o_ev1;
+    const size_t o_grp = o_cnt + 256;
+    const size_t o_work = o_grp + al((size_t)G * sizeof(HistGroup));
+    const size_t o_red = o_work + al((size_t)max_work * sizeof(HistWork));
+    const size_t plan_bytes = o_red + al((size_t)max_level_nodes * sizeof(HistReduce));
+    char *plan;
+    GBT_TRY(scratch_t(c, kScrPlan, plan_bytes, &plan));
+    EvalNode *evA = (EvalNode *)plan, *evB = (EvalNode *)(plan + o_ev1);
+    int32_t *cnt = (int32_t *)(plan + o_cnt);  // [0,1] level counts, [2] works, [3] reduces
+    unsigned long long *stat = (unsigned long long *)(plan + o_cnt + 64);  // rows built, partials
+    HistGroup *groups_d = (HistGroup *)(plan + o_grp);
+    HistWork *work_d = (HistWork *)(plan + o_work);
+    HistReduce *red_d = (HistReduce *)(plan + o_red);
+    {
+        // root list, counts and the groups, in one upload
+        std::vector<char> h(o_work - 0, 0);
+        EvalNode root{so.root_g, so.root_h, 0, 0};
+        memcpy(h.data(), &root, sizeof(root));
+        int32_t c0[4] = {1, 0, 0, 0};
+        memcpy(h.data() + o_cnt, c0, sizeof(c0));
+        memcpy(h.data() + o_grp, groups.data(), groups.size() * sizeof(HistGroup));
+        GBT_HIP(hipMemcpyAsync(plan, h.data(), h.size(), hipMemcpyHostToDevice, c->stream));
+    }
+    int64_t *partials = nullptr;
+    GBT_TRY(scratch(c, kScrPartialsDev, (size_t)std::max(max_work, 1) * mx->total_bins * 16, (void **)&partials));
     k_tree_init<<<blocks(NN), 256, 0, c->stream>>>(nodes, NN, so.root_g, so.root_h, R);
     GBT_LAUNCHED();
     if (R) {
@@ -542,67 +694,43 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         GBT_LAUNCHED();
     }
     EvalParams ep{p->lambda, p->gamma, p->min_child_weight, so.e_g, so.e_h};
-    std::vector<LevelNode> cur{{0, 0, 0, R, so.root_g, so.root_h}};
+    int32_t hist_launches = 0;
     if (D > 0) {
         gbt_seg root{0, 0, 0, R};
         GBT_TRY(build_hist_impl(c, mx, so.page, so.q, nullptr, &root, 1, nullptr, 0, nullptr, histA, stats));
+        hist_launches += R > 0;
     }
-    std::vector<DevNode> hnodes;
-    for (int32_t d = 0; d < D && !cur.empty(); ++d) {
-        const int32_t nc = (int32_t)cur.size();
-        std::vector<EvalNode> ev(nc);
-        for (int32_t k = 0; k < nc; ++k) ev[k] = {cur[k].sum_g, cur[k].sum_h, cur[k].slot, cur[k].heap};
-        GBT_HIP(hipMemcpyAsync(ev_d, ev.data(), nc * sizeof(EvalNode), hipMemcpyHostToDevice, c->stream));
+    int32_t *cntA = cnt, *cntB = cnt + 1;
+    for (int32_t d = 0; d < D; ++d) {
+        const int32_t maxn = (int32_t)std::min<int64_t>((int64_t)1 << d, max_level_nodes);
         mark = timer_begin(c, kPhSplit);
-        GBT_TRY(eval_impl(c, mx, histA, ev_d, nc, ep, splits_d));
-        k_decide<<<blocks(nc), 256, 0, c->stream>>>(nodes, ev_d, splits_d, nc);
-        GBT_LAUNCHED();
+        GBT_TRY(eval_impl(c, mx, histA, evA, maxn, ep, splits_d, cntA, nodes));
         int32_t *P = nullptr;
         GBT_TRY(partition_impl(c, mx, so.page, rows, R, position, nullptr, nodes, rows_tmp, &P));
         std::swap(rows, rows_tmp);
+        const bool plan_next = d + 1 < D && R > 0;
         if (P) {
-            k_children<<<blocks(nc), 256, 0, c->stream>>>(nodes, ev_d, nc, P);
+            k_plan_level<<<1, 1024, 0, c->stream>>>(evA, cntA, nodes, P, plan_next ? 1 : 0, chunk, evB, cntB,
+                                                    work_d, cnt + 2, red_d, cnt + 3, stat);
             GBT_LAUNCHED();
         }
         timer_end(c, mark);
-        // the next level's nodes
-        const int32_t first = (1 << (d + 1)) - 1, count = 1 << (d + 1);
-        hnodes.resize(count);
-        GBT_HIP(hipMemcpyAsync(hnodes.data(), nodes + first, count * sizeof(DevNode), hipMemcpyDeviceToHost,
-                               c->stream));
-        GBT_HIP(hipStreamSynchronize(c->stream));
-        std::vector<LevelNode> next;
-        for (int32_t k = 0; k < count; ++k) {
-            const DevNode &h = hnodes[k];
-            if (!h.present) continue;
-            next.push_back({first + k, (int32_t)next.size(), h.begin, h.end, h.sum_g, h.sum_h});
-        }
-        if (d + 1 < D && !next.empty()) {
-            // build the smaller child of each pair, subtract for its sibling
-            std::vector<int32_t> slot_of(count, -1);
-            for (auto &x : next) slot_of[x.heap - first] = x.slot;
-            std::vector<gbt_seg> build;
-            std::vector<gbt_sub> sub;
-            for (auto &par : cur) {
-                int32_t l = 2 * par.heap + 1, r = l + 1;
-                int32_t sl = slot_of[l - first], sr = slot_of[r - first];
-                if (sl < 0) continue;  // not split
-                const DevNode &L = hnodes[l - first], &Rn = hnodes[r - first];
-                bool left_small = (L.end - L.begin) <= (Rn.end - Rn.begin);
-                const DevNode &S = left_small ? L : Rn;
-                int32_t ss = left_small ? sl : sr, so2 = left_small ? sr : sl;
-                build.push_back({ss, 0, S.begin, S.end});
-                sub.push_back({par.slot, ss, so2, 0});
-            }
-            GBT_TRY(build_hist_impl(c, mx, so.page, so.q, rows, build.data(), (int32_t)build.size(), sub.data(),
-                                    (int32_t)sub.size(), histA, histB, stats));
+        if (plan_next) {
+            HistLaunch hl{groups_d, G, 0, work_d, cnt + 2, max_work, red_d, cnt + 3, maxn, partials};
+            for (auto &g : groups) hl.max_groups_bins = std::max(hl.max_groups_bins, g.b1 - g.b0);
+            GBT_TRY(hist_launch_device(c, mx, so.page, so.q, rows, hl, histA, histB, upd));
+            ++hist_launches;
             std::swap(histA, histB);
+            std::swap(evA, evB);
+            std::swap(cntA, cntB);
         }
-        cur.swap(next);
     }
     // ---- leaves and the margin update of all n rows (Eq. 1)
     mark = timer_begin(c, kPhMargin);
-    k_leaves<<<blocks(NN), 256, 0, c->stream>>>(nodes, NN, so.e_g, so.e_h, p->lambda, p->eta, leaf);
+    uint2 *compact;
+    GBT_TRY(scratch_t(c, kScrCompact, (size_t)NN, &compact));
+    k_leaves<<<blocks(NN), 256, 0, c->stream>>>(nodes, NN, so.e_g, so.e_h, p->lambda, p->eta, leaf,
+                                                compact);
     GBT_LAUNCHED();
     if (so.alias) {
         if (n) {
@@ -614,7 +742,13 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         GBT_TRY(for_each_chunk(
             c, mx,
             [&](const uint32_t *words, int64_t row0, int64_t rows_n) -> gbt_status {
-                if (geo.row_words <= kWalkMaxWords)
+                const size_t lds_bytes = (size_t)NN * 12 + (size_t)kWalkTileRows * (geo.row_words + 1) * 4;
+                if (geo.row_words <= kWalkMaxWords && NN <= kWalkLdsNodes && lds_bytes <= 64 * 1024) {
+                    int64_t tiles = (rows_n + kWalkTileRows - 1) / kWalkTileRows;
+                    unsigned grid = (unsigned)std::min<int64_t>(tiles, 4 * kCUs);
+                    k_margin_walk_lds<<<grid, kWalkTileRows, lds_bytes, c->stream>>>(words, rows_n, geo, compact,
+                                                                                     leaf, NN, margin + row0);
+                } else if (geo.row_words <= kWalkMaxWords)
                     k_margin_walk<true><<<blocks(rows_n), kWalkThreads, walk_lds_bytes(geo), c->stream>>>(
                         words, rows_n, geo, nodes, leaf, margin + row0);
                 else
@@ -659,10 +793,24 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     double ms[kPhCount] = {0.0};
     timer_collect(c, ms);
     if (stats) {
-        unsigned long long u = 0;
-        GBT_HIP(hipMemcpyAsync(&u, upd, 8, hipMemcpyDeviceToHost, c->stream));
+        unsigned long long u[kUpdCounters];
+        GBT_HIP(hipMemcpyAsync(u, upd, sizeof(u), hipMemcpyDeviceToHost, c->stream));
         GBT_HIP(hipStreamSynchronize(c->stream));
-        stats->hist_updates = (int64_t)u;
+        stats->hist_updates = 0;
+        for (int k = 0; k < kUpdCounters; ++k) stats->hist_updates += (int64_t)u[k];
+        unsigned long long st2[2] = {0, 0};
+        GBT_HIP(hipMemcpyAsync(st2, stat, sizeof(st2), hipMemcpyDeviceToHost, c->stream));
+        GBT_HIP(hipStreamSynchronize(c->stream));
+        // algorithmic bytes: the packed symbols of each row, its 16-byte
+        // fixed-point pair, its 4-byte row id below the root, and one write of
+        // every chunk's partial histogram
+        const int64_t wbytes = 4 * (((int64_t)mx->stride * mx->w + 31) / 32);
+        const int64_t root_chunk = std::max<int64_t>(2048, (R * G + 2 * kCUs - 1) / (2 * kCUs));
+        const int64_t root_parts = (D > 0 && R > 0) ? (R + root_chunk - 1) / root_chunk : 0;
+        stats->hist_launches = hist_launches;
+        stats->hist_rows = (D > 0 ? R : 0) + (int64_t)st2[0];
+        stats->hist_bytes = (D > 0 ? R : 0) * (wbytes + 16) + (int64_t)st2[0] * (wbytes + 20) +
+                            (root_parts + (int64_t)st2[1]) * mx->total_bins * 16;
         stats->ms_sample = ms[kPhSample];
         stats->ms_hist = ms[kPhHist];
         stats->ms_hist_aux = ms[kPhHistAux];

@@ -239,8 +239,9 @@ class Context:
         _check(_lib.gbt_ctx_memory(self.h, C.byref(used), C.byref(peak)))
         return used.value, peak.value
 
-    def set_timing(self, on: bool):
-        _check(_lib.gbt_ctx_set_timing(self.h, int(on)))
+    def set_timing(self, level: int):
+        """0 off, 1 events around the histogram kernel only, 2 every phase."""
+        _check(_lib.gbt_ctx_set_timing(self.h, int(level)))
 
     @property
     def torch_device(self):
