@@ -31,6 +31,81 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 METRIC = "histogram row-feature updates/sec (G/s), sec/tree, achieved HBM GB/s on 1 MI355X"
+HIST_KERNEL = "k_hist_dense"
+# sources of the histogram kernel: stored counter traffic is reported only
+# while these are unchanged
+HIST_SOURCES = ["hist.hip", "hist_impl.h", "common.h"]
+# a plain device-to-device copy of this size after the timed region scales the
+# HBM counters (FETCH_SIZE / WRITE_SIZE) to bytes
+CALIB_BYTES = 1 << 30
+
+
+def hist_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for name in HIST_SOURCES:
+        with open(os.path.join(ROOT, "paper_2005_09148_amd", "csrc", name), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def traffic_file(workload_key):
+    return os.path.join(ROOT, "profiles", f"{HIST_KERNEL}_traffic_{workload_key}.json")
+
+
+def stored_traffic(workload_key):
+    """HBM bytes per histogram launch from the stored counter runs, or None
+    when there are none or the kernel's sources changed since."""
+    path = traffic_file(workload_key)
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        rec = json.load(fh)
+    if rec.get("source_sha256") != hist_source_hash():
+        return None
+    return rec["traffic_bytes_per_launch"]
+
+
+def read_counters(path):
+    """Per-dispatch counter values from one rocprofv3 --pmc run (csv output):
+    {dispatch_id: (kernel_name, grid_size, value)}."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(path, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {path}")
+    out = {}
+    for fn in files:
+        with open(fn) as fh:
+            for r in csv.DictReader(fh):
+                key = (fn, r["Dispatch_Id"])
+                prev = out.get(key, (r["Kernel_Name"], int(r["Grid_Size"]), 0.0))
+                out[key] = (prev[0], prev[1], prev[2] + float(r["Counter_Value"]))
+    return out
+
+
+def pmc_summary(fetch_dir, write_dir, workload_key, commands):
+    """Turns the FETCH_SIZE and WRITE_SIZE runs into HBM bytes per histogram
+    launch, each counter scaled by what it reads for the calibration copy."""
+    res = {}
+    for name, path, calib_field in (("fetch", fetch_dir, "FETCH_SIZE"), ("write", write_dir, "WRITE_SIZE")):
+        rows = read_counters(path)
+        hist = [v for (k, g, v) in rows.values() if HIST_KERNEL in k]
+        copies = [(g, v) for (k, g, v) in rows.values() if "copyBuffer" in k]
+        if not hist or not copies:
+            raise SystemExit(f"{calib_field}: no {HIST_KERNEL} or copy dispatches in {path}")
+        grid, copy_kib = max(copies)
+        factor = CALIB_BYTES / (copy_kib * 1024.0)
+        res[name] = {"counter": calib_field, "dispatches": len(hist),
+                     "kib_per_dispatch": sum(hist) / len(hist),
+                     "calib_copy_kib": copy_kib, "calib_copy_grid": grid, "scale": factor}
+    traffic = sum(r["kib_per_dispatch"] * 1024.0 * r["scale"] for r in res.values())
+    rec = {"kernel": HIST_KERNEL, "workload": workload_key, "source_sha256": hist_source_hash(),
+           "calib_copy_bytes": CALIB_BYTES, "commands": commands, "counters": res,
+           "traffic_bytes_per_launch": round(traffic)}
+    with open(traffic_file(workload_key), "w") as fh:
+        json.dump(rec, fh, indent=1)
+    print(json.dumps(rec, indent=1))
 
 
 def parse():
@@ -42,6 +117,9 @@ def parse():
     ap.add_argument("--f", type=float, default=None, help="override the sampling fraction")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-trees", type=int, default=2)
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="summarize two rocprofv3 --pmc runs of this script (no GPU work)")
+    ap.add_argument("--pmc-commands", nargs="*", default=[], help="the commands of those runs")
     return ap.parse_args()
 
 
@@ -106,8 +184,18 @@ def cpu_baseline(X, y, cfg, n_trees, gpu_trees):
     }
 
 
+def workload_key(args):
+    from paper_2005_09148_amd import datagen
+    n = args.rows or datagen.FULL_ROWS[3]
+    f = args.f if args.f is not None else datagen.CONFIGS[3].f
+    return f"regression_{n}x50_f{f:g}"
+
+
 def main():
     args = parse()
+    if args.pmc_summary:
+        pmc_summary(*args.pmc_summary, workload_key(args), args.pmc_commands)
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU: the hot path here runs on a single MI355X "
               "(no multi-GPU path is built); run it with --gpus 1", file=sys.stderr)
@@ -164,6 +252,12 @@ def main():
         P.iteration = args.warmup + args.steps + k
         pstats.append(gbt.gbt_train_tree(ctx, mx, label, margin, P).stats)
     ctx.set_timing(0)
+    # counter calibration: one plain device-to-device copy of known size
+    src = torch.empty(CALIB_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
     upd = sum(s.hist_updates for s in stats)
     hbytes = sum(s.hist_bytes for s in stats)
     hms = sum(s.ms_hist for s in stats)
@@ -193,8 +287,9 @@ def main():
         "hist_updates_per_tree": upd // args.steps,
         "phase_ms_per_tree_untimed_run": phases,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                     "kernel": "k_hist_lds", "launches": launches,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": stored_traffic(workload_key(args)),
+                     "kernel": HIST_KERNEL, "launches": launches,
                      "avg_launch_us": round(hms * 1e3 / max(launches, 1), 2),
                      "algorithmic_bytes_per_launch": hbytes // max(launches, 1)},
     }

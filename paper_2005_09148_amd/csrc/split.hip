@@ -281,8 +281,9 @@ __global__ void k_part_scatter(const int32_t *__restrict__ rows, int64_t n,
     position[r] = child;
 }
 
-// Left flags of 16 consecutive slots per thread and the count of each tile
-// of 4096 slots (the first pass of the scan).
+// Left flags of one tile of 4096 slots per block (16 slots per thread, a
+// block stride apart so that loads and stores coalesce) and the count of
+// each tile (the first pass of the scan).
 __global__ void __launch_bounds__(256)
     k_part_flags_tiles(const int32_t *__restrict__ rows, int64_t n, const uint32_t *__restrict__ page, Geo geo,
                        const int32_t *__restrict__ position, const int32_t *__restrict__ slot_node,
@@ -290,10 +291,10 @@ __global__ void __launch_bounds__(256)
                        int32_t *__restrict__ tile_cnt)
 {
     __shared__ int32_t red[4];
-    const int64_t base = (int64_t)blockIdx.x * 4096 + (int64_t)threadIdx.x * 16;
+    const int64_t base = (int64_t)blockIdx.x * 4096 + threadIdx.x;
     int32_t cnt = 0;
     for (int k = 0; k < 16; ++k) {
-        const int64_t i = base + k;
+        const int64_t i = base + k * 256;
         if (i >= n) break;
         const int32_t r = rows[i];
         const int32_t nid = slot_node ? slot_node[i] : position[r];
