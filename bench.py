@@ -31,7 +31,8 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 METRIC = "histogram row-feature updates/sec (G/s), sec/tree, achieved HBM GB/s on 1 MI355X"
-HIST_KERNEL = "k_hist_dense"
+# the dense histogram kernels, by the hist_kernel field of the tree stats
+HIST_KERNELS = {1: "k_hist_dense", 2: "k_hist_rot"}
 # sources of the histogram kernel: stored counter traffic is reported only
 # while these are unchanged
 HIST_SOURCES = ["hist.hip", "hist_impl.h", "common.h"]
@@ -49,14 +50,14 @@ def hist_source_hash():
     return h.hexdigest()
 
 
-def traffic_file(workload_key):
-    return os.path.join(ROOT, "profiles", f"{HIST_KERNEL}_traffic_{workload_key}.json")
+def traffic_file(workload_key, kernel):
+    return os.path.join(ROOT, "profiles", f"{kernel}_traffic_{workload_key}.json")
 
 
-def stored_traffic(workload_key):
+def stored_traffic(workload_key, kernel):
     """HBM bytes per histogram launch from the stored counter runs, or None
     when there are none or the kernel's sources changed since."""
-    path = traffic_file(workload_key)
+    path = traffic_file(workload_key, kernel)
     if not os.path.exists(path):
         return None
     with open(path) as fh:
@@ -84,26 +85,26 @@ def read_counters(path):
     return out
 
 
-def pmc_summary(fetch_dir, write_dir, workload_key, commands):
+def pmc_summary(fetch_dir, write_dir, workload_key, commands, kernel):
     """Turns the FETCH_SIZE and WRITE_SIZE runs into HBM bytes per histogram
     launch, each counter scaled by what it reads for the calibration copy."""
     res = {}
     for name, path, calib_field in (("fetch", fetch_dir, "FETCH_SIZE"), ("write", write_dir, "WRITE_SIZE")):
         rows = read_counters(path)
-        hist = [v for (k, g, v) in rows.values() if HIST_KERNEL in k]
+        hist = [v for (k, g, v) in rows.values() if kernel + "<" in k]
         copies = [(g, v) for (k, g, v) in rows.values() if "copyBuffer" in k]
         if not hist or not copies:
-            raise SystemExit(f"{calib_field}: no {HIST_KERNEL} or copy dispatches in {path}")
+            raise SystemExit(f"{calib_field}: no {kernel} or copy dispatches in {path}")
         grid, copy_kib = max(copies)
         factor = CALIB_BYTES / (copy_kib * 1024.0)
         res[name] = {"counter": calib_field, "dispatches": len(hist),
                      "kib_per_dispatch": sum(hist) / len(hist),
                      "calib_copy_kib": copy_kib, "calib_copy_grid": grid, "scale": factor}
     traffic = sum(r["kib_per_dispatch"] * 1024.0 * r["scale"] for r in res.values())
-    rec = {"kernel": HIST_KERNEL, "workload": workload_key, "source_sha256": hist_source_hash(),
+    rec = {"kernel": kernel, "workload": workload_key, "source_sha256": hist_source_hash(),
            "calib_copy_bytes": CALIB_BYTES, "commands": commands, "counters": res,
            "traffic_bytes_per_launch": round(traffic)}
-    with open(traffic_file(workload_key), "w") as fh:
+    with open(traffic_file(workload_key, kernel), "w") as fh:
         json.dump(rec, fh, indent=1)
     print(json.dumps(rec, indent=1))
 
@@ -120,6 +121,7 @@ def parse():
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarize two rocprofv3 --pmc runs of this script (no GPU work)")
     ap.add_argument("--pmc-commands", nargs="*", default=[], help="the commands of those runs")
+    ap.add_argument("--pmc-kernel", default="k_hist_dense", choices=sorted(HIST_KERNELS.values()))
     return ap.parse_args()
 
 
@@ -194,7 +196,7 @@ def workload_key(args):
 def main():
     args = parse()
     if args.pmc_summary:
-        pmc_summary(*args.pmc_summary, workload_key(args), args.pmc_commands)
+        pmc_summary(*args.pmc_summary, workload_key(args), args.pmc_commands, args.pmc_kernel)
         return
     if args.gpus != 1:
         print("bench.py measures one GPU: the hot path here runs on a single MI355X "
@@ -265,6 +267,8 @@ def main():
     phases = {k: round(sum(getattr(s, "ms_" + k) for s in pstats) / len(pstats), 4)
               for k in ("sample", "hist", "hist_aux", "split", "margin", "total")}
     achieved = hbytes / (hms * 1e-3) / 1e9 if hms > 0 else 0.0
+    kernels = {HIST_KERNELS.get(s.hist_kernel, "k_hist_sparse") for s in stats}
+    kernel = kernels.pop() if len(kernels) == 1 else "+".join(sorted(kernels))
     line = {
         "metric": METRIC,
         "value": round(upd / dt / 1e9, 4),
@@ -288,8 +292,8 @@ def main():
         "phase_ms_per_tree_untimed_run": phases,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": stored_traffic(workload_key(args)),
-                     "kernel": HIST_KERNEL, "launches": launches,
+                     "traffic": stored_traffic(workload_key(args), kernel),
+                     "kernel": kernel, "launches": launches,
                      "avg_launch_us": round(hms * 1e3 / max(launches, 1), 2),
                      "algorithmic_bytes_per_launch": hbytes // max(launches, 1)},
     }

@@ -180,6 +180,8 @@ typedef struct {
     double ms_margin;       /* leaves and the margin update */
     double ms_total;        /* wall time of the call */
     double h2d_bytes;       /* bytes streamed from pinned-host pages */
+    int32_t hist_kernel;    /* GBT_HIST_PLAIN or GBT_HIST_ROTATED (dense), 0 sparse */
+    int32_t pad0;
 } gbt_tree_stats;
 
 typedef struct {
@@ -221,6 +223,15 @@ gbt_status gbt_ctx_memory(gbt_ctx *ctx, uint64_t *used_bytes, uint64_t *peak_byt
 /* HIP events on the context stream (gbt_tree_stats.ms_*): 0 off, 1 around
  * the histogram-building kernel only, 2 around every phase. */
 gbt_status gbt_ctx_set_timing(gbt_ctx *ctx, int32_t level);
+/* Which dense histogram kernel the context uses (results are identical):
+ * GBT_HIST_AUTO chooses by pass size, GBT_HIST_PLAIN forces one lane per row
+ * over a feature's contiguous bins, GBT_HIST_ROTATED forces the
+ * rotated-feature kernel (features of at most 256 bins; others fall back to
+ * the plain one).  GBT_E_INVALID for another value. */
+#define GBT_HIST_AUTO 0
+#define GBT_HIST_PLAIN 1
+#define GBT_HIST_ROTATED 2
+gbt_status gbt_ctx_set_hist_kernel(gbt_ctx *ctx, int32_t choice);
 
 /* ---- quantile cuts and ELLPACK pages: Sec. 2.2, Sec. 3.1 (Alg. 2, 3),
  * Sec. 3.2 (Alg. 4, 5) ------------------------------------------------------
@@ -289,7 +300,11 @@ gbt_status gbt_sampled_free(gbt_sampled *s);
  * [slots][total_bins][2] and the built slots are overwritten.  Then for each
  * sub entry: hist_d[target] = parent_hist_d[parent] - hist_d[built] (the
  * sibling of a built child), exact in integers.  `page` is a device page of
- * the matrix geometry of `layout` (page_d rows of row_words words). */
+ * the matrix geometry of `layout` (page_d rows of row_words words), as
+ * gbt_quantize writes it, 16-byte aligned (else GBT_E_INVALID).  Symbols
+ * outside a feature's bin range (only in a page not written by this library)
+ * add nothing.  GBT_E_UNSUPPORTED when a feature has more bins than one
+ * histogram group holds (2560 for dense pages, 4096 for sparse ones). */
 gbt_status gbt_build_hist(gbt_ctx *ctx, const gbt_matrix *layout, const uint32_t *page_d,
                           const int64_t *gpair_fx_d, const int32_t *rows_d, const gbt_seg *build_h,
                           int32_t n_build, const gbt_sub *sub_h, int32_t n_sub,

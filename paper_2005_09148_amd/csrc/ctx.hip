@@ -190,4 +190,13 @@ gbt_status gbt_ctx_set_timing(gbt_ctx *c, int32_t enable)
     return GBT_OK;
 }
 
+gbt_status gbt_ctx_set_hist_kernel(gbt_ctx *c, int32_t choice)
+{
+    if (!c) return set_error(GBT_E_INVALID, "gbt_ctx_set_hist_kernel: ctx is NULL");
+    if (choice != GBT_HIST_AUTO && choice != GBT_HIST_PLAIN && choice != GBT_HIST_ROTATED)
+        return set_error(GBT_E_INVALID, "gbt_ctx_set_hist_kernel: unknown kernel %d", choice);
+    c->hist_kernel = choice;
+    return GBT_OK;
+}
+
 }  // extern "C"

@@ -19,52 +19,60 @@
 namespace gbt {
 
 constexpr int kHistThreads = 512;
-constexpr int kLdsBins = 4096;  // 64 KiB of int64 (g, h) per workgroup
+// Sparse groups: up to 4096 bins, g then h (64 KiB of LDS).
+constexpr int kLdsBins = 4096;
+// Dense groups: up to 2560 bins; the h sums sit a fixed 2560 words after the
+// g sums so that one address serves both atomics (an immediate offset), and
+// four workgroups fit a CU's LDS.
+constexpr int kDenseBins = 2560;
 
 // A dense group spans at most this many words of a row and this many features.
 constexpr int kGroupWords = 8;
 constexpr int kMaxGroupFeat = 32;
 
-// Zero the LDS histogram (sg | sh, nb bins each).
-__device__ inline void lds_zero(unsigned long long *lds, int32_t nb)
+// Zero nb entries of the g sums at sg and of the h sums at sh.
+__device__ inline void lds_zero(unsigned long long *sg, unsigned long long *sh, int32_t nb)
 {
-    for (int t = threadIdx.x; t < 2 * nb; t += kHistThreads) lds[t] = 0ull;
+    for (int t = threadIdx.x; t < nb; t += kHistThreads) {
+        sg[t] = 0ull;
+        sh[t] = 0ull;
+    }
     __syncthreads();
 }
 
-// Write the LDS histogram as the chunk's partial and count the updates.
+// Write the LDS histogram as the chunk's partial and count the updates
+// (cnt: this wave's count, the same in every lane).
 __device__ inline void lds_flush(const unsigned long long *sg, const unsigned long long *sh,
-                                 int32_t nb, longlong2 *__restrict__ dst, unsigned int cnt,
+                                 int32_t nb, longlong2 *__restrict__ dst, unsigned long long cnt,
                                  unsigned long long *__restrict__ n_updates)
 {
+    __shared__ unsigned long long red[kHistThreads / 64];
+    if (n_updates && (threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = cnt;
     __syncthreads();
     for (int t = threadIdx.x; t < nb; t += kHistThreads)
         dst[t] = make_longlong2((long long)sg[t], (long long)sh[t]);
-    if (n_updates) {
+    if (n_updates && threadIdx.x == 0) {
         // one atomic per block, spread over kUpdCounters addresses
-        __shared__ unsigned int red[kHistThreads / 64];
-        for (int d = 32; d > 0; d >>= 1) cnt += __shfl_xor(cnt, d, 64);
-        if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = cnt;
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            unsigned long long t = 0;
-            for (int w = 0; w < kHistThreads / 64; ++w) t += red[w];
-            if (t) atomicAdd(&n_updates[blockIdx.x % kUpdCounters], t);
-        }
+        unsigned long long t = 0;
+        for (int w = 0; w < kHistThreads / 64; ++w) t += red[w];
+        if (t) atomicAdd(&n_updates[blockIdx.x % kUpdCounters], t);
     }
 }
 
-// Dense rows: slot j holds feature j.  The group's bin offsets live in scalar
-// registers; each lane fetches the next row's pair and words while it
-// decodes the current row from a register queue (constant indices only).
-template <bool kRows>
+// Dense rows: slot j holds feature j, W bits per symbol.  Each lane owns one
+// row at a time: it fetches the next row's pair and group words while it
+// decodes the current row.  The group's words are first shifted so that
+// feature u of the group starts at bit u*W of the word window; with W a
+// compile-time constant every symbol is then one bit-field extract from a
+// fixed register.  Null symbols are masked off; the update count comes from
+// the wave's ballot.
+template <int W, bool kRows>
 __global__ void __launch_bounds__(kHistThreads)
-    k_hist_dense(const uint32_t *__restrict__ page, int32_t row_words, int32_t w, uint32_t mask,
-                 uint32_t null_sym, const longlong2 *__restrict__ q, const int32_t *__restrict__ rows,
-                 const HistWork *__restrict__ work, const HistGroup *__restrict__ groups,
-                 int32_t n_groups, const int32_t *__restrict__ n_work_d, const int32_t *__restrict__ bin_ptr,
-                 int64_t total_bins, longlong2 *__restrict__ partials,
-                 unsigned long long *__restrict__ n_updates)
+    k_hist_dense(const uint32_t *__restrict__ page, int32_t row_words, uint32_t null_sym,
+                 const longlong2 *__restrict__ q, const int32_t *__restrict__ rows,
+                 const HistWork *__restrict__ work, const HistGroup *__restrict__ groups, int32_t n_groups,
+                 const int32_t *__restrict__ n_work_d, const int32_t *__restrict__ bin_ptr, int64_t total_bins,
+                 longlong2 *__restrict__ partials, unsigned long long *__restrict__ n_updates)
 {
     extern __shared__ unsigned long long lds[];
     const uint32_t active = n_work_d ? (uint32_t)(*n_work_d * n_groups) : gridDim.x;
@@ -73,13 +81,16 @@ __global__ void __launch_bounds__(kHistThreads)
     const HistWork wk = work[L / n_groups];
     const HistGroup gr = groups[L % n_groups];
     const int32_t nb = gr.b1 - gr.b0, nf = gr.f1 - gr.f0;
-    unsigned long long *sg = lds, *sh = lds + nb;
-    int32_t off[kMaxGroupFeat];
+    unsigned long long *sg = lds, *sh = lds + kDenseBins;
+    constexpr uint32_t kMask = (1u << W) - 1u;
+    constexpr int kMaxF = (kGroupWords * 32 / W) < kMaxGroupFeat ? (kGroupWords * 32 / W) : kMaxGroupFeat;
+    // byte address of each feature's first g sum (uniform)
+    char *base[kMaxF];
 #pragma unroll
-    for (int u = 0; u < kMaxGroupFeat; ++u) off[u] = u < nf ? bin_ptr[gr.f0 + u] - gr.b0 : 0;
-    lds_zero(lds, nb);
+    for (int u = 0; u < kMaxF; ++u) base[u] = (char *)(sg + (u < nf ? bin_ptr[gr.f0 + u] - gr.b0 : 0));
+    lds_zero(sg, sh, nb);
 
-    unsigned int cnt = 0;
+    unsigned int cnt = 0;  // this wave's updates
     int64_t i = wk.begin + threadIdx.x;
     longlong2 qn = make_longlong2(0, 0);
     uint32_t wn[kGroupWords];
@@ -93,36 +104,198 @@ __global__ void __launch_bounds__(kHistThreads)
     if (i < wk.end) fetch(i);
     for (; i < wk.end; i += kHistThreads) {
         const unsigned long long qg = (unsigned long long)qn.x, qh = (unsigned long long)qn.y;
-        uint32_t wq[kGroupWords];
+        uint32_t a[kGroupWords];
+        // a[k] = bits [32k + skip, 32k + skip + 32) of the group's words
 #pragma unroll
-        for (int k = 0; k < kGroupWords; ++k) wq[k] = wn[k];
+        for (int k = 0; k < kGroupWords; ++k)
+            a[k] = __builtin_amdgcn_alignbit(k + 1 < kGroupWords ? wn[k + 1] : 0u, wn[k], (uint32_t)gr.skip);
         if (i + kHistThreads < wk.end) fetch(i + kHistThreads);
-        uint64_t buf = (uint64_t)wq[0] >> gr.skip;
-        int32_t nbits = 32 - gr.skip;
 #pragma unroll
-        for (int k = 0; k + 1 < kGroupWords; ++k) wq[k] = wq[k + 1];
-#pragma unroll
-        for (int u = 0; u < kMaxGroupFeat; ++u) {
+        for (int u = 0; u < kMaxF; ++u) {
             if (u < nf) {
-                if (nbits < w) {
-                    buf |= (uint64_t)wq[0] << nbits;
-                    nbits += 32;
-#pragma unroll
-                    for (int k = 0; k + 1 < kGroupWords; ++k) wq[k] = wq[k + 1];
-                }
-                const uint32_t sym = (uint32_t)buf & mask;
-                buf >>= w;
-                nbits -= w;
-                if (sym != null_sym) {
-                    const int32_t idx = off[u] + (int32_t)sym;
-                    atomicAdd(&sg[idx], qg);
-                    atomicAdd(&sh[idx], qh);
-                    ++cnt;
+                const int bit = u * W, k = bit >> 5, sft = bit & 31;
+                uint32_t sym;
+                if (sft + W <= 32)
+                    sym = (a[k] >> sft) & kMask;
+                else
+                    sym = __builtin_amdgcn_alignbit(a[k + 1], a[k], (uint32_t)sft) & kMask;
+                const bool ok = sym != null_sym;
+                cnt += (unsigned int)__popcll(__ballot(ok));
+                if (ok) {
+                    unsigned long long *pg = (unsigned long long *)(base[u] + sym * 8u);
+                    atomicAdd(pg, qg);
+                    atomicAdd(pg + kDenseBins, qh);
                 }
             }
         }
     }
     lds_flush(sg, sh, nb, partials + (int64_t)wk.part * total_bins + gr.b0, cnt, n_updates);
+}
+
+// ---------------------------------------------------------------- rotated
+// Dense rows whose features have at most 256 bins.  One row per lane; a
+// group holds at most 16 features.  The LDS sums are 256 bin rows of 16
+// columns, column c holding one feature, so the address of (feature, bin) is
+// bin*128 + column*8 and its LDS bank pair is set by the column.  Lane l
+// visits the group's features starting at feature l mod nf: in every atomic
+// the 64 lanes spread over the features, hence over the bank pairs, instead
+// of colliding at random bins of one feature.  The rotation is applied once
+// per row to the group's bit string (a per-lane funnel shift), so each
+// step's symbol is still a fixed bit field.  The row's group words come
+// from two 16-byte loads.
+constexpr int kRotThreads = 1024;
+constexpr int kRotCols = 16;
+constexpr int kRotBins = 256;
+constexpr int kRotWords = 6;  // bit string of a group: at most 192 bits
+// rows per tree level from which the rotated kernel is chosen by default
+constexpr int64_t kRotMinRows = (int64_t)2 << 20;
+
+__device__ inline uint32_t pick(bool c, uint32_t a, uint32_t b) { return c ? a : b; }
+
+template <int W, bool kRows>
+__global__ void __launch_bounds__(kRotThreads)
+    k_hist_rot(const uint32_t *__restrict__ page, int32_t row_words, uint32_t null_sym,
+               const longlong2 *__restrict__ q, const int32_t *__restrict__ rows,
+               const HistWork *__restrict__ work, const HistGroup *__restrict__ groups, int32_t n_groups,
+               const int32_t *__restrict__ n_work_d, const int32_t *__restrict__ bin_ptr, int64_t total_bins,
+               longlong2 *__restrict__ partials, unsigned long long *__restrict__ n_updates)
+{
+    extern __shared__ unsigned long long lds[];
+    constexpr int kH = kRotBins * kRotCols;  // h sums follow the g sums
+    const uint32_t active = n_work_d ? (uint32_t)(*n_work_d * n_groups) : gridDim.x;
+    if (blockIdx.x >= active) return;
+    const uint32_t L = xcd_remap(blockIdx.x, active);
+    const HistWork wk = work[L / n_groups];
+    const HistGroup gr = groups[L % n_groups];
+    const int32_t nf = gr.f1 - gr.f0;
+    constexpr uint32_t kMask = (1u << W) - 1u;
+    constexpr int kMaxF = (kRotWords * 32 / W) < kRotCols ? (kRotWords * 32 / W) : kRotCols;
+
+    for (int t = threadIdx.x; t < 2 * kH; t += kRotThreads) lds[t] = 0ull;
+    __syncthreads();
+
+    const int lane = threadIdx.x & 63;
+    const int c0 = lane % nf;
+    // LDS byte address of the column visited at step u
+    uint32_t colb[kMaxF];
+#pragma unroll
+    for (int u = 0; u < kMaxF; ++u) {
+        int c = c0 + u;
+        c = c >= nf ? c - nf : c;
+        c = c >= nf ? c - nf : c;
+        colb[u] = (uint32_t)c * 8u;
+    }
+    const int wq0 = gr.w0 & ~3, ws = gr.w0 & 3;
+    const bool second = wq0 + 4 < gr.w0 + gr.nw;
+    const int nfw = nf * W;
+    // rotation: R = (S >> rho) | (S << (nfw - rho)) over the group's nfw bits
+    const int rho = c0 * W, rw = rho >> 5, rb = rho & 31;
+    const int lam = nfw - rho, lw = lam >> 5, lb = lam & 31;
+    uint32_t keep[kRotWords];
+#pragma unroll
+    for (int k = 0; k < kRotWords; ++k) {
+        const int lo = k * 32;
+        keep[k] = nfw >= lo + 32 ? 0xffffffffu : (nfw <= lo ? 0u : ((1u << (nfw - lo)) - 1u));
+    }
+    char *const base = (char *)lds;
+
+    unsigned int cnt = 0;  // this wave's updates
+    int64_t i = wk.begin + threadIdx.x;
+    longlong2 qn = make_longlong2(0, 0);
+    uint4 v0 = make_uint4(0u, 0u, 0u, 0u), v1 = v0;
+    // row ids run one iteration ahead of the row data they address
+    auto row_of = [&](int64_t ii) -> int64_t { return kRows ? (int64_t)rows[ii] : ii; };
+    auto fetch = [&](int64_t r) {
+        qn = q[r];
+        const uint4 *p = (const uint4 *)(page + r * row_words + wq0);
+        v0 = p[0];
+        v1 = second ? p[1] : make_uint4(0u, 0u, 0u, 0u);
+    };
+    int64_t r_next = 0;
+    if (i < wk.end) fetch(row_of(i));
+    if (i + kRotThreads < wk.end) r_next = row_of(i + kRotThreads);
+    for (; i < wk.end; i += kRotThreads) {
+        const unsigned long long qg = (unsigned long long)qn.x, qh = (unsigned long long)qn.y;
+        const uint32_t x[10] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w, 0u, 0u};
+        if (i + kRotThreads < wk.end) fetch(r_next);
+        if (i + 2 * kRotThreads < wk.end) r_next = row_of(i + 2 * kRotThreads);
+        // the group's words: y[k] = x[k + ws] (ws is the same for every lane)
+        uint32_t t1[9], y[kRotWords + 1];
+#pragma unroll
+        for (int k = 0; k < 9; ++k) t1[k] = pick(ws & 1, x[k + 1], x[k]);
+#pragma unroll
+        for (int k = 0; k <= kRotWords; ++k) y[k] = pick(ws & 2, k + 2 < 9 ? t1[k + 2] : 0u, t1[k]);
+        // S: the group's bit string from bit 0
+        uint32_t a[kRotWords];
+#pragma unroll
+        for (int k = 0; k < kRotWords; ++k)
+            a[k] = __builtin_amdgcn_alignbit(y[k + 1], y[k], (uint32_t)gr.skip) & keep[k];
+        // S >> rho: word shift rw (0..5) by three selects, then the bit shift
+        uint32_t s1[kRotWords + 4], s2[kRotWords + 4], s3[kRotWords + 1], rr[kRotWords];
+#pragma unroll
+        for (int k = 0; k < kRotWords + 4; ++k) {
+            const uint32_t z0 = k < kRotWords ? a[k] : 0u, z1 = k + 1 < kRotWords ? a[k + 1] : 0u;
+            s1[k] = pick(rw & 1, z1, z0);
+        }
+#pragma unroll
+        for (int k = 0; k < kRotWords + 4; ++k) s2[k] = pick(rw & 2, k + 2 < kRotWords + 4 ? s1[k + 2] : 0u, s1[k]);
+#pragma unroll
+        for (int k = 0; k <= kRotWords; ++k) s3[k] = pick(rw & 4, k + 4 < kRotWords + 4 ? s2[k + 4] : 0u, s2[k]);
+#pragma unroll
+        for (int k = 0; k < kRotWords; ++k) rr[k] = __builtin_amdgcn_alignbit(s3[k + 1], s3[k], (uint32_t)rb);
+        // S << lam: word k = funnel of a[k - lw] and a[k - lw - 1]
+        uint32_t rot[kRotWords];
+#pragma unroll
+        for (int k = 0; k < kRotWords; ++k) {
+            uint32_t hw = 0u, lw_ = 0u;
+#pragma unroll
+            for (int j = 0; j <= kRotWords; ++j) {
+                const bool c = lw == j;
+                hw = c ? (k - j >= 0 ? a[k - j] : 0u) : hw;
+                lw_ = c ? (k - j - 1 >= 0 ? a[k - j - 1] : 0u) : lw_;
+            }
+            const uint32_t ls = lb ? ((hw << lb) | (lw_ >> (32 - lb))) : hw;
+            rot[k] = rr[k] | ls;
+        }
+#pragma unroll
+        for (int u = 0; u < kMaxF; ++u) {
+            if (u < nf) {
+                const int bit = u * W, k = bit >> 5, sft = bit & 31;
+                uint32_t sym;
+                if (sft + W <= 32)
+                    sym = (rot[k] >> sft) & kMask;
+                else
+                    sym = __builtin_amdgcn_alignbit(rot[k + 1], rot[k], (uint32_t)sft) & kMask;
+                // symbols outside the bin range (only in a malformed page) are skipped
+                const bool ok = sym != null_sym && sym < (uint32_t)kRotBins;
+                cnt += (unsigned int)__popcll(__ballot(ok));
+                if (ok) {
+                    unsigned long long *pg = (unsigned long long *)(base + colb[u] + sym * (kRotCols * 8u));
+                    atomicAdd(pg, qg);
+                    atomicAdd(pg + kH, qh);
+                }
+            }
+        }
+    }
+    // the update count: one atomic per wave (the LDS is all histogram)
+    if (n_updates && lane == 0 && cnt)
+        atomicAdd(&n_updates[(blockIdx.x * (kRotThreads / 64) + (threadIdx.x >> 6)) % kUpdCounters],
+                  (unsigned long long)cnt);
+    // partial of this chunk: feature f's bins are column f of the bin rows;
+    // consecutive lanes read consecutive columns (no bank conflicts), and the
+    // four bins of a wave's 64 lanes write 64-byte runs per feature
+    __syncthreads();
+    longlong2 *dst = partials + (int64_t)wk.part * total_bins;
+    for (int t = threadIdx.x; t < kRotBins * kRotCols; t += kRotThreads) {
+        const int b = t / kRotCols, ff = t - b * kRotCols;
+        if (ff < nf) {
+            const int32_t g0 = bin_ptr[gr.f0 + ff];
+            if (g0 + b < bin_ptr[gr.f0 + ff + 1]) {
+                const unsigned long long *src = lds + t;
+                dst[g0 + b] = make_longlong2((long long)src[0], (long long)src[kH]);
+            }
+        }
+    }
 }
 
 // Sparse rows: the row's present features in ascending order as global
@@ -143,8 +316,8 @@ __global__ void __launch_bounds__(kHistThreads)
     const HistGroup gr = groups[L % n_groups];
     const int32_t nb = gr.b1 - gr.b0;
     unsigned long long *sg = lds, *sh = lds + nb;
-    lds_zero(lds, nb);
-    unsigned int cnt = 0;
+    lds_zero(sg, sh, nb);
+    unsigned long long cnt = 0;
     for (int64_t i = wk.begin + threadIdx.x; i < wk.end; i += kHistThreads) {
         const int64_t r = kRows ? (int64_t)rows[i] : i;
         const longlong2 qq = q[r];
@@ -169,66 +342,148 @@ __global__ void __launch_bounds__(kHistThreads)
             }
         }
     }
+    // the flush takes one count per wave
+    for (int d = 32; d > 0; d >>= 1) cnt += __shfl_xor(cnt, d, 64);
     lds_flush(sg, sh, nb, partials + (int64_t)wk.part * total_bins + gr.b0, cnt, n_updates);
 }
 
-__global__ void k_hist_reduce(const longlong2 *__restrict__ partials, const HistReduce *__restrict__ red,
-                              const int32_t *__restrict__ n_red_d, const longlong2 *__restrict__ parent,
-                              longlong2 *__restrict__ hist, int64_t total_bins)
+// Sums each built node's partials into its histogram and, in the same pass,
+// writes the sibling as parent minus that sum.  A block covers 64 bins; its
+// four waves sum every fourth partial and fold through LDS, so even a single
+// node's reduction spreads over total_bins / 64 blocks.
+constexpr int kRedBins = 64;
+constexpr int kRedSplit = 4;
+
+__global__ void __launch_bounds__(kRedBins * kRedSplit)
+    k_hist_reduce(const longlong2 *__restrict__ partials, const HistReduce *__restrict__ red,
+                  const int32_t *__restrict__ n_red_d, const longlong2 *__restrict__ parent,
+                  longlong2 *__restrict__ hist, int64_t total_bins)
 {
     if (n_red_d && (int32_t)blockIdx.y >= *n_red_d) return;
+    __shared__ long long sg[kRedSplit][kRedBins], sh[kRedSplit][kRedBins];
     const HistReduce rd = red[blockIdx.y];
-    for (int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; b < total_bins;
-         b += (int64_t)gridDim.x * blockDim.x) {
-        long long g = 0, h = 0;
-        for (int32_t k = 0; k < rd.nparts; ++k) {
-            longlong2 v = partials[(int64_t)(rd.part0 + k) * total_bins + b];
+    const int lane = threadIdx.x % kRedBins, s = threadIdx.x / kRedBins;
+    const int64_t b = (int64_t)blockIdx.x * kRedBins + lane;
+    long long g = 0, h = 0;
+    if (b < total_bins) {
+        for (int32_t k = s; k < rd.nparts; k += kRedSplit) {
+            const longlong2 v = partials[(int64_t)(rd.part0 + k) * total_bins + b];
             g += v.x;
             h += v.y;
         }
+    }
+    sg[s][lane] = g;
+    sh[s][lane] = h;
+    __syncthreads();
+    if (s == 0 && b < total_bins) {
+        for (int t = 1; t < kRedSplit; ++t) {
+            g += sg[t][lane];
+            h += sh[t][lane];
+        }
         hist[(int64_t)rd.slot * total_bins + b] = make_longlong2(g, h);
         if (rd.sub_target >= 0) {
-            longlong2 pv = parent[(int64_t)rd.sub_parent * total_bins + b];
+            const longlong2 pv = parent[(int64_t)rd.sub_parent * total_bins + b];
             hist[(int64_t)rd.sub_target * total_bins + b] = make_longlong2(pv.x - g, pv.y - h);
         }
     }
 }
 
-// Feature groups with at most kLdsBins bins each and about equal bin counts;
-// a dense group's symbols also span at most kGroupWords words.
-bool hist_groups(const gbt_matrix *mx, std::vector<HistGroup> *out)
+// Feature groups: contiguous features with about equal bin counts, each
+// group within its kernel's limits (LDS bins; for dense rows also the words
+// and features one lane decodes).
+static bool dense_groups(const gbt_matrix *mx, int64_t max_bins, int max_feat, int max_words, bool rot,
+                         std::vector<HistGroup> *out)
 {
     out->clear();
-    bool fits = true;
     const int64_t tb = mx->total_bins;
-    const int64_t G = std::max<int64_t>(1, (tb + kLdsBins - 1) / kLdsBins);
-    const int64_t target = (tb + G - 1) / G;
-    auto span_words = [&](int32_t f0, int32_t f1) {
-        int64_t b0 = (int64_t)f0 * mx->w, b1 = (int64_t)f1 * mx->w;
-        return (int32_t)((b1 + 31) / 32 - b0 / 32);
+    const int64_t G = std::max<int64_t>(
+        {(int64_t)1, (tb + max_bins - 1) / max_bins, ((int64_t)mx->m + max_feat - 1) / max_feat});
+    const int64_t target_bins = (tb + G - 1) / G;
+    const int64_t target_feat = (mx->m + G - 1) / G;
+    auto fits = [&](int32_t f0, int32_t f1) {
+        const int64_t b0 = (int64_t)f0 * mx->w, b1 = (int64_t)f1 * mx->w;
+        const int32_t nw = (int32_t)((b1 + 31) / 32 - b0 / 32);
+        // the rotated kernel reads the words from a 16-byte aligned window of 8
+        const int32_t need = rot ? (int32_t)((b0 >> 5) & 3) + nw : nw;
+        return need <= max_words && f1 - f0 <= max_feat &&
+               mx->bin_ptr_h[f1] - mx->bin_ptr_h[f0] <= max_bins && (!rot || (f1 - f0) * mx->w <= 192);
     };
     int32_t f0 = 0;
     while (f0 < mx->m) {
+        if (!fits(f0, f0 + 1)) return false;
         int32_t f1 = f0 + 1;
-        while (f1 < mx->m && mx->bin_ptr_h[f1 + 1] - mx->bin_ptr_h[f0] <= target &&
-               (mx->sparse || (span_words(f0, f1 + 1) <= kGroupWords && f1 + 1 - f0 <= kMaxGroupFeat)))
+        while (f1 < mx->m && fits(f0, f1 + 1) && mx->bin_ptr_h[f1 + 1] - mx->bin_ptr_h[f0] <= target_bins &&
+               f1 + 1 - f0 <= target_feat)
             ++f1;
         HistGroup g;
         g.f0 = f0;
         g.f1 = f1;
         g.b0 = mx->bin_ptr_h[f0];
         g.b1 = mx->bin_ptr_h[f1];
-        int64_t bit = (int64_t)f0 * mx->w;
+        const int64_t bit = (int64_t)f0 * mx->w;
         g.w0 = (int32_t)(bit >> 5);
         g.skip = (int32_t)(bit & 31);
-        g.nw = span_words(f0, f1);
+        g.nw = (int32_t)(((int64_t)f1 * mx->w + 31) / 32 - bit / 32);
         g.pad0 = 0;
-        if (g.b1 - g.b0 > kLdsBins) fits = false;
-        if (!mx->sparse && g.nw > kGroupWords) fits = false;
         out->push_back(g);
         f0 = f1;
     }
-    return fits;
+    return true;
+}
+
+static void sparse_groups(const gbt_matrix *mx, std::vector<HistGroup> *out)
+{
+    out->clear();
+    const int64_t tb = mx->total_bins;
+    const int64_t G = std::max<int64_t>(1, (tb + kLdsBins - 1) / kLdsBins);
+    const int64_t target = (tb + G - 1) / G;
+    int32_t f0 = 0;
+    while (f0 < mx->m) {
+        int32_t f1 = f0 + 1;
+        while (f1 < mx->m && mx->bin_ptr_h[f1 + 1] - mx->bin_ptr_h[f0] <= target) ++f1;
+        HistGroup g{f0, f1, mx->bin_ptr_h[f0], mx->bin_ptr_h[f1], 0, 0, 0, 0};
+        out->push_back(g);
+        f0 = f1;
+    }
+}
+
+gbt_status hist_plan(const gbt_matrix *mx, int64_t rows_hint, int choice, HistPlan *out)
+{
+    out->groups.clear();
+    int32_t max_feature_bins = 0;
+    for (int32_t f = 0; f < mx->m; ++f)
+        max_feature_bins = std::max(max_feature_bins, mx->bin_ptr_h[f + 1] - mx->bin_ptr_h[f]);
+    if (mx->sparse) {
+        if (max_feature_bins > kLdsBins)
+            return set_error(GBT_E_UNSUPPORTED, "a feature has %d bins (at most %d)", max_feature_bins,
+                             kLdsBins);
+        out->kind = kHistSparse;
+        out->threads = kHistThreads;
+        out->target_wgs = 2 * kCUs;
+        sparse_groups(mx, &out->groups);
+    } else {
+        if (mx->w < 1 || mx->w > 12 || max_feature_bins > kDenseBins)
+            return set_error(GBT_E_UNSUPPORTED, "a feature has %d bins (at most %d in a dense page)",
+                             max_feature_bins, kDenseBins);
+        // the rotated kernel pays off on large passes; smaller ones keep more
+        // workgroups per CU with the plain kernel
+        const bool want_rot = choice == GBT_HIST_ROTATED || (choice == GBT_HIST_AUTO && rows_hint >= kRotMinRows);
+        if (want_rot && max_feature_bins <= kRotBins &&
+            dense_groups(mx, (int64_t)kRotBins * kRotCols, kRotCols, 8, true, &out->groups)) {
+            out->kind = kHistRot;
+            out->threads = kRotThreads;
+            out->target_wgs = kCUs;  // one 1024-thread workgroup per CU
+        } else {
+            if (!dense_groups(mx, kDenseBins, kMaxGroupFeat, kGroupWords, false, &out->groups))
+                return set_error(GBT_E_UNSUPPORTED, "no feature grouping fits the histogram kernel");
+            out->kind = kHistDense;
+            out->threads = kHistThreads;
+            out->target_wgs = 2 * kCUs;
+        }
+    }
+    out->max_groups_bins = 0;
+    for (auto &g : out->groups) out->max_groups_bins = std::max(out->max_groups_bins, g.b1 - g.b0);
+    return GBT_OK;
 }
 
 gbt_status build_hist_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int64_t *q,
@@ -241,18 +496,16 @@ gbt_status build_hist_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *pag
         GBT_CHECK(n_sub == 0, "a subtraction needs its built sibling in the same call");
         return GBT_OK;
     }
-    std::vector<HistGroup> groups;
-    const bool fits = hist_groups(mx, &groups);
-    if (!fits)
-        return set_error(GBT_E_UNSUPPORTED, "a feature has more than %d bins or %d words of symbols",
-                         kLdsBins, kGroupWords);
-    const int32_t G = (int32_t)groups.size();
-
     int64_t total_rows = 0;
     for (int32_t k = 0; k < n_build; ++k) total_rows += std::max<int64_t>(0, build[k].end - build[k].begin);
-    // chunks: about two workgroups per CU over all groups, at least 2048 rows each
-    const int64_t target_wg = 2 * kCUs;
-    int64_t chunk = (total_rows * G + target_wg - 1) / target_wg;
+    HistPlan hp;
+    GBT_TRY(hist_plan(mx, total_rows, c->hist_kernel, &hp));
+    const std::vector<HistGroup> &groups = hp.groups;
+    const int32_t G = (int32_t)groups.size();
+    // chunks: at most the kernel's workgroup target over all groups (each node
+    // adds at most one chunk), at least 2048 rows each
+    const int64_t items = std::max<int64_t>(1, hp.target_wgs / G - n_build);
+    int64_t chunk = (total_rows + items - 1) / items;
     chunk = std::max<int64_t>(chunk, 2048);
     std::vector<HistWork> work;
     std::vector<HistReduce> red;
@@ -297,9 +550,8 @@ gbt_status build_hist_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *pag
     unsigned long long *upd = nullptr;
     if (stats) GBT_TRY(scratch_t(c, kScrUpd, kUpdCounters, &upd));
 
-    HistLaunch hl{groups_d, G, 0, work_d, nullptr, (int32_t)work.size(), red_d, nullptr, (int32_t)red.size(),
-                  (int64_t *)partials};
-    for (auto &g : groups) hl.max_groups_bins = std::max(hl.max_groups_bins, g.b1 - g.b0);
+    HistLaunch hl{hp.kind, groups_d, G, hp.max_groups_bins, work_d, nullptr, (int32_t)work.size(), red_d,
+                  nullptr, (int32_t)red.size(), (int64_t *)partials};
     GBT_CHECK(n_sub == 0 || parent_hist, "subtraction needs the parent histograms");
     GBT_TRY(hist_launch_device(c, mx, page, q, rows, hl, parent_hist, hist, upd));
     if (stats && !work.empty()) {
@@ -321,43 +573,100 @@ gbt_status hist_launch_device(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
     const int64_t tb = mx->total_bins;
     const int32_t G = hl.n_groups;
     longlong2 *partials = (longlong2 *)hl.partials;
-    if (hl.max_work > 0) {
-        size_t lds = (size_t)hl.max_groups_bins * 16;
+    if (!mx->sparse && (mx->w < 1 || mx->w > 12))
+        return set_error(GBT_E_UNSUPPORTED, "dense symbols of %d bits", mx->w);
+    if (hl.max_work > 0 && hl.kind == kHistRot) {
+        const uint32_t null_sym = mx->has_missing ? mx->null_sym : 0xffffffffu;
+        const unsigned grid = (unsigned)((size_t)hl.max_work * (size_t)G);
+        const size_t lds = (size_t)kRotBins * kRotCols * 16;
+        const longlong2 *qq = (const longlong2 *)q;
+        const int mark = timer_begin(c, kPhHist);
+#define GBT_HIST_ROT(WB)                                                                                 \
+    case WB:                                                                                             \
+        if (rows)                                                                                        \
+            k_hist_rot<WB, true><<<grid, kRotThreads, lds, c->stream>>>(page, mx->row_words, null_sym, qq,  \
+                                                                       rows, hl.work, hl.groups, G,      \
+                                                                       hl.n_work_d, mx->bin_ptr_d, tb,   \
+                                                                       partials, upd);                   \
+        else                                                                                             \
+            k_hist_rot<WB, false><<<grid, kRotThreads, lds, c->stream>>>(page, mx->row_words, null_sym, qq, \
+                                                                        rows, hl.work, hl.groups, G,     \
+                                                                        hl.n_work_d, mx->bin_ptr_d, tb,  \
+                                                                        partials, upd);                  \
+        break;
+        switch (mx->w) {
+            GBT_HIST_ROT(1)
+            GBT_HIST_ROT(2)
+            GBT_HIST_ROT(3)
+            GBT_HIST_ROT(4)
+            GBT_HIST_ROT(5)
+            GBT_HIST_ROT(6)
+            GBT_HIST_ROT(7)
+            GBT_HIST_ROT(8)
+            GBT_HIST_ROT(9)
+            GBT_HIST_ROT(10)
+            GBT_HIST_ROT(11)
+            GBT_HIST_ROT(12)
+        }
+#undef GBT_HIST_ROT
+        GBT_LAUNCHED();
+        timer_end(c, mark);
+    } else if (hl.max_work > 0) {
         uint32_t null_sym = (mx->sparse || mx->has_missing) ? mx->null_sym : 0xffffffffu;
         uint32_t mask = mx->w >= 32 ? 0xffffffffu : ((1u << mx->w) - 1u);
         unsigned grid = (unsigned)((size_t)hl.max_work * (size_t)G);
         const int mark = timer_begin(c, kPhHist);
-#define GBT_HIST_DENSE(RW)                                                                          \
-    k_hist_dense<RW><<<grid, kHistThreads, lds, c->stream>>>(page, mx->row_words, mx->w, mask, null_sym,   \
-                                                             (const longlong2 *)q, rows, hl.work,        \
-                                                             hl.groups, G, hl.n_work_d, mx->bin_ptr_d, tb, \
-                                                             partials, upd)
-#define GBT_HIST_SPARSE(RW)                                                                        \
-    k_hist_sparse<RW><<<grid, kHistThreads, lds, c->stream>>>(page, mx->row_words, mx->w, mask,      \
-                                                              mx->stride, (const longlong2 *)q, rows,  \
-                                                              hl.work, hl.groups, G, hl.n_work_d, tb,  \
-                                                              partials, upd)
         if (mx->sparse) {
+            size_t lds = (size_t)hl.max_groups_bins * 16;
             if (rows)
-                GBT_HIST_SPARSE(true);
+                k_hist_sparse<true><<<grid, kHistThreads, lds, c->stream>>>(
+                    page, mx->row_words, mx->w, mask, mx->stride, (const longlong2 *)q, rows, hl.work, hl.groups,
+                    G, hl.n_work_d, tb, partials, upd);
             else
-                GBT_HIST_SPARSE(false);
+                k_hist_sparse<false><<<grid, kHistThreads, lds, c->stream>>>(
+                    page, mx->row_words, mx->w, mask, mx->stride, (const longlong2 *)q, rows, hl.work, hl.groups,
+                    G, hl.n_work_d, tb, partials, upd);
         } else {
-            if (rows)
-                GBT_HIST_DENSE(true);
-            else
-                GBT_HIST_DENSE(false);
-        }
+            const size_t lds = (size_t)(kDenseBins + hl.max_groups_bins) * 8;
+            const longlong2 *qq = (const longlong2 *)q;
+#define GBT_HIST_DENSE(WB)                                                                                  \
+    case WB:                                                                                                \
+        if (rows)                                                                                           \
+            k_hist_dense<WB, true><<<grid, kHistThreads, lds, c->stream>>>(page, mx->row_words, null_sym, qq,  \
+                                                                          rows, hl.work, hl.groups, G,      \
+                                                                          hl.n_work_d, mx->bin_ptr_d, tb,   \
+                                                                          partials, upd);                   \
+        else                                                                                                \
+            k_hist_dense<WB, false><<<grid, kHistThreads, lds, c->stream>>>(page, mx->row_words, null_sym, qq, \
+                                                                           rows, hl.work, hl.groups, G,     \
+                                                                           hl.n_work_d, mx->bin_ptr_d, tb,  \
+                                                                           partials, upd);                  \
+        break;
+            switch (mx->w) {
+                GBT_HIST_DENSE(1)
+                GBT_HIST_DENSE(2)
+                GBT_HIST_DENSE(3)
+                GBT_HIST_DENSE(4)
+                GBT_HIST_DENSE(5)
+                GBT_HIST_DENSE(6)
+                GBT_HIST_DENSE(7)
+                GBT_HIST_DENSE(8)
+                GBT_HIST_DENSE(9)
+                GBT_HIST_DENSE(10)
+                GBT_HIST_DENSE(11)
+                GBT_HIST_DENSE(12)
+            }
 #undef GBT_HIST_DENSE
-#undef GBT_HIST_SPARSE
+        }
         GBT_LAUNCHED();
         timer_end(c, mark);
     }
     if (hl.max_red > 0) {
         const int aux = timer_begin(c, kPhHistAux);
-        dim3 rg((unsigned)std::min<int64_t>((tb + 255) / 256, 256), (unsigned)hl.max_red);
-        k_hist_reduce<<<rg, 256, 0, c->stream>>>(partials, hl.red, hl.n_red_d, (const longlong2 *)parent_hist,
-                                                 (longlong2 *)hist, tb);
+        dim3 rg((unsigned)((tb + kRedBins - 1) / kRedBins), (unsigned)hl.max_red);
+        k_hist_reduce<<<rg, kRedBins * kRedSplit, 0, c->stream>>>(partials, hl.red, hl.n_red_d,
+                                                                  (const longlong2 *)parent_hist,
+                                                                  (longlong2 *)hist, tb);
         GBT_LAUNCHED();
         timer_end(c, aux);
     }
@@ -377,6 +686,7 @@ extern "C" gbt_status gbt_build_hist(gbt_ctx *c, const gbt_matrix *layout, const
     GBT_CHECK(n_build >= 0 && n_sub >= 0, "negative counts");
     GBT_CHECK(n_build == 0 || (page_d && gpair_fx_d && build_h), "gbt_build_hist: NULL rows input");
     GBT_CHECK(n_sub == 0 || (sub_h && parent_hist_d), "gbt_build_hist: NULL subtraction input");
+    GBT_CHECK(((uintptr_t)page_d & 15) == 0, "gbt_build_hist: the page must be 16-byte aligned");
     for (int32_t k = 0; k < n_build; ++k)
         GBT_CHECK(build_h[k].begin >= 0 && build_h[k].begin <= build_h[k].end && build_h[k].node_slot >= 0,
                   "bad build segment %d", k);

@@ -34,12 +34,31 @@ struct HistReduce {
     int32_t pad0;
 };
 
-// Feature groups of the histogram kernels; false when a feature does not fit.
-bool hist_groups(const gbt_matrix *mx, std::vector<HistGroup> *out);
+// Which histogram kernel a matrix uses.
+enum HistKind {
+    kHistSparse = 0,  // CSR pages: global-bin symbols, groups of bin ranges
+    kHistDense = 1,   // dense pages, any feature up to 2560 bins
+    kHistRot = 2,     // dense pages, features of at most 256 bins: lanes visit
+                      // the group's features in rotated order (conflict-free LDS)
+};
+
+struct HistPlan {
+    int kind;
+    int threads;      // workgroup size
+    int target_wgs;   // workgroups a launch aims at
+    std::vector<HistGroup> groups;
+    int32_t max_groups_bins;
+};
+
+// The kernel and feature groups for a matrix whose passes cover about
+// rows_hint rows; choice is a GBT_HIST_* value.  GBT_E_UNSUPPORTED when a
+// feature does not fit any kernel.
+gbt_status hist_plan(const gbt_matrix *mx, int64_t rows_hint, int choice, HistPlan *out);
 
 // A histogram pass whose work lists live on the device.  Counts are read
 // from device memory (n_work_d, n_red_d); the grids are sized by the maxima.
 struct HistLaunch {
+    int kind;
     const HistGroup *groups;
     int32_t n_groups;
     int32_t max_groups_bins;  // largest group, in bins

@@ -268,10 +268,14 @@ __device__ inline int32_t scan1024(int32_t v, int32_t *lds16, int32_t *total)
 // is set, the plan of the next level: the list of present children in heap
 // order with their histogram slots, and for each split parent the smaller
 // child to build (chunked into work items) with the larger one as parent
-// minus it.
+// minus it.  The chunk size is chosen so that the level has at most
+// `items` work items per feature group (one per workgroup slot), unless it
+// builds more nodes than that.
+constexpr int64_t kMinChunk = 1024;
+
 __global__ void __launch_bounds__(1024)
     k_plan_level(const EvalNode *__restrict__ cur, const int32_t *__restrict__ n_cur_d,
-                 DevNode *__restrict__ nodes, const int32_t *__restrict__ P, int32_t plan, int64_t chunk,
+                 DevNode *__restrict__ nodes, const int32_t *__restrict__ P, int32_t plan, int32_t items,
                  EvalNode *__restrict__ next, int32_t *__restrict__ n_next_d, HistWork *__restrict__ work,
                  int32_t *__restrict__ n_work_d, HistReduce *__restrict__ red, int32_t *__restrict__ n_red_d,
                  unsigned long long *__restrict__ stat)
@@ -298,6 +302,40 @@ __global__ void __launch_bounds__(1024)
     if (!plan) return;
     __threadfence_block();
     __syncthreads();
+    // rows and nodes to build, for the chunk size
+    __shared__ unsigned long long red_rows[16];
+    __shared__ int32_t red_nodes[16];
+    unsigned long long rb = 0;
+    int32_t nbuild = 0;
+    for (int32_t t = threadIdx.x; t < n_cur; t += 1024) {
+        const int32_t p = cur[t].heap;
+        if (!nodes[p].split) continue;
+        const int64_t a = nodes[2 * p + 1].end - nodes[2 * p + 1].begin;
+        const int64_t b = nodes[2 * p + 2].end - nodes[2 * p + 2].begin;
+        rb += (unsigned long long)(a <= b ? a : b);
+        ++nbuild;
+    }
+    for (int d = 32; d > 0; d >>= 1) {
+        rb += __shfl_xor(rb, d, 64);
+        nbuild += __shfl_xor(nbuild, d, 64);
+    }
+    if ((threadIdx.x & 63) == 0) {
+        red_rows[threadIdx.x >> 6] = rb;
+        red_nodes[threadIdx.x >> 6] = nbuild;
+    }
+    __syncthreads();
+    unsigned long long rows_total = 0;
+    int32_t nodes_total = 0;
+    for (int w = 0; w < 16; ++w) {
+        rows_total += red_rows[w];
+        nodes_total += red_nodes[w];
+    }
+    // room for the chunks of large nodes: what the node count leaves of the
+    // target, but at least half of it (a level of many nodes may then take
+    // up to 1.5 times the target)
+    const int64_t room = items - nodes_total > items / 2 ? items - nodes_total : (items / 2 > 1 ? items / 2 : 1);
+    int64_t chunk = ((int64_t)rows_total + room - 1) / room;
+    chunk = chunk > kMinChunk ? chunk : kMinChunk;
     int32_t c_build = 0, c_part = 0;
     unsigned long long rows_built = 0;
     for (int32_t base = 0; base < n_cur; base += 1024) {
@@ -654,12 +692,15 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         GBT_TRY(scratch(c, kScrHistB, std::max<size_t>(hist_bytes, 16), (void **)&histB));
     }
     // plan buffers: two level lists, their counts, work items, reduce items, stats
-    std::vector<HistGroup> groups;
-    if (!hist_groups(mx, &groups))
-        return set_error(GBT_E_UNSUPPORTED, "a feature has too many bins or symbol words for LDS");
+    HistPlan hp;
+    GBT_TRY(hist_plan(mx, R, c->hist_kernel, &hp));
+    const std::vector<HistGroup> &groups = hp.groups;
     const int32_t G = (int32_t)groups.size();
-    const int64_t chunk = std::max<int64_t>(2048, ((R / 2) * G + 2 * kCUs - 1) / (2 * kCUs));
-    const int32_t max_work = (int32_t)((R / 2) / chunk + max_level_nodes + 1);
+    const int64_t twg = hp.target_wgs;
+    // work items per group and level: one per workgroup slot (more only when
+    // a level builds more nodes)
+    const int32_t items = (int32_t)std::max<int64_t>(1, twg / G);
+    const int32_t max_work = std::max(items, items / 2 + max_level_nodes) + 1;
     auto al = [](size_t b) { return (b + 255) / 256 * 256; };
     const size_t o_ev1 = al((size_t)max_level_nodes * sizeof(EvalNode));
     const size_t o_cnt = o_ev1 + o_ev1;
@@ -710,14 +751,14 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         std::swap(rows, rows_tmp);
         const bool plan_next = d + 1 < D && R > 0;
         if (P) {
-            k_plan_level<<<1, 1024, 0, c->stream>>>(evA, cntA, nodes, P, plan_next ? 1 : 0, chunk, evB, cntB,
+            k_plan_level<<<1, 1024, 0, c->stream>>>(evA, cntA, nodes, P, plan_next ? 1 : 0, items, evB, cntB,
                                                     work_d, cnt + 2, red_d, cnt + 3, stat);
             GBT_LAUNCHED();
         }
         timer_end(c, mark);
         if (plan_next) {
-            HistLaunch hl{groups_d, G, 0, work_d, cnt + 2, max_work, red_d, cnt + 3, maxn, partials};
-            for (auto &g : groups) hl.max_groups_bins = std::max(hl.max_groups_bins, g.b1 - g.b0);
+            HistLaunch hl{hp.kind, groups_d, G, hp.max_groups_bins, work_d, cnt + 2, max_work, red_d, cnt + 3, maxn,
+                          partials};
             GBT_TRY(hist_launch_device(c, mx, so.page, so.q, rows, hl, histA, histB, upd));
             ++hist_launches;
             std::swap(histA, histB);
@@ -805,7 +846,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         // fixed-point pair, its 4-byte row id below the root, and one write of
         // every chunk's partial histogram
         const int64_t wbytes = 4 * (((int64_t)mx->stride * mx->w + 31) / 32);
-        const int64_t root_chunk = std::max<int64_t>(2048, (R * G + 2 * kCUs - 1) / (2 * kCUs));
+        const int64_t root_chunk = std::max<int64_t>(2048, (R * G + twg - 1) / twg);
         const int64_t root_parts = (D > 0 && R > 0) ? (R + root_chunk - 1) / root_chunk : 0;
         stats->hist_launches = hist_launches;
         stats->hist_rows = (D > 0 ? R : 0) + (int64_t)st2[0];
@@ -817,6 +858,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         stats->ms_split = ms[kPhSplit];
         stats->ms_margin = ms[kPhMargin];
         stats->h2d_bytes = h2d;
+        stats->hist_kernel = hp.kind == kHistRot ? GBT_HIST_ROTATED : (hp.kind == kHistDense ? GBT_HIST_PLAIN : 0);
         stats->ms_total =
             std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t_start).count();
     }

@@ -105,7 +105,8 @@ class TreeStats(C.Structure):
                 ("hist_launches", C.c_int32), ("hist_rows", C.c_int64),
                 ("hist_updates", C.c_int64), ("hist_bytes", C.c_int64), ("ms_hist", C.c_double),
                 ("ms_hist_aux", C.c_double), ("ms_sample", C.c_double), ("ms_split", C.c_double),
-                ("ms_margin", C.c_double), ("ms_total", C.c_double), ("h2d_bytes", C.c_double)]
+                ("ms_margin", C.c_double), ("ms_total", C.c_double), ("h2d_bytes", C.c_double),
+                ("hist_kernel", C.c_int32), ("pad0", C.c_int32)]
 
 
 class SampleParams(C.Structure):
@@ -130,6 +131,7 @@ SIGNATURES = {
     "gbt_ctx_destroy": (_i32, [_vp]),
     "gbt_ctx_memory": (_i32, [_vp, _vp, _vp]),
     "gbt_ctx_set_timing": (_i32, [_vp, _i32]),
+    "gbt_ctx_set_hist_kernel": (_i32, [_vp, _i32]),
     "gbt_quantize": (_i32, [_vp, _vp, _vp, _vp]),
     "gbt_quantize_begin": (_i32, [_vp, _vp, _i32, _i64, _i32, _vp]),
     "gbt_quantize_sketch_batch": (_i32, [_vp, _vp]),
@@ -242,6 +244,13 @@ class Context:
     def set_timing(self, level: int):
         """0 off, 1 events around the histogram kernel only, 2 every phase."""
         _check(_lib.gbt_ctx_set_timing(self.h, int(level)))
+
+    HIST_AUTO, HIST_PLAIN, HIST_ROTATED = 0, 1, 2
+
+    def set_hist_kernel(self, choice: int):
+        """Dense histogram kernel: HIST_AUTO (by pass size), HIST_PLAIN or
+        HIST_ROTATED; results are identical."""
+        _check(_lib.gbt_ctx_set_hist_kernel(self.h, int(choice)))
 
     @property
     def torch_device(self):

@@ -30,6 +30,14 @@ def ctx(gbt):
     c.close()
 
 
+@pytest.fixture(params=["plain", "rotated"])
+def hist_kernel(request, gbt, ctx):
+    """Runs the test with each dense histogram kernel forced on the context."""
+    ctx.set_hist_kernel(ctx.HIST_PLAIN if request.param == "plain" else ctx.HIST_ROTATED)
+    yield request.param
+    ctx.set_hist_kernel(ctx.HIST_AUTO)
+
+
 def dense_case(seed, n, m, missing, dist="normal"):
     rng = np.random.default_rng(seed)
     if dist == "normal":
@@ -215,7 +223,7 @@ def test_sample_from_margins_matches_stored_gradients(gbt, ctx):
 
 
 # ------------------------------------------------------------ histograms
-def test_build_hist_and_subtraction(gbt, ctx):
+def test_build_hist_and_subtraction(gbt, ctx, hist_kernel):
     rng = np.random.default_rng(30)
     for (n, m, missing, sparse) in [(9000, 28, 0.0, False), (7001, 50, 0.2, False),
                                     (4000, 300, 0.03, True)]:
@@ -251,6 +259,46 @@ def test_build_hist_and_subtraction(gbt, ctx):
         assert not h[0].any()
         rest = np.setdiff1d(np.arange(n), A)
         assert same_bits(h[2], orc.build_hist(b, rest, q))
+
+
+@pytest.mark.parametrize("n,m,missing,max_bin,dist", [
+    (3001, 70, 0.0, 2, "normal"),      # 1-bit symbols, 32-feature groups
+    (3001, 70, 0.1, 2, "normal"),      # 2 bits with the null symbol
+    (2999, 41, 0.3, 6, "normal"),      # 3 bits
+    (4003, 37, 0.0, 20, "normal"),     # 5 bits
+    (4003, 19, 0.05, 100, "normal"),   # 7 bits
+    (5000, 7, 0.0, 1000, "normal"),    # 10 bits
+    (6001, 5, 0.1, 2560, "normal"),    # 12 bits, a 2560-bin feature
+])
+def test_build_hist_symbol_widths(gbt, ctx, hist_kernel, n, m, missing, max_bin, dist):
+    """Every dense symbol width the histogram kernel is specialised for, with
+    groups that start inside a word."""
+    rng = np.random.default_rng(33)
+    X = dense_case(34, n, m, missing, dist)
+    _, b, _, _ = oracle_quantize(X, max_bin)
+    mx = gbt.gbt_quantize(ctx, X, max_bin=max_bin)
+    tb = mx.info().total_bins
+    q = rng.integers(-2**41, 2**41, size=(n, 2)).astype(np.int64)
+    page = torch.from_numpy(mx.page(0).view(np.int32)).cuda()
+    qd = torch.from_numpy(q).cuda()
+    sel = np.sort(rng.choice(n, size=n // 3, replace=False)).astype(np.int32)
+    hist = torch.zeros((2, tb, 2), dtype=torch.int64, device="cuda")
+    gbt.gbt_build_hist(ctx, mx, page, qd, None, [(0, 0, n)], hist=hist[:1])
+    gbt.gbt_build_hist(ctx, mx, page, qd, torch.from_numpy(sel).cuda(), [(1, 0, len(sel))], hist=hist)
+    h = hist.cpu().numpy()
+    assert same_bits(h[0], orc.build_hist(b, np.arange(n), q))
+    assert same_bits(h[1], orc.build_hist(b, sel, q))
+
+
+def test_build_hist_rejects_oversized_feature(gbt, ctx):
+    X = dense_case(35, 4000, 3, 0.0, "normal")
+    mx = gbt.gbt_quantize(ctx, X, max_bin=3000)
+    assert mx.info().total_bins > 3 * 2560
+    q = torch.zeros((4000, 2), dtype=torch.int64, device="cuda")
+    page = torch.from_numpy(mx.page(0).view(np.int32)).cuda()
+    hist = torch.zeros((1, mx.info().total_bins, 2), dtype=torch.int64, device="cuda")
+    with pytest.raises(RuntimeError, match="bins"):
+        gbt.gbt_build_hist(ctx, mx, page, q, None, [(0, 0, 4000)], hist=hist)
 
 
 # ------------------------------------------------------------ split evaluation
@@ -349,7 +397,7 @@ def assert_same_trees(trees, margin, otrees, omargin):
 
 @pytest.mark.parametrize("cfg_id,n,n_trees", [(1, 10_000, 10), (2, 30_000, 4), (3, 60_000, 4),
                                                (5, 6_000, 3)])
-def test_train_trees_match_oracle(gbt, ctx, cfg_id, n, n_trees):
+def test_train_trees_match_oracle(gbt, ctx, hist_kernel, cfg_id, n, n_trees):
     cfg = datagen.CONFIGS[cfg_id]
     if cfg_id == 5:
         d = datagen.config5(n=n, m=400)
@@ -373,7 +421,7 @@ def test_out_of_core_equals_in_core(gbt, ctx):
     assert_same_trees(b[0], b[1], a[2], a[3])
 
 
-def test_out_of_core_sampled_matches_oracle(gbt, ctx):
+def test_out_of_core_sampled_matches_oracle(gbt, ctx, hist_kernel):
     cfg = datagen.TrainConfig("t", 0, 256, 6, 3, eta=0.1, f=0.3)
     d = datagen.config2(n=20_000)
     r = train_both(gbt, ctx, d["X"], d["y"], cfg, 3, page_rows=3000, home=gbt.HOME_PINNED_HOST)
@@ -381,7 +429,7 @@ def test_out_of_core_sampled_matches_oracle(gbt, ctx):
 
 
 @pytest.mark.parametrize("depth,n", [(0, 1000), (1, 65), (3, 1), (4, 63)])
-def test_degenerate_trees(gbt, ctx, depth, n):
+def test_degenerate_trees(gbt, ctx, hist_kernel, depth, n):
     cfg = datagen.TrainConfig("t", 1, 32, depth, 2, eta=0.5, f=0.5 if n > 10 else 1.0)
     d = datagen.config3(n=n, m=6)
     r = train_both(gbt, ctx, d["X"], d["y"], cfg, 2)
