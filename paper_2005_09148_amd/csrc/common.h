@@ -103,7 +103,7 @@ enum ScratchSlot {
     kScrSel,         // global ids of the sampled rows
     kScrGw,          // reweighted (g', h') in double
     kScrQ,           // fixed-point (q_g, q_h)
-    kScrRows, kScrRowsTmp, kScrPosition,
+    kScrRows, kScrRowsTmp, kScrPosition, kScrSlotA, kScrSlotB,
     kScrHistA, kScrHistB,
     kScrNodes,       // DevNode table
     kScrEvalNodes,   // EvalNode list
@@ -224,20 +224,25 @@ __device__ inline int32_t row_feature_bin(const uint32_t *__restrict__ row, cons
     return -1;
 }
 
-// Device node table entry used by the tree driver (heap order).
-struct DevNode {
+// Device node table entry used by the tree driver (heap order).  The split
+// record {split, feature, split_bin, default_left} is 16-byte aligned so
+// that the partition reads it with one load.
+struct __align__(16) DevNode {
     int64_t sum_g, sum_h;
     int64_t begin, end;
-    int32_t present;
     int32_t split;          // 1 if the node splits
     int32_t feature, split_bin;
     int32_t default_left;
+    int32_t present;
     int32_t left_child;     // node ids of the children (heap: 2i+1, 2i+2)
     int32_t right_child;
     int32_t pad0;
+    int64_t pleft;          // partition: left flags before begin (all slots)
+    int64_t nleft;          // partition: rows of the segment that go left
     double gain;
     int64_t left_g, left_h, right_g, right_h;
 };
+static_assert(sizeof(DevNode) % 16 == 0, "DevNode is read with 16-byte loads");
 
 // ---------------------------------------------------------------- scans
 // Exclusive prefix sum of n flags (bytes 0/1) or counts (uint32): out[i] for
@@ -247,9 +252,9 @@ gbt_status scan_u32(gbt_ctx *c, const uint32_t *in, int64_t n, int32_t *out);
 // Exclusive sums of the per-tile counts of n flags (tiles of 4096);
 // tile_off[ceil(n/4096)] = total.
 gbt_status scan_tiles_u8(gbt_ctx *c, const uint8_t *in, int64_t n, int32_t *tile_off);
-// The scan given the per-tile counts of its first pass (tile_cnt is
-// overwritten with the tile offsets).
-gbt_status scan_u8_from_tiles(gbt_ctx *c, const uint8_t *in, int64_t n, int32_t *tile_cnt, int32_t *out);
+// Exclusive sums of `tiles` per-tile counts, in place; tile_cnt[tiles]
+// receives the total.
+gbt_status scan_tile_counts(gbt_ctx *c, int32_t *tile_cnt, int64_t tiles);
 
 // ---------------------------------------------------------------- shared launches
 gbt_status launch_gradients(gbt_ctx *c, int32_t loss, const float *margin, const float *label,

@@ -139,15 +139,10 @@ gbt_status scan_tiles_u8(gbt_ctx *c, const uint8_t *in, int64_t n, int32_t *tile
     return GBT_OK;
 }
 
-gbt_status scan_u8_from_tiles(gbt_ctx *c, const uint8_t *in, int64_t n, int32_t *tile_cnt, int32_t *out)
+gbt_status scan_tile_counts(gbt_ctx *c, int32_t *tile_cnt, int64_t tiles)
 {
-    int64_t nb = (n + kScanTile - 1) / kScanTile;
-    k_scan_spine<<<1, 1024, 0, c->stream>>>(tile_cnt, nb, out + n);
+    k_scan_spine<<<1, 1024, 0, c->stream>>>(tile_cnt, tiles, tile_cnt + tiles);
     GBT_LAUNCHED();
-    if (nb > 0) {
-        k_scan_down<uint8_t><<<(unsigned)nb, kScanThreads, 0, c->stream>>>(in, n, tile_cnt, out);
-        GBT_LAUNCHED();
-    }
     return GBT_OK;
 }
 

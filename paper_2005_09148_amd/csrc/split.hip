@@ -250,93 +250,238 @@ gbt_status eval_impl(gbt_ctx *c, const gbt_matrix *mx, const int64_t *hist, cons
 }
 
 // ------------------------------------------------------------ partition
-// node of slot i: slot_node[i] when given, else position[rows[i]]
-__global__ void k_part_scatter(const int32_t *__restrict__ rows, int64_t n,
-                               const uint8_t *__restrict__ flags, const int32_t *__restrict__ P,
-                               int32_t *__restrict__ position, const int32_t *__restrict__ slot_node,
-                               const DevNode *__restrict__ nodes, int32_t *__restrict__ rows_out)
+// ------------------------------------------------------------ partition
+// Slots are processed in tiles of 4096, one 1024-thread block per tile; a
+// thread owns four consecutive slots, so its row ids, node ids and flags are
+// one vector load each, and the loads of the four slots are issued together.
+constexpr int kPartThreads = 1024;
+constexpr int kPartItems = 4;
+constexpr int kPartTile = kPartThreads * kPartItems;  // the scan's tile
+
+// Exclusive sum over a 1024-thread block; *total receives the block's sum.
+__device__ inline int32_t part_block_scan(int32_t v, int32_t *lds16, int32_t *total)
 {
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n) return;
-    int32_t r = rows[i];
-    int32_t nid = slot_node ? slot_node[i] : position[r];
-    if (nid < 0 || !nodes[nid].split) {
-        rows_out[i] = r;
-        return;
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    int32_t x = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int32_t y = __shfl_up(x, d, 64);
+        if (lane >= d) x += y;
     }
-    const DevNode &nd = nodes[nid];
-    int64_t b = nd.begin, e = nd.end;
-    int64_t nl = (int64_t)P[e] - P[b];
-    int64_t pl = (int64_t)P[i] - P[b];
-    int64_t dest;
-    int32_t child;
-    if (flags[i]) {
-        dest = b + pl;
-        child = nd.left_child;
-    } else {
-        dest = b + nl + (i - b - pl);
-        child = nd.right_child;
+    if (lane == 63) lds16[wid] = x;
+    __syncthreads();
+    int32_t off = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < kPartThreads / 64; ++w) {
+        const int32_t t = lds16[w];
+        off += w < wid ? t : 0;
+        tot += t;
     }
-    rows_out[dest] = r;
-    position[r] = child;
+    *total = tot;
+    return x - v + off;
 }
 
-// Left flags of one tile of 4096 slots per block (16 slots per thread, a
-// block stride apart so that loads and stores coalesce) and the count of
-// each tile (the first pass of the scan).
-__global__ void __launch_bounds__(256)
+// The four slots' row ids and node ids (node of slot i: slot_node[i] when
+// given, else position[rows[i]]); slots past n get node -1.
+__device__ inline void part_load(const int32_t *__restrict__ rows, const int32_t *__restrict__ position,
+                                 const int32_t *__restrict__ slot_node, int64_t i0, int64_t n,
+                                 int32_t r[kPartItems], int32_t nid[kPartItems])
+{
+    if (i0 + kPartItems <= n) {
+        const int4 rv = *(const int4 *)(rows + i0);
+        r[0] = rv.x, r[1] = rv.y, r[2] = rv.z, r[3] = rv.w;
+        if (slot_node) {
+            const int4 nv = *(const int4 *)(slot_node + i0);
+            nid[0] = nv.x, nid[1] = nv.y, nid[2] = nv.z, nid[3] = nv.w;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < kPartItems; ++k) {
+            r[k] = i0 + k < n ? rows[i0 + k] : 0;
+            if (slot_node) nid[k] = i0 + k < n ? slot_node[i0 + k] : -1;
+        }
+    }
+    if (!slot_node) {
+#pragma unroll
+        for (int k = 0; k < kPartItems; ++k) nid[k] = i0 + k < n ? position[r[k]] : -1;
+    }
+}
+
+// Left flags of each slot and the count of each tile (the scan's first pass).
+__global__ void __launch_bounds__(kPartThreads)
     k_part_flags_tiles(const int32_t *__restrict__ rows, int64_t n, const uint32_t *__restrict__ page, Geo geo,
                        const int32_t *__restrict__ position, const int32_t *__restrict__ slot_node,
                        const DevNode *__restrict__ nodes, uint8_t *__restrict__ flags,
                        int32_t *__restrict__ tile_cnt)
 {
-    __shared__ int32_t red[4];
-    const int64_t base = (int64_t)blockIdx.x * 4096 + threadIdx.x;
+    __shared__ int32_t red[kPartThreads / 64];
+    const int64_t i0 = (int64_t)blockIdx.x * kPartTile + (int64_t)threadIdx.x * kPartItems;
+    int32_t r[kPartItems], nid[kPartItems];
+    part_load(rows, position, slot_node, i0, n, r, nid);
+    int4 rec[kPartItems];  // {split, feature, split_bin, default_left}
+#pragma unroll
+    for (int k = 0; k < kPartItems; ++k)
+        rec[k] = nid[k] >= 0 ? *(const int4 *)&nodes[nid[k]].split : make_int4(0, 0, 0, 0);
+    uint32_t f4 = 0;
     int32_t cnt = 0;
-    for (int k = 0; k < 16; ++k) {
-        const int64_t i = base + k * 256;
-        if (i >= n) break;
-        const int32_t r = rows[i];
-        const int32_t nid = slot_node ? slot_node[i] : position[r];
-        uint8_t f = 0;
-        if (nid >= 0 && nodes[nid].split) {
-            const DevNode &nd = nodes[nid];
-            const int32_t b = row_feature_bin(page + (int64_t)r * geo.row_words, geo, nd.feature);
-            f = (b < 0) ? (uint8_t)(nd.default_left != 0) : (uint8_t)(b < nd.split_bin);
+#pragma unroll
+    for (int k = 0; k < kPartItems; ++k) {
+        uint32_t f = 0;
+        if (rec[k].x) {
+            const int32_t b = row_feature_bin(page + (int64_t)r[k] * geo.row_words, geo, rec[k].y);
+            f = (b < 0) ? (rec[k].w != 0 ? 1u : 0u) : (b < rec[k].z ? 1u : 0u);
         }
-        flags[i] = f;
-        cnt += f;
+        f4 |= f << (8 * k);
+        cnt += (int32_t)f;
+    }
+    if (i0 + kPartItems <= n) {
+        *(uint32_t *)(flags + i0) = f4;
+    } else {
+#pragma unroll
+        for (int k = 0; k < kPartItems; ++k)
+            if (i0 + k < n) flags[i0 + k] = (uint8_t)((f4 >> (8 * k)) & 1u);
     }
     for (int d = 32; d > 0; d >>= 1) cnt += __shfl_xor(cnt, d, 64);
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = cnt;
     __syncthreads();
-    if (threadIdx.x == 0) tile_cnt[blockIdx.x] = red[0] + red[1] + red[2] + red[3];
+    if (threadIdx.x == 0) {
+        int32_t t = 0;
+        for (int w = 0; w < kPartThreads / 64; ++w) t += red[w];
+        tile_cnt[blockIdx.x] = t;
+    }
+}
+
+// Left flags before slot x: the tile's offset plus the flags of the tile
+// before x, summed by the 256 threads of the block (16 flags each).
+constexpr int kBoundThreads = 256;
+
+__device__ inline uint32_t byte_sum4(uint32_t v)
+{
+    return ((v & 0x01010101u) * 0x01010101u) >> 24;  // four 0/1 bytes
+}
+
+__device__ inline int64_t part_prefix(const uint8_t *__restrict__ flags, const int32_t *__restrict__ tile_off,
+                                      int64_t x, int32_t *lds4)
+{
+    const int64_t t = x / kPartTile, s = t * kPartTile;
+    const int64_t j = s + (int64_t)threadIdx.x * 16;
+    uint32_t c = 0;
+    if (j + 16 <= x) {
+        const uint4 v = *(const uint4 *)(flags + j);
+        c = byte_sum4(v.x) + byte_sum4(v.y) + byte_sum4(v.z) + byte_sum4(v.w);
+    } else {
+        for (int64_t k = j; k < x; ++k) c += flags[k];
+    }
+    for (int d = 32; d > 0; d >>= 1) c += __shfl_xor(c, d, 64);
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) lds4[threadIdx.x >> 6] = (int32_t)c;
+    __syncthreads();
+    return (int64_t)tile_off[t] + lds4[0] + lds4[1] + lds4[2] + lds4[3];
+}
+
+// For every splitting node of the list: the left flags before its segment
+// and the count of its rows that go left.  One block per node.
+__global__ void __launch_bounds__(kBoundThreads)
+    k_part_bounds(const EvalNode *__restrict__ list, const int32_t *__restrict__ n_list_d, int32_t n_list,
+                  DevNode *__restrict__ nodes, const uint8_t *__restrict__ flags,
+                  const int32_t *__restrict__ tile_off)
+{
+    __shared__ int32_t lds4[kBoundThreads / 64];
+    const int32_t count = n_list_d ? *n_list_d : n_list;
+    if ((int32_t)blockIdx.x >= count) return;
+    const int32_t nid = list ? list[blockIdx.x].heap : (int32_t)blockIdx.x;
+    DevNode &d = nodes[nid];
+    if (!d.split) return;
+    const int64_t pb = part_prefix(flags, tile_off, d.begin, lds4);
+    const int64_t pe = part_prefix(flags, tile_off, d.end, lds4);
+    if (threadIdx.x == 0) {
+        d.pleft = pb;
+        d.nleft = pe - pb;
+    }
+}
+
+// Stable scatter: the slot's exclusive left count comes from the tile offset
+// and a block scan; a splitting node's left rows go to the front of its
+// segment, the others after them, both in slot order.
+__global__ void __launch_bounds__(kPartThreads)
+    k_part_scatter(const int32_t *__restrict__ rows, int64_t n, const uint8_t *__restrict__ flags,
+                   const int32_t *__restrict__ tile_off, const int32_t *__restrict__ position,
+                   int32_t *__restrict__ position_out,
+                   const int32_t *__restrict__ slot_node, int32_t *__restrict__ slot_node_out,
+                   const DevNode *__restrict__ nodes, int32_t *__restrict__ rows_out)
+{
+    __shared__ int32_t lds16[kPartThreads / 64];
+    const int64_t i0 = (int64_t)blockIdx.x * kPartTile + (int64_t)threadIdx.x * kPartItems;
+    int32_t r[kPartItems], nid[kPartItems];
+    part_load(rows, position, slot_node, i0, n, r, nid);
+    uint32_t f4 = 0;
+    if (i0 + kPartItems <= n) {
+        f4 = *(const uint32_t *)(flags + i0);
+    } else {
+#pragma unroll
+        for (int k = 0; k < kPartItems; ++k)
+            if (i0 + k < n) f4 |= (uint32_t)flags[i0 + k] << (8 * k);
+    }
+    const int32_t mine = (int32_t)((f4 & 1u) + ((f4 >> 8) & 1u) + ((f4 >> 16) & 1u) + ((f4 >> 24) & 1u));
+    int32_t total;
+    int64_t P = (int64_t)tile_off[blockIdx.x] + part_block_scan(mine, lds16, &total);
+#pragma unroll
+    for (int k = 0; k < kPartItems; ++k) {
+        const int64_t i = i0 + k;
+        const uint32_t f = (f4 >> (8 * k)) & 1u;
+        if (i < n) {
+            int64_t dest = i;
+            int32_t child = nid[k];
+            if (nid[k] >= 0) {
+                const DevNode &nd = nodes[nid[k]];
+                const int4 rec = *(const int4 *)&nd.split;
+                if (rec.x) {
+                    const int64_t pl = P - nd.pleft;
+                    if (f) {
+                        dest = nd.begin + pl;
+                        child = nd.left_child;
+                    } else {
+                        dest = nd.begin + nd.nleft + (i - nd.begin - pl);
+                        child = nd.right_child;
+                    }
+                    if (position_out) position_out[r[k]] = child;
+                }
+            }
+            rows_out[dest] = r[k];
+            if (slot_node_out) slot_node_out[dest] = child;
+        }
+        P += f;
+    }
 }
 
 gbt_status partition_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int32_t *rows,
-                          int64_t n, int32_t *position, const int32_t *slot_node,
-                          const DevNode *nodes, int32_t *rows_out, int32_t **P_out)
+                          int64_t n, int32_t *position, const int32_t *slot_node, int32_t *slot_node_out,
+                          DevNode *nodes, const EvalNode *list, const int32_t *n_list_d, int32_t n_list,
+                          int32_t *rows_out)
 {
-    if (n == 0) {
-        *P_out = nullptr;
-        return GBT_OK;
-    }
+    if (n == 0) return GBT_OK;
+    GBT_CHECK(n < ((int64_t)1 << 31) - 1, "partition of %lld rows (limit 2^31-2)", (long long)n);
     uint8_t *flags;
-    int32_t *P;
-    GBT_TRY(scratch_t(c, kScrPartFlags, (size_t)n, &flags));
-    GBT_TRY(scratch_t(c, kScrPartPos, (size_t)n + 1, &P));
+    GBT_TRY(scratch_t(c, kScrPartFlags, (size_t)n + 16, &flags));
     Geo geo = geo_of(mx);
-    unsigned grid = (unsigned)((n + 255) / 256);
-    const int64_t tiles = (n + 4095) / 4096;
+    const int64_t tiles = (n + kPartTile - 1) / kPartTile;
     int32_t *tile_off;
     GBT_TRY(scratch_t(c, kScrScan, (size_t)tiles + 1, &tile_off));
-    k_part_flags_tiles<<<(unsigned)tiles, 256, 0, c->stream>>>(rows, n, page, geo, position, slot_node, nodes,
-                                                               flags, tile_off);
+    k_part_flags_tiles<<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(rows, n, page, geo, position, slot_node,
+                                                                       nodes, flags, tile_off);
     GBT_LAUNCHED();
-    GBT_TRY(scan_u8_from_tiles(c, flags, n, tile_off, P));
-    k_part_scatter<<<grid, 256, 0, c->stream>>>(rows, n, flags, P, position, slot_node, nodes, rows_out);
+    GBT_TRY(scan_tile_counts(c, tile_off, tiles));
+    if (n_list > 0) {
+        k_part_bounds<<<(unsigned)n_list, kBoundThreads, 0, c->stream>>>(list, n_list_d, n_list, nodes, flags,
+                                                                         tile_off);
+        GBT_LAUNCHED();
+    }
+    // with slot nodes kept the caller derives positions at the end; without
+    // them, positions are the partition's output
+    k_part_scatter<<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(
+        rows, n, flags, tile_off, position, slot_node_out ? nullptr : position, slot_node, slot_node_out, nodes,
+        rows_out);
     GBT_LAUNCHED();
-    *P_out = P;
     return GBT_OK;
 }
 
@@ -394,6 +539,8 @@ gbt_status gbt_partition(gbt_ctx *c, const gbt_matrix *layout, const uint32_t *p
     GBT_CHECK(c && layout && page_d && split_h && seg_h && child_h && rows_d && rows_tmp_d && position_d,
               "gbt_partition: NULL argument");
     GBT_CHECK(n_nodes >= 0 && n_rows >= 0, "negative sizes");
+    GBT_CHECK(((uintptr_t)rows_d & 15) == 0 && ((uintptr_t)rows_tmp_d & 15) == 0,
+              "gbt_partition: rows_d and rows_tmp_d must be 16-byte aligned");
     for (int32_t k = 0; k < n_nodes; ++k) {
         GBT_CHECK(seg_h[k].begin >= 0 && seg_h[k].begin <= seg_h[k].end && seg_h[k].end <= n_rows,
                   "segment %d outside [0, n_rows]", k);
@@ -428,17 +575,18 @@ gbt_status gbt_partition(gbt_ctx *c, const gbt_matrix *layout, const uint32_t *p
         k_fill_slot_node<<<(unsigned)((n_rows + 255) / 256), 256, 0, c->stream>>>(segs_d, n_nodes, slot_node, n_rows);
         GBT_LAUNCHED();
     }
-    int32_t *P = nullptr;
-    GBT_TRY(partition_impl(c, layout, page_d, rows_d, n_rows, position_d, slot_node, nodes_d, rows_tmp_d, &P));
+    GBT_TRY(partition_impl(c, layout, page_d, rows_d, n_rows, position_d, slot_node, nullptr, nodes_d, nullptr,
+                           nullptr, n_nodes, rows_tmp_d));
     if (n_rows)
         GBT_HIP(hipMemcpyAsync(rows_d, rows_tmp_d, (size_t)n_rows * 4, hipMemcpyDeviceToDevice, c->stream));
-    std::vector<int32_t> Ph(n_rows + 1, 0);
-    if (P) GBT_HIP(hipMemcpyAsync(Ph.data(), P, (size_t)(n_rows + 1) * 4, hipMemcpyDeviceToHost, c->stream));
+    if (n_rows && n_nodes)
+        GBT_HIP(hipMemcpyAsync(nodes.data(), nodes_d, (size_t)n_nodes * sizeof(DevNode), hipMemcpyDeviceToHost,
+                               c->stream));
     GBT_HIP(hipStreamSynchronize(c->stream));
     if (seg_out_h) {
         for (int32_t k = 0; k < n_nodes; ++k) {
             int64_t b = seg_h[k].begin, e = seg_h[k].end;
-            int64_t nl = split_h[k].valid ? (int64_t)Ph[e] - Ph[b] : e - b;
+            int64_t nl = (split_h[k].valid && n_rows) ? nodes[k].nleft : e - b;
             seg_out_h[2 * k] = {child_h[2 * k], 0, b, b + nl};
             seg_out_h[2 * k + 1] = {child_h[2 * k + 1], 0, b + nl, e};
         }

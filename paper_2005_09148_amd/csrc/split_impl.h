@@ -35,11 +35,17 @@ gbt_status eval_impl(gbt_ctx *c, const gbt_matrix *mx, const int64_t *hist, cons
                      int32_t n_nodes, const EvalParams &ep, gbt_split *out_d,
                      const int32_t *n_nodes_d = nullptr, DevNode *decide = nullptr);
 // Stable partition of rows[0, n) by each slot's node (slot_node[i], or
-// position[rows[i]] when slot_node is NULL).  rows_out receives the new
-// order, position[row] the child id.  *P receives the exclusive scan of the
-// left flags (n+1 entries, device).
+// position[rows[i]] when slot_node is NULL): the rows of every splitting
+// node go left or right within its segment.  rows_out receives the new
+// order, slot_node_out (if not NULL) each new slot's node; when
+// slot_node_out is NULL, position[row] receives the child of every row of a
+// splitting node.  nodes[id].pleft / nleft receive the
+// counts behind the child segments.  The nodes that may split are listed in
+// `list` (heap ids, count *n_list_d, at most n_list) or, when list is NULL,
+// are nodes[0, n_list).
 gbt_status partition_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int32_t *rows,
-                          int64_t n, int32_t *position, const int32_t *slot_node,
-                          const DevNode *nodes, int32_t *rows_out, int32_t **P);
+                          int64_t n, int32_t *position, const int32_t *slot_node, int32_t *slot_node_out,
+                          DevNode *nodes, const EvalNode *list, const int32_t *n_list_d, int32_t n_list,
+                          int32_t *rows_out);
 
 }  // namespace gbt

@@ -233,12 +233,12 @@ __global__ void k_tree_init(DevNode *__restrict__ nodes, int32_t n_nodes, long l
     nodes[i] = d;
 }
 
-__global__ void k_rows_init(int32_t *__restrict__ rows, int32_t *__restrict__ position, int64_t R)
+__global__ void k_rows_init(int32_t *__restrict__ rows, int32_t *__restrict__ slot_node, int64_t R)
 {
     int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= R) return;
     rows[i] = (int32_t)i;
-    position[i] = 0;
+    slot_node[i] = 0;
 }
 
 // Exclusive scan across a 1024-thread block; *total receives the sum.
@@ -264,7 +264,7 @@ __device__ inline int32_t scan1024(int32_t v, int32_t *lds16, int32_t *total)
 }
 
 // After a level's partition (one block of 1024 threads): the child segments
-// of every split node from the partition's left counts P, then, when `plan`
+// of every split node from the partition's left count (nleft), then, when `plan`
 // is set, the plan of the next level: the list of present children in heap
 // order with their histogram slots, and for each split parent the smaller
 // child to build (chunked into work items) with the larger one as parent
@@ -275,7 +275,7 @@ constexpr int64_t kMinChunk = 1024;
 
 __global__ void __launch_bounds__(1024)
     k_plan_level(const EvalNode *__restrict__ cur, const int32_t *__restrict__ n_cur_d,
-                 DevNode *__restrict__ nodes, const int32_t *__restrict__ P, int32_t plan, int32_t items,
+                 DevNode *__restrict__ nodes, int32_t plan, int32_t items,
                  EvalNode *__restrict__ next, int32_t *__restrict__ n_next_d, HistWork *__restrict__ work,
                  int32_t *__restrict__ n_work_d, HistReduce *__restrict__ red, int32_t *__restrict__ n_red_d,
                  unsigned long long *__restrict__ stat)
@@ -285,7 +285,7 @@ __global__ void __launch_bounds__(1024)
     for (int32_t t = threadIdx.x; t < n_cur; t += 1024) {
         const DevNode d = nodes[cur[t].heap];
         if (!d.split) continue;
-        const int64_t nl = (int64_t)P[d.end] - P[d.begin];
+        const int64_t nl = d.nleft;
         DevNode &L = nodes[d.left_child];
         DevNode &Rn = nodes[d.right_child];
         L.present = 1;
@@ -407,12 +407,15 @@ __global__ void k_leaves(const DevNode *__restrict__ nodes, int32_t n_nodes, int
                          : make_uint2(0u, 0u);
 }
 
-// Margin update from the final node of each training row (no sampling).
-__global__ void k_margin_pos(float *__restrict__ margin, const int32_t *__restrict__ position,
-                             const float *__restrict__ leaf, int64_t n)
+// Margin update from the final node of each training slot (no sampling:
+// the slots hold every row once).
+__global__ void k_margin_slots(float *__restrict__ margin, const int32_t *__restrict__ rows,
+                               const int32_t *__restrict__ slot_node, const float *__restrict__ leaf, int64_t n)
 {
     int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n) margin[i] = margin[i] + leaf[position[i]];
+    if (i >= n) return;
+    const int32_t r = rows[i];
+    margin[r] = margin[r] + leaf[slot_node[i]];
 }
 
 // Row staging for the tree walks: the block's 256 consecutive rows are read
@@ -674,14 +677,17 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     // ---- Alg. 1 on the sampled page, level by level.  Levels below the root
     // are planned on the device: no host round trip inside the tree.
     DevNode *nodes;
-    int32_t *rows, *rows_tmp, *position;
+    int32_t *rows, *rows_tmp;
     float *leaf;
     gbt_split *splits_d;
     GBT_TRY(scratch_t(c, kScrNodes, (size_t)NN, &nodes));
     GBT_TRY(scratch_t(c, kScrLeaf, (size_t)NN, &leaf));
     GBT_TRY(scratch_t(c, kScrRows, (size_t)std::max<int64_t>(R, 1), &rows));
     GBT_TRY(scratch_t(c, kScrRowsTmp, (size_t)std::max<int64_t>(R, 1), &rows_tmp));
-    GBT_TRY(scratch_t(c, kScrPosition, (size_t)std::max<int64_t>(R, 1), &position));
+    // each slot's node, permuted with the rows
+    int32_t *slot_node, *slot_tmp;
+    GBT_TRY(scratch_t(c, kScrSlotA, (size_t)std::max<int64_t>(R, 1), &slot_node));
+    GBT_TRY(scratch_t(c, kScrSlotB, (size_t)std::max<int64_t>(R, 1), &slot_tmp));
     const int32_t max_level_nodes =
         (int32_t)std::min<int64_t>((int64_t)1 << std::max(D - 1, 0), std::max<int64_t>(R, 1));
     GBT_TRY(scratch_t(c, kScrSplits, (size_t)max_level_nodes, &splits_d));
@@ -731,7 +737,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     k_tree_init<<<blocks(NN), 256, 0, c->stream>>>(nodes, NN, so.root_g, so.root_h, R);
     GBT_LAUNCHED();
     if (R) {
-        k_rows_init<<<blocks(R), 256, 0, c->stream>>>(rows, position, R);
+        k_rows_init<<<blocks(R), 256, 0, c->stream>>>(rows, slot_node, R);
         GBT_LAUNCHED();
     }
     EvalParams ep{p->lambda, p->gamma, p->min_child_weight, so.e_g, so.e_h};
@@ -746,12 +752,13 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         const int32_t maxn = (int32_t)std::min<int64_t>((int64_t)1 << d, max_level_nodes);
         mark = timer_begin(c, kPhSplit);
         GBT_TRY(eval_impl(c, mx, histA, evA, maxn, ep, splits_d, cntA, nodes));
-        int32_t *P = nullptr;
-        GBT_TRY(partition_impl(c, mx, so.page, rows, R, position, nullptr, nodes, rows_tmp, &P));
+        GBT_TRY(partition_impl(c, mx, so.page, rows, R, nullptr, slot_node, slot_tmp, nodes, evA, cntA, maxn,
+                               rows_tmp));
         std::swap(rows, rows_tmp);
+        std::swap(slot_node, slot_tmp);
         const bool plan_next = d + 1 < D && R > 0;
-        if (P) {
-            k_plan_level<<<1, 1024, 0, c->stream>>>(evA, cntA, nodes, P, plan_next ? 1 : 0, items, evB, cntB,
+        if (R > 0) {
+            k_plan_level<<<1, 1024, 0, c->stream>>>(evA, cntA, nodes, plan_next ? 1 : 0, items, evB, cntB,
                                                     work_d, cnt + 2, red_d, cnt + 3, stat);
             GBT_LAUNCHED();
         }
@@ -775,7 +782,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     GBT_LAUNCHED();
     if (so.alias) {
         if (n) {
-            k_margin_pos<<<blocks(n), 256, 0, c->stream>>>(margin, position, leaf, n);
+            k_margin_slots<<<blocks(n), 256, 0, c->stream>>>(margin, rows, slot_node, leaf, n);
             GBT_LAUNCHED();
         }
     } else {
