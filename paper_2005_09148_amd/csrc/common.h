@@ -75,6 +75,10 @@ struct gbt_ctx {
         size_t bytes = 0;
     };
     std::vector<Scratch> scratch;   // reusable workspaces, by slot id
+    // pinned host memory the kernels write results into (read after a sync)
+    void *hio = nullptr;
+    void *hio_d = nullptr;
+    size_t hio_bytes = 0;
 };
 
 namespace gbt {
@@ -90,6 +94,10 @@ gbt_status dev_alloc(gbt_ctx *c, size_t bytes, void **p);
 void dev_free(gbt_ctx *c, void *p, size_t bytes);
 // Grow-only workspace in slot `slot` of the context.
 gbt_status scratch(gbt_ctx *c, int slot, size_t bytes, void **p);
+// Grow-only pinned host buffer that kernels write into: *host for the host,
+// *dev for kernels.  The stream must not be using it (the call syncs
+// before growing).
+gbt_status host_io(gbt_ctx *c, size_t bytes, void **host, void **dev);
 gbt_status set_device(gbt_ctx *c);
 
 enum ScratchSlot {
@@ -160,6 +168,10 @@ struct gbt_matrix {
     int32_t *bin_ptr_d = nullptr;       // m+1 global bin offsets (cut_ptr[j] + j)
     std::vector<int32_t> bin_ptr_h;
     std::vector<GbtPage> pages;
+    // the histogram kernel's feature groups on the device, cached per kernel kind
+    mutable void *groups_d = nullptr;
+    mutable size_t groups_bytes = 0;
+    mutable int32_t groups_kind = -1;
 };
 
 namespace gbt {

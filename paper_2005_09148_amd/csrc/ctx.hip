@@ -60,6 +60,23 @@ void dev_free(gbt_ctx *c, void *p, size_t bytes)
     c->used -= bytes;
 }
 
+gbt_status host_io(gbt_ctx *c, size_t bytes, void **host, void **dev)
+{
+    if (c->hio_bytes < bytes) {
+        GBT_HIP(hipStreamSynchronize(c->stream));
+        if (c->hio) GBT_HIP(hipHostFree(c->hio));
+        c->hio = c->hio_d = nullptr;
+        c->hio_bytes = 0;
+        const size_t sz = std::max<size_t>(bytes, 1 << 16);
+        GBT_HIP(hipHostMalloc(&c->hio, sz, hipHostMallocMapped | hipHostMallocCoherent));
+        GBT_HIP(hipHostGetDevicePointer(&c->hio_d, c->hio, 0));
+        c->hio_bytes = sz;
+    }
+    *host = c->hio;
+    *dev = c->hio_d;
+    return GBT_OK;
+}
+
 gbt_status scratch(gbt_ctx *c, int slot, size_t bytes, void **p)
 {
     if ((int)c->scratch.size() <= slot) c->scratch.resize(slot + 1);
@@ -169,6 +186,7 @@ gbt_status gbt_ctx_destroy(gbt_ctx *c)
     (void)hipStreamSynchronize(c->stream);
     (void)hipStreamSynchronize(c->side);
     for (auto &s : c->scratch) dev_free(c, s.p, s.bytes);
+    if (c->hio) (void)hipHostFree(c->hio);
     for (auto e : c->events) (void)hipEventDestroy(e);
     (void)hipStreamDestroy(c->side);
     delete c;

@@ -930,6 +930,7 @@ gbt_status gbt_matrix_free(gbt_matrix *mx)
     dev_free(c, mx->cut_ptr_d, (size_t)(mx->m + 1) * 4);
     dev_free(c, mx->cut_values_d, std::max<size_t>(mx->cut_values_h.size(), 1) * 4);
     dev_free(c, mx->bin_ptr_d, (size_t)(mx->m + 1) * 4);
+    if (mx->groups_d) dev_free(c, mx->groups_d, mx->groups_bytes);
     delete mx;
     return GBT_OK;
 }

@@ -149,6 +149,10 @@ __global__ void __launch_bounds__(kEvalThreads)
 {
     __shared__ EvalCand wbest[kEvalThreads / 64];
     if (n_nodes_d && (int32_t)blockIdx.y >= *n_nodes_d) return;
+    if (ep.e_dev) {
+        ep.e_g = ep.e_dev[0];
+        ep.e_h = ep.e_dev[1];
+    }
     const EvalNode nd = nodes[blockIdx.y];
     const int wid = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const longlong2 *h = hist + (int64_t)nd.slot * total_bins;
@@ -514,7 +518,7 @@ gbt_status gbt_eval_splits(gbt_ctx *c, const gbt_matrix *layout, const int64_t *
     GBT_TRY(scratch_t(c, kScrEvalNodes, (size_t)n_nodes, &nodes_d));
     GBT_HIP(hipMemcpyAsync(nodes_d, nodes.data(), nodes.size() * sizeof(EvalNode), hipMemcpyHostToDevice,
                            c->stream));
-    EvalParams ep{tp->lambda, tp->gamma, tp->min_child_weight, exp_g, exp_h};
+    EvalParams ep{tp->lambda, tp->gamma, tp->min_child_weight, exp_g, exp_h, nullptr};
     GBT_TRY(eval_impl(c, layout, hist_d, nodes_d, n_nodes, ep, out_d));
     GBT_HIP(hipStreamSynchronize(c->stream));
     return GBT_OK;

@@ -12,6 +12,7 @@ struct EvalParams {
     double mcw;
     int32_t e_g;
     int32_t e_h;
+    const int32_t *e_dev;  // when set, {e_g, e_h} are read from device memory
 };
 
 struct EvalNode {

@@ -133,12 +133,20 @@ struct SampleOut {
     SampleState *st = nullptr;
 };
 
+// One int32 from device memory into the pinned host buffer.
+__global__ void k_to_host_i32(const int32_t *__restrict__ src, int32_t *__restrict__ dst)
+{
+    if (threadIdx.x == 0) *dst = *src;
+}
+
 // Alg. 7: g' <- Sample(g); AllocateOnGPU(sampled_page); Compact each page.
 // st_ready: the caller has initialized st and folded the maximum of r into
-// it while computing the gradients.
+// it while computing the gradients.  read_state: copy the threshold,
+// exponents and root sums to the host (o->T ... o->root_h); otherwise they
+// stay in o->st on the device.
 gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, const float *margin,
                       const float *label, const gbt_sample_params &sp, Buffers &bufs, SampleOut *o,
-                      double *h2d_bytes, SampleState *st_ready = nullptr)
+                      double *h2d_bytes, SampleState *st_ready = nullptr, bool read_state = true)
 {
     const int64_t n = mx->n_rows;
     GBT_CHECK(sp.f > 0.0 && sp.f <= 1.0, "sampling fraction %g outside (0, 1]", sp.f);
@@ -174,10 +182,13 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
         // with f = 1 the state keeps T = 0: every row is kept with weight 1
         GBT_TRY(mvs_select(c, src, kind, nullptr, n, sp.mvs_lambda, st, sp.seed, sp.iteration, 0, keep));
         GBT_TRY(keep_tile_offsets(c, keep, n, tile_off));
-        int32_t R32 = 0;
-        GBT_HIP(hipMemcpyAsync(&R32, tile_off + ntiles, 4, hipMemcpyDeviceToHost, c->stream));
+        // the sample size sizes the buffers below: one round trip
+        void *hio, *hio_d;
+        GBT_TRY(host_io(c, 64, &hio, &hio_d));
+        k_to_host_i32<<<1, 64, 0, c->stream>>>(tile_off + ntiles, (int32_t *)hio_d);
+        GBT_LAUNCHED();
         GBT_HIP(hipStreamSynchronize(c->stream));
-        o->R = R32;
+        o->R = *(volatile int32_t *)hio;
         size_t rb = (size_t)mx->row_words * 4;
         uint32_t *spage;
         GBT_TRY(bufs.get(kScrSampled, (size_t)std::max<int64_t>(o->R, 1) * rb, (void **)&spage));
@@ -195,6 +206,7 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
     }
     GBT_TRY(bufs.get(kScrQ, (size_t)std::max<int64_t>(o->R, 1) * 16, (void **)&o->q));
     GBT_TRY(fixed_point(c, o->gw, o->R, st, o->q, fx_max_done));
+    if (!read_state) return GBT_OK;
     SampleState hst;
     GBT_HIP(hipMemcpyAsync(&hst, st, sizeof(SampleState), hipMemcpyDeviceToHost, c->stream));
     GBT_HIP(hipStreamSynchronize(c->stream));
@@ -214,23 +226,40 @@ __global__ void k_zero_counter(unsigned long long *p)
     if (threadIdx.x < kUpdCounters) p[threadIdx.x] = 0ull;
 }
 
-__global__ void k_tree_init(DevNode *__restrict__ nodes, int32_t n_nodes, long long rg, long long rh,
-                            int64_t R)
+// The node table, the root (its sums from the sampling state), the root
+// level list and counts, and the root histogram's work: R rows in chunks of
+// `chunk` (n_root items) summed into slot 0.
+__global__ void k_tree_init(DevNode *__restrict__ nodes, int32_t n_nodes, const SampleState *__restrict__ st,
+                            int64_t R, EvalNode *__restrict__ level, int32_t *__restrict__ cnt,
+                            HistWork *__restrict__ work, HistReduce *__restrict__ red, int64_t chunk,
+                            int32_t n_root)
 {
     int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n_nodes) return;
-    DevNode d;
-    memset(&d, 0, sizeof(d));
-    d.left_child = 2 * i + 1;
-    d.right_child = 2 * i + 2;
-    if (i == 0) {
-        d.present = 1;
-        d.sum_g = rg;
-        d.sum_h = rh;
-        d.begin = 0;
-        d.end = R;
+    const long long rg = (long long)fold_sum(st->root_g), rh = (long long)fold_sum(st->root_h);
+    if (i < n_nodes) {
+        DevNode d;
+        memset(&d, 0, sizeof(d));
+        d.left_child = 2 * i + 1;
+        d.right_child = 2 * i + 2;
+        if (i == 0) {
+            d.present = 1;
+            d.sum_g = rg;
+            d.sum_h = rh;
+            d.begin = 0;
+            d.end = R;
+        }
+        nodes[i] = d;
     }
-    nodes[i] = d;
+    if (i < n_root) {
+        const int64_t b = (int64_t)i * chunk;
+        work[i] = {b, b + chunk < R ? b + chunk : R, i, 0};
+    }
+    if (i == 0) {
+        level[0] = {rg, rh, 0, 0};
+        cnt[0] = 1;
+        cnt[1] = cnt[2] = cnt[3] = 0;
+        red[0] = {0, 0, n_root, -1, -1, 0};
+    }
 }
 
 __global__ void k_rows_init(int32_t *__restrict__ rows, int32_t *__restrict__ slot_node, int64_t R)
@@ -395,16 +424,74 @@ __device__ inline float leaf_of(long long Qg, long long Qh, int32_t eg, int32_t 
 
 // Leaf values, and the compact form of the tree used by the row walk:
 // {feature, split_bin << 2 | default_left << 1 | splits} per node.
-__global__ void k_leaves(const DevNode *__restrict__ nodes, int32_t n_nodes, int32_t eg, int32_t eh,
+__global__ void k_leaves(const DevNode *__restrict__ nodes, int32_t n_nodes, const int32_t *__restrict__ e_dev,
                          double lambda, double eta, float *__restrict__ leaf, uint2 *__restrict__ compact)
 {
     int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n_nodes) return;
+    const int32_t eg = e_dev[0], eh = e_dev[1];
     const DevNode d = nodes[i];
     leaf[i] = (d.present && !d.split) ? leaf_of(d.sum_g, d.sum_h, eg, eh, lambda, eta) : 0.0f;
     compact[i] = d.split ? make_uint2((uint32_t)d.feature, ((uint32_t)d.split_bin << 2) |
                                                                ((d.default_left ? 1u : 0u) << 1) | 1u)
                          : make_uint2(0u, 0u);
+}
+
+// What the host reads after a tree, written by the device into pinned memory.
+struct TreeResult {
+    unsigned long long updates;     // histogram updates (the counters folded)
+    unsigned long long rows_built;  // rows streamed below the root
+    unsigned long long partials;    // partial histograms written below the root
+    long long T;
+    int32_t e_key, e_g, e_h;
+    uint32_t bad;
+    gbt_node nodes[1];  // n_nodes entries
+};
+
+// The tree in its public form (threshold = the split's cut value) and the
+// call's counters.
+__global__ void k_finalize(const DevNode *__restrict__ nodes, int32_t n_nodes, const float *__restrict__ leaf,
+                           const int32_t *__restrict__ cut_ptr, const float *__restrict__ cut_values,
+                           const SampleState *__restrict__ st, const unsigned long long *__restrict__ upd,
+                           const unsigned long long *__restrict__ stat, TreeResult *__restrict__ out)
+{
+    const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i == 0) {
+        unsigned long long u = 0;
+        if (upd)
+            for (int k = 0; k < kUpdCounters; ++k) u += upd[k];
+        out->updates = u;
+        out->rows_built = stat[0];
+        out->partials = stat[1];
+        out->T = st->T;
+        out->e_key = st->e_key;
+        out->e_g = st->e_g;
+        out->e_h = st->e_h;
+        out->bad = st->bad;
+    }
+    if (i >= n_nodes) return;
+    const DevNode d = nodes[i];
+    gbt_node o;
+    memset(&o, 0, sizeof(o));
+    if (d.present) {
+        o.flags = GBT_NODE_PRESENT;
+        o.sum_g = d.sum_g;
+        o.sum_h = d.sum_h;
+        o.n_rows = (int32_t)(d.end - d.begin);
+        if (d.split) {
+            o.feature = d.feature;
+            o.split_bin = d.split_bin;
+            o.threshold = cut_values[cut_ptr[d.feature] + d.split_bin - 1];
+            o.gain = d.gain;
+            if (d.default_left) o.flags |= GBT_NODE_DEFAULT_LEFT;
+        } else {
+            o.feature = -1;
+            o.split_bin = -1;
+            o.flags |= GBT_NODE_LEAF;
+            o.leaf_value = leaf[i];
+        }
+    }
+    out->nodes[i] = o;  // absent nodes stay all zero
 }
 
 // Margin update from the final node of each training slot (no sampling:
@@ -665,14 +752,10 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     Buffers bufs{c, false, {}};
     gbt_sample_params sp{p->f, p->mvs_lambda, p->seed, p->iteration, p->loss, 0};
     SampleOut so;
-    GBT_TRY(sample_run(c, mx, gpair, margin, label, sp, bufs, &so, &h2d, st_ready));
+    GBT_TRY(sample_run(c, mx, gpair, margin, label, sp, bufs, &so, &h2d, st_ready, false));
     timer_end(c, mark);
     const int64_t R = so.R;
-    if (stats) {
-        stats->n_sampled = R;
-        stats->threshold = so.T;
-        stats->exp_key = so.e_key;
-    }
+    const int32_t *e_dev = &so.st->e_g;  // {e_g, e_h} on the device
 
     // ---- Alg. 1 on the sampled page, level by level.  Levels below the root
     // are planned on the device: no host round trip inside the tree.
@@ -710,42 +793,55 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     auto al = [](size_t b) { return (b + 255) / 256 * 256; };
     const size_t o_ev1 = al((size_t)max_level_nodes * sizeof(EvalNode));
     const size_t o_cnt = o_ev1 + o_ev1;
-    const size_t o_grp = o_cnt + 256;
-    const size_t o_work = o_grp + al((size_t)G * sizeof(HistGroup));
-    const size_t o_red = o_work + al((size_t)max_work * sizeof(HistWork));
+    // the root histogram: R rows in chunks, at most `items` - 1 per group
+    const int64_t root_chunk =
+        std::max<int64_t>(2048, (R + std::max(items - 1, 1) - 1) / std::max(items - 1, 1));
+    const int32_t n_root = (int32_t)std::max<int64_t>(1, (R + root_chunk - 1) / root_chunk);
+    const int32_t max_items = std::max(max_work, n_root);
+    const size_t o_work = o_cnt + 256;
+    const size_t o_red = o_work + al((size_t)max_items * sizeof(HistWork));
     const size_t plan_bytes = o_red + al((size_t)max_level_nodes * sizeof(HistReduce));
     char *plan;
     GBT_TRY(scratch_t(c, kScrPlan, plan_bytes, &plan));
     EvalNode *evA = (EvalNode *)plan, *evB = (EvalNode *)(plan + o_ev1);
     int32_t *cnt = (int32_t *)(plan + o_cnt);  // [0,1] level counts, [2] works, [3] reduces
     unsigned long long *stat = (unsigned long long *)(plan + o_cnt + 64);  // rows built, partials
-    HistGroup *groups_d = (HistGroup *)(plan + o_grp);
     HistWork *work_d = (HistWork *)(plan + o_work);
     HistReduce *red_d = (HistReduce *)(plan + o_red);
-    {
-        // root list, counts and the groups, in one upload
-        std::vector<char> h(o_work - 0, 0);
-        EvalNode root{so.root_g, so.root_h, 0, 0};
-        memcpy(h.data(), &root, sizeof(root));
-        int32_t c0[4] = {1, 0, 0, 0};
-        memcpy(h.data() + o_cnt, c0, sizeof(c0));
-        memcpy(h.data() + o_grp, groups.data(), groups.size() * sizeof(HistGroup));
-        GBT_HIP(hipMemcpyAsync(plan, h.data(), h.size(), hipMemcpyHostToDevice, c->stream));
+    // the feature groups live with the matrix (uploaded once per kernel kind)
+    if (mx->groups_kind != hp.kind) {
+        const size_t gb = std::max<size_t>(groups.size(), 1) * sizeof(HistGroup);
+        if (mx->groups_d) dev_free(c, mx->groups_d, mx->groups_bytes);
+        mx->groups_d = nullptr;
+        mx->groups_kind = -1;
+        GBT_TRY(dev_alloc(c, gb, &mx->groups_d));
+        mx->groups_bytes = gb;
+        GBT_HIP(hipMemcpyAsync(mx->groups_d, groups.data(), groups.size() * sizeof(HistGroup),
+                               hipMemcpyHostToDevice, c->stream));
+        GBT_HIP(hipStreamSynchronize(c->stream));
+        mx->groups_kind = hp.kind;
     }
+    const HistGroup *groups_d = (const HistGroup *)mx->groups_d;
     int64_t *partials = nullptr;
-    GBT_TRY(scratch(c, kScrPartialsDev, (size_t)std::max(max_work, 1) * mx->total_bins * 16, (void **)&partials));
-    k_tree_init<<<blocks(NN), 256, 0, c->stream>>>(nodes, NN, so.root_g, so.root_h, R);
+    GBT_TRY(scratch(c, kScrPartialsDev, (size_t)std::max(max_items, 1) * mx->total_bins * 16, (void **)&partials));
+    k_tree_init<<<blocks(std::max(NN, n_root)), 256, 0, c->stream>>>(nodes, NN, so.st, R, evA, cnt, work_d,
+                                                                     red_d, root_chunk, n_root);
     GBT_LAUNCHED();
+    if (stat) {
+        k_zero_counter<<<1, 64, 0, c->stream>>>(stat);
+        GBT_LAUNCHED();
+    }
     if (R) {
         k_rows_init<<<blocks(R), 256, 0, c->stream>>>(rows, slot_node, R);
         GBT_LAUNCHED();
     }
-    EvalParams ep{p->lambda, p->gamma, p->min_child_weight, so.e_g, so.e_h};
+    EvalParams ep{p->lambda, p->gamma, p->min_child_weight, 0, 0, e_dev};
     int32_t hist_launches = 0;
-    if (D > 0) {
-        gbt_seg root{0, 0, 0, R};
-        GBT_TRY(build_hist_impl(c, mx, so.page, so.q, nullptr, &root, 1, nullptr, 0, nullptr, histA, stats));
-        hist_launches += R > 0;
+    if (D > 0 && R > 0) {
+        HistLaunch hl{hp.kind, groups_d, G, hp.max_groups_bins, work_d, nullptr, n_root, red_d, nullptr, 1,
+                      partials};
+        GBT_TRY(hist_launch_device(c, mx, so.page, so.q, nullptr, hl, nullptr, histA, upd));
+        ++hist_launches;
     }
     int32_t *cntA = cnt, *cntB = cnt + 1;
     for (int32_t d = 0; d < D; ++d) {
@@ -777,8 +873,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     mark = timer_begin(c, kPhMargin);
     uint2 *compact;
     GBT_TRY(scratch_t(c, kScrCompact, (size_t)NN, &compact));
-    k_leaves<<<blocks(NN), 256, 0, c->stream>>>(nodes, NN, so.e_g, so.e_h, p->lambda, p->eta, leaf,
-                                                compact);
+    k_leaves<<<blocks(NN), 256, 0, c->stream>>>(nodes, NN, e_dev, p->lambda, p->eta, leaf, compact);
     GBT_LAUNCHED();
     if (so.alias) {
         if (n) {
@@ -808,57 +903,36 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
             &h2d));
     }
     timer_end(c, mark);
-    // ---- the tree, host side
-    std::vector<DevNode> all(NN);
-    std::vector<float> leafh(NN);
-    GBT_HIP(hipMemcpyAsync(all.data(), nodes, NN * sizeof(DevNode), hipMemcpyDeviceToHost, c->stream));
-    GBT_HIP(hipMemcpyAsync(leafh.data(), leaf, NN * 4, hipMemcpyDeviceToHost, c->stream));
+    // ---- the tree and the counters: written by the device into pinned
+    // memory, read after the one synchronization of the call
+    void *hio, *hio_d;
+    const size_t res_bytes = sizeof(TreeResult) + (size_t)NN * sizeof(gbt_node);
+    GBT_TRY(host_io(c, res_bytes, &hio, &hio_d));
+    k_finalize<<<blocks(NN), 256, 0, c->stream>>>(nodes, NN, leaf, mx->cut_ptr_d, mx->cut_values_d, so.st, upd,
+                                                  stat, (TreeResult *)hio_d);
+    GBT_LAUNCHED();
     GBT_HIP(hipStreamSynchronize(c->stream));
-    tree->exp_g = so.e_g;
-    tree->exp_h = so.e_h;
-    for (int32_t i = 0; i < NN; ++i) {
-        gbt_node &o = tree->nodes[i];
-        memset(&o, 0, sizeof(o));
-        const DevNode &d = all[i];
-        if (!d.present) continue;
-        o.flags = GBT_NODE_PRESENT;
-        o.sum_g = d.sum_g;
-        o.sum_h = d.sum_h;
-        o.n_rows = (int32_t)(d.end - d.begin);
-        if (d.split) {
-            o.feature = d.feature;
-            o.split_bin = d.split_bin;
-            o.threshold = mx->cut_values_h[mx->cut_ptr_h[d.feature] + d.split_bin - 1];
-            o.gain = d.gain;
-            if (d.default_left) o.flags |= GBT_NODE_DEFAULT_LEFT;
-        } else {
-            o.feature = -1;
-            o.split_bin = -1;
-            o.flags |= GBT_NODE_LEAF;
-            o.leaf_value = leafh[i];
-        }
-    }
+    const TreeResult *res = (const TreeResult *)hio;
+    if (res->bad) return set_error(GBT_E_INVALID, "sampling failed (state flags %u)", res->bad);
+    tree->exp_g = res->e_g;
+    tree->exp_h = res->e_h;
+    memcpy(tree->nodes, res->nodes, (size_t)NN * sizeof(gbt_node));
     double ms[kPhCount] = {0.0};
     timer_collect(c, ms);
     if (stats) {
-        unsigned long long u[kUpdCounters];
-        GBT_HIP(hipMemcpyAsync(u, upd, sizeof(u), hipMemcpyDeviceToHost, c->stream));
-        GBT_HIP(hipStreamSynchronize(c->stream));
-        stats->hist_updates = 0;
-        for (int k = 0; k < kUpdCounters; ++k) stats->hist_updates += (int64_t)u[k];
-        unsigned long long st2[2] = {0, 0};
-        GBT_HIP(hipMemcpyAsync(st2, stat, sizeof(st2), hipMemcpyDeviceToHost, c->stream));
-        GBT_HIP(hipStreamSynchronize(c->stream));
+        stats->n_sampled = R;
+        stats->threshold = res->T;
+        stats->exp_key = res->e_key;
+        stats->hist_updates = (int64_t)res->updates;
         // algorithmic bytes: the packed symbols of each row, its 16-byte
         // fixed-point pair, its 4-byte row id below the root, and one write of
         // every chunk's partial histogram
         const int64_t wbytes = 4 * (((int64_t)mx->stride * mx->w + 31) / 32);
-        const int64_t root_chunk = std::max<int64_t>(2048, (R * G + twg - 1) / twg);
-        const int64_t root_parts = (D > 0 && R > 0) ? (R + root_chunk - 1) / root_chunk : 0;
+        const int64_t root_parts = (D > 0 && R > 0) ? n_root : 0;
         stats->hist_launches = hist_launches;
-        stats->hist_rows = (D > 0 ? R : 0) + (int64_t)st2[0];
-        stats->hist_bytes = (D > 0 ? R : 0) * (wbytes + 16) + (int64_t)st2[0] * (wbytes + 20) +
-                            (root_parts + (int64_t)st2[1]) * mx->total_bins * 16;
+        stats->hist_rows = (D > 0 ? R : 0) + (int64_t)res->rows_built;
+        stats->hist_bytes = (D > 0 ? R : 0) * (wbytes + 16) + (int64_t)res->rows_built * (wbytes + 20) +
+                            (root_parts + (int64_t)res->partials) * mx->total_bins * 16;
         stats->ms_sample = ms[kPhSample];
         stats->ms_hist = ms[kPhHist];
         stats->ms_hist_aux = ms[kPhHistAux];
