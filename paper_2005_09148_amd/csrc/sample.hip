@@ -345,32 +345,47 @@ __global__ void __launch_bounds__(256) k_mvs_radix_decide(SampleState *__restric
     }
 }
 
+// Keep decision of every row; a block covers one compaction tile of 4096
+// rows (16 per thread, a block stride apart) and writes its kept count.
 template <int kSrc>
 __global__ void __launch_bounds__(256) k_mvs_select(SampleSrc src, const int64_t *__restrict__ keys,
                                                     int64_t n, double lambda,
                                                     const SampleState *__restrict__ st,
                                                     uint64_t seed, uint64_t iteration,
-                                                    int64_t row_offset, uint8_t *__restrict__ keep)
+                                                    int64_t row_offset, uint8_t *__restrict__ keep,
+                                                    int32_t *__restrict__ tile_cnt)
 {
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n) return;
-    unsigned long long a;
-    if (keys) {
-        a = (unsigned long long)keys[i];
-    } else {
-        double g, h;
-        row_gh<kSrc>(src, i, &g, &h);
-        a = (unsigned long long)(long long)rint(ldexp(mvs_r(g, h, lambda), st->e_key));
+    __shared__ int32_t red4[4];
+    const unsigned long long T = (unsigned long long)st->T;
+    const int32_t e = st->e_key;
+    const int64_t base = (int64_t)blockIdx.x * kCompactTile + threadIdx.x;
+    int32_t cnt = 0;
+#pragma unroll 4
+    for (int k = 0; k < kCompactTile / 256; ++k) {
+        const int64_t i = base + k * 256;
+        if (i >= n) break;
+        unsigned long long a;
+        if (keys) {
+            a = (unsigned long long)keys[i];
+        } else {
+            double g, h;
+            row_gh<kSrc>(src, i, &g, &h);
+            a = (unsigned long long)(long long)rint(ldexp(mvs_r(g, h, lambda), e));
+        }
+        bool kp;
+        if (a >= T) {
+            kp = true;
+        } else {
+            const uint64_t U = philox_word0((uint64_t)(row_offset + i), iteration, 0, 0, seed, 0);
+            kp = __umul64hi(U, T) < a;
+        }
+        keep[i] = kp ? 1 : 0;
+        cnt += kp ? 1 : 0;
     }
-    unsigned long long T = (unsigned long long)st->T;
-    bool k;
-    if (a >= T) {
-        k = true;
-    } else {
-        uint64_t U = philox_word0((uint64_t)(row_offset + i), iteration, 0, 0, seed, 0);
-        k = __umul64hi(U, T) < a;
-    }
-    keep[i] = k ? 1 : 0;
+    for (int d = 32; d > 0; d >>= 1) cnt += __shfl_xor(cnt, d, 64);
+    if ((threadIdx.x & 63) == 0) red4[threadIdx.x >> 6] = cnt;
+    __syncthreads();
+    if (threadIdx.x == 0 && tile_cnt) tile_cnt[blockIdx.x] = red4[0] + red4[1] + red4[2] + red4[3];
 }
 
 // f = 1: every row trains, unweighted.
@@ -383,9 +398,10 @@ __global__ void k_gw_all(const float2 *__restrict__ gpair, int64_t n, double2 *_
 }
 
 // Compaction of one range of rows, tile by tile: the block rescans its tile's
-// keep flags (exclusive, from the tile offset), gathers each kept row of the
-// range into the sampled page, records its global id and its reweighted
-// pair, and folds the maxima of |g'| and |h'|.
+// keep flags (exclusive, from the tile offset) into a list of the tile's
+// kept rows; its threads then copy those rows into the sampled page
+// together (16-byte pieces), and record each kept row's global id and
+// reweighted pair, folding the maxima of |g'| and |h'|.
 template <int kSrc>
 __global__ void __launch_bounds__(256)
     k_compact_tiles(SampleSrc src, int64_t n, double lambda, SampleState *__restrict__ st,
@@ -396,8 +412,10 @@ __global__ void __launch_bounds__(256)
 {
     __shared__ int32_t lds4[4];
     __shared__ unsigned long long red4[4];
+    __shared__ uint16_t klist[kCompactTile];
     const int64_t tile = tile0 + blockIdx.x;
-    const int64_t base = tile * kCompactTile + (int64_t)threadIdx.x * 16;
+    const int64_t tbase = tile * kCompactTile;
+    const int64_t base = tbase + (int64_t)threadIdx.x * 16;
     uint32_t bits = 0;
     if (base + 16 <= n) {
         uint4 v = *(const uint4 *)(keep + base);
@@ -419,24 +437,35 @@ __global__ void __launch_bounds__(256)
     }
     if (lane == 63) lds4[wid] = x;
     __syncthreads();
-    int32_t run = tile_off[tile] + x - cnt;
+    int32_t run = x - cnt;
     for (int w = 0; w < wid; ++w) run += lds4[w];
-    const unsigned long long T = (unsigned long long)st->T;
-    const int32_t e = st->e_key;
-    unsigned long long mg = 0, mh = 0;
+    const int32_t nk = lds4[0] + lds4[1] + lds4[2] + lds4[3];
     while (bits) {
         const int k = __ffs(bits) - 1;
         bits &= bits - 1;
-        const int64_t i = base + k;
-        const int32_t pos = run++;
+        klist[run++] = (uint16_t)(threadIdx.x * 16 + k);
+    }
+    __syncthreads();
+    const int64_t pos0 = tile_off[tile];
+    // the rows, 16 bytes per thread and step
+    for (int32_t e = threadIdx.x; e < nk * row_q4; e += 256) {
+        const int32_t j = e / row_q4, t = e - j * row_q4;
+        const int64_t i = tbase + klist[j];
         if (i < row_lo || i >= row_hi) continue;
-        const uint4 *src_row = words + (i - row_lo) * row_q4;
-        uint4 *dst = out_page + (int64_t)pos * row_q4;
-        for (int32_t t = 0; t < row_q4; ++t) dst[t] = src_row[t];
+        out_page[(pos0 + j) * row_q4 + t] = words[(i - row_lo) * row_q4 + t];
+    }
+    // ids and reweighted pairs
+    const unsigned long long T = (unsigned long long)st->T;
+    const int32_t ek = st->e_key;
+    unsigned long long mg = 0, mh = 0;
+    for (int32_t j = threadIdx.x; j < nk; j += 256) {
+        const int64_t i = tbase + klist[j];
+        if (i < row_lo || i >= row_hi) continue;
+        const int64_t pos = pos0 + j;
         sel[pos] = (int32_t)i;
         double g, h;
         row_gh<kSrc>(src, i, &g, &h);
-        unsigned long long a = (unsigned long long)(long long)rint(ldexp(mvs_r(g, h, lambda), e));
+        unsigned long long a = (unsigned long long)(long long)rint(ldexp(mvs_r(g, h, lambda), ek));
         double w = a >= T ? 1.0 : (double)(long long)T / (double)(long long)a;
         double2 v = make_double2(g * w, h * w);
         gw[pos] = v;
@@ -596,15 +625,16 @@ gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64
 
 gbt_status mvs_select(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
                       double lambda, const SampleState *st, uint64_t seed, uint64_t iteration,
-                      int64_t row_offset, uint8_t *keep)
+                      int64_t row_offset, uint8_t *keep, int32_t *tile_cnt)
 {
     if (n == 0) return GBT_OK;
+    const unsigned grid = (unsigned)((n + kCompactTile - 1) / kCompactTile);
     if (kind == kSrcGpair)
-        k_mvs_select<kSrcGpair><<<blocks(n), 256, 0, c->stream>>>(src, keys, n, lambda, st, seed,
-                                                                  iteration, row_offset, keep);
+        k_mvs_select<kSrcGpair><<<grid, 256, 0, c->stream>>>(src, keys, n, lambda, st, seed, iteration,
+                                                             row_offset, keep, tile_cnt);
     else
-        k_mvs_select<kSrcMargin><<<blocks(n), 256, 0, c->stream>>>(src, keys, n, lambda, st, seed,
-                                                                   iteration, row_offset, keep);
+        k_mvs_select<kSrcMargin><<<grid, 256, 0, c->stream>>>(src, keys, n, lambda, st, seed, iteration,
+                                                              row_offset, keep, tile_cnt);
     GBT_LAUNCHED();
     return GBT_OK;
 }
@@ -626,9 +656,9 @@ gbt_status gradients_rmax(gbt_ctx *c, int32_t loss, const float *margin, const f
     return GBT_OK;
 }
 
-gbt_status keep_tile_offsets(gbt_ctx *c, const uint8_t *keep, int64_t n, int32_t *tile_off)
+gbt_status keep_tile_offsets(gbt_ctx *c, int64_t n, int32_t *tile_off)
 {
-    return scan_tiles_u8(c, keep, n, tile_off);
+    return scan_tile_counts(c, tile_off, (n + kCompactTile - 1) / kCompactTile);
 }
 
 gbt_status mvs_compact_tiles(gbt_ctx *c, const SampleSrc &src, int kind, int64_t n, double lambda,

@@ -8,6 +8,7 @@
 
 namespace gbt {
 
+constexpr int kCompactTile = 4096;  // rows per compaction tile
 constexpr int kDigitBits = 11;
 constexpr int kDigitBuckets = 1 << kDigitBits;
 
@@ -69,9 +70,11 @@ gbt_status state_init(gbt_ctx *c, SampleState *st);
 gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
                          double lambda, int64_t K, SampleState *st, SampleState *host_st,
                          bool rmax_done = false);
+// Keep flags of rows [0, n) and, when tile_cnt is given, the kept count of
+// each tile of kCompactTile rows.
 gbt_status mvs_select(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
                       double lambda, const SampleState *st, uint64_t seed, uint64_t iteration,
-                      int64_t row_offset, uint8_t *keep);
+                      int64_t row_offset, uint8_t *keep, int32_t *tile_cnt);
 gbt_status gw_all(gbt_ctx *c, const float *gpair, int64_t n, double *gw);
 // fx_max_done: the maxima of |g'| and |h'| are already in st (fused upstream)
 gbt_status fixed_point(gbt_ctx *c, const double *gw, int64_t R, SampleState *st, int64_t *q,
@@ -79,9 +82,9 @@ gbt_status fixed_point(gbt_ctx *c, const double *gw, int64_t R, SampleState *st,
 // Gradients of all rows and, fused, the maximum of r = sqrt(g^2 + lambda h^2).
 gbt_status gradients_rmax(gbt_ctx *c, int32_t loss, const float *margin, const float *label, int64_t n,
                           float *gpair, double lambda, SampleState *st);
-// Exclusive per-tile offsets (tiles of kCompactTile flags) and the total.
-constexpr int kCompactTile = 4096;
-gbt_status keep_tile_offsets(gbt_ctx *c, const uint8_t *keep, int64_t n, int32_t *tile_off);
+// Exclusive per-tile offsets from the per-tile counts mvs_select wrote into
+// tile_off (tiles of kCompactTile rows), and the total at tile_off[tiles].
+gbt_status keep_tile_offsets(gbt_ctx *c, int64_t n, int32_t *tile_off);
 // Compaction of the kept rows among global rows [row_lo, row_hi) whose page
 // words start at `words`; positions come from the tile offsets; also folds
 // the maxima of |g'| and |h'| into st.

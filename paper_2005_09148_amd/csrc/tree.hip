@@ -180,8 +180,8 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
             GBT_TRY(mvs_threshold(c, src, kind, nullptr, n, sp.mvs_lambda, o->K, st, &hst, st_ready != nullptr));
         }
         // with f = 1 the state keeps T = 0: every row is kept with weight 1
-        GBT_TRY(mvs_select(c, src, kind, nullptr, n, sp.mvs_lambda, st, sp.seed, sp.iteration, 0, keep));
-        GBT_TRY(keep_tile_offsets(c, keep, n, tile_off));
+        GBT_TRY(mvs_select(c, src, kind, nullptr, n, sp.mvs_lambda, st, sp.seed, sp.iteration, 0, keep, tile_off));
+        GBT_TRY(keep_tile_offsets(c, n, tile_off));
         // the sample size sizes the buffers below: one round trip
         void *hio, *hio_d;
         GBT_TRY(host_io(c, 64, &hio, &hio_d));
@@ -605,6 +605,92 @@ __global__ void __launch_bounds__(kWalkTileRows)
     }
 }
 
+// The same walk with the next tile's rows and margins prefetched into
+// registers (kQ 16-byte pieces per row) while the current tile is walked.
+template <int kQ>
+__global__ void __launch_bounds__(kWalkTileRows)
+    k_margin_walk_pf(const uint32_t *__restrict__ words, int64_t rows, Geo geo,
+                     const uint2 *__restrict__ compact, const float *__restrict__ leaf, int32_t nn,
+                     float *__restrict__ margin)
+{
+    extern __shared__ uint32_t walk_lds[];
+    uint2 *tn = (uint2 *)walk_lds;
+    float *tl = (float *)(tn + nn);
+    uint32_t *rb = (uint32_t *)(tl + nn);
+    for (int32_t t = threadIdx.x; t < nn; t += kWalkTileRows) {
+        tn[t] = compact[t];
+        tl[t] = leaf[t];
+    }
+    constexpr int32_t ps = 4 * kQ + 1;  // odd row pitch in LDS
+    const int64_t n_tiles = (rows + kWalkTileRows - 1) / kWalkTileRows;
+    uint4 nxt[kQ];
+    float mnext = 0.0f;
+    auto load = [&](int64_t tile) {
+        const int64_t r0 = tile * kWalkTileRows;
+        const int32_t nr = (int32_t)min((int64_t)kWalkTileRows, rows - r0);
+        const uint4 *src = (const uint4 *)(words + r0 * geo.row_words);
+#pragma unroll
+        for (int j = 0; j < kQ; ++j) {
+            const int32_t e = threadIdx.x + j * kWalkTileRows;
+            nxt[j] = e < nr * kQ ? src[e] : make_uint4(0u, 0u, 0u, 0u);
+        }
+        mnext = (int32_t)threadIdx.x < nr ? margin[r0 + threadIdx.x] : 0.0f;
+    };
+    int64_t tile = blockIdx.x;
+    if (tile < n_tiles) load(tile);
+    for (; tile < n_tiles; tile += gridDim.x) {
+        const int64_t r0 = tile * kWalkTileRows;
+        const int32_t nr = (int32_t)min((int64_t)kWalkTileRows, rows - r0);
+        __syncthreads();  // the previous tile's rows are consumed (and the tree is loaded)
+#pragma unroll
+        for (int j = 0; j < kQ; ++j) {
+            const int32_t e = threadIdx.x + j * kWalkTileRows;
+            uint32_t *d = rb + (e / kQ) * ps + (e % kQ) * 4;
+            d[0] = nxt[j].x;
+            d[1] = nxt[j].y;
+            d[2] = nxt[j].z;
+            d[3] = nxt[j].w;
+        }
+        const float m = mnext;
+        __syncthreads();
+        if (tile + gridDim.x < n_tiles) load(tile + gridDim.x);
+        if ((int32_t)threadIdx.x < nr) {
+            const uint32_t *row = rb + threadIdx.x * ps;
+            int32_t id = 0;
+            uint2 nd = tn[0];
+            while (nd.y & 1u) {
+                const int32_t b = row_feature_bin(row, geo, (int32_t)nd.x);
+                const bool left = b < 0 ? ((nd.y >> 1) & 1u) != 0 : b < (int32_t)(nd.y >> 2);
+                id = 2 * id + (left ? 1 : 2);
+                nd = tn[id];
+            }
+            margin[r0 + threadIdx.x] = m + tl[id];
+        }
+    }
+}
+
+static void launch_walk_pf(gbt_ctx *c, int q4, unsigned grid, size_t lds_bytes, const uint32_t *words,
+                           int64_t rows, const Geo &geo, const uint2 *compact, const float *leaf, int32_t nn,
+                           float *margin)
+{
+#define GBT_WALK_PF(Q)                                                                                         \
+    case Q:                                                                                                    \
+        k_margin_walk_pf<Q><<<grid, kWalkTileRows, lds_bytes, c->stream>>>(words, rows, geo, compact, leaf, nn, \
+                                                                            margin);                           \
+        break;
+    switch (q4) {
+        GBT_WALK_PF(1)
+        GBT_WALK_PF(2)
+        GBT_WALK_PF(3)
+        GBT_WALK_PF(4)
+        GBT_WALK_PF(5)
+        GBT_WALK_PF(6)
+        GBT_WALK_PF(7)
+        GBT_WALK_PF(8)
+    }
+#undef GBT_WALK_PF
+}
+
 // ------------------------------------------------------------ prediction
 __device__ inline int32_t walk_binned(const gbt_node *__restrict__ t, int64_t nn, const uint32_t *row,
                                       const Geo &geo)
@@ -886,7 +972,12 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
             c, mx,
             [&](const uint32_t *words, int64_t row0, int64_t rows_n) -> gbt_status {
                 const size_t lds_bytes = (size_t)NN * 12 + (size_t)kWalkTileRows * (geo.row_words + 1) * 4;
-                if (geo.row_words <= kWalkMaxWords && NN <= kWalkLdsNodes && lds_bytes <= 64 * 1024) {
+                const int q4 = geo.row_words / 4;
+                if (q4 <= 8 && NN <= kWalkLdsNodes && lds_bytes <= 64 * 1024) {
+                    int64_t tiles = (rows_n + kWalkTileRows - 1) / kWalkTileRows;
+                    unsigned grid = (unsigned)std::min<int64_t>(tiles, 4 * kCUs);
+                    launch_walk_pf(c, q4, grid, lds_bytes, words, rows_n, geo, compact, leaf, NN, margin + row0);
+                } else if (geo.row_words <= kWalkMaxWords && NN <= kWalkLdsNodes && lds_bytes <= 64 * 1024) {
                     int64_t tiles = (rows_n + kWalkTileRows - 1) / kWalkTileRows;
                     unsigned grid = (unsigned)std::min<int64_t>(tiles, 4 * kCUs);
                     k_margin_walk_lds<<<grid, kWalkTileRows, lds_bytes, c->stream>>>(words, rows_n, geo, compact,
