@@ -122,6 +122,9 @@ def parse():
                     help="summarize two rocprofv3 --pmc runs of this script (no GPU work)")
     ap.add_argument("--pmc-commands", nargs="*", default=[], help="the commands of those runs")
     ap.add_argument("--pmc-kernel", default="k_hist_dense", choices=sorted(HIST_KERNELS.values()))
+    ap.add_argument("--workload", default="regression", choices=["regression", "outofcore"],
+                    help="regression: 10M x 50 in HBM (the default line); outofcore: 200M x 100 in "
+                         "pinned host pages under an 8 GB device budget")
     return ap.parse_args()
 
 
@@ -186,6 +189,124 @@ def cpu_baseline(X, y, cfg, n_trees, gpu_trees):
     }
 
 
+def pinned_h2d_peak(torch, nbytes=1 << 30, reps=5):
+    """Host-to-device GB/s of plain copies from pinned memory."""
+    src = torch.empty(nbytes, dtype=torch.uint8).pin_memory()
+    dst = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    dst.copy_(src, non_blocking=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        dst.copy_(src, non_blocking=True)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    del src, dst
+    return nbytes * reps / dt / 1e9
+
+
+def run_outofcore(args):
+    """The 200M x 100 workload: twelve 2^24-row pages of binned rows in pinned
+    host memory, an 8 GB cap on the library's device memory, MVS f = 0.1.
+    Every tree streams the pages twice over the host link (compaction of the
+    sampled rows, then the margin update of all rows)."""
+    import torch
+
+    from paper_2005_09148_amd import datagen, gbt
+
+    cfg = datagen.CONFIGS[4]
+    n = args.rows or datagen.FULL_ROWS[4]
+    page_rows = datagen.C4_PAGE_ROWS
+    sizes = datagen.config4_page_rows(n, page_rows)
+    budget = 8 << 30
+    ctx = gbt.Context(0, budget_bytes=budget)
+    sub = 1 << 21  # rows per host batch handed to the quantizer
+    t = time.perf_counter()
+    q = gbt.Quantizer(ctx, 100, n, max_bin=cfg.max_bin, page_rows=page_rows, page_home=gbt.HOME_PINNED_HOST)
+    raw, labels = [], []
+    for p, rows in enumerate(sizes):
+        d = datagen.config4_page(p, rows=rows)
+        for lo in range(0, rows, sub):
+            q.sketch(d["X"][lo:lo + sub])
+        raw.append(d["X"])
+        labels.append(d["y"])
+        print(f"[bench] page {p}: generated and sketched ({time.perf_counter() - t:.0f} s)", file=sys.stderr,
+              flush=True)
+    q.finalize()
+    for p in range(len(sizes)):
+        X = raw[p]
+        for lo in range(0, len(X), sub):
+            q.encode(X[lo:lo + sub])
+        raw[p] = None
+        print(f"[bench] page {p}: encoded ({time.perf_counter() - t:.0f} s)", file=sys.stderr, flush=True)
+    mx = q.end()
+    info = mx.info()
+    y = np.concatenate(labels)
+    del labels
+    print(f"[bench] {info.n_pages} pinned pages, row_words {info.row_words}, quantized in "
+          f"{time.perf_counter() - t:.0f} s", file=sys.stderr, flush=True)
+    label = torch.from_numpy(y).cuda()
+    margin = torch.full((n,), cfg.base_margin, dtype=torch.float32, device="cuda")
+    P = gbt.make_train_params(loss=cfg.loss, max_depth=cfg.max_depth, eta=cfg.eta, lambda_=cfg.lambda_,
+                              gamma=cfg.gamma, min_child_weight=cfg.min_child_weight, f=cfg.f,
+                              mvs_lambda=cfg.mvs_lambda, seed=cfg.seed)
+    ctx.set_timing(1)
+    for w in range(args.warmup):
+        P.iteration = w
+        gbt.gbt_train_tree(ctx, mx, label, margin, P)
+        print(f"[bench] warm-up tree {w}", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    stats = []
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        P.iteration = args.warmup + k
+        stats.append(gbt.gbt_train_tree(ctx, mx, label, margin, P).stats)
+        print(f"[bench] tree {k}: {stats[-1].ms_total:.0f} ms", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    ctx.set_timing(0)
+    used, peak = ctx.memory()
+    h2d = sum(s.h2d_bytes for s in stats)
+    upd = sum(s.hist_updates for s in stats)
+    hbytes = sum(s.hist_bytes for s in stats)
+    hms = sum(s.ms_hist for s in stats)
+    launches = sum(s.hist_launches for s in stats)
+    achieved = hbytes / (hms * 1e-3) / 1e9 if hms > 0 else 0.0
+    link_peak = pinned_h2d_peak(torch)
+    kernels = {HIST_KERNELS.get(s.hist_kernel, "k_hist_sparse") for s in stats}
+    line = {
+        "metric": METRIC,
+        "value": round(upd / dt / 1e9, 4),
+        "unit": "G updates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(dt * 1e3 / args.steps, 2),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic",
+        "config": {"workload": f"out-of-core {n:,} x 100 in {info.n_pages} pinned pages of {page_rows:,} rows, "
+                               f"logistic, max_bin 256, depth 8, MVS f={cfg.f}, 8 GB device budget",
+                   "rows": n, "features": 100, "page_rows": page_rows, "f": cfg.f},
+        "sec_per_tree": round(dt / args.steps, 4),
+        "rows_sampled_per_tree": round(sum(s.n_sampled for s in stats) / args.steps),
+        "host_link": {"h2d_bytes_per_tree": round(h2d / args.steps), "achieved_gbs": round(h2d / dt / 1e9, 2),
+                      "pinned_copy_peak_gbs": round(link_peak, 2),
+                      "frac": round(h2d / dt / 1e9 / link_peak, 4)},
+        "device_memory": {"budget_bytes": budget, "peak_bytes": peak},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "+".join(sorted(kernels)), "launches": launches,
+                     "avg_launch_us": round(hms * 1e3 / max(launches, 1), 2),
+                     "algorithmic_bytes_per_launch": hbytes // max(launches, 1)},
+        "cpu_baseline": None,
+        "cpu_baseline_note": "not run at this size (the oracle needs minutes per tree on 200M rows); "
+                             "tests/test_gpu_fullsize.py checks the same page shape against the oracle",
+    }
+    print(json.dumps(line), flush=True)
+
+
 def workload_key(args):
     from paper_2005_09148_amd import datagen
     n = args.rows or datagen.FULL_ROWS[3]
@@ -202,6 +323,9 @@ def main():
         print("bench.py measures one GPU: the hot path here runs on a single MI355X "
               "(no multi-GPU path is built); run it with --gpus 1", file=sys.stderr)
         sys.exit(2)
+    if args.workload == "outofcore":
+        run_outofcore(args)
+        return
     import torch
 
     from paper_2005_09148_amd import datagen, gbt

@@ -896,11 +896,12 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     HistReduce *red_d = (HistReduce *)(plan + o_red);
     // the feature groups live with the matrix (uploaded once per kernel kind)
     if (mx->groups_kind != hp.kind) {
+        // owned (and budgeted) by the matrix's context, like its other arrays
         const size_t gb = std::max<size_t>(groups.size(), 1) * sizeof(HistGroup);
-        if (mx->groups_d) dev_free(c, mx->groups_d, mx->groups_bytes);
+        if (mx->groups_d) dev_free(mx->ctx, mx->groups_d, mx->groups_bytes);
         mx->groups_d = nullptr;
         mx->groups_kind = -1;
-        GBT_TRY(dev_alloc(c, gb, &mx->groups_d));
+        GBT_TRY(dev_alloc(mx->ctx, gb, &mx->groups_d));
         mx->groups_bytes = gb;
         GBT_HIP(hipMemcpyAsync(mx->groups_d, groups.data(), groups.size() * sizeof(HistGroup),
                                hipMemcpyHostToDevice, c->stream));
