@@ -265,8 +265,9 @@ gbt_status scan_u32(gbt_ctx *c, const uint32_t *in, int64_t n, int32_t *out);
 // tile_off[ceil(n/4096)] = total.
 gbt_status scan_tiles_u8(gbt_ctx *c, const uint8_t *in, int64_t n, int32_t *tile_off);
 // Exclusive sums of `tiles` per-tile counts, in place; tile_cnt[tiles]
-// receives the total.
-gbt_status scan_tile_counts(gbt_ctx *c, int32_t *tile_cnt, int64_t tiles);
+// receives the total, and so does *total_host (pinned, device-mapped) when
+// given.
+gbt_status scan_tile_counts(gbt_ctx *c, int32_t *tile_cnt, int64_t tiles, int32_t *total_host = nullptr);
 
 // ---------------------------------------------------------------- shared launches
 gbt_status launch_gradients(gbt_ctx *c, int32_t loss, const float *margin, const float *label,

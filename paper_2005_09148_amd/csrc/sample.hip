@@ -656,9 +656,9 @@ gbt_status gradients_rmax(gbt_ctx *c, int32_t loss, const float *margin, const f
     return GBT_OK;
 }
 
-gbt_status keep_tile_offsets(gbt_ctx *c, int64_t n, int32_t *tile_off)
+gbt_status keep_tile_offsets(gbt_ctx *c, int64_t n, int32_t *tile_off, int32_t *total_host)
 {
-    return scan_tile_counts(c, tile_off, (n + kCompactTile - 1) / kCompactTile);
+    return scan_tile_counts(c, tile_off, (n + kCompactTile - 1) / kCompactTile, total_host);
 }
 
 gbt_status mvs_compact_tiles(gbt_ctx *c, const SampleSrc &src, int kind, int64_t n, double lambda,

@@ -83,8 +83,9 @@ gbt_status fixed_point(gbt_ctx *c, const double *gw, int64_t R, SampleState *st,
 gbt_status gradients_rmax(gbt_ctx *c, int32_t loss, const float *margin, const float *label, int64_t n,
                           float *gpair, double lambda, SampleState *st);
 // Exclusive per-tile offsets from the per-tile counts mvs_select wrote into
-// tile_off (tiles of kCompactTile rows), and the total at tile_off[tiles].
-gbt_status keep_tile_offsets(gbt_ctx *c, int64_t n, int32_t *tile_off);
+// tile_off (tiles of kCompactTile rows), and the total at tile_off[tiles]
+// (and at *total_host, pinned host memory, when given).
+gbt_status keep_tile_offsets(gbt_ctx *c, int64_t n, int32_t *tile_off, int32_t *total_host = nullptr);
 // Compaction of the kept rows among global rows [row_lo, row_hi) whose page
 // words start at `words`; positions come from the tile offsets; also folds
 // the maxima of |g'| and |h'| into st.

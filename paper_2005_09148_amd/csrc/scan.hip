@@ -48,9 +48,11 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_reduce(const T *__restric
     if (threadIdx.x == 0) bsum[blockIdx.x] = tot;
 }
 
-// One block scans the per-tile sums (in place, exclusive) and writes the total.
+// One block scans the per-tile sums (in place, exclusive) and writes the total
+// (also to total_host, pinned host memory, when given).
 __global__ void __launch_bounds__(1024) k_scan_spine(int32_t *__restrict__ bsum, int64_t nb,
-                                                     int32_t *__restrict__ total_out)
+                                                     int32_t *__restrict__ total_out,
+                                                     int32_t *__restrict__ total_host = nullptr)
 {
     __shared__ int32_t lds16[16];
     __shared__ int32_t carry;
@@ -78,7 +80,10 @@ __global__ void __launch_bounds__(1024) k_scan_spine(int32_t *__restrict__ bsum,
         if (threadIdx.x == 0) carry += tot;
         __syncthreads();
     }
-    if (threadIdx.x == 0) *total_out = carry;
+    if (threadIdx.x == 0) {
+        *total_out = carry;
+        if (total_host) *total_host = carry;
+    }
 }
 
 template <typename T>
@@ -139,9 +144,9 @@ gbt_status scan_tiles_u8(gbt_ctx *c, const uint8_t *in, int64_t n, int32_t *tile
     return GBT_OK;
 }
 
-gbt_status scan_tile_counts(gbt_ctx *c, int32_t *tile_cnt, int64_t tiles)
+gbt_status scan_tile_counts(gbt_ctx *c, int32_t *tile_cnt, int64_t tiles, int32_t *total_host)
 {
-    k_scan_spine<<<1, 1024, 0, c->stream>>>(tile_cnt, tiles, tile_cnt + tiles);
+    k_scan_spine<<<1, 1024, 0, c->stream>>>(tile_cnt, tiles, tile_cnt + tiles, total_host);
     GBT_LAUNCHED();
     return GBT_OK;
 }

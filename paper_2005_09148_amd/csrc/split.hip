@@ -49,24 +49,86 @@ __device__ inline double eq8_gain(double GL, double HL, double GR, double HR, do
     return 0.5 * ((a + b) - c) - gamma;
 }
 
+// The best candidate of the wavefront (every lane receives it): the highest
+// gain among valid lanes, then the lowest order; one max reduction, one min
+// reduction and a broadcast from the winning lane.
 __device__ inline Cand wave_best(Cand x)
 {
-    for (int d = 32; d > 0; d >>= 1) {
-        Cand o;
-        o.gain = __shfl_xor(x.gain, d, 64);
-        o.order = __shfl_xor(x.order, d, 64);
-        o.valid = __shfl_xor(x.valid, d, 64);
-        o.lg = __shfl_xor(x.lg, d, 64);
-        o.lh = __shfl_xor(x.lh, d, 64);
-        if (better(o, x)) x = o;
-    }
-    return x;
+    const unsigned long long any = __ballot(x.valid != 0);
+    Cand r;
+    r.valid = 0;
+    r.gain = 0.0;
+    r.order = 0;
+    r.lg = r.lh = 0;
+    if (!any) return r;
+    double m = x.valid ? x.gain : -__builtin_inf();
+    for (int d = 32; d > 0; d >>= 1) m = fmax(m, __shfl_xor(m, d, 64));
+    const bool cand = x.valid && x.gain == m;
+    int32_t o = cand ? x.order : 0x7fffffff;
+    for (int d = 32; d > 0; d >>= 1) o = min(o, __shfl_xor(o, d, 64));
+    const unsigned long long win = __ballot(cand && x.order == o);
+    const int wl = __ffsll((long long)win) - 1;
+    r.valid = 1;
+    r.gain = __shfl(x.gain, wl, 64);  // the winner's own bits (+0 and -0 compare equal)
+    r.order = o;
+    r.lg = __shfl(x.lg, wl, 64);
+    r.lh = __shfl(x.lh, wl, 64);
+    return r;
 }
 
 __device__ inline long long wave_sum(long long v)
 {
     for (int d = 32; d > 0; d >>= 1) v += __shfl_xor(v, d, 64);
     return v;
+}
+
+// Best split of one feature for one node, evaluated by one wavefront.  The
+// result (valid in every lane) carries order = s*2 + dir.
+// The gains of the four cuts after this lane's bins of one 256-bin chunk:
+// pg, ph enter as the sums of all bins before the lane's first bin.
+__device__ inline void eval_chunk(const longlong2 v[4], int32_t base, int32_t B, long long pg, long long ph,
+                                  long long Qg, long long Qh, long long mg, long long mh, double G, double H,
+                                  const EvalParams &ep, Cand &best)
+{
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        const int32_t b = base + lane * 4 + t;
+        pg += v[t].x;
+        ph += v[t].y;
+        const int32_t s = b + 1;  // left = bins < s
+        if (s > B - 1) continue;
+#pragma unroll
+        for (int dir = 0; dir < 2; ++dir) {
+            const long long lg = pg + (dir ? mg : 0), lh = ph + (dir ? mh : 0);
+            const double GL = fx(lg, ep.e_g), HL = fx(lh, ep.e_h);
+            const double GR = fx(Qg - lg, ep.e_g), HR = fx(Qh - lh, ep.e_h);
+            if (!(HL >= ep.mcw && HR >= ep.mcw)) continue;
+            const double gain = eq8_gain(GL, HL, GR, HR, G, H, ep.lambda, ep.gamma);
+            if (gain != gain) continue;
+            Cand c;
+            c.gain = gain;
+            c.order = s * 2 + dir;
+            c.valid = 1;
+            c.lg = lg;
+            c.lh = lh;
+            if (better(c, best)) best = c;
+        }
+    }
+}
+
+// Inclusive wavefront scan of a pair of int64 values.
+__device__ inline void wave_scan2(long long &xg, long long &xh)
+{
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const long long yg = __shfl_up(xg, d, 64), yh = __shfl_up(xh, d, 64);
+        if (lane >= d) {
+            xg += yg;
+            xh += yh;
+        }
+    }
 }
 
 // Best split of one feature for one node, evaluated by one wavefront.  The
@@ -80,6 +142,24 @@ __device__ Cand eval_feature(const longlong2 *__restrict__ hj, int32_t B, long l
     best.gain = 0.0;
     best.order = 0;
     best.lg = best.lh = 0;
+    const double G = fx(Qg, ep.e_g), H = fx(Qh, ep.e_h);
+    if (B <= 256) {
+        // one chunk: the scan's last lane holds the feature's bin totals
+        longlong2 v[4];
+        long long sg = 0, sh = 0;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const int32_t b = lane * 4 + t;
+            v[t] = b < B ? hj[b] : make_longlong2(0, 0);
+            sg += v[t].x;
+            sh += v[t].y;
+        }
+        long long xg = sg, xh = sh;
+        wave_scan2(xg, xh);
+        const long long tg = __shfl(xg, 63, 64), th = __shfl(xh, 63, 64);
+        eval_chunk(v, 0, B, xg - sg, xh - sh, Qg, Qh, Qg - tg, Qh - th, G, H, ep, best);
+        return wave_best(best);
+    }
     // totals over the feature's bins -> missing sums
     long long tg = 0, th = 0;
     for (int32_t b = lane; b < B; b += 64) {
@@ -90,56 +170,72 @@ __device__ Cand eval_feature(const longlong2 *__restrict__ hj, int32_t B, long l
     tg = wave_sum(tg);
     th = wave_sum(th);
     const long long mg = Qg - tg, mh = Qh - th;
-    const double G = fx(Qg, ep.e_g), H = fx(Qh, ep.e_h);
     long long carry_g = 0, carry_h = 0;
     for (int32_t base = 0; base < B; base += 256) {
         longlong2 v[4];
         long long sg = 0, sh = 0;
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-            int32_t b = base + lane * 4 + t;
+            const int32_t b = base + lane * 4 + t;
             v[t] = b < B ? hj[b] : make_longlong2(0, 0);
             sg += v[t].x;
             sh += v[t].y;
         }
-        // exclusive wavefront scan of the lane totals
         long long xg = sg, xh = sh;
-        for (int d = 1; d < 64; d <<= 1) {
-            long long yg = __shfl_up(xg, d, 64), yh = __shfl_up(xh, d, 64);
-            if (lane >= d) {
-                xg += yg;
-                xh += yh;
-            }
-        }
-        long long pg = carry_g + xg - sg, ph = carry_h + xh - sh;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            int32_t b = base + lane * 4 + t;
-            pg += v[t].x;
-            ph += v[t].y;
-            int32_t s = b + 1;  // left = bins < s
-            if (s > B - 1) continue;
-#pragma unroll
-            for (int dir = 0; dir < 2; ++dir) {
-                long long lg = pg + (dir ? mg : 0), lh = ph + (dir ? mh : 0);
-                double GL = fx(lg, ep.e_g), HL = fx(lh, ep.e_h);
-                double GR = fx(Qg - lg, ep.e_g), HR = fx(Qh - lh, ep.e_h);
-                if (!(HL >= ep.mcw && HR >= ep.mcw)) continue;
-                double gain = eq8_gain(GL, HL, GR, HR, G, H, ep.lambda, ep.gamma);
-                if (gain != gain) continue;
-                Cand c;
-                c.gain = gain;
-                c.order = s * 2 + dir;
-                c.valid = 1;
-                c.lg = lg;
-                c.lh = lh;
-                if (better(c, best)) best = c;
-            }
-        }
+        wave_scan2(xg, xh);
+        eval_chunk(v, base, B, carry_g + xg - sg, carry_h + xh - sh, Qg, Qh, mg, mh, G, H, ep, best);
         carry_g += __shfl(xg, 63, 64);
         carry_h += __shfl(xh, 63, 64);
     }
     return wave_best(best);
+}
+
+// The best of node k's per-feature-block candidates as a gbt_split; with
+// `decide` given, a node whose best valid gain is > 0 is also marked as
+// split in the tree driver's node table (depth < max_depth is the caller's).
+__device__ inline void reduce_node(const EvalCand *cand, int32_t n_fblocks, const EvalNode &node, int32_t k,
+                                   gbt_split *__restrict__ out, DevNode *__restrict__ decide)
+{
+    EvalCand b;
+    b.valid = 0;
+    for (int32_t f = 0; f < n_fblocks; ++f) {
+        const EvalCand &o = cand[(int64_t)k * n_fblocks + f];
+        if (!o.valid) continue;
+        if (!b.valid || o.gain > b.gain) b = o;
+    }
+    gbt_split s;
+    s.valid = b.valid;
+    s.gain = b.valid ? b.gain : 0.0;
+    s.feature = b.valid ? b.feature : -1;
+    s.split_bin = b.valid ? b.split_bin : -1;
+    s.default_left = b.valid ? b.default_left : 0;
+    s.left_g = b.valid ? b.lg : 0;
+    s.left_h = b.valid ? b.lh : 0;
+    s.right_g = b.valid ? node.sum_g - b.lg : 0;
+    s.right_h = b.valid ? node.sum_h - b.lh : 0;
+    out[k] = s;
+    if (decide && s.valid && s.gain > 0.0) {
+        DevNode &d = decide[node.heap];
+        d.split = 1;
+        d.feature = s.feature;
+        d.split_bin = s.split_bin;
+        d.default_left = s.default_left;
+        d.gain = s.gain;
+        d.left_g = s.left_g;
+        d.left_h = s.left_h;
+        d.right_g = s.right_g;
+        d.right_h = s.right_h;
+    }
+}
+
+__global__ void k_eval_reduce(const EvalCand *__restrict__ cand, int32_t n_fblocks,
+                              const EvalNode *__restrict__ nodes, int32_t n_nodes,
+                              const int32_t *__restrict__ n_nodes_d, gbt_split *__restrict__ out,
+                              DevNode *__restrict__ decide)
+{
+    int32_t k = blockIdx.x * blockDim.x + threadIdx.x;
+    if (k >= n_nodes || (n_nodes_d && k >= *n_nodes_d)) return;
+    reduce_node(cand, n_fblocks, nodes[k], k, out, decide);
 }
 
 __global__ void __launch_bounds__(kEvalThreads)
@@ -189,49 +285,6 @@ __global__ void __launch_bounds__(kEvalThreads)
             if (!b.valid || o.gain > b.gain || (o.gain == b.gain && o.feature < b.feature)) b = o;
         }
         out[(int64_t)blockIdx.y * gridDim.x + blockIdx.x] = b;
-    }
-}
-
-// Reduce the per-feature-block candidates of each node into a gbt_split.
-// With `decide` given, a node whose best valid gain is > 0 is also marked
-// as split in the tree driver's node table (depth < max_depth is the
-// caller's).
-__global__ void k_eval_reduce(const EvalCand *__restrict__ cand, int32_t n_fblocks,
-                              const EvalNode *__restrict__ nodes, int32_t n_nodes,
-                              const int32_t *__restrict__ n_nodes_d, gbt_split *__restrict__ out,
-                              DevNode *__restrict__ decide)
-{
-    int32_t k = blockIdx.x * blockDim.x + threadIdx.x;
-    if (k >= n_nodes || (n_nodes_d && k >= *n_nodes_d)) return;
-    EvalCand b;
-    b.valid = 0;
-    for (int32_t f = 0; f < n_fblocks; ++f) {
-        const EvalCand &o = cand[(int64_t)k * n_fblocks + f];
-        if (!o.valid) continue;
-        if (!b.valid || o.gain > b.gain) b = o;
-    }
-    gbt_split s;
-    s.valid = b.valid;
-    s.gain = b.valid ? b.gain : 0.0;
-    s.feature = b.valid ? b.feature : -1;
-    s.split_bin = b.valid ? b.split_bin : -1;
-    s.default_left = b.valid ? b.default_left : 0;
-    s.left_g = b.valid ? b.lg : 0;
-    s.left_h = b.valid ? b.lh : 0;
-    s.right_g = b.valid ? nodes[k].sum_g - b.lg : 0;
-    s.right_h = b.valid ? nodes[k].sum_h - b.lh : 0;
-    out[k] = s;
-    if (decide && s.valid && s.gain > 0.0) {
-        DevNode &d = decide[nodes[k].heap];
-        d.split = 1;
-        d.feature = s.feature;
-        d.split_bin = s.split_bin;
-        d.default_left = s.default_left;
-        d.gain = s.gain;
-        d.left_g = s.left_g;
-        d.left_h = s.left_h;
-        d.right_g = s.right_g;
-        d.right_h = s.right_h;
     }
 }
 

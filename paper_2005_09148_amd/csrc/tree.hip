@@ -133,12 +133,6 @@ struct SampleOut {
     SampleState *st = nullptr;
 };
 
-// One int32 from device memory into the pinned host buffer.
-__global__ void k_to_host_i32(const int32_t *__restrict__ src, int32_t *__restrict__ dst)
-{
-    if (threadIdx.x == 0) *dst = *src;
-}
-
 // Alg. 7: g' <- Sample(g); AllocateOnGPU(sampled_page); Compact each page.
 // st_ready: the caller has initialized st and folded the maximum of r into
 // it while computing the gradients.  read_state: copy the threshold,
@@ -181,12 +175,10 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
         }
         // with f = 1 the state keeps T = 0: every row is kept with weight 1
         GBT_TRY(mvs_select(c, src, kind, nullptr, n, sp.mvs_lambda, st, sp.seed, sp.iteration, 0, keep, tile_off));
-        GBT_TRY(keep_tile_offsets(c, n, tile_off));
         // the sample size sizes the buffers below: one round trip
         void *hio, *hio_d;
         GBT_TRY(host_io(c, 64, &hio, &hio_d));
-        k_to_host_i32<<<1, 64, 0, c->stream>>>(tile_off + ntiles, (int32_t *)hio_d);
-        GBT_LAUNCHED();
+        GBT_TRY(keep_tile_offsets(c, n, tile_off, (int32_t *)hio_d));
         GBT_HIP(hipStreamSynchronize(c->stream));
         o->R = *(volatile int32_t *)hio;
         size_t rb = (size_t)mx->row_words * 4;
@@ -221,53 +213,46 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
 }
 
 // ------------------------------------------------------------ tree kernels
-__global__ void k_zero_counter(unsigned long long *p)
-{
-    if (threadIdx.x < kUpdCounters) p[threadIdx.x] = 0ull;
-}
-
 // The node table, the root (its sums from the sampling state), the root
-// level list and counts, and the root histogram's work: R rows in chunks of
-// `chunk` (n_root items) summed into slot 0.
+// level list and counts, the root histogram's work (R rows in chunks of
+// `chunk`, n_root items, summed into slot 0), the identity slot order, and
+// zeroed counters (histogram updates, level statistics).
 __global__ void k_tree_init(DevNode *__restrict__ nodes, int32_t n_nodes, const SampleState *__restrict__ st,
                             int64_t R, EvalNode *__restrict__ level, int32_t *__restrict__ cnt,
                             HistWork *__restrict__ work, HistReduce *__restrict__ red, int64_t chunk,
-                            int32_t n_root)
+                            int32_t n_root, int32_t *__restrict__ rows, int32_t *__restrict__ slot_node,
+                            unsigned long long *__restrict__ upd, unsigned long long *__restrict__ stat)
 {
-    int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-    const long long rg = (long long)fold_sum(st->root_g), rh = (long long)fold_sum(st->root_h);
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < R) {
+        rows[i] = (int32_t)i;
+        slot_node[i] = 0;
+    }
+    if (upd && i < kUpdCounters) upd[i] = 0ull;
+    if (i < 2) stat[i] = 0ull;
     if (i < n_nodes) {
+        const long long rg = (long long)fold_sum(st->root_g), rh = (long long)fold_sum(st->root_h);
         DevNode d;
         memset(&d, 0, sizeof(d));
-        d.left_child = 2 * i + 1;
-        d.right_child = 2 * i + 2;
+        d.left_child = 2 * (int32_t)i + 1;
+        d.right_child = 2 * (int32_t)i + 2;
         if (i == 0) {
             d.present = 1;
             d.sum_g = rg;
             d.sum_h = rh;
             d.begin = 0;
             d.end = R;
+            level[0] = {rg, rh, 0, 0};
+            cnt[0] = 1;
+            cnt[1] = cnt[2] = cnt[3] = 0;
+            red[0] = {0, 0, n_root, -1, -1, 0};
         }
         nodes[i] = d;
     }
     if (i < n_root) {
-        const int64_t b = (int64_t)i * chunk;
-        work[i] = {b, b + chunk < R ? b + chunk : R, i, 0};
+        const int64_t b = i * chunk;
+        work[i] = {b, b + chunk < R ? b + chunk : R, (int32_t)i, 0};
     }
-    if (i == 0) {
-        level[0] = {rg, rh, 0, 0};
-        cnt[0] = 1;
-        cnt[1] = cnt[2] = cnt[3] = 0;
-        red[0] = {0, 0, n_root, -1, -1, 0};
-    }
-}
-
-__global__ void k_rows_init(int32_t *__restrict__ rows, int32_t *__restrict__ slot_node, int64_t R)
-{
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= R) return;
-    rows[i] = (int32_t)i;
-    slot_node[i] = 0;
 }
 
 // Exclusive scan across a 1024-thread block; *total receives the sum.
@@ -813,12 +798,8 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     const bool host_pages = any_host_pages(mx);
     double h2d = 0.0;
 
-    unsigned long long *upd = nullptr;
-    if (stats) {
-        GBT_TRY(scratch_t(c, kScrUpd, kUpdCounters, &upd));
-        k_zero_counter<<<1, 64, 0, c->stream>>>(upd);
-        GBT_LAUNCHED();
-    }
+    unsigned long long *upd = nullptr;  // zeroed with the tree's other counters
+    if (stats) GBT_TRY(scratch_t(c, kScrUpd, kUpdCounters, &upd));
     c->marks.clear();
     c->events_used = 0;
     int mark = timer_begin(c, kPhSample);
@@ -911,17 +892,10 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     const HistGroup *groups_d = (const HistGroup *)mx->groups_d;
     int64_t *partials = nullptr;
     GBT_TRY(scratch(c, kScrPartialsDev, (size_t)std::max(max_items, 1) * mx->total_bins * 16, (void **)&partials));
-    k_tree_init<<<blocks(std::max(NN, n_root)), 256, 0, c->stream>>>(nodes, NN, so.st, R, evA, cnt, work_d,
-                                                                     red_d, root_chunk, n_root);
+    const int64_t n_init = std::max<int64_t>({(int64_t)NN, (int64_t)n_root, R, (int64_t)kUpdCounters});
+    k_tree_init<<<blocks(n_init), 256, 0, c->stream>>>(nodes, NN, so.st, R, evA, cnt, work_d, red_d, root_chunk,
+                                                       n_root, rows, slot_node, upd, stat);
     GBT_LAUNCHED();
-    if (stat) {
-        k_zero_counter<<<1, 64, 0, c->stream>>>(stat);
-        GBT_LAUNCHED();
-    }
-    if (R) {
-        k_rows_init<<<blocks(R), 256, 0, c->stream>>>(rows, slot_node, R);
-        GBT_LAUNCHED();
-    }
     EvalParams ep{p->lambda, p->gamma, p->min_child_weight, 0, 0, e_dev};
     int32_t hist_launches = 0;
     if (D > 0 && R > 0) {
