@@ -408,8 +408,8 @@ __global__ void __launch_bounds__(kPartThreads)
     }
 }
 
-// Left flags before slot x: the tile's offset plus the flags of the tile
-// before x, summed by the 256 threads of the block (16 flags each).
+// Left flags before slot x: the counts of the tiles before x's tile plus the
+// flags of that tile before x, summed by the 256 threads of the block.
 constexpr int kBoundThreads = 256;
 
 __device__ inline uint32_t byte_sum4(uint32_t v)
@@ -417,23 +417,24 @@ __device__ inline uint32_t byte_sum4(uint32_t v)
     return ((v & 0x01010101u) * 0x01010101u) >> 24;  // four 0/1 bytes
 }
 
-__device__ inline int64_t part_prefix(const uint8_t *__restrict__ flags, const int32_t *__restrict__ tile_off,
-                                      int64_t x, int32_t *lds4)
+__device__ inline int64_t part_prefix(const uint8_t *__restrict__ flags, const int32_t *__restrict__ tile_cnt,
+                                      int64_t x, long long *lds4)
 {
     const int64_t t = x / kPartTile, s = t * kPartTile;
     const int64_t j = s + (int64_t)threadIdx.x * 16;
-    uint32_t c = 0;
+    long long c = 0;
     if (j + 16 <= x) {
         const uint4 v = *(const uint4 *)(flags + j);
         c = byte_sum4(v.x) + byte_sum4(v.y) + byte_sum4(v.z) + byte_sum4(v.w);
     } else {
         for (int64_t k = j; k < x; ++k) c += flags[k];
     }
+    for (int64_t k = threadIdx.x; k < t; k += kBoundThreads) c += tile_cnt[k];
     for (int d = 32; d > 0; d >>= 1) c += __shfl_xor(c, d, 64);
     __syncthreads();
-    if ((threadIdx.x & 63) == 0) lds4[threadIdx.x >> 6] = (int32_t)c;
+    if ((threadIdx.x & 63) == 0) lds4[threadIdx.x >> 6] = c;
     __syncthreads();
-    return (int64_t)tile_off[t] + lds4[0] + lds4[1] + lds4[2] + lds4[3];
+    return lds4[0] + lds4[1] + lds4[2] + lds4[3];
 }
 
 // For every splitting node of the list: the left flags before its segment
@@ -441,16 +442,16 @@ __device__ inline int64_t part_prefix(const uint8_t *__restrict__ flags, const i
 __global__ void __launch_bounds__(kBoundThreads)
     k_part_bounds(const EvalNode *__restrict__ list, const int32_t *__restrict__ n_list_d, int32_t n_list,
                   DevNode *__restrict__ nodes, const uint8_t *__restrict__ flags,
-                  const int32_t *__restrict__ tile_off)
+                  const int32_t *__restrict__ tile_cnt)
 {
-    __shared__ int32_t lds4[kBoundThreads / 64];
+    __shared__ long long lds4[kBoundThreads / 64];
     const int32_t count = n_list_d ? *n_list_d : n_list;
     if ((int32_t)blockIdx.x >= count) return;
     const int32_t nid = list ? list[blockIdx.x].heap : (int32_t)blockIdx.x;
     DevNode &d = nodes[nid];
     if (!d.split) return;
-    const int64_t pb = part_prefix(flags, tile_off, d.begin, lds4);
-    const int64_t pe = part_prefix(flags, tile_off, d.end, lds4);
+    const int64_t pb = part_prefix(flags, tile_cnt, d.begin, lds4);
+    const int64_t pe = part_prefix(flags, tile_cnt, d.end, lds4);
     if (threadIdx.x == 0) {
         d.pleft = pb;
         d.nleft = pe - pb;
@@ -462,7 +463,7 @@ __global__ void __launch_bounds__(kBoundThreads)
 // segment, the others after them, both in slot order.
 __global__ void __launch_bounds__(kPartThreads)
     k_part_scatter(const int32_t *__restrict__ rows, int64_t n, const uint8_t *__restrict__ flags,
-                   const int32_t *__restrict__ tile_off, const int32_t *__restrict__ position,
+                   const int32_t *__restrict__ tile_cnt, const int32_t *__restrict__ position,
                    int32_t *__restrict__ position_out,
                    const int32_t *__restrict__ slot_node, int32_t *__restrict__ slot_node_out,
                    const DevNode *__restrict__ nodes, int32_t *__restrict__ rows_out)
@@ -480,8 +481,18 @@ __global__ void __launch_bounds__(kPartThreads)
             if (i0 + k < n) f4 |= (uint32_t)flags[i0 + k] << (8 * k);
     }
     const int32_t mine = (int32_t)((f4 & 1u) + ((f4 >> 8) & 1u) + ((f4 >> 16) & 1u) + ((f4 >> 24) & 1u));
+    // left flags of the tiles before this one (their counts, summed here)
+    __shared__ long long tl16[kPartThreads / 64];
+    long long before = 0;
+    for (int64_t k = threadIdx.x; k < (int64_t)blockIdx.x; k += kPartThreads) before += tile_cnt[k];
+    for (int d = 32; d > 0; d >>= 1) before += __shfl_xor(before, d, 64);
+    if ((threadIdx.x & 63) == 0) tl16[threadIdx.x >> 6] = before;
     int32_t total;
-    int64_t P = (int64_t)tile_off[blockIdx.x] + part_block_scan(mine, lds16, &total);
+    const int32_t in_tile = part_block_scan(mine, lds16, &total);  // synchronizes the block
+    before = 0;
+#pragma unroll
+    for (int w = 0; w < kPartThreads / 64; ++w) before += tl16[w];
+    int64_t P = before + in_tile;
 #pragma unroll
     for (int k = 0; k < kPartItems; ++k) {
         const int64_t i = i0 + k;
@@ -524,10 +535,11 @@ gbt_status partition_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page
     const int64_t tiles = (n + kPartTile - 1) / kPartTile;
     int32_t *tile_off;
     GBT_TRY(scratch_t(c, kScrScan, (size_t)tiles + 1, &tile_off));
+    // tile_off receives each tile's left count; the bounds and the scatter
+    // sum the counts before their tiles themselves
     k_part_flags_tiles<<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(rows, n, page, geo, position, slot_node,
                                                                        nodes, flags, tile_off);
     GBT_LAUNCHED();
-    GBT_TRY(scan_tile_counts(c, tile_off, tiles));
     if (n_list > 0) {
         k_part_bounds<<<(unsigned)n_list, kBoundThreads, 0, c->stream>>>(list, n_list_d, n_list, nodes, flags,
                                                                          tile_off);
