@@ -111,7 +111,7 @@ enum ScratchSlot {
     kScrSel,         // global ids of the sampled rows
     kScrGw,          // reweighted (g', h') in double
     kScrQ,           // fixed-point (q_g, q_h)
-    kScrRows, kScrRowsTmp, kScrPosition, kScrSlotA, kScrSlotB,
+    kScrRows, kScrRowsTmp, kScrPosition, kScrSlotA, kScrSlotB, kScrCand,
     kScrHistA, kScrHistB,
     kScrNodes,       // DevNode table
     kScrEvalNodes,   // EvalNode list

@@ -88,6 +88,18 @@ gbt_status launch_gradients(gbt_ctx *c, int32_t loss, const float *margin, const
 // ------------------------------------------------------------ Philox4x64-10
 // Salmon et al., SC'11: ten rounds of two 64x64->128 multiplies, the key
 // advanced by the Weyl increments between rounds.
+// The full 128-bit product of x and a constant m, from four 32 x 32 -> 64
+// multiply-adds (no partial sum overflows 64 bits).
+__device__ inline void mul_128(uint64_t m, uint64_t x, uint64_t *hi, uint64_t *lo)
+{
+    const uint64_t ml = (uint32_t)m, mh = m >> 32, xl = (uint32_t)x, xh = x >> 32;
+    const uint64_t p0 = xl * ml;
+    const uint64_t p1 = xl * mh + (p0 >> 32);
+    const uint64_t p2 = xh * ml + (uint32_t)p1;
+    *hi = xh * mh + (p1 >> 32) + (p2 >> 32);
+    *lo = (p2 << 32) | (uint32_t)p0;
+}
+
 __device__ inline uint64_t philox_word0(uint64_t c0, uint64_t c1, uint64_t c2, uint64_t c3,
                                         uint64_t k0, uint64_t k1)
 {
@@ -95,8 +107,9 @@ __device__ inline uint64_t philox_word0(uint64_t c0, uint64_t c1, uint64_t c2, u
     constexpr uint64_t kWeyl0 = 0x9E3779B97F4A7C15ull, kWeyl1 = 0xBB67AE8584CAA73Bull;
 #pragma unroll
     for (int round = 0; round < 10; ++round) {
-        uint64_t p0hi = __umul64hi(kMul0, c0), p0lo = kMul0 * c0;
-        uint64_t p1hi = __umul64hi(kMul1, c2), p1lo = kMul1 * c2;
+        uint64_t p0hi, p0lo, p1hi, p1lo;
+        mul_128(kMul0, c0, &p0hi, &p0lo);
+        mul_128(kMul1, c2, &p1hi, &p1lo);
         uint64_t n0 = p1hi ^ c1 ^ k0, n2 = p0hi ^ c3 ^ k1;
         c0 = n0;
         c1 = p1lo;

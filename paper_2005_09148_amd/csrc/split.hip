@@ -288,6 +288,168 @@ __global__ void __launch_bounds__(kEvalThreads)
     }
 }
 
+// ------------------------------------------------------------ reduce + evaluate
+// One block per (feature, reduce item): its 16 waves cover the feature's
+// bins 64 at a time (4 chunks) and every fourth partial (4 subsets); the
+// built node's and the sibling's bins go to hist and to LDS, then wave 0
+// evaluates the built node and wave 1 the sibling on the LDS copy.
+constexpr int kRedEvalThreads = 1024;
+
+__global__ void __launch_bounds__(kRedEvalThreads)
+    k_reduce_eval(const longlong2 *__restrict__ partials, const HistReduce *__restrict__ red,
+                  const int32_t *__restrict__ n_red_d, const longlong2 *__restrict__ parent,
+                  longlong2 *__restrict__ hist, int64_t total_bins, const int32_t *__restrict__ bin_ptr,
+                  int32_t m, const EvalNode *__restrict__ ev, EvalParams ep, EvalCand *__restrict__ cand)
+{
+    if (n_red_d && (int32_t)blockIdx.y >= *n_red_d) return;
+    __shared__ longlong2 hb[256], hs[256];
+    __shared__ long long sg[4][256], sh[4][256];
+    const HistReduce rd = red[blockIdx.y];
+    const int32_t f = blockIdx.x;
+    const int32_t b0 = bin_ptr[f], B = bin_ptr[f + 1] - b0;
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    const int sub = wid >> 2;                 // partial subset
+    const int32_t b = (wid & 3) * 64 + lane;  // bin of the feature (B <= 256)
+    const bool sib = rd.sub_target >= 0;
+    long long g = 0, h = 0;
+    if (b < B) {
+        const longlong2 *src = partials + (int64_t)rd.part0 * total_bins + b0 + b;
+        int32_t k = sub;
+        for (; k + 12 < rd.nparts; k += 16) {
+            const longlong2 v0 = src[(int64_t)k * total_bins], v1 = src[(int64_t)(k + 4) * total_bins];
+            const longlong2 v2 = src[(int64_t)(k + 8) * total_bins], v3 = src[(int64_t)(k + 12) * total_bins];
+            g += (v0.x + v1.x) + (v2.x + v3.x);
+            h += (v0.y + v1.y) + (v2.y + v3.y);
+        }
+        for (; k < rd.nparts; k += 4) {
+            const longlong2 v = src[(int64_t)k * total_bins];
+            g += v.x;
+            h += v.y;
+        }
+    }
+    sg[sub][b] = g;
+    sh[sub][b] = h;
+    __syncthreads();
+    if (sub == 0 && b < B) {
+        for (int t = 1; t < 4; ++t) {
+            g += sg[t][b];
+            h += sh[t][b];
+        }
+        const longlong2 bv = make_longlong2(g, h);
+        hist[(int64_t)rd.slot * total_bins + b0 + b] = bv;
+        hb[b] = bv;
+        if (sib) {
+            const longlong2 pv = parent[(int64_t)rd.sub_parent * total_bins + b0 + b];
+            const longlong2 sv = make_longlong2(pv.x - g, pv.y - h);
+            hist[(int64_t)rd.sub_target * total_bins + b0 + b] = sv;
+            hs[b] = sv;
+        }
+    }
+    __syncthreads();
+    if (wid > (sib ? 1 : 0)) return;
+    const int32_t slot = wid == 0 ? rd.slot : rd.sub_target;
+    if (ep.e_dev) {
+        ep.e_g = ep.e_dev[0];
+        ep.e_h = ep.e_dev[1];
+    }
+    EvalCand o;
+    o.valid = 0;
+    o.gain = 0.0;
+    o.feature = f;
+    o.split_bin = -1;
+    o.default_left = 0;
+    o.lg = o.lh = 0;
+    if (B >= 2) {
+        const EvalNode nd = ev[slot];
+        const Cand cb = eval_feature(wid == 0 ? hb : hs, B, nd.sum_g, nd.sum_h, ep);
+        if (cb.valid) {
+            o.valid = 1;
+            o.gain = cb.gain;
+            o.split_bin = cb.order >> 1;
+            o.default_left = cb.order & 1;
+            o.lg = cb.lg;
+            o.lh = cb.lh;
+        }
+    }
+    if (lane == 0) cand[(int64_t)slot * m + f] = o;
+}
+
+// Each node's best candidate over its features, one wave per node: the
+// highest gain, ties to the lowest feature (candidates are in feature order).
+__global__ void __launch_bounds__(256)
+    k_eval_reduce_wave(const EvalCand *__restrict__ cand, int32_t n_fblocks, const EvalNode *__restrict__ nodes,
+                       int32_t n_nodes, const int32_t *__restrict__ n_nodes_d, gbt_split *__restrict__ out,
+                       DevNode *__restrict__ decide)
+{
+    const int lane = threadIdx.x & 63;
+    const int32_t k = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (k >= n_nodes || (n_nodes_d && k >= *n_nodes_d)) return;
+    // each lane keeps the best of its features (ascending), then the wave
+    // takes the highest gain and, among equal gains, the lowest feature
+    int32_t bi = -1;
+    double bg = 0.0;
+    for (int32_t f = lane; f < n_fblocks; f += 64) {
+        const EvalCand &o = cand[(int64_t)k * n_fblocks + f];
+        if (o.valid && (bi < 0 || o.gain > bg)) {
+            bi = f;
+            bg = o.gain;
+        }
+    }
+    double m = bi >= 0 ? bg : -__builtin_inf();
+    for (int d = 32; d > 0; d >>= 1) m = fmax(m, __shfl_xor(m, d, 64));
+    int32_t best = (bi >= 0 && bg == m) ? bi : 0x7fffffff;
+    for (int d = 32; d > 0; d >>= 1) best = min(best, __shfl_xor(best, d, 64));
+    if (lane != 0) return;
+    const EvalCand b = best != 0x7fffffff ? cand[(int64_t)k * n_fblocks + best] : EvalCand{0.0, 0, 0, -1, -1, 0, 0};
+    const EvalNode node = nodes[k];
+    gbt_split sp;
+    sp.valid = b.valid;
+    sp.gain = b.valid ? b.gain : 0.0;
+    sp.feature = b.valid ? b.feature : -1;
+    sp.split_bin = b.valid ? b.split_bin : -1;
+    sp.default_left = b.valid ? b.default_left : 0;
+    sp.left_g = b.valid ? b.lg : 0;
+    sp.left_h = b.valid ? b.lh : 0;
+    sp.right_g = b.valid ? node.sum_g - b.lg : 0;
+    sp.right_h = b.valid ? node.sum_h - b.lh : 0;
+    out[k] = sp;
+    if (decide && sp.valid && sp.gain > 0.0) {
+        DevNode &d = decide[node.heap];
+        d.split = 1;
+        d.feature = sp.feature;
+        d.split_bin = sp.split_bin;
+        d.default_left = sp.default_left;
+        d.gain = sp.gain;
+        d.left_g = sp.left_g;
+        d.left_h = sp.left_h;
+        d.right_g = sp.right_g;
+        d.right_h = sp.right_h;
+    }
+}
+
+gbt_status reduce_eval_impl(gbt_ctx *c, const gbt_matrix *mx, const int64_t *partials, const HistReduce *red,
+                            const int32_t *n_red_d, int32_t max_red, const int64_t *parent, int64_t *hist,
+                            const EvalNode *ev, const EvalParams &ep, EvalCand *cand)
+{
+    if (max_red <= 0) return GBT_OK;
+    dim3 grid((unsigned)mx->m, (unsigned)max_red);
+    k_reduce_eval<<<grid, kRedEvalThreads, 0, c->stream>>>((const longlong2 *)partials, red, n_red_d,
+                                                           (const longlong2 *)parent, (longlong2 *)hist,
+                                                           mx->total_bins, mx->bin_ptr_d, mx->m, ev, ep, cand);
+    GBT_LAUNCHED();
+    return GBT_OK;
+}
+
+gbt_status eval_reduce_impl(gbt_ctx *c, const EvalCand *cand, int32_t n_fblocks, const EvalNode *nodes_d,
+                            int32_t n_nodes, const int32_t *n_nodes_d, gbt_split *out_d, DevNode *decide)
+{
+    if (n_nodes <= 0) return GBT_OK;
+    k_eval_reduce_wave<<<(n_nodes + 3) / 4, 256, 0, c->stream>>>(cand, n_fblocks, nodes_d, n_nodes, n_nodes_d,
+                                                                 out_d, decide);
+    GBT_LAUNCHED();
+    return GBT_OK;
+}
+
 gbt_status eval_impl(gbt_ctx *c, const gbt_matrix *mx, const int64_t *hist, const EvalNode *nodes_d,
                      int32_t n_nodes, const EvalParams &ep, gbt_split *out_d, const int32_t *n_nodes_d,
                      DevNode *decide)

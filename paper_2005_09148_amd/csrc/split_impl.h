@@ -3,6 +3,7 @@
 #pragma once
 
 #include "common.h"
+#include "hist_impl.h"
 
 namespace gbt {
 
@@ -35,6 +36,20 @@ struct EvalCand {
 gbt_status eval_impl(gbt_ctx *c, const gbt_matrix *mx, const int64_t *hist, const EvalNode *nodes_d,
                      int32_t n_nodes, const EvalParams &ep, gbt_split *out_d,
                      const int32_t *n_nodes_d = nullptr, DevNode *decide = nullptr);
+// The tree driver's fused step after a histogram pass whose features all
+// have at most 256 bins: for every reduce item (count *n_red_d, at most
+// max_red) and feature, sum the built node's partials into hist, write the
+// sibling as parent minus it, and evaluate the feature for both nodes (the
+// EvalNode of a histogram slot is ev[slot]); cand[slot * m + feature]
+// receives the candidates.  Then eval_reduce_impl picks each node's split.
+gbt_status reduce_eval_impl(gbt_ctx *c, const gbt_matrix *mx, const int64_t *partials, const HistReduce *red,
+                            const int32_t *n_red_d, int32_t max_red, const int64_t *parent, int64_t *hist,
+                            const EvalNode *ev, const EvalParams &ep, EvalCand *cand);
+// Each listed node's best split from cand (n_fblocks entries per node);
+// count *n_nodes_d (at most n_nodes); decide as in eval_impl.
+gbt_status eval_reduce_impl(gbt_ctx *c, const EvalCand *cand, int32_t n_fblocks, const EvalNode *nodes_d,
+                            int32_t n_nodes, const int32_t *n_nodes_d, gbt_split *out_d, DevNode *decide);
+
 // Stable partition of rows[0, n) by each slot's node (slot_node[i], or
 // position[rows[i]] when slot_node is NULL): the rows of every splitting
 // node go left or right within its segment.  rows_out receives the new

@@ -897,18 +897,32 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
                                                        n_root, rows, slot_node, upd, stat);
     GBT_LAUNCHED();
     EvalParams ep{p->lambda, p->gamma, p->min_child_weight, 0, 0, e_dev};
+    // features of at most 256 bins: each histogram pass ends with the fused
+    // reduce + evaluate step, which evaluates the pass's nodes
+    int32_t max_feature_bins = 0;
+    for (int32_t f = 0; f < mx->m; ++f)
+        max_feature_bins = std::max(max_feature_bins, mx->bin_ptr_h[f + 1] - mx->bin_ptr_h[f]);
+    const bool fused = max_feature_bins <= 256;
+    EvalCand *cand = nullptr;
+    if (fused) GBT_TRY(scratch_t(c, kScrCand, (size_t)max_level_nodes * std::max(mx->m, 1), &cand));
     int32_t hist_launches = 0;
+    int32_t *cntA = cnt, *cntB = cnt + 1;
     if (D > 0 && R > 0) {
-        HistLaunch hl{hp.kind, groups_d, G, hp.max_groups_bins, work_d, nullptr, n_root, red_d, nullptr, 1,
-                      partials};
+        HistLaunch hl{hp.kind, groups_d, G, hp.max_groups_bins, work_d, nullptr, n_root, red_d, nullptr,
+                      fused ? 0 : 1, partials};
         GBT_TRY(hist_launch_device(c, mx, so.page, so.q, nullptr, hl, nullptr, histA, upd));
         ++hist_launches;
+        if (fused) {
+            mark = timer_begin(c, kPhHistAux);
+            GBT_TRY(reduce_eval_impl(c, mx, partials, red_d, nullptr, 1, nullptr, histA, evA, ep, cand));
+            GBT_TRY(eval_reduce_impl(c, cand, mx->m, evA, 1, cntA, splits_d, nodes));
+            timer_end(c, mark);
+        }
     }
-    int32_t *cntA = cnt, *cntB = cnt + 1;
     for (int32_t d = 0; d < D; ++d) {
         const int32_t maxn = (int32_t)std::min<int64_t>((int64_t)1 << d, max_level_nodes);
         mark = timer_begin(c, kPhSplit);
-        GBT_TRY(eval_impl(c, mx, histA, evA, maxn, ep, splits_d, cntA, nodes));
+        if (!fused && R > 0) GBT_TRY(eval_impl(c, mx, histA, evA, maxn, ep, splits_d, cntA, nodes));
         GBT_TRY(partition_impl(c, mx, so.page, rows, R, nullptr, slot_node, slot_tmp, nodes, evA, cntA, maxn,
                                rows_tmp));
         std::swap(rows, rows_tmp);
@@ -921,10 +935,18 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         }
         timer_end(c, mark);
         if (plan_next) {
-            HistLaunch hl{hp.kind, groups_d, G, hp.max_groups_bins, work_d, cnt + 2, max_work, red_d, cnt + 3, maxn,
-                          partials};
+            HistLaunch hl{hp.kind, groups_d, G, hp.max_groups_bins, work_d, cnt + 2, max_work, red_d, cnt + 3,
+                          fused ? 0 : maxn, partials};
             GBT_TRY(hist_launch_device(c, mx, so.page, so.q, rows, hl, histA, histB, upd));
             ++hist_launches;
+            if (fused) {
+                // the next level: at most 2 maxn nodes, in evB
+                const int32_t nxt = (int32_t)std::min<int64_t>(2 * (int64_t)maxn, max_level_nodes);
+                mark = timer_begin(c, kPhHistAux);
+                GBT_TRY(reduce_eval_impl(c, mx, partials, red_d, cnt + 3, maxn, histA, histB, evB, ep, cand));
+                GBT_TRY(eval_reduce_impl(c, cand, mx->m, evB, nxt, cntB, splits_d, nodes));
+                timer_end(c, mark);
+            }
             std::swap(histA, histB);
             std::swap(evA, evB);
             std::swap(cntA, cntB);

@@ -428,6 +428,20 @@ def test_out_of_core_sampled_matches_oracle(gbt, ctx, hist_kernel):
     assert_same_trees(*r[:4])
 
 
+def test_empty_sample_tree(gbt, ctx, hist_kernel):
+    """All gradients zero, MVS lambda 0 and f < 1: every key sqrt(g^2 + 0 h^2)
+    is 0, no row is kept, and the tree is one leaf (the oracle's empty-sample
+    case); a previous tree on the same context must leave no trace."""
+    d = datagen.config3(n=5000, m=8)
+    train_both(gbt, ctx, d["X"], d["y"], datagen.TrainConfig("t", 1, 64, 4, 1, eta=0.3, f=0.5), 1)
+    cfg = datagen.TrainConfig("t", 1, 64, 4, 1, eta=0.3, f=0.5, mvs_lambda=0.0)
+    y0 = np.full(len(d["y"]), cfg.base_margin, np.float32)  # squared error: g = 0
+    trees, margin, otrees, omargin, _, _ = train_both(gbt, ctx, d["X"], y0, cfg, 2)
+    assert_same_trees(trees, margin, otrees, omargin)
+    assert all(t.stats.n_sampled == 0 for t in trees)
+    assert trees[0].nodes["flags"][0] & orc.NODE_LEAF
+
+
 @pytest.mark.parametrize("depth,n", [(0, 1000), (1, 65), (3, 1), (4, 63)])
 def test_degenerate_trees(gbt, ctx, hist_kernel, depth, n):
     cfg = datagen.TrainConfig("t", 1, 32, depth, 2, eta=0.5, f=0.5 if n > 10 else 1.0)
