@@ -26,8 +26,9 @@ constexpr int kLdsBins = 4096;
 // four workgroups fit a CU's LDS.
 constexpr int kDenseBins = 2560;
 
-// A dense group spans at most this many words of a row and this many features.
-constexpr int kGroupWords = 8;
+// A dense group's bits lie within this many words from its first word (one
+// 16-byte load), and it holds at most this many features.
+constexpr int kGroupWords = 4;
 constexpr int kMaxGroupFeat = 32;
 
 // Zero nb entries of the g sums at sg and of the h sums at sh.
@@ -60,12 +61,16 @@ __device__ inline void lds_flush(const unsigned long long *sg, const unsigned lo
 }
 
 // Dense rows: slot j holds feature j, W bits per symbol.  Each lane owns one
-// row at a time: it fetches the next row's pair and group words while it
-// decodes the current row.  The group's words are first shifted so that
-// feature u of the group starts at bit u*W of the word window; with W a
-// compile-time constant every symbol is then one bit-field extract from a
+// row at a time: it fetches the next row's pair and the group's words while
+// it decodes the current row.  A group's bits lie within four words from its
+// first word, so the words arrive in one 16-byte load (dword aligned) and
+// cost the memory pipeline one cache access per row.  After one funnel
+// shift per word, feature u of the group starts at bit u*W of the window;
+// with W a compile-time constant every symbol is one bit-field extract from a
 // fixed register.  Null symbols are masked off; the update count comes from
 // the wave's ballot.
+typedef uint32_t u32x4_a4 __attribute__((ext_vector_type(4), aligned(4)));
+
 template <int W, bool kRows>
 __global__ void __launch_bounds__(kHistThreads)
     k_hist_dense(const uint32_t *__restrict__ page, int32_t row_words, uint32_t null_sym,
@@ -84,6 +89,10 @@ __global__ void __launch_bounds__(kHistThreads)
     unsigned long long *sg = lds, *sh = lds + kDenseBins;
     constexpr uint32_t kMask = (1u << W) - 1u;
     constexpr int kMaxF = (kGroupWords * 32 / W) < kMaxGroupFeat ? (kGroupWords * 32 / W) : kMaxGroupFeat;
+    // the 16-byte window starts at the group's first word, or ends at the
+    // row's last word when the group sits in the row's last three words
+    const int32_t ws = gr.w0 < row_words - kGroupWords ? gr.w0 : row_words - kGroupWords;
+    const int32_t dw = gr.w0 - ws;  // 0..3 words, the same in every lane
     // byte address of each feature's first g sum (uniform)
     char *base[kMaxF];
 #pragma unroll
@@ -93,22 +102,29 @@ __global__ void __launch_bounds__(kHistThreads)
     unsigned int cnt = 0;  // this wave's updates
     int64_t i = wk.begin + threadIdx.x;
     longlong2 qn = make_longlong2(0, 0);
-    uint32_t wn[kGroupWords];
+    u32x4_a4 wn = {0u, 0u, 0u, 0u};
     auto fetch = [&](int64_t ii) {
         const int64_t r = kRows ? (int64_t)rows[ii] : ii;
         qn = q[r];
-        const uint32_t *p = page + r * row_words + gr.w0;
-#pragma unroll
-        for (int k = 0; k < kGroupWords; ++k) wn[k] = k < gr.nw ? p[k] : 0u;
+        wn = *(const u32x4_a4 *)(page + r * row_words + ws);
     };
     if (i < wk.end) fetch(i);
     for (; i < wk.end; i += kHistThreads) {
         const unsigned long long qg = (unsigned long long)qn.x, qh = (unsigned long long)qn.y;
-        uint32_t a[kGroupWords];
-        // a[k] = bits [32k + skip, 32k + skip + 32) of the group's words
+        uint32_t y[kGroupWords + 1] = {wn.x, wn.y, wn.z, wn.w, 0u};
+        if (dw) {  // uniform: drop the dw words before the group
 #pragma unroll
-        for (int k = 0; k < kGroupWords; ++k)
-            a[k] = __builtin_amdgcn_alignbit(k + 1 < kGroupWords ? wn[k + 1] : 0u, wn[k], (uint32_t)gr.skip);
+            for (int k = 0; k < kGroupWords; ++k) {
+                const uint32_t y1 = k + 1 < kGroupWords ? y[k + 1] : 0u, y2 = k + 2 < kGroupWords ? y[k + 2] : 0u,
+                               y3 = k + 3 < kGroupWords ? y[k + 3] : 0u;
+                y[k] = dw == 1 ? y1 : (dw == 2 ? y2 : y3);
+            }
+        }
+        // a[k] = bits [32k + skip, 32k + skip + 32) of the group's words
+        uint32_t a[kGroupWords + 1];
+#pragma unroll
+        for (int k = 0; k < kGroupWords; ++k) a[k] = __builtin_amdgcn_alignbit(y[k + 1], y[k], (uint32_t)gr.skip);
+        a[kGroupWords] = 0u;
         if (i + kHistThreads < wk.end) fetch(i + kHistThreads);
 #pragma unroll
         for (int u = 0; u < kMaxF; ++u) {
@@ -398,8 +414,6 @@ static bool dense_groups(const gbt_matrix *mx, int64_t max_bins, int max_feat, i
     const int64_t tb = mx->total_bins;
     const int64_t G = std::max<int64_t>(
         {(int64_t)1, (tb + max_bins - 1) / max_bins, ((int64_t)mx->m + max_feat - 1) / max_feat});
-    const int64_t target_bins = (tb + G - 1) / G;
-    const int64_t target_feat = (mx->m + G - 1) / G;
     auto fits = [&](int32_t f0, int32_t f1) {
         const int64_t b0 = (int64_t)f0 * mx->w, b1 = (int64_t)f1 * mx->w;
         const int32_t nw = (int32_t)((b1 + 31) / 32 - b0 / 32);
@@ -409,8 +423,12 @@ static bool dense_groups(const gbt_matrix *mx, int64_t max_bins, int max_feat, i
                mx->bin_ptr_h[f1] - mx->bin_ptr_h[f0] <= max_bins && (!rot || (f1 - f0) * mx->w <= 192);
     };
     int32_t f0 = 0;
+    int64_t left = G;  // groups still to form; each takes an equal share of what remains
     while (f0 < mx->m) {
         if (!fits(f0, f0 + 1)) return false;
+        const int64_t share = std::max<int64_t>(1, left--);
+        const int64_t target_bins = (tb - mx->bin_ptr_h[f0] + share - 1) / share;
+        const int64_t target_feat = (mx->m - f0 + share - 1) / share;
         int32_t f1 = f0 + 1;
         while (f1 < mx->m && fits(f0, f1 + 1) && mx->bin_ptr_h[f1 + 1] - mx->bin_ptr_h[f0] <= target_bins &&
                f1 + 1 - f0 <= target_feat)
