@@ -117,6 +117,8 @@ def parse():
     ap.add_argument("--rows", type=int, default=None, help="override the row count (testing)")
     ap.add_argument("--f", type=float, default=None, help="override the sampling fraction")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--hist-kernel", default="auto", choices=["auto", "plain", "rotated"],
+                    help="dense histogram kernel (auto: the library's choice by pass size)")
     ap.add_argument("--cpu-trees", type=int, default=2)
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarize two rocprofv3 --pmc runs of this script (no GPU work)")
@@ -341,6 +343,7 @@ def main():
           file=sys.stderr, flush=True)
 
     ctx = gbt.Context(0)
+    ctx.set_hist_kernel({"auto": ctx.HIST_AUTO, "plain": ctx.HIST_PLAIN, "rotated": ctx.HIST_ROTATED}[args.hist_kernel])
     t = time.perf_counter()
     mx = gbt.gbt_quantize(ctx, X, max_bin=cfg.max_bin)
     info = mx.info()

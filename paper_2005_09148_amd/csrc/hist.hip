@@ -149,24 +149,39 @@ __global__ void __launch_bounds__(kHistThreads)
 }
 
 // ---------------------------------------------------------------- rotated
-// Dense rows whose features have at most 256 bins.  One row per lane; a
-// group holds at most 16 features.  The LDS sums are 256 bin rows of 16
-// columns, column c holding one feature, so the address of (feature, bin) is
-// bin*128 + column*8 and its LDS bank pair is set by the column.  Lane l
+// Dense rows whose features have at most 256 bins (symbols of at most 9
+// bits).  One row per lane; a group holds at most 16 features whose bits lie
+// within four words from its first word (one 16-byte load, as in the plain
+// kernel).  The LDS sums are 256 bin rows of 16 columns, column c holding
+// one feature, so the address of (feature, bin) is bin*128 + column*8 and
+// its LDS bank pair is set by the column and the bin's parity.  Lane l
 // visits the group's features starting at feature l mod nf: in every atomic
-// the 64 lanes spread over the features, hence over the bank pairs, instead
-// of colliding at random bins of one feature.  The rotation is applied once
-// per row to the group's bit string (a per-lane funnel shift), so each
-// step's symbol is still a fixed bit field.  The row's group words come
-// from two 16-byte loads.
-constexpr int kRotThreads = 1024;
+// the 64 lanes spread over the columns instead of colliding at random bins
+// of one feature.  The rotation is applied once per row: the group's bit
+// string S (nf*W bits) is doubled to D = S | S << nf*W (a shift that is the
+// same in every lane), and each lane takes D >> (c0*W), so each step's
+// symbol is still a fixed bit field.  Two workgroups share a CU.
+constexpr int kRotThreads = 512;
 constexpr int kRotCols = 16;
 constexpr int kRotBins = 256;
-constexpr int kRotWords = 6;  // bit string of a group: at most 192 bits
+constexpr int kRotMaxW = 9;
 // rows per tree level from which the rotated kernel is chosen by default
 constexpr int64_t kRotMinRows = (int64_t)2 << 20;
 
 __device__ inline uint32_t pick(bool c, uint32_t a, uint32_t b) { return c ? a : b; }
+
+// D[k] = S[k] | word k of (S << nfw), for the word part lq of the shift
+template <int lq>
+__device__ inline void shl_words(const uint32_t S[kGroupWords], uint32_t sh, uint32_t D[2 * kGroupWords])
+{
+#pragma unroll
+    for (int k = 0; k < 2 * kGroupWords; ++k) {
+        const int j = k - lq;
+        const uint32_t hi = (j + 1 >= 0 && j + 1 < kGroupWords) ? S[j + 1] : 0u;
+        const uint32_t lo = (j >= 0 && j < kGroupWords) ? S[j] : 0u;
+        D[k] = (k < kGroupWords ? S[k] : 0u) | __builtin_amdgcn_alignbit(hi, lo, sh);
+    }
+}
 
 template <int W, bool kRows>
 __global__ void __launch_bounds__(kRotThreads)
@@ -185,7 +200,7 @@ __global__ void __launch_bounds__(kRotThreads)
     const HistGroup gr = groups[L % n_groups];
     const int32_t nf = gr.f1 - gr.f0;
     constexpr uint32_t kMask = (1u << W) - 1u;
-    constexpr int kMaxF = (kRotWords * 32 / W) < kRotCols ? (kRotWords * 32 / W) : kRotCols;
+    constexpr int kMaxF = (kGroupWords * 32 / W) < kRotCols ? (kGroupWords * 32 / W) : kRotCols;
 
     for (int t = threadIdx.x; t < 2 * kH; t += kRotThreads) lds[t] = 0ull;
     __syncthreads();
@@ -201,87 +216,78 @@ __global__ void __launch_bounds__(kRotThreads)
         c = c >= nf ? c - nf : c;
         colb[u] = (uint32_t)c * 8u;
     }
-    const int wq0 = gr.w0 & ~3, ws = gr.w0 & 3;
-    const bool second = wq0 + 4 < gr.w0 + gr.nw;
-    const int nfw = nf * W;
-    // rotation: R = (S >> rho) | (S << (nfw - rho)) over the group's nfw bits
-    const int rho = c0 * W, rw = rho >> 5, rb = rho & 31;
-    const int lam = nfw - rho, lw = lam >> 5, lb = lam & 31;
-    uint32_t keep[kRotWords];
+    const int32_t ws = gr.w0 < row_words - kGroupWords ? gr.w0 : row_words - kGroupWords;
+    const int32_t dw = gr.w0 - ws;  // words before the group in the window (uniform)
+    const int nfw = nf * W;         // bits of the group, at most 128
+    // bits of S: keep[k] masks word k
+    uint32_t keep[kGroupWords];
 #pragma unroll
-    for (int k = 0; k < kRotWords; ++k) {
+    for (int k = 0; k < kGroupWords; ++k) {
         const int lo = k * 32;
         keep[k] = nfw >= lo + 32 ? 0xffffffffu : (nfw <= lo ? 0u : ((1u << (nfw - lo)) - 1u));
     }
+    // D = S | S << nfw: word k of S << nfw is bits [32k - nfw, 32k - nfw + 32)
+    // of S, a funnel of S[k - lq + 1] and S[k - lq] by (-nfw) mod 32
+    const int lq = (nfw + 31) >> 5;
+    const uint32_t sh_nfw = (uint32_t)(-nfw) & 31u;
+    // lane's rotation: D >> rho
+    const int rho = c0 * W, rw = rho >> 5, rb = rho & 31;
     char *const base = (char *)lds;
 
     unsigned int cnt = 0;  // this wave's updates
     int64_t i = wk.begin + threadIdx.x;
     longlong2 qn = make_longlong2(0, 0);
-    uint4 v0 = make_uint4(0u, 0u, 0u, 0u), v1 = v0;
-    // row ids run one iteration ahead of the row data they address
-    auto row_of = [&](int64_t ii) -> int64_t { return kRows ? (int64_t)rows[ii] : ii; };
-    auto fetch = [&](int64_t r) {
+    u32x4_a4 wn = {0u, 0u, 0u, 0u};
+    auto fetch = [&](int64_t ii) {
+        const int64_t r = kRows ? (int64_t)rows[ii] : ii;
         qn = q[r];
-        const uint4 *p = (const uint4 *)(page + r * row_words + wq0);
-        v0 = p[0];
-        v1 = second ? p[1] : make_uint4(0u, 0u, 0u, 0u);
+        wn = *(const u32x4_a4 *)(page + r * row_words + ws);
     };
-    int64_t r_next = 0;
-    if (i < wk.end) fetch(row_of(i));
-    if (i + kRotThreads < wk.end) r_next = row_of(i + kRotThreads);
+    if (i < wk.end) fetch(i);
     for (; i < wk.end; i += kRotThreads) {
         const unsigned long long qg = (unsigned long long)qn.x, qh = (unsigned long long)qn.y;
-        const uint32_t x[10] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w, 0u, 0u};
-        if (i + kRotThreads < wk.end) fetch(r_next);
-        if (i + 2 * kRotThreads < wk.end) r_next = row_of(i + 2 * kRotThreads);
-        // the group's words: y[k] = x[k + ws] (ws is the same for every lane)
-        uint32_t t1[9], y[kRotWords + 1];
+        uint32_t y[kGroupWords + 1] = {wn.x, wn.y, wn.z, wn.w, 0u};
+        if (i + kRotThreads < wk.end) fetch(i + kRotThreads);
+        if (dw) {  // uniform: drop the dw words before the group
 #pragma unroll
-        for (int k = 0; k < 9; ++k) t1[k] = pick(ws & 1, x[k + 1], x[k]);
-#pragma unroll
-        for (int k = 0; k <= kRotWords; ++k) y[k] = pick(ws & 2, k + 2 < 9 ? t1[k + 2] : 0u, t1[k]);
-        // S: the group's bit string from bit 0
-        uint32_t a[kRotWords];
-#pragma unroll
-        for (int k = 0; k < kRotWords; ++k)
-            a[k] = __builtin_amdgcn_alignbit(y[k + 1], y[k], (uint32_t)gr.skip) & keep[k];
-        // S >> rho: word shift rw (0..5) by three selects, then the bit shift
-        uint32_t s1[kRotWords + 4], s2[kRotWords + 4], s3[kRotWords + 1], rr[kRotWords];
-#pragma unroll
-        for (int k = 0; k < kRotWords + 4; ++k) {
-            const uint32_t z0 = k < kRotWords ? a[k] : 0u, z1 = k + 1 < kRotWords ? a[k + 1] : 0u;
-            s1[k] = pick(rw & 1, z1, z0);
-        }
-#pragma unroll
-        for (int k = 0; k < kRotWords + 4; ++k) s2[k] = pick(rw & 2, k + 2 < kRotWords + 4 ? s1[k + 2] : 0u, s1[k]);
-#pragma unroll
-        for (int k = 0; k <= kRotWords; ++k) s3[k] = pick(rw & 4, k + 4 < kRotWords + 4 ? s2[k + 4] : 0u, s2[k]);
-#pragma unroll
-        for (int k = 0; k < kRotWords; ++k) rr[k] = __builtin_amdgcn_alignbit(s3[k + 1], s3[k], (uint32_t)rb);
-        // S << lam: word k = funnel of a[k - lw] and a[k - lw - 1]
-        uint32_t rot[kRotWords];
-#pragma unroll
-        for (int k = 0; k < kRotWords; ++k) {
-            uint32_t hw = 0u, lw_ = 0u;
-#pragma unroll
-            for (int j = 0; j <= kRotWords; ++j) {
-                const bool c = lw == j;
-                hw = c ? (k - j >= 0 ? a[k - j] : 0u) : hw;
-                lw_ = c ? (k - j - 1 >= 0 ? a[k - j - 1] : 0u) : lw_;
+            for (int k = 0; k < kGroupWords; ++k) {
+                const uint32_t y1 = k + 1 < kGroupWords ? y[k + 1] : 0u, y2 = k + 2 < kGroupWords ? y[k + 2] : 0u,
+                               y3 = k + 3 < kGroupWords ? y[k + 3] : 0u;
+                y[k] = dw == 1 ? y1 : (dw == 2 ? y2 : y3);
             }
-            const uint32_t ls = lb ? ((hw << lb) | (lw_ >> (32 - lb))) : hw;
-            rot[k] = rr[k] | ls;
         }
+        // S: the group's bit string from bit 0, zero above nfw
+        uint32_t S[kGroupWords];
+#pragma unroll
+        for (int k = 0; k < kGroupWords; ++k)
+            S[k] = __builtin_amdgcn_alignbit(y[k + 1], y[k], (uint32_t)gr.skip) & keep[k];
+        // D, eight words; the shift by nfw is the same in every lane (a scalar branch)
+        uint32_t D[2 * kGroupWords];
+        switch (lq) {
+            case 0: shl_words<0>(S, sh_nfw, D); break;
+            case 1: shl_words<1>(S, sh_nfw, D); break;
+            case 2: shl_words<2>(S, sh_nfw, D); break;
+            case 3: shl_words<3>(S, sh_nfw, D); break;
+            default: shl_words<4>(S, sh_nfw, D); break;
+        }
+        // R = D >> rho (word shift rw = 0..3 by two selects, then the bit shift)
+        uint32_t s1[7], s2[5], R[kGroupWords + 1];
+#pragma unroll
+        for (int k = 0; k < 7; ++k) s1[k] = pick(rw & 1, D[k + 1], D[k]);
+#pragma unroll
+        for (int k = 0; k < 5; ++k) s2[k] = pick(rw & 2, s1[k + 2], s1[k]);
+#pragma unroll
+        for (int k = 0; k < kGroupWords; ++k) R[k] = __builtin_amdgcn_alignbit(s2[k + 1], s2[k], (uint32_t)rb);
+        R[kGroupWords] = 0u;
 #pragma unroll
         for (int u = 0; u < kMaxF; ++u) {
             if (u < nf) {
                 const int bit = u * W, k = bit >> 5, sft = bit & 31;
                 uint32_t sym;
                 if (sft + W <= 32)
-                    sym = (rot[k] >> sft) & kMask;
+                    sym = (R[k] >> sft) & kMask;
                 else
-                    sym = __builtin_amdgcn_alignbit(rot[k + 1], rot[k], (uint32_t)sft) & kMask;
+                    sym = __builtin_amdgcn_alignbit(R[k + 1], R[k], (uint32_t)sft) & kMask;
                 // symbols outside the bin range (only in a malformed page) are skipped
                 const bool ok = sym != null_sym && sym < (uint32_t)kRotBins;
                 cnt += (unsigned int)__popcll(__ballot(ok));
@@ -407,7 +413,7 @@ __global__ void __launch_bounds__(kRedBins * kRedSplit)
 // Feature groups: contiguous features with about equal bin counts, each
 // group within its kernel's limits (LDS bins; for dense rows also the words
 // and features one lane decodes).
-static bool dense_groups(const gbt_matrix *mx, int64_t max_bins, int max_feat, int max_words, bool rot,
+static bool dense_groups(const gbt_matrix *mx, int64_t max_bins, int max_feat, int max_words,
                          std::vector<HistGroup> *out)
 {
     out->clear();
@@ -417,10 +423,7 @@ static bool dense_groups(const gbt_matrix *mx, int64_t max_bins, int max_feat, i
     auto fits = [&](int32_t f0, int32_t f1) {
         const int64_t b0 = (int64_t)f0 * mx->w, b1 = (int64_t)f1 * mx->w;
         const int32_t nw = (int32_t)((b1 + 31) / 32 - b0 / 32);
-        // the rotated kernel reads the words from a 16-byte aligned window of 8
-        const int32_t need = rot ? (int32_t)((b0 >> 5) & 3) + nw : nw;
-        return need <= max_words && f1 - f0 <= max_feat &&
-               mx->bin_ptr_h[f1] - mx->bin_ptr_h[f0] <= max_bins && (!rot || (f1 - f0) * mx->w <= 192);
+        return nw <= max_words && f1 - f0 <= max_feat && mx->bin_ptr_h[f1] - mx->bin_ptr_h[f0] <= max_bins;
     };
     int32_t f0 = 0;
     int64_t left = G;  // groups still to form; each takes an equal share of what remains
@@ -486,13 +489,13 @@ gbt_status hist_plan(const gbt_matrix *mx, int64_t rows_hint, int choice, HistPl
         // the rotated kernel pays off on large passes; smaller ones keep more
         // workgroups per CU with the plain kernel
         const bool want_rot = choice == GBT_HIST_ROTATED || (choice == GBT_HIST_AUTO && rows_hint >= kRotMinRows);
-        if (want_rot && max_feature_bins <= kRotBins &&
-            dense_groups(mx, (int64_t)kRotBins * kRotCols, kRotCols, 8, true, &out->groups)) {
+        if (want_rot && max_feature_bins <= kRotBins && mx->w <= kRotMaxW &&
+            dense_groups(mx, (int64_t)kRotBins * kRotCols, kRotCols, kGroupWords, &out->groups)) {
             out->kind = kHistRot;
             out->threads = kRotThreads;
-            out->target_wgs = kCUs;  // one 1024-thread workgroup per CU
+            out->target_wgs = 2 * kCUs;  // two workgroups per CU
         } else {
-            if (!dense_groups(mx, kDenseBins, kMaxGroupFeat, kGroupWords, false, &out->groups))
+            if (!dense_groups(mx, kDenseBins, kMaxGroupFeat, kGroupWords, &out->groups))
                 return set_error(GBT_E_UNSUPPORTED, "no feature grouping fits the histogram kernel");
             out->kind = kHistDense;
             out->threads = kHistThreads;
@@ -602,7 +605,7 @@ gbt_status hist_launch_device(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
 #define GBT_HIST_ROT(WB)                                                                                 \
     case WB:                                                                                             \
         if (rows)                                                                                        \
-            k_hist_rot<WB, true><<<grid, kRotThreads, lds, c->stream>>>(page, mx->row_words, null_sym, qq,  \
+            k_hist_rot<WB, true><<<grid, kRotThreads, lds, c->stream>>>(page, mx->row_words, null_sym, qq, \
                                                                        rows, hl.work, hl.groups, G,      \
                                                                        hl.n_work_d, mx->bin_ptr_d, tb,   \
                                                                        partials, upd);                   \
@@ -622,9 +625,8 @@ gbt_status hist_launch_device(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
             GBT_HIST_ROT(7)
             GBT_HIST_ROT(8)
             GBT_HIST_ROT(9)
-            GBT_HIST_ROT(10)
-            GBT_HIST_ROT(11)
-            GBT_HIST_ROT(12)
+            default:
+                return set_error(GBT_E_UNSUPPORTED, "rotated histogram kernel with %d-bit symbols", mx->w);
         }
 #undef GBT_HIST_ROT
         GBT_LAUNCHED();
@@ -650,7 +652,7 @@ gbt_status hist_launch_device(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
 #define GBT_HIST_DENSE(WB)                                                                                  \
     case WB:                                                                                                \
         if (rows)                                                                                           \
-            k_hist_dense<WB, true><<<grid, kHistThreads, lds, c->stream>>>(page, mx->row_words, null_sym, qq,  \
+            k_hist_dense<WB, true><<<grid, kHistThreads, lds, c->stream>>>(page, mx->row_words, null_sym, qq, \
                                                                           rows, hl.work, hl.groups, G,      \
                                                                           hl.n_work_d, mx->bin_ptr_d, tb,   \
                                                                           partials, upd);                   \
