@@ -578,11 +578,11 @@ gbt_status build_hist_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *pag
     if (stats && !work.empty()) {
         // algorithmic bytes: the packed symbols of each row, its 16-byte
         // fixed-point pair, its 4-byte row id (when indirect), and one write
-        // of every chunk's partial histogram
+        // of every built node's histogram
         int64_t wbytes = 4 * (((int64_t)mx->stride * mx->w + 31) / 32);
         stats->hist_launches += 1;
         stats->hist_rows += total_rows;
-        stats->hist_bytes += total_rows * (wbytes + 16 + (rows ? 4 : 0)) + (int64_t)nparts * tb * 16;
+        stats->hist_bytes += total_rows * (wbytes + 16 + (rows ? 4 : 0)) + (int64_t)n_build * tb * 16;
     }
     return GBT_OK;
 }

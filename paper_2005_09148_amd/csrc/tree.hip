@@ -393,7 +393,7 @@ __global__ void __launch_bounds__(1024)
         *n_next_d = 2 * c_build;
         *n_red_d = c_build;
         *n_work_d = c_part;
-        atomicAdd(&stat[1], (unsigned long long)c_part);
+        atomicAdd(&stat[1], (unsigned long long)c_build);
     }
 }
 
@@ -426,7 +426,7 @@ __global__ void k_leaves(const DevNode *__restrict__ nodes, int32_t n_nodes, con
 struct TreeResult {
     unsigned long long updates;     // histogram updates (the counters folded)
     unsigned long long rows_built;  // rows streamed below the root
-    unsigned long long partials;    // partial histograms written below the root
+    unsigned long long built;       // histograms built below the root
     long long T;
     int32_t e_key, e_g, e_h;
     uint32_t bad;
@@ -447,7 +447,7 @@ __global__ void k_finalize(const DevNode *__restrict__ nodes, int32_t n_nodes, c
             for (int k = 0; k < kUpdCounters; ++k) u += upd[k];
         out->updates = u;
         out->rows_built = stat[0];
-        out->partials = stat[1];
+        out->built = stat[1];
         out->T = st->T;
         out->e_key = st->e_key;
         out->e_g = st->e_g;
@@ -1014,13 +1014,13 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         stats->hist_updates = (int64_t)res->updates;
         // algorithmic bytes: the packed symbols of each row, its 16-byte
         // fixed-point pair, its 4-byte row id below the root, and one write of
-        // every chunk's partial histogram
+        // every built node's histogram (the chunk partials are not counted)
         const int64_t wbytes = 4 * (((int64_t)mx->stride * mx->w + 31) / 32);
-        const int64_t root_parts = (D > 0 && R > 0) ? n_root : 0;
+        const int64_t root_built = (D > 0 && R > 0) ? 1 : 0;
         stats->hist_launches = hist_launches;
         stats->hist_rows = (D > 0 ? R : 0) + (int64_t)res->rows_built;
         stats->hist_bytes = (D > 0 ? R : 0) * (wbytes + 16) + (int64_t)res->rows_built * (wbytes + 20) +
-                            (root_parts + (int64_t)res->partials) * mx->total_bins * 16;
+                            (root_built + (int64_t)res->built) * mx->total_bins * 16;
         stats->ms_sample = ms[kPhSample];
         stats->ms_hist = ms[kPhHist];
         stats->ms_hist_aux = ms[kPhHistAux];
