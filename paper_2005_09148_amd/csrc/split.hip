@@ -684,6 +684,135 @@ __global__ void __launch_bounds__(kPartThreads)
     }
 }
 
+// The tree driver's scatter, which also takes the place of k_part_bounds: a
+// splitting node's left rows go to the front of its segment in slot order
+// and its right rows to the back in reverse slot order, so no block needs a
+// node's total left count.  The left flags before a node's first slot come
+// from this tile's scan when the node starts in the tile; the one node that
+// starts in an earlier tile (the node of the tile's first slot) gets them
+// from the tile counts before its first tile and that tile's flags.  The
+// block holding a node's last slot writes the node's left count.  The order
+// of rows within a node enters no result.
+__global__ void __launch_bounds__(kPartThreads)
+    k_part_scatter_rev(const int32_t *__restrict__ rows, int64_t n, const uint8_t *__restrict__ flags,
+                       const int32_t *__restrict__ tile_cnt, const int32_t *__restrict__ slot_node,
+                       int32_t *__restrict__ slot_node_out, DevNode *__restrict__ nodes,
+                       int32_t *__restrict__ rows_out)
+{
+    __shared__ int32_t lds16[kPartThreads / 64];
+    __shared__ long long s_red[2][kPartThreads / 64];
+    __shared__ int32_t s_pref[kPartThreads];  // left flags of the tile before each thread's slots
+    __shared__ uint32_t s_f4[kPartThreads];   // each thread's four flags, one per byte
+    const int64_t ts = (int64_t)blockIdx.x * kPartTile;
+    const int64_t i0 = ts + (int64_t)threadIdx.x * kPartItems;
+    int32_t r[kPartItems], nid[kPartItems];
+    part_load(rows, nullptr, slot_node, i0, n, r, nid);
+    uint32_t f4 = 0;
+    if (i0 + kPartItems <= n) {
+        f4 = *(const uint32_t *)(flags + i0);
+    } else {
+#pragma unroll
+        for (int k = 0; k < kPartItems; ++k)
+            if (i0 + k < n) f4 |= (uint32_t)flags[i0 + k] << (8 * k);
+    }
+    const int32_t mine = (int32_t)((f4 & 1u) + ((f4 >> 8) & 1u) + ((f4 >> 16) & 1u) + ((f4 >> 24) & 1u));
+    // the node of the tile's first slot, when it starts in an earlier tile
+    const int32_t n0 = slot_node[ts];
+    const int64_t b0 = n0 >= 0 ? nodes[n0].begin : ts;
+    const bool ext = b0 < ts;
+    const int64_t tb = b0 / kPartTile;  // its first tile
+    // left flags before this tile and before b0: tile counts, plus the
+    // flags of tile tb before b0
+    long long before = 0, before_b = 0;
+    for (int64_t k = threadIdx.x; k < (int64_t)blockIdx.x; k += kPartThreads) {
+        const int32_t v = tile_cnt[k];
+        before += v;
+        before_b += k < tb ? v : 0;
+    }
+    if (ext) {
+        const int64_t j = tb * kPartTile + (int64_t)threadIdx.x * kPartItems;
+#pragma unroll
+        for (int k = 0; k < kPartItems; ++k) before_b += j + k < b0 ? flags[j + k] : 0;
+    }
+    for (int d = 32; d > 0; d >>= 1) {
+        before += __shfl_xor(before, d, 64);
+        before_b += __shfl_xor(before_b, d, 64);
+    }
+    if ((threadIdx.x & 63) == 0) {
+        s_red[0][threadIdx.x >> 6] = before;
+        s_red[1][threadIdx.x >> 6] = before_b;
+    }
+    int32_t total;
+    const int32_t in_tile = part_block_scan(mine, lds16, &total);  // synchronizes the block
+    s_pref[threadIdx.x] = in_tile;
+    s_f4[threadIdx.x] = f4;
+    before = 0;
+    before_b = 0;
+#pragma unroll
+    for (int w = 0; w < kPartThreads / 64; ++w) {
+        before += s_red[0][w];
+        before_b += s_red[1][w];
+    }
+    __syncthreads();
+    long long P = before + in_tile;  // left flags before slot i (all slots)
+#pragma unroll
+    for (int k = 0; k < kPartItems; ++k) {
+        const int64_t i = i0 + k;
+        const uint32_t f = (f4 >> (8 * k)) & 1u;
+        if (i < n) {
+            int64_t dest = i;
+            int32_t child = nid[k];
+            if (nid[k] >= 0) {
+                DevNode &nd = nodes[nid[k]];
+                const int4 rec = *(const int4 *)&nd.split;
+                if (rec.x) {
+                    const int64_t begin = nd.begin, end = nd.end;
+                    long long pl;  // left flags before the node's first slot
+                    if (begin < ts) {
+                        pl = before_b;
+                    } else {
+                        const int o = (int)(begin - ts), th = o / kPartItems, kk = o % kPartItems;
+                        const uint32_t fb = s_f4[th] & ((1u << (8 * kk)) - 1u);
+                        pl = before + s_pref[th] + (long long)((fb & 1u) + ((fb >> 8) & 1u) + ((fb >> 16) & 1u));
+                    }
+                    const long long lb = P - pl;  // the node's left rows before slot i
+                    if (f) {
+                        dest = begin + lb;
+                        child = nd.left_child;
+                    } else {
+                        dest = end - 1 - ((i - begin) - lb);
+                        child = nd.right_child;
+                    }
+                    if (i == end - 1) nd.nleft = P + f - pl;
+                }
+            }
+            rows_out[dest] = r[k];
+            slot_node_out[dest] = child;
+        }
+        P += f;
+    }
+}
+
+gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int32_t *rows,
+                              int64_t n, const int32_t *slot_node, int32_t *slot_node_out, DevNode *nodes,
+                              int32_t *rows_out)
+{
+    if (n == 0) return GBT_OK;
+    GBT_CHECK(n < ((int64_t)1 << 31) - 1, "partition of %lld rows (limit 2^31-2)", (long long)n);
+    uint8_t *flags;
+    GBT_TRY(scratch_t(c, kScrPartFlags, (size_t)n + 16, &flags));
+    const int64_t tiles = (n + kPartTile - 1) / kPartTile;
+    int32_t *tile_cnt;
+    GBT_TRY(scratch_t(c, kScrScan, (size_t)tiles + 1, &tile_cnt));
+    k_part_flags_tiles<<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(rows, n, page, geo_of(mx), nullptr,
+                                                                       slot_node, nodes, flags, tile_cnt);
+    GBT_LAUNCHED();
+    k_part_scatter_rev<<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(rows, n, flags, tile_cnt, slot_node,
+                                                                       slot_node_out, nodes, rows_out);
+    GBT_LAUNCHED();
+    return GBT_OK;
+}
+
 gbt_status partition_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int32_t *rows,
                           int64_t n, int32_t *position, const int32_t *slot_node, int32_t *slot_node_out,
                           DevNode *nodes, const EvalNode *list, const int32_t *n_list_d, int32_t n_list,

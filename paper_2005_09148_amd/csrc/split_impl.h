@@ -64,4 +64,12 @@ gbt_status partition_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page
                           DevNode *nodes, const EvalNode *list, const int32_t *n_list_d, int32_t n_list,
                           int32_t *rows_out);
 
+// The tree driver's partition: rows[0, n) by slot_node as partition_impl,
+// except that a splitting node's right rows land at the back of its segment
+// in reverse slot order; nodes[id].nleft receives each splitting node's left
+// count (pleft is not written).  Two kernels.
+gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int32_t *rows,
+                              int64_t n, const int32_t *slot_node, int32_t *slot_node_out, DevNode *nodes,
+                              int32_t *rows_out);
+
 }  // namespace gbt

@@ -923,8 +923,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         const int32_t maxn = (int32_t)std::min<int64_t>((int64_t)1 << d, max_level_nodes);
         mark = timer_begin(c, kPhSplit);
         if (!fused && R > 0) GBT_TRY(eval_impl(c, mx, histA, evA, maxn, ep, splits_d, cntA, nodes));
-        GBT_TRY(partition_impl(c, mx, so.page, rows, R, nullptr, slot_node, slot_tmp, nodes, evA, cntA, maxn,
-                               rows_tmp));
+        GBT_TRY(partition_rev_impl(c, mx, so.page, rows, R, slot_node, slot_tmp, nodes, rows_tmp));
         std::swap(rows, rows_tmp);
         std::swap(slot_node, slot_tmp);
         const bool plan_next = d + 1 < D && R > 0;
