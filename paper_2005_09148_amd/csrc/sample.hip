@@ -165,9 +165,17 @@ __device__ inline void row_gh(const SampleSrc &src, int64_t i, double *g, double
     }
 }
 
+// r^2 as r is formed: the square root of this value, rounded, is r.  The
+// square root is monotone, so the largest r is the root of the largest r^2
+// and the maximum passes need no root per row.
+__device__ inline double mvs_r2(double g, double h, double lambda)
+{
+    return g * g + lambda * (h * h);
+}
+
 __device__ inline double mvs_r(double g, double h, double lambda)
 {
-    return sqrt(g * g + lambda * (h * h));
+    return sqrt(mvs_r2(g, h, lambda));
 }
 
 template <int kSrc>
@@ -181,10 +189,10 @@ __global__ void __launch_bounds__(256) k_mvs_rmax(SampleSrc src, int64_t n, doub
          i += (int64_t)gridDim.x * blockDim.x) {
         double g, h;
         row_gh<kSrc>(src, i, &g, &h);
-        double r = mvs_r(g, h, lambda);
-        bad |= (r != r || r > 1.7e308);
-        unsigned long long rb = __double_as_longlong(r);  // r >= 0: bit order = value order
-        b = rb > b ? rb : b;
+        const double x = mvs_r2(g, h, lambda);
+        bad |= !(x <= 1.7976931348623157e308);  // NaN or infinite
+        const unsigned long long xb = __double_as_longlong(x);  // x >= 0: bit order = value order
+        b = xb > b ? xb : b;
     }
     if (bad) atomicOr(&st->bad, 1u);
     b = block_max_u64(b, lds4);
@@ -200,7 +208,7 @@ __global__ void __launch_bounds__(256) k_mvs_keys(SampleSrc src, int64_t n, doub
 {
     __shared__ unsigned long long lds4[4];
     int E;
-    frexp(__longlong_as_double(fold_max(st->rmax)), &E);
+    frexp(sqrt(__longlong_as_double(fold_max(st->rmax))), &E);
     const int32_t e = 62 - E - log2n;
     unsigned long long mx = 0, sm = 0;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
@@ -502,16 +510,30 @@ __global__ void __launch_bounds__(256) k_gradients_rmax(int32_t loss, const floa
     __shared__ unsigned long long lds4[4];
     unsigned long long b = 0;
     bool bad = false;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-         i += (int64_t)gridDim.x * blockDim.x) {
+    auto one = [&](float m, float y, float2 *out) {
         double g, h;
-        gradient_pair(loss, margin[i], label[i], &g, &h);
-        float2 p = make_float2((float)g, (float)h);
-        gpair[i] = p;
-        double r = mvs_r((double)p.x, (double)p.y, lambda);
-        bad |= (r != r || r > 1.7e308);
-        unsigned long long rb = __double_as_longlong(r);
-        b = rb > b ? rb : b;
+        gradient_pair(loss, m, y, &g, &h);
+        const float2 p = make_float2((float)g, (float)h);
+        *out = p;
+        const double x = mvs_r2((double)p.x, (double)p.y, lambda);
+        bad |= !(x <= 1.7976931348623157e308);  // NaN or infinite
+        const unsigned long long xb = __double_as_longlong(x);
+        b = xb > b ? xb : b;
+    };
+    const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x, step = (int64_t)gridDim.x * blockDim.x;
+    if (((uintptr_t)margin & 7u) == 0 && ((uintptr_t)label & 7u) == 0 && ((uintptr_t)gpair & 15u) == 0) {
+        // two rows per thread and step: 8-byte loads, one 16-byte store
+        const int64_t np = n / 2;
+        for (int64_t t = t0; t < np; t += step) {
+            const float2 mv = ((const float2 *)margin)[t], lv = ((const float2 *)label)[t];
+            float2 p0, p1;
+            one(mv.x, lv.x, &p0);
+            one(mv.y, lv.y, &p1);
+            ((float4 *)gpair)[t] = make_float4(p0.x, p0.y, p1.x, p1.y);
+        }
+        if ((n & 1) && t0 == 0) one(margin[n - 1], label[n - 1], &gpair[n - 1]);
+    } else {
+        for (int64_t i = t0; i < n; i += step) one(margin[i], label[i], &gpair[i]);
     }
     if (bad) atomicOr(&st->bad, 1u);
     b = block_max_u64(b, lds4);

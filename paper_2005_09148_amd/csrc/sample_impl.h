@@ -31,7 +31,7 @@ constexpr int kSpread = 16;
 
 // Device-side state of one sampling + fixed-point pass.
 struct SampleState {
-    unsigned long long rmax[kSpread];    // max r (double bits; r >= 0)
+    unsigned long long rmax[kSpread];    // max of r^2 = g^2 + lambda h^2 (double bits; >= 0)
     unsigned long long amax[kSpread];    // max key
     unsigned long long asum[kSpread];    // sum of keys (< 2^62 in total)
     unsigned long long gmax[kSpread];    // max |g'| (double bits)
@@ -79,7 +79,7 @@ gbt_status gw_all(gbt_ctx *c, const float *gpair, int64_t n, double *gw);
 // fx_max_done: the maxima of |g'| and |h'| are already in st (fused upstream)
 gbt_status fixed_point(gbt_ctx *c, const double *gw, int64_t R, SampleState *st, int64_t *q,
                        bool fx_max_done = false);
-// Gradients of all rows and, fused, the maximum of r = sqrt(g^2 + lambda h^2).
+// Gradients of all rows and, fused, the maximum of r^2 = g^2 + lambda h^2.
 gbt_status gradients_rmax(gbt_ctx *c, int32_t loss, const float *margin, const float *label, int64_t n,
                           float *gpair, double lambda, SampleState *st);
 // Exclusive per-tile offsets from the per-tile counts mvs_select wrote into

@@ -291,7 +291,8 @@ __global__ void __launch_bounds__(kEvalThreads)
 // ------------------------------------------------------------ reduce + evaluate
 // One block per (feature, reduce item): its 16 waves cover the feature's
 // bins 64 at a time (4 chunks) and every fourth partial (4 subsets); the
-// built node's and the sibling's bins go to hist and to LDS, then wave 0
+// built node's and the sibling's bins go to hist (unless hist is NULL: the
+// level's histograms are parents of no later level) and to LDS, then wave 0
 // evaluates the built node and wave 1 the sibling on the LDS copy.
 constexpr int kRedEvalThreads = 1024;
 
@@ -336,12 +337,12 @@ __global__ void __launch_bounds__(kRedEvalThreads)
             h += sh[t][b];
         }
         const longlong2 bv = make_longlong2(g, h);
-        hist[(int64_t)rd.slot * total_bins + b0 + b] = bv;
+        if (hist) hist[(int64_t)rd.slot * total_bins + b0 + b] = bv;
         hb[b] = bv;
         if (sib) {
             const longlong2 pv = parent[(int64_t)rd.sub_parent * total_bins + b0 + b];
             const longlong2 sv = make_longlong2(pv.x - g, pv.y - h);
-            hist[(int64_t)rd.sub_target * total_bins + b0 + b] = sv;
+            if (hist) hist[(int64_t)rd.sub_target * total_bins + b0 + b] = sv;
             hs[b] = sv;
         }
     }

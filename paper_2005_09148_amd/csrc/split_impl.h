@@ -39,7 +39,8 @@ gbt_status eval_impl(gbt_ctx *c, const gbt_matrix *mx, const int64_t *hist, cons
 // The tree driver's fused step after a histogram pass whose features all
 // have at most 256 bins: for every reduce item (count *n_red_d, at most
 // max_red) and feature, sum the built node's partials into hist, write the
-// sibling as parent minus it, and evaluate the feature for both nodes (the
+// sibling as parent minus it (hist may be NULL: then the sums are only
+// evaluated), and evaluate the feature for both nodes (the
 // EvalNode of a histogram slot is ev[slot]); cand[slot * m + feature]
 // receives the candidates.  Then eval_reduce_impl picks each node's split.
 gbt_status reduce_eval_impl(gbt_ctx *c, const gbt_matrix *mx, const int64_t *partials, const HistReduce *red,

@@ -942,7 +942,9 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
                 // the next level: at most 2 maxn nodes, in evB
                 const int32_t nxt = (int32_t)std::min<int64_t>(2 * (int64_t)maxn, max_level_nodes);
                 mark = timer_begin(c, kPhHistAux);
-                GBT_TRY(reduce_eval_impl(c, mx, partials, red_d, cnt + 3, maxn, histA, histB, evB, ep, cand));
+                // the deepest evaluated level's histograms are nobody's parents
+                GBT_TRY(reduce_eval_impl(c, mx, partials, red_d, cnt + 3, maxn, histA, d + 2 < D ? histB : nullptr,
+                                         evB, ep, cand));
                 GBT_TRY(eval_reduce_impl(c, cand, mx->m, evB, nxt, cntB, splits_d, nodes));
                 timer_end(c, mark);
             }
