@@ -178,6 +178,22 @@ __device__ inline double mvs_r(double g, double h, double lambda)
     return sqrt(mvs_r2(g, h, lambda));
 }
 
+// A spread maximum folded by the block's first wave and shared through LDS;
+// every thread of the block calls it.
+__device__ inline unsigned long long block_fold_max(const Spread &a, unsigned long long *lds1)
+{
+    if (threadIdx.x < 64) {
+        unsigned long long v = threadIdx.x < kSpread ? a[threadIdx.x][0] : 0ull;
+        for (int d = 32; d > 0; d >>= 1) {
+            const unsigned long long o = __shfl_xor(v, d, 64);
+            v = o > v ? o : v;
+        }
+        if (threadIdx.x == 0) *lds1 = v;
+    }
+    __syncthreads();
+    return *lds1;
+}
+
 template <int kSrc>
 __global__ void __launch_bounds__(256) k_mvs_rmax(SampleSrc src, int64_t n, double lambda,
                                                   SampleState *__restrict__ st)
@@ -196,7 +212,7 @@ __global__ void __launch_bounds__(256) k_mvs_rmax(SampleSrc src, int64_t n, doub
     }
     if (bad) atomicOr(&st->bad, 1u);
     b = block_max_u64(b, lds4);
-    if (threadIdx.x == 0 && b) atomicMax(&st->rmax[blockIdx.x % kSpread], b);
+    if (threadIdx.x == 0 && b) atomicMax(spread_at(st->rmax, blockIdx.x), b);
 }
 
 // a_i = rint(r_i * 2^e), e = 62 - E - L with max r < 2^E; also max and sum
@@ -206,9 +222,9 @@ __global__ void __launch_bounds__(256) k_mvs_keys(SampleSrc src, int64_t n, doub
                                                   int32_t log2n, SampleState *__restrict__ st,
                                                   int64_t *__restrict__ keys)
 {
-    __shared__ unsigned long long lds4[4];
+    __shared__ unsigned long long lds4[4], m1;
     int E;
-    frexp(sqrt(__longlong_as_double(fold_max(st->rmax))), &E);
+    frexp(sqrt(__longlong_as_double(block_fold_max(st->rmax, &m1))), &E);
     const int32_t e = 62 - E - log2n;
     unsigned long long mx = 0, sm = 0;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
@@ -223,8 +239,8 @@ __global__ void __launch_bounds__(256) k_mvs_keys(SampleSrc src, int64_t n, doub
     mx = block_max_u64(mx, lds4);
     sm = block_sum_u64(sm, lds4);
     if (threadIdx.x == 0) {
-        if (mx) atomicMax(&st->amax[blockIdx.x % kSpread], mx);
-        if (sm) atomicAdd(&st->asum[blockIdx.x % kSpread], sm);
+        if (mx) atomicMax(spread_at(st->amax, blockIdx.x), mx);
+        if (sm) atomicAdd(spread_at(st->asum, blockIdx.x), sm);
         if (blockIdx.x == 0) st->e_key = e;
     }
 }
@@ -497,8 +513,8 @@ __global__ void __launch_bounds__(256)
     mg = block_max_u64(mg, red4);
     mh = block_max_u64(mh, red4);
     if (threadIdx.x == 0) {
-        if (mg) atomicMax(&st->gmax[blockIdx.x % kSpread], mg);
-        if (mh) atomicMax(&st->hmax[blockIdx.x % kSpread], mh);
+        if (mg) atomicMax(spread_at(st->gmax, blockIdx.x), mg);
+        if (mh) atomicMax(spread_at(st->hmax, blockIdx.x), mh);
     }
 }
 
@@ -537,7 +553,7 @@ __global__ void __launch_bounds__(256) k_gradients_rmax(int32_t loss, const floa
     }
     if (bad) atomicOr(&st->bad, 1u);
     b = block_max_u64(b, lds4);
-    if (threadIdx.x == 0 && b) atomicMax(&st->rmax[blockIdx.x % kSpread], b);
+    if (threadIdx.x == 0 && b) atomicMax(spread_at(st->rmax, blockIdx.x), b);
 }
 
 // ------------------------------------------------------------ fixed point
@@ -556,8 +572,8 @@ __global__ void __launch_bounds__(256) k_fx_max(const double2 *__restrict__ gw, 
     bg = block_max_u64(bg, lds4);
     bh = block_max_u64(bh, lds4);
     if (threadIdx.x == 0) {
-        if (bg) atomicMax(&st->gmax[blockIdx.x % kSpread], bg);
-        if (bh) atomicMax(&st->hmax[blockIdx.x % kSpread], bh);
+        if (bg) atomicMax(spread_at(st->gmax, blockIdx.x), bg);
+        if (bh) atomicMax(spread_at(st->hmax, blockIdx.x), bh);
     }
 }
 
@@ -567,10 +583,10 @@ __global__ void __launch_bounds__(256) k_fx_convert(const double2 *__restrict__ 
                                                     int32_t log2R, SampleState *__restrict__ st,
                                                     longlong2 *__restrict__ q)
 {
-    __shared__ unsigned long long lds4[4];
+    __shared__ unsigned long long lds4[4], m2[2];
     int Eg, Eh;
-    frexp(__longlong_as_double(fold_max(st->gmax)), &Eg);
-    frexp(__longlong_as_double(fold_max(st->hmax)), &Eh);
+    frexp(__longlong_as_double(block_fold_max(st->gmax, &m2[0])), &Eg);
+    frexp(__longlong_as_double(block_fold_max(st->hmax, &m2[1])), &Eh);
     const int32_t eg = 62 - Eg - log2R, eh = 62 - Eh - log2R;
     unsigned long long sg = 0, sh = 0;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < R;
@@ -584,8 +600,8 @@ __global__ void __launch_bounds__(256) k_fx_convert(const double2 *__restrict__ 
     sg = block_sum_u64(sg, lds4);
     sh = block_sum_u64(sh, lds4);
     if (threadIdx.x == 0) {
-        if (sg) atomicAdd(&st->root_g[blockIdx.x % kSpread], sg);
-        if (sh) atomicAdd(&st->root_h[blockIdx.x % kSpread], sh);
+        if (sg) atomicAdd(spread_at(st->root_g, blockIdx.x), sg);
+        if (sh) atomicAdd(spread_at(st->root_h, blockIdx.x), sh);
         if (blockIdx.x == 0) {
             st->e_g = eg;
             st->e_h = eh;
@@ -595,10 +611,9 @@ __global__ void __launch_bounds__(256) k_fx_convert(const double2 *__restrict__ 
 
 __global__ void k_state_init(SampleState *st)
 {
-    if (threadIdx.x == 0) {
-        SampleState z = {};
-        *st = z;
-    }
+    static_assert(sizeof(SampleState) % 8 == 0, "SampleState is zeroed in 64-bit words");
+    unsigned long long *w = (unsigned long long *)st;
+    for (int i = threadIdx.x; i < (int)(sizeof(SampleState) / 8); i += blockDim.x) w[i] = 0ull;
 }
 
 __global__ void k_zero_u64(unsigned long long *p, int64_t n)
@@ -735,7 +750,7 @@ gbt_status fixed_point(gbt_ctx *c, const double *gw, int64_t R, SampleState *st,
 
 gbt_status state_init(gbt_ctx *c, SampleState *st)
 {
-    k_state_init<<<1, 64, 0, c->stream>>>(st);
+    k_state_init<<<1, 256, 0, c->stream>>>(st);
     GBT_LAUNCHED();
     return GBT_OK;
 }

@@ -24,20 +24,23 @@ struct SampleSrc {
     int32_t pad0;
 };
 
-// Reductions over all rows land in kSpread copies (block b uses copy
-// b % kSpread) so that same-address atomics do not serialize; readers fold
-// the copies.
-constexpr int kSpread = 16;
+// Reductions over all rows land in kSpread copies, each in a 128-byte line
+// of its own (block b uses copy b % kSpread), so that the blocks' atomics
+// spread over kSpread cache lines instead of serializing on one; readers
+// fold the copies.
+constexpr int kSpread = 32;
+constexpr int kLineWords = 16;  // 64-bit words per 128-byte line
+typedef unsigned long long Spread[kSpread][kLineWords];
 
 // Device-side state of one sampling + fixed-point pass.
 struct SampleState {
-    unsigned long long rmax[kSpread];    // max of r^2 = g^2 + lambda h^2 (double bits; >= 0)
-    unsigned long long amax[kSpread];    // max key
-    unsigned long long asum[kSpread];    // sum of keys (< 2^62 in total)
-    unsigned long long gmax[kSpread];    // max |g'| (double bits)
-    unsigned long long hmax[kSpread];    // max |h'| (double bits)
-    unsigned long long root_g[kSpread];  // fixed-point sums of all training rows
-    unsigned long long root_h[kSpread];
+    Spread rmax;    // max of r^2 = g^2 + lambda h^2 (double bits; >= 0)
+    Spread amax;    // max key
+    Spread asum;    // sum of keys (< 2^62 in total)
+    Spread gmax;    // max |g'| (double bits)
+    Spread hmax;    // max |h'| (double bits)
+    Spread root_g;  // fixed-point sums of all training rows
+    Spread root_h;
     unsigned long long C_above;    // radix descent: #keys >= upper end of the range
     unsigned long long F_below;    // radix descent: sum of keys below the range
     long long lo;                  // radix descent: range start
@@ -51,17 +54,20 @@ struct SampleState {
     unsigned int bad;
 };
 
-__host__ __device__ inline unsigned long long fold_max(const unsigned long long *a)
+// Block b's copy of a spread reduction.
+__host__ __device__ inline unsigned long long *spread_at(Spread &a, unsigned b) { return &a[b % kSpread][0]; }
+
+__host__ __device__ inline unsigned long long fold_max(const Spread &a)
 {
     unsigned long long m = 0;
-    for (int i = 0; i < kSpread; ++i) m = a[i] > m ? a[i] : m;
+    for (int i = 0; i < kSpread; ++i) m = a[i][0] > m ? a[i][0] : m;
     return m;
 }
 
-__host__ __device__ inline unsigned long long fold_sum(const unsigned long long *a)
+__host__ __device__ inline unsigned long long fold_sum(const Spread &a)
 {
     unsigned long long m = 0;
-    for (int i = 0; i < kSpread; ++i) m += a[i];
+    for (int i = 0; i < kSpread; ++i) m += a[i][0];
     return m;
 }
 

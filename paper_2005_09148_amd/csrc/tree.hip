@@ -231,12 +231,12 @@ __global__ void k_tree_init(DevNode *__restrict__ nodes, int32_t n_nodes, const 
     if (upd && i < kUpdCounters) upd[i] = 0ull;
     if (i < 2) stat[i] = 0ull;
     if (i < n_nodes) {
-        const long long rg = (long long)fold_sum(st->root_g), rh = (long long)fold_sum(st->root_h);
         DevNode d;
         memset(&d, 0, sizeof(d));
         d.left_child = 2 * (int32_t)i + 1;
         d.right_child = 2 * (int32_t)i + 2;
         if (i == 0) {
+            const long long rg = (long long)fold_sum(st->root_g), rh = (long long)fold_sum(st->root_h);
             d.present = 1;
             d.sum_g = rg;
             d.sum_h = rh;
@@ -971,9 +971,11 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
             [&](const uint32_t *words, int64_t row0, int64_t rows_n) -> gbt_status {
                 const size_t lds_bytes = (size_t)NN * 12 + (size_t)kWalkTileRows * (geo.row_words + 1) * 4;
                 const int q4 = geo.row_words / 4;
+                // one block per tile: independent blocks hide the page's
+                // latency better than a smaller grid that prefetches
                 if (q4 <= 8 && NN <= kWalkLdsNodes && lds_bytes <= 64 * 1024) {
                     int64_t tiles = (rows_n + kWalkTileRows - 1) / kWalkTileRows;
-                    unsigned grid = (unsigned)std::min<int64_t>(tiles, 4 * kCUs);
+                    unsigned grid = (unsigned)tiles;
                     launch_walk_pf(c, q4, grid, lds_bytes, words, rows_n, geo, compact, leaf, NN, margin + row0);
                 } else if (geo.row_words <= kWalkMaxWords && NN <= kWalkLdsNodes && lds_bytes <= 64 * 1024) {
                     int64_t tiles = (rows_n + kWalkTileRows - 1) / kWalkTileRows;
