@@ -40,7 +40,12 @@ gbt_status hip_error(hipError_t e, const char *what, const char *file, int line)
 #define GBT_LAUNCHED() GBT_HIP(hipGetLastError())
 
 constexpr int kXcds = 8;         // gfx950: 8 XCDs of 32 CUs
-constexpr int kUpdCounters = 16; // spread copies of the histogram update counter
+// Spread copies of the histogram update counter, one 128-byte line apart
+// (copy k at word k * kUpdStride), so that the workgroups' atomics do not
+// serialize on one line.
+constexpr int kUpdCounters = 32;
+constexpr int kUpdStride = 16;
+constexpr int kUpdWords = kUpdCounters * kUpdStride;
 constexpr int kCUs = 256;
 
 // Map a linear workgroup id so that logically adjacent ids run on the same

@@ -56,7 +56,7 @@ __device__ inline void lds_flush(const unsigned long long *sg, const unsigned lo
         // one atomic per block, spread over kUpdCounters addresses
         unsigned long long t = 0;
         for (int w = 0; w < kHistThreads / 64; ++w) t += red[w];
-        if (t) atomicAdd(&n_updates[blockIdx.x % kUpdCounters], t);
+        if (t) atomicAdd(&n_updates[(blockIdx.x % kUpdCounters) * kUpdStride], t);
     }
 }
 
@@ -301,7 +301,7 @@ __global__ void __launch_bounds__(kRotThreads)
     }
     // the update count: one atomic per wave (the LDS is all histogram)
     if (n_updates && lane == 0 && cnt)
-        atomicAdd(&n_updates[(blockIdx.x * (kRotThreads / 64) + (threadIdx.x >> 6)) % kUpdCounters],
+        atomicAdd(&n_updates[((blockIdx.x * (kRotThreads / 64) + (threadIdx.x >> 6)) % kUpdCounters) * kUpdStride],
                   (unsigned long long)cnt);
     // partial of this chunk: feature f's bins are column f of the bin rows;
     // consecutive lanes read consecutive columns (no bank conflicts), and the
@@ -569,7 +569,7 @@ gbt_status build_hist_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *pag
 
     // the tree driver zeroes these counters per tree and reads them once
     unsigned long long *upd = nullptr;
-    if (stats) GBT_TRY(scratch_t(c, kScrUpd, kUpdCounters, &upd));
+    if (stats) GBT_TRY(scratch_t(c, kScrUpd, kUpdWords, &upd));
 
     HistLaunch hl{hp.kind, groups_d, G, hp.max_groups_bins, work_d, nullptr, (int32_t)work.size(), red_d,
                   nullptr, (int32_t)red.size(), (int64_t *)partials};

@@ -228,7 +228,7 @@ __global__ void k_tree_init(DevNode *__restrict__ nodes, int32_t n_nodes, const 
         rows[i] = (int32_t)i;
         slot_node[i] = 0;
     }
-    if (upd && i < kUpdCounters) upd[i] = 0ull;
+    if (upd && i < kUpdCounters) upd[i * kUpdStride] = 0ull;
     if (i < 2) stat[i] = 0ull;
     if (i < n_nodes) {
         DevNode d;
@@ -444,7 +444,7 @@ __global__ void k_finalize(const DevNode *__restrict__ nodes, int32_t n_nodes, c
     if (i == 0) {
         unsigned long long u = 0;
         if (upd)
-            for (int k = 0; k < kUpdCounters; ++k) u += upd[k];
+            for (int k = 0; k < kUpdCounters; ++k) u += upd[k * kUpdStride];
         out->updates = u;
         out->rows_built = stat[0];
         out->built = stat[1];
@@ -799,7 +799,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     double h2d = 0.0;
 
     unsigned long long *upd = nullptr;  // zeroed with the tree's other counters
-    if (stats) GBT_TRY(scratch_t(c, kScrUpd, kUpdCounters, &upd));
+    if (stats) GBT_TRY(scratch_t(c, kScrUpd, kUpdWords, &upd));
     c->marks.clear();
     c->events_used = 0;
     int mark = timer_begin(c, kPhSample);
