@@ -289,14 +289,16 @@ __global__ void __launch_bounds__(kEvalThreads)
 }
 
 // ------------------------------------------------------------ reduce + evaluate
-// One block per (feature, reduce item): its 16 waves cover the feature's
-// bins 64 at a time (4 chunks) and every fourth partial (4 subsets); the
-// built node's and the sibling's bins go to hist (unless hist is NULL: the
-// level's histograms are parents of no later level) and to LDS, then wave 0
-// evaluates the built node and wave 1 the sibling on the LDS copy.
-constexpr int kRedEvalThreads = 1024;
-
-__global__ void __launch_bounds__(kRedEvalThreads)
+// One block per (feature, reduce item): 4 waves cover the feature's bins 64
+// at a time, and kSub such wave sets take every kSub-th partial; the built
+// node's and the sibling's bins go to hist (unless hist is NULL: the level's
+// histograms are parents of no later level) and to LDS, then wave 0
+// evaluates the built node and wave 1 the sibling on the LDS copy.  Levels
+// of few nodes and many partials per node use kSub = 4 (1024 threads);
+// levels of many nodes use kSub = 1 (256 threads), so that more blocks are
+// resident while two waves of each evaluate.
+template <int kSub>
+__global__ void __launch_bounds__(256 * kSub)
     k_reduce_eval(const longlong2 *__restrict__ partials, const HistReduce *__restrict__ red,
                   const int32_t *__restrict__ n_red_d, const longlong2 *__restrict__ parent,
                   longlong2 *__restrict__ hist, int64_t total_bins, const int32_t *__restrict__ bin_ptr,
@@ -304,7 +306,7 @@ __global__ void __launch_bounds__(kRedEvalThreads)
 {
     if (n_red_d && (int32_t)blockIdx.y >= *n_red_d) return;
     __shared__ longlong2 hb[256], hs[256];
-    __shared__ long long sg[4][256], sh[4][256];
+    __shared__ long long sg[kSub][256], sh[kSub][256];
     const HistReduce rd = red[blockIdx.y];
     const int32_t f = blockIdx.x;
     const int32_t b0 = bin_ptr[f], B = bin_ptr[f + 1] - b0;
@@ -316,13 +318,14 @@ __global__ void __launch_bounds__(kRedEvalThreads)
     if (b < B) {
         const longlong2 *src = partials + (int64_t)rd.part0 * total_bins + b0 + b;
         int32_t k = sub;
-        for (; k + 12 < rd.nparts; k += 16) {
-            const longlong2 v0 = src[(int64_t)k * total_bins], v1 = src[(int64_t)(k + 4) * total_bins];
-            const longlong2 v2 = src[(int64_t)(k + 8) * total_bins], v3 = src[(int64_t)(k + 12) * total_bins];
+        for (; k + 3 * kSub < rd.nparts; k += 4 * kSub) {
+            const longlong2 v0 = src[(int64_t)k * total_bins], v1 = src[(int64_t)(k + kSub) * total_bins];
+            const longlong2 v2 = src[(int64_t)(k + 2 * kSub) * total_bins];
+            const longlong2 v3 = src[(int64_t)(k + 3 * kSub) * total_bins];
             g += (v0.x + v1.x) + (v2.x + v3.x);
             h += (v0.y + v1.y) + (v2.y + v3.y);
         }
-        for (; k < rd.nparts; k += 4) {
+        for (; k < rd.nparts; k += kSub) {
             const longlong2 v = src[(int64_t)k * total_bins];
             g += v.x;
             h += v.y;
@@ -332,7 +335,7 @@ __global__ void __launch_bounds__(kRedEvalThreads)
     sh[sub][b] = h;
     __syncthreads();
     if (sub == 0 && b < B) {
-        for (int t = 1; t < 4; ++t) {
+        for (int t = 1; t < kSub; ++t) {
             g += sg[t][b];
             h += sh[t][b];
         }
@@ -434,9 +437,15 @@ gbt_status reduce_eval_impl(gbt_ctx *c, const gbt_matrix *mx, const int64_t *par
 {
     if (max_red <= 0) return GBT_OK;
     dim3 grid((unsigned)mx->m, (unsigned)max_red);
-    k_reduce_eval<<<grid, kRedEvalThreads, 0, c->stream>>>((const longlong2 *)partials, red, n_red_d,
-                                                           (const longlong2 *)parent, (longlong2 *)hist,
-                                                           mx->total_bins, mx->bin_ptr_d, mx->m, ev, ep, cand);
+    // many (feature, node) blocks: the narrow form keeps more of them resident
+    if ((int64_t)max_red * mx->m >= 2 * kCUs)
+        k_reduce_eval<1><<<grid, 256, 0, c->stream>>>((const longlong2 *)partials, red, n_red_d,
+                                                      (const longlong2 *)parent, (longlong2 *)hist,
+                                                      mx->total_bins, mx->bin_ptr_d, mx->m, ev, ep, cand);
+    else
+        k_reduce_eval<4><<<grid, 1024, 0, c->stream>>>((const longlong2 *)partials, red, n_red_d,
+                                                       (const longlong2 *)parent, (longlong2 *)hist,
+                                                       mx->total_bins, mx->bin_ptr_d, mx->m, ev, ep, cand);
     GBT_LAUNCHED();
     return GBT_OK;
 }
