@@ -11,8 +11,10 @@ the level-wise tree (histograms with the sibling subtraction, split search,
 partitions), the leaves and the margin update of all 10M rows.
 
 Prints one JSON line: value = histogram row-feature updates performed per
-second of step time (G/s); ms_per_step is seconds per tree x 1000; roofline
-is that of the histogram kernel (algorithmic bytes / its HIP-event time);
+second of step time (G/s); ms_per_step is seconds per tree x 1000 (the timed
+trees carry no events); roofline is that of the histogram kernel
+(algorithmic bytes / its HIP-event time, the events around every histogram
+launch of as many further timed trees);
 cpu_baseline times the CPU oracle on the first two trees of the same
 workload on the host (single-threaded) and reports the same unit.
 """
@@ -355,14 +357,15 @@ def main():
                               lambda_=cfg.lambda_, gamma=cfg.gamma,
                               min_child_weight=cfg.min_child_weight, f=cfg.f,
                               mvs_lambda=cfg.mvs_lambda, seed=cfg.seed)
-    # events around the histogram kernel only during the timed steps
-    ctx.set_timing(1)
+    ctx.set_timing(0)
     first_trees = []
     for w in range(args.warmup):
         P.iteration = w
         tr = gbt.gbt_train_tree(ctx, mx, label, margin, P)
         first_trees.append(tr.nodes.copy())
     torch.cuda.synchronize()
+    # the timed steps carry no events: a HIP event pair around each histogram
+    # launch leaves the GPU idle for a few microseconds per event
     stats = []
     t0 = time.perf_counter()
     for k in range(args.steps):
@@ -372,13 +375,24 @@ def main():
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     print(f"[bench] {args.steps} trees in {dt:.3f} s", file=sys.stderr, flush=True)
+    # the histogram kernel's launch time: HIP events on the compute stream
+    # around every histogram launch, over as many further timed trees of the
+    # same workload
+    ctx.set_timing(1)
+    estats = []
+    t1 = time.perf_counter()
+    for k in range(args.steps):
+        P.iteration = args.warmup + args.steps + k
+        estats.append(gbt.gbt_train_tree(ctx, mx, label, margin, P).stats)
+    torch.cuda.synchronize()
+    dt_ev = time.perf_counter() - t1
 
     # phase breakdown from extra trees with every phase bracketed by events
     # (outside the timed region: the events themselves add gaps)
     ctx.set_timing(2)
     pstats = []
     for k in range(3):
-        P.iteration = args.warmup + args.steps + k
+        P.iteration = args.warmup + 2 * args.steps + k
         pstats.append(gbt.gbt_train_tree(ctx, mx, label, margin, P).stats)
     ctx.set_timing(0)
     # counter calibration: one plain device-to-device copy of known size
@@ -388,13 +402,13 @@ def main():
     torch.cuda.synchronize()
     del src, dst
     upd = sum(s.hist_updates for s in stats)
-    hbytes = sum(s.hist_bytes for s in stats)
-    hms = sum(s.ms_hist for s in stats)
-    launches = sum(s.hist_launches for s in stats)
+    hbytes = sum(s.hist_bytes for s in estats)
+    hms = sum(s.ms_hist for s in estats)
+    launches = sum(s.hist_launches for s in estats)
     phases = {k: round(sum(getattr(s, "ms_" + k) for s in pstats) / len(pstats), 4)
               for k in ("sample", "hist", "hist_aux", "split", "margin", "total")}
     achieved = hbytes / (hms * 1e-3) / 1e9 if hms > 0 else 0.0
-    kernels = {HIST_KERNELS.get(s.hist_kernel, "k_hist_sparse") for s in stats}
+    kernels = {HIST_KERNELS.get(s.hist_kernel, "k_hist_sparse") for s in stats + estats}
     kernel = kernels.pop() if len(kernels) == 1 else "+".join(sorted(kernels))
     line = {
         "metric": METRIC,
@@ -422,7 +436,9 @@ def main():
                      "traffic": stored_traffic(workload_key(args), kernel),
                      "kernel": kernel, "launches": launches,
                      "avg_launch_us": round(hms * 1e3 / max(launches, 1), 2),
-                     "algorithmic_bytes_per_launch": hbytes // max(launches, 1)},
+                     "algorithmic_bytes_per_launch": hbytes // max(launches, 1),
+                     "timing": f"HIP events around each histogram launch over {args.steps} further timed "
+                               f"trees ({round(dt_ev * 1e3 / args.steps, 4)} ms per tree with the events)"},
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(X, y, cfg, args.cpu_trees, first_trees)

@@ -287,6 +287,31 @@ __device__ inline int32_t scan1024(int32_t v, int32_t *lds16, int32_t *total)
 // builds more nodes than that.
 constexpr int64_t kMinChunk = 1024;
 
+// What the plan needs of one split parent, all from the parent's record.
+struct PlanNode {
+    int64_t begin, nl, nr;  // segment start, left and right row counts
+    long long lg, lh, rg, rh;
+    int32_t p, slot, split, pad0;
+};
+
+__device__ inline PlanNode plan_node(const EvalNode *__restrict__ cur, const DevNode *__restrict__ nodes, int32_t t)
+{
+    PlanNode x;
+    x.p = cur[t].heap;
+    x.slot = cur[t].slot;
+    const DevNode &d = nodes[x.p];
+    x.split = d.split;
+    x.begin = d.begin;
+    x.nl = d.nleft;
+    x.nr = d.end - d.begin - d.nleft;
+    x.lg = d.left_g;
+    x.lh = d.left_h;
+    x.rg = d.right_g;
+    x.rh = d.right_h;
+    x.pad0 = 0;
+    return x;
+}
+
 __global__ void __launch_bounds__(1024)
     k_plan_level(const EvalNode *__restrict__ cur, const int32_t *__restrict__ n_cur_d,
                  DevNode *__restrict__ nodes, int32_t plan, int32_t items,
@@ -295,40 +320,35 @@ __global__ void __launch_bounds__(1024)
                  unsigned long long *__restrict__ stat)
 {
     __shared__ int32_t lds16[16];
-    const int32_t n_cur = *n_cur_d;
-    for (int32_t t = threadIdx.x; t < n_cur; t += 1024) {
-        const DevNode d = nodes[cur[t].heap];
-        if (!d.split) continue;
-        const int64_t nl = d.nleft;
-        DevNode &L = nodes[d.left_child];
-        DevNode &Rn = nodes[d.right_child];
-        L.present = 1;
-        L.sum_g = d.left_g;
-        L.sum_h = d.left_h;
-        L.begin = d.begin;
-        L.end = d.begin + nl;
-        Rn.present = 1;
-        Rn.sum_g = d.right_g;
-        Rn.sum_h = d.right_h;
-        Rn.begin = d.begin + nl;
-        Rn.end = d.end;
-    }
-    if (!plan) return;
-    __threadfence_block();
-    __syncthreads();
-    // rows and nodes to build, for the chunk size
     __shared__ unsigned long long red_rows[16];
     __shared__ int32_t red_nodes[16];
+    const int32_t n_cur = *n_cur_d;
+    // the children's segments and sums; the rows and nodes to build, for the
+    // chunk size (a level of at most 1024 nodes keeps each thread's node in
+    // registers for the second pass)
+    PlanNode mine{};
     unsigned long long rb = 0;
     int32_t nbuild = 0;
     for (int32_t t = threadIdx.x; t < n_cur; t += 1024) {
-        const int32_t p = cur[t].heap;
-        if (!nodes[p].split) continue;
-        const int64_t a = nodes[2 * p + 1].end - nodes[2 * p + 1].begin;
-        const int64_t b = nodes[2 * p + 2].end - nodes[2 * p + 2].begin;
-        rb += (unsigned long long)(a <= b ? a : b);
+        const PlanNode x = plan_node(cur, nodes, t);
+        if (t < 1024) mine = x;
+        if (!x.split) continue;
+        DevNode &L = nodes[2 * x.p + 1];
+        DevNode &Rn = nodes[2 * x.p + 2];
+        L.present = 1;
+        L.sum_g = x.lg;
+        L.sum_h = x.lh;
+        L.begin = x.begin;
+        L.end = x.begin + x.nl;
+        Rn.present = 1;
+        Rn.sum_g = x.rg;
+        Rn.sum_h = x.rh;
+        Rn.begin = x.begin + x.nl;
+        Rn.end = x.begin + x.nl + x.nr;
+        rb += (unsigned long long)(x.nl <= x.nr ? x.nl : x.nr);
         ++nbuild;
     }
+    if (!plan) return;
     for (int d = 32; d > 0; d >>= 1) {
         rb += __shfl_xor(rb, d, 64);
         nbuild += __shfl_xor(nbuild, d, 64);
@@ -354,34 +374,29 @@ __global__ void __launch_bounds__(1024)
     unsigned long long rows_built = 0;
     for (int32_t base = 0; base < n_cur; base += 1024) {
         const int32_t t = base + (int32_t)threadIdx.x;
-        bool split = false;
-        int32_t p = 0, nchunks = 0;
-        int64_t nl = 0, nr = 0;
-        if (t < n_cur) {
-            p = cur[t].heap;
-            split = nodes[p].split != 0;
-            if (split) {
-                nl = nodes[2 * p + 1].end - nodes[2 * p + 1].begin;
-                nr = nodes[2 * p + 2].end - nodes[2 * p + 2].begin;
-                int64_t ns = nl <= nr ? nl : nr;
-                nchunks = (int32_t)(ns > 0 ? (ns + chunk - 1) / chunk : 1);
-                rows_built += (unsigned long long)ns;
-            }
+        PlanNode x{};
+        if (t < n_cur) x = n_cur <= 1024 ? mine : plan_node(cur, nodes, t);
+        const bool split = t < n_cur && x.split;
+        int32_t nchunks = 0;
+        if (split) {
+            const int64_t ns = x.nl <= x.nr ? x.nl : x.nr;
+            nchunks = (int32_t)(ns > 0 ? (ns + chunk - 1) / chunk : 1);
+            rows_built += (unsigned long long)ns;
         }
         int32_t tot_b, tot_p;
         const int32_t kb = scan1024(split ? 1 : 0, lds16, &tot_b) + c_build;
         const int32_t kp = scan1024(nchunks, lds16, &tot_p) + c_part;
         if (split) {
             const int32_t sl = 2 * kb, sr = sl + 1;  // the children of split parents, in heap order
-            const DevNode &L = nodes[2 * p + 1], &Rn = nodes[2 * p + 2];
-            next[sl] = {L.sum_g, L.sum_h, sl, 2 * p + 1};
-            next[sr] = {Rn.sum_g, Rn.sum_h, sr, 2 * p + 2};
-            const bool left_small = nl <= nr;
-            const DevNode &S = left_small ? L : Rn;
-            red[kb] = {left_small ? sl : sr, kp, nchunks, cur[t].slot, left_small ? sr : sl, 0};
+            next[sl] = {x.lg, x.lh, sl, 2 * x.p + 1};
+            next[sr] = {x.rg, x.rh, sr, 2 * x.p + 2};
+            const bool left_small = x.nl <= x.nr;
+            const int64_t sb = left_small ? x.begin : x.begin + x.nl;
+            const int64_t se = left_small ? x.begin + x.nl : x.begin + x.nl + x.nr;
+            red[kb] = {left_small ? sl : sr, kp, nchunks, x.slot, left_small ? sr : sl, 0};
             for (int32_t j = 0; j < nchunks; ++j) {
-                int64_t b = S.begin + (int64_t)j * chunk;
-                work[kp + j] = {b, b + chunk < S.end ? b + chunk : S.end, kp + j, 0};
+                int64_t b = sb + (int64_t)j * chunk;
+                work[kp + j] = {b, b + chunk < se ? b + chunk : se, kp + j, 0};
             }
         }
         c_build += tot_b;
