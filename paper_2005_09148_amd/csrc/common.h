@@ -253,7 +253,7 @@ struct __align__(16) DevNode {
     int32_t present;
     int32_t left_child;     // node ids of the children (heap: 2i+1, 2i+2)
     int32_t right_child;
-    int32_t pad0;
+    int32_t slot;           // tree driver: the node's index in its level's list (its histogram slot)
     int64_t pleft;          // partition: left flags before begin (all slots)
     int64_t nleft;          // partition: rows of the segment that go left
     double gain;

@@ -536,21 +536,96 @@ __device__ inline void part_load(const int32_t *__restrict__ rows, const int32_t
     }
 }
 
-// Left flags of each slot and the count of each tile (the scan's first pass).
+// The split choice of one node, made by one wave from the node's candidates
+// (one per feature): the highest gain, equal gains to the lowest feature; the
+// node splits when that gain is positive.  Returns {split, feature,
+// split_bin, default_left} (all lanes).  write: record the choice in the
+// node (lane 0).
+__device__ inline int4 wave_decide(const EvalCand *__restrict__ cand, int32_t m, DevNode *__restrict__ nodes,
+                                   int32_t id, bool write)
+{
+    const int lane = threadIdx.x & 63;
+    const DevNode &nd = nodes[id];
+    const EvalCand *c = cand + (int64_t)nd.slot * m;
+    int32_t bi = -1;
+    double bg = 0.0;
+    for (int32_t f = lane; f < m; f += 64) {
+        const EvalCand &o = c[f];
+        if (o.valid && (bi < 0 || o.gain > bg)) {
+            bi = f;
+            bg = o.gain;
+        }
+    }
+    double mx = bi >= 0 ? bg : -__builtin_inf();
+    for (int d = 32; d > 0; d >>= 1) mx = fmax(mx, __shfl_xor(mx, d, 64));
+    int32_t best = (bi >= 0 && bg == mx) ? bi : 0x7fffffff;
+    for (int d = 32; d > 0; d >>= 1) best = min(best, __shfl_xor(best, d, 64));
+    if (best == 0x7fffffff) return make_int4(0, 0, 0, 0);
+    const EvalCand b = c[best];
+    if (!(b.gain > 0.0)) return make_int4(0, 0, 0, 0);
+    if (write && lane == 0) {
+        DevNode &d = nodes[id];
+        d.split = 1;
+        d.feature = b.feature;
+        d.split_bin = b.split_bin;
+        d.default_left = b.default_left;
+        d.gain = b.gain;
+        d.left_g = b.lg;
+        d.left_h = b.lh;
+        d.right_g = nd.sum_g - b.lg;
+        d.right_h = nd.sum_h - b.lh;
+    }
+    return make_int4(1, b.feature, b.split_bin, b.default_left);
+}
+
+// Left flags of each slot and the count of each tile (the scan's first
+// pass).  kChoose: the split records are not yet in the node table; each
+// wave chooses the splits of the level's nodes among its slots from their
+// candidates, and the wave holding a node's first slot records the choice
+// (a node without slots cannot split).
+template <bool kChoose>
 __global__ void __launch_bounds__(kPartThreads)
     k_part_flags_tiles(const int32_t *__restrict__ rows, int64_t n, const uint32_t *__restrict__ page, Geo geo,
                        const int32_t *__restrict__ position, const int32_t *__restrict__ slot_node,
-                       const DevNode *__restrict__ nodes, uint8_t *__restrict__ flags,
-                       int32_t *__restrict__ tile_cnt)
+                       DevNode *__restrict__ nodes, uint8_t *__restrict__ flags,
+                       int32_t *__restrict__ tile_cnt, LevelChoice lc)
 {
     __shared__ int32_t red[kPartThreads / 64];
     const int64_t i0 = (int64_t)blockIdx.x * kPartTile + (int64_t)threadIdx.x * kPartItems;
     int32_t r[kPartItems], nid[kPartItems];
     part_load(rows, position, slot_node, i0, n, r, nid);
     int4 rec[kPartItems];  // {split, feature, split_bin, default_left}
+    if (kChoose) {
+        const int lane = threadIdx.x & 63;
+        const int64_t w_lo = i0 - (int64_t)lane * kPartItems;  // the wave's first slot
+        uint32_t need = 0;
 #pragma unroll
-    for (int k = 0; k < kPartItems; ++k)
-        rec[k] = nid[k] >= 0 ? *(const int4 *)&nodes[nid[k]].split : make_int4(0, 0, 0, 0);
+        for (int k = 0; k < kPartItems; ++k) {
+            rec[k] = make_int4(0, 0, 0, 0);
+            if (nid[k] >= lc.lo && nid[k] < lc.hi) need |= 1u << k;
+        }
+        for (;;) {
+            // the wave's smallest node still to choose for (uniform)
+            int32_t t = 0x7fffffff;
+#pragma unroll
+            for (int k = 0; k < kPartItems; ++k)
+                if ((need >> k) & 1u) t = min(t, nid[k]);
+            for (int d = 32; d > 0; d >>= 1) t = min(t, __shfl_xor(t, d, 64));
+            if (t == 0x7fffffff) break;
+            const int64_t b0 = nodes[t].begin;
+            const int4 ch = wave_decide(lc.cand, lc.m, nodes, t, b0 >= w_lo && b0 < w_lo + 64 * kPartItems);
+#pragma unroll
+            for (int k = 0; k < kPartItems; ++k)
+                if (((need >> k) & 1u) && nid[k] == t) {
+                    rec[k] = ch;
+                    need &= ~(1u << k);
+                }
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < kPartItems; ++k)
+            rec[k] = nid[k] >= 0 ? *(const int4 *)&nodes[nid[k]].split : make_int4(0, 0, 0, 0);
+    }
     uint32_t f4 = 0;
     int32_t cnt = 0;
 #pragma unroll
@@ -805,7 +880,7 @@ __global__ void __launch_bounds__(kPartThreads)
 
 gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int32_t *rows,
                               int64_t n, const int32_t *slot_node, int32_t *slot_node_out, DevNode *nodes,
-                              int32_t *rows_out)
+                              int32_t *rows_out, const LevelChoice *choice)
 {
     if (n == 0) return GBT_OK;
     GBT_CHECK(n < ((int64_t)1 << 31) - 1, "partition of %lld rows (limit 2^31-2)", (long long)n);
@@ -814,8 +889,12 @@ gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
     const int64_t tiles = (n + kPartTile - 1) / kPartTile;
     int32_t *tile_cnt;
     GBT_TRY(scratch_t(c, kScrScan, (size_t)tiles + 1, &tile_cnt));
-    k_part_flags_tiles<<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(rows, n, page, geo_of(mx), nullptr,
-                                                                       slot_node, nodes, flags, tile_cnt);
+    if (choice)
+        k_part_flags_tiles<true><<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(
+            rows, n, page, geo_of(mx), nullptr, slot_node, nodes, flags, tile_cnt, *choice);
+    else
+        k_part_flags_tiles<false><<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(
+            rows, n, page, geo_of(mx), nullptr, slot_node, nodes, flags, tile_cnt, LevelChoice{});
     GBT_LAUNCHED();
     k_part_scatter_rev<<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(rows, n, flags, tile_cnt, slot_node,
                                                                        slot_node_out, nodes, rows_out);
@@ -838,8 +917,8 @@ gbt_status partition_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page
     GBT_TRY(scratch_t(c, kScrScan, (size_t)tiles + 1, &tile_off));
     // tile_off receives each tile's left count; the bounds and the scatter
     // sum the counts before their tiles themselves
-    k_part_flags_tiles<<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(rows, n, page, geo, position, slot_node,
-                                                                       nodes, flags, tile_off);
+    k_part_flags_tiles<false><<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(rows, n, page, geo, position, slot_node,
+                                                                       nodes, flags, tile_off, LevelChoice{});
     GBT_LAUNCHED();
     if (n_list > 0) {
         k_part_bounds<<<(unsigned)n_list, kBoundThreads, 0, c->stream>>>(list, n_list_d, n_list, nodes, flags,

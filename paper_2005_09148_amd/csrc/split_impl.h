@@ -65,12 +65,23 @@ gbt_status partition_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page
                           DevNode *nodes, const EvalNode *list, const int32_t *n_list_d, int32_t n_list,
                           int32_t *rows_out);
 
+// The level's split choices made inside the partition: the candidates of the
+// level's nodes (heap ids [lo, hi); a node's m candidates start at
+// cand[DevNode::slot * m]).
+struct LevelChoice {
+    const EvalCand *cand;
+    int32_t m;
+    int32_t lo, hi;
+};
+
 // The tree driver's partition: rows[0, n) by slot_node as partition_impl,
 // except that a splitting node's right rows land at the back of its segment
 // in reverse slot order; nodes[id].nleft receives each splitting node's left
-// count (pleft is not written).  Two kernels.
+// count (pleft is not written).  Two kernels.  With `choice`, the split
+// records of the level's nodes are chosen from the candidates and written
+// by the first kernel (instead of by eval_reduce_impl).
 gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int32_t *rows,
                               int64_t n, const int32_t *slot_node, int32_t *slot_node_out, DevNode *nodes,
-                              int32_t *rows_out);
+                              int32_t *rows_out, const LevelChoice *choice = nullptr);
 
 }  // namespace gbt

@@ -390,6 +390,8 @@ __global__ void __launch_bounds__(1024)
             const int32_t sl = 2 * kb, sr = sl + 1;  // the children of split parents, in heap order
             next[sl] = {x.lg, x.lh, sl, 2 * x.p + 1};
             next[sr] = {x.rg, x.rh, sr, 2 * x.p + 2};
+            nodes[2 * x.p + 1].slot = sl;
+            nodes[2 * x.p + 2].slot = sr;
             const bool left_small = x.nl <= x.nr;
             const int64_t sb = left_small ? x.begin : x.begin + x.nl;
             const int64_t se = left_small ? x.begin + x.nl : x.begin + x.nl + x.nr;
@@ -918,6 +920,10 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     for (int32_t f = 0; f < mx->m; ++f)
         max_feature_bins = std::max(max_feature_bins, mx->bin_ptr_h[f + 1] - mx->bin_ptr_h[f]);
     const bool fused = max_feature_bins <= 256;
+    // the partition's flags pass makes each level's split choices from the
+    // candidates (one wave per node and wave of slots) when a node has few
+    // candidates and a level few nodes; otherwise a pass of its own does
+    const bool choose = fused && mx->m <= 128 && max_level_nodes <= 4096;
     EvalCand *cand = nullptr;
     if (fused) GBT_TRY(scratch_t(c, kScrCand, (size_t)max_level_nodes * std::max(mx->m, 1), &cand));
     int32_t hist_launches = 0;
@@ -930,7 +936,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         if (fused) {
             mark = timer_begin(c, kPhHistAux);
             GBT_TRY(reduce_eval_impl(c, mx, partials, red_d, nullptr, 1, nullptr, histA, evA, ep, cand));
-            GBT_TRY(eval_reduce_impl(c, cand, mx->m, evA, 1, cntA, splits_d, nodes));
+            if (!choose) GBT_TRY(eval_reduce_impl(c, cand, mx->m, evA, 1, cntA, splits_d, nodes));
             timer_end(c, mark);
         }
     }
@@ -938,7 +944,9 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         const int32_t maxn = (int32_t)std::min<int64_t>((int64_t)1 << d, max_level_nodes);
         mark = timer_begin(c, kPhSplit);
         if (!fused && R > 0) GBT_TRY(eval_impl(c, mx, histA, evA, maxn, ep, splits_d, cntA, nodes));
-        GBT_TRY(partition_rev_impl(c, mx, so.page, rows, R, slot_node, slot_tmp, nodes, rows_tmp));
+        const LevelChoice lc{cand, mx->m, (int32_t)((1u << d) - 1), (int32_t)((2u << d) - 1)};
+        GBT_TRY(partition_rev_impl(c, mx, so.page, rows, R, slot_node, slot_tmp, nodes, rows_tmp,
+                                   choose ? &lc : nullptr));
         std::swap(rows, rows_tmp);
         std::swap(slot_node, slot_tmp);
         const bool plan_next = d + 1 < D && R > 0;
@@ -960,7 +968,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
                 // the deepest evaluated level's histograms are nobody's parents
                 GBT_TRY(reduce_eval_impl(c, mx, partials, red_d, cnt + 3, maxn, histA, d + 2 < D ? histB : nullptr,
                                          evB, ep, cand));
-                GBT_TRY(eval_reduce_impl(c, cand, mx->m, evB, nxt, cntB, splits_d, nodes));
+                if (!choose) GBT_TRY(eval_reduce_impl(c, cand, mx->m, evB, nxt, cntB, splits_d, nodes));
                 timer_end(c, mark);
             }
             std::swap(histA, histB);
