@@ -609,6 +609,9 @@ __global__ void __launch_bounds__(kWalkTileRows)
 
 // The same walk with the next tile's rows and margins prefetched into
 // registers (kQ 16-byte pieces per row) while the current tile is walked.
+// Dense rows: the tree in LDS holds each split's bit offset (feature * w),
+// and a symbol is one funnel shift of two words of the staged row (the row
+// pitch leaves a word after the last one).
 template <int kQ>
 __global__ void __launch_bounds__(kWalkTileRows)
     k_margin_walk_pf(const uint32_t *__restrict__ words, int64_t rows, Geo geo,
@@ -619,8 +622,11 @@ __global__ void __launch_bounds__(kWalkTileRows)
     uint2 *tn = (uint2 *)walk_lds;
     float *tl = (float *)(tn + nn);
     uint32_t *rb = (uint32_t *)(tl + nn);
+    const bool dense = !geo.sparse;
     for (int32_t t = threadIdx.x; t < nn; t += kWalkTileRows) {
-        tn[t] = compact[t];
+        uint2 c = compact[t];
+        if (dense && (c.y & 1u)) c.x *= (uint32_t)geo.w;
+        tn[t] = c;
         tl[t] = leaf[t];
     }
     constexpr int32_t ps = 4 * kQ + 1;  // odd row pitch in LDS
@@ -660,11 +666,21 @@ __global__ void __launch_bounds__(kWalkTileRows)
             const uint32_t *row = rb + threadIdx.x * ps;
             int32_t id = 0;
             uint2 nd = tn[0];
-            while (nd.y & 1u) {
-                const int32_t b = row_feature_bin(row, geo, (int32_t)nd.x);
-                const bool left = b < 0 ? ((nd.y >> 1) & 1u) != 0 : b < (int32_t)(nd.y >> 2);
-                id = 2 * id + (left ? 1 : 2);
-                nd = tn[id];
+            if (dense) {
+                while (nd.y & 1u) {
+                    const uint32_t k = nd.x >> 5;
+                    const uint32_t sym = __builtin_amdgcn_alignbit(row[k + 1], row[k], nd.x & 31u) & geo.mask;
+                    const bool left = sym == geo.null_sym ? ((nd.y >> 1) & 1u) != 0 : sym < (nd.y >> 2);
+                    id = 2 * id + (left ? 1 : 2);
+                    nd = tn[id];
+                }
+            } else {
+                while (nd.y & 1u) {
+                    const int32_t b = row_feature_bin(row, geo, (int32_t)nd.x);
+                    const bool left = b < 0 ? ((nd.y >> 1) & 1u) != 0 : b < (int32_t)(nd.y >> 2);
+                    id = 2 * id + (left ? 1 : 2);
+                    nd = tn[id];
+                }
             }
             margin[r0 + threadIdx.x] = m + tl[id];
         }
