@@ -217,6 +217,9 @@ const char *gbt_last_error(void);
  * (NULL = the device's null stream).  A second stream at default priority
  * is created for host-to-device page copies. */
 gbt_status gbt_ctx_create(int32_t device, uint64_t budget_bytes, void *hip_stream, gbt_ctx **out);
+/* Releases the context.  Every matrix, quantizer and sampled set made on it
+ * must be freed first: they hold device memory of the context and refer to
+ * it. */
 gbt_status gbt_ctx_destroy(gbt_ctx *ctx);
 /* Bytes of device memory the context currently holds (budgeted). */
 gbt_status gbt_ctx_memory(gbt_ctx *ctx, uint64_t *used_bytes, uint64_t *peak_bytes);

@@ -9,6 +9,7 @@ from __future__ import annotations
 
 import ctypes as C
 import os
+import weakref
 from dataclasses import dataclass
 
 import numpy as np
@@ -224,9 +225,16 @@ class Context:
         h = C.c_void_p()
         _check(_lib.gbt_ctx_create(device, budget_bytes, s.cuda_stream, C.byref(h)))
         self.h = h
+        # library objects made on this context, released before it
+        self._owned = weakref.WeakSet()
+
+    def _own(self, obj):
+        self._owned.add(obj)
 
     def close(self):
         if self.h:
+            for obj in list(self._owned):
+                obj.free()
             _lib.gbt_ctx_destroy(self.h)
             self.h = None
 
@@ -311,6 +319,7 @@ class Matrix:
         self.ctx = ctx
         self.h = handle
         self._info = None
+        ctx._own(self)
 
     def free(self):
         if self.h:
@@ -381,6 +390,7 @@ class Quantizer:
         _check(_lib.gbt_quantize_begin(ctx.h, C.byref(qp), n_cols, n_rows_total, kind,
                                        C.byref(h)))
         self.h = h
+        ctx._own(self)
 
     def sketch(self, X):
         inp, keep = dense_input(X)
@@ -399,9 +409,16 @@ class Quantizer:
         self.h = None
         return Matrix(self.ctx, m)
 
-    def __del__(self):
+    def free(self):
         if getattr(self, "h", None):
             _lib.gbt_quantizer_free(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
 
 
 # ---------------------------------------------------------------- iteration steps

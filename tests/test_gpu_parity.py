@@ -133,6 +133,19 @@ def test_quantize_rejects_bad_input(gbt, ctx):
         gbt.gbt_quantize(ctx, dense_case(9, 10, 2, 0.0), max_bin=1)
 
 
+def test_context_close_releases_its_objects(gbt):
+    """Closing a context first frees the matrices and quantizers made on it,
+    so that objects outliving the close do not touch the released context."""
+    c = gbt.Context(0)
+    X = dense_case(11, 500, 4, 0.1)
+    mx = gbt.gbt_quantize(c, X, max_bin=32)
+    q = gbt.Quantizer(c, 4, 500, max_bin=32)
+    c.close()
+    assert mx.h is None and q.h is None
+    mx.free()
+    del mx, q
+
+
 # ------------------------------------------------------------ gradients
 @pytest.mark.parametrize("loss", [0, 1])
 def test_gradients(gbt, ctx, loss):
@@ -291,14 +304,17 @@ def test_build_hist_symbol_widths(gbt, ctx, hist_kernel, n, m, missing, max_bin,
 
 
 def test_build_hist_rejects_oversized_feature(gbt, ctx):
-    X = dense_case(35, 4000, 3, 0.0, "normal")
-    mx = gbt.gbt_quantize(ctx, X, max_bin=3000)
+    """A dense feature of more bins than a histogram group holds (2560) is an
+    error, not a wrong histogram."""
+    n = 12000
+    X = dense_case(35, n, 3, 0.0, "normal")
+    mx = gbt.gbt_quantize(ctx, X, max_bin=8000)
     assert mx.info().total_bins > 3 * 2560
-    q = torch.zeros((4000, 2), dtype=torch.int64, device="cuda")
+    q = torch.zeros((n, 2), dtype=torch.int64, device="cuda")
     page = torch.from_numpy(mx.page(0).view(np.int32)).cuda()
     hist = torch.zeros((1, mx.info().total_bins, 2), dtype=torch.int64, device="cuda")
     with pytest.raises(RuntimeError, match="bins"):
-        gbt.gbt_build_hist(ctx, mx, page, q, None, [(0, 0, 4000)], hist=hist)
+        gbt.gbt_build_hist(ctx, mx, page, q, None, [(0, 0, n)], hist=hist)
 
 
 # ------------------------------------------------------------ split evaluation
