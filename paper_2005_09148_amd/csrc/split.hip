@@ -318,12 +318,16 @@ __global__ void __launch_bounds__(256 * kSub)
     if (b < B) {
         const longlong2 *src = partials + (int64_t)rd.part0 * total_bins + b0 + b;
         int32_t k = sub;
-        for (; k + 3 * kSub < rd.nparts; k += 4 * kSub) {
-            const longlong2 v0 = src[(int64_t)k * total_bins], v1 = src[(int64_t)(k + kSub) * total_bins];
-            const longlong2 v2 = src[(int64_t)(k + 2 * kSub) * total_bins];
-            const longlong2 v3 = src[(int64_t)(k + 3 * kSub) * total_bins];
-            g += (v0.x + v1.x) + (v2.x + v3.x);
-            h += (v0.y + v1.y) + (v2.y + v3.y);
+        // eight loads in flight per thread
+        for (; k + 7 * kSub < rd.nparts; k += 8 * kSub) {
+            longlong2 v[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) v[j] = src[(int64_t)(k + j * kSub) * total_bins];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                g += v[j].x;
+                h += v[j].y;
+            }
         }
         for (; k < rd.nparts; k += kSub) {
             const longlong2 v = src[(int64_t)k * total_bins];
@@ -479,15 +483,15 @@ gbt_status eval_impl(gbt_ctx *c, const gbt_matrix *mx, const int64_t *hist, cons
 }
 
 // ------------------------------------------------------------ partition
-// ------------------------------------------------------------ partition
-// Slots are processed in tiles of 4096, one 1024-thread block per tile; a
-// thread owns four consecutive slots, so its row ids, node ids and flags are
-// one vector load each, and the loads of the four slots are issued together.
-constexpr int kPartThreads = 1024;
+// Slots are processed in tiles of 1024, one 256-thread block per tile (small
+// blocks keep several tiles in flight on each CU); a thread owns four
+// consecutive slots, so its row ids, node ids and flags are one vector load
+// each, and the loads of the four slots are issued together.
+constexpr int kPartThreads = 256;
 constexpr int kPartItems = 4;
 constexpr int kPartTile = kPartThreads * kPartItems;  // the scan's tile
 
-// Exclusive sum over a 1024-thread block; *total receives the block's sum.
+// Exclusive sum over a block of kPartThreads; *total receives the block's sum.
 __device__ inline int32_t part_block_scan(int32_t v, int32_t *lds16, int32_t *total)
 {
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
@@ -667,6 +671,7 @@ __device__ inline uint32_t byte_sum4(uint32_t v)
 __device__ inline int64_t part_prefix(const uint8_t *__restrict__ flags, const int32_t *__restrict__ tile_cnt,
                                       int64_t x, long long *lds4)
 {
+    static_assert(kBoundThreads * 16 >= kPartTile, "one block covers a tile's flags, 16 per thread");
     const int64_t t = x / kPartTile, s = t * kPartTile;
     const int64_t j = s + (int64_t)threadIdx.x * 16;
     long long c = 0;
