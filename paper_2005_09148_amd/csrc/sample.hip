@@ -10,6 +10,8 @@
 // it has the closed form ceil(sum a / K).
 #include "sample_impl.h"
 
+#include <chrono>
+
 namespace gbt {
 
 // ------------------------------------------------------------ exp (device)
@@ -246,8 +248,9 @@ __global__ void __launch_bounds__(256) k_mvs_keys(SampleSrc src, int64_t n, doub
 }
 
 // Closed form when T* exceeds every key; otherwise the radix descent
-// starts on [0, 2^S) with 2^S > amax + 1.
-__global__ void k_mvs_thresh_init(SampleState *__restrict__ st, int64_t K)
+// starts on [0, 2^S) with 2^S > amax + 1.  done_host (pinned host memory,
+// may be NULL) receives 1 for the closed form, else 0.
+__global__ void k_mvs_thresh_init(SampleState *__restrict__ st, int64_t K, int32_t *__restrict__ done_host)
 {
     if (threadIdx.x != 0) return;
     unsigned long long amax = fold_max(st->amax), asum = fold_sum(st->asum);
@@ -259,8 +262,10 @@ __global__ void k_mvs_thresh_init(SampleState *__restrict__ st, int64_t K)
         st->T = (long long)q;
         st->done = 1;
         st->levels = 0;
+        if (done_host) __hip_atomic_store(done_host, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
         return;
     }
+    if (done_host) __hip_atomic_store(done_host, 0, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
     int S = 64 - __clzll((long long)(amax + 1));  // 2^S > amax + 1
     int levels = (S + kDigitBits - 1) / kDigitBits;
     st->shift = (levels - 1) * kDigitBits;
@@ -630,7 +635,7 @@ static int32_t log2_ceil(int64_t v) { return v <= 1 ? 0 : ceil_log2_u64((uint64_
 
 // ------------------------------------------------------------ drivers
 gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
-                         double lambda, int64_t K, SampleState *st, SampleState *host_st, bool rmax_done)
+                         double lambda, int64_t K, SampleState *st, bool skip_closed, bool rmax_done)
 {
     int32_t l2 = log2_ceil(n);
     unsigned long long *hist = nullptr;
@@ -649,14 +654,35 @@ gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64
             k_mvs_keys<kSrcMargin><<<rblocks(n), 256, 0, c->stream>>>(src, n, lambda, l2, st, (int64_t *)keys);
         GBT_LAUNCHED();
     }
-    k_mvs_thresh_init<<<1, 64, 0, c->stream>>>(st, K);
+    // skip_closed: the host learns from pinned memory whether the closed form
+    // holds (it waits for the passes above, nothing else is queued) and then
+    // launches no descent levels, which would all return at once
+    volatile int32_t *done_poll = nullptr;
+    int32_t *done_dev = nullptr;
+    if (skip_closed) {
+        void *hio, *hio_d;
+        GBT_TRY(host_io(c, 64, &hio, &hio_d));
+        done_poll = (volatile int32_t *)hio;
+        done_dev = (int32_t *)hio_d;
+        *done_poll = -1;
+    }
+    k_mvs_thresh_init<<<1, 64, 0, c->stream>>>(st, K, done_dev);
     GBT_LAUNCHED();
+    if (done_poll) {
+        const auto t0 = std::chrono::steady_clock::now();
+        for (uint32_t spin = 0; *done_poll < 0; ++spin) {
+            if ((spin & 1023u) == 0 && std::chrono::steady_clock::now() - t0 > std::chrono::seconds(2)) {
+                GBT_HIP(hipStreamSynchronize(c->stream));  // the flag is written by then
+                break;
+            }
+        }
+        if (*done_poll == 1) return GBT_OK;
+    }
     k_zero_u64<<<blocks(2 * kDigitBuckets), 256, 0, c->stream>>>(hist, 2 * kDigitBuckets);
     GBT_LAUNCHED();
     // Every key is at most 2^(62 - ceil(log2 n)), so the descent needs at
     // most ceil((63 - ceil(log2 n)) / 11) levels; levels past the answer (or
     // past the closed form) return at once.
-    (void)host_st;
     const int levels = std::max(1, (63 - l2 + kDigitBits - 1) / kDigitBits);
     unsigned grid = (unsigned)std::min<int64_t>(std::max<int64_t>(blocks(n), 1), 2 * kCUs);
     for (int lev = 0; lev < levels; ++lev) {

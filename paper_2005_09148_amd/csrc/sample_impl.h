@@ -73,8 +73,11 @@ __host__ __device__ inline unsigned long long fold_sum(const Spread &a)
 
 gbt_status state_init(gbt_ctx *c, SampleState *st);
 // keys may be NULL (recomputed on every pass).  Leaves T* in st (device).
+// skip_closed: wait on the host for the closed-form test and launch the
+// radix descent only when it fails (the context's pinned host buffer is
+// used).
 gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
-                         double lambda, int64_t K, SampleState *st, SampleState *host_st,
+                         double lambda, int64_t K, SampleState *st, bool skip_closed,
                          bool rmax_done = false);
 // Keep flags of rows [0, n) and, when tile_cnt is given, the kept count of
 // each tile of kCompactTile rows.

@@ -168,10 +168,9 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
         const int64_t ntiles = (n + kCompactTile - 1) / kCompactTile;
         GBT_TRY(bufs.get(kScrFlags, (size_t)std::max<int64_t>(n, 16) + 16, (void **)&keep));
         GBT_TRY(bufs.get(kScrPos, (size_t)(ntiles + 1) * 4, (void **)&tile_off));
-        SampleState hst;
         if (sp.f < 1.0) {
             o->K = std::max<int64_t>(1, (int64_t)std::nearbyint(sp.f * (double)n));
-            GBT_TRY(mvs_threshold(c, src, kind, nullptr, n, sp.mvs_lambda, o->K, st, &hst, st_ready != nullptr));
+            GBT_TRY(mvs_threshold(c, src, kind, nullptr, n, sp.mvs_lambda, o->K, st, true, st_ready != nullptr));
         }
         // with f = 1 the state keeps T = 0: every row is kept with weight 1
         GBT_TRY(mvs_select(c, src, kind, nullptr, n, sp.mvs_lambda, st, sp.seed, sp.iteration, 0, keep, tile_off));
