@@ -111,6 +111,17 @@ def pmc_summary(fetch_dir, write_dir, workload_key, commands, kernel):
     print(json.dumps(rec, indent=1))
 
 
+# the in-HBM workloads: name -> (config id, description)
+INHBM = {
+    "tiny": (1, "tiny dense {n:,} x 28, logistic, max_bin 256, depth 6, no sampling"),
+    "higgs": (2, "Higgs-shaped dense {n:,} x 28, logistic, max_bin 256, depth 8, no sampling"),
+    "regression": (3, "sampled regression {n:,} x 50, 20% missing, squared error, max_bin 256, depth 8, "
+                      "MVS f={f}"),
+    "sparse": (5, "wide sparse CSR {n:,} x 2000 (1% dense, Zipf features), logistic, max_bin 64, depth 10, "
+                  "gamma 0.1, no sampling"),
+}
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -126,8 +137,9 @@ def parse():
                     help="summarize two rocprofv3 --pmc runs of this script (no GPU work)")
     ap.add_argument("--pmc-commands", nargs="*", default=[], help="the commands of those runs")
     ap.add_argument("--pmc-kernel", default="k_hist_dense", choices=sorted(HIST_KERNELS.values()))
-    ap.add_argument("--workload", default="regression", choices=["regression", "outofcore"],
-                    help="regression: 10M x 50 in HBM (the default line); outofcore: 200M x 100 in "
+    ap.add_argument("--workload", default="regression", choices=sorted(INHBM) + ["outofcore"],
+                    help="regression: 10M x 50 in HBM, MVS f = 0.1 (the default line); tiny: 10k x 28; "
+                         "higgs: 1M x 28 Higgs-shaped; sparse: 2M x 2000 CSR; outofcore: 200M x 100 in "
                          "pinned host pages under an 8 GB device budget")
     return ap.parse_args()
 
@@ -160,27 +172,35 @@ def oracle_updates(b, res, depth):
     return int((nonnull * levels).sum())
 
 
-def cpu_baseline(X, y, cfg, n_trees, gpu_trees):
-    """Times the oracle on the first n_trees iterations of the same workload."""
+def cpu_baseline(X, y, cfg, n_trees, gpu_trees, gpu_updates):
+    """Times the oracle on the first n_trees iterations of the same workload.
+    Updates per tree: counted from the oracle's tree for dense data; for CSR
+    data the GPU's count of the same (identical) tree."""
     from oracle import oracle as orc
     print("[bench] cpu baseline: oracle cuts and bins", file=sys.stderr, flush=True)
     t0 = time.perf_counter()
-    cuts = orc.sketch_cuts_dense(X, cfg.max_bin)
-    b = orc.bin_dense(X, cuts)
+    if isinstance(X, dict):
+        cuts = orc.sketch_cuts_csr(X["indptr"], X["indices"], X["values"], X["m"], cfg.max_bin)
+        b = orc.bin_csr(X["indptr"], X["indices"], X["values"], X["m"], cuts)
+    else:
+        cuts = orc.sketch_cuts_dense(X, cfg.max_bin)
+        b = orc.bin_dense(X, cuts)
     prep = time.perf_counter() - t0
     P = orc.Params(loss=cfg.loss, max_depth=cfg.max_depth, eta=cfg.eta, lambda_=cfg.lambda_,
                    gamma=cfg.gamma, min_child_weight=cfg.min_child_weight, f=cfg.f,
                    mvs_lambda=cfg.mvs_lambda, seed=cfg.seed)
     margin = np.full(len(y), cfg.base_margin, np.float32)
     secs, updates, same = 0.0, 0, True
+    if b.sparse:  # the update count comes from the GPU's identical trees
+        n_trees = min(n_trees, len(gpu_updates))
     for t in range(n_trees):
         t1 = time.perf_counter()
         res = orc.train_tree(b, y, margin, P, iteration=t, want_detail=True)
         secs += time.perf_counter() - t1
-        updates += oracle_updates(b, res, cfg.max_depth)
         print(f"[bench] oracle tree {t}: {time.perf_counter() - t1:.1f} s", file=sys.stderr, flush=True)
         if t < len(gpu_trees):
             same &= res.nodes.tobytes() == gpu_trees[t].tobytes()
+        updates += oracle_updates(b, res, cfg.max_depth) if not b.sparse else gpu_updates[t]
     return {
         "value": round(updates / secs / 1e9, 4),
         "unit": "G updates/s",
@@ -313,9 +333,11 @@ def run_outofcore(args):
 
 def workload_key(args):
     from paper_2005_09148_amd import datagen
-    n = args.rows or datagen.FULL_ROWS[3]
-    f = args.f if args.f is not None else datagen.CONFIGS[3].f
-    return f"regression_{n}x50_f{f:g}"
+    cfg_id = INHBM.get(args.workload, (3, ""))[0]
+    n = args.rows or datagen.FULL_ROWS[cfg_id]
+    f = args.f if args.f is not None else datagen.CONFIGS[cfg_id].f
+    m = {1: 28, 2: 28, 3: 50, 5: 2000}[cfg_id]
+    return f"{args.workload if args.workload in INHBM else 'regression'}_{n}x{m}_f{f:g}"
 
 
 def main():
@@ -334,15 +356,17 @@ def main():
 
     from paper_2005_09148_amd import datagen, gbt
 
-    cfg = datagen.CONFIGS[3]
+    cfg_id, desc = INHBM[args.workload]
+    cfg = datagen.CONFIGS[cfg_id]
     if args.f is not None:
         cfg.f = args.f
-    n = args.rows or datagen.FULL_ROWS[3]
+    n = args.rows or datagen.FULL_ROWS[cfg_id]
     t = time.perf_counter()
-    data = datagen.config3(n)
-    X, y = data["X"], data["y"]
-    print(f"[bench] generated {n:,} x {X.shape[1]} rows in {time.perf_counter() - t:.1f} s",
-          file=sys.stderr, flush=True)
+    data = datagen.make(cfg_id, n)
+    X = data["X"] if data["kind"] == "dense" else data
+    y = data["y"]
+    m = X.shape[1] if data["kind"] == "dense" else data["m"]
+    print(f"[bench] generated {n:,} x {m} rows in {time.perf_counter() - t:.1f} s", file=sys.stderr, flush=True)
 
     ctx = gbt.Context(0)
     ctx.set_hist_kernel({"auto": ctx.HIST_AUTO, "plain": ctx.HIST_PLAIN, "rotated": ctx.HIST_ROTATED}[args.hist_kernel])
@@ -358,11 +382,12 @@ def main():
                               min_child_weight=cfg.min_child_weight, f=cfg.f,
                               mvs_lambda=cfg.mvs_lambda, seed=cfg.seed)
     ctx.set_timing(0)
-    first_trees = []
+    first_trees, first_updates = [], []
     for w in range(args.warmup):
         P.iteration = w
         tr = gbt.gbt_train_tree(ctx, mx, label, margin, P)
         first_trees.append(tr.nodes.copy())
+        first_updates.append(tr.stats.hist_updates)
     torch.cuda.synchronize()
     # the timed steps carry no events: a HIP event pair around each histogram
     # launch leaves the GPU idle for a few microseconds per event
@@ -423,9 +448,8 @@ def main():
         "vs_baseline": None,
         "dtype": "int64",
         "data": "synthetic",
-        "config": {"workload": f"sampled regression {n:,} x 50, 20% missing, squared error, "
-                               f"max_bin 256, depth 8, MVS f={cfg.f}",
-                   "rows": n, "features": 50, "max_bin": cfg.max_bin, "max_depth": cfg.max_depth,
+        "config": {"workload": desc.format(n=n, f=cfg.f),
+                   "rows": n, "features": m, "max_bin": cfg.max_bin, "max_depth": cfg.max_depth,
                    "f": cfg.f},
         "sec_per_tree": round(dt / args.steps, 6),
         "rows_sampled_per_tree": round(sum(s.n_sampled for s in stats) / args.steps),
@@ -441,7 +465,7 @@ def main():
                                f"trees ({round(dt_ev * 1e3 / args.steps, 4)} ms per tree with the events)"},
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(X, y, cfg, args.cpu_trees, first_trees)
+        line["cpu_baseline"] = cpu_baseline(X, y, cfg, args.cpu_trees, first_trees, first_updates)
     print(json.dumps(line), flush=True)
 
 

@@ -172,6 +172,7 @@ struct gbt_matrix {
     float *cut_values_d = nullptr;
     int32_t *bin_ptr_d = nullptr;       // m+1 global bin offsets (cut_ptr[j] + j)
     std::vector<int32_t> bin_ptr_h;
+    std::vector<int64_t> feat_count_h;  // sparse: present values per feature in the sketch rows (m)
     std::vector<GbtPage> pages;
     // the histogram kernel's feature groups on the device, cached per kernel kind
     mutable void *groups_d = nullptr;
@@ -232,13 +233,20 @@ __device__ inline int32_t row_feature_bin(const uint32_t *__restrict__ row, cons
         uint32_t s = row_symbol(row, j, g.w, g.mask);
         return s == g.null_sym ? -1 : (int32_t)s;
     }
-    uint32_t lo = (uint32_t)g.bin_ptr[j], hi = (uint32_t)g.bin_ptr[j + 1];
-    for (int32_t s = 0; s < g.stride; ++s) {
-        uint32_t v = row_symbol(row, s, g.w, g.mask);
-        if (v >= hi) return -1;  // ascending global bins; null = total_bins ends the row
-        if (v >= lo) return (int32_t)(v - lo);
+    // the row's symbols are ascending global bins, padded with the null
+    // symbol (the largest): binary search for the first symbol >= lo
+    const uint32_t lo = (uint32_t)g.bin_ptr[j], hi = (uint32_t)g.bin_ptr[j + 1];
+    int32_t a = 0, b = g.stride;
+    while (a < b) {
+        const int32_t mid = (a + b) >> 1;
+        if (row_symbol(row, mid, g.w, g.mask) < lo)
+            a = mid + 1;
+        else
+            b = mid;
     }
-    return -1;
+    if (a == g.stride) return -1;
+    const uint32_t v = row_symbol(row, a, g.w, g.mask);
+    return v < hi ? (int32_t)(v - lo) : -1;
 }
 
 // Device node table entry used by the tree driver (heap order).  The split

@@ -19,8 +19,12 @@
 namespace gbt {
 
 constexpr int kHistThreads = 512;
-// Sparse groups: up to 4096 bins, g then h (64 KiB of LDS).
-constexpr int kLdsBins = 4096;
+// Sparse groups: up to 8192 bins, g then h (128 KiB of LDS), one
+// 1024-thread workgroup per CU: fewer groups, so fewer reads of every row.
+constexpr int kLdsBins = 8192;
+constexpr int kSparseThreads = 1024;
+// value-balanced sparse groups: at least this many
+constexpr int kSparseMinGroups = 16;
 // Dense groups: up to 2560 bins; the h sums sit a fixed 2560 words after the
 // g sums so that one address serves both atomics (an immediate offset), and
 // four workgroups fit a CU's LDS.
@@ -34,7 +38,7 @@ constexpr int kMaxGroupFeat = 32;
 // Zero nb entries of the g sums at sg and of the h sums at sh.
 __device__ inline void lds_zero(unsigned long long *sg, unsigned long long *sh, int32_t nb)
 {
-    for (int t = threadIdx.x; t < nb; t += kHistThreads) {
+    for (int t = threadIdx.x; t < nb; t += blockDim.x) {
         sg[t] = 0ull;
         sh[t] = 0ull;
     }
@@ -47,15 +51,15 @@ __device__ inline void lds_flush(const unsigned long long *sg, const unsigned lo
                                  int32_t nb, longlong2 *__restrict__ dst, unsigned long long cnt,
                                  unsigned long long *__restrict__ n_updates)
 {
-    __shared__ unsigned long long red[kHistThreads / 64];
+    __shared__ unsigned long long red[16];  // one count per wave (at most 1024 threads)
     if (n_updates && (threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = cnt;
     __syncthreads();
-    for (int t = threadIdx.x; t < nb; t += kHistThreads)
+    for (int t = threadIdx.x; t < nb; t += blockDim.x)
         dst[t] = make_longlong2((long long)sg[t], (long long)sh[t]);
     if (n_updates && threadIdx.x == 0) {
         // one atomic per block, spread over kUpdCounters addresses
         unsigned long long t = 0;
-        for (int w = 0; w < kHistThreads / 64; ++w) t += red[w];
+        for (int w = 0; w < (int)(blockDim.x / 64); ++w) t += red[w];
         if (t) atomicAdd(&n_updates[(blockIdx.x % kUpdCounters) * kUpdStride], t);
     }
 }
@@ -321,9 +325,19 @@ __global__ void __launch_bounds__(kRotThreads)
 }
 
 // Sparse rows: the row's present features in ascending order as global
-// bins, null padded; the group keeps the symbols in its bin range.
+// bins, null padded; the group keeps the symbols in its bin range.  A lane
+// finds the row's first symbol of the group by binary search (the symbols
+// are ascending) and reads on until the group's end.
+__device__ inline uint32_t sparse_symbol(const uint32_t *__restrict__ row, int32_t s, int32_t w, uint32_t mask)
+{
+    const uint32_t bit = (uint32_t)s * (uint32_t)w, k = bit >> 5, sh = bit & 31u;
+    uint32_t v = row[k] >> sh;
+    if (sh + (uint32_t)w > 32u) v |= row[k + 1] << (32u - sh);
+    return v & mask;
+}
+
 template <bool kRows>
-__global__ void __launch_bounds__(kHistThreads)
+__global__ void __launch_bounds__(kSparseThreads)
     k_hist_sparse(const uint32_t *__restrict__ page, int32_t row_words, int32_t w, uint32_t mask,
                   int32_t stride, const longlong2 *__restrict__ q, const int32_t *__restrict__ rows,
                   const HistWork *__restrict__ work, const HistGroup *__restrict__ groups,
@@ -340,28 +354,28 @@ __global__ void __launch_bounds__(kHistThreads)
     unsigned long long *sg = lds, *sh = lds + nb;
     lds_zero(sg, sh, nb);
     unsigned long long cnt = 0;
-    for (int64_t i = wk.begin + threadIdx.x; i < wk.end; i += kHistThreads) {
+    const uint32_t b0 = (uint32_t)gr.b0, b1 = (uint32_t)gr.b1;
+    for (int64_t i = wk.begin + threadIdx.x; i < wk.end; i += kSparseThreads) {
         const int64_t r = kRows ? (int64_t)rows[i] : i;
         const longlong2 qq = q[r];
         const unsigned long long qg = (unsigned long long)qq.x, qh = (unsigned long long)qq.y;
         const uint32_t *p = page + r * row_words;
-        uint64_t buf = (uint64_t)(*p++);
-        int32_t nbits = 32;
-        for (int32_t s = 0; s < stride; ++s) {
-            if (nbits < w) {
-                buf |= (uint64_t)(*p++) << nbits;
-                nbits += 32;
-            }
-            const uint32_t sym = (uint32_t)buf & mask;
-            buf >>= w;
-            nbits -= w;
-            if (sym >= (uint32_t)gr.b1) break;  // ascending; padding is the largest symbol
-            if (sym >= (uint32_t)gr.b0) {
-                const int32_t idx = (int32_t)sym - gr.b0;
-                atomicAdd(&sg[idx], qg);
-                atomicAdd(&sh[idx], qh);
-                ++cnt;
-            }
+        int32_t a = 0, e = stride;  // first slot whose symbol is >= b0
+        while (a < e) {
+            const int32_t mid = (a + e) >> 1;
+            if (sparse_symbol(p, mid, w, mask) < b0)
+                a = mid + 1;
+            else
+                e = mid;
+        }
+        for (int32_t s = a; s < stride; ++s) {
+            const uint32_t sym = sparse_symbol(p, s, w, mask);
+            if (sym >= b1) break;  // ascending; padding is the largest symbol
+            if (sym < b0) continue;  // only in a page whose symbols are not ascending
+            const int32_t idx = (int32_t)(sym - b0);
+            atomicAdd(&sg[idx], qg);
+            atomicAdd(&sh[idx], qh);
+            ++cnt;
         }
     }
     // the flush takes one count per wave
@@ -452,16 +466,32 @@ static bool dense_groups(const gbt_matrix *mx, int64_t max_bins, int max_feat, i
     return true;
 }
 
+// Sparse groups: contiguous features of at most kLdsBins bins.  With the
+// features' value counts known, a group also holds at most an equal share
+// of the values (popular features make groups of their own, so that no
+// group's workgroups carry most of the updates); otherwise the groups take
+// equal shares of the bins.
 static void sparse_groups(const gbt_matrix *mx, std::vector<HistGroup> *out)
 {
     out->clear();
     const int64_t tb = mx->total_bins;
     const int64_t G = std::max<int64_t>(1, (tb + kLdsBins - 1) / kLdsBins);
-    const int64_t target = (tb + G - 1) / G;
+    const bool counts = (int32_t)mx->feat_count_h.size() == mx->m;
+    int64_t total = 0;
+    if (counts)
+        for (int64_t v : mx->feat_count_h) total += v;
+    const int64_t Gc = std::max<int64_t>(G, kSparseMinGroups);
+    const int64_t target = counts ? kLdsBins : (tb + G - 1) / G;
+    const int64_t target_cnt = counts ? std::max<int64_t>(1, (total + Gc - 1) / Gc) : INT64_MAX;
     int32_t f0 = 0;
     while (f0 < mx->m) {
         int32_t f1 = f0 + 1;
-        while (f1 < mx->m && mx->bin_ptr_h[f1 + 1] - mx->bin_ptr_h[f0] <= target) ++f1;
+        int64_t cnt = counts ? mx->feat_count_h[f0] : 0;
+        while (f1 < mx->m && mx->bin_ptr_h[f1 + 1] - mx->bin_ptr_h[f0] <= target &&
+               (!counts || cnt + mx->feat_count_h[f1] <= target_cnt)) {
+            if (counts) cnt += mx->feat_count_h[f1];
+            ++f1;
+        }
         HistGroup g{f0, f1, mx->bin_ptr_h[f0], mx->bin_ptr_h[f1], 0, 0, 0, 0};
         out->push_back(g);
         f0 = f1;
@@ -479,8 +509,8 @@ gbt_status hist_plan(const gbt_matrix *mx, int64_t rows_hint, int choice, HistPl
             return set_error(GBT_E_UNSUPPORTED, "a feature has %d bins (at most %d)", max_feature_bins,
                              kLdsBins);
         out->kind = kHistSparse;
-        out->threads = kHistThreads;
-        out->target_wgs = 2 * kCUs;
+        out->threads = kSparseThreads;
+        out->target_wgs = kCUs;  // one workgroup per CU
         sparse_groups(mx, &out->groups);
     } else {
         if (mx->w < 1 || mx->w > 12 || max_feature_bins > kDenseBins)
@@ -639,11 +669,11 @@ gbt_status hist_launch_device(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
         if (mx->sparse) {
             size_t lds = (size_t)hl.max_groups_bins * 16;
             if (rows)
-                k_hist_sparse<true><<<grid, kHistThreads, lds, c->stream>>>(
+                k_hist_sparse<true><<<grid, kSparseThreads, lds, c->stream>>>(
                     page, mx->row_words, mx->w, mask, mx->stride, (const longlong2 *)q, rows, hl.work, hl.groups,
                     G, hl.n_work_d, tb, partials, upd);
             else
-                k_hist_sparse<false><<<grid, kHistThreads, lds, c->stream>>>(
+                k_hist_sparse<false><<<grid, kSparseThreads, lds, c->stream>>>(
                     page, mx->row_words, mx->w, mask, mx->stride, (const longlong2 *)q, rows, hl.work, hl.groups,
                     G, hl.n_work_d, tb, partials, upd);
         } else {

@@ -508,6 +508,7 @@ gbt_status gbt_quantize_finalize_cuts(gbt_quantizer *q)
 
     // per-feature key segments
     std::vector<int64_t> seg(m + 1, 0);
+    std::vector<int64_t> feat_count;  // CSR: present values per feature in the sketch rows
     uint32_t *keys = q->keys;
     uint32_t *sorted = nullptr;
     size_t sorted_bytes = 0;
@@ -526,6 +527,7 @@ gbt_status gbt_quantize_finalize_cuts(gbt_quantizer *q)
         GBT_HIP(hipMemcpyAsync(h.data(), cnt, m * 8, hipMemcpyDeviceToHost, c->stream));
         GBT_HIP(hipStreamSynchronize(c->stream));
         for (int32_t j = 0; j < m; ++j) seg[j + 1] = seg[j] + (int64_t)h[j];
+        feat_count.assign(h.begin(), h.begin() + m);
         std::vector<unsigned long long> cur(m);
         for (int32_t j = 0; j < m; ++j) cur[j] = (unsigned long long)seg[j];
         GBT_HIP(hipMemcpyAsync(cnt, cur.data(), m * 8, hipMemcpyHostToDevice, c->stream));
@@ -705,6 +707,7 @@ gbt_status gbt_quantize_finalize_cuts(gbt_quantizer *q)
     gbt_matrix *mx = new gbt_matrix();
     q->mat = mx;
     mx->ctx = c;
+    mx->feat_count_h = std::move(feat_count);
     mx->n_rows = q->n_total;
     mx->m = m;
     mx->sparse = q->kind == GBT_INPUT_CSR_F32;
