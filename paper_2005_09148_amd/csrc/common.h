@@ -134,6 +134,7 @@ enum ScratchSlot {
     kScrCompact,     // compact tree for the row walk
     kScrPlan,        // device-side level plans (lists, work items, counts)
     kScrPartialsDev, // partial histograms of the device-planned levels
+    kScrSlotTbl,     // slot table of a sparse training page
     kScrCount
 };
 
@@ -245,6 +246,38 @@ __device__ inline int32_t row_feature_bin(const uint32_t *__restrict__ row, cons
             b = mid;
     }
     if (a == g.stride) return -1;
+    const uint32_t v = row_symbol(row, a, g.w, g.mask);
+    return v < hi ? (int32_t)(v - lo) : -1;
+}
+
+// Sparse pages: for each row, the first slot of every histogram feature
+// group's symbols, so that group g's symbols are the row's slots
+// [slot[g], slot[g + 1]) (the symbols ascend and the groups are contiguous
+// bin ranges).  Built by the tree driver for the page it trains on; a
+// search for a feature then looks only among its group's few slots.
+struct SlotTable {
+    const uint8_t *slot;      // rows x stride bytes; NULL: no table
+    const uint8_t *feat_grp;  // m: the group of each feature
+    int32_t stride;           // bytes per row (> number of groups)
+    int32_t pad0;
+};
+
+// row_feature_bin for a sparse row with the row's slot-table entry `ts`.
+__device__ inline int32_t row_feature_bin_tbl(const uint32_t *__restrict__ row, const uint8_t *__restrict__ ts,
+                                              const Geo &g, const uint8_t *__restrict__ feat_grp, int32_t j)
+{
+    const uint32_t lo = (uint32_t)g.bin_ptr[j], hi = (uint32_t)g.bin_ptr[j + 1];
+    const int32_t fg = feat_grp[j];
+    int32_t a = ts[fg], b = ts[fg + 1];
+    const int32_t e = b;
+    while (a < b) {
+        const int32_t mid = (a + b) >> 1;
+        if (row_symbol(row, mid, g.w, g.mask) < lo)
+            a = mid + 1;
+        else
+            b = mid;
+    }
+    if (a == e) return -1;
     const uint32_t v = row_symbol(row, a, g.w, g.mask);
     return v < hi ? (int32_t)(v - lo) : -1;
 }

@@ -342,14 +342,16 @@ __global__ void __launch_bounds__(kSparseThreads)
                   int32_t stride, const longlong2 *__restrict__ q, const int32_t *__restrict__ rows,
                   const HistWork *__restrict__ work, const HistGroup *__restrict__ groups,
                   int32_t n_groups, const int32_t *__restrict__ n_work_d, int64_t total_bins,
-                  longlong2 *__restrict__ partials, unsigned long long *__restrict__ n_updates)
+                  longlong2 *__restrict__ partials, unsigned long long *__restrict__ n_updates,
+                  const uint8_t *__restrict__ slot_tbl, int32_t tbl_stride)
 {
     extern __shared__ unsigned long long lds[];
     const uint32_t active = n_work_d ? (uint32_t)(*n_work_d * n_groups) : gridDim.x;
     if (blockIdx.x >= active) return;
     const uint32_t L = xcd_remap(blockIdx.x, active);
     const HistWork wk = work[L / n_groups];
-    const HistGroup gr = groups[L % n_groups];
+    const int32_t gi = (int32_t)(L % n_groups);
+    const HistGroup gr = groups[gi];
     const int32_t nb = gr.b1 - gr.b0;
     unsigned long long *sg = lds, *sh = lds + nb;
     lds_zero(sg, sh, nb);
@@ -357,18 +359,27 @@ __global__ void __launch_bounds__(kSparseThreads)
     const uint32_t b0 = (uint32_t)gr.b0, b1 = (uint32_t)gr.b1;
     for (int64_t i = wk.begin + threadIdx.x; i < wk.end; i += kSparseThreads) {
         const int64_t r = kRows ? (int64_t)rows[i] : i;
+        const uint32_t *p = page + r * row_words;
+        int32_t a = 0, e = stride;  // the slots to read: [a, e)
+        if (slot_tbl) {
+            const uint8_t *t = slot_tbl + r * tbl_stride + gi;
+            a = t[0];
+            e = t[1];
+            if (a >= e) continue;  // no symbol of the group in this row
+        } else {
+            int32_t x = 0, y = stride;  // first slot whose symbol is >= b0
+            while (x < y) {
+                const int32_t mid = (x + y) >> 1;
+                if (sparse_symbol(p, mid, w, mask) < b0)
+                    x = mid + 1;
+                else
+                    y = mid;
+            }
+            a = x;
+        }
         const longlong2 qq = q[r];
         const unsigned long long qg = (unsigned long long)qq.x, qh = (unsigned long long)qq.y;
-        const uint32_t *p = page + r * row_words;
-        int32_t a = 0, e = stride;  // first slot whose symbol is >= b0
-        while (a < e) {
-            const int32_t mid = (a + e) >> 1;
-            if (sparse_symbol(p, mid, w, mask) < b0)
-                a = mid + 1;
-            else
-                e = mid;
-        }
-        for (int32_t s = a; s < stride; ++s) {
+        for (int32_t s = a; s < e; ++s) {
             const uint32_t sym = sparse_symbol(p, s, w, mask);
             if (sym >= b1) break;  // ascending; padding is the largest symbol
             if (sym < b0) continue;  // only in a page whose symbols are not ascending
@@ -381,6 +392,77 @@ __global__ void __launch_bounds__(kSparseThreads)
     // the flush takes one count per wave
     for (int d = 32; d > 0; d >>= 1) cnt += __shfl_xor(cnt, d, 64);
     lds_flush(sg, sh, nb, partials + (int64_t)wk.part * total_bins + gr.b0, cnt, n_updates);
+}
+
+// Slot table of a sparse page.  A block stages 256 consecutive rows in LDS
+// (one word of padding per row keeps the threads' reads on distinct banks),
+// each thread walks its row's ascending symbols once and records where each
+// group's bin range starts, and the block writes its rows' table entries
+// with word stores.
+constexpr int kTblThreads = 256;
+constexpr int kTblMaxStride = 64;  // bytes per table row
+constexpr int kTblMaxWords = 63;   // row words a block stages
+
+__global__ void __launch_bounds__(kTblThreads)
+    k_sparse_slot_table(const uint32_t *__restrict__ page, int64_t n, int32_t row_words, int32_t stride, int32_t w,
+                        uint32_t mask, const HistGroup *__restrict__ groups, int32_t G, uint8_t *__restrict__ tbl,
+                        int32_t tstride)
+{
+    extern __shared__ uint32_t rows_l[];  // kTblThreads x (row_words + 1)
+    __shared__ uint32_t ends[kTblMaxStride];
+    __shared__ uint32_t out_l[kTblThreads * kTblMaxStride / 4];
+    uint8_t *out_b = (uint8_t *)out_l;
+    const int64_t r0 = (int64_t)blockIdx.x * kTblThreads;
+    const int32_t nr = (int32_t)min<int64_t>(kTblThreads, n - r0);
+    const int32_t nw = nr * row_words, lw = row_words + 1;
+    const uint32_t *src = page + r0 * row_words;
+    for (int32_t k = threadIdx.x; k < nw; k += kTblThreads) {
+        const int32_t rr = k / row_words;
+        rows_l[rr * lw + (k - rr * row_words)] = src[k];
+    }
+    for (int32_t g = threadIdx.x; g < G; g += kTblThreads) ends[g] = (uint32_t)groups[g].b1;
+    __syncthreads();
+    if ((int32_t)threadIdx.x < nr) {
+        const uint32_t *row = rows_l + threadIdx.x * lw;
+        uint8_t *o = out_b + threadIdx.x * tstride;
+        int32_t g = 0;
+        o[0] = 0;
+        for (int32_t s = 0; s < stride && g < G; ++s) {
+            const uint32_t bit = (uint32_t)s * (uint32_t)w, k = bit >> 5, sh = bit & 31u;
+            uint32_t v = row[k] >> sh;
+            if (sh + (uint32_t)w > 32u) v |= row[k + 1] << (32u - sh);
+            v &= mask;
+            while (g < G && v >= ends[g]) o[++g] = (uint8_t)s;
+        }
+        while (g < G) o[++g] = (uint8_t)stride;
+        for (int32_t k = G + 1; k < tstride; ++k) o[k] = 0;
+    }
+    __syncthreads();
+    const int32_t ow = nr * tstride / 4;
+    uint32_t *dst = (uint32_t *)(tbl + r0 * tstride);
+    for (int32_t k = threadIdx.x; k < ow; k += kTblThreads) dst[k] = out_l[k];
+}
+
+int32_t slot_table_stride(const gbt_matrix *mx, int32_t G)
+{
+    if (!mx->sparse || G < 1 || mx->stride > 255 || mx->row_words > kTblMaxWords) return 0;
+    const int32_t s = (G + 1 + 3) / 4 * 4;
+    return s <= kTblMaxStride ? s : 0;
+}
+
+gbt_status sparse_slot_table(gbt_ctx *c, const gbt_matrix *mx, const HistGroup *groups_d, int32_t G,
+                             const uint32_t *page, int64_t n, uint8_t *tbl, int32_t stride)
+{
+    if (stride != slot_table_stride(mx, G) || stride == 0)
+        return set_error(GBT_E_INVALID, "slot table stride %d does not fit the page", stride);
+    if (n <= 0) return GBT_OK;
+    const uint32_t mask = mx->w >= 32 ? 0xffffffffu : ((1u << mx->w) - 1u);
+    const size_t lds = (size_t)kTblThreads * (mx->row_words + 1) * 4;
+    const unsigned grid = (unsigned)((n + kTblThreads - 1) / kTblThreads);
+    k_sparse_slot_table<<<grid, kTblThreads, lds, c->stream>>>(page, n, mx->row_words, mx->stride, mx->w, mask,
+                                                               groups_d, G, tbl, stride);
+    GBT_LAUNCHED();
+    return GBT_OK;
 }
 
 // Sums each built node's partials into its histogram and, in the same pass,
@@ -671,11 +753,11 @@ gbt_status hist_launch_device(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
             if (rows)
                 k_hist_sparse<true><<<grid, kSparseThreads, lds, c->stream>>>(
                     page, mx->row_words, mx->w, mask, mx->stride, (const longlong2 *)q, rows, hl.work, hl.groups,
-                    G, hl.n_work_d, tb, partials, upd);
+                    G, hl.n_work_d, tb, partials, upd, hl.slot_tbl, hl.tbl_stride);
             else
                 k_hist_sparse<false><<<grid, kSparseThreads, lds, c->stream>>>(
                     page, mx->row_words, mx->w, mask, mx->stride, (const longlong2 *)q, rows, hl.work, hl.groups,
-                    G, hl.n_work_d, tb, partials, upd);
+                    G, hl.n_work_d, tb, partials, upd, hl.slot_tbl, hl.tbl_stride);
         } else {
             const size_t lds = (size_t)(kDenseBins + hl.max_groups_bins) * 8;
             const longlong2 *qq = (const longlong2 *)q;

@@ -69,7 +69,20 @@ struct HistLaunch {
     const int32_t *n_red_d;
     int32_t max_red;
     int64_t *partials;
+    const uint8_t *slot_tbl = nullptr;  // sparse: the page's slot table (SlotTable::slot), or NULL
+    int32_t tbl_stride = 0;
 };
+
+// Bytes per row of a sparse page's slot table for G groups, or 0 when the
+// page does not take one (a row of more than 255 slots, more than 63 groups,
+// or rows too long to stage in LDS).
+int32_t slot_table_stride(const gbt_matrix *mx, int32_t G);
+// The slot table of rows [0, n) of `page` (a page of mx's geometry) for the
+// groups groups_d[0, G): tbl[r * stride + g] = first slot of row r whose
+// symbol is >= groups_d[g].b0; tbl[r * stride + G] = first slot past the
+// last group.
+gbt_status sparse_slot_table(gbt_ctx *c, const gbt_matrix *mx, const HistGroup *groups_d, int32_t G,
+                             const uint32_t *page, int64_t n, uint8_t *tbl, int32_t stride);
 
 gbt_status hist_launch_device(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int64_t *q,
                               const int32_t *rows, const HistLaunch &hl, const int64_t *parent_hist,

@@ -592,7 +592,7 @@ __global__ void __launch_bounds__(kPartThreads)
     k_part_flags_tiles(const int32_t *__restrict__ rows, int64_t n, const uint32_t *__restrict__ page, Geo geo,
                        const int32_t *__restrict__ position, const int32_t *__restrict__ slot_node,
                        DevNode *__restrict__ nodes, uint8_t *__restrict__ flags,
-                       int32_t *__restrict__ tile_cnt, LevelChoice lc)
+                       int32_t *__restrict__ tile_cnt, LevelChoice lc, SlotTable stbl)
 {
     __shared__ int32_t red[kPartThreads / 64];
     const int64_t i0 = (int64_t)blockIdx.x * kPartTile + (int64_t)threadIdx.x * kPartItems;
@@ -636,7 +636,10 @@ __global__ void __launch_bounds__(kPartThreads)
     for (int k = 0; k < kPartItems; ++k) {
         uint32_t f = 0;
         if (rec[k].x) {
-            const int32_t b = row_feature_bin(page + (int64_t)r[k] * geo.row_words, geo, rec[k].y);
+            const uint32_t *row = page + (int64_t)r[k] * geo.row_words;
+            const int32_t b = stbl.slot ? row_feature_bin_tbl(row, stbl.slot + (int64_t)r[k] * stbl.stride, geo,
+                                                              stbl.feat_grp, rec[k].y)
+                                        : row_feature_bin(row, geo, rec[k].y);
             f = (b < 0) ? (rec[k].w != 0 ? 1u : 0u) : (b < rec[k].z ? 1u : 0u);
         }
         f4 |= f << (8 * k);
@@ -885,9 +888,10 @@ __global__ void __launch_bounds__(kPartThreads)
 
 gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int32_t *rows,
                               int64_t n, const int32_t *slot_node, int32_t *slot_node_out, DevNode *nodes,
-                              int32_t *rows_out, const LevelChoice *choice)
+                              int32_t *rows_out, const LevelChoice *choice, const SlotTable *stbl)
 {
     if (n == 0) return GBT_OK;
+    const SlotTable st = stbl ? *stbl : SlotTable{nullptr, nullptr, 0, 0};
     GBT_CHECK(n < ((int64_t)1 << 31) - 1, "partition of %lld rows (limit 2^31-2)", (long long)n);
     uint8_t *flags;
     GBT_TRY(scratch_t(c, kScrPartFlags, (size_t)n + 16, &flags));
@@ -896,10 +900,10 @@ gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
     GBT_TRY(scratch_t(c, kScrScan, (size_t)tiles + 1, &tile_cnt));
     if (choice)
         k_part_flags_tiles<true><<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(
-            rows, n, page, geo_of(mx), nullptr, slot_node, nodes, flags, tile_cnt, *choice);
+            rows, n, page, geo_of(mx), nullptr, slot_node, nodes, flags, tile_cnt, *choice, st);
     else
         k_part_flags_tiles<false><<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(
-            rows, n, page, geo_of(mx), nullptr, slot_node, nodes, flags, tile_cnt, LevelChoice{});
+            rows, n, page, geo_of(mx), nullptr, slot_node, nodes, flags, tile_cnt, LevelChoice{}, st);
     GBT_LAUNCHED();
     k_part_scatter_rev<<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(rows, n, flags, tile_cnt, slot_node,
                                                                        slot_node_out, nodes, rows_out);
@@ -923,7 +927,8 @@ gbt_status partition_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page
     // tile_off receives each tile's left count; the bounds and the scatter
     // sum the counts before their tiles themselves
     k_part_flags_tiles<false><<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(rows, n, page, geo, position, slot_node,
-                                                                       nodes, flags, tile_off, LevelChoice{});
+                                                                       nodes, flags, tile_off, LevelChoice{},
+                                                                       SlotTable{nullptr, nullptr, 0, 0});
     GBT_LAUNCHED();
     if (n_list > 0) {
         k_part_bounds<<<(unsigned)n_list, kBoundThreads, 0, c->stream>>>(list, n_list_d, n_list, nodes, flags,

@@ -79,9 +79,12 @@ struct LevelChoice {
 // in reverse slot order; nodes[id].nleft receives each splitting node's left
 // count (pleft is not written).  Two kernels.  With `choice`, the split
 // records of the level's nodes are chosen from the candidates and written
-// by the first kernel (instead of by eval_reduce_impl).
+// by the first kernel (instead of by eval_reduce_impl).  With `stbl` (a
+// sparse page's slot table), the search for a row's split feature looks
+// only among the slots of the feature's group.
 gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int32_t *rows,
                               int64_t n, const int32_t *slot_node, int32_t *slot_node_out, DevNode *nodes,
-                              int32_t *rows_out, const LevelChoice *choice = nullptr);
+                              int32_t *rows_out, const LevelChoice *choice = nullptr,
+                              const SlotTable *stbl = nullptr);
 
 }  // namespace gbt

@@ -908,9 +908,19 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     HistWork *work_d = (HistWork *)(plan + o_work);
     HistReduce *red_d = (HistReduce *)(plan + o_red);
     // the feature groups live with the matrix (uploaded once per kernel kind)
+    // sparse pages: the slot table of the training page, and each feature's
+    // group (stored after the groups)
+    const int32_t tstride = hp.kind == kHistSparse ? slot_table_stride(mx, G) : 0;
+    const size_t fg_off = (std::max<size_t>(groups.size(), 1) * sizeof(HistGroup) + 15) / 16 * 16;
     if (mx->groups_kind != hp.kind) {
         // owned (and budgeted) by the matrix's context, like its other arrays
-        const size_t gb = std::max<size_t>(groups.size(), 1) * sizeof(HistGroup);
+        std::vector<uint8_t> fg;
+        if (tstride) {
+            fg.assign((size_t)mx->m, 0);
+            for (int32_t g = 0; g < G; ++g)
+                for (int32_t f = groups[g].f0; f < groups[g].f1; ++f) fg[f] = (uint8_t)g;
+        }
+        const size_t gb = fg_off + fg.size();
         if (mx->groups_d) dev_free(mx->ctx, mx->groups_d, mx->groups_bytes);
         mx->groups_d = nullptr;
         mx->groups_kind = -1;
@@ -918,10 +928,20 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         mx->groups_bytes = gb;
         GBT_HIP(hipMemcpyAsync(mx->groups_d, groups.data(), groups.size() * sizeof(HistGroup),
                                hipMemcpyHostToDevice, c->stream));
+        if (!fg.empty())
+            GBT_HIP(hipMemcpyAsync((char *)mx->groups_d + fg_off, fg.data(), fg.size(), hipMemcpyHostToDevice,
+                                   c->stream));
         GBT_HIP(hipStreamSynchronize(c->stream));
         mx->groups_kind = hp.kind;
     }
     const HistGroup *groups_d = (const HistGroup *)mx->groups_d;
+    SlotTable stbl{nullptr, nullptr, 0, 0};
+    if (tstride && D > 0 && R > 0) {
+        uint8_t *tb;
+        GBT_TRY(scratch_t(c, kScrSlotTbl, (size_t)R * tstride, &tb));
+        GBT_TRY(sparse_slot_table(c, mx, groups_d, G, so.page, R, tb, tstride));
+        stbl = SlotTable{tb, (const uint8_t *)mx->groups_d + fg_off, tstride, 0};
+    }
     int64_t *partials = nullptr;
     GBT_TRY(scratch(c, kScrPartialsDev, (size_t)std::max(max_items, 1) * mx->total_bins * 16, (void **)&partials));
     const int64_t n_init = std::max<int64_t>({(int64_t)NN, (int64_t)n_root, R, (int64_t)kUpdCounters});
@@ -945,7 +965,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     int32_t *cntA = cnt, *cntB = cnt + 1;
     if (D > 0 && R > 0) {
         HistLaunch hl{hp.kind, groups_d, G, hp.max_groups_bins, work_d, nullptr, n_root, red_d, nullptr,
-                      fused ? 0 : 1, partials};
+                      fused ? 0 : 1, partials, stbl.slot, stbl.stride};
         GBT_TRY(hist_launch_device(c, mx, so.page, so.q, nullptr, hl, nullptr, histA, upd));
         ++hist_launches;
         if (fused) {
@@ -961,7 +981,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         if (!fused && R > 0) GBT_TRY(eval_impl(c, mx, histA, evA, maxn, ep, splits_d, cntA, nodes));
         const LevelChoice lc{cand, mx->m, (int32_t)((1u << d) - 1), (int32_t)((2u << d) - 1)};
         GBT_TRY(partition_rev_impl(c, mx, so.page, rows, R, slot_node, slot_tmp, nodes, rows_tmp,
-                                   choose ? &lc : nullptr));
+                                   choose ? &lc : nullptr, stbl.slot ? &stbl : nullptr));
         std::swap(rows, rows_tmp);
         std::swap(slot_node, slot_tmp);
         const bool plan_next = d + 1 < D && R > 0;
@@ -973,7 +993,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         timer_end(c, mark);
         if (plan_next) {
             HistLaunch hl{hp.kind, groups_d, G, hp.max_groups_bins, work_d, cnt + 2, max_work, red_d, cnt + 3,
-                          fused ? 0 : maxn, partials};
+                          fused ? 0 : maxn, partials, stbl.slot, stbl.stride};
             GBT_TRY(hist_launch_device(c, mx, so.page, so.q, rows, hl, histA, histB, upd));
             ++hist_launches;
             if (fused) {
