@@ -416,9 +416,22 @@ __global__ void __launch_bounds__(kTblThreads)
     const int32_t nr = (int32_t)min<int64_t>(kTblThreads, n - r0);
     const int32_t nw = nr * row_words, lw = row_words + 1;
     const uint32_t *src = page + r0 * row_words;
-    for (int32_t k = threadIdx.x; k < nw; k += kTblThreads) {
-        const int32_t rr = k / row_words;
-        rows_l[rr * lw + (k - rr * row_words)] = src[k];
+    // eight loads in flight per thread before their LDS stores
+    for (int32_t k0 = 0; k0 < nw; k0 += kTblThreads * 8) {
+        uint32_t v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int32_t k = k0 + j * kTblThreads + (int32_t)threadIdx.x;
+            v[j] = k < nw ? src[k] : 0u;
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int32_t k = k0 + j * kTblThreads + (int32_t)threadIdx.x;
+            if (k < nw) {
+                const int32_t rr = k / row_words;
+                rows_l[rr * lw + (k - rr * row_words)] = v[j];
+            }
+        }
     }
     for (int32_t g = threadIdx.x; g < G; g += kTblThreads) ends[g] = (uint32_t)groups[g].b1;
     __syncthreads();
@@ -549,10 +562,10 @@ static bool dense_groups(const gbt_matrix *mx, int64_t max_bins, int max_feat, i
 }
 
 // Sparse groups: contiguous features of at most kLdsBins bins.  With the
-// features' value counts known, a group also holds at most an equal share
-// of the values (popular features make groups of their own, so that no
-// group's workgroups carry most of the updates); otherwise the groups take
-// equal shares of the bins.
+// features' value counts known, a group also holds at most twice an equal
+// share (over max(groups by bins, kSparseMinGroups)) of the values, so that
+// popular features make small groups and no group's workgroups carry most
+// of the updates; otherwise the groups take equal shares of the bins.
 static void sparse_groups(const gbt_matrix *mx, std::vector<HistGroup> *out)
 {
     out->clear();
@@ -564,7 +577,7 @@ static void sparse_groups(const gbt_matrix *mx, std::vector<HistGroup> *out)
         for (int64_t v : mx->feat_count_h) total += v;
     const int64_t Gc = std::max<int64_t>(G, kSparseMinGroups);
     const int64_t target = counts ? kLdsBins : (tb + G - 1) / G;
-    const int64_t target_cnt = counts ? std::max<int64_t>(1, (total + Gc - 1) / Gc) : INT64_MAX;
+    const int64_t target_cnt = counts ? std::max<int64_t>(1, 2 * ((total + Gc - 1) / Gc)) : INT64_MAX;
     int32_t f0 = 0;
     while (f0 < mx->m) {
         int32_t f1 = f0 + 1;
@@ -592,7 +605,7 @@ gbt_status hist_plan(const gbt_matrix *mx, int64_t rows_hint, int choice, HistPl
                              kLdsBins);
         out->kind = kHistSparse;
         out->threads = kSparseThreads;
-        out->target_wgs = kCUs;  // one workgroup per CU
+        out->target_wgs = 2 * kCUs;  // two rounds of one workgroup per CU
         sparse_groups(mx, &out->groups);
     } else {
         if (mx->w < 1 || mx->w > 12 || max_feature_bins > kDenseBins)

@@ -382,6 +382,88 @@ __global__ void __launch_bounds__(256 * kSub)
     if (lane == 0) cand[(int64_t)slot * m + f] = o;
 }
 
+// k_reduce_eval for features of at most 64 bins: one wave per (feature,
+// node), four features per block, each lane one bin; the wave evaluates the
+// built node and then its sibling.
+constexpr int kNarrowBins = 64;
+
+__global__ void __launch_bounds__(256)
+    k_reduce_eval_narrow(const longlong2 *__restrict__ partials, const HistReduce *__restrict__ red,
+                         const int32_t *__restrict__ n_red_d, const longlong2 *__restrict__ parent,
+                         longlong2 *__restrict__ hist, int64_t total_bins, const int32_t *__restrict__ bin_ptr,
+                         int32_t m, const EvalNode *__restrict__ ev, EvalParams ep, EvalCand *__restrict__ cand)
+{
+    if (n_red_d && (int32_t)blockIdx.y >= *n_red_d) return;
+    __shared__ longlong2 hb[4][kNarrowBins], hs[4][kNarrowBins];
+    const HistReduce rd = red[blockIdx.y];
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    const int32_t f = blockIdx.x * 4 + wid;
+    const bool live = f < m;
+    const int32_t b0 = live ? bin_ptr[f] : 0, B = live ? bin_ptr[f + 1] - b0 : 0;
+    const bool sib = rd.sub_target >= 0;
+    long long g = 0, h = 0, pg = 0, ph = 0;
+    if (lane < B) {
+        const longlong2 *src = partials + (int64_t)rd.part0 * total_bins + b0 + lane;
+        int32_t k = 0;
+        // eight loads in flight per lane
+        for (; k + 7 < rd.nparts; k += 8) {
+            longlong2 v[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) v[j] = src[(int64_t)(k + j) * total_bins];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                g += v[j].x;
+                h += v[j].y;
+            }
+        }
+        for (; k < rd.nparts; ++k) {
+            const longlong2 v = src[(int64_t)k * total_bins];
+            g += v.x;
+            h += v.y;
+        }
+        if (sib) {
+            const longlong2 pv = parent[(int64_t)rd.sub_parent * total_bins + b0 + lane];
+            pg = pv.x - g;
+            ph = pv.y - h;
+        }
+        if (hist) {
+            hist[(int64_t)rd.slot * total_bins + b0 + lane] = make_longlong2(g, h);
+            if (sib) hist[(int64_t)rd.sub_target * total_bins + b0 + lane] = make_longlong2(pg, ph);
+        }
+    }
+    hb[wid][lane] = make_longlong2(g, h);
+    hs[wid][lane] = make_longlong2(pg, ph);
+    __syncthreads();
+    if (!live) return;
+    if (ep.e_dev) {
+        ep.e_g = ep.e_dev[0];
+        ep.e_h = ep.e_dev[1];
+    }
+    for (int which = 0; which < (sib ? 2 : 1); ++which) {
+        const int32_t slot = which == 0 ? rd.slot : rd.sub_target;
+        EvalCand o;
+        o.valid = 0;
+        o.gain = 0.0;
+        o.feature = f;
+        o.split_bin = -1;
+        o.default_left = 0;
+        o.lg = o.lh = 0;
+        if (B >= 2) {
+            const EvalNode nd = ev[slot];
+            const Cand cb = eval_feature(which == 0 ? hb[wid] : hs[wid], B, nd.sum_g, nd.sum_h, ep);
+            if (cb.valid) {
+                o.valid = 1;
+                o.gain = cb.gain;
+                o.split_bin = cb.order >> 1;
+                o.default_left = cb.order & 1;
+                o.lg = cb.lg;
+                o.lh = cb.lh;
+            }
+        }
+        if (lane == 0) cand[(int64_t)slot * m + f] = o;
+    }
+}
+
 // Each node's best candidate over its features, one wave per node: the
 // highest gain, ties to the lowest feature (candidates are in feature order).
 __global__ void __launch_bounds__(256)
@@ -440,6 +522,17 @@ gbt_status reduce_eval_impl(gbt_ctx *c, const gbt_matrix *mx, const int64_t *par
                             const EvalNode *ev, const EvalParams &ep, EvalCand *cand)
 {
     if (max_red <= 0) return GBT_OK;
+    int32_t max_feature_bins = 0;
+    for (int32_t f = 0; f < mx->m; ++f)
+        max_feature_bins = std::max(max_feature_bins, mx->bin_ptr_h[f + 1] - mx->bin_ptr_h[f]);
+    if (max_feature_bins <= kNarrowBins) {
+        dim3 g4((unsigned)((mx->m + 3) / 4), (unsigned)max_red);
+        k_reduce_eval_narrow<<<g4, 256, 0, c->stream>>>((const longlong2 *)partials, red, n_red_d,
+                                                        (const longlong2 *)parent, (longlong2 *)hist,
+                                                        mx->total_bins, mx->bin_ptr_d, mx->m, ev, ep, cand);
+        GBT_LAUNCHED();
+        return GBT_OK;
+    }
     dim3 grid((unsigned)mx->m, (unsigned)max_red);
     // many (feature, node) blocks: the narrow form keeps more of them resident
     if ((int64_t)max_red * mx->m >= 2 * kCUs)
