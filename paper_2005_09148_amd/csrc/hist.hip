@@ -394,61 +394,72 @@ __global__ void __launch_bounds__(kSparseThreads)
     lds_flush(sg, sh, nb, partials + (int64_t)wk.part * total_bins + gr.b0, cnt, n_updates);
 }
 
-// Slot table of a sparse page.  A block stages 256 consecutive rows in LDS
-// (one word of padding per row keeps the threads' reads on distinct banks),
-// each thread walks its row's ascending symbols once and records where each
-// group's bin range starts, and the block writes its rows' table entries
-// with word stores.
+// Slot table of a sparse page: a thread per row loads the row's words into
+// registers with 16-byte loads (all in flight at once) and reads its
+// symbols in order through a 64-bit bit buffer (the symbol width is the
+// same for every row, so the decode loop is uniform); a symbol at or past
+// the current group's end opens the next groups.  The block assembles its
+// rows' entries in LDS and writes them with word stores.
 constexpr int kTblThreads = 256;
 constexpr int kTblMaxStride = 64;  // bytes per table row
-constexpr int kTblMaxWords = 63;   // row words a block stages
+constexpr int kTblMaxWords = 64;   // row words held in registers
 
+typedef uint32_t u32x4_t4 __attribute__((ext_vector_type(4), aligned(4)));
+
+template <int kMaxWords>
 __global__ void __launch_bounds__(kTblThreads)
     k_sparse_slot_table(const uint32_t *__restrict__ page, int64_t n, int32_t row_words, int32_t stride, int32_t w,
                         uint32_t mask, const HistGroup *__restrict__ groups, int32_t G, uint8_t *__restrict__ tbl,
                         int32_t tstride)
 {
-    extern __shared__ uint32_t rows_l[];  // kTblThreads x (row_words + 1)
     __shared__ uint32_t ends[kTblMaxStride];
     __shared__ uint32_t out_l[kTblThreads * kTblMaxStride / 4];
-    uint8_t *out_b = (uint8_t *)out_l;
+    uint8_t *o = (uint8_t *)out_l + threadIdx.x * tstride;
+    for (int32_t g = threadIdx.x; g < kTblMaxStride; g += kTblThreads)
+        ends[g] = g < G ? (uint32_t)groups[g].b1 : 0xffffffffu;
     const int64_t r0 = (int64_t)blockIdx.x * kTblThreads;
     const int32_t nr = (int32_t)min<int64_t>(kTblThreads, n - r0);
-    const int32_t nw = nr * row_words, lw = row_words + 1;
-    const uint32_t *src = page + r0 * row_words;
-    // eight loads in flight per thread before their LDS stores
-    for (int32_t k0 = 0; k0 < nw; k0 += kTblThreads * 8) {
-        uint32_t v[8];
+    uint32_t wd[kMaxWords];
+    if ((int32_t)threadIdx.x < nr) {
+        const uint32_t *row = page + (r0 + threadIdx.x) * row_words;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int32_t k = k0 + j * kTblThreads + (int32_t)threadIdx.x;
-            v[j] = k < nw ? src[k] : 0u;
-        }
+        for (int q = 0; q < kMaxWords / 4; ++q) {
+            if (4 * q + 4 <= row_words) {
+                const u32x4_t4 v = *(const u32x4_t4 *)(row + 4 * q);
+                wd[4 * q] = v.x;
+                wd[4 * q + 1] = v.y;
+                wd[4 * q + 2] = v.z;
+                wd[4 * q + 3] = v.w;
+            } else {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int32_t k = k0 + j * kTblThreads + (int32_t)threadIdx.x;
-            if (k < nw) {
-                const int32_t rr = k / row_words;
-                rows_l[rr * lw + (k - rr * row_words)] = v[j];
+                for (int j = 0; j < 4; ++j) wd[4 * q + j] = 4 * q + j < row_words ? row[4 * q + j] : 0u;
             }
         }
     }
-    for (int32_t g = threadIdx.x; g < G; g += kTblThreads) ends[g] = (uint32_t)groups[g].b1;
     __syncthreads();
     if ((int32_t)threadIdx.x < nr) {
-        const uint32_t *row = rows_l + threadIdx.x * lw;
-        uint8_t *o = out_b + threadIdx.x * tstride;
-        int32_t g = 0;
+        uint64_t buf = 0;
+        int32_t nb = 0, s = 0, g = 0;
+        uint32_t end = ends[0];
         o[0] = 0;
-        for (int32_t s = 0; s < stride && g < G; ++s) {
-            const uint32_t bit = (uint32_t)s * (uint32_t)w, k = bit >> 5, sh = bit & 31u;
-            uint32_t v = row[k] >> sh;
-            if (sh + (uint32_t)w > 32u) v |= row[k + 1] << (32u - sh);
-            v &= mask;
-            while (g < G && v >= ends[g]) o[++g] = (uint8_t)s;
+#pragma unroll
+        for (int k = 0; k < kMaxWords; ++k) {
+            if (k < row_words) {
+                buf |= (uint64_t)wd[k] << nb;
+                nb += 32;
+                while (nb >= w && s < stride) {
+                    const uint32_t v = (uint32_t)buf & mask;
+                    buf >>= w;
+                    nb -= w;
+                    while (v >= end && g < G) {
+                        o[++g] = (uint8_t)s;
+                        end = ends[g];
+                    }
+                    ++s;
+                }
+            }
         }
         while (g < G) o[++g] = (uint8_t)stride;
-        for (int32_t k = G + 1; k < tstride; ++k) o[k] = 0;
     }
     __syncthreads();
     const int32_t ow = nr * tstride / 4;
@@ -470,10 +481,20 @@ gbt_status sparse_slot_table(gbt_ctx *c, const gbt_matrix *mx, const HistGroup *
         return set_error(GBT_E_INVALID, "slot table stride %d does not fit the page", stride);
     if (n <= 0) return GBT_OK;
     const uint32_t mask = mx->w >= 32 ? 0xffffffffu : ((1u << mx->w) - 1u);
-    const size_t lds = (size_t)kTblThreads * (mx->row_words + 1) * 4;
     const unsigned grid = (unsigned)((n + kTblThreads - 1) / kTblThreads);
-    k_sparse_slot_table<<<grid, kTblThreads, lds, c->stream>>>(page, n, mx->row_words, mx->stride, mx->w, mask,
-                                                               groups_d, G, tbl, stride);
+    const int32_t rw = mx->row_words;
+#define GBT_TBL(MW)                                                                                      \
+    k_sparse_slot_table<MW><<<grid, kTblThreads, 0, c->stream>>>(page, n, rw, mx->stride, mx->w, mask, \
+                                                                 groups_d, G, tbl, stride)
+    if (rw <= 8)
+        GBT_TBL(8);
+    else if (rw <= 16)
+        GBT_TBL(16);
+    else if (rw <= 32)
+        GBT_TBL(32);
+    else
+        GBT_TBL(64);
+#undef GBT_TBL
     GBT_LAUNCHED();
     return GBT_OK;
 }

@@ -74,13 +74,13 @@ struct HistLaunch {
 };
 
 // Bytes per row of a sparse page's slot table for G groups, or 0 when the
-// page does not take one (a row of more than 255 slots, more than 63 groups,
-// or rows too long to stage in LDS).
+// page does not take one (a row of more than 255 slots or 64 words, or more
+// than 63 groups).
 int32_t slot_table_stride(const gbt_matrix *mx, int32_t G);
 // The slot table of rows [0, n) of `page` (a page of mx's geometry) for the
 // groups groups_d[0, G): tbl[r * stride + g] = first slot of row r whose
-// symbol is >= groups_d[g].b0; tbl[r * stride + G] = first slot past the
-// last group.
+// symbol is >= groups_d[g].b0 (g < G), tbl[r * stride + G] = first slot
+// past the last group's bins.  Bytes past G are not written.
 gbt_status sparse_slot_table(gbt_ctx *c, const gbt_matrix *mx, const HistGroup *groups_d, int32_t G,
                              const uint32_t *page, int64_t n, uint8_t *tbl, int32_t stride);
 

@@ -382,10 +382,49 @@ __global__ void __launch_bounds__(256 * kSub)
     if (lane == 0) cand[(int64_t)slot * m + f] = o;
 }
 
-// k_reduce_eval for features of at most 64 bins: one wave per (feature,
-// node), four features per block, each lane one bin; the wave evaluates the
-// built node and then its sibling.
+// Best split of one feature of at most 64 bins for one node, one bin per
+// lane (lanes >= B hold zeros): the same cuts, gains and choice as
+// eval_feature.
+__device__ Cand eval_feature_lanes(long long g, long long h, int32_t B, long long Qg, long long Qh,
+                                   const EvalParams &ep)
+{
+    const int lane = threadIdx.x & 63;
+    Cand best;
+    best.valid = 0;
+    best.gain = 0.0;
+    best.order = 0;
+    best.lg = best.lh = 0;
+    const double G = fx(Qg, ep.e_g), H = fx(Qh, ep.e_h);
+    long long xg = g, xh = h;
+    wave_scan2(xg, xh);
+    const long long mg = Qg - __shfl(xg, 63, 64), mh = Qh - __shfl(xh, 63, 64);
+    const int32_t s = lane + 1;  // left = bins < s
+    if (s <= B - 1) {
+#pragma unroll
+        for (int dir = 0; dir < 2; ++dir) {
+            const long long lg = xg + (dir ? mg : 0), lh = xh + (dir ? mh : 0);
+            const double GL = fx(lg, ep.e_g), HL = fx(lh, ep.e_h);
+            const double GR = fx(Qg - lg, ep.e_g), HR = fx(Qh - lh, ep.e_h);
+            if (!(HL >= ep.mcw && HR >= ep.mcw)) continue;
+            const double gain = eq8_gain(GL, HL, GR, HR, G, H, ep.lambda, ep.gamma);
+            if (gain != gain) continue;
+            Cand c;
+            c.gain = gain;
+            c.order = s * 2 + dir;
+            c.valid = 1;
+            c.lg = lg;
+            c.lh = lh;
+            if (better(c, best)) best = c;
+        }
+    }
+    return wave_best(best);
+}
+
+// k_reduce_eval for features of at most 64 bins: a wave takes four
+// features of one node, a lane one bin of each; the parent's and the
+// partials' loads of all four are in flight together.  No LDS.
 constexpr int kNarrowBins = 64;
+constexpr int kNarrowFeat = 4;  // features per wave
 
 __global__ void __launch_bounds__(256)
     k_reduce_eval_narrow(const longlong2 *__restrict__ partials, const HistReduce *__restrict__ red,
@@ -394,73 +433,97 @@ __global__ void __launch_bounds__(256)
                          int32_t m, const EvalNode *__restrict__ ev, EvalParams ep, EvalCand *__restrict__ cand)
 {
     if (n_red_d && (int32_t)blockIdx.y >= *n_red_d) return;
-    __shared__ longlong2 hb[4][kNarrowBins], hs[4][kNarrowBins];
+    const int lane = threadIdx.x & 63;
+    const int32_t f0 = (int32_t)(blockIdx.x * 4 + (threadIdx.x >> 6)) * kNarrowFeat;
+    if (f0 >= m) return;  // the whole wave; the kernel has no block barrier
     const HistReduce rd = red[blockIdx.y];
-    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-    const int32_t f = blockIdx.x * 4 + wid;
-    const bool live = f < m;
-    const int32_t b0 = live ? bin_ptr[f] : 0, B = live ? bin_ptr[f + 1] - b0 : 0;
     const bool sib = rd.sub_target >= 0;
-    long long g = 0, h = 0, pg = 0, ph = 0;
-    if (lane < B) {
-        const longlong2 *src = partials + (int64_t)rd.part0 * total_bins + b0 + lane;
-        int32_t k = 0;
-        // eight loads in flight per lane
-        for (; k + 7 < rd.nparts; k += 8) {
-            longlong2 v[8];
+    int32_t b0[kNarrowFeat];
+    bool on[kNarrowFeat];
 #pragma unroll
-            for (int j = 0; j < 8; ++j) v[j] = src[(int64_t)(k + j) * total_bins];
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                g += v[j].x;
-                h += v[j].y;
-            }
-        }
-        for (; k < rd.nparts; ++k) {
-            const longlong2 v = src[(int64_t)k * total_bins];
-            g += v.x;
-            h += v.y;
-        }
-        if (sib) {
-            const longlong2 pv = parent[(int64_t)rd.sub_parent * total_bins + b0 + lane];
-            pg = pv.x - g;
-            ph = pv.y - h;
-        }
-        if (hist) {
-            hist[(int64_t)rd.slot * total_bins + b0 + lane] = make_longlong2(g, h);
-            if (sib) hist[(int64_t)rd.sub_target * total_bins + b0 + lane] = make_longlong2(pg, ph);
+    for (int j = 0; j < kNarrowFeat; ++j) {
+        const int32_t f = f0 + j;
+        b0[j] = 0;
+        on[j] = false;
+        if (f < m) {
+            b0[j] = bin_ptr[f];
+            on[j] = lane < bin_ptr[f + 1] - b0[j];
         }
     }
-    hb[wid][lane] = make_longlong2(g, h);
-    hs[wid][lane] = make_longlong2(pg, ph);
-    __syncthreads();
-    if (!live) return;
+    longlong2 pv[kNarrowFeat];
+#pragma unroll
+    for (int j = 0; j < kNarrowFeat; ++j)
+        pv[j] = (sib && on[j]) ? parent[(int64_t)rd.sub_parent * total_bins + b0[j] + lane] : make_longlong2(0, 0);
+    long long g[kNarrowFeat], h[kNarrowFeat];
+#pragma unroll
+    for (int j = 0; j < kNarrowFeat; ++j) g[j] = h[j] = 0;
+    const longlong2 *src = partials + (int64_t)rd.part0 * total_bins + lane;
+    int32_t k = 0;
+    for (; k + 1 < rd.nparts; k += 2) {
+        longlong2 v[2][kNarrowFeat];
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int j = 0; j < kNarrowFeat; ++j)
+                v[u][j] = on[j] ? src[(int64_t)(k + u) * total_bins + b0[j]] : make_longlong2(0, 0);
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int j = 0; j < kNarrowFeat; ++j) {
+                g[j] += v[u][j].x;
+                h[j] += v[u][j].y;
+            }
+    }
+    if (k < rd.nparts) {
+#pragma unroll
+        for (int j = 0; j < kNarrowFeat; ++j) {
+            const longlong2 v = on[j] ? src[(int64_t)k * total_bins + b0[j]] : make_longlong2(0, 0);
+            g[j] += v.x;
+            h[j] += v.y;
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < kNarrowFeat; ++j) {
+        pv[j].x -= g[j];
+        pv[j].y -= h[j];
+        if (hist && on[j]) {
+            hist[(int64_t)rd.slot * total_bins + b0[j] + lane] = make_longlong2(g[j], h[j]);
+            if (sib) hist[(int64_t)rd.sub_target * total_bins + b0[j] + lane] = pv[j];
+        }
+    }
     if (ep.e_dev) {
         ep.e_g = ep.e_dev[0];
         ep.e_h = ep.e_dev[1];
     }
     for (int which = 0; which < (sib ? 2 : 1); ++which) {
         const int32_t slot = which == 0 ? rd.slot : rd.sub_target;
-        EvalCand o;
-        o.valid = 0;
-        o.gain = 0.0;
-        o.feature = f;
-        o.split_bin = -1;
-        o.default_left = 0;
-        o.lg = o.lh = 0;
-        if (B >= 2) {
-            const EvalNode nd = ev[slot];
-            const Cand cb = eval_feature(which == 0 ? hb[wid] : hs[wid], B, nd.sum_g, nd.sum_h, ep);
-            if (cb.valid) {
-                o.valid = 1;
-                o.gain = cb.gain;
-                o.split_bin = cb.order >> 1;
-                o.default_left = cb.order & 1;
-                o.lg = cb.lg;
-                o.lh = cb.lh;
+        const EvalNode nd = ev[slot];
+#pragma unroll
+        for (int j = 0; j < kNarrowFeat; ++j) {
+            const int32_t f = f0 + j;
+            if (f >= m) break;
+            const int32_t B = bin_ptr[f + 1] - b0[j];
+            EvalCand o;
+            o.valid = 0;
+            o.gain = 0.0;
+            o.feature = f;
+            o.split_bin = -1;
+            o.default_left = 0;
+            o.lg = o.lh = 0;
+            if (B >= 2) {
+                const Cand cb = which == 0 ? eval_feature_lanes(g[j], h[j], B, nd.sum_g, nd.sum_h, ep)
+                                           : eval_feature_lanes(pv[j].x, pv[j].y, B, nd.sum_g, nd.sum_h, ep);
+                if (cb.valid) {
+                    o.valid = 1;
+                    o.gain = cb.gain;
+                    o.split_bin = cb.order >> 1;
+                    o.default_left = cb.order & 1;
+                    o.lg = cb.lg;
+                    o.lh = cb.lh;
+                }
             }
+            if (lane == 0) cand[(int64_t)slot * m + f] = o;
         }
-        if (lane == 0) cand[(int64_t)slot * m + f] = o;
     }
 }
 
@@ -526,7 +589,7 @@ gbt_status reduce_eval_impl(gbt_ctx *c, const gbt_matrix *mx, const int64_t *par
     for (int32_t f = 0; f < mx->m; ++f)
         max_feature_bins = std::max(max_feature_bins, mx->bin_ptr_h[f + 1] - mx->bin_ptr_h[f]);
     if (max_feature_bins <= kNarrowBins) {
-        dim3 g4((unsigned)((mx->m + 3) / 4), (unsigned)max_red);
+        dim3 g4((unsigned)((mx->m + 4 * kNarrowFeat - 1) / (4 * kNarrowFeat)), (unsigned)max_red);
         k_reduce_eval_narrow<<<g4, 256, 0, c->stream>>>((const longlong2 *)partials, red, n_red_d,
                                                         (const longlong2 *)parent, (longlong2 *)hist,
                                                         mx->total_bins, mx->bin_ptr_d, mx->m, ev, ep, cand);
