@@ -506,8 +506,9 @@ int orc_gradients(int32_t loss, const float *margin, const float *label, const f
 /*   K   = max(1, rint(f*n))                                                  */
 /*   T*  = least integer T >= 1 with sum_i min(1, a_i/T) <= K, i.e.           */
 /*         F(T) <= (K - C(T)) * T, C(T) = #{a_i >= T}, F(T) = sum_{a_i<T} a_i  */
-/*   keep i iff a_i >= T* or U_i * T* < a_i * 2^64, U_i = first word of       */
-/*         Philox4x64-10(counter = (row, iteration, 0, 0), key = (seed, 0))   */
+/*   keep i iff a_i >= T* or U_i * T* < a_i * 2^64, U_i = word (row mod 4) of */
+/*         Philox4x64-10(counter = (row div 4, iteration, 0, 0),             */
+/*         key = (seed, 0)): one block gives the words of four rows          */
 /*   weight w_i = 1 if a_i >= T*, else T* / a_i (the inverse of the        */
 /*         inclusion probability)                                            */
 /* Rows with a_i = 0 are never kept (only rows with non-zero gradients stay). */
@@ -579,9 +580,9 @@ int64_t orc_mvs_threshold(const int64_t *keys, int64_t n, int64_t K)
 
 uint64_t orc_mvs_uniform(uint64_t seed, uint64_t iteration, uint64_t row)
 {
-    uint64_t ctr[4] = {row, iteration, 0, 0}, key[2] = {seed, 0}, out[4];
+    uint64_t ctr[4] = {row >> 2, iteration, 0, 0}, key[2] = {seed, 0}, out[4];
     orc_philox4x64_10(ctr, key, out);
-    return out[0];
+    return out[row & 3];
 }
 
 /* keep[i] = 1 when row (row_offset + i) is sampled. */

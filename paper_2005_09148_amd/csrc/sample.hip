@@ -102,11 +102,12 @@ __device__ inline void mul_128(uint64_t m, uint64_t x, uint64_t *hi, uint64_t *l
     *lo = (p2 << 32) | (uint32_t)p0;
 }
 
-__device__ inline uint64_t philox_word0(uint64_t c0, uint64_t c1, uint64_t c2, uint64_t c3,
-                                        uint64_t k0, uint64_t k1)
+// The block of counter (c0, c1, 0, 0) and key (k0, 0): its four words.
+__device__ inline void philox_block(uint64_t c0, uint64_t c1, uint64_t k0, uint64_t out[4])
 {
     constexpr uint64_t kMul0 = 0xD2E7470EE14C6C93ull, kMul1 = 0xCA5A826395121157ull;
     constexpr uint64_t kWeyl0 = 0x9E3779B97F4A7C15ull, kWeyl1 = 0xBB67AE8584CAA73Bull;
+    uint64_t c2 = 0, c3 = 0, k1 = 0;
 #pragma unroll
     for (int round = 0; round < 10; ++round) {
         uint64_t p0hi, p0lo, p1hi, p1lo;
@@ -120,7 +121,10 @@ __device__ inline uint64_t philox_word0(uint64_t c0, uint64_t c1, uint64_t c2, u
         k0 += kWeyl0;
         k1 += kWeyl1;
     }
-    return c0;
+    out[0] = c0;
+    out[1] = c1;
+    out[2] = c2;
+    out[3] = c3;
 }
 
 // ------------------------------------------------------------ block reductions
@@ -400,29 +404,76 @@ __global__ void __launch_bounds__(256) k_mvs_select(SampleSrc src, const int64_t
     __shared__ int32_t red4[4];
     const unsigned long long T = (unsigned long long)st->T;
     const int32_t e = st->e_key;
-    const int64_t base = (int64_t)blockIdx.x * kCompactTile + threadIdx.x;
+    const int64_t tbase = (int64_t)blockIdx.x * kCompactTile;
+    // global row r draws word r mod 4 of the Philox block r div 4; when the
+    // offset is a multiple of 4, a thread's four consecutive rows share one
+    // block
+    const bool aligned = (row_offset & 3) == 0;
     int32_t cnt = 0;
-#pragma unroll 4
-    for (int k = 0; k < kCompactTile / 256; ++k) {
-        const int64_t i = base + k * 256;
-        if (i >= n) break;
-        unsigned long long a;
-        if (keys) {
-            a = (unsigned long long)keys[i];
+#pragma unroll 2
+    for (int k = 0; k < kCompactTile / 1024; ++k) {
+        const int64_t i0 = tbase + k * 1024 + 4 * (int64_t)threadIdx.x;
+        if (i0 >= n) break;
+        const bool full = i0 + 4 <= n;
+        unsigned long long a[4];
+        if (keys && full) {
+            const longlong2 x = *(const longlong2 *)(keys + i0), y = *(const longlong2 *)(keys + i0 + 2);
+            a[0] = (unsigned long long)x.x;
+            a[1] = (unsigned long long)x.y;
+            a[2] = (unsigned long long)y.x;
+            a[3] = (unsigned long long)y.y;
         } else {
-            double g, h;
-            row_gh<kSrc>(src, i, &g, &h);
-            a = (unsigned long long)(long long)rint(ldexp(mvs_r(g, h, lambda), e));
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                a[j] = 0;
+                if (i0 + j >= n) continue;
+                if (keys) {
+                    a[j] = (unsigned long long)keys[i0 + j];
+                } else {
+                    double g, h;
+                    row_gh<kSrc>(src, i0 + j, &g, &h);
+                    a[j] = (unsigned long long)(long long)rint(ldexp(mvs_r(g, h, lambda), e));
+                }
+            }
         }
-        bool kp;
-        if (a >= T) {
-            kp = true;
+        bool need = false;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) need |= (i0 + j < n) && a[j] < T;
+        uint64_t U[4] = {0, 0, 0, 0};
+        if (need) {
+            const uint64_t g0 = (uint64_t)(row_offset + i0);
+            uint64_t w[4];
+            philox_block(g0 >> 2, iteration, seed, w);
+            if (aligned) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) U[j] = w[j];
+            } else {
+                uint64_t w2[4];
+                philox_block((g0 >> 2) + 1, iteration, seed, w2);
+                const uint32_t s = (uint32_t)(g0 & 3);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const uint32_t q = s + (uint32_t)j;  // 0..6: word q of the first block, else q - 4 of the next
+                    U[j] = q == 0 ? w[0] : q == 1 ? w[1] : q == 2 ? w[2] : q == 3 ? w[3]
+                         : q == 4 ? w2[0] : q == 5 ? w2[1] : w2[2];
+                }
+            }
+        }
+        uint32_t kb = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            if (i0 + j >= n) continue;
+            const bool kp = a[j] >= T || __umul64hi(U[j], T) < a[j];
+            kb |= (kp ? 1u : 0u) << (8 * j);
+            cnt += kp ? 1 : 0;
+        }
+        if (full) {
+            *(uint32_t *)(keep + i0) = kb;
         } else {
-            const uint64_t U = philox_word0((uint64_t)(row_offset + i), iteration, 0, 0, seed, 0);
-            kp = __umul64hi(U, T) < a;
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (i0 + j < n) keep[i0 + j] = (uint8_t)((kb >> (8 * j)) & 1u);
         }
-        keep[i] = kp ? 1 : 0;
-        cnt += kp ? 1 : 0;
     }
     for (int d = 32; d > 0; d >>= 1) cnt += __shfl_xor(cnt, d, 64);
     if ((threadIdx.x & 63) == 0) red4[threadIdx.x >> 6] = cnt;

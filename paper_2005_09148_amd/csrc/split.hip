@@ -382,11 +382,12 @@ __global__ void __launch_bounds__(256 * kSub)
     if (lane == 0) cand[(int64_t)slot * m + f] = o;
 }
 
-// Best split of one feature of at most 64 bins for one node, one bin per
-// lane (lanes >= B hold zeros): the same cuts, gains and choice as
-// eval_feature.
-__device__ Cand eval_feature_lanes(long long g, long long h, int32_t B, long long Qg, long long Qh,
-                                   const EvalParams &ep)
+// Best split of one feature of at most 64 kBL bins for one node, held in
+// registers: lane l's t-th value is bin t * 64 + l (zeros past B).  The same
+// cuts, gains and choice as eval_feature.
+template <int kBL>
+__device__ Cand eval_feature_regs(const long long *g, const long long *h, int32_t B, long long Qg, long long Qh,
+                                  const EvalParams &ep)
 {
     const int lane = threadIdx.x & 63;
     Cand best;
@@ -395,14 +396,26 @@ __device__ Cand eval_feature_lanes(long long g, long long h, int32_t B, long lon
     best.order = 0;
     best.lg = best.lh = 0;
     const double G = fx(Qg, ep.e_g), H = fx(Qh, ep.e_h);
-    long long xg = g, xh = h;
-    wave_scan2(xg, xh);
-    const long long mg = Qg - __shfl(xg, 63, 64), mh = Qh - __shfl(xh, 63, 64);
-    const int32_t s = lane + 1;  // left = bins < s
-    if (s <= B - 1) {
+    long long tg = 0, th = 0;
+#pragma unroll
+    for (int t = 0; t < kBL; ++t) {
+        tg += g[t];
+        th += h[t];
+    }
+    const long long mg = Qg - wave_sum(tg), mh = Qh - wave_sum(th);
+    long long cg = 0, ch = 0;  // sums of the chunks before chunk t
+#pragma unroll
+    for (int t = 0; t < kBL; ++t) {
+        long long xg = g[t], xh = h[t];
+        wave_scan2(xg, xh);
+        const long long pg = cg + xg, ph = ch + xh;
+        cg += __shfl(xg, 63, 64);
+        ch += __shfl(xh, 63, 64);
+        const int32_t s = t * 64 + lane + 1;  // left = bins < s
+        if (s > B - 1) continue;
 #pragma unroll
         for (int dir = 0; dir < 2; ++dir) {
-            const long long lg = xg + (dir ? mg : 0), lh = xh + (dir ? mh : 0);
+            const long long lg = pg + (dir ? mg : 0), lh = ph + (dir ? mh : 0);
             const double GL = fx(lg, ep.e_g), HL = fx(lh, ep.e_h);
             const double GR = fx(Qg - lg, ep.e_g), HR = fx(Qh - lh, ep.e_h);
             if (!(HL >= ep.mcw && HR >= ep.mcw)) continue;
@@ -420,75 +433,77 @@ __device__ Cand eval_feature_lanes(long long g, long long h, int32_t B, long lon
     return wave_best(best);
 }
 
-// k_reduce_eval for features of at most 64 bins: a wave takes four
-// features of one node, a lane one bin of each; the parent's and the
-// partials' loads of all four are in flight together.  No LDS.
-constexpr int kNarrowBins = 64;
-constexpr int kNarrowFeat = 4;  // features per wave
-
+// k_reduce_eval with the histograms in registers: a wave takes 4 / kBL
+// features of one node (features of at most 64 kBL bins), lane l bins
+// l, l + 64, ...; the parent's and the partials' loads of all of them are
+// in flight together.  No LDS and no block barrier.
+template <int kBL>
 __global__ void __launch_bounds__(256)
-    k_reduce_eval_narrow(const longlong2 *__restrict__ partials, const HistReduce *__restrict__ red,
-                         const int32_t *__restrict__ n_red_d, const longlong2 *__restrict__ parent,
-                         longlong2 *__restrict__ hist, int64_t total_bins, const int32_t *__restrict__ bin_ptr,
-                         int32_t m, const EvalNode *__restrict__ ev, EvalParams ep, EvalCand *__restrict__ cand)
+    k_reduce_eval_regs(const longlong2 *__restrict__ partials, const HistReduce *__restrict__ red,
+                       const int32_t *__restrict__ n_red_d, const longlong2 *__restrict__ parent,
+                       longlong2 *__restrict__ hist, int64_t total_bins, const int32_t *__restrict__ bin_ptr,
+                       int32_t m, const EvalNode *__restrict__ ev, EvalParams ep, EvalCand *__restrict__ cand)
 {
+    constexpr int kFW = 4 / kBL;  // features per wave
+    constexpr int kV = kFW * kBL; // values per lane
     if (n_red_d && (int32_t)blockIdx.y >= *n_red_d) return;
     const int lane = threadIdx.x & 63;
-    const int32_t f0 = (int32_t)(blockIdx.x * 4 + (threadIdx.x >> 6)) * kNarrowFeat;
-    if (f0 >= m) return;  // the whole wave; the kernel has no block barrier
+    const int32_t f0 = (int32_t)(blockIdx.x * 4 + (threadIdx.x >> 6)) * kFW;
+    if (f0 >= m) return;  // the whole wave
     const HistReduce rd = red[blockIdx.y];
     const bool sib = rd.sub_target >= 0;
-    int32_t b0[kNarrowFeat];
-    bool on[kNarrowFeat];
+    int32_t off[kV];  // bin offset of each value, -1 past its feature's bins
 #pragma unroll
-    for (int j = 0; j < kNarrowFeat; ++j) {
+    for (int j = 0; j < kFW; ++j) {
         const int32_t f = f0 + j;
-        b0[j] = 0;
-        on[j] = false;
+        int32_t b0 = 0, B = 0;
         if (f < m) {
-            b0[j] = bin_ptr[f];
-            on[j] = lane < bin_ptr[f + 1] - b0[j];
+            b0 = bin_ptr[f];
+            B = bin_ptr[f + 1] - b0;
         }
+#pragma unroll
+        for (int t = 0; t < kBL; ++t) off[j * kBL + t] = t * 64 + lane < B ? b0 + t * 64 + lane : -1;
     }
-    longlong2 pv[kNarrowFeat];
+    longlong2 pv[kV];
 #pragma unroll
-    for (int j = 0; j < kNarrowFeat; ++j)
-        pv[j] = (sib && on[j]) ? parent[(int64_t)rd.sub_parent * total_bins + b0[j] + lane] : make_longlong2(0, 0);
-    long long g[kNarrowFeat], h[kNarrowFeat];
+    for (int i = 0; i < kV; ++i)
+        pv[i] = (sib && off[i] >= 0) ? parent[(int64_t)rd.sub_parent * total_bins + off[i]] : make_longlong2(0, 0);
+    long long g[kV], h[kV];
 #pragma unroll
-    for (int j = 0; j < kNarrowFeat; ++j) g[j] = h[j] = 0;
-    const longlong2 *src = partials + (int64_t)rd.part0 * total_bins + lane;
+    for (int i = 0; i < kV; ++i) g[i] = h[i] = 0;
+    const longlong2 *src = partials + (int64_t)rd.part0 * total_bins;
     int32_t k = 0;
     for (; k + 1 < rd.nparts; k += 2) {
-        longlong2 v[2][kNarrowFeat];
+        longlong2 v[2][kV];
 #pragma unroll
         for (int u = 0; u < 2; ++u)
 #pragma unroll
-            for (int j = 0; j < kNarrowFeat; ++j)
-                v[u][j] = on[j] ? src[(int64_t)(k + u) * total_bins + b0[j]] : make_longlong2(0, 0);
+            for (int i = 0; i < kV; ++i)
+                v[u][i] = off[i] >= 0 ? src[(int64_t)(k + u) * total_bins + off[i]] : make_longlong2(0, 0);
 #pragma unroll
         for (int u = 0; u < 2; ++u)
 #pragma unroll
-            for (int j = 0; j < kNarrowFeat; ++j) {
-                g[j] += v[u][j].x;
-                h[j] += v[u][j].y;
+            for (int i = 0; i < kV; ++i) {
+                g[i] += v[u][i].x;
+                h[i] += v[u][i].y;
             }
     }
     if (k < rd.nparts) {
 #pragma unroll
-        for (int j = 0; j < kNarrowFeat; ++j) {
-            const longlong2 v = on[j] ? src[(int64_t)k * total_bins + b0[j]] : make_longlong2(0, 0);
-            g[j] += v.x;
-            h[j] += v.y;
+        for (int i = 0; i < kV; ++i) {
+            const longlong2 v = off[i] >= 0 ? src[(int64_t)k * total_bins + off[i]] : make_longlong2(0, 0);
+            g[i] += v.x;
+            h[i] += v.y;
         }
     }
+    long long sg[kV], sh[kV];
 #pragma unroll
-    for (int j = 0; j < kNarrowFeat; ++j) {
-        pv[j].x -= g[j];
-        pv[j].y -= h[j];
-        if (hist && on[j]) {
-            hist[(int64_t)rd.slot * total_bins + b0[j] + lane] = make_longlong2(g[j], h[j]);
-            if (sib) hist[(int64_t)rd.sub_target * total_bins + b0[j] + lane] = pv[j];
+    for (int i = 0; i < kV; ++i) {
+        sg[i] = pv[i].x - g[i];
+        sh[i] = pv[i].y - h[i];
+        if (hist && off[i] >= 0) {
+            hist[(int64_t)rd.slot * total_bins + off[i]] = make_longlong2(g[i], h[i]);
+            if (sib) hist[(int64_t)rd.sub_target * total_bins + off[i]] = make_longlong2(sg[i], sh[i]);
         }
     }
     if (ep.e_dev) {
@@ -499,10 +514,10 @@ __global__ void __launch_bounds__(256)
         const int32_t slot = which == 0 ? rd.slot : rd.sub_target;
         const EvalNode nd = ev[slot];
 #pragma unroll
-        for (int j = 0; j < kNarrowFeat; ++j) {
+        for (int j = 0; j < kFW; ++j) {
             const int32_t f = f0 + j;
             if (f >= m) break;
-            const int32_t B = bin_ptr[f + 1] - b0[j];
+            const int32_t B = bin_ptr[f + 1] - bin_ptr[f];
             EvalCand o;
             o.valid = 0;
             o.gain = 0.0;
@@ -511,8 +526,8 @@ __global__ void __launch_bounds__(256)
             o.default_left = 0;
             o.lg = o.lh = 0;
             if (B >= 2) {
-                const Cand cb = which == 0 ? eval_feature_lanes(g[j], h[j], B, nd.sum_g, nd.sum_h, ep)
-                                           : eval_feature_lanes(pv[j].x, pv[j].y, B, nd.sum_g, nd.sum_h, ep);
+                const Cand cb = which == 0 ? eval_feature_regs<kBL>(g + j * kBL, h + j * kBL, B, nd.sum_g, nd.sum_h, ep)
+                                           : eval_feature_regs<kBL>(sg + j * kBL, sh + j * kBL, B, nd.sum_g, nd.sum_h, ep);
                 if (cb.valid) {
                     o.valid = 1;
                     o.gain = cb.gain;
@@ -588,11 +603,23 @@ gbt_status reduce_eval_impl(gbt_ctx *c, const gbt_matrix *mx, const int64_t *par
     int32_t max_feature_bins = 0;
     for (int32_t f = 0; f < mx->m; ++f)
         max_feature_bins = std::max(max_feature_bins, mx->bin_ptr_h[f + 1] - mx->bin_ptr_h[f]);
-    if (max_feature_bins <= kNarrowBins) {
-        dim3 g4((unsigned)((mx->m + 4 * kNarrowFeat - 1) / (4 * kNarrowFeat)), (unsigned)max_red);
-        k_reduce_eval_narrow<<<g4, 256, 0, c->stream>>>((const longlong2 *)partials, red, n_red_d,
-                                                        (const longlong2 *)parent, (longlong2 *)hist,
-                                                        mx->total_bins, mx->bin_ptr_d, mx->m, ev, ep, cand);
+    // features of at most 64 bins, or many (feature, node) pairs: the
+    // register form (a wave per 1, 2 or 4 features)
+    const int kbl = max_feature_bins <= 64 ? 1 : max_feature_bins <= 128 ? 2 : max_feature_bins <= 256 ? 4 : 0;
+    if (kbl == 1 || (kbl > 0 && (int64_t)max_red * mx->m >= 2 * kCUs)) {
+        const int fpb = 4 * (4 / kbl);  // features per block
+        dim3 gr((unsigned)((mx->m + fpb - 1) / fpb), (unsigned)max_red);
+#define GBT_REG_EVAL(BL)                                                                                       \
+    k_reduce_eval_regs<BL><<<gr, 256, 0, c->stream>>>((const longlong2 *)partials, red, n_red_d,           \
+                                                      (const longlong2 *)parent, (longlong2 *)hist,         \
+                                                      mx->total_bins, mx->bin_ptr_d, mx->m, ev, ep, cand)
+        if (kbl == 1)
+            GBT_REG_EVAL(1);
+        else if (kbl == 2)
+            GBT_REG_EVAL(2);
+        else
+            GBT_REG_EVAL(4);
+#undef GBT_REG_EVAL
         GBT_LAUNCHED();
         return GBT_OK;
     }

@@ -458,6 +458,16 @@ def test_empty_sample_tree(gbt, ctx, hist_kernel):
     assert trees[0].nodes["flags"][0] & orc.NODE_LEAF
 
 
+@pytest.mark.parametrize("max_bin,m", [(100, 40), (128, 130), (20, 300)])
+def test_trees_feature_widths(gbt, ctx, max_bin, m):
+    # deep levels evaluate many (feature, node) pairs: features of at most
+    # 64, 128 and 256 bins take one, two and four bins per lane
+    cfg = datagen.TrainConfig("t", 1, max_bin, 7, 2, eta=0.3, gamma=0.5)
+    d = datagen.config3(n=12_000, m=m)
+    r = train_both(gbt, ctx, d["X"], d["y"], cfg, 2)
+    assert_same_trees(*r[:4])
+
+
 @pytest.mark.parametrize("depth,n", [(0, 1000), (1, 65), (3, 1), (4, 63)])
 def test_degenerate_trees(gbt, ctx, hist_kernel, depth, n):
     cfg = datagen.TrainConfig("t", 1, 32, depth, 2, eta=0.5, f=0.5 if n > 10 else 1.0)

@@ -50,15 +50,25 @@ def test_equal_keys_reduce_to_uniform_sampling(orc):
     assert Fraction(12345, T) == Fraction(K, n)
 
 
-def test_selection_uses_philox_first_word(orc):
+def numpy_philox_block(block, it, seed):
+    # numpy's Philox increments its 256-bit counter (little-endian words)
+    # before producing a block: start from (block, it, 0, 0) - 1
+    c = (block + (it << 64)) - 1
+    ctr = np.array([c & (2**64 - 1), c >> 64, 0, 0], np.uint64)
+    return np.random.Philox(counter=ctr, key=np.array([seed, 0], np.uint64)).random_raw(4)
+
+
+@pytest.mark.parametrize("off", [1000, 1001, 2])
+def test_selection_uses_philox_words(orc, off):
+    # row r draws word r mod 4 of the Philox block r div 4
     rng = np.random.default_rng(2)
     keys = rng.integers(0, 1000, 500).astype(np.int64)
-    T, seed, it, off = 700, 17, 3, 1000
+    T, seed, it = 700, 17, 3
     keep = orc.mvs_select(keys, T, seed, it, off)
     for i in range(500):
         row = off + i
-        U = int(np.random.Philox(counter=np.array([row - 1, it, 0, 0], np.uint64),
-                                 key=np.array([seed, 0], np.uint64)).random_raw(1)[0])
+        U = int(numpy_philox_block(row // 4, it, seed)[row % 4])
+        assert orc.mvs_uniform(seed, it, row) == U
         want = keys[i] >= T or U * T < int(keys[i]) * 2**64
         assert keep[i] == want
 
