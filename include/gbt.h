@@ -282,8 +282,8 @@ gbt_status gbt_gradients(gbt_ctx *ctx, int32_t loss, const float *margin_d, cons
  *   a_i = rint(r_i 2^e), e = 62 - E - ceil(log2 n), max r < 2^E
  *   K = max(1, rint(f n)); T* = least T >= 1 with
  *       sum_{a_i<T} a_i <= (K - #{a_i >= T}) T
- *   keep iff a_i >= T* or hi64(U_i T*) < a_i, U_i = word 0 of
- *       Philox4x64-10(counter (i, iteration, 0, 0), key (seed, 0))
+ *   keep iff a_i >= T* or hi64(U_i T*) < a_i, U_i = word (i mod 4) of
+ *       Philox4x64-10(counter (i div 4, iteration, 0, 0), key (seed, 0))
  *   w_i = 1 if a_i >= T* else T* / a_i;  (g', h') = (g w_i, h w_i)
  *   q = rint((g', h') 2^(e_g, e_h)), e = 62 - E - ceil(log2 R)
  * gpair_d (n pairs) may be NULL for pinned-host data: gradients are then
