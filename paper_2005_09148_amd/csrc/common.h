@@ -99,6 +99,9 @@ gbt_status dev_alloc(gbt_ctx *c, size_t bytes, void **p);
 void dev_free(gbt_ctx *c, void *p, size_t bytes);
 // Grow-only workspace in slot `slot` of the context.
 gbt_status scratch(gbt_ctx *c, int slot, size_t bytes, void **p);
+// Whether scratch(c, slot, bytes) stays within the context's byte budget
+// (for optional workspaces that are skipped when it would not).
+bool scratch_fits(const gbt_ctx *c, int slot, size_t bytes);
 // Grow-only pinned host buffer that kernels write into: *host for the host,
 // *dev for kernels.  The stream must not be using it (the call syncs
 // before growing).
@@ -135,6 +138,7 @@ enum ScratchSlot {
     kScrPlan,        // device-side level plans (lists, work items, counts)
     kScrPartialsDev, // partial histograms of the device-planned levels
     kScrSlotTbl,     // slot table of a sparse training page
+    kScrCols,        // column copy of a dense training page
     kScrCount
 };
 

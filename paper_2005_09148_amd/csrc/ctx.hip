@@ -95,6 +95,14 @@ gbt_status scratch(gbt_ctx *c, int slot, size_t bytes, void **p)
     return GBT_OK;
 }
 
+bool scratch_fits(const gbt_ctx *c, int slot, size_t bytes)
+{
+    const size_t have = slot < (int)c->scratch.size() ? c->scratch[slot].bytes : 0;
+    if (have >= bytes || !c->budget) return true;
+    const size_t want = bytes + bytes / 8 + 4096;
+    return c->used - have + want <= c->budget;
+}
+
 static int next_event(gbt_ctx *c)
 {
     if (c->events_used == (int)c->events.size()) {

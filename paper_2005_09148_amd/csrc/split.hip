@@ -775,7 +775,8 @@ __global__ void __launch_bounds__(kPartThreads)
     k_part_flags_tiles(const int32_t *__restrict__ rows, int64_t n, const uint32_t *__restrict__ page, Geo geo,
                        const int32_t *__restrict__ position, const int32_t *__restrict__ slot_node,
                        DevNode *__restrict__ nodes, uint8_t *__restrict__ flags,
-                       int32_t *__restrict__ tile_cnt, LevelChoice lc, SlotTable stbl)
+                       int32_t *__restrict__ tile_cnt, LevelChoice lc, SlotTable stbl,
+                       const uint16_t *__restrict__ cols)
 {
     __shared__ int32_t red[kPartThreads / 64];
     const int64_t i0 = (int64_t)blockIdx.x * kPartTile + (int64_t)threadIdx.x * kPartItems;
@@ -820,9 +821,15 @@ __global__ void __launch_bounds__(kPartThreads)
         uint32_t f = 0;
         if (rec[k].x) {
             const uint32_t *row = page + (int64_t)r[k] * geo.row_words;
-            const int32_t b = stbl.slot ? row_feature_bin_tbl(row, stbl.slot + (int64_t)r[k] * stbl.stride, geo,
-                                                              stbl.feat_grp, rec[k].y)
-                                        : row_feature_bin(row, geo, rec[k].y);
+            int32_t b;
+            if (cols) {
+                const uint32_t s = cols[(int64_t)rec[k].y * n + r[k]];
+                b = s == geo.null_sym ? -1 : (int32_t)s;
+            } else {
+                b = stbl.slot ? row_feature_bin_tbl(row, stbl.slot + (int64_t)r[k] * stbl.stride, geo,
+                                                    stbl.feat_grp, rec[k].y)
+                              : row_feature_bin(row, geo, rec[k].y);
+            }
             f = (b < 0) ? (rec[k].w != 0 ? 1u : 0u) : (b < rec[k].z ? 1u : 0u);
         }
         f4 |= f << (8 * k);
@@ -1069,9 +1076,66 @@ __global__ void __launch_bounds__(kPartThreads)
     }
 }
 
+// Column copy of a dense page: cols[f * n + r] = symbol of feature f in row
+// r.  A block stages 256 consecutive rows in LDS (an odd pitch keeps the
+// threads' reads on distinct banks) and writes each feature's 256 symbols
+// with consecutive 2-byte stores.
+constexpr int kColRows = 256;
+
+__global__ void __launch_bounds__(kColRows)
+    k_page_columns(const uint32_t *__restrict__ page, int64_t n, int32_t row_words, int32_t m, int32_t w,
+                   uint32_t mask, uint16_t *__restrict__ cols)
+{
+    extern __shared__ uint32_t rows_l[];  // kColRows x (row_words | 1)
+    const int64_t r0 = (int64_t)blockIdx.x * kColRows;
+    const int32_t nr = (int32_t)min<int64_t>(kColRows, n - r0);
+    const int32_t nw = nr * row_words, lw = row_words | 1;
+    const uint32_t *src = page + r0 * row_words;
+    for (int32_t k0 = 0; k0 < nw; k0 += kColRows * 8) {
+        uint32_t v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int32_t k = k0 + j * kColRows + (int32_t)threadIdx.x;
+            v[j] = k < nw ? src[k] : 0u;
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int32_t k = k0 + j * kColRows + (int32_t)threadIdx.x;
+            if (k < nw) {
+                const int32_t rr = k / row_words;
+                rows_l[rr * lw + (k - rr * row_words)] = v[j];
+            }
+        }
+    }
+    __syncthreads();
+    if ((int32_t)threadIdx.x >= nr) return;
+    const uint32_t *row = rows_l + threadIdx.x * lw;
+    uint16_t *dst = cols + r0 + threadIdx.x;
+    for (int32_t f = 0; f < m; ++f) {
+        const uint32_t bit = (uint32_t)f * (uint32_t)w, k = bit >> 5;
+        const uint32_t hi = k + 1 < (uint32_t)row_words ? row[k + 1] : 0u;
+        dst[(int64_t)f * n] = (uint16_t)(__builtin_amdgcn_alignbit(hi, row[k], bit & 31u) & mask);
+    }
+}
+
+bool split_columns_fit(const gbt_matrix *mx) { return !mx->sparse && mx->w <= 16 && mx->row_words <= 64; }
+
+gbt_status split_columns(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, int64_t n, uint16_t *cols)
+{
+    GBT_CHECK(split_columns_fit(mx), "column copy of a page with %d-bit symbols", mx->w);
+    if (n <= 0) return GBT_OK;
+    const uint32_t mask = mx->w >= 32 ? 0xffffffffu : ((1u << mx->w) - 1u);
+    const size_t lds = (size_t)kColRows * (mx->row_words | 1) * 4;
+    k_page_columns<<<(unsigned)((n + kColRows - 1) / kColRows), kColRows, lds, c->stream>>>(
+        page, n, mx->row_words, mx->m, mx->w, mask, cols);
+    GBT_LAUNCHED();
+    return GBT_OK;
+}
+
 gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int32_t *rows,
                               int64_t n, const int32_t *slot_node, int32_t *slot_node_out, DevNode *nodes,
-                              int32_t *rows_out, const LevelChoice *choice, const SlotTable *stbl)
+                              int32_t *rows_out, const LevelChoice *choice, const SlotTable *stbl,
+                              const uint16_t *cols)
 {
     if (n == 0) return GBT_OK;
     const SlotTable st = stbl ? *stbl : SlotTable{nullptr, nullptr, 0, 0};
@@ -1083,10 +1147,10 @@ gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
     GBT_TRY(scratch_t(c, kScrScan, (size_t)tiles + 1, &tile_cnt));
     if (choice)
         k_part_flags_tiles<true><<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(
-            rows, n, page, geo_of(mx), nullptr, slot_node, nodes, flags, tile_cnt, *choice, st);
+            rows, n, page, geo_of(mx), nullptr, slot_node, nodes, flags, tile_cnt, *choice, st, cols);
     else
         k_part_flags_tiles<false><<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(
-            rows, n, page, geo_of(mx), nullptr, slot_node, nodes, flags, tile_cnt, LevelChoice{}, st);
+            rows, n, page, geo_of(mx), nullptr, slot_node, nodes, flags, tile_cnt, LevelChoice{}, st, cols);
     GBT_LAUNCHED();
     k_part_scatter_rev<<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(rows, n, flags, tile_cnt, slot_node,
                                                                        slot_node_out, nodes, rows_out);
@@ -1111,7 +1175,7 @@ gbt_status partition_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page
     // sum the counts before their tiles themselves
     k_part_flags_tiles<false><<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(rows, n, page, geo, position, slot_node,
                                                                        nodes, flags, tile_off, LevelChoice{},
-                                                                       SlotTable{nullptr, nullptr, 0, 0});
+                                                                       SlotTable{nullptr, nullptr, 0, 0}, nullptr);
     GBT_LAUNCHED();
     if (n_list > 0) {
         k_part_bounds<<<(unsigned)n_list, kBoundThreads, 0, c->stream>>>(list, n_list_d, n_list, nodes, flags,

@@ -81,10 +81,20 @@ struct LevelChoice {
 // records of the level's nodes are chosen from the candidates and written
 // by the first kernel (instead of by eval_reduce_impl).  With `stbl` (a
 // sparse page's slot table), the search for a row's split feature looks
-// only among the slots of the feature's group.
+// only among the slots of the feature's group.  With `cols` (the page's
+// column copy, split_columns), a row's split-feature symbol is read from
+// its feature's column: the rows of a node ascend (or descend) along its
+// segment, so a column's lines serve many of them.
 gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int32_t *rows,
                               int64_t n, const int32_t *slot_node, int32_t *slot_node_out, DevNode *nodes,
                               int32_t *rows_out, const LevelChoice *choice = nullptr,
-                              const SlotTable *stbl = nullptr);
+                              const SlotTable *stbl = nullptr, const uint16_t *cols = nullptr);
+
+// Whether a page of mx's geometry takes a column copy (dense, symbols of at
+// most 16 bits).
+bool split_columns_fit(const gbt_matrix *mx);
+// cols[f * n + r] = symbol of feature f in row r of `page` (n rows of mx's
+// geometry); cols holds m * n entries.
+gbt_status split_columns(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, int64_t n, uint16_t *cols);
 
 }  // namespace gbt

@@ -942,6 +942,16 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         GBT_TRY(sparse_slot_table(c, mx, groups_d, G, so.page, R, tb, tstride));
         stbl = SlotTable{tb, (const uint8_t *)mx->groups_d + fg_off, tstride, 0};
     }
+    // dense pages: the partition reads each row's split symbol from a column
+    // copy of the training page, made once per tree
+    const uint16_t *cols = nullptr;
+    if (D >= 2 && R > 0 && split_columns_fit(mx) &&
+        scratch_fits(c, kScrCols, (size_t)mx->m * (size_t)R * sizeof(uint16_t))) {
+        uint16_t *cd;
+        GBT_TRY(scratch_t(c, kScrCols, (size_t)mx->m * (size_t)R, &cd));
+        GBT_TRY(split_columns(c, mx, so.page, R, cd));
+        cols = cd;
+    }
     int64_t *partials = nullptr;
     GBT_TRY(scratch(c, kScrPartialsDev, (size_t)std::max(max_items, 1) * mx->total_bins * 16, (void **)&partials));
     const int64_t n_init = std::max<int64_t>({(int64_t)NN, (int64_t)n_root, R, (int64_t)kUpdCounters});
@@ -981,7 +991,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         if (!fused && R > 0) GBT_TRY(eval_impl(c, mx, histA, evA, maxn, ep, splits_d, cntA, nodes));
         const LevelChoice lc{cand, mx->m, (int32_t)((1u << d) - 1), (int32_t)((2u << d) - 1)};
         GBT_TRY(partition_rev_impl(c, mx, so.page, rows, R, slot_node, slot_tmp, nodes, rows_tmp,
-                                   choose ? &lc : nullptr, stbl.slot ? &stbl : nullptr));
+                                   choose ? &lc : nullptr, stbl.slot ? &stbl : nullptr, cols));
         std::swap(rows, rows_tmp);
         std::swap(slot_node, slot_tmp);
         const bool plan_next = d + 1 < D && R > 0;
