@@ -5,6 +5,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cstdarg>
 #include <cstdint>
 #include <cstdio>
@@ -84,6 +85,12 @@ struct gbt_ctx {
     void *hio = nullptr;
     void *hio_d = nullptr;
     size_t hio_bytes = 0;
+    // what the column-copy workspace holds: a matrix's own device page
+    // (kept across trees, since such a page does not change)
+    uint64_t cols_uid = 0;
+    const void *cols_page = nullptr;
+    const void *cols_at = nullptr;
+    int64_t cols_rows = 0;
 };
 
 namespace gbt {
@@ -158,8 +165,16 @@ struct GbtPage {
     bool host = false;
 };
 
+// A process-unique id per matrix (never reused, unlike an address).
+inline uint64_t next_matrix_uid()
+{
+    static std::atomic<uint64_t> n{0};
+    return ++n;
+}
+
 struct gbt_matrix {
     gbt_ctx *ctx = nullptr;
+    uint64_t uid = next_matrix_uid();
     int64_t n_rows = 0;
     int32_t m = 0;
     int32_t sparse = 0;

@@ -943,13 +943,25 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         stbl = SlotTable{tb, (const uint8_t *)mx->groups_d + fg_off, tstride, 0};
     }
     // dense pages: the partition reads each row's split symbol from a column
-    // copy of the training page, made once per tree
+    // copy of the training page, made once per tree (once per matrix when
+    // the training page is the matrix's own device page)
     const uint16_t *cols = nullptr;
     if (D >= 2 && R > 0 && split_columns_fit(mx) &&
         scratch_fits(c, kScrCols, (size_t)mx->m * (size_t)R * sizeof(uint16_t))) {
         uint16_t *cd;
         GBT_TRY(scratch_t(c, kScrCols, (size_t)mx->m * (size_t)R, &cd));
-        GBT_TRY(split_columns(c, mx, so.page, R, cd));
+        const bool kept = so.alias && c->cols_uid == mx->uid && c->cols_page == so.page && c->cols_at == cd &&
+                          c->cols_rows == R;
+        if (!kept) {
+            c->cols_uid = 0;
+            GBT_TRY(split_columns(c, mx, so.page, R, cd));
+            if (so.alias) {
+                c->cols_uid = mx->uid;
+                c->cols_page = so.page;
+                c->cols_at = cd;
+                c->cols_rows = R;
+            }
+        }
         cols = cd;
     }
     int64_t *partials = nullptr;
