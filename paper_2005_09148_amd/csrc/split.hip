@@ -978,9 +978,9 @@ __global__ void __launch_bounds__(kPartThreads)
 // of rows within a node enters no result.
 __global__ void __launch_bounds__(kPartThreads)
     k_part_scatter_rev(const int32_t *__restrict__ rows, int64_t n, const uint8_t *__restrict__ flags,
-                       const int32_t *__restrict__ tile_cnt, const int32_t *__restrict__ slot_node,
-                       int32_t *__restrict__ slot_node_out, DevNode *__restrict__ nodes,
-                       int32_t *__restrict__ rows_out)
+                       const int32_t *__restrict__ tile_cnt, const long long *__restrict__ tile_off,
+                       const int32_t *__restrict__ slot_node, int32_t *__restrict__ slot_node_out,
+                       DevNode *__restrict__ nodes, int32_t *__restrict__ rows_out)
 {
     __shared__ int32_t lds16[kPartThreads / 64];
     __shared__ long long s_red[2][kPartThreads / 64];
@@ -1007,10 +1007,18 @@ __global__ void __launch_bounds__(kPartThreads)
     // left flags before this tile and before b0: tile counts, plus the
     // flags of tile tb before b0
     long long before = 0, before_b = 0;
-    for (int64_t k = threadIdx.x; k < (int64_t)blockIdx.x; k += kPartThreads) {
-        const int32_t v = tile_cnt[k];
-        before += v;
-        before_b += k < tb ? v : 0;
+    if (tile_off) {
+        // exclusive tile offsets: the first wave's first lane takes both
+        if (threadIdx.x == 0) {
+            before = tile_off[blockIdx.x];
+            before_b = tile_off[tb];
+        }
+    } else {
+        for (int64_t k = threadIdx.x; k < (int64_t)blockIdx.x; k += kPartThreads) {
+            const int32_t v = tile_cnt[k];
+            before += v;
+            before_b += k < tb ? v : 0;
+        }
     }
     if (ext) {
         const int64_t j = tb * kPartTile + (int64_t)threadIdx.x * kPartItems;
@@ -1073,6 +1081,56 @@ __global__ void __launch_bounds__(kPartThreads)
             slot_node_out[dest] = child;
         }
         P += f;
+    }
+}
+
+// Exclusive offsets of the partition's tile counts, by one block: each
+// thread sums a contiguous run of counts, the block scans the run totals,
+// and each thread writes its run's offsets.
+constexpr int kTileScanThreads = 1024;
+constexpr int64_t kScanTilesAbove = 2048;
+
+__global__ void __launch_bounds__(kTileScanThreads)
+    k_tile_offsets(const int32_t *__restrict__ cnt, int64_t tiles, long long *__restrict__ off)
+{
+    __shared__ long long s_w[kTileScanThreads / 64];
+    const int64_t per = (tiles + kTileScanThreads - 1) / kTileScanThreads;
+    const int64_t a = min<int64_t>(tiles, (int64_t)threadIdx.x * per), b = min<int64_t>(tiles, a + per);
+    constexpr int kHeld = 16;  // runs this short are loaded at once (all loads in flight)
+    int32_t v[kHeld];
+    long long run = 0;
+    if (per <= kHeld) {
+#pragma unroll
+        for (int j = 0; j < kHeld; ++j) v[j] = a + j < b ? cnt[a + j] : 0;
+#pragma unroll
+        for (int j = 0; j < kHeld; ++j) run += v[j];
+    } else {
+        for (int64_t k = a; k < b; ++k) run += cnt[k];
+    }
+    // inclusive scan of the run totals: within the wave, then over waves
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    long long x = run;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const long long y = __shfl_up(x, d, 64);
+        if (lane >= d) x += y;
+    }
+    if (lane == 63) s_w[wid] = x;
+    __syncthreads();
+    long long base = x - run;
+    for (int w = 0; w < wid; ++w) base += s_w[w];
+    if (per <= kHeld) {
+#pragma unroll
+        for (int j = 0; j < kHeld; ++j)
+            if (a + j < b) {
+                off[a + j] = base;
+                base += v[j];
+            }
+    } else {
+        for (int64_t k = a; k < b; ++k) {
+            off[k] = base;
+            base += cnt[k];
+        }
     }
 }
 
@@ -1152,8 +1210,16 @@ gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
         k_part_flags_tiles<false><<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(
             rows, n, page, geo_of(mx), nullptr, slot_node, nodes, flags, tile_cnt, LevelChoice{}, st, cols);
     GBT_LAUNCHED();
-    k_part_scatter_rev<<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(rows, n, flags, tile_cnt, slot_node,
-                                                                       slot_node_out, nodes, rows_out);
+    // many tiles: one block scans the tile counts first, instead of every
+    // block summing the counts before it
+    long long *tile_off = nullptr;
+    if (tiles > kScanTilesAbove) {
+        GBT_TRY(scratch_t(c, kScrPartPos, (size_t)tiles, &tile_off));
+        k_tile_offsets<<<1, kTileScanThreads, 0, c->stream>>>(tile_cnt, tiles, tile_off);
+        GBT_LAUNCHED();
+    }
+    k_part_scatter_rev<<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(rows, n, flags, tile_cnt, tile_off,
+                                                                       slot_node, slot_node_out, nodes, rows_out);
     GBT_LAUNCHED();
     return GBT_OK;
 }

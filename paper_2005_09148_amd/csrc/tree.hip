@@ -1039,7 +1039,10 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     GBT_TRY(scratch_t(c, kScrCompact, (size_t)NN, &compact));
     k_leaves<<<blocks(NN), 256, 0, c->stream>>>(nodes, NN, e_dev, p->lambda, p->eta, leaf, compact);
     GBT_LAUNCHED();
-    if (so.alias) {
+    // the rows' final slots give their leaves when every row trained; on
+    // dense pages the walk of the page in row order is cheaper than adding
+    // into the margins at the slots' (scattered) rows
+    if (so.alias && mx->sparse) {
         if (n) {
             k_margin_slots<<<blocks(n), 256, 0, c->stream>>>(margin, rows, slot_node, leaf, n);
             GBT_LAUNCHED();

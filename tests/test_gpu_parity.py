@@ -468,6 +468,15 @@ def test_trees_feature_widths(gbt, ctx, max_bin, m):
     assert_same_trees(*r[:4])
 
 
+def test_trees_many_partition_tiles(gbt, ctx):
+    # over 2048 partition tiles of 1024 slots: the tile counts are scanned
+    # by a kernel of their own before the scatter
+    cfg = datagen.TrainConfig("t", 1, 32, 4, 1, eta=0.3)
+    d = datagen.config3(n=2_200_000, m=4)
+    r = train_both(gbt, ctx, d["X"], d["y"], cfg, 1)
+    assert_same_trees(*r[:4])
+
+
 @pytest.mark.parametrize("depth,n", [(0, 1000), (1, 65), (3, 1), (4, 63)])
 def test_degenerate_trees(gbt, ctx, hist_kernel, depth, n):
     cfg = datagen.TrainConfig("t", 1, 32, depth, 2, eta=0.5, f=0.5 if n > 10 else 1.0)
