@@ -269,26 +269,30 @@ __device__ inline int32_t row_feature_bin(const uint32_t *__restrict__ row, cons
     return v < hi ? (int32_t)(v - lo) : -1;
 }
 
-// Sparse pages: for each row, the first slot of every histogram feature
-// group's symbols, so that group g's symbols are the row's slots
-// [slot[g], slot[g + 1]) (the symbols ascend and the groups are contiguous
-// bin ranges).  Built by the tree driver for the page it trains on; a
-// search for a feature then looks only among its group's few slots.
+// Sparse pages: for each row and histogram feature group g, the row's slots
+// that hold the group's symbols (the symbols ascend and the groups are
+// contiguous bin ranges).  Built by the tree driver for the page it trains
+// on, in two layouts: by row (row[r * row_stride + g] = first slot of group
+// g, g <= groups), which the histogram passes read (the groups' workgroups
+// of one row share its line), and by group (col[g * rows + r] = first |
+// (end << 8)), which the partition reads for the split feature's group (a
+// node's rows are monotone, so a column line serves several of them).
 struct SlotTable {
-    const uint8_t *slot;      // rows x stride bytes; NULL: no table
+    const uint8_t *row;       // rows x row_stride; NULL: no table
+    const uint16_t *col;      // groups x rows
     const uint8_t *feat_grp;  // m: the group of each feature
-    int32_t stride;           // bytes per row (> number of groups)
+    int64_t rows;
+    int32_t row_stride;
     int32_t pad0;
 };
 
-// row_feature_bin for a sparse row with the row's slot-table entry `ts`.
-__device__ inline int32_t row_feature_bin_tbl(const uint32_t *__restrict__ row, const uint8_t *__restrict__ ts,
-                                              const Geo &g, const uint8_t *__restrict__ feat_grp, int32_t j)
+// row_feature_bin for a sparse row whose feature-j group occupies slots
+// [a, e) of the row.
+__device__ inline int32_t row_feature_bin_range(const uint32_t *__restrict__ row, const Geo &g, int32_t j,
+                                                int32_t a, int32_t e)
 {
     const uint32_t lo = (uint32_t)g.bin_ptr[j], hi = (uint32_t)g.bin_ptr[j + 1];
-    const int32_t fg = feat_grp[j];
-    int32_t a = ts[fg], b = ts[fg + 1];
-    const int32_t e = b;
+    int32_t b = e;
     while (a < b) {
         const int32_t mid = (a + b) >> 1;
         if (row_symbol(row, mid, g.w, g.mask) < lo)

@@ -398,10 +398,11 @@ __global__ void __launch_bounds__(kSparseThreads)
 // registers with 16-byte loads (all in flight at once) and reads its
 // symbols in order through a 64-bit bit buffer (the symbol width is the
 // same for every row, so the decode loop is uniform); a symbol at or past
-// the current group's end opens the next groups.  The block assembles its
-// rows' entries in LDS and writes them with word stores.
+// the current group's end opens the next groups.  Each thread keeps its
+// row's group starts in LDS and writes the row's entry of every group's
+// 2-byte column (consecutive threads, consecutive rows).
 constexpr int kTblThreads = 256;
-constexpr int kTblMaxStride = 64;  // bytes per table row
+constexpr int kTblMaxStride = 64;  // group starts per row (groups + 1)
 constexpr int kTblMaxWords = 64;   // row words held in registers
 
 typedef uint32_t u32x4_t4 __attribute__((ext_vector_type(4), aligned(4)));
@@ -409,12 +410,13 @@ typedef uint32_t u32x4_t4 __attribute__((ext_vector_type(4), aligned(4)));
 template <int kMaxWords>
 __global__ void __launch_bounds__(kTblThreads)
     k_sparse_slot_table(const uint32_t *__restrict__ page, int64_t n, int32_t row_words, int32_t stride, int32_t w,
-                        uint32_t mask, const HistGroup *__restrict__ groups, int32_t G, uint8_t *__restrict__ tbl,
-                        int32_t tstride)
+                        uint32_t mask, const HistGroup *__restrict__ groups, int32_t G, uint8_t *__restrict__ row_tbl,
+                        int32_t rs, uint16_t *__restrict__ col_tbl)
 {
     __shared__ uint32_t ends[kTblMaxStride];
-    __shared__ uint32_t out_l[kTblThreads * kTblMaxStride / 4];
-    uint8_t *o = (uint8_t *)out_l + threadIdx.x * tstride;
+    constexpr int kPitch = kTblMaxStride + 4;  // 17 words: the threads' bytes on distinct banks
+    __shared__ uint8_t out_l[kTblThreads * kPitch];
+    uint8_t *o = out_l + threadIdx.x * kPitch;
     for (int32_t g = threadIdx.x; g < kTblMaxStride; g += kTblThreads)
         ends[g] = g < G ? (uint32_t)groups[g].b1 : 0xffffffffu;
     const int64_t r0 = (int64_t)blockIdx.x * kTblThreads;
@@ -460,32 +462,32 @@ __global__ void __launch_bounds__(kTblThreads)
             }
         }
         while (g < G) o[++g] = (uint8_t)stride;
+        // the row's entry (word stores), then its place in each group's
+        // 2-byte column (consecutive threads, consecutive rows)
+        uint32_t *dr = (uint32_t *)(row_tbl + (r0 + threadIdx.x) * rs);
+        for (int32_t k = 0; k < rs / 4; ++k) dr[k] = ((const uint32_t *)o)[k];
+        uint16_t *dc = col_tbl + r0 + threadIdx.x;
+        for (int32_t k = 0; k < G; ++k) dc[(int64_t)k * n] = (uint16_t)(o[k] | (o[k + 1] << 8));
     }
-    __syncthreads();
-    const int32_t ow = nr * tstride / 4;
-    uint32_t *dst = (uint32_t *)(tbl + r0 * tstride);
-    for (int32_t k = threadIdx.x; k < ow; k += kTblThreads) dst[k] = out_l[k];
 }
 
-int32_t slot_table_stride(const gbt_matrix *mx, int32_t G)
+bool slot_table_fits(const gbt_matrix *mx, int32_t G)
 {
-    if (!mx->sparse || G < 1 || mx->stride > 255 || mx->row_words > kTblMaxWords) return 0;
-    const int32_t s = (G + 1 + 3) / 4 * 4;
-    return s <= kTblMaxStride ? s : 0;
+    return mx->sparse && G >= 1 && G < kTblMaxStride && mx->stride <= 255 && mx->row_words <= kTblMaxWords;
 }
 
 gbt_status sparse_slot_table(gbt_ctx *c, const gbt_matrix *mx, const HistGroup *groups_d, int32_t G,
-                             const uint32_t *page, int64_t n, uint8_t *tbl, int32_t stride)
+                             const uint32_t *page, int64_t n, uint8_t *row_tbl, uint16_t *col_tbl)
 {
-    if (stride != slot_table_stride(mx, G) || stride == 0)
-        return set_error(GBT_E_INVALID, "slot table stride %d does not fit the page", stride);
+    if (!slot_table_fits(mx, G)) return set_error(GBT_E_INVALID, "the page takes no slot table (%d groups)", G);
     if (n <= 0) return GBT_OK;
     const uint32_t mask = mx->w >= 32 ? 0xffffffffu : ((1u << mx->w) - 1u);
     const unsigned grid = (unsigned)((n + kTblThreads - 1) / kTblThreads);
     const int32_t rw = mx->row_words;
 #define GBT_TBL(MW)                                                                                      \
     k_sparse_slot_table<MW><<<grid, kTblThreads, 0, c->stream>>>(page, n, rw, mx->stride, mx->w, mask, \
-                                                                 groups_d, G, tbl, stride)
+                                                                 groups_d, G, row_tbl,                 \
+                                                                 slot_table_row_stride(G), col_tbl)
     if (rw <= 8)
         GBT_TBL(8);
     else if (rw <= 16)

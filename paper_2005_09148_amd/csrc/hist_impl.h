@@ -69,20 +69,22 @@ struct HistLaunch {
     const int32_t *n_red_d;
     int32_t max_red;
     int64_t *partials;
-    const uint8_t *slot_tbl = nullptr;  // sparse: the page's slot table (SlotTable::slot), or NULL
+    const uint8_t *slot_tbl = nullptr;  // sparse: the page's slot table by row (SlotTable::row), or NULL
     int32_t tbl_stride = 0;
 };
 
-// Bytes per row of a sparse page's slot table for G groups, or 0 when the
-// page does not take one (a row of more than 255 slots or 64 words, or more
-// than 63 groups).
-int32_t slot_table_stride(const gbt_matrix *mx, int32_t G);
+// Whether a sparse page of mx's geometry takes a slot table for G groups
+// (rows of at most 255 slots and 64 words, at most 63 groups).
+bool slot_table_fits(const gbt_matrix *mx, int32_t G);
+// Bytes per row of the by-row layout for G groups.
+inline int32_t slot_table_row_stride(int32_t G) { return (G + 1 + 3) / 4 * 4; }
 // The slot table of rows [0, n) of `page` (a page of mx's geometry) for the
-// groups groups_d[0, G): tbl[r * stride + g] = first slot of row r whose
-// symbol is >= groups_d[g].b0 (g < G), tbl[r * stride + G] = first slot
-// past the last group's bins.  Bytes past G are not written.
+// groups groups_d[0, G), s_g(r) being the first slot of row r whose symbol
+// is >= groups_d[g].b0 (s_G(r): the first past the last group's bins):
+// row_tbl[r * slot_table_row_stride(G) + g] = s_g(r) for g <= G, and
+// col_tbl[g * n + r] = s_g(r) | (s_{g+1}(r) << 8) for g < G.
 gbt_status sparse_slot_table(gbt_ctx *c, const gbt_matrix *mx, const HistGroup *groups_d, int32_t G,
-                             const uint32_t *page, int64_t n, uint8_t *tbl, int32_t stride);
+                             const uint32_t *page, int64_t n, uint8_t *row_tbl, uint16_t *col_tbl);
 
 gbt_status hist_launch_device(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int64_t *q,
                               const int32_t *rows, const HistLaunch &hl, const int64_t *parent_hist,

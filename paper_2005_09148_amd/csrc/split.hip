@@ -396,21 +396,23 @@ __device__ Cand eval_feature_regs(const long long *g, const long long *h, int32_
     best.order = 0;
     best.lg = best.lh = 0;
     const double G = fx(Qg, ep.e_g), H = fx(Qh, ep.e_h);
-    long long tg = 0, th = 0;
-#pragma unroll
-    for (int t = 0; t < kBL; ++t) {
-        tg += g[t];
-        th += h[t];
-    }
-    const long long mg = Qg - wave_sum(tg), mh = Qh - wave_sum(th);
-    long long cg = 0, ch = 0;  // sums of the chunks before chunk t
+    // inclusive prefix sums in bin order: chunk by chunk, each carried by
+    // the totals of the chunks before it; the last carry is the total
+    long long pgs[kBL], phs[kBL];
+    long long cg = 0, ch = 0;
 #pragma unroll
     for (int t = 0; t < kBL; ++t) {
         long long xg = g[t], xh = h[t];
         wave_scan2(xg, xh);
-        const long long pg = cg + xg, ph = ch + xh;
+        pgs[t] = cg + xg;
+        phs[t] = ch + xh;
         cg += __shfl(xg, 63, 64);
         ch += __shfl(xh, 63, 64);
+    }
+    const long long mg = Qg - cg, mh = Qh - ch;
+#pragma unroll
+    for (int t = 0; t < kBL; ++t) {
+        const long long pg = pgs[t], ph = phs[t];
         const int32_t s = t * 64 + lane + 1;  // left = bins < s
         if (s > B - 1) continue;
 #pragma unroll
@@ -496,15 +498,21 @@ __global__ void __launch_bounds__(256)
             h[i] += v.y;
         }
     }
-    long long sg[kV], sh[kV];
+    // the sibling in place of the parent
 #pragma unroll
     for (int i = 0; i < kV; ++i) {
-        sg[i] = pv[i].x - g[i];
-        sh[i] = pv[i].y - h[i];
+        pv[i].x -= g[i];
+        pv[i].y -= h[i];
         if (hist && off[i] >= 0) {
             hist[(int64_t)rd.slot * total_bins + off[i]] = make_longlong2(g[i], h[i]);
-            if (sib) hist[(int64_t)rd.sub_target * total_bins + off[i]] = make_longlong2(sg[i], sh[i]);
+            if (sib) hist[(int64_t)rd.sub_target * total_bins + off[i]] = pv[i];
         }
+    }
+    long long sgv[kV], shv[kV];
+#pragma unroll
+    for (int i = 0; i < kV; ++i) {
+        sgv[i] = pv[i].x;
+        shv[i] = pv[i].y;
     }
     if (ep.e_dev) {
         ep.e_g = ep.e_dev[0];
@@ -527,7 +535,7 @@ __global__ void __launch_bounds__(256)
             o.lg = o.lh = 0;
             if (B >= 2) {
                 const Cand cb = which == 0 ? eval_feature_regs<kBL>(g + j * kBL, h + j * kBL, B, nd.sum_g, nd.sum_h, ep)
-                                           : eval_feature_regs<kBL>(sg + j * kBL, sh + j * kBL, B, nd.sum_g, nd.sum_h, ep);
+                                           : eval_feature_regs<kBL>(sgv + j * kBL, shv + j * kBL, B, nd.sum_g, nd.sum_h, ep);
                 if (cb.valid) {
                     o.valid = 1;
                     o.gain = cb.gain;
@@ -826,9 +834,12 @@ __global__ void __launch_bounds__(kPartThreads)
                 const uint32_t s = cols[(int64_t)rec[k].y * n + r[k]];
                 b = s == geo.null_sym ? -1 : (int32_t)s;
             } else {
-                b = stbl.slot ? row_feature_bin_tbl(row, stbl.slot + (int64_t)r[k] * stbl.stride, geo,
-                                                    stbl.feat_grp, rec[k].y)
-                              : row_feature_bin(row, geo, rec[k].y);
+                if (stbl.col) {
+                    const uint32_t se = stbl.col[(int64_t)stbl.feat_grp[rec[k].y] * stbl.rows + r[k]];
+                    b = row_feature_bin_range(row, geo, rec[k].y, (int32_t)(se & 0xffu), (int32_t)(se >> 8));
+                } else {
+                    b = row_feature_bin(row, geo, rec[k].y);
+                }
             }
             f = (b < 0) ? (rec[k].w != 0 ? 1u : 0u) : (b < rec[k].z ? 1u : 0u);
         }
@@ -1196,7 +1207,7 @@ gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
                               const uint16_t *cols)
 {
     if (n == 0) return GBT_OK;
-    const SlotTable st = stbl ? *stbl : SlotTable{nullptr, nullptr, 0, 0};
+    const SlotTable st = stbl ? *stbl : SlotTable{nullptr, nullptr, nullptr, 0, 0, 0};
     GBT_CHECK(n < ((int64_t)1 << 31) - 1, "partition of %lld rows (limit 2^31-2)", (long long)n);
     uint8_t *flags;
     GBT_TRY(scratch_t(c, kScrPartFlags, (size_t)n + 16, &flags));
@@ -1241,7 +1252,8 @@ gbt_status partition_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page
     // sum the counts before their tiles themselves
     k_part_flags_tiles<false><<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(rows, n, page, geo, position, slot_node,
                                                                        nodes, flags, tile_off, LevelChoice{},
-                                                                       SlotTable{nullptr, nullptr, 0, 0}, nullptr);
+                                                                       SlotTable{nullptr, nullptr, nullptr, 0, 0, 0},
+                                                                       nullptr);
     GBT_LAUNCHED();
     if (n_list > 0) {
         k_part_bounds<<<(unsigned)n_list, kBoundThreads, 0, c->stream>>>(list, n_list_d, n_list, nodes, flags,

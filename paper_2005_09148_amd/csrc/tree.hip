@@ -910,12 +910,12 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     // the feature groups live with the matrix (uploaded once per kernel kind)
     // sparse pages: the slot table of the training page, and each feature's
     // group (stored after the groups)
-    const int32_t tstride = hp.kind == kHistSparse ? slot_table_stride(mx, G) : 0;
+    const bool use_tbl = hp.kind == kHistSparse && slot_table_fits(mx, G);
     const size_t fg_off = (std::max<size_t>(groups.size(), 1) * sizeof(HistGroup) + 15) / 16 * 16;
     if (mx->groups_kind != hp.kind) {
         // owned (and budgeted) by the matrix's context, like its other arrays
         std::vector<uint8_t> fg;
-        if (tstride) {
+        if (use_tbl) {
             fg.assign((size_t)mx->m, 0);
             for (int32_t g = 0; g < G; ++g)
                 for (int32_t f = groups[g].f0; f < groups[g].f1; ++f) fg[f] = (uint8_t)g;
@@ -935,12 +935,15 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         mx->groups_kind = hp.kind;
     }
     const HistGroup *groups_d = (const HistGroup *)mx->groups_d;
-    SlotTable stbl{nullptr, nullptr, 0, 0};
-    if (tstride && D > 0 && R > 0) {
+    SlotTable stbl{nullptr, nullptr, nullptr, 0, 0, 0};
+    if (use_tbl && D > 0 && R > 0) {
+        const int32_t rs = slot_table_row_stride(G);
+        const size_t col_off = ((size_t)R * rs + 255) / 256 * 256;
         uint8_t *tb;
-        GBT_TRY(scratch_t(c, kScrSlotTbl, (size_t)R * tstride, &tb));
-        GBT_TRY(sparse_slot_table(c, mx, groups_d, G, so.page, R, tb, tstride));
-        stbl = SlotTable{tb, (const uint8_t *)mx->groups_d + fg_off, tstride, 0};
+        GBT_TRY(scratch_t(c, kScrSlotTbl, col_off + (size_t)R * G * sizeof(uint16_t), &tb));
+        uint16_t *tc = (uint16_t *)(tb + col_off);
+        GBT_TRY(sparse_slot_table(c, mx, groups_d, G, so.page, R, tb, tc));
+        stbl = SlotTable{tb, tc, (const uint8_t *)mx->groups_d + fg_off, R, rs, 0};
     }
     // dense pages: the partition reads each row's split symbol from a column
     // copy of the training page, made once per tree (once per matrix when
@@ -987,7 +990,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     int32_t *cntA = cnt, *cntB = cnt + 1;
     if (D > 0 && R > 0) {
         HistLaunch hl{hp.kind, groups_d, G, hp.max_groups_bins, work_d, nullptr, n_root, red_d, nullptr,
-                      fused ? 0 : 1, partials, stbl.slot, stbl.stride};
+                      fused ? 0 : 1, partials, stbl.row, stbl.row_stride};
         GBT_TRY(hist_launch_device(c, mx, so.page, so.q, nullptr, hl, nullptr, histA, upd));
         ++hist_launches;
         if (fused) {
@@ -1003,7 +1006,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         if (!fused && R > 0) GBT_TRY(eval_impl(c, mx, histA, evA, maxn, ep, splits_d, cntA, nodes));
         const LevelChoice lc{cand, mx->m, (int32_t)((1u << d) - 1), (int32_t)((2u << d) - 1)};
         GBT_TRY(partition_rev_impl(c, mx, so.page, rows, R, slot_node, slot_tmp, nodes, rows_tmp,
-                                   choose ? &lc : nullptr, stbl.slot ? &stbl : nullptr, cols));
+                                   choose ? &lc : nullptr, stbl.row ? &stbl : nullptr, cols));
         std::swap(rows, rows_tmp);
         std::swap(slot_node, slot_tmp);
         const bool plan_next = d + 1 < D && R > 0;
@@ -1015,7 +1018,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         timer_end(c, mark);
         if (plan_next) {
             HistLaunch hl{hp.kind, groups_d, G, hp.max_groups_bins, work_d, cnt + 2, max_work, red_d, cnt + 3,
-                          fused ? 0 : maxn, partials, stbl.slot, stbl.stride};
+                          fused ? 0 : maxn, partials, stbl.row, stbl.row_stride};
             GBT_TRY(hist_launch_device(c, mx, so.page, so.q, rows, hl, histA, histB, upd));
             ++hist_launches;
             if (fused) {
