@@ -307,7 +307,7 @@ gbt_status gbt_sampled_free(gbt_sampled *s);
  * gbt_quantize writes it, 16-byte aligned (else GBT_E_INVALID).  Symbols
  * outside a feature's bin range (only in a page not written by this library)
  * add nothing.  GBT_E_UNSUPPORTED when a feature has more bins than one
- * histogram group holds (2560 for dense pages, 8192 for sparse ones). */
+ * histogram group holds (2560 for dense pages, 10176 for sparse ones). */
 gbt_status gbt_build_hist(gbt_ctx *ctx, const gbt_matrix *layout, const uint32_t *page_d,
                           const int64_t *gpair_fx_d, const int32_t *rows_d, const gbt_seg *build_h,
                           int32_t n_build, const gbt_sub *sub_h, int32_t n_sub,

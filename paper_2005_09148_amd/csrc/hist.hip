@@ -21,7 +21,7 @@ namespace gbt {
 constexpr int kHistThreads = 512;
 // Sparse groups: up to 8192 bins, g then h (128 KiB of LDS), one
 // 1024-thread workgroup per CU: fewer groups, so fewer reads of every row.
-constexpr int kLdsBins = 8192;
+constexpr int kLdsBins = 10176;  // 159 KiB of int64 (g, h) sums: all of a CU's LDS
 constexpr int kSparseThreads = 1024;
 // value-balanced sparse groups: at least this many
 constexpr int kSparseMinGroups = 16;
