@@ -468,6 +468,29 @@ def test_trees_feature_widths(gbt, ctx, max_bin, m):
     assert_same_trees(*r[:4])
 
 
+@pytest.mark.parametrize("f,dense_row", [(0.5, False), (1.0, True), (0.4, True)])
+def test_sparse_trees_sampling_and_long_rows(gbt, ctx, f, dense_row):
+    # CSR data with MVS sampling (the sampled page is a compacted sparse
+    # page with its own slot table), and with one row of 300 values (rows
+    # of more than 255 slots take no slot table: binary-searched rows)
+    d, _ = small_csr(4000, 300, 0.05, 57)
+    if dense_row:
+        X = np.full((4000, 300), np.nan, np.float32)
+        lens = np.diff(d["indptr"])
+        rows = np.repeat(np.arange(4000), lens)
+        X[rows, d["indices"]] = d["values"]
+        X[17, :] = np.random.default_rng(58).lognormal(size=300).astype(np.float32)
+        r, c = np.nonzero(~np.isnan(X))
+        d = {"kind": "csr", "indptr": np.concatenate([[0], np.cumsum(np.bincount(r, minlength=4000))]).astype(np.int64),
+             "indices": c.astype(np.int32), "values": X[r, c].astype(np.float32), "m": 300}
+    y = (np.random.default_rng(59).random(4000) < 0.4).astype(np.float32)
+    cfg = datagen.TrainConfig("t", 0, 64, 6, 2, eta=0.3, gamma=0.1, f=f)
+    r = train_both(gbt, ctx, d, y, cfg, 2)
+    assert_same_trees(*r[:4])
+    if dense_row:
+        assert r[4].info().stride == 300
+
+
 def test_trees_many_partition_tiles(gbt, ctx):
     # over 2048 partition tiles of 1024 slots: the tile counts are scanned
     # by a kernel of their own before the scatter
