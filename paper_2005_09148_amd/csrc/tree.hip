@@ -321,6 +321,9 @@ __global__ void __launch_bounds__(1024)
     __shared__ int32_t lds16[16];
     __shared__ unsigned long long red_rows[16];
     __shared__ int32_t red_nodes[16];
+    // one pass's nodes: first work item (and the pass's end), row segment
+    __shared__ int32_t s_kp[1025];
+    __shared__ long long s_sb[1024], s_se[1024];
     const int32_t n_cur = *n_cur_d;
     // the children's segments and sums; the rows and nodes to build, for the
     // chunk size (a level of at most 1024 nodes keeps each thread's node in
@@ -395,11 +398,28 @@ __global__ void __launch_bounds__(1024)
             const int64_t sb = left_small ? x.begin : x.begin + x.nl;
             const int64_t se = left_small ? x.begin + x.nl : x.begin + x.nl + x.nr;
             red[kb] = {left_small ? sl : sr, kp, nchunks, x.slot, left_small ? sr : sl, 0};
-            for (int32_t j = 0; j < nchunks; ++j) {
-                int64_t b = sb + (int64_t)j * chunk;
-                work[kp + j] = {b, b + chunk < se ? b + chunk : se, kp + j, 0};
-            }
+            s_sb[threadIdx.x] = sb;
+            s_se[threadIdx.x] = se;
         }
+        s_kp[threadIdx.x] = kp;
+        if (threadIdx.x == 1023) s_kp[1024] = c_part + tot_p;
+        __syncthreads();
+        // the pass's work items, written by all threads: item e belongs to
+        // the last node whose first item is <= e (nodes without items have
+        // the next node's first item)
+        for (int32_t e = c_part + (int32_t)threadIdx.x; e < c_part + tot_p; e += 1024) {
+            int32_t lo = 0, hi = 1024;  // s_kp[lo] <= e < s_kp[hi]
+            while (hi - lo > 1) {
+                const int32_t mid = (lo + hi) >> 1;
+                if (s_kp[mid] <= e)
+                    lo = mid;
+                else
+                    hi = mid;
+            }
+            const int64_t b = s_sb[lo] + (int64_t)(e - s_kp[lo]) * chunk;
+            work[e] = {b, b + chunk < s_se[lo] ? b + chunk : s_se[lo], e, 0};
+        }
+        __syncthreads();
         c_build += tot_b;
         c_part += tot_p;
     }
