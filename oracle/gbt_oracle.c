@@ -21,6 +21,7 @@
  *   orc_gradients .................... Sec. 2.1, Eq. 4-5: g and h
  *   orc_mvs_* ........................ Sec. 2.4 Eq. 9 + Sec. 3.4 (Alg. 7):
  *                                       minimal variance sampling
+ *   orc_sgb_* / orc_goss_* ........... Sec. 2.3: the SGB and GOSS samplers
  *   orc_fixed_point .................. exact integer gradient sums
  *   orc_build_hist ................... Alg. 1 BuildHistograms
  *   orc_eval_node .................... Alg. 1 EvaluateSplit with Eq. 8
@@ -82,7 +83,12 @@ typedef struct {
     double mvs_lambda; /* the lambda of Eq. 9 */
     uint64_t seed;
     uint64_t iteration;
+    int32_t sampler;   /* ORC_SAMPLE_MVS, _SGB or _GOSS (used when f < 1) */
+    int32_t pad0;
+    double goss_a;     /* GOSS: the top fraction a (the rest fraction is f - a) */
 } orc_params;
+
+enum { ORC_SAMPLE_MVS = 0, ORC_SAMPLE_SGB = 1, ORC_SAMPLE_GOSS = 2 };
 
 typedef struct {
     int32_t feature;
@@ -607,6 +613,68 @@ double orc_mvs_weight(int64_t a, int64_t T)
 }
 
 /* ------------------------------------------------------------------------ */
+/* Sec. 2.3, the other two samplers (a reading: each random draw is the     */
+/* row's Philox word U_i of the MVS stream, compared with a probability     */
+/* scaled to 2^64; p < 1 gives the integer floor(p 2^64), p = 1 keeps all).  */
+/* SGB (Friedman): each row is kept with probability f, weight 1.            */
+/* GOSS (Ke et al.): the top a*100% rows by |g| -- keys k_i = rint(|g_i| 2^e) */
+/* as in orc_mvs_keys with lambda = 0, A = rint(a n), every row whose key is */
+/* at least the A-th largest key (ties included; none when A = 0) -- plus   */
+/* each other row with probability p = b / (1 - a), b = f - a, weighted by   */
+/* (1 - a) / b = 1/p.                                                        */
+/* ------------------------------------------------------------------------ */
+static int bernoulli(uint64_t U, double p)
+{
+    if (p >= 1.0) return 1;
+    return U < (uint64_t)ldexp(p, 64);
+}
+
+void orc_sgb_select(int64_t n, double f, uint64_t seed, uint64_t iteration, int64_t row_offset, uint8_t *keep)
+{
+    for (int64_t i = 0; i < n; ++i)
+        keep[i] = (uint8_t)bernoulli(orc_mvs_uniform(seed, iteration, (uint64_t)(row_offset + i)), f);
+}
+
+static int cmp_i64_desc(const void *a, const void *b)
+{
+    int64_t x = *(const int64_t *)a, y = *(const int64_t *)b;
+    return x < y ? 1 : (x > y ? -1 : 0);
+}
+
+/* The top threshold: the A-th largest key, or INT64_MAX when A = 0. */
+int64_t orc_goss_top_threshold(const int64_t *keys, int64_t n, int64_t A)
+{
+    if (A <= 0 || n <= 0) return INT64_MAX;
+    if (A > n) A = n;
+    int64_t *s = (int64_t *)malloc(sizeof(int64_t) * (size_t)n);
+    memcpy(s, keys, sizeof(int64_t) * (size_t)n);
+    qsort(s, (size_t)n, sizeof(int64_t), cmp_i64_desc);
+    int64_t t = s[A - 1];
+    free(s);
+    return t;
+}
+
+int64_t orc_goss_top_count(double a, int64_t n)
+{
+    int64_t A = (int64_t)rint(a * (double)n);
+    return A < 0 ? 0 : (A > n ? n : A);
+}
+
+void orc_goss_select(const int64_t *keys, int64_t n, int64_t T_top, double a, double b, uint64_t seed,
+                     uint64_t iteration, int64_t row_offset, uint8_t *keep)
+{
+    const double p = b / (1.0 - a);
+    for (int64_t i = 0; i < n; ++i)
+        keep[i] = (uint8_t)(keys[i] >= T_top ||
+                            bernoulli(orc_mvs_uniform(seed, iteration, (uint64_t)(row_offset + i)), p));
+}
+
+double orc_goss_weight(int64_t key, int64_t T_top, double a, double b)
+{
+    return key >= T_top ? 1.0 : (1.0 - a) / b;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Exact integer gradient sums.  Over the R training rows:                   */
 /*   M = max |x| < 2^E, e = 62 - E - ceil(log2 R), q = rint(x * 2^e) (int64)  */
 /* so any sum of R values stays below 2^62 in magnitude.  Sums go back to    */
@@ -840,14 +908,28 @@ int orc_train_tree(const orc_data *d, const float *label, float *margin, const o
         int64_t *keys = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n + 1));
         uint8_t *keep = (uint8_t *)malloc((size_t)n + 1);
         if (!keys || !keep) return ORC_ENOMEM;
-        rc = orc_mvs_keys(gpair, n, p->mvs_lambda, keys, &info->e_key);
-        if (rc) return rc;
-        info->K = orc_mvs_target(p->f, n);
-        info->T = orc_mvs_threshold(keys, n, info->K);
-        orc_mvs_select(keys, n, info->T, p->seed, p->iteration, 0, keep);
+        const double ga = p->goss_a, gb = p->f - p->goss_a;
+        if (p->sampler == ORC_SAMPLE_SGB) {
+            orc_sgb_select(n, p->f, p->seed, p->iteration, 0, keep);
+        } else if (p->sampler == ORC_SAMPLE_GOSS) {
+            if (!(ga >= 0.0 && ga < 1.0 && gb > 0.0)) return ORC_EINVAL;
+            rc = orc_mvs_keys(gpair, n, 0.0, keys, &info->e_key);
+            if (rc) return rc;
+            info->K = orc_goss_top_count(ga, n);
+            info->T = orc_goss_top_threshold(keys, n, info->K);
+            orc_goss_select(keys, n, info->T, ga, gb, p->seed, p->iteration, 0, keep);
+        } else {
+            rc = orc_mvs_keys(gpair, n, p->mvs_lambda, keys, &info->e_key);
+            if (rc) return rc;
+            info->K = orc_mvs_target(p->f, n);
+            info->T = orc_mvs_threshold(keys, n, info->K);
+            orc_mvs_select(keys, n, info->T, p->seed, p->iteration, 0, keep);
+        }
         for (int64_t i = 0; i < n; ++i) {
             if (!keep[i]) continue;
-            double w = orc_mvs_weight(keys[i], info->T);
+            double w = p->sampler == ORC_SAMPLE_SGB    ? 1.0
+                       : p->sampler == ORC_SAMPLE_GOSS ? orc_goss_weight(keys[i], info->T, ga, gb)
+                                                       : orc_mvs_weight(keys[i], info->T);
             grow[R] = i;
             gw[2 * R] = (double)gpair[2 * i] * w;
             gw[2 * R + 1] = (double)gpair[2 * i + 1] * w;

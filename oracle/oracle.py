@@ -52,7 +52,8 @@ class OrcParams(C.Structure):
     _fields_ = [("loss", C.c_int32), ("max_depth", C.c_int32), ("eta", C.c_double),
                 ("lambda_", C.c_double), ("gamma", C.c_double),
                 ("min_child_weight", C.c_double), ("f", C.c_double),
-                ("mvs_lambda", C.c_double), ("seed", C.c_uint64), ("iteration", C.c_uint64)]
+                ("mvs_lambda", C.c_double), ("seed", C.c_uint64), ("iteration", C.c_uint64),
+                ("sampler", C.c_int32), ("pad0", C.c_int32), ("goss_a", C.c_double)]
 
 
 class OrcInfo(C.Structure):
@@ -100,6 +101,11 @@ def lib():
             "orc_mvs_uniform": (u64, [u64, u64, u64]),
             "orc_mvs_select": (None, [vp, i64, i64, u64, u64, i64, vp]),
             "orc_mvs_weight": (f64, [i64, i64]),
+            "orc_sgb_select": (None, [i64, f64, u64, u64, i64, vp]),
+            "orc_goss_top_threshold": (i64, [vp, i64, i64]),
+            "orc_goss_top_count": (i64, [f64, i64]),
+            "orc_goss_select": (None, [vp, i64, i64, f64, f64, u64, u64, i64, vp]),
+            "orc_goss_weight": (f64, [i64, i64, f64, f64]),
             "orc_fixed_point": (None, [vp, i64, vp, vp, vp]),
             "orc_build_hist": (None, [vp, vp, i64, vp, vp]),
             "orc_eval_node": (None, [vp, vp, vp, i32, vp, i32, i32, vp]),
@@ -325,6 +331,39 @@ def mvs_weight(a, T):
     return lib().orc_mvs_weight(int(a), int(T))
 
 
+SAMPLE_MVS, SAMPLE_SGB, SAMPLE_GOSS = 0, 1, 2
+
+
+def sgb_select(n, f, seed, iteration, row_offset=0):
+    keep = np.zeros(max(n, 1), np.uint8)
+    lib().orc_sgb_select(int(n), float(f), seed, iteration, row_offset, _p(keep))
+    return keep[:n].astype(bool)
+
+
+def goss_top_count(a, n):
+    return int(lib().orc_goss_top_count(float(a), int(n)))
+
+
+def goss_top_threshold(keys, A):
+    keys = _c(keys, np.int64)
+    if keys.size == 0:
+        keys = np.zeros(1, np.int64)
+        return int(lib().orc_goss_top_threshold(_p(keys), 0, int(A)))
+    return int(lib().orc_goss_top_threshold(_p(keys), len(keys), int(A)))
+
+
+def goss_select(keys, T_top, a, b, seed, iteration, row_offset=0):
+    keys = _c(keys, np.int64)
+    keep = np.zeros(len(keys), np.uint8)
+    lib().orc_goss_select(_p(keys), len(keys), int(T_top), float(a), float(b), seed, iteration, row_offset,
+                          _p(keep))
+    return keep.astype(bool)
+
+
+def goss_weight(key, T_top, a, b):
+    return lib().orc_goss_weight(int(key), int(T_top), float(a), float(b))
+
+
 def fixed_point(gw):
     gw = _c(gw, np.float64).reshape(-1, 2)
     q = np.empty_like(gw, dtype=np.int64)
@@ -357,10 +396,13 @@ class Params:
     f: float = 1.0
     mvs_lambda: float = 1.0
     seed: int = 0
+    sampler: int = 0      # SAMPLE_MVS, SAMPLE_SGB or SAMPLE_GOSS (when f < 1)
+    goss_a: float = 0.0   # GOSS top fraction a (the rest fraction is f - a)
 
     def struct(self, iteration=0) -> OrcParams:
         return OrcParams(self.loss, self.max_depth, self.eta, self.lambda_, self.gamma,
-                         self.min_child_weight, self.f, self.mvs_lambda, self.seed, iteration)
+                         self.min_child_weight, self.f, self.mvs_lambda, self.seed, iteration,
+                         self.sampler, 0, self.goss_a)
 
 
 def eval_node(hist, node_sum, nbins, params: Params, e_g, e_h):

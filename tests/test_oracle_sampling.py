@@ -157,3 +157,113 @@ def test_fixed_point_bounds_and_error(orc):
 def test_fixed_point_zero_input(orc):
     q, eg, eh = orc.fixed_point(np.zeros((4, 2)))
     assert (q == 0).all() and eg == 60 and eh == 60
+
+
+# ---------------------------------------------------------------- SGB and GOSS
+# Sec. 2.3.  Each random draw is the row's Philox word (the MVS stream),
+# compared with floor(p 2^64) for p < 1; the thresholds below are computed
+# with exact rationals, independently of the oracle's floating-point ldexp.
+def draw_limit(p):
+    return math.floor(Fraction(p) * 2**64)
+
+
+@pytest.mark.parametrize("f,off", [(0.5, 0), (0.3, 1001), (0.07, 6)])
+def test_sgb_keeps_rows_whose_word_is_below_f(orc, f, off):
+    seed, it = 21, 4
+    keep = orc.sgb_select(400, f, seed, it, off)
+    lim = draw_limit(f)
+    for i in range(400):
+        row = off + i
+        U = int(numpy_philox_block(row // 4, it, seed)[row % 4])
+        assert keep[i] == (U < lim)
+
+
+def test_sgb_fraction_is_close_to_f(orc):
+    keep = orc.sgb_select(200_000, 0.3, 5, 0)
+    # Binomial(n, 0.3): 6 standard deviations
+    assert abs(keep.mean() - 0.3) < 6 * math.sqrt(0.3 * 0.7 / 200_000)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_goss_top_threshold_is_the_a_th_largest_key(orc, seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 60))
+    keys = rng.integers(0, 12, n).astype(np.int64)  # many ties
+    for A in range(0, n + 1):
+        t = orc.goss_top_threshold(keys, A)
+        if A == 0:
+            assert t == 2**63 - 1
+            continue
+        assert t == np.sort(keys)[::-1][A - 1]
+        # at least A rows at or above it, fewer than A strictly above it
+        assert (keys >= t).sum() >= A > (keys > t).sum()
+
+
+def test_goss_top_count_rounds(orc):
+    assert orc.goss_top_count(0.1, 1000) == 100
+    assert orc.goss_top_count(0.0, 1000) == 0
+    assert orc.goss_top_count(0.25, 10) == 2  # rint(2.5) to even
+    assert orc.goss_top_count(1.0, 7) == 7
+
+
+@pytest.mark.parametrize("off", [0, 3])
+def test_goss_selection_and_weights(orc, off):
+    rng = np.random.default_rng(7)
+    keys = rng.integers(0, 1000, 500).astype(np.int64)
+    a, b, seed, it = 0.1, 0.2, 9, 2
+    A = orc.goss_top_count(a, len(keys))
+    t = orc.goss_top_threshold(keys, A)
+    keep = orc.goss_select(keys, t, a, b, seed, it, off)
+    lim = draw_limit(b / (1.0 - a))
+    for i in range(len(keys)):
+        row = off + i
+        U = int(numpy_philox_block(row // 4, it, seed)[row % 4])
+        assert keep[i] == (keys[i] >= t or U < lim)
+        w = orc.goss_weight(keys[i], t, a, b)
+        assert w == (1.0 if keys[i] >= t else (1.0 - a) / b)
+
+
+def test_goss_rest_weights_are_unbiased(orc):
+    # E[keep_i * w_i] over the draw, for a row outside the top set:
+    # floor(p 2^64) / 2^64 * (1 - a) / b, with p = b / (1 - a)
+    for a, b in [(0.1, 0.2), (0.05, 0.05), (0.2, 0.8)]:
+        p = b / (1.0 - a)
+        e = Fraction(draw_limit(p), 2**64) * Fraction((1.0 - a) / b) if p < 1 else Fraction((1.0 - a) / b)
+        assert abs(e - 1) < Fraction(1, 2**50)
+
+
+def test_goss_keys_are_gradient_magnitudes(orc):
+    # the top set ranks rows by |g| alone (the MVS lambda does not enter):
+    # rows with large hessians but small gradients stay out of it
+    n = 64
+    g = np.linspace(-1.0, 1.0, n).astype(np.float32)
+    h = np.where(np.arange(n) % 2 == 0, 50.0, 0.01).astype(np.float32)
+    gp = np.stack([g, h], 1).astype(np.float32)
+    keys, _ = orc.mvs_keys(gp, 0.0)
+    A = 10
+    t = orc.goss_top_threshold(keys, A)
+    top = set(np.nonzero(keys >= t)[0].tolist())
+    assert top == set(np.argsort(-np.abs(g.astype(np.float64)), kind="stable")[:A].tolist())
+
+
+@pytest.mark.parametrize("sampler", [1, 2])
+def test_training_with_sgb_and_goss(orc, sampler):
+    # a whole iteration samples as the selection functions say, and the
+    # training rows are the kept rows in ascending order
+    rng = np.random.default_rng(11)
+    X = rng.normal(size=(3000, 5)).astype(np.float32)
+    y = (X[:, 0] + 0.3 * rng.normal(size=3000) > 0).astype(np.float32)
+    b = orc.bin_dense(X, orc.sketch_cuts_dense(X, 32))
+    P = orc.Params(loss=orc.LOSS_LOGISTIC, max_depth=4, eta=0.3, f=0.3, seed=3, sampler=sampler, goss_a=0.1)
+    margin = np.zeros(3000, np.float32)
+    r = orc.train_tree(b, y, margin, P, iteration=1, want_detail=True)
+    gp = r.gpair
+    if sampler == 1:
+        want = orc.sgb_select(3000, 0.3, 3, 1)
+    else:
+        keys, _ = orc.mvs_keys(gp, 0.0)
+        t = orc.goss_top_threshold(keys, orc.goss_top_count(0.1, 3000))
+        want = orc.goss_select(keys, t, 0.1, 0.3 - 0.1, 3, 1)
+        assert r.info.T == t
+    assert np.array_equal(r.sel, np.nonzero(want)[0])
+    assert (margin != 0).any()
