@@ -46,6 +46,11 @@ typedef int32_t gbt_status;
 #define GBT_E_DEVICE (-4)
 #define GBT_E_UNSUPPORTED (-5)
 
+/* Samplers (Sec. 2.3 and 2.4). */
+#define GBT_SAMPLE_MVS 0  /* minimal variance sampling, Eq. 9 */
+#define GBT_SAMPLE_SGB 1  /* stochastic gradient boosting: uniform rows */
+#define GBT_SAMPLE_GOSS 2 /* gradient-based one-side sampling */
+
 #define GBT_ABI_VERSION 1
 
 enum { GBT_INPUT_DENSE_F32 = 0, GBT_INPUT_CSR_F32 = 1 };
@@ -114,6 +119,9 @@ typedef struct {
     double mvs_lambda;        /* lambda of Eq. 9 */
     uint64_t seed;
     uint64_t iteration;       /* tree index; keys the sampling stream */
+    int32_t sampler;          /* GBT_SAMPLE_*: the sampler used when f < 1 */
+    int32_t pad0;
+    double goss_a;            /* GBT_SAMPLE_GOSS: the top fraction a (rest f - a) */
 } gbt_train_params;
 
 /* A node's row segment rows[begin, end) and its histogram slot. */
@@ -190,13 +198,14 @@ typedef struct {
     uint64_t seed;
     uint64_t iteration;
     int32_t loss;           /* used when gradients are recomputed from margins */
-    int32_t pad0;
+    int32_t sampler;        /* GBT_SAMPLE_* */
+    double goss_a;          /* GBT_SAMPLE_GOSS: the top fraction a (rest f - a) */
 } gbt_sample_params;
 
 typedef struct {
     int64_t n_sampled;
-    int64_t threshold;
-    int64_t target;         /* K = max(1, rint(f*n)) */
+    int64_t threshold;      /* MVS: T*; GOSS: the top threshold t; SGB: 0 */
+    int64_t target;         /* MVS: K = max(1, rint(f*n)); GOSS: A; SGB: 0 */
     int32_t exp_key;
     int32_t exp_g;
     int32_t exp_h;
@@ -286,6 +295,14 @@ gbt_status gbt_gradients(gbt_ctx *ctx, int32_t loss, const float *margin_d, cons
  *       Philox4x64-10(counter (i div 4, iteration, 0, 0), key (seed, 0))
  *   w_i = 1 if a_i >= T* else T* / a_i;  (g', h') = (g w_i, h w_i)
  *   q = rint((g', h') 2^(e_g, e_h)), e = 62 - E - ceil(log2 R)
+ * Sec. 2.3's other samplers (sp->sampler), with the same draws U_i, p < 1
+ * compared as U_i < floor(p 2^64) (p = 1 keeps):
+ *   GBT_SAMPLE_SGB : keep iff U_i < floor(f 2^64); w_i = 1
+ *   GBT_SAMPLE_GOSS: keys k_i = rint(|g_i| 2^e) (the keys above with
+ *       mvs_lambda = 0), A = rint(a n), a = sp->goss_a, b = f - a > 0;
+ *       t = the A-th largest key (none when A = 0); keep iff k_i >= t or
+ *       U_i < floor(p 2^64), p = b / (1 - a); w_i = 1 if k_i >= t else
+ *       (1 - a) / b
  * gpair_d (n pairs) may be NULL for pinned-host data: gradients are then
  * recomputed from margin_d/label_d with sp->loss while pages stream.
  * f = 1 keeps every row without copying (is_alias) when the data is one

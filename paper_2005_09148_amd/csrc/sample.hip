@@ -254,16 +254,19 @@ __global__ void __launch_bounds__(256) k_mvs_keys(SampleSrc src, int64_t n, doub
 // Closed form when T* exceeds every key; otherwise the radix descent
 // starts on [0, 2^S) with 2^S > amax + 1.  done_host (pinned host memory,
 // may be NULL) receives 1 for the closed form, else 0.
-__global__ void k_mvs_thresh_init(SampleState *__restrict__ st, int64_t K, int32_t *__restrict__ done_host)
+__global__ void k_mvs_thresh_init(SampleState *__restrict__ st, int64_t K, int32_t *__restrict__ done_host,
+                                  int32_t count_mode)
 {
     if (threadIdx.x != 0) return;
     unsigned long long amax = fold_max(st->amax), asum = fold_sum(st->asum);
-    unsigned long long q = (asum + (unsigned long long)K - 1) / (unsigned long long)K;
     st->C_above = 0;
     st->F_below = 0;
     st->lo = 0;
-    if (q > amax + 1) {
-        st->T = (long long)q;
+    // count mode: no top rows when A = 0; otherwise always a descent
+    const bool closed = count_mode ? K <= 0 : (asum + (unsigned long long)K - 1) / (unsigned long long)K > amax + 1;
+    if (closed) {
+        st->T = count_mode ? 0x7fffffffffffffffll
+                           : (long long)((asum + (unsigned long long)K - 1) / (unsigned long long)K);
         st->done = 1;
         st->levels = 0;
         if (done_host) __hip_atomic_store(done_host, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
@@ -339,7 +342,8 @@ __device__ inline bool thresh_ok(unsigned long long F, unsigned long long C, int
 // histogram for the next level.
 __global__ void __launch_bounds__(256) k_mvs_radix_decide(SampleState *__restrict__ st, int64_t K,
                                                           unsigned long long *__restrict__ hcnt,
-                                                          unsigned long long *__restrict__ hsum)
+                                                          unsigned long long *__restrict__ hsum,
+                                                          int32_t count_mode)
 {
     __shared__ unsigned long long s_c[kDigitBuckets + 1], s_f[kDigitBuckets + 1];
     __shared__ int s_best;
@@ -364,7 +368,9 @@ __global__ void __launch_bounds__(256) k_mvs_radix_decide(SampleState *__restric
     __syncthreads();
     for (int b = threadIdx.x; b <= nb; b += blockDim.x) {
         unsigned long long T = lo + ((unsigned long long)b << shift);
-        if (thresh_ok(s_f[b], s_c[b], K, T)) atomicMin(&s_best, b);
+        // count mode: the least T with fewer than K keys at or above it
+        const bool ok = count_mode ? s_c[b] < (unsigned long long)K : thresh_ok(s_f[b], s_c[b], K, T);
+        if (ok) atomicMin(&s_best, b);
     }
     __syncthreads();
     int best = s_best;
@@ -374,7 +380,8 @@ __global__ void __launch_bounds__(256) k_mvs_radix_decide(SampleState *__restric
             st->bad |= 2u;
             st->done = 1;
         } else if (shift == 0) {
-            st->T = (long long)(lo + (unsigned long long)best);
+            // count mode keeps the K-th largest key, one below that least T
+            st->T = (long long)(lo + (unsigned long long)best) - (count_mode ? 1 : 0);
             st->done = 1;
         } else {
             st->F_below = s_f[best - 1];
@@ -399,10 +406,12 @@ __global__ void __launch_bounds__(256) k_mvs_select(SampleSrc src, const int64_t
                                                     const SampleState *__restrict__ st,
                                                     uint64_t seed, uint64_t iteration,
                                                     int64_t row_offset, uint8_t *__restrict__ keep,
-                                                    int32_t *__restrict__ tile_cnt)
+                                                    int32_t *__restrict__ tile_cnt, SampleRule rule)
 {
     __shared__ int32_t red4[4];
-    const unsigned long long T = (unsigned long long)st->T;
+    const bool sgb = rule.mode == GBT_SAMPLE_SGB, goss = rule.mode == GBT_SAMPLE_GOSS;
+    // SGB reads no key: every row's key stands at 0 below T = 1
+    const unsigned long long T = sgb ? 1ull : (unsigned long long)st->T;
     const int32_t e = st->e_key;
     const int64_t tbase = (int64_t)blockIdx.x * kCompactTile;
     // global row r draws word r mod 4 of the Philox block r div 4; when the
@@ -415,8 +424,9 @@ __global__ void __launch_bounds__(256) k_mvs_select(SampleSrc src, const int64_t
         const int64_t i0 = tbase + k * 1024 + 4 * (int64_t)threadIdx.x;
         if (i0 >= n) break;
         const bool full = i0 + 4 <= n;
-        unsigned long long a[4];
-        if (keys && full) {
+        unsigned long long a[4] = {0, 0, 0, 0};
+        if (sgb) {
+        } else if (keys && full) {
             const longlong2 x = *(const longlong2 *)(keys + i0), y = *(const longlong2 *)(keys + i0 + 2);
             a[0] = (unsigned long long)x.x;
             a[1] = (unsigned long long)x.y;
@@ -439,6 +449,7 @@ __global__ void __launch_bounds__(256) k_mvs_select(SampleSrc src, const int64_t
         bool need = false;
 #pragma unroll
         for (int j = 0; j < 4; ++j) need |= (i0 + j < n) && a[j] < T;
+        need = need && !(rule.all_rest && !(rule.mode == GBT_SAMPLE_MVS));
         uint64_t U[4] = {0, 0, 0, 0};
         if (need) {
             const uint64_t g0 = (uint64_t)(row_offset + i0);
@@ -463,7 +474,8 @@ __global__ void __launch_bounds__(256) k_mvs_select(SampleSrc src, const int64_t
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             if (i0 + j >= n) continue;
-            const bool kp = a[j] >= T || __umul64hi(U[j], T) < a[j];
+            const bool drawn = rule.all_rest || U[j] < rule.P;  // SGB, GOSS: the draw passes
+            const bool kp = (sgb || goss) ? (!sgb && a[j] >= T) || drawn : a[j] >= T || __umul64hi(U[j], T) < a[j];
             kb |= (kp ? 1u : 0u) << (8 * j);
             cnt += kp ? 1 : 0;
         }
@@ -501,7 +513,7 @@ __global__ void __launch_bounds__(256)
                     const uint8_t *__restrict__ keep, const int32_t *__restrict__ tile_off,
                     int64_t tile0, int64_t row_lo, int64_t row_hi, const uint4 *__restrict__ words,
                     int32_t row_q4, uint4 *__restrict__ out_page, int32_t *__restrict__ sel,
-                    double2 *__restrict__ gw)
+                    double2 *__restrict__ gw, SampleRule rule)
 {
     __shared__ int32_t lds4[4];
     __shared__ unsigned long long red4[4];
@@ -558,8 +570,11 @@ __global__ void __launch_bounds__(256)
         sel[pos] = (int32_t)i;
         double g, h;
         row_gh<kSrc>(src, i, &g, &h);
-        unsigned long long a = (unsigned long long)(long long)rint(ldexp(mvs_r(g, h, lambda), ek));
-        double w = a >= T ? 1.0 : (double)(long long)T / (double)(long long)a;
+        double w = 1.0;  // SGB
+        if (rule.mode != GBT_SAMPLE_SGB) {
+            unsigned long long a = (unsigned long long)(long long)rint(ldexp(mvs_r(g, h, lambda), ek));
+            w = a >= T ? 1.0 : rule.mode == GBT_SAMPLE_GOSS ? rule.w_rest : (double)(long long)T / (double)(long long)a;
+        }
         double2 v = make_double2(g * w, h * w);
         gw[pos] = v;
         unsigned long long bg = __double_as_longlong(fabs(v.x)), bh = __double_as_longlong(fabs(v.y));
@@ -686,7 +701,8 @@ static int32_t log2_ceil(int64_t v) { return v <= 1 ? 0 : ceil_log2_u64((uint64_
 
 // ------------------------------------------------------------ drivers
 gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
-                         double lambda, int64_t K, SampleState *st, bool skip_closed, bool rmax_done)
+                         double lambda, int64_t K, SampleState *st, bool skip_closed, bool rmax_done,
+                         bool count_mode)
 {
     int32_t l2 = log2_ceil(n);
     unsigned long long *hist = nullptr;
@@ -717,7 +733,7 @@ gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64
         done_dev = (int32_t *)hio_d;
         *done_poll = -1;
     }
-    k_mvs_thresh_init<<<1, 64, 0, c->stream>>>(st, K, done_dev);
+    k_mvs_thresh_init<<<1, 64, 0, c->stream>>>(st, K, done_dev, count_mode ? 1 : 0);
     GBT_LAUNCHED();
     if (done_poll) {
         const auto t0 = std::chrono::steady_clock::now();
@@ -744,7 +760,7 @@ gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64
             k_mvs_radix_hist<kSrcMargin><<<grid, 256, 0, c->stream>>>(src, keys, n, lambda, l2, st, hist,
                                                                       hist + kDigitBuckets);
         GBT_LAUNCHED();
-        k_mvs_radix_decide<<<1, 256, 0, c->stream>>>(st, K, hist, hist + kDigitBuckets);
+        k_mvs_radix_decide<<<1, 256, 0, c->stream>>>(st, K, hist, hist + kDigitBuckets, count_mode ? 1 : 0);
         GBT_LAUNCHED();
     }
     return GBT_OK;
@@ -752,16 +768,16 @@ gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64
 
 gbt_status mvs_select(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
                       double lambda, const SampleState *st, uint64_t seed, uint64_t iteration,
-                      int64_t row_offset, uint8_t *keep, int32_t *tile_cnt)
+                      int64_t row_offset, uint8_t *keep, int32_t *tile_cnt, const SampleRule &rule)
 {
     if (n == 0) return GBT_OK;
     const unsigned grid = (unsigned)((n + kCompactTile - 1) / kCompactTile);
     if (kind == kSrcGpair)
         k_mvs_select<kSrcGpair><<<grid, 256, 0, c->stream>>>(src, keys, n, lambda, st, seed, iteration,
-                                                             row_offset, keep, tile_cnt);
+                                                             row_offset, keep, tile_cnt, rule);
     else
         k_mvs_select<kSrcMargin><<<grid, 256, 0, c->stream>>>(src, keys, n, lambda, st, seed, iteration,
-                                                              row_offset, keep, tile_cnt);
+                                                              row_offset, keep, tile_cnt, rule);
     GBT_LAUNCHED();
     return GBT_OK;
 }
@@ -791,7 +807,7 @@ gbt_status keep_tile_offsets(gbt_ctx *c, int64_t n, int32_t *tile_off, int32_t *
 gbt_status mvs_compact_tiles(gbt_ctx *c, const SampleSrc &src, int kind, int64_t n, double lambda,
                              SampleState *st, const uint8_t *keep, const int32_t *tile_off,
                              int64_t row_lo, int64_t row_hi, const uint32_t *words, int32_t row_words,
-                             uint32_t *out_page, int32_t *sel, double *gw)
+                             uint32_t *out_page, int32_t *sel, double *gw, const SampleRule &rule)
 {
     if (row_hi <= row_lo) return GBT_OK;
     const int64_t t0 = row_lo / kCompactTile, t1 = (row_hi - 1) / kCompactTile + 1;
@@ -799,11 +815,11 @@ gbt_status mvs_compact_tiles(gbt_ctx *c, const SampleSrc &src, int kind, int64_t
     if (kind == kSrcGpair)
         k_compact_tiles<kSrcGpair><<<grid, 256, 0, c->stream>>>(
             src, n, lambda, st, keep, tile_off, t0, row_lo, row_hi, (const uint4 *)words, row_words / 4,
-            (uint4 *)out_page, sel, (double2 *)gw);
+            (uint4 *)out_page, sel, (double2 *)gw, rule);
     else
         k_compact_tiles<kSrcMargin><<<grid, 256, 0, c->stream>>>(
             src, n, lambda, st, keep, tile_off, t0, row_lo, row_hi, (const uint4 *)words, row_words / 4,
-            (uint4 *)out_page, sel, (double2 *)gw);
+            (uint4 *)out_page, sel, (double2 *)gw, rule);
     GBT_LAUNCHED();
     return GBT_OK;
 }

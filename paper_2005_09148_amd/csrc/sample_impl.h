@@ -14,6 +14,18 @@ constexpr int kDigitBuckets = 1 << kDigitBits;
 
 enum { kSrcGpair = 0, kSrcMargin = 1 };
 
+// Which rows a sampler keeps (GBT_SAMPLE_*), given the threshold in the
+// sampling state: MVS keeps a row when its key reaches T* or its draw falls
+// below its key's share of T*; SGB keeps a row when its draw is below P;
+// GOSS keeps the rows whose |g| key reaches the top threshold and any other
+// row whose draw is below P.  all_rest: the draw always passes (p = 1).
+struct SampleRule {
+    int32_t mode;
+    int32_t all_rest;
+    uint64_t P;      // floor(p 2^64), p < 1
+    double w_rest;   // GOSS: the weight of a row outside the top set
+};
+
 // Where the per-row gradient pairs come from: a float pair array, or
 // recomputed from margins and labels (streamed out-of-core data).
 struct SampleSrc {
@@ -76,14 +88,16 @@ gbt_status state_init(gbt_ctx *c, SampleState *st);
 // skip_closed: wait on the host for the closed-form test and launch the
 // radix descent only when it fails (the context's pinned host buffer is
 // used).
+// count_mode (GOSS): K is the top count A, and T in st becomes the A-th
+// largest key (INT64_MAX when A = 0) instead of the MVS threshold.
 gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
                          double lambda, int64_t K, SampleState *st, bool skip_closed,
-                         bool rmax_done = false);
+                         bool rmax_done = false, bool count_mode = false);
 // Keep flags of rows [0, n) and, when tile_cnt is given, the kept count of
 // each tile of kCompactTile rows.
 gbt_status mvs_select(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
                       double lambda, const SampleState *st, uint64_t seed, uint64_t iteration,
-                      int64_t row_offset, uint8_t *keep, int32_t *tile_cnt);
+                      int64_t row_offset, uint8_t *keep, int32_t *tile_cnt, const SampleRule &rule);
 gbt_status gw_all(gbt_ctx *c, const float *gpair, int64_t n, double *gw);
 // fx_max_done: the maxima of |g'| and |h'| are already in st (fused upstream)
 gbt_status fixed_point(gbt_ctx *c, const double *gw, int64_t R, SampleState *st, int64_t *q,
@@ -101,6 +115,6 @@ gbt_status keep_tile_offsets(gbt_ctx *c, int64_t n, int32_t *tile_off, int32_t *
 gbt_status mvs_compact_tiles(gbt_ctx *c, const SampleSrc &src, int kind, int64_t n, double lambda,
                              SampleState *st, const uint8_t *keep, const int32_t *tile_off,
                              int64_t row_lo, int64_t row_hi, const uint32_t *words, int32_t row_words,
-                             uint32_t *out_page, int32_t *sel, double *gw);
+                             uint32_t *out_page, int32_t *sel, double *gw, const SampleRule &rule);
 
 }  // namespace gbt

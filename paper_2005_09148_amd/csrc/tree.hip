@@ -4,6 +4,7 @@
 // stream, double buffered and overlapped with the kernels that consume them.
 #include <algorithm>
 #include <chrono>
+#include <cmath>
 #include <cstring>
 #include <functional>
 
@@ -133,6 +134,12 @@ struct SampleOut {
     SampleState *st = nullptr;
 };
 
+// The lambda of the sampling keys: 0 for GOSS (keys are |g|).
+static double sample_lambda(const gbt_sample_params &sp)
+{
+    return sp.sampler == GBT_SAMPLE_GOSS && sp.f < 1.0 ? 0.0 : sp.mvs_lambda;
+}
+
 // Alg. 7: g' <- Sample(g); AllocateOnGPU(sampled_page); Compact each page.
 // st_ready: the caller has initialized st and folded the maximum of r into
 // it while computing the gradients.  read_state: copy the threshold,
@@ -144,6 +151,13 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
 {
     const int64_t n = mx->n_rows;
     GBT_CHECK(sp.f > 0.0 && sp.f <= 1.0, "sampling fraction %g outside (0, 1]", sp.f);
+    GBT_CHECK(sp.sampler >= GBT_SAMPLE_MVS && sp.sampler <= GBT_SAMPLE_GOSS, "unknown sampler %d", sp.sampler);
+    GBT_CHECK(sp.sampler != GBT_SAMPLE_GOSS || sp.f >= 1.0 ||
+                  (sp.goss_a >= 0.0 && sp.goss_a < 1.0 && sp.f - sp.goss_a > 0.0),
+              "GOSS needs 0 <= a < 1 and a < f (a = %g, f = %g)", sp.goss_a, sp.f);
+    // GOSS ranks rows by |g|: its keys are the MVS keys with lambda = 0
+    const double lam = sample_lambda(sp);
+    SampleRule rule{GBT_SAMPLE_MVS, 0, 0, 1.0};
     GBT_CHECK(gpair || (margin && label), "sampling needs gradient pairs or margins and labels");
     SampleState *st = st_ready;
     if (!st) {
@@ -168,12 +182,21 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
         const int64_t ntiles = (n + kCompactTile - 1) / kCompactTile;
         GBT_TRY(bufs.get(kScrFlags, (size_t)std::max<int64_t>(n, 16) + 16, (void **)&keep));
         GBT_TRY(bufs.get(kScrPos, (size_t)(ntiles + 1) * 4, (void **)&tile_off));
-        if (sp.f < 1.0) {
+        // a draw passes with probability p < 1 when U < floor(p 2^64)
+        auto draw_limit = [](double p) -> uint64_t { return (uint64_t)std::ldexp(p, 64); };
+        if (sp.f < 1.0 && sp.sampler == GBT_SAMPLE_SGB) {
+            rule = SampleRule{GBT_SAMPLE_SGB, 0, draw_limit(sp.f), 1.0};
+        } else if (sp.f < 1.0 && sp.sampler == GBT_SAMPLE_GOSS) {
+            const double a = sp.goss_a, b = sp.f - sp.goss_a, p = b / (1.0 - a);
+            o->K = std::min<int64_t>(n, std::max<int64_t>(0, (int64_t)std::nearbyint(a * (double)n)));
+            GBT_TRY(mvs_threshold(c, src, kind, nullptr, n, lam, o->K, st, true, st_ready != nullptr, true));
+            rule = SampleRule{GBT_SAMPLE_GOSS, p >= 1.0 ? 1 : 0, p >= 1.0 ? 0 : draw_limit(p), (1.0 - a) / b};
+        } else if (sp.f < 1.0) {
             o->K = std::max<int64_t>(1, (int64_t)std::nearbyint(sp.f * (double)n));
-            GBT_TRY(mvs_threshold(c, src, kind, nullptr, n, sp.mvs_lambda, o->K, st, true, st_ready != nullptr));
+            GBT_TRY(mvs_threshold(c, src, kind, nullptr, n, lam, o->K, st, true, st_ready != nullptr));
         }
         // with f = 1 the state keeps T = 0: every row is kept with weight 1
-        GBT_TRY(mvs_select(c, src, kind, nullptr, n, sp.mvs_lambda, st, sp.seed, sp.iteration, 0, keep, tile_off));
+        GBT_TRY(mvs_select(c, src, kind, nullptr, n, lam, st, sp.seed, sp.iteration, 0, keep, tile_off, rule));
         // the sample size sizes the buffers below: one round trip
         void *hio, *hio_d;
         GBT_TRY(host_io(c, 64, &hio, &hio_d));
@@ -189,8 +212,8 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
         GBT_TRY(for_each_chunk(
             c, mx,
             [&](const uint32_t *words, int64_t row0, int64_t rows) -> gbt_status {
-                return mvs_compact_tiles(c, src, kind, n, sp.mvs_lambda, st, keep, tile_off, row0, row0 + rows,
-                                         words, mx->row_words, spage, o->sel, o->gw);
+                return mvs_compact_tiles(c, src, kind, n, lam, st, keep, tile_off, row0, row0 + rows,
+                                         words, mx->row_words, spage, o->sel, o->gw, rule);
             },
             h2d_bytes));
         fx_max_done = true;
@@ -857,19 +880,19 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     int mark = timer_begin(c, kPhSample);
     float *gpair = nullptr;
     SampleState *st_ready = nullptr;
+    const gbt_sample_params sp{p->f, p->mvs_lambda, p->seed, p->iteration, p->loss, p->sampler, p->goss_a};
     if (!host_pages) {
         GBT_TRY(scratch_t(c, kScrGpair, (size_t)std::max<int64_t>(n, 1) * 2, &gpair));
         if (p->f < 1.0) {
             // the gradient pass also folds the maximum of r for the sampling keys
             GBT_TRY(scratch_t(c, kScrState, 1, &st_ready));
             GBT_TRY(state_init(c, st_ready));
-            GBT_TRY(gradients_rmax(c, p->loss, margin, label, n, gpair, p->mvs_lambda, st_ready));
+            GBT_TRY(gradients_rmax(c, p->loss, margin, label, n, gpair, sample_lambda(sp), st_ready));
         } else {
             GBT_TRY(launch_gradients(c, p->loss, margin, label, nullptr, n, gpair));
         }
     }
     Buffers bufs{c, false, {}};
-    gbt_sample_params sp{p->f, p->mvs_lambda, p->seed, p->iteration, p->loss, 0};
     SampleOut so;
     GBT_TRY(sample_run(c, mx, gpair, margin, label, sp, bufs, &so, &h2d, st_ready, false));
     timer_end(c, mark);

@@ -32,6 +32,9 @@ HOME_DEVICE = 0
 HOME_PINNED_HOST = 1
 LOSS_LOGISTIC = 0
 LOSS_SQUARED = 1
+SAMPLE_MVS = 0
+SAMPLE_SGB = 1
+SAMPLE_GOSS = 2
 NODE_PRESENT = 1
 NODE_LEAF = 2
 NODE_DEFAULT_LEFT = 4
@@ -67,7 +70,8 @@ class TrainParams(C.Structure):
     _fields_ = [("loss", C.c_int32), ("max_depth", C.c_int32), ("eta", C.c_double),
                 ("lambda_", C.c_double), ("gamma", C.c_double), ("min_child_weight", C.c_double),
                 ("f", C.c_double), ("mvs_lambda", C.c_double), ("seed", C.c_uint64),
-                ("iteration", C.c_uint64)]
+                ("iteration", C.c_uint64), ("sampler", C.c_int32), ("pad0", C.c_int32),
+                ("goss_a", C.c_double)]
 
 
 class Seg(C.Structure):
@@ -112,7 +116,8 @@ class TreeStats(C.Structure):
 
 class SampleParams(C.Structure):
     _fields_ = [("f", C.c_double), ("mvs_lambda", C.c_double), ("seed", C.c_uint64),
-                ("iteration", C.c_uint64), ("loss", C.c_int32), ("pad0", C.c_int32)]
+                ("iteration", C.c_uint64), ("loss", C.c_int32), ("sampler", C.c_int32),
+                ("goss_a", C.c_double)]
 
 
 class SampledInfo(C.Structure):
@@ -463,10 +468,10 @@ class SampleResult:
 
 
 def gbt_sample(ctx, matrix: Matrix, gpair=None, margin=None, label=None, f=1.0, mvs_lambda=1.0,
-               seed=0, iteration=0, loss=LOSS_LOGISTIC, keep_handle=False):
+               seed=0, iteration=0, loss=LOSS_LOGISTIC, keep_handle=False, sampler=SAMPLE_MVS, goss_a=0.0):
     """Alg. 7 sampling + compaction; returns copies of the sampled arrays."""
     torch = _torch()
-    sp = SampleParams(f, mvs_lambda, seed, iteration, loss, 0)
+    sp = SampleParams(f, mvs_lambda, seed, iteration, loss, sampler, goss_a)
     h = C.c_void_p()
     _check(_lib.gbt_sample(ctx.h, matrix.h, _ptr(gpair), _ptr(margin), _ptr(label),
                            C.byref(sp), C.byref(h)))
@@ -496,9 +501,10 @@ def gbt_build_hist(ctx, matrix: Matrix, page, q, rows, build, sub=(), parent_his
 
 
 def make_train_params(loss=LOSS_LOGISTIC, max_depth=6, eta=0.3, lambda_=1.0, gamma=0.0,
-                      min_child_weight=1.0, f=1.0, mvs_lambda=1.0, seed=0, iteration=0):
+                      min_child_weight=1.0, f=1.0, mvs_lambda=1.0, seed=0, iteration=0,
+                      sampler=SAMPLE_MVS, goss_a=0.0):
     return TrainParams(loss, max_depth, eta, lambda_, gamma, min_child_weight, f, mvs_lambda,
-                       seed, iteration)
+                       seed, iteration, sampler, 0, goss_a)
 
 
 def gbt_eval_splits(ctx, matrix: Matrix, hist, node_sums, slots, params: TrainParams, e_g, e_h):

@@ -220,6 +220,66 @@ def test_sample(gbt, ctx, f, kind):
         assert same_bits(r.q.cpu().numpy(), q)
 
 
+def oracle_sample_other(gp, f, sampler, a, seed, it):
+    """SGB / GOSS selection, weights and fixed point from the oracle."""
+    n = len(gp)
+    if sampler == orc.SAMPLE_SGB:
+        keep = orc.sgb_select(n, f, seed, it)
+        sel = np.nonzero(keep)[0]
+        w = np.ones(len(sel))
+        t, A = 0, 0
+    else:
+        keys, _ = orc.mvs_keys(gp, 0.0)
+        A = orc.goss_top_count(a, n)
+        t = orc.goss_top_threshold(keys, A)
+        keep = orc.goss_select(keys, t, a, f - a, seed, it)
+        sel = np.nonzero(keep)[0]
+        w = np.array([orc.goss_weight(int(keys[i]), t, a, f - a) for i in sel], np.float64)
+    gw = gp[sel].astype(np.float64) * w[:, None]
+    q, eg, eh = orc.fixed_point(gw.reshape(-1, 2)) if len(sel) else (np.zeros((0, 2), np.int64), 60, 60)
+    return sel, t, A, gw, q, eg, eh
+
+
+@pytest.mark.parametrize("sampler,f,a,kind", [(1, 0.5, 0.0, "normal"), (1, 0.1, 0.0, "normal"),
+                                              (2, 0.2, 0.1, "normal"), (2, 0.3, 0.0, "normal"),
+                                              (2, 0.15, 0.05, "ties"), (2, 0.999, 0.5, "normal"),
+                                              (2, 1.0 - 1e-9, 0.2, "normal")])
+def test_sample_sgb_goss(gbt, ctx, sampler, f, a, kind):
+    rng = np.random.default_rng(24)
+    n, m = 20_011, 9
+    X = dense_case(25, n, m, 0.1)
+    _, _, _, page = oracle_quantize(X, 256)
+    mx = gbt.gbt_quantize(ctx, X, max_bin=256)
+    if kind == "ties":
+        gp = np.stack([rng.integers(-3, 4, n) * 0.25, rng.uniform(0.01, 0.25, n)], 1)
+    else:
+        gp = np.stack([rng.normal(size=n), rng.uniform(0.01, 0.25, n)], 1)
+    gp = gp.astype(np.float32)
+    seed, it = 13, 6
+    sel, t, A, gw, q, eg, eh = oracle_sample_other(gp, f, sampler, a, seed, it)
+    # the MVS lambda does not enter GOSS's keys: pass a large one
+    r = gbt.gbt_sample(ctx, mx, gpair=torch.from_numpy(gp).cuda(), f=f, mvs_lambda=5.0, seed=seed,
+                       iteration=it, sampler=sampler, goss_a=a)
+    assert r.info.n_sampled == len(sel)
+    if sampler == orc.SAMPLE_GOSS:
+        assert r.info.threshold == t and r.info.target == A
+    assert same_bits(r.rows.cpu().numpy(), sel.astype(np.int32))
+    assert same_bits(r.page.cpu().numpy().view(np.uint32), page[sel])
+    assert same_bits(r.gw.cpu().numpy(), gw)
+    if len(sel):
+        assert (r.info.exp_g, r.info.exp_h) == (eg, eh)
+        assert same_bits(r.q.cpu().numpy(), q)
+
+
+def test_goss_rejects_bad_fractions(gbt, ctx):
+    X = dense_case(26, 1000, 3, 0.0)
+    mx = gbt.gbt_quantize(ctx, X, max_bin=16)
+    gp = torch.zeros((1000, 2), dtype=torch.float32, device="cuda")
+    for f, a in [(0.2, 0.2), (0.2, 0.3), (0.5, -0.1)]:
+        with pytest.raises(RuntimeError, match="GOSS"):
+            gbt.gbt_sample(ctx, mx, gpair=gp, f=f, sampler=gbt.SAMPLE_GOSS, goss_a=a)
+
+
 def test_sample_from_margins_matches_stored_gradients(gbt, ctx):
     rng = np.random.default_rng(22)
     n = 30_000
@@ -489,6 +549,31 @@ def test_sparse_trees_sampling_and_long_rows(gbt, ctx, f, dense_row):
     assert_same_trees(*r[:4])
     if dense_row:
         assert r[4].info().stride == 300
+
+
+@pytest.mark.parametrize("sampler,f,a,pages", [(1, 0.4, 0.0, False), (2, 0.2, 0.1, False),
+                                               (2, 0.25, 0.05, True), (1, 0.3, 0.0, True)])
+def test_trees_sgb_goss_match_oracle(gbt, ctx, sampler, f, a, pages):
+    # whole iterations with the SGB and GOSS samplers, in HBM and from
+    # pinned-host pages (gradients recomputed while the pages stream)
+    d = datagen.config2(n=20_000)
+    cfg = datagen.TrainConfig("t", 0, 256, 6, 3, eta=0.1, f=f, mvs_lambda=3.0)
+    mb = cfg.max_bin
+    c = ctx
+    kw = dict(page_rows=3000, page_home=gbt.HOME_PINNED_HOST) if pages else {}
+    mx = gbt.gbt_quantize(c, d["X"], max_bin=mb, **kw)
+    P = gbt.make_train_params(loss=cfg.loss, max_depth=cfg.max_depth, eta=cfg.eta, f=f, mvs_lambda=3.0,
+                              seed=4, sampler=sampler, goss_a=a)
+    trees, margin = gbt.train(c, mx, torch.from_numpy(d["y"]).cuda(), P, 3, 0.0)
+    _, b, _, _ = oracle_quantize(d["X"], mb)
+    OP = orc.Params(loss=cfg.loss, max_depth=cfg.max_depth, eta=cfg.eta, f=f, mvs_lambda=3.0, seed=4,
+                    sampler=sampler, goss_a=a)
+    otrees, omargin = orc.train(b, d["y"], OP, 3, 0.0)
+    assert_same_trees(trees, margin.cpu().numpy(), otrees, omargin)
+    # (GOSS keeps every row of the first tree: from a zero margin all |g|
+    # are equal, and ties at the top threshold are kept)
+    assert all(0 < t.stats.n_sampled <= 20_000 for t in trees)
+    assert trees[-1].stats.n_sampled < 20_000
 
 
 def test_trees_many_partition_tiles(gbt, ctx):
