@@ -133,6 +133,10 @@ def parse():
     ap.add_argument("--hist-kernel", default="auto", choices=["auto", "plain", "rotated"],
                     help="dense histogram kernel (auto: the library's choice by pass size)")
     ap.add_argument("--cpu-trees", type=int, default=2)
+    ap.add_argument("--sampler", default="mvs", choices=["mvs", "sgb", "goss"],
+                    help="the sampler used when f < 1 (Sec. 2.3-2.4)")
+    ap.add_argument("--goss-a", type=float, default=0.05,
+                    help="GOSS top fraction a (the rest fraction is f - a)")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="summarize two rocprofv3 --pmc runs of this script (no GPU work)")
     ap.add_argument("--pmc-commands", nargs="*", default=[], help="the commands of those runs")
@@ -172,7 +176,7 @@ def oracle_updates(b, res, depth):
     return int((nonnull * levels).sum())
 
 
-def cpu_baseline(X, y, cfg, n_trees, gpu_trees, gpu_updates):
+def cpu_baseline(X, y, cfg, n_trees, gpu_trees, gpu_updates, sampler=(0, 0.0)):
     """Times the oracle on the first n_trees iterations of the same workload.
     Updates per tree: counted from the oracle's tree for dense data; for CSR
     data the GPU's count of the same (identical) tree."""
@@ -188,7 +192,7 @@ def cpu_baseline(X, y, cfg, n_trees, gpu_trees, gpu_updates):
     prep = time.perf_counter() - t0
     P = orc.Params(loss=cfg.loss, max_depth=cfg.max_depth, eta=cfg.eta, lambda_=cfg.lambda_,
                    gamma=cfg.gamma, min_child_weight=cfg.min_child_weight, f=cfg.f,
-                   mvs_lambda=cfg.mvs_lambda, seed=cfg.seed)
+                   mvs_lambda=cfg.mvs_lambda, seed=cfg.seed, sampler=sampler[0], goss_a=sampler[1])
     margin = np.full(len(y), cfg.base_margin, np.float32)
     secs, updates, same = 0.0, 0, True
     if b.sparse:  # the update count comes from the GPU's identical trees
@@ -337,7 +341,8 @@ def workload_key(args):
     n = args.rows or datagen.FULL_ROWS[cfg_id]
     f = args.f if args.f is not None else datagen.CONFIGS[cfg_id].f
     m = {1: 28, 2: 28, 3: 50, 5: 2000}[cfg_id]
-    return f"{args.workload if args.workload in INHBM else 'regression'}_{n}x{m}_f{f:g}"
+    smp = "" if args.sampler == "mvs" or f >= 1 else f"_{args.sampler}"
+    return f"{args.workload if args.workload in INHBM else 'regression'}_{n}x{m}_f{f:g}{smp}"
 
 
 def main():
@@ -377,10 +382,12 @@ def main():
           f"row_words={info.row_words} total_bins={info.total_bins}", file=sys.stderr, flush=True)
     label = torch.from_numpy(y).cuda()
     margin = torch.full((n,), cfg.base_margin, dtype=torch.float32, device="cuda")
+    sampler = ({"mvs": gbt.SAMPLE_MVS, "sgb": gbt.SAMPLE_SGB, "goss": gbt.SAMPLE_GOSS}[args.sampler],
+               args.goss_a if args.sampler == "goss" else 0.0)
     P = gbt.make_train_params(loss=cfg.loss, max_depth=cfg.max_depth, eta=cfg.eta,
                               lambda_=cfg.lambda_, gamma=cfg.gamma,
                               min_child_weight=cfg.min_child_weight, f=cfg.f,
-                              mvs_lambda=cfg.mvs_lambda, seed=cfg.seed)
+                              mvs_lambda=cfg.mvs_lambda, seed=cfg.seed, sampler=sampler[0], goss_a=sampler[1])
     ctx.set_timing(0)
     first_trees, first_updates = [], []
     for w in range(args.warmup):
@@ -420,6 +427,15 @@ def main():
         P.iteration = args.warmup + 2 * args.steps + k
         pstats.append(gbt.gbt_train_tree(ctx, mx, label, margin, P).stats)
     ctx.set_timing(0)
+    # the training loss after every tree of this run (warm-up, timed, event
+    # and phase trees), for comparing samplers
+    with torch.no_grad():
+        if cfg.loss == gbt.LOSS_SQUARED:
+            train_loss = float(((margin.double() - label.double()) ** 2).mean() / 2)
+        else:
+            z = margin.double()
+            train_loss = float((torch.nn.functional.softplus(z) - label.double() * z).mean())
+    n_trees_run = args.warmup + 2 * args.steps + 3
     # counter calibration: one plain device-to-device copy of known size
     src = torch.empty(CALIB_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
     dst = torch.empty_like(src)
@@ -448,12 +464,15 @@ def main():
         "vs_baseline": None,
         "dtype": "int64",
         "data": "synthetic",
-        "config": {"workload": desc.format(n=n, f=cfg.f),
+        "config": {"workload": desc.format(n=n, f=cfg.f) + ("" if args.sampler == "mvs" or cfg.f >= 1
+                                                              else f", {args.sampler.upper()} sampler"),
                    "rows": n, "features": m, "max_bin": cfg.max_bin, "max_depth": cfg.max_depth,
-                   "f": cfg.f},
+                   "f": cfg.f, "sampler": args.sampler if cfg.f < 1 else "none",
+                   **({"goss_a": args.goss_a} if args.sampler == "goss" and cfg.f < 1 else {})},
         "sec_per_tree": round(dt / args.steps, 6),
         "rows_sampled_per_tree": round(sum(s.n_sampled for s in stats) / args.steps),
         "hist_updates_per_tree": upd // args.steps,
+        "train_loss_after": {"trees": n_trees_run, "loss": round(train_loss, 6)},
         "phase_ms_per_tree_untimed_run": phases,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
@@ -465,7 +484,7 @@ def main():
                                f"trees ({round(dt_ev * 1e3 / args.steps, 4)} ms per tree with the events)"},
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(X, y, cfg, args.cpu_trees, first_trees, first_updates)
+        line["cpu_baseline"] = cpu_baseline(X, y, cfg, args.cpu_trees, first_trees, first_updates, sampler)
     print(json.dumps(line), flush=True)
 
 

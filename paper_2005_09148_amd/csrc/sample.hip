@@ -351,19 +351,61 @@ __global__ void __launch_bounds__(256) k_mvs_radix_decide(SampleState *__restric
     const int32_t nb = st->nbuckets;
     const int shift = st->shift;
     const unsigned long long lo = (unsigned long long)st->lo;
-    if (threadIdx.x == 0) {
-        // serial prefix/suffix over at most 2048 buckets
-        unsigned long long f = st->F_below;
-        for (int b = 0; b <= nb; ++b) {
-            s_f[b] = f;
-            if (b < nb) f += hsum[b];
+    // s_f[b] = F_below + the key sums of buckets below b; s_c[b] = C_above +
+    // the counts of buckets b and above (b = 0..nb): each thread takes a run
+    // of kPer buckets, the block scans the runs' totals
+    constexpr int kPer = (kDigitBuckets + 255) / 256;
+    __shared__ unsigned long long s_wf[4], s_wc[4];
+    const int b0 = (int)threadIdx.x * kPer;
+    unsigned long long cnt[kPer], sum[kPer], rf = 0, rc = 0;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+        const int b = b0 + j;
+        cnt[j] = b < nb ? hcnt[b] : 0ull;
+        sum[j] = b < nb ? hsum[b] : 0ull;
+        rf += sum[j];
+        rc += cnt[j];
+    }
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    unsigned long long xf = rf, xc = rc;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const unsigned long long yf = __shfl_up(xf, d, 64), yc = __shfl_up(xc, d, 64);
+        if (lane >= d) {
+            xf += yf;
+            xc += yc;
         }
-        unsigned long long cabove = st->C_above;
-        for (int b = nb; b >= 0; --b) {
-            s_c[b] = cabove;
-            if (b > 0) cabove += hcnt[b - 1];
+    }
+    if (lane == 63) {
+        s_wf[wid] = xf;
+        s_wc[wid] = xc;
+    }
+    if (threadIdx.x == 0) s_best = nb + 1;
+    __syncthreads();
+    unsigned long long pf = xf - rf, pc = xc - rc, ctot = 0, ftot = 0;  // exclusive prefixes; totals
+    for (int w = 0; w < 4; ++w) {
+        if (w < wid) {
+            pf += s_wf[w];
+            pc += s_wc[w];
         }
-        s_best = nb + 1;
+        ctot += s_wc[w];
+        ftot += s_wf[w];
+    }
+    const unsigned long long F0 = st->F_below, C0 = st->C_above;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+        const int b = b0 + j;
+        if (b <= nb) {
+            s_f[b] = F0 + pf;
+            s_c[b] = C0 + (ctot - pc);
+        }
+        pf += sum[j];
+        pc += cnt[j];
+    }
+    // the boundary past the last bucket, when the runs end before it
+    if (threadIdx.x == 0 && nb >= 256 * kPer) {
+        s_f[nb] = F0 + ftot;
+        s_c[nb] = C0;
     }
     __syncthreads();
     for (int b = threadIdx.x; b <= nb; b += blockDim.x) {
