@@ -51,7 +51,7 @@ typedef int32_t gbt_status;
 #define GBT_SAMPLE_SGB 1  /* stochastic gradient boosting: uniform rows */
 #define GBT_SAMPLE_GOSS 2 /* gradient-based one-side sampling */
 
-#define GBT_ABI_VERSION 1
+#define GBT_ABI_VERSION 2
 
 enum { GBT_INPUT_DENSE_F32 = 0, GBT_INPUT_CSR_F32 = 1 };
 enum { GBT_LOC_HOST = 0, GBT_LOC_DEVICE = 1 };
@@ -370,6 +370,19 @@ gbt_status gbt_update_leaves(gbt_ctx *ctx, gbt_tree *tree, const gbt_train_param
 gbt_status gbt_train_tree(gbt_ctx *ctx, const gbt_matrix *data, const float *label_d,
                           float *margin_d, const gbt_train_params *p, gbt_tree *tree,
                           gbt_tree_stats *stats);
+
+/* ---- Alg. 6: the naive out-of-core tree construction (Sec. 3.3) ------------
+ * A measured negative baseline, not the path to use: every row trains
+ * (p->f must be 1) and each level streams every page of `data` once,
+ * moving each row to its node and building the histograms of all of the
+ * level's nodes from each chunk (no sibling subtraction, since no page stays
+ * on the device); one last pass moves the rows to the leaves, whose ids
+ * give the margin update.  Tree, margins and stats as gbt_train_tree's with
+ * f = 1 (the same tree, bit for bit); p->max_depth <= 11.  Holds a node id
+ * (4 bytes) and the fixed-point pair (16 bytes) of every row on the device. */
+gbt_status gbt_train_tree_naive(gbt_ctx *ctx, const gbt_matrix *data, const float *label_d,
+                                float *margin_d, const gbt_train_params *params, gbt_tree *tree_out,
+                                gbt_tree_stats *stats);
 
 /* ---- Eq. 1 prediction -------------------------------------------------------
  * margin_out_d[i] = base_margin + sum_t leaf(tree t, row i), in float, tree

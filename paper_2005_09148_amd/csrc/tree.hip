@@ -1266,6 +1266,329 @@ gbt_status gbt_sampled_free(gbt_sampled *s)
     return GBT_OK;
 }
 
+// ------------------------------------------------------------ Alg. 6
+// The naive out-of-core construction (Sec. 3.3), a measured negative
+// baseline: every row trains and every level streams every page once.  A
+// level's pass moves each row to its node (the row's node id is kept for all
+// n rows), groups the chunk's rows by the level's nodes and builds every
+// node's histogram from them (both children: no page stays resident, so a
+// parent's histogram cannot be reused across passes).  One last pass moves
+// the rows to the leaves, whose ids give the margin update.
+constexpr int32_t kNaiveMaxDepth = 11;  // at most 2048 nodes per level (LDS counts)
+constexpr int32_t kNaiveSlots = 1 << kNaiveMaxDepth;
+
+// Route the chunk's rows one level down (when `move`) and count them per
+// node slot of the current level (slot_of: heap id -> slot, -1 outside it).
+__global__ void __launch_bounds__(256)
+    k_naive_route(const uint32_t *__restrict__ words, int64_t rows, int64_t row0, Geo geo,
+                  const DevNode *__restrict__ nodes, int32_t *__restrict__ position,
+                  const int32_t *__restrict__ slot_of, int32_t n_slots, int32_t move, uint32_t *__restrict__ cnt)
+{
+    __shared__ uint32_t lc[kNaiveSlots];
+    for (int32_t s = threadIdx.x; s < n_slots; s += 256) lc[s] = 0;
+    __syncthreads();
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < rows) {
+        int32_t p = position[row0 + i];
+        if (move) {
+            const int4 rec = *(const int4 *)&nodes[p].split;
+            if (rec.x) {
+                const int32_t b = row_feature_bin(words + i * geo.row_words, geo, rec.y);
+                const bool left = b < 0 ? rec.w != 0 : b < rec.z;
+                p = left ? nodes[p].left_child : nodes[p].right_child;
+                position[row0 + i] = p;
+            }
+        }
+        const int32_t s = slot_of[p];
+        if (s >= 0) atomicAdd(&lc[s], 1u);
+    }
+    __syncthreads();
+    for (int32_t s = threadIdx.x; s < n_slots; s += 256)
+        if (lc[s]) atomicAdd(&cnt[s], lc[s]);
+}
+
+// The chunk's rows grouped by slot: a block ranks its rows per slot in LDS,
+// reserves each slot's range with one atomic, and writes the local row ids.
+__global__ void __launch_bounds__(256)
+    k_naive_group(int64_t rows, int64_t row0, const int32_t *__restrict__ position,
+                  const int32_t *__restrict__ slot_of, int32_t n_slots, uint32_t *__restrict__ cursor,
+                  int32_t *__restrict__ grouped)
+{
+    __shared__ uint32_t lc[kNaiveSlots];
+    __shared__ uint32_t base[kNaiveSlots];
+    for (int32_t s = threadIdx.x; s < n_slots; s += 256) lc[s] = 0;
+    __syncthreads();
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    int32_t s = -1;
+    uint32_t rank = 0;
+    if (i < rows) {
+        s = slot_of[position[row0 + i]];
+        if (s >= 0) rank = atomicAdd(&lc[s], 1u);
+    }
+    __syncthreads();
+    for (int32_t t = threadIdx.x; t < n_slots; t += 256) base[t] = lc[t] ? atomicAdd(&cursor[t], lc[t]) : 0u;
+    __syncthreads();
+    if (s >= 0) grouped[base[s] + rank] = (int32_t)i;
+}
+
+// hist[slot] += part[slot] for the listed slots.
+__global__ void k_naive_accumulate(longlong2 *__restrict__ hist, const longlong2 *__restrict__ part,
+                                   const int32_t *__restrict__ slots, int32_t n, int64_t tb)
+{
+    const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= tb) return;
+    const int64_t s = slots[blockIdx.y];
+    longlong2 h = hist[s * tb + b];
+    const longlong2 v = part[s * tb + b];
+    h.x += v.x;
+    h.y += v.y;
+    hist[s * tb + b] = h;
+}
+
+// margin[r] += leaf of the row's final node.
+__global__ void k_naive_margin(float *__restrict__ margin, const int32_t *__restrict__ position,
+                               const float *__restrict__ leaf, int64_t n)
+{
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r < n) margin[r] += leaf[position[r]];
+}
+
+__global__ void k_naive_zero(unsigned long long *__restrict__ p, int64_t n)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0ull;
+}
+
+__global__ void k_fill_i32(int32_t *__restrict__ p, int64_t n, int32_t v)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+static gbt_status train_tree_naive_impl(gbt_ctx *c, const gbt_matrix *mx, const float *label, float *margin,
+                                        const gbt_train_params *p, gbt_tree *tree, gbt_tree_stats *stats)
+{
+    const int64_t n = mx->n_rows;
+    const int32_t D = p->max_depth;
+    const int32_t NN = (1 << (D + 1)) - 1;
+    const int64_t tb = mx->total_bins;
+    double h2d = 0.0;
+    c->marks.clear();
+    c->events_used = 0;
+    // gradients and their exact fixed point over all n rows (no sampling)
+    int mark = timer_begin(c, kPhSample);
+    float *gpair;
+    double *gw;
+    int64_t *q;
+    SampleState *st;
+    GBT_TRY(scratch_t(c, kScrGpair, (size_t)std::max<int64_t>(n, 1) * 2, &gpair));
+    GBT_TRY(scratch_t(c, kScrGw, (size_t)std::max<int64_t>(n, 1) * 2, &gw));
+    GBT_TRY(scratch_t(c, kScrQ, (size_t)std::max<int64_t>(n, 1) * 2, &q));
+    GBT_TRY(scratch_t(c, kScrState, 1, &st));
+    GBT_TRY(state_init(c, st));
+    GBT_TRY(launch_gradients(c, p->loss, margin, label, nullptr, n, gpair));
+    GBT_TRY(gw_all(c, gpair, n, gw));
+    GBT_TRY(fixed_point(c, gw, n, st, q, false));
+    SampleState hst;
+    GBT_HIP(hipMemcpyAsync(&hst, st, sizeof(SampleState), hipMemcpyDeviceToHost, c->stream));
+    GBT_HIP(hipStreamSynchronize(c->stream));
+    timer_end(c, mark);
+    // the node table on the host (uploaded each level), each row's node
+    std::vector<DevNode> hn((size_t)NN);
+    for (int32_t i = 0; i < NN; ++i) {
+        memset(&hn[i], 0, sizeof(DevNode));
+        hn[i].left_child = 2 * i + 1;
+        hn[i].right_child = 2 * i + 2;
+    }
+    hn[0].present = 1;
+    hn[0].sum_g = (long long)fold_sum(hst.root_g);
+    hn[0].sum_h = (long long)fold_sum(hst.root_h);
+    hn[0].end = n;
+    DevNode *nodes;
+    int32_t *position, *slot_of, *grouped;
+    uint32_t *cnt;
+    gbt_split *splits_d;
+    EvalNode *ev_d;
+    int32_t *slots_d;
+    const int32_t max_level = 1 << D;
+    int64_t chunk_rows = 1;  // the largest chunk for_each_chunk passes
+    for (const auto &pg : mx->pages)
+        chunk_rows = std::max(chunk_rows, pg.host ? std::min(pg.rows, g_stream_chunk_rows) : pg.rows);
+    GBT_TRY(scratch_t(c, kScrNodes, (size_t)NN, &nodes));
+    GBT_TRY(scratch_t(c, kScrPosition, (size_t)std::max<int64_t>(n, 1), &position));
+    GBT_TRY(scratch_t(c, kScrSlotNode, (size_t)NN, &slot_of));
+    GBT_TRY(scratch_t(c, kScrRows, (size_t)chunk_rows, &grouped));
+    GBT_TRY(scratch_t(c, kScrScan, (size_t)2 * max_level, &cnt));
+    GBT_TRY(scratch_t(c, kScrSplits, (size_t)max_level, &splits_d));
+    GBT_TRY(scratch_t(c, kScrEvalNodes, (size_t)max_level, &ev_d));
+    GBT_TRY(scratch_t(c, kScrPlan, (size_t)max_level, &slots_d));
+    int64_t *hist = nullptr, *part = nullptr;
+    if (D > 0) {
+        GBT_TRY(scratch_t(c, kScrHistA, (size_t)max_level * tb * 2, &hist));
+        GBT_TRY(scratch_t(c, kScrHistB, (size_t)max_level * tb * 2, &part));
+    }
+    if (n) {
+        k_fill_i32<<<blocks(n), 256, 0, c->stream>>>(position, n, 0);
+        GBT_LAUNCHED();
+    }
+    const Geo geo = geo_of(mx);
+    const EvalParams ep{p->lambda, p->gamma, p->min_child_weight, 0, 0, &st->e_g};
+    int32_t hist_launches = 0;
+    std::vector<int32_t> level{0}, so((size_t)NN, -1);
+    std::vector<uint32_t> hcnt;
+    for (int32_t d = 0; d <= D && n > 0; ++d) {
+        const int32_t L = (int32_t)level.size();
+        if (L == 0) break;
+        const bool build = d < D;
+        std::fill(so.begin(), so.end(), -1);
+        for (int32_t s = 0; s < L; ++s) so[level[s]] = s;
+        GBT_HIP(hipMemcpyAsync(nodes, hn.data(), (size_t)NN * sizeof(DevNode), hipMemcpyHostToDevice, c->stream));
+        GBT_HIP(hipMemcpyAsync(slot_of, so.data(), (size_t)NN * 4, hipMemcpyHostToDevice, c->stream));
+        if (build) {
+            k_naive_zero<<<blocks((int64_t)L * tb * 2), 256, 0, c->stream>>>((unsigned long long *)hist, (int64_t)L * tb * 2);
+            GBT_LAUNCHED();
+        }
+        std::vector<uint64_t> total((size_t)L, 0);
+        mark = timer_begin(c, kPhHist);
+        GBT_TRY(for_each_chunk(
+            c, mx,
+            [&](const uint32_t *words, int64_t row0, int64_t rows) -> gbt_status {
+                k_naive_zero<<<blocks(L), 256, 0, c->stream>>>((unsigned long long *)cnt, (L + 1) / 2);
+                GBT_LAUNCHED();
+                k_naive_route<<<(unsigned)((rows + 255) / 256), 256, 0, c->stream>>>(
+                    words, rows, row0, geo, nodes, position, slot_of, L, d > 0 ? 1 : 0, cnt);
+                GBT_LAUNCHED();
+                hcnt.assign((size_t)L, 0);
+                GBT_HIP(hipMemcpyAsync(hcnt.data(), cnt, (size_t)L * 4, hipMemcpyDeviceToHost, c->stream));
+                GBT_HIP(hipStreamSynchronize(c->stream));
+                for (int32_t s = 0; s < L; ++s) total[s] += hcnt[s];
+                if (!build) return GBT_OK;
+                // group the chunk's rows by slot and build their histograms
+                std::vector<uint32_t> cur((size_t)L);
+                std::vector<gbt_seg> segs;
+                std::vector<int32_t> built;
+                uint32_t off = 0;
+                for (int32_t s = 0; s < L; ++s) {
+                    cur[s] = off;
+                    if (hcnt[s]) {
+                        segs.push_back(gbt_seg{s, 0, off, off + hcnt[s]});
+                        built.push_back(s);
+                    }
+                    off += hcnt[s];
+                }
+                if (segs.empty()) return GBT_OK;
+                GBT_HIP(hipMemcpyAsync(cnt, cur.data(), (size_t)L * 4, hipMemcpyHostToDevice, c->stream));
+                k_naive_group<<<(unsigned)((rows + 255) / 256), 256, 0, c->stream>>>(rows, row0, position, slot_of,
+                                                                                      L, cnt, grouped);
+                GBT_LAUNCHED();
+                GBT_TRY(build_hist_impl(c, mx, words, q + 2 * row0, grouped, segs.data(), (int32_t)segs.size(),
+                                        nullptr, 0, nullptr, part, nullptr));
+                ++hist_launches;
+                GBT_HIP(hipMemcpyAsync(slots_d, built.data(), built.size() * 4, hipMemcpyHostToDevice, c->stream));
+                dim3 g((unsigned)((tb + 255) / 256), (unsigned)built.size());
+                k_naive_accumulate<<<g, 256, 0, c->stream>>>((longlong2 *)hist, (const longlong2 *)part, slots_d,
+                                                             (int32_t)built.size(), tb);
+                GBT_LAUNCHED();
+                // the host vectors above are read by the copies before this
+                // chunk returns
+                GBT_HIP(hipStreamSynchronize(c->stream));
+                return GBT_OK;
+            },
+            &h2d));
+        timer_end(c, mark);
+        for (int32_t s = 0; s < L; ++s) {
+            hn[level[s]].begin = 0;
+            hn[level[s]].end = (int64_t)total[s];
+        }
+        if (!build) break;
+        // Eq. 8 for every node of the level; the split records land in the
+        // device node table, then come back to the host
+        mark = timer_begin(c, kPhSplit);
+        std::vector<EvalNode> ev((size_t)L);
+        for (int32_t s = 0; s < L; ++s) ev[s] = EvalNode{hn[level[s]].sum_g, hn[level[s]].sum_h, s, level[s]};
+        GBT_HIP(hipMemcpyAsync(ev_d, ev.data(), (size_t)L * sizeof(EvalNode), hipMemcpyHostToDevice, c->stream));
+        GBT_HIP(hipMemcpyAsync(nodes, hn.data(), (size_t)NN * sizeof(DevNode), hipMemcpyHostToDevice, c->stream));
+        GBT_TRY(eval_impl(c, mx, hist, ev_d, L, ep, splits_d, nullptr, nodes));
+        GBT_HIP(hipMemcpyAsync(hn.data(), nodes, (size_t)NN * sizeof(DevNode), hipMemcpyDeviceToHost, c->stream));
+        GBT_HIP(hipStreamSynchronize(c->stream));
+        timer_end(c, mark);
+        std::vector<int32_t> next;
+        for (int32_t s = 0; s < L; ++s) {
+            const DevNode &x = hn[level[s]];
+            if (!x.split) continue;
+            DevNode &l = hn[x.left_child], &r = hn[x.right_child];
+            l.present = r.present = 1;
+            l.sum_g = x.left_g;
+            l.sum_h = x.left_h;
+            r.sum_g = x.right_g;
+            r.sum_h = x.right_h;
+            next.push_back(x.left_child);
+            next.push_back(x.right_child);
+        }
+        // the children's rows move in the next pass
+        level.swap(next);
+        if (level.empty()) break;
+    }
+    // ---- leaves, the margin update of all n rows, the public tree
+    mark = timer_begin(c, kPhMargin);
+    GBT_HIP(hipMemcpyAsync(nodes, hn.data(), (size_t)NN * sizeof(DevNode), hipMemcpyHostToDevice, c->stream));
+    float *leaf;
+    uint2 *compact;
+    GBT_TRY(scratch_t(c, kScrLeaf, (size_t)NN, &leaf));
+    GBT_TRY(scratch_t(c, kScrCompact, (size_t)NN, &compact));
+    k_leaves<<<blocks(NN), 256, 0, c->stream>>>(nodes, NN, &st->e_g, p->lambda, p->eta, leaf, compact);
+    GBT_LAUNCHED();
+    if (n) {
+        k_naive_margin<<<blocks(n), 256, 0, c->stream>>>(margin, position, leaf, n);
+        GBT_LAUNCHED();
+    }
+    timer_end(c, mark);
+    unsigned long long *stat;
+    GBT_TRY(scratch_t(c, kScrWork, 2, &stat));
+    k_naive_zero<<<1, 256, 0, c->stream>>>(stat, 2);
+    GBT_LAUNCHED();
+    void *hio, *hio_d;
+    GBT_TRY(host_io(c, sizeof(TreeResult) + (size_t)NN * sizeof(gbt_node), &hio, &hio_d));
+    k_finalize<<<blocks(NN), 256, 0, c->stream>>>(nodes, NN, leaf, mx->cut_ptr_d, mx->cut_values_d, st, nullptr,
+                                                  stat, (TreeResult *)hio_d);
+    GBT_LAUNCHED();
+    GBT_HIP(hipStreamSynchronize(c->stream));
+    const TreeResult *res = (const TreeResult *)hio;
+    tree->exp_g = res->e_g;
+    tree->exp_h = res->e_h;
+    memcpy(tree->nodes, res->nodes, (size_t)NN * sizeof(gbt_node));
+    double ms[kPhCount] = {0.0};
+    timer_collect(c, ms);
+    if (stats) {
+        stats->n_sampled = n;
+        stats->hist_launches = hist_launches;
+        stats->h2d_bytes = (int64_t)h2d;
+        stats->ms_sample = ms[kPhSample];
+        stats->ms_hist = ms[kPhHist];
+        stats->ms_split = ms[kPhSplit];
+        stats->ms_margin = ms[kPhMargin];
+    }
+    return GBT_OK;
+}
+
+gbt_status gbt_train_tree_naive(gbt_ctx *c, const gbt_matrix *data, const float *label_d, float *margin_d,
+                                const gbt_train_params *p, gbt_tree *tree, gbt_tree_stats *stats)
+{
+    GBT_CHECK(c && data && p && tree && tree->nodes, "gbt_train_tree_naive: NULL argument");
+    GBT_CHECK(data->n_rows == 0 || (label_d && margin_d), "gbt_train_tree_naive: NULL labels/margins");
+    GBT_CHECK(p->max_depth >= 0 && p->max_depth <= kNaiveMaxDepth, "max_depth %d outside [0, %d]", p->max_depth,
+              kNaiveMaxDepth);
+    GBT_CHECK(p->f == 1.0, "the naive construction trains every row (f = 1, got %g)", p->f);
+    GBT_CHECK(p->loss == GBT_LOSS_LOGISTIC || p->loss == GBT_LOSS_SQUARED, "unknown loss %d", p->loss);
+    GBT_CHECK(data->n_rows < ((int64_t)1 << 31) - 1, "more than 2^31-2 rows");
+    const int32_t NN = (1 << (p->max_depth + 1)) - 1;
+    GBT_CHECK(tree->n_nodes >= NN, "tree holds %d nodes, needs %d", tree->n_nodes, NN);
+    tree->max_depth = p->max_depth;
+    if (stats) memset(stats, 0, sizeof(*stats));
+    GBT_TRY(set_device(c));
+    return train_tree_naive_impl(c, data, label_d, margin_d, p, tree, stats);
+}
+
 gbt_status gbt_train_tree(gbt_ctx *c, const gbt_matrix *data, const float *label_d, float *margin_d,
                           const gbt_train_params *p, gbt_tree *tree, gbt_tree_stats *stats)
 {

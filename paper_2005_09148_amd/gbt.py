@@ -159,6 +159,7 @@ SIGNATURES = {
     "gbt_partition": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _i64, _vp, _vp]),
     "gbt_update_leaves": (_i32, [_vp, _vp, _vp, _vp, _vp]),
     "gbt_train_tree": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "gbt_train_tree_naive": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     "gbt_predict": (_i32, [_vp, _vp, _i32, _vp, _vp, _f32, _vp]),
 }
 
@@ -554,6 +555,17 @@ def gbt_train_tree(ctx, matrix: Matrix, label, margin, params: TrainParams, stat
     st = TreeStats() if stats else None
     _check(_lib.gbt_train_tree(ctx.h, matrix.h, _ptr(label), _ptr(margin), C.byref(params),
                                C.byref(t), C.byref(st) if st is not None else None))
+    return TreeOut(nodes, t.exp_g, t.exp_h, params.max_depth, st)
+
+
+def gbt_train_tree_naive(ctx, matrix: Matrix, label, margin, params: TrainParams, stats=True) -> TreeOut:
+    """Alg. 6, the naive out-of-core construction (a negative baseline)."""
+    nn = (1 << (params.max_depth + 1)) - 1
+    nodes = np.zeros(nn, NODE_DTYPE)
+    t = Tree(params.max_depth, nn, 0, 0, nodes.ctypes.data)
+    st = TreeStats() if stats else None
+    _check(_lib.gbt_train_tree_naive(ctx.h, matrix.h, _ptr(label), _ptr(margin), C.byref(params),
+                                     C.byref(t), C.byref(st) if st is not None else None))
     return TreeOut(nodes, t.exp_g, t.exp_h, params.max_depth, st)
 
 

@@ -576,6 +576,51 @@ def test_trees_sgb_goss_match_oracle(gbt, ctx, sampler, f, a, pages):
     assert trees[-1].stats.n_sampled < 20_000
 
 
+def train_naive(gbt, c, mx, y, cfg, n_trees):
+    P = gbt.make_train_params(loss=cfg.loss, max_depth=cfg.max_depth, eta=cfg.eta, lambda_=cfg.lambda_,
+                              gamma=cfg.gamma, min_child_weight=cfg.min_child_weight, f=1.0, seed=cfg.seed)
+    margin = torch.full((len(y),), cfg.base_margin, dtype=torch.float32, device="cuda")
+    label = torch.from_numpy(y).cuda()
+    trees = []
+    for t in range(n_trees):
+        P.iteration = t
+        trees.append(gbt.gbt_train_tree_naive(c, mx, label, margin, P))
+    return trees, margin
+
+
+@pytest.mark.parametrize("case", ["device", "pinned", "sparse", "depth0"])
+def test_naive_out_of_core_trees_match_oracle(gbt, ctx, case):
+    # Alg. 6: the per-level streaming construction gives the in-core trees
+    if case == "sparse":
+        d = datagen.config5(n=5000, m=300)
+        data, y = d, d["y"]
+        cfg = datagen.TrainConfig("t", 0, 64, 6, 2, eta=0.3, gamma=0.1)
+    else:
+        d = datagen.config3(n=15_000, m=12)
+        data, y = d["X"], d["y"]
+        cfg = datagen.TrainConfig("t", 1, 64, 0 if case == "depth0" else 7, 2, eta=0.3)
+    kw = dict(page_rows=4096, page_home=gbt.HOME_PINNED_HOST) if case == "pinned" else {}
+    mx = gbt.gbt_quantize(ctx, data, max_bin=cfg.max_bin, **kw)
+    trees, margin = train_naive(gbt, ctx, mx, y, cfg, 2)
+    _, b, _, _ = oracle_quantize(data, cfg.max_bin)
+    OP = orc.Params(loss=cfg.loss, max_depth=cfg.max_depth, eta=cfg.eta, lambda_=cfg.lambda_, gamma=cfg.gamma,
+                    min_child_weight=cfg.min_child_weight, f=1.0, seed=cfg.seed)
+    otrees, omargin = orc.train(b, y, OP, 2, cfg.base_margin)
+    assert_same_trees(trees, margin.cpu().numpy(), otrees, omargin)
+    if case == "pinned":
+        assert all(t.stats.h2d_bytes > 0 for t in trees)
+
+
+def test_naive_rejects_sampling_and_deep_trees(gbt, ctx):
+    d = datagen.config3(n=2000, m=4)
+    mx = gbt.gbt_quantize(ctx, d["X"], max_bin=16)
+    y = torch.from_numpy(d["y"]).cuda()
+    m = torch.zeros(2000, dtype=torch.float32, device="cuda")
+    for P in [gbt.make_train_params(f=0.5, max_depth=3), gbt.make_train_params(max_depth=12)]:
+        with pytest.raises(RuntimeError):
+            gbt.gbt_train_tree_naive(ctx, mx, y, m, P)
+
+
 def test_trees_many_partition_tiles(gbt, ctx):
     # over 2048 partition tiles of 1024 slots: the tile counts are scanned
     # by a kernel of their own before the scatter
