@@ -135,6 +135,8 @@ def parse():
     ap.add_argument("--cpu-trees", type=int, default=2)
     ap.add_argument("--sampler", default="mvs", choices=["mvs", "sgb", "goss"],
                     help="the sampler used when f < 1 (Sec. 2.3-2.4)")
+    ap.add_argument("--naive", action="store_true",
+                    help="outofcore: Alg. 6, the naive construction (f = 1, every level streams every page)")
     ap.add_argument("--goss-a", type=float, default=0.05,
                     help="GOSS top fraction a (the rest fraction is f - a)")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -275,19 +277,20 @@ def run_outofcore(args):
     label = torch.from_numpy(y).cuda()
     margin = torch.full((n,), cfg.base_margin, dtype=torch.float32, device="cuda")
     P = gbt.make_train_params(loss=cfg.loss, max_depth=cfg.max_depth, eta=cfg.eta, lambda_=cfg.lambda_,
-                              gamma=cfg.gamma, min_child_weight=cfg.min_child_weight, f=cfg.f,
-                              mvs_lambda=cfg.mvs_lambda, seed=cfg.seed)
+                              gamma=cfg.gamma, min_child_weight=cfg.min_child_weight,
+                              f=1.0 if args.naive else cfg.f, mvs_lambda=cfg.mvs_lambda, seed=cfg.seed)
+    train = gbt.gbt_train_tree_naive if args.naive else gbt.gbt_train_tree
     ctx.set_timing(1)
     for w in range(args.warmup):
         P.iteration = w
-        gbt.gbt_train_tree(ctx, mx, label, margin, P)
+        train(ctx, mx, label, margin, P)
         print(f"[bench] warm-up tree {w}", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     stats = []
     t0 = time.perf_counter()
     for k in range(args.steps):
         P.iteration = args.warmup + k
-        stats.append(gbt.gbt_train_tree(ctx, mx, label, margin, P).stats)
+        stats.append(train(ctx, mx, label, margin, P).stats)
         print(f"[bench] tree {k}: {stats[-1].ms_total:.0f} ms", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
@@ -315,8 +318,11 @@ def run_outofcore(args):
         "dtype": "int64",
         "data": "synthetic",
         "config": {"workload": f"out-of-core {n:,} x 100 in {info.n_pages} pinned pages of {page_rows:,} rows, "
-                               f"logistic, max_bin 256, depth 8, MVS f={cfg.f}, 8 GB device budget",
-                   "rows": n, "features": 100, "page_rows": page_rows, "f": cfg.f},
+                               f"logistic, max_bin 256, depth 8, "
+                               + ("Alg. 6 naive construction (f = 1, every level streams every page)"
+                                  if args.naive else f"MVS f={cfg.f}") + ", 8 GB device budget",
+                   "rows": n, "features": 100, "page_rows": page_rows, "f": 1.0 if args.naive else cfg.f,
+                   "naive": bool(args.naive)},
         "sec_per_tree": round(dt / args.steps, 4),
         "rows_sampled_per_tree": round(sum(s.n_sampled for s in stats) / args.steps),
         "host_link": {"h2d_bytes_per_tree": round(h2d / args.steps), "achieved_gbs": round(h2d / dt / 1e9, 2),
