@@ -1368,6 +1368,7 @@ __global__ void k_fill_i32(int32_t *__restrict__ p, int64_t n, int32_t v)
 static gbt_status train_tree_naive_impl(gbt_ctx *c, const gbt_matrix *mx, const float *label, float *margin,
                                         const gbt_train_params *p, gbt_tree *tree, gbt_tree_stats *stats)
 {
+    const auto t_start = std::chrono::steady_clock::now();
     const int64_t n = mx->n_rows;
     const int32_t D = p->max_depth;
     const int32_t NN = (1 << (D + 1)) - 1;
@@ -1433,7 +1434,15 @@ static gbt_status train_tree_naive_impl(gbt_ctx *c, const gbt_matrix *mx, const 
     }
     const Geo geo = geo_of(mx);
     const EvalParams ep{p->lambda, p->gamma, p->min_child_weight, 0, 0, &st->e_g};
-    int32_t hist_launches = 0;
+    // the histogram launches' counters: updates on the device, rows and
+    // algorithmic bytes on the host
+    unsigned long long *upd;
+    GBT_TRY(scratch_t(c, kScrUpd, kUpdWords, &upd));
+    k_naive_zero<<<blocks(kUpdWords), 256, 0, c->stream>>>(upd, kUpdWords);
+    GBT_LAUNCHED();
+    gbt_tree_stats hs;
+    memset(&hs, 0, sizeof(hs));
+    int64_t kind_rows[3] = {0, 0, 0};  // rows built by the sparse, plain and rotated kernels
     std::vector<int32_t> level{0}, so((size_t)NN, -1);
     std::vector<uint32_t> hcnt;
     for (int32_t d = 0; d <= D && n > 0; ++d) {
@@ -1449,7 +1458,6 @@ static gbt_status train_tree_naive_impl(gbt_ctx *c, const gbt_matrix *mx, const 
             GBT_LAUNCHED();
         }
         std::vector<uint64_t> total((size_t)L, 0);
-        mark = timer_begin(c, kPhHist);
         GBT_TRY(for_each_chunk(
             c, mx,
             [&](const uint32_t *words, int64_t row0, int64_t rows) -> gbt_status {
@@ -1477,13 +1485,15 @@ static gbt_status train_tree_naive_impl(gbt_ctx *c, const gbt_matrix *mx, const 
                     off += hcnt[s];
                 }
                 if (segs.empty()) return GBT_OK;
+                HistPlan hpk;
+                GBT_TRY(hist_plan(mx, off, c->hist_kernel, &hpk));
+                kind_rows[hpk.kind == kHistRot ? 2 : (hpk.kind == kHistDense ? 1 : 0)] += off;
                 GBT_HIP(hipMemcpyAsync(cnt, cur.data(), (size_t)L * 4, hipMemcpyHostToDevice, c->stream));
                 k_naive_group<<<(unsigned)((rows + 255) / 256), 256, 0, c->stream>>>(rows, row0, position, slot_of,
                                                                                       L, cnt, grouped);
                 GBT_LAUNCHED();
                 GBT_TRY(build_hist_impl(c, mx, words, q + 2 * row0, grouped, segs.data(), (int32_t)segs.size(),
-                                        nullptr, 0, nullptr, part, nullptr));
-                ++hist_launches;
+                                        nullptr, 0, nullptr, part, &hs));
                 GBT_HIP(hipMemcpyAsync(slots_d, built.data(), built.size() * 4, hipMemcpyHostToDevice, c->stream));
                 dim3 g((unsigned)((tb + 255) / 256), (unsigned)built.size());
                 k_naive_accumulate<<<g, 256, 0, c->stream>>>((longlong2 *)hist, (const longlong2 *)part, slots_d,
@@ -1495,7 +1505,6 @@ static gbt_status train_tree_naive_impl(gbt_ctx *c, const gbt_matrix *mx, const 
                 return GBT_OK;
             },
             &h2d));
-        timer_end(c, mark);
         for (int32_t s = 0; s < L; ++s) {
             hn[level[s]].begin = 0;
             hn[level[s]].end = (int64_t)total[s];
@@ -1549,7 +1558,7 @@ static gbt_status train_tree_naive_impl(gbt_ctx *c, const gbt_matrix *mx, const 
     GBT_LAUNCHED();
     void *hio, *hio_d;
     GBT_TRY(host_io(c, sizeof(TreeResult) + (size_t)NN * sizeof(gbt_node), &hio, &hio_d));
-    k_finalize<<<blocks(NN), 256, 0, c->stream>>>(nodes, NN, leaf, mx->cut_ptr_d, mx->cut_values_d, st, nullptr,
+    k_finalize<<<blocks(NN), 256, 0, c->stream>>>(nodes, NN, leaf, mx->cut_ptr_d, mx->cut_values_d, st, upd,
                                                   stat, (TreeResult *)hio_d);
     GBT_LAUNCHED();
     GBT_HIP(hipStreamSynchronize(c->stream));
@@ -1561,12 +1570,20 @@ static gbt_status train_tree_naive_impl(gbt_ctx *c, const gbt_matrix *mx, const 
     timer_collect(c, ms);
     if (stats) {
         stats->n_sampled = n;
-        stats->hist_launches = hist_launches;
+        stats->hist_launches = hs.hist_launches;
+        stats->hist_rows = hs.hist_rows;
+        stats->hist_bytes = hs.hist_bytes;
+        stats->hist_updates = (int64_t)res->updates;
+        // the kernel that built the most rows
+        stats->hist_kernel = mx->sparse ? 0
+                             : (kind_rows[2] >= kind_rows[1] ? GBT_HIST_ROTATED : GBT_HIST_PLAIN);
         stats->h2d_bytes = (int64_t)h2d;
         stats->ms_sample = ms[kPhSample];
         stats->ms_hist = ms[kPhHist];
         stats->ms_split = ms[kPhSplit];
         stats->ms_margin = ms[kPhMargin];
+        stats->ms_total =
+            std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t_start).count();
     }
     return GBT_OK;
 }

@@ -609,6 +609,18 @@ def test_naive_out_of_core_trees_match_oracle(gbt, ctx, case):
     assert_same_trees(trees, margin.cpu().numpy(), otrees, omargin)
     if case == "pinned":
         assert all(t.stats.h2d_bytes > 0 for t in trees)
+    # every level below the last builds the histograms of all its nodes'
+    # rows: the root level alone updates every non-null entry once
+    for t in trees:
+        s = t.stats
+        if case == "depth0":
+            assert s.hist_updates == 0 and s.hist_launches == 0
+        elif case != "sparse":
+            nonnull = int(np.count_nonzero(~np.isnan(data)))
+            n = len(data)
+            assert nonnull <= s.hist_updates <= cfg.max_depth * nonnull
+            assert n <= s.hist_rows <= cfg.max_depth * n
+            assert s.hist_launches >= cfg.max_depth and s.hist_bytes > 0
 
 
 def test_naive_rejects_sampling_and_deep_trees(gbt, ctx):
