@@ -135,6 +135,9 @@ def parse():
     ap.add_argument("--cpu-trees", type=int, default=2)
     ap.add_argument("--sampler", default="mvs", choices=["mvs", "sgb", "goss"],
                     help="the sampler used when f < 1 (Sec. 2.3-2.4)")
+    ap.add_argument("--compaction", choices=["auto", "stream", "gather"], default="auto",
+                    help="outofcore: how the compaction reads the pinned pages (stream every page, or gather "
+                         "only the kept rows through their device mapping)")
     ap.add_argument("--naive", action="store_true",
                     help="outofcore: Alg. 6, the naive construction (f = 1, every level streams every page)")
     ap.add_argument("--goss-a", type=float, default=0.05,
@@ -249,6 +252,8 @@ def run_outofcore(args):
     sizes = datagen.config4_page_rows(n, page_rows)
     budget = 8 << 30
     ctx = gbt.Context(0, budget_bytes=budget)
+    ctx.set_compaction({"auto": ctx.COMPACT_AUTO, "stream": ctx.COMPACT_STREAM,
+                        "gather": ctx.COMPACT_GATHER}[args.compaction])
     sub = 1 << 21  # rows per host batch handed to the quantizer
     t = time.perf_counter()
     q = gbt.Quantizer(ctx, 100, n, max_bin=cfg.max_bin, page_rows=page_rows, page_home=gbt.HOME_PINNED_HOST)
@@ -322,7 +327,7 @@ def run_outofcore(args):
                                + ("Alg. 6 naive construction (f = 1, every level streams every page)"
                                   if args.naive else f"MVS f={cfg.f}") + ", 8 GB device budget",
                    "rows": n, "features": 100, "page_rows": page_rows, "f": 1.0 if args.naive else cfg.f,
-                   "naive": bool(args.naive)},
+                   "naive": bool(args.naive), "compaction": args.compaction},
         "sec_per_tree": round(dt / args.steps, 4),
         "rows_sampled_per_tree": round(sum(s.n_sampled for s in stats) / args.steps),
         "host_link": {"h2d_bytes_per_tree": round(h2d / args.steps), "achieved_gbs": round(h2d / dt / 1e9, 2),

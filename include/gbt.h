@@ -245,6 +245,19 @@ gbt_status gbt_ctx_set_timing(gbt_ctx *ctx, int32_t level);
 #define GBT_HIST_ROTATED 2
 gbt_status gbt_ctx_set_hist_kernel(gbt_ctx *ctx, int32_t choice);
 
+/* How the compaction of Alg. 7 (Sec. 3.4) reads pages held in pinned host
+ * memory (results are identical): GBT_COMPACT_STREAM copies every page over
+ * the host link in chunks and compacts each chunk on the device;
+ * GBT_COMPACT_GATHER has the compaction kernel read only the kept rows
+ * straight from the pinned pages (device-mapped host memory), so about R of
+ * the n rows cross the link; GBT_COMPACT_AUTO gathers when at most half of
+ * the rows are kept.  Device-resident pages are read in place either way.
+ * GBT_E_INVALID for another value. */
+#define GBT_COMPACT_AUTO 0
+#define GBT_COMPACT_STREAM 1
+#define GBT_COMPACT_GATHER 2
+gbt_status gbt_ctx_set_compaction(gbt_ctx *ctx, int32_t mode);
+
 /* ---- quantile cuts and ELLPACK pages: Sec. 2.2, Sec. 3.1 (Alg. 2, 3),
  * Sec. 3.2 (Alg. 4, 5) ------------------------------------------------------
  * Cuts are exact quantiles of a sketch sample: for a feature with sorted

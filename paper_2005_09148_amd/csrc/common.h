@@ -69,6 +69,7 @@ struct gbt_ctx {
     uint64_t used = 0, peak = 0;
     int timing = 0;  // 0 off, 1 histogram kernel only, 2 every phase
     int hist_kernel = GBT_HIST_AUTO;
+    int compaction = GBT_COMPACT_AUTO;
     struct Mark {
         int a, b;    // indices into events
         int phase;

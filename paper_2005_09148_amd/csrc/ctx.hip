@@ -225,4 +225,13 @@ gbt_status gbt_ctx_set_hist_kernel(gbt_ctx *c, int32_t choice)
     return GBT_OK;
 }
 
+gbt_status gbt_ctx_set_compaction(gbt_ctx *c, int32_t mode)
+{
+    if (!c) return set_error(GBT_E_INVALID, "gbt_ctx_set_compaction: ctx is NULL");
+    if (mode != GBT_COMPACT_AUTO && mode != GBT_COMPACT_STREAM && mode != GBT_COMPACT_GATHER)
+        return set_error(GBT_E_INVALID, "gbt_ctx_set_compaction: unknown mode %d", mode);
+    c->compaction = mode;
+    return GBT_OK;
+}
+
 }  // extern "C"

@@ -803,7 +803,8 @@ gbt_status gbt_quantize_encode_batch(gbt_quantizer *q, const gbt_input *batch)
             size_t pb = (size_t)std::max<int64_t>(pg.rows, 1) * mx->row_words * 4;
             if (mx->page_home == GBT_HOME_PINNED_HOST) {
                 pg.host = true;
-                hipError_t e = hipHostMalloc((void **)&pg.words, pb, hipHostMallocDefault);
+                // mapped: the gather compaction reads kept rows in place
+                hipError_t e = hipHostMalloc((void **)&pg.words, pb, hipHostMallocMapped);
                 if (e != hipSuccess) {
                     (void)hipGetLastError();
                     return set_error(GBT_E_OOM, "hipHostMalloc(%zu) for a page failed", pb);

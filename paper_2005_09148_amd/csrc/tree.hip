@@ -91,6 +91,20 @@ gbt_status for_each_chunk(gbt_ctx *c, const gbt_matrix *mx, const ChunkFn &fn, d
     return GBT_OK;
 }
 
+// Holds the staging buffers for_each_chunk uses for mx's pinned pages, so
+// that later workspaces sized by the remaining budget leave room for them.
+static gbt_status reserve_stage(gbt_ctx *c, const gbt_matrix *mx)
+{
+    int64_t maxrows = 0;
+    for (const auto &pg : mx->pages)
+        if (pg.host) maxrows = std::max(maxrows, std::min(pg.rows, g_stream_chunk_rows));
+    if (maxrows == 0) return GBT_OK;
+    void *p;
+    GBT_TRY(scratch(c, kScrStage0, (size_t)maxrows * mx->row_words * 4, &p));
+    GBT_TRY(scratch(c, kScrStage1, (size_t)maxrows * mx->row_words * 4, &p));
+    return GBT_OK;
+}
+
 static bool all_device_single(const gbt_matrix *mx)
 {
     return mx->pages.size() == 1 && !mx->pages[0].host;
@@ -209,13 +223,37 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
         GBT_TRY(bufs.get(kScrSel, (size_t)std::max<int64_t>(o->R, 1) * 4, (void **)&o->sel));
         GBT_TRY(bufs.get(kScrGw, (size_t)std::max<int64_t>(o->R, 1) * 16, (void **)&o->gw));
         o->page = spage;
-        GBT_TRY(for_each_chunk(
-            c, mx,
-            [&](const uint32_t *words, int64_t row0, int64_t rows) -> gbt_status {
-                return mvs_compact_tiles(c, src, kind, n, lam, st, keep, tile_off, row0, row0 + rows,
-                                         words, mx->row_words, spage, o->sel, o->gw, rule);
-            },
-            h2d_bytes));
+        const bool host = any_host_pages(mx);
+        const bool gather = host && (c->compaction == GBT_COMPACT_GATHER ||
+                                     (c->compaction == GBT_COMPACT_AUTO && 2 * (int64_t)o->R <= n));
+        if (gather) {
+            // the kernel reads the kept rows of each pinned page through its
+            // device mapping: only those rows cross the host link
+            for (const auto &pg : mx->pages) {
+                if (!pg.rows) continue;
+                const uint32_t *w = pg.words;
+                if (pg.host) {
+                    void *dp = nullptr;
+                    GBT_HIP(hipHostGetDevicePointer(&dp, (void *)pg.words, 0));
+                    GBT_CHECK(dp != nullptr, "no device mapping of a pinned page");
+                    w = (const uint32_t *)dp;
+                }
+                GBT_TRY(mvs_compact_tiles(c, src, kind, n, lam, st, keep, tile_off, pg.row0, pg.row0 + pg.rows, w,
+                                          mx->row_words, spage, o->sel, o->gw, rule));
+            }
+            // every page of a matrix has the same home
+            if (h2d_bytes) *h2d_bytes += (double)o->R * (double)rb;
+            // the margin update still streams every page
+            GBT_TRY(reserve_stage(c, mx));
+        } else {
+            GBT_TRY(for_each_chunk(
+                c, mx,
+                [&](const uint32_t *words, int64_t row0, int64_t rows) -> gbt_status {
+                    return mvs_compact_tiles(c, src, kind, n, lam, st, keep, tile_off, row0, row0 + rows,
+                                             words, mx->row_words, spage, o->sel, o->gw, rule);
+                },
+                h2d_bytes));
+        }
         fx_max_done = true;
     }
     GBT_TRY(bufs.get(kScrQ, (size_t)std::max<int64_t>(o->R, 1) * 16, (void **)&o->q));

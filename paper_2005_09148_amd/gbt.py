@@ -138,6 +138,7 @@ SIGNATURES = {
     "gbt_ctx_memory": (_i32, [_vp, _vp, _vp]),
     "gbt_ctx_set_timing": (_i32, [_vp, _i32]),
     "gbt_ctx_set_hist_kernel": (_i32, [_vp, _i32]),
+    "gbt_ctx_set_compaction": (_i32, [_vp, _i32]),
     "gbt_quantize": (_i32, [_vp, _vp, _vp, _vp]),
     "gbt_quantize_begin": (_i32, [_vp, _vp, _i32, _i64, _i32, _vp]),
     "gbt_quantize_sketch_batch": (_i32, [_vp, _vp]),
@@ -265,6 +266,15 @@ class Context:
         """Dense histogram kernel: HIST_AUTO (by pass size), HIST_PLAIN or
         HIST_ROTATED; results are identical."""
         _check(_lib.gbt_ctx_set_hist_kernel(self.h, int(choice)))
+
+    COMPACT_AUTO, COMPACT_STREAM, COMPACT_GATHER = 0, 1, 2
+
+    def set_compaction(self, mode: int):
+        """How the compaction reads pinned-host pages: COMPACT_STREAM (copy
+        every page over the link), COMPACT_GATHER (read only the kept rows
+        through the pages' device mapping) or COMPACT_AUTO; results are
+        identical."""
+        _check(_lib.gbt_ctx_set_compaction(self.h, int(mode)))
 
     @property
     def torch_device(self):

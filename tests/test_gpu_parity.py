@@ -504,6 +504,29 @@ def test_out_of_core_sampled_matches_oracle(gbt, ctx, hist_kernel):
     assert_same_trees(*r[:4])
 
 
+@pytest.mark.parametrize("f", [0.3, 1.0])
+def test_out_of_core_compaction_modes(gbt, ctx, f):
+    # Alg. 7's compaction from pinned pages: streaming every page and
+    # gathering only the kept rows through the pages' device mapping give
+    # the oracle's trees; the gather moves (n - R) fewer rows per tree
+    cfg = datagen.TrainConfig("t", 0, 256, 6, 3, eta=0.1, f=f)
+    d = datagen.config2(n=20_000)
+    out = {}
+    try:
+        for mode in (ctx.COMPACT_STREAM, ctx.COMPACT_GATHER):
+            ctx.set_compaction(mode)
+            out[mode] = train_both(gbt, ctx, d["X"], d["y"], cfg, 3, page_rows=3000, home=gbt.HOME_PINNED_HOST)
+            assert_same_trees(*out[mode][:4])
+    finally:
+        ctx.set_compaction(ctx.COMPACT_AUTO)
+    rb = out[ctx.COMPACT_STREAM][4].info().row_words * 4
+    for ts, tg in zip(out[ctx.COMPACT_STREAM][0], out[ctx.COMPACT_GATHER][0]):
+        assert ts.stats.n_sampled == tg.stats.n_sampled
+        assert ts.stats.h2d_bytes - tg.stats.h2d_bytes == (20_000 - tg.stats.n_sampled) * rb
+    with pytest.raises(gbt.GbtError):
+        ctx.set_compaction(3)
+
+
 def test_empty_sample_tree(gbt, ctx, hist_kernel):
     """All gradients zero, MVS lambda 0 and f < 1: every key sqrt(g^2 + 0 h^2)
     is 0, no row is kept, and the tree is one leaf (the oracle's empty-sample
