@@ -855,6 +855,40 @@ int64_t orc_partition(const orc_data *d, const int64_t *rows, int64_t n_rows, in
     return nl;
 }
 
+/* Sec. 2.4 (MVS): lambda estimated from the data as the square of the      */
+/* initial leaf value, read as the unregularized Newton step of all n rows  */
+/* at the given margins: gradients (Eq. 4-5), their fixed point over the n  */
+/* rows, G and H the exact integer sums, w0 = -G/H, lambda = w0^2 (0 when H */
+/* is 0).                                                                    */
+double orc_mvs_lambda_estimate(int32_t loss, const float *margin, const float *label, int64_t n)
+{
+    if (n <= 0) return 0.0;
+    float *gp = (float *)malloc((size_t)n * 2 * sizeof(float));
+    double *gw = (double *)malloc((size_t)n * 2 * sizeof(double));
+    int64_t *q = (int64_t *)malloc((size_t)n * 2 * sizeof(int64_t));
+    double lam = 0.0;
+    if (gp && gw && q && orc_gradients(loss, margin, label, NULL, n, gp) == 0) {
+        for (int64_t i = 0; i < 2 * n; ++i) gw[i] = (double)gp[i];
+        int32_t eg, eh;
+        orc_fixed_point(gw, n, q, &eg, &eh);
+        int64_t G = 0, H = 0;
+        for (int64_t i = 0; i < n; ++i) {
+            G += q[2 * i];
+            H += q[2 * i + 1];
+        }
+        if (H != 0) {
+            double w0 = -to_double(G, eg) / to_double(H, eh);
+            lam = w0 * w0;
+        }
+    } else {
+        lam = -1.0;
+    }
+    free(gp);
+    free(gw);
+    free(q);
+    return lam;
+}
+
 /* Eq. 6, scaled by the learning rate: leaf = (float)((-G/(H+lambda)) * eta) */
 float orc_leaf_value(int64_t Qg, int64_t Qh, int32_t e_g, int32_t e_h, double lambda, double eta)
 {

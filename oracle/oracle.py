@@ -111,6 +111,7 @@ def lib():
             "orc_eval_node": (None, [vp, vp, vp, i32, vp, i32, i32, vp]),
             "orc_partition": (i64, [vp, vp, i64, i32, i32, i32, vp]),
             "orc_leaf_value": (C.c_float, [i64, i64, i32, i32, f64, f64]),
+            "orc_mvs_lambda_estimate": (f64, [i32, vp, vp, i64]),
             "orc_train_tree": (C.c_int, [vp, vp, vp, vp, vp, vp, vp, vp, vp]),
             "orc_predict_binned": (None, [vp, vp, vp, i32, C.c_float, vp]),
             "orc_predict_raw_dense": (None, [vp, i64, i64, vp, vp, i32, C.c_float, vp]),
@@ -424,6 +425,16 @@ def partition(b: Binned, rows, feature, split_bin, default_left):
     nl = lib().orc_partition(C.byref(s), _p(rows), len(rows), feature, split_bin,
                              int(default_left), _p(out))
     return out[:nl], out[nl:]
+
+
+def mvs_lambda_estimate(loss, margin, label):
+    """Sec. 2.4: MVS lambda as the squared initial leaf value (-G/H of every
+    row at the given margins, from the exact fixed-point sums)."""
+    margin, label = _c(margin, np.float32), _c(label, np.float32)
+    v = lib().orc_mvs_lambda_estimate(int(loss), _p(margin), _p(label), len(margin))
+    if v < 0:
+        raise ValueError("orc_mvs_lambda_estimate failed")
+    return float(v)
 
 
 def leaf_value(Qg, Qh, e_g, e_h, lambda_, eta):

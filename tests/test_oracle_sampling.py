@@ -267,3 +267,43 @@ def test_training_with_sgb_and_goss(orc, sampler):
         assert r.info.T == t
     assert np.array_equal(r.sel, np.nonzero(want)[0])
     assert (margin != 0).any()
+
+
+# ------------------------------------------------- MVS lambda estimated from data
+@pytest.mark.parametrize("n", [1, 7, 1000])
+def test_lambda_estimate_squared_loss_is_squared_mean_label(orc, n):
+    # squared error at margin 0: g = -y, h = 1, so the initial Newton leaf is
+    # mean(y) and lambda = mean(y)^2; labels are multiples of 1/8, so the
+    # fixed-point sums are exact and the result is the correctly rounded
+    # (sum y / n)^2
+    rng = np.random.default_rng(n)
+    y = (rng.integers(-16, 40, n) / 8.0).astype(np.float32)
+    lam = orc.mvs_lambda_estimate(orc.LOSS_SQUARED, np.zeros(n, np.float32), y)
+    w0 = float(np.sum(y.astype(np.float64))) / n
+    assert lam == w0 * w0
+
+
+def test_lambda_estimate_logistic_at_zero_margin(orc):
+    # logistic at margin 0: p = 1/2, g = 1/2 - y, h = 1/4, so the leaf is
+    # -4 * sum(1/2 - y) / n
+    rng = np.random.default_rng(5)
+    y = (rng.random(777) < 0.3).astype(np.float32)
+    lam = orc.mvs_lambda_estimate(orc.LOSS_LOGISTIC, np.zeros(777, np.float32), y)
+    w0 = -float(np.sum(0.5 - y.astype(np.float64))) / (0.25 * 777)
+    assert lam == w0 * w0
+    assert lam > 0
+
+
+def test_lambda_estimate_general_margins_and_degenerate_cases(orc):
+    # at arbitrary margins the estimate is (sum g / sum h)^2 of the float32
+    # gradients up to the fixed-point rounding (relative 2^-40 here)
+    rng = np.random.default_rng(9)
+    n = 5000
+    m = rng.normal(0.0, 1.5, n).astype(np.float32)
+    y = (rng.random(n) < 0.8).astype(np.float32)
+    gp = orc.gradients(orc.LOSS_LOGISTIC, m, y).astype(np.float64)
+    want = (gp[:, 0].sum() / gp[:, 1].sum()) ** 2
+    assert orc.mvs_lambda_estimate(orc.LOSS_LOGISTIC, m, y) == pytest.approx(want, rel=2.0**-40)
+    # a label equal to every margin gives a zero leaf; no rows give 0
+    assert orc.mvs_lambda_estimate(orc.LOSS_SQUARED, y, y) == 0.0
+    assert orc.mvs_lambda_estimate(orc.LOSS_SQUARED, np.zeros(0, np.float32), np.zeros(0, np.float32)) == 0.0
