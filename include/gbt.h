@@ -397,6 +397,17 @@ gbt_status gbt_train_tree_naive(gbt_ctx *ctx, const gbt_matrix *data, const floa
                                 float *margin_d, const gbt_train_params *params, gbt_tree *tree_out,
                                 gbt_tree_stats *stats);
 
+/* ---- MVS lambda estimated from the data: Sec. 2.4 ---------------------------
+ * *lambda_out = w0^2 with w0 = -G/H the initial leaf value, read as the
+ * unregularized Newton step of all n rows at margin_d (length n, device):
+ * G and H are the exact integer sums of the rows' gradients (Eq. 4-5, loss
+ * as in gbt_gradients) in their fixed point over the n rows (the
+ * representation the histograms use), scaled back to double; 0 when H or n
+ * is 0.  Pass the value as mvs_lambda of later iterations.  Synchronizes
+ * the context stream. */
+gbt_status gbt_mvs_lambda_estimate(gbt_ctx *ctx, int32_t loss, const float *margin_d,
+                                   const float *label_d, int64_t n, double *lambda_out);
+
 /* ---- Eq. 1 prediction -------------------------------------------------------
  * margin_out_d[i] = base_margin + sum_t leaf(tree t, row i), in float, tree
  * order.  Exactly one of raw (rows traverse by x <= threshold, missing by

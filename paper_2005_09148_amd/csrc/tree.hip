@@ -1251,6 +1251,41 @@ gbt_status gbt_gradients(gbt_ctx *c, int32_t loss, const float *margin_d, const 
     return GBT_OK;
 }
 
+gbt_status gbt_mvs_lambda_estimate(gbt_ctx *c, int32_t loss, const float *margin_d, const float *label_d, int64_t n,
+                                   double *lambda_out)
+{
+    GBT_CHECK(c && lambda_out, "gbt_mvs_lambda_estimate: NULL argument");
+    GBT_CHECK(n >= 0, "n < 0");
+    GBT_CHECK(loss == GBT_LOSS_LOGISTIC || loss == GBT_LOSS_SQUARED, "unknown loss %d", loss);
+    GBT_CHECK(n == 0 || (margin_d && label_d), "gbt_mvs_lambda_estimate: NULL array");
+    *lambda_out = 0.0;
+    if (n == 0) return GBT_OK;
+    GBT_TRY(set_device(c));
+    // every row's pair in its exact fixed point; the state folds the sums
+    float *gpair;
+    double *gw;
+    int64_t *q;
+    SampleState *st;
+    GBT_TRY(scratch_t(c, kScrGpair, (size_t)n * 2, &gpair));
+    GBT_TRY(scratch_t(c, kScrGw, (size_t)n * 2, &gw));
+    GBT_TRY(scratch_t(c, kScrQ, (size_t)n * 2, &q));
+    GBT_TRY(scratch_t(c, kScrState, 1, &st));
+    GBT_TRY(state_init(c, st));
+    GBT_TRY(launch_gradients(c, loss, margin_d, label_d, nullptr, n, gpair));
+    GBT_TRY(gw_all(c, gpair, n, gw));
+    GBT_TRY(fixed_point(c, gw, n, st, q, false));
+    SampleState hst;
+    GBT_HIP(hipMemcpyAsync(&hst, st, sizeof(SampleState), hipMemcpyDeviceToHost, c->stream));
+    GBT_HIP(hipStreamSynchronize(c->stream));
+    if (hst.bad) return set_error(GBT_E_INVALID, "gradient sums failed (state flags %u)", hst.bad);
+    const long long G = (long long)fold_sum(hst.root_g), H = (long long)fold_sum(hst.root_h);
+    if (H != 0) {
+        const double w0 = -std::ldexp((double)G, -hst.e_g) / std::ldexp((double)H, -hst.e_h);
+        *lambda_out = w0 * w0;
+    }
+    return GBT_OK;
+}
+
 gbt_status gbt_sample(gbt_ctx *c, const gbt_matrix *data, const float *gpair_d, const float *margin_d,
                       const float *label_d, const gbt_sample_params *sp, gbt_sampled **out)
 {

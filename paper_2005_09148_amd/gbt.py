@@ -139,6 +139,7 @@ SIGNATURES = {
     "gbt_ctx_set_timing": (_i32, [_vp, _i32]),
     "gbt_ctx_set_hist_kernel": (_i32, [_vp, _i32]),
     "gbt_ctx_set_compaction": (_i32, [_vp, _i32]),
+    "gbt_mvs_lambda_estimate": (_i32, [_vp, _i32, _vp, _vp, _i64, _vp]),
     "gbt_quantize": (_i32, [_vp, _vp, _vp, _vp]),
     "gbt_quantize_begin": (_i32, [_vp, _vp, _i32, _i64, _i32, _vp]),
     "gbt_quantize_sketch_batch": (_i32, [_vp, _vp]),
@@ -445,6 +446,15 @@ def gbt_gradients(ctx, loss, margin, label, weight=None, out=None):
         out = torch.empty((n, 2), dtype=torch.float32, device=margin.device)
     _check(_lib.gbt_gradients(ctx.h, loss, _ptr(margin), _ptr(label), _ptr(weight), n, _ptr(out)))
     return out
+
+
+def gbt_mvs_lambda_estimate(ctx, loss, margin, label):
+    """MVS lambda as the squared initial leaf value -G/H of every row at
+    `margin` (device tensors of equal length)."""
+    out = C.c_double()
+    _check(_lib.gbt_mvs_lambda_estimate(ctx.h, int(loss), _ptr(margin), _ptr(label), margin.numel(),
+                                        C.byref(out)))
+    return out.value
 
 
 def _hip():

@@ -504,6 +504,21 @@ def test_out_of_core_sampled_matches_oracle(gbt, ctx, hist_kernel):
     assert_same_trees(*r[:4])
 
 
+@pytest.mark.parametrize("loss,n,margins", [(orc.LOSS_SQUARED, 1, "zero"), (orc.LOSS_SQUARED, 1000, "zero"),
+                                            (orc.LOSS_LOGISTIC, 300_001, "random"),
+                                            (orc.LOSS_SQUARED, 65_537, "random"), (orc.LOSS_LOGISTIC, 0, "zero")])
+def test_mvs_lambda_estimate(gbt, ctx, loss, n, margins):
+    # Sec. 2.4: lambda from the squared initial leaf value, the same bits as
+    # the oracle's (exact fixed-point sums of every row)
+    rng = np.random.default_rng(n)
+    m = (rng.normal(0, 1.5, n) if margins == "random" else np.zeros(n)).astype(np.float32)
+    y = ((rng.random(n) < 0.7) if loss == orc.LOSS_LOGISTIC else rng.normal(0.5, 2.0, n)).astype(np.float32)
+    got = gbt.gbt_mvs_lambda_estimate(ctx, loss, torch.from_numpy(m).cuda(), torch.from_numpy(y).cuda())
+    want = orc.mvs_lambda_estimate(loss, m, y)
+    assert same_bits(np.float64(got), np.float64(want)), (got, want)
+    assert n == 0 or got > 0
+
+
 @pytest.mark.parametrize("f", [0.3, 1.0])
 def test_out_of_core_compaction_modes(gbt, ctx, f):
     # Alg. 7's compaction from pinned pages: streaming every page and
