@@ -138,6 +138,9 @@ def parse():
     ap.add_argument("--compaction", choices=["auto", "stream", "gather"], default="auto",
                     help="outofcore: how the compaction reads the pinned pages (stream every page, or gather "
                          "only the kept rows through their device mapping)")
+    ap.add_argument("--page-dir", default=None,
+                    help="outofcore: keep the pages in (unlinked) files under this directory instead of "
+                         "pinned host memory")
     ap.add_argument("--naive", action="store_true",
                     help="outofcore: Alg. 6, the naive construction (f = 1, every level streams every page)")
     ap.add_argument("--goss-a", type=float, default=0.05,
@@ -256,7 +259,9 @@ def run_outofcore(args):
                         "gather": ctx.COMPACT_GATHER}[args.compaction])
     sub = 1 << 21  # rows per host batch handed to the quantizer
     t = time.perf_counter()
-    q = gbt.Quantizer(ctx, 100, n, max_bin=cfg.max_bin, page_rows=page_rows, page_home=gbt.HOME_PINNED_HOST)
+    home = gbt.HOME_DISK if args.page_dir else gbt.HOME_PINNED_HOST
+    q = gbt.Quantizer(ctx, 100, n, max_bin=cfg.max_bin, page_rows=page_rows, page_home=home,
+                      page_dir=args.page_dir)
     raw, labels = [], []
     for p, rows in enumerate(sizes):
         d = datagen.config4_page(p, rows=rows)
@@ -277,7 +282,7 @@ def run_outofcore(args):
     info = mx.info()
     y = np.concatenate(labels)
     del labels
-    print(f"[bench] {info.n_pages} pinned pages, row_words {info.row_words}, quantized in "
+    print(f"[bench] {info.n_pages} {'disk' if args.page_dir else 'pinned'} pages, row_words {info.row_words}, quantized in "
           f"{time.perf_counter() - t:.0f} s", file=sys.stderr, flush=True)
     label = torch.from_numpy(y).cuda()
     margin = torch.full((n,), cfg.base_margin, dtype=torch.float32, device="cuda")
@@ -322,12 +327,14 @@ def run_outofcore(args):
         "vs_baseline": None,
         "dtype": "int64",
         "data": "synthetic",
-        "config": {"workload": f"out-of-core {n:,} x 100 in {info.n_pages} pinned pages of {page_rows:,} rows, "
+        "config": {"workload": f"out-of-core {n:,} x 100 in {info.n_pages} "
+                               + ("disk" if args.page_dir else "pinned") + f" pages of {page_rows:,} rows, "
                                f"logistic, max_bin 256, depth 8, "
                                + ("Alg. 6 naive construction (f = 1, every level streams every page)"
                                   if args.naive else f"MVS f={cfg.f}") + ", 8 GB device budget",
                    "rows": n, "features": 100, "page_rows": page_rows, "f": 1.0 if args.naive else cfg.f,
-                   "naive": bool(args.naive), "compaction": args.compaction},
+                   "naive": bool(args.naive), "compaction": args.compaction,
+                   "pages": "disk" if args.page_dir else "pinned host"},
         "sec_per_tree": round(dt / args.steps, 4),
         "rows_sampled_per_tree": round(sum(s.n_sampled for s in stats) / args.steps),
         "host_link": {"h2d_bytes_per_tree": round(h2d / args.steps), "achieved_gbs": round(h2d / dt / 1e9, 2),

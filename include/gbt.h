@@ -27,6 +27,7 @@
  *                     (the out-of-memory limit of the paper's Table 1)
  *  GBT_E_DEVICE       a HIP runtime error (message saved)
  *  GBT_E_UNSUPPORTED  a valid request this build does not implement
+ *  GBT_E_IO           a page file could not be created, written or read
  */
 #ifndef GBT_H
 #define GBT_H
@@ -45,17 +46,18 @@ typedef int32_t gbt_status;
 #define GBT_E_BUDGET (-3)
 #define GBT_E_DEVICE (-4)
 #define GBT_E_UNSUPPORTED (-5)
+#define GBT_E_IO (-6)
 
 /* Samplers (Sec. 2.3 and 2.4). */
 #define GBT_SAMPLE_MVS 0  /* minimal variance sampling, Eq. 9 */
 #define GBT_SAMPLE_SGB 1  /* stochastic gradient boosting: uniform rows */
 #define GBT_SAMPLE_GOSS 2 /* gradient-based one-side sampling */
 
-#define GBT_ABI_VERSION 2
+#define GBT_ABI_VERSION 3
 
 enum { GBT_INPUT_DENSE_F32 = 0, GBT_INPUT_CSR_F32 = 1 };
 enum { GBT_LOC_HOST = 0, GBT_LOC_DEVICE = 1 };
-enum { GBT_HOME_DEVICE = 0, GBT_HOME_PINNED_HOST = 1 };
+enum { GBT_HOME_DEVICE = 0, GBT_HOME_PINNED_HOST = 1, GBT_HOME_DISK = 2 };
 enum { GBT_LOSS_LOGISTIC = 0, GBT_LOSS_SQUARED = 1 };
 enum { GBT_NODE_PRESENT = 1, GBT_NODE_LEAF = 2, GBT_NODE_DEFAULT_LEFT = 4 };
 
@@ -82,9 +84,10 @@ typedef struct {
 
 typedef struct {
     int32_t max_bin;          /* Sec. 2.2: bins per feature, default 256 */
-    int32_t page_home;        /* GBT_HOME_DEVICE | GBT_HOME_PINNED_HOST */
+    int32_t page_home;        /* GBT_HOME_DEVICE | GBT_HOME_PINNED_HOST | GBT_HOME_DISK */
     int64_t sketch_max_rows;  /* 0 = 2^24: above it, every ceil(n/this)-th row is sketched */
     int64_t page_rows;        /* rows per ELLPACK page; 0 = one page */
+    const char *page_dir;     /* GBT_HOME_DISK: an existing directory for the page files */
 } gbt_quant_params;
 
 /* Geometry of a quantized matrix.  Symbols: dense pages hold feature j's
@@ -187,7 +190,7 @@ typedef struct {
     double ms_split;        /* split evaluation and partitioning */
     double ms_margin;       /* leaves and the margin update */
     double ms_total;        /* wall time of the call */
-    double h2d_bytes;       /* bytes streamed from pinned-host pages */
+    double h2d_bytes;       /* bytes streamed from pinned-host or disk pages */
     int32_t hist_kernel;    /* GBT_HIST_PLAIN or GBT_HIST_ROTATED (dense), 0 sparse */
     int32_t pad0;
 } gbt_tree_stats;
@@ -251,7 +254,8 @@ gbt_status gbt_ctx_set_hist_kernel(gbt_ctx *ctx, int32_t choice);
  * GBT_COMPACT_GATHER has the compaction kernel read only the kept rows
  * straight from the pinned pages (device-mapped host memory), so about R of
  * the n rows cross the link; GBT_COMPACT_AUTO gathers when at most half of
- * the rows are kept.  Device-resident pages are read in place either way.
+ * the rows are kept.  Device-resident pages are read in place either way,
+ * and disk pages always stream.
  * GBT_E_INVALID for another value. */
 #define GBT_COMPACT_AUTO 0
 #define GBT_COMPACT_STREAM 1
@@ -267,7 +271,13 @@ gbt_status gbt_ctx_set_compaction(gbt_ctx *ctx, int32_t mode);
  * form takes batches (Alg. 3 sketch, then Alg. 5 pages):
  *   begin -> sketch_batch* (every batch, in row order) -> finalize_cuts ->
  *   encode_batch* (every batch again, same order) -> end.
- * n_rows_total fixes the sketch stride.  page_home PINNED_HOST keeps pages
+ * n_rows_total fixes the sketch stride.  page_home DISK writes each page to
+ * a file of its own under page_dir (Sec. 3.2: pages on disk), created
+ * exclusively and unlinked at once, so the files vanish with the matrix or
+ * the process; each tree then reads the pages back through pinned staging
+ * buffers, as it streams pinned pages (GBT_E_INVALID without page_dir,
+ * GBT_E_IO when a file cannot be created, written or read).  page_home
+ * PINNED_HOST keeps pages
  * in page-locked host memory for streaming. */
 gbt_status gbt_quantize(gbt_ctx *ctx, const gbt_input *in, const gbt_quant_params *p,
                         gbt_matrix **out);

@@ -92,6 +92,9 @@ struct gbt_ctx {
     const void *cols_page = nullptr;
     const void *cols_at = nullptr;
     int64_t cols_rows = 0;
+    // pinned buffers that disk pages are read into before their copy
+    void *disk_stage[2] = {nullptr, nullptr};
+    size_t disk_stage_bytes = 0;
 };
 
 namespace gbt {
@@ -109,6 +112,10 @@ void dev_free(gbt_ctx *c, void *p, size_t bytes);
 gbt_status scratch(gbt_ctx *c, int slot, size_t bytes, void **p);
 // Whether scratch(c, slot, bytes) stays within the context's byte budget
 // (for optional workspaces that are skipped when it would not).
+// Whole reads and writes of page files at a byte offset (retried on short
+// transfers and EINTR).
+gbt_status file_read(int fd, void *dst, size_t bytes, int64_t off);
+gbt_status file_write(int fd, const void *src, size_t bytes, int64_t off);
 bool scratch_fits(const gbt_ctx *c, int slot, size_t bytes);
 // Grow-only pinned host buffer that kernels write into: *host for the host,
 // *dev for kernels.  The stream must not be using it (the call syncs
@@ -162,8 +169,10 @@ gbt_status scratch_t(gbt_ctx *c, int slot, size_t n, T **p)
 struct GbtPage {
     int64_t row0 = 0;
     int64_t rows = 0;
-    uint32_t *words = nullptr;  // device or pinned host
-    bool host = false;
+    uint32_t *words = nullptr;  // device or pinned host (NULL on disk)
+    bool host = false;          // pinned host memory
+    int fd = -1;                // the page's (unlinked) file, when on disk
+    bool streamed() const { return host || fd >= 0; }
 };
 
 // A process-unique id per matrix (never reused, unlike an address).

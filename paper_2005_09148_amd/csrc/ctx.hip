@@ -3,6 +3,10 @@
 
 #include <mutex>
 
+#include <cerrno>
+#include <cstring>
+#include <unistd.h>
+
 namespace gbt {
 
 static thread_local std::string g_last_error;
@@ -92,6 +96,34 @@ gbt_status scratch(gbt_ctx *c, int slot, size_t bytes, void **p)
         s.bytes = want;
     }
     *p = s.p;
+    return GBT_OK;
+}
+
+gbt_status file_read(int fd, void *dst, size_t bytes, int64_t off)
+{
+    char *p = (char *)dst;
+    while (bytes) {
+        ssize_t k = pread(fd, p, bytes, (off_t)off);
+        if (k < 0 && errno == EINTR) continue;
+        if (k <= 0) return set_error(GBT_E_IO, "page file read failed: %s", k < 0 ? strerror(errno) : "end of file");
+        p += k;
+        off += k;
+        bytes -= (size_t)k;
+    }
+    return GBT_OK;
+}
+
+gbt_status file_write(int fd, const void *src, size_t bytes, int64_t off)
+{
+    const char *p = (const char *)src;
+    while (bytes) {
+        ssize_t k = pwrite(fd, p, bytes, (off_t)off);
+        if (k < 0 && errno == EINTR) continue;
+        if (k <= 0) return set_error(GBT_E_IO, "page file write failed: %s", k < 0 ? strerror(errno) : "no progress");
+        p += k;
+        off += k;
+        bytes -= (size_t)k;
+    }
     return GBT_OK;
 }
 
@@ -195,6 +227,8 @@ gbt_status gbt_ctx_destroy(gbt_ctx *c)
     (void)hipStreamSynchronize(c->side);
     for (auto &s : c->scratch) dev_free(c, s.p, s.bytes);
     if (c->hio) (void)hipHostFree(c->hio);
+    for (void *p : c->disk_stage)
+        if (p) (void)hipHostFree(p);
     for (auto e : c->events) (void)hipEventDestroy(e);
     (void)hipStreamDestroy(c->side);
     delete c;

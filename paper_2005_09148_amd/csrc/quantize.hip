@@ -15,7 +15,10 @@
 #include "common.h"
 
 #include <algorithm>
+#include <cerrno>
 #include <cstring>
+#include <fcntl.h>
+#include <unistd.h>
 
 using namespace gbt;
 
@@ -292,6 +295,11 @@ struct gbt_quantizer {
     size_t stage_bytes = 0;
     uint32_t *enc = nullptr;         // encoded rows of one batch
     size_t enc_bytes = 0;
+    // disk pages: their directory, and a pinned buffer the encoded rows
+    // pass through on their way to the files
+    std::string dir;
+    void *bounce = nullptr;
+    size_t bounce_bytes = 0;
 };
 
 namespace {
@@ -385,6 +393,7 @@ void free_quantizer(gbt_quantizer *q)
     dev_free(c, q->st, kStWords * sizeof(unsigned long long));
     dev_free(c, q->stage, q->stage_bytes);
     dev_free(c, q->enc, q->enc_bytes);
+    if (q->bounce) (void)hipHostFree(q->bounce);
     if (q->mat) gbt_matrix_free(q->mat);
     delete q;
 }
@@ -403,13 +412,17 @@ gbt_status gbt_quantize_begin(gbt_ctx *c, const gbt_quant_params *p, int32_t n_c
     GBT_CHECK(n_rows_total >= 0, "n_rows must be >= 0");
     GBT_CHECK(input_kind == GBT_INPUT_DENSE_F32 || input_kind == GBT_INPUT_CSR_F32,
               "unknown input kind %d", input_kind);
-    GBT_CHECK(p->page_home == GBT_HOME_DEVICE || p->page_home == GBT_HOME_PINNED_HOST,
+    GBT_CHECK(p->page_home == GBT_HOME_DEVICE || p->page_home == GBT_HOME_PINNED_HOST ||
+                  p->page_home == GBT_HOME_DISK,
               "unknown page_home %d", p->page_home);
+    GBT_CHECK(p->page_home != GBT_HOME_DISK || (p->page_dir && p->page_dir[0]), "disk pages need page_dir");
     GBT_CHECK(p->page_rows >= 0 && p->sketch_max_rows >= 0, "negative page/sketch rows");
     GBT_TRY(set_device(c));
     auto *q = new gbt_quantizer();
     q->ctx = c;
     q->p = *p;
+    if (p->page_home == GBT_HOME_DISK) q->dir = p->page_dir;
+    q->p.page_dir = nullptr;  // the caller's string is not kept
     if (q->p.sketch_max_rows == 0) q->p.sketch_max_rows = (int64_t)1 << 24;
     q->m = n_cols;
     q->kind = input_kind;
@@ -809,6 +822,16 @@ gbt_status gbt_quantize_encode_batch(gbt_quantizer *q, const gbt_input *batch)
                     (void)hipGetLastError();
                     return set_error(GBT_E_OOM, "hipHostMalloc(%zu) for a page failed", pb);
                 }
+            } else if (mx->page_home == GBT_HOME_DISK) {
+                char name[64];
+                snprintf(name, sizeof name, "/gbt-%d-%llu-%zu.pages", (int)getpid(),
+                         (unsigned long long)mx->uid, mx->pages.size());
+                const std::string path = q->dir + name;
+                pg.fd = open(path.c_str(), O_RDWR | O_CREAT | O_EXCL | O_CLOEXEC, 0600);
+                if (pg.fd < 0) return set_error(GBT_E_IO, "cannot create %s: %s", path.c_str(), strerror(errno));
+                (void)unlink(path.c_str());  // the open descriptor keeps the file
+                mx->pages.push_back(pg);
+                continue;
             } else {
                 GBT_TRY(dev_alloc(c, pb, (void **)&pg.words));
             }
@@ -816,6 +839,23 @@ gbt_status gbt_quantize_encode_batch(gbt_quantizer *q, const gbt_input *batch)
         }
         int64_t take = std::min(end, p0 + prow) - r;
         GbtPage &pg = mx->pages[pi];
+        if (pg.fd >= 0) {
+            const size_t bytes = (size_t)take * mx->row_words * 4;
+            if (q->bounce_bytes < bytes) {
+                GBT_HIP(hipStreamSynchronize(c->stream));
+                if (q->bounce) GBT_HIP(hipHostFree(q->bounce));
+                q->bounce = nullptr;
+                q->bounce_bytes = 0;
+                GBT_HIP(hipHostMalloc(&q->bounce, bytes, hipHostMallocDefault));
+                q->bounce_bytes = bytes;
+            }
+            GBT_HIP(hipMemcpyAsync(q->bounce, q->enc + (r - q->encoded_rows) * mx->row_words, bytes,
+                                   hipMemcpyDeviceToHost, c->stream));
+            GBT_HIP(hipStreamSynchronize(c->stream));
+            GBT_TRY(file_write(pg.fd, q->bounce, bytes, (r - p0) * mx->row_words * 4));
+            r += take;
+            continue;
+        }
         GBT_HIP(hipMemcpyAsync(pg.words + (r - p0) * mx->row_words,
                                q->enc + (r - q->encoded_rows) * mx->row_words,
                                (size_t)take * mx->row_words * 4,
@@ -914,7 +954,13 @@ gbt_status gbt_matrix_copy_page(const gbt_matrix *mx, int32_t page, void *dst, i
               (long long)dst_words, (long long)words);
     GBT_TRY(set_device(mx->ctx));
     GBT_HIP(hipStreamSynchronize(mx->ctx->stream));
-    if (words) GBT_HIP(hipMemcpy(dst, pg.words, (size_t)words * 4, hipMemcpyDefault));
+    if (words && pg.fd >= 0) {
+        std::vector<uint32_t> tmp((size_t)words);
+        GBT_TRY(file_read(pg.fd, tmp.data(), (size_t)words * 4, 0));
+        GBT_HIP(hipMemcpy(dst, tmp.data(), (size_t)words * 4, hipMemcpyDefault));
+    } else if (words) {
+        GBT_HIP(hipMemcpy(dst, pg.words, (size_t)words * 4, hipMemcpyDefault));
+    }
     return GBT_OK;
 }
 
@@ -926,7 +972,9 @@ gbt_status gbt_matrix_free(gbt_matrix *mx)
     (void)hipStreamSynchronize(c->stream);
     (void)hipStreamSynchronize(c->side);
     for (auto &pg : mx->pages) {
-        if (pg.host)
+        if (pg.fd >= 0)
+            (void)close(pg.fd);
+        else if (pg.host)
             (void)hipHostFree(pg.words);
         else
             dev_free(c, pg.words, (size_t)std::max<int64_t>(pg.rows, 1) * mx->row_words * 4);

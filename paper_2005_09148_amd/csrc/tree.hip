@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstring>
 #include <functional>
+#include <future>
 
 #include "sample_impl.h"
 #include "hist_impl.h"
@@ -45,7 +46,7 @@ gbt_status for_each_chunk(gbt_ctx *c, const gbt_matrix *mx, const ChunkFn &fn, d
     };
     std::vector<Chunk> host_chunks;
     for (const auto &pg : mx->pages) {
-        if (!pg.host) {
+        if (!pg.streamed()) {
             if (pg.rows) GBT_TRY(fn(pg.words, pg.row0, pg.rows));
             continue;
         }
@@ -55,7 +56,23 @@ gbt_status for_each_chunk(gbt_ctx *c, const gbt_matrix *mx, const ChunkFn &fn, d
     if (host_chunks.empty()) return GBT_OK;
     const size_t row_bytes = (size_t)mx->row_words * 4;
     int64_t maxrows = 0;
-    for (auto &ch : host_chunks) maxrows = std::max(maxrows, ch.rows);
+    bool disk = false;
+    for (auto &ch : host_chunks) {
+        maxrows = std::max(maxrows, ch.rows);
+        disk = disk || ch.pg->fd >= 0;
+    }
+    if (disk && c->disk_stage_bytes < (size_t)maxrows * row_bytes) {
+        // pinned buffers the page files are read into (grow-only)
+        GBT_HIP(hipStreamSynchronize(c->side));
+        GBT_HIP(hipStreamSynchronize(c->stream));
+        for (void *&p : c->disk_stage) {
+            if (p) GBT_HIP(hipHostFree(p));
+            p = nullptr;
+        }
+        c->disk_stage_bytes = 0;
+        for (void *&p : c->disk_stage) GBT_HIP(hipHostMalloc(&p, (size_t)maxrows * row_bytes, hipHostMallocDefault));
+        c->disk_stage_bytes = (size_t)maxrows * row_bytes;
+    }
     uint32_t *buf[2];
     GBT_TRY(scratch(c, kScrStage0, (size_t)maxrows * row_bytes, (void **)&buf[0]));
     GBT_TRY(scratch(c, kScrStage1, (size_t)maxrows * row_bytes, (void **)&buf[1]));
@@ -67,24 +84,51 @@ gbt_status for_each_chunk(gbt_ctx *c, const gbt_matrix *mx, const ChunkFn &fn, d
     // the buffers may still be read by earlier work on the compute stream
     GBT_HIP(hipEventRecord(ev.consumed[0], c->stream));
     GBT_HIP(hipEventRecord(ev.consumed[1], c->stream));
+    GBT_HIP(hipEventRecord(ev.copied[0], c->side));
+    GBT_HIP(hipEventRecord(ev.copied[1], c->side));
+    // A disk chunk is first read into pinned buffer k & 1 by a worker
+    // thread (once the copy of chunk k - 2 out of that buffer is done), so
+    // that the file read overlaps the device's work on the chunk before it.
+    std::future<gbt_status> reading;
+    auto start_read = [&](size_t k) -> gbt_status {
+        const Chunk &ch = host_chunks[k];
+        int b = (int)(k & 1);
+        GBT_HIP(hipEventSynchronize(ev.copied[b]));
+        const int fd = ch.pg->fd;
+        void *dst = c->disk_stage[b];
+        const size_t bytes = (size_t)ch.rows * row_bytes;
+        const int64_t off = ch.off * (int64_t)row_bytes;
+        reading = std::async(std::launch::async, [=] { return file_read(fd, dst, bytes, off); });
+        return GBT_OK;
+    };
     auto issue = [&](size_t k) -> gbt_status {
         const Chunk &ch = host_chunks[k];
         int b = (int)(k & 1);
+        const void *src = ch.pg->words + ch.off * mx->row_words;
+        if (ch.pg->fd >= 0) {
+            if (reading.get() != GBT_OK) return set_error(GBT_E_IO, "reading a page file failed");
+            src = c->disk_stage[b];
+        }
         GBT_HIP(hipStreamWaitEvent(c->side, ev.consumed[b], 0));
-        GBT_HIP(hipMemcpyAsync(buf[b], ch.pg->words + ch.off * mx->row_words, (size_t)ch.rows * row_bytes,
-                               hipMemcpyHostToDevice, c->side));
+        GBT_HIP(hipMemcpyAsync(buf[b], src, (size_t)ch.rows * row_bytes, hipMemcpyHostToDevice, c->side));
         GBT_HIP(hipEventRecord(ev.copied[b], c->side));
         if (h2d_bytes) *h2d_bytes += (double)ch.rows * row_bytes;
         return GBT_OK;
     };
+    auto on_disk = [&](size_t k) { return host_chunks[k].pg->fd >= 0; };
+    if (on_disk(0)) GBT_TRY(start_read(0));
     GBT_TRY(issue(0));
     for (size_t k = 0; k < host_chunks.size(); ++k) {
-        if (k + 1 < host_chunks.size()) GBT_TRY(issue(k + 1));
+        const bool next = k + 1 < host_chunks.size();
+        // pinned chunks: the next copy goes out before this chunk's work;
+        // disk chunks: the next read runs during it, its copy after it
+        if (next) GBT_TRY(on_disk(k + 1) ? start_read(k + 1) : issue(k + 1));
         int b = (int)(k & 1);
         GBT_HIP(hipStreamWaitEvent(c->stream, ev.copied[b], 0));
         const Chunk &ch = host_chunks[k];
         GBT_TRY(fn(buf[b], ch.pg->row0 + ch.off, ch.rows));
         GBT_HIP(hipEventRecord(ev.consumed[b], c->stream));
+        if (next && on_disk(k + 1)) GBT_TRY(issue(k + 1));
     }
     // keep the events alive until the side stream is done with them
     GBT_HIP(hipStreamSynchronize(c->side));
@@ -97,7 +141,7 @@ static gbt_status reserve_stage(gbt_ctx *c, const gbt_matrix *mx)
 {
     int64_t maxrows = 0;
     for (const auto &pg : mx->pages)
-        if (pg.host) maxrows = std::max(maxrows, std::min(pg.rows, g_stream_chunk_rows));
+        if (pg.streamed()) maxrows = std::max(maxrows, std::min(pg.rows, g_stream_chunk_rows));
     if (maxrows == 0) return GBT_OK;
     void *p;
     GBT_TRY(scratch(c, kScrStage0, (size_t)maxrows * mx->row_words * 4, &p));
@@ -107,13 +151,13 @@ static gbt_status reserve_stage(gbt_ctx *c, const gbt_matrix *mx)
 
 static bool all_device_single(const gbt_matrix *mx)
 {
-    return mx->pages.size() == 1 && !mx->pages[0].host;
+    return mx->pages.size() == 1 && !mx->pages[0].streamed();
 }
 
 static bool any_host_pages(const gbt_matrix *mx)
 {
     for (auto &pg : mx->pages)
-        if (pg.host) return true;
+        if (pg.streamed()) return true;
     return false;
 }
 
@@ -223,7 +267,8 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
         GBT_TRY(bufs.get(kScrSel, (size_t)std::max<int64_t>(o->R, 1) * 4, (void **)&o->sel));
         GBT_TRY(bufs.get(kScrGw, (size_t)std::max<int64_t>(o->R, 1) * 16, (void **)&o->gw));
         o->page = spage;
-        const bool host = any_host_pages(mx);
+        // (disk pages have no device mapping: they always stream)
+        const bool host = any_host_pages(mx) && mx->page_home == GBT_HOME_PINNED_HOST;
         const bool gather = host && (c->compaction == GBT_COMPACT_GATHER ||
                                      (c->compaction == GBT_COMPACT_AUTO && 2 * (int64_t)o->R <= n));
         if (gather) {
@@ -1487,7 +1532,7 @@ static gbt_status train_tree_naive_impl(gbt_ctx *c, const gbt_matrix *mx, const 
     const int32_t max_level = 1 << D;
     int64_t chunk_rows = 1;  // the largest chunk for_each_chunk passes
     for (const auto &pg : mx->pages)
-        chunk_rows = std::max(chunk_rows, pg.host ? std::min(pg.rows, g_stream_chunk_rows) : pg.rows);
+        chunk_rows = std::max(chunk_rows, pg.streamed() ? std::min(pg.rows, g_stream_chunk_rows) : pg.rows);
     GBT_TRY(scratch_t(c, kScrNodes, (size_t)NN, &nodes));
     GBT_TRY(scratch_t(c, kScrPosition, (size_t)std::max<int64_t>(n, 1), &position));
     GBT_TRY(scratch_t(c, kScrSlotNode, (size_t)NN, &slot_of));

@@ -23,6 +23,7 @@ GBT_E_OOM = -2
 GBT_E_BUDGET = -3
 GBT_E_DEVICE = -4
 GBT_E_UNSUPPORTED = -5
+GBT_E_IO = -6
 
 INPUT_DENSE = 0
 INPUT_CSR = 1
@@ -30,6 +31,7 @@ LOC_HOST = 0
 LOC_DEVICE = 1
 HOME_DEVICE = 0
 HOME_PINNED_HOST = 1
+HOME_DISK = 2
 LOSS_LOGISTIC = 0
 LOSS_SQUARED = 1
 SAMPLE_MVS = 0
@@ -55,7 +57,12 @@ class Input(C.Structure):
 
 class QuantParams(C.Structure):
     _fields_ = [("max_bin", C.c_int32), ("page_home", C.c_int32),
-                ("sketch_max_rows", C.c_int64), ("page_rows", C.c_int64)]
+                ("sketch_max_rows", C.c_int64), ("page_rows", C.c_int64), ("page_dir", C.c_char_p)]
+
+
+def _quant_params(max_bin, page_home, sketch_max_rows, page_rows, page_dir):
+    return QuantParams(max_bin, page_home, sketch_max_rows, page_rows,
+                       None if page_dir is None else os.fsencode(page_dir))
 
 
 class MatrixInfo(C.Structure):
@@ -381,15 +388,16 @@ class Matrix:
 
 
 def gbt_quantize(ctx: Context, data, max_bin=256, page_rows=0, page_home=HOME_DEVICE,
-                 sketch_max_rows=0) -> Matrix:
+                 sketch_max_rows=0, page_dir=None) -> Matrix:
     """Sec. 3.1-3.2: quantile cuts and ELLPACK pages of dense X (numpy host
-    array or device tensor) or CSR (a dict kind='csr')."""
+    array or device tensor) or CSR (a dict kind='csr'); HOME_DISK pages live
+    in files under page_dir."""
     if isinstance(data, dict):
         loc = LOC_HOST if isinstance(data["indptr"], np.ndarray) else LOC_DEVICE
         inp, keep = csr_input(data["indptr"], data["indices"], data["values"], data["m"], loc)
     else:
         inp, keep = dense_input(data)
-    qp = QuantParams(max_bin, page_home, sketch_max_rows, page_rows)
+    qp = _quant_params(max_bin, page_home, sketch_max_rows, page_rows, page_dir)
     h = C.c_void_p()
     _check(_lib.gbt_quantize(ctx.h, C.byref(inp), C.byref(qp), C.byref(h)))
     del keep
@@ -400,9 +408,9 @@ class Quantizer:
     """Incremental quantization (Alg. 3 sketch batches, then Alg. 5 pages)."""
 
     def __init__(self, ctx, n_cols, n_rows_total, max_bin=256, page_rows=0,
-                 page_home=HOME_DEVICE, sketch_max_rows=0, kind=INPUT_DENSE):
+                 page_home=HOME_DEVICE, sketch_max_rows=0, kind=INPUT_DENSE, page_dir=None):
         self.ctx = ctx
-        qp = QuantParams(max_bin, page_home, sketch_max_rows, page_rows)
+        qp = _quant_params(max_bin, page_home, sketch_max_rows, page_rows, page_dir)
         h = C.c_void_p()
         _check(_lib.gbt_quantize_begin(ctx.h, C.byref(qp), n_cols, n_rows_total, kind,
                                        C.byref(h)))

@@ -3,6 +3,8 @@ the CPU oracle on the same seeded inputs.  Integer results (cuts, pages,
 selections, fixed-point gradients, histograms, partitions, chosen splits)
 must be bit-exact; floating-point results are computed by the same IEEE
 operations on both sides and must be bit-exact too."""
+import os
+
 import numpy as np
 import pytest
 
@@ -103,12 +105,12 @@ def test_quantize_csr(gbt, ctx, n, m, density, max_bin):
     assert same_bits(mx.page(0), page)
 
 
-@pytest.mark.parametrize("home", ["device", "pinned"])
-def test_quantize_pages_and_batches(gbt, ctx, home):
+@pytest.mark.parametrize("home", ["device", "pinned", "disk"])
+def test_quantize_pages_and_batches(gbt, ctx, home, tmp_path):
     X = dense_case(7, 5000, 11, 0.1)
     _, _, _, page = oracle_quantize(X, 64)
-    h = gbt.HOME_DEVICE if home == "device" else gbt.HOME_PINNED_HOST
-    q = gbt.Quantizer(ctx, 11, 5000, max_bin=64, page_rows=1536, page_home=h)
+    h = {"device": gbt.HOME_DEVICE, "pinned": gbt.HOME_PINNED_HOST, "disk": gbt.HOME_DISK}[home]
+    q = gbt.Quantizer(ctx, 11, 5000, max_bin=64, page_rows=1536, page_home=h, page_dir=str(tmp_path))
     for lo in range(0, 5000, 1300):
         q.sketch(X[lo:lo + 1300])
     q.finalize()
@@ -448,11 +450,11 @@ def test_partition(gbt, ctx):
 
 
 # ------------------------------------------------------------ whole trees
-def train_both(gbt, ctx, data, y, cfg, n_trees, page_rows=0, home=0, budget_ctx=None):
+def train_both(gbt, ctx, data, y, cfg, n_trees, page_rows=0, home=0, budget_ctx=None, page_dir=None):
     c = budget_ctx or ctx
     mb = cfg.max_bin
     _, b, _, _ = oracle_quantize(data, mb)
-    mx = gbt.gbt_quantize(c, data, max_bin=mb, page_rows=page_rows, page_home=home)
+    mx = gbt.gbt_quantize(c, data, max_bin=mb, page_rows=page_rows, page_home=home, page_dir=page_dir)
     P = gbt.make_train_params(loss=cfg.loss, max_depth=cfg.max_depth, eta=cfg.eta, lambda_=cfg.lambda_,
                               gamma=cfg.gamma, min_child_weight=cfg.min_child_weight, f=cfg.f,
                               mvs_lambda=cfg.mvs_lambda, seed=cfg.seed)
@@ -517,6 +519,32 @@ def test_mvs_lambda_estimate(gbt, ctx, loss, n, margins):
     want = orc.mvs_lambda_estimate(loss, m, y)
     assert same_bits(np.float64(got), np.float64(want)), (got, want)
     assert n == 0 or got > 0
+
+
+@pytest.mark.parametrize("f", [0.3, 1.0])
+def test_disk_pages_match_oracle(gbt, ctx, f, tmp_path):
+    # Sec. 3.2: pages in files, read back through pinned staging each tree,
+    # give the oracle's pages and trees; the files are unlinked at once
+    cfg = datagen.TrainConfig("t", 0, 256, 6, 3, eta=0.1, f=f)
+    d = datagen.config2(n=20_000)
+    r = train_both(gbt, ctx, d["X"], d["y"], cfg, 3, page_rows=3000, home=gbt.HOME_DISK, page_dir=str(tmp_path))
+    assert_same_trees(*r[:4])
+    mx, b = r[4], r[5]
+    assert mx.info().page_home == gbt.HOME_DISK and mx.info().n_pages == 7
+    assert same_bits(mx.pages(), orc.ellpack(b, orc.ellpack_geometry(b)))
+    assert os.listdir(tmp_path) == []
+    assert all(t.stats.h2d_bytes > 0 for t in r[0])
+    if f == 1.0:
+        # Alg. 6 over the disk pages: every level reads every file
+        trees, margin = train_naive(gbt, ctx, mx, d["y"], cfg, 2)
+        OP = orc.Params(loss=cfg.loss, max_depth=cfg.max_depth, eta=cfg.eta, lambda_=cfg.lambda_,
+                        gamma=cfg.gamma, min_child_weight=cfg.min_child_weight, f=1.0, seed=cfg.seed)
+        otrees, omargin = orc.train(b, d["y"], OP, 2, cfg.base_margin)
+        assert_same_trees(trees, margin.cpu().numpy(), otrees, omargin)
+    with pytest.raises(gbt.GbtError):
+        gbt.gbt_quantize(ctx, d["X"][:100], page_home=gbt.HOME_DISK)
+    with pytest.raises(gbt.GbtError):
+        gbt.gbt_quantize(ctx, d["X"][:100], page_home=gbt.HOME_DISK, page_dir=str(tmp_path / "absent"))
 
 
 @pytest.mark.parametrize("f", [0.3, 1.0])
