@@ -98,7 +98,21 @@ gbt_status for_each_chunk(gbt_ctx *c, const gbt_matrix *mx, const ChunkFn &fn, d
         void *dst = c->disk_stage[b];
         const size_t bytes = (size_t)ch.rows * row_bytes;
         const int64_t off = ch.off * (int64_t)row_bytes;
-        reading = std::async(std::launch::async, [=] { return file_read(fd, dst, bytes, off); });
+        reading = std::async(std::launch::async, [=] {
+            // in kReadParts pieces at once (page-aligned), this thread
+            // reading the first
+            constexpr size_t kReadParts = 8;
+            if (bytes == 0) return GBT_OK;
+            const size_t part = (bytes / kReadParts + 4095) & ~(size_t)4095;
+            std::vector<std::future<gbt_status>> rest;
+            for (size_t o = part; o < bytes; o += part)
+                rest.push_back(std::async(std::launch::async, file_read, fd, (char *)dst + o,
+                                          std::min(part, bytes - o), off + (int64_t)o));
+            gbt_status s = file_read(fd, dst, std::min(part, bytes), off);
+            for (auto &f : rest)
+                if (f.get() != GBT_OK) s = GBT_E_IO;
+            return s;
+        });
         return GBT_OK;
     };
     auto issue = [&](size_t k) -> gbt_status {
