@@ -48,3 +48,49 @@ def test_oracle_is_not_imported_by_the_product():
                 text = open(os.path.join(dirpath, f)).read()
                 assert "from oracle" not in text and "import oracle" not in text, f
                 assert "gbt_oracle" not in text, f
+
+
+def _c_layout(names):
+    """sizeof and the #define/enum constants of include/gbt.h, from a C
+    program compiled with the host compiler."""
+    import subprocess
+    import tempfile
+    structs = [s for s, _ in names]
+    consts = ["GBT_E_INVALID", "GBT_E_OOM", "GBT_E_BUDGET", "GBT_E_DEVICE", "GBT_E_UNSUPPORTED", "GBT_E_IO",
+              "GBT_HOME_DEVICE", "GBT_HOME_PINNED_HOST", "GBT_HOME_DISK", "GBT_COMPACT_AUTO",
+              "GBT_COMPACT_STREAM", "GBT_COMPACT_GATHER", "GBT_SAMPLE_MVS", "GBT_SAMPLE_SGB", "GBT_SAMPLE_GOSS",
+              "GBT_HIST_AUTO", "GBT_HIST_PLAIN", "GBT_HIST_ROTATED"]
+    body = "".join(f'printf("{s} %zu\\n", sizeof({s}));' for s in structs)
+    body += "".join(f'printf("{k} %d\\n", (int)({k}));' for k in consts)
+    with tempfile.TemporaryDirectory() as d:
+        src, exe = os.path.join(d, "layout.c"), os.path.join(d, "layout")
+        with open(src, "w") as fh:
+            fh.write('#include <stdio.h>\n#include "gbt.h"\nint main(void){' + body + "return 0;}\n")
+        subprocess.run(["gcc", "-std=c11", "-I", os.path.dirname(HEADER), src, "-o", exe], check=True)
+        out = subprocess.run([exe], check=True, capture_output=True, text=True).stdout
+    return dict((k, int(v)) for k, v in (line.split() for line in out.splitlines()))
+
+
+def test_binding_layouts_and_constants_match_the_header():
+    # the ctypes mirrors of the header's structs and constants (host logic:
+    # a layout drift would pass garbage through the boundary)
+    from paper_2005_09148_amd import gbt
+    pairs = [("gbt_input", gbt.Input), ("gbt_quant_params", gbt.QuantParams),
+             ("gbt_matrix_info", gbt.MatrixInfo), ("gbt_train_params", gbt.TrainParams),
+             ("gbt_seg", gbt.Seg), ("gbt_sub", gbt.Sub), ("gbt_split", gbt.Split), ("gbt_tree", gbt.Tree),
+             ("gbt_tree_stats", gbt.TreeStats), ("gbt_sample_params", gbt.SampleParams),
+             ("gbt_sampled_info", gbt.SampledInfo)]
+    c = _c_layout(pairs + [("gbt_node", None)])
+    for name, cls in pairs:
+        assert c[name] == ctypes.sizeof(cls), name
+    assert c["gbt_node"] == gbt.NODE_DTYPE.itemsize and c["gbt_split"] == gbt.SPLIT_DTYPE.itemsize
+    py = {"GBT_E_INVALID": gbt.GBT_E_INVALID, "GBT_E_OOM": gbt.GBT_E_OOM, "GBT_E_BUDGET": gbt.GBT_E_BUDGET,
+          "GBT_E_DEVICE": gbt.GBT_E_DEVICE, "GBT_E_UNSUPPORTED": gbt.GBT_E_UNSUPPORTED, "GBT_E_IO": gbt.GBT_E_IO,
+          "GBT_HOME_DEVICE": gbt.HOME_DEVICE, "GBT_HOME_PINNED_HOST": gbt.HOME_PINNED_HOST,
+          "GBT_HOME_DISK": gbt.HOME_DISK, "GBT_SAMPLE_MVS": gbt.SAMPLE_MVS, "GBT_SAMPLE_SGB": gbt.SAMPLE_SGB,
+          "GBT_SAMPLE_GOSS": gbt.SAMPLE_GOSS, "GBT_COMPACT_AUTO": gbt.Context.COMPACT_AUTO,
+          "GBT_COMPACT_STREAM": gbt.Context.COMPACT_STREAM, "GBT_COMPACT_GATHER": gbt.Context.COMPACT_GATHER,
+          "GBT_HIST_AUTO": gbt.Context.HIST_AUTO, "GBT_HIST_PLAIN": gbt.Context.HIST_PLAIN,
+          "GBT_HIST_ROTATED": gbt.Context.HIST_ROTATED}
+    for k, v in py.items():
+        assert c[k] == v, k
