@@ -262,6 +262,15 @@ gbt_status gbt_ctx_set_hist_kernel(gbt_ctx *ctx, int32_t choice);
 #define GBT_COMPACT_GATHER 2
 gbt_status gbt_ctx_set_compaction(gbt_ctx *ctx, int32_t mode);
 
+/* Rows per chunk when pages held in pinned host memory or on disk are
+ * streamed through the device (Sec. 3.3-3.4: pages are processed in
+ * batches; Alg. 7's compaction and the margin update stream them): each
+ * chunk is copied (or read from its file, then copied) into one of two
+ * device staging buffers of this many rows on the side stream while the
+ * previous chunk is processed.  0 restores the default 2^22; results do not
+ * depend on the value.  GBT_E_INVALID for rows < 0 or > 2^30. */
+gbt_status gbt_ctx_set_stream_chunk_rows(gbt_ctx *ctx, int64_t rows);
+
 /* ---- quantile cuts and ELLPACK pages: Sec. 2.2, Sec. 3.1 (Alg. 2, 3),
  * Sec. 3.2 (Alg. 4, 5) ------------------------------------------------------
  * Cuts are exact quantiles of a sketch sample: for a feature with sorted

@@ -10,7 +10,12 @@
  * design notes.
  *
  * Built with -O2 -ffp-contract=off and no fast-math, so every floating-point
- * operation is the single IEEE operation written here.  Single threaded.
+ * operation is the single IEEE operation written here.  The plain build is
+ * single threaded.  A second build with -fopenmp spreads the loops marked
+ * "omp" over threads; each such loop either treats rows (or features)
+ * independently or reduces integers or maxima, whose results do not depend
+ * on the order, so both builds return the same bits (a CPU test checks
+ * whole trees).
  *
  * Contents, in the order the paper presents them:
  *   orc_exp / orc_philox4x64_10 ...... helpers (Cody-Waite exp; Philox of
@@ -38,6 +43,9 @@
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 
 #define ORC_OK 0
 #define ORC_EINVAL (-1)
@@ -51,6 +59,18 @@
 #define ORC_NODE_PRESENT 1u
 #define ORC_NODE_LEAF 2u
 #define ORC_NODE_DEFAULT_LEFT 4u
+
+/* Threads of the omp build (n > 0 sets them); 1 for the plain build. */
+int32_t orc_threads(int32_t n)
+{
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+    return (int32_t)omp_get_max_threads();
+#else
+    (void)n;
+    return 1;
+#endif
+}
 
 /* ------------------------------------------------------------------------ */
 /* Data types shared with oracle.py (ctypes mirrors them field by field).    */
@@ -239,26 +259,48 @@ int orc_sketch_cuts_dense(const float *X, int64_t n, int32_t m, int64_t ld, int3
 {
     if (n < 0 || m <= 0 || max_bin < 2 || ld < m) return ORC_EINVAL;
     int64_t stride = sketch_stride(n, sketch_max_rows);
-    float *vals = (float *)malloc(sizeof(float) * (size_t)(n / stride + 1));
-    if (!vals) return ORC_ENOMEM;
-    cut_ptr[0] = 0;
+    /* each feature's cuts go to its own max_bin-1 slots first, then are
+     * packed in feature order */
+    float *tmp = (float *)malloc(sizeof(float) * (size_t)m * (size_t)(max_bin - 1));
+    int32_t *cnt = (int32_t *)malloc(sizeof(int32_t) * (size_t)m);
+    if (!tmp || !cnt) {
+        free(tmp);
+        free(cnt);
+        return ORC_ENOMEM;
+    }
+    int bad = 0, oom = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : bad, oom)
     for (int32_t j = 0; j < m; ++j) {
+        float *vals = (float *)malloc(sizeof(float) * (size_t)(n / stride + 1));
+        cnt[j] = 0;
+        if (!vals) {
+            oom = 1;
+            continue;
+        }
         int64_t N = 0;
         for (int64_t i = 0; i < n; i += stride) {
             float x = X[i * ld + j];
             if (isnan(x)) continue;
             if (isinf(x)) {
-                free(vals);
-                return ORC_EINVAL;
+                bad = 1;
+                break;
             }
             if (x == 0.0f) x = 0.0f; /* -0 -> +0 */
             vals[N++] = x;
         }
-        int32_t c = cuts_from_values(vals, N, max_bin, cut_values + cut_ptr[j]);
-        cut_ptr[j + 1] = cut_ptr[j] + c;
+        cnt[j] = cuts_from_values(vals, N, max_bin, tmp + (size_t)j * (size_t)(max_bin - 1));
+        free(vals);
     }
-    free(vals);
-    return ORC_OK;
+    if (!bad && !oom) {
+        cut_ptr[0] = 0;
+        for (int32_t j = 0; j < m; ++j) {
+            memcpy(cut_values + cut_ptr[j], tmp + (size_t)j * (size_t)(max_bin - 1), sizeof(float) * (size_t)cnt[j]);
+            cut_ptr[j + 1] = cut_ptr[j] + cnt[j];
+        }
+    }
+    free(tmp);
+    free(cnt);
+    return oom ? ORC_ENOMEM : (bad ? ORC_EINVAL : ORC_OK);
 }
 
 /* CSR float input: absent entries and NaN values are missing. */
@@ -301,12 +343,27 @@ int orc_sketch_cuts_csr(const int64_t *indptr, const int32_t *indices, const flo
             if (x == 0.0f) x = 0.0f;
             vals[fill[indices[e]]++] = x;
         }
+    float *tmp = (float *)malloc(sizeof(float) * (size_t)m * (size_t)(max_bin - 1));
+    int32_t *nc = (int32_t *)malloc(sizeof(int32_t) * (size_t)m);
+    if (!tmp || !nc) {
+        free(vals);
+        free(fill);
+        free(cnt);
+        free(tmp);
+        free(nc);
+        return ORC_ENOMEM;
+    }
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int32_t j = 0; j < m; ++j)
+        nc[j] = cuts_from_values(vals + cnt[j], cnt[j + 1] - cnt[j], max_bin,
+                                 tmp + (size_t)j * (size_t)(max_bin - 1));
     cut_ptr[0] = 0;
     for (int32_t j = 0; j < m; ++j) {
-        int32_t c = cuts_from_values(vals + cnt[j], cnt[j + 1] - cnt[j], max_bin,
-                                     cut_values + cut_ptr[j]);
-        cut_ptr[j + 1] = cut_ptr[j] + c;
+        memcpy(cut_values + cut_ptr[j], tmp + (size_t)j * (size_t)(max_bin - 1), sizeof(float) * (size_t)nc[j]);
+        cut_ptr[j + 1] = cut_ptr[j] + nc[j];
     }
+    free(tmp);
+    free(nc);
     free(vals);
     free(fill);
     free(cnt);
@@ -332,15 +389,17 @@ static int32_t lookup_bin(const float *cuts, int32_t nc, float x)
 int orc_bin_dense(const float *X, int64_t n, int32_t m, int64_t ld, const int32_t *cut_ptr,
                   const float *cut_values, uint16_t *bins)
 {
+    int bad = 0;
+#pragma omp parallel for schedule(static) reduction(| : bad)
     for (int64_t i = 0; i < n; ++i)
         for (int32_t j = 0; j < m; ++j) {
             float x = X[i * ld + j];
-            if (isinf(x)) return ORC_EINVAL;
-            bins[i * m + j] = isnan(x) ? (uint16_t)ORC_MISSING
-                                       : (uint16_t)lookup_bin(cut_values + cut_ptr[j],
-                                                              cut_ptr[j + 1] - cut_ptr[j], x);
+            if (isinf(x)) bad = 1;
+            bins[i * m + j] = isnan(x) || isinf(x) ? (uint16_t)ORC_MISSING
+                                                   : (uint16_t)lookup_bin(cut_values + cut_ptr[j],
+                                                                          cut_ptr[j + 1] - cut_ptr[j], x);
         }
-    return ORC_OK;
+    return bad ? ORC_EINVAL : ORC_OK;
 }
 
 /* CSR raw -> CSR bins.  NaN entries are dropped (they are missing), so the
@@ -478,6 +537,7 @@ int orc_gradients(int32_t loss, const float *margin, const float *label, const f
                   int64_t n, float *gpair)
 {
     if (loss != ORC_LOSS_LOGISTIC && loss != ORC_LOSS_SQUARED) return ORC_EINVAL;
+#pragma omp parallel for schedule(static)
     for (int64_t i = 0; i < n; ++i) {
         double z = (double)margin[i];
         double y = (double)label[i];
@@ -522,15 +582,19 @@ int orc_gradients(int32_t loss, const float *margin, const float *label, const f
 int orc_mvs_keys(const float *gpair, int64_t n, double mvs_lambda, int64_t *keys, int32_t *e_out)
 {
     double M = 0.0;
+    int bad = 0;
+#pragma omp parallel for schedule(static) reduction(max : M) reduction(| : bad)
     for (int64_t i = 0; i < n; ++i) {
         double g = (double)gpair[2 * i], h = (double)gpair[2 * i + 1];
         double r = sqrt(g * g + mvs_lambda * (h * h));
-        if (isnan(r) || isinf(r)) return ORC_EINVAL;
-        if (r > M) M = r;
+        if (isnan(r) || isinf(r)) bad = 1;
+        else if (r > M) M = r;
     }
+    if (bad) return ORC_EINVAL;
     int E;
     frexp(M, &E); /* M < 2^E (E = 0 when M = 0) */
     int32_t e = 62 - E - ceil_log2_i64(n);
+#pragma omp parallel for schedule(static)
     for (int64_t i = 0; i < n; ++i) {
         double g = (double)gpair[2 * i], h = (double)gpair[2 * i + 1];
         double r = sqrt(g * g + mvs_lambda * (h * h));
@@ -551,11 +615,22 @@ static int threshold_ok(const int64_t *keys, int64_t n, int64_t K, int64_t T)
 {
     int64_t C = 0;
     __int128 F = 0;
-    for (int64_t i = 0; i < n; ++i) {
-        if (keys[i] >= T)
-            ++C;
-        else
-            F += keys[i];
+#pragma omp parallel
+    {
+        int64_t c = 0;
+        __int128 f = 0;
+#pragma omp for schedule(static) nowait
+        for (int64_t i = 0; i < n; ++i) {
+            if (keys[i] >= T)
+                ++c;
+            else
+                f += keys[i];
+        }
+#pragma omp critical
+        {
+            C += c;
+            F += f;
+        }
     }
     return F <= (__int128)(K - C) * (__int128)T;
 }
@@ -565,9 +640,20 @@ int64_t orc_mvs_threshold(const int64_t *keys, int64_t n, int64_t K)
 {
     __int128 sum = 0;
     int64_t mx = 0;
-    for (int64_t i = 0; i < n; ++i) {
-        sum += keys[i];
-        if (keys[i] > mx) mx = keys[i];
+#pragma omp parallel
+    {
+        __int128 s = 0;
+        int64_t x = 0;
+#pragma omp for schedule(static) nowait
+        for (int64_t i = 0; i < n; ++i) {
+            s += keys[i];
+            if (keys[i] > x) x = keys[i];
+        }
+#pragma omp critical
+        {
+            sum += s;
+            if (x > mx) mx = x;
+        }
     }
     /* at T = hi every key is below T and sum/T <= K, so hi satisfies it */
     __int128 hi = (__int128)mx + 1;
@@ -595,6 +681,7 @@ uint64_t orc_mvs_uniform(uint64_t seed, uint64_t iteration, uint64_t row)
 void orc_mvs_select(const int64_t *keys, int64_t n, int64_t T, uint64_t seed, uint64_t iteration,
                     int64_t row_offset, uint8_t *keep)
 {
+#pragma omp parallel for schedule(static)
     for (int64_t i = 0; i < n; ++i) {
         int64_t a = keys[i];
         if (a >= T) {
@@ -683,6 +770,7 @@ double orc_goss_weight(int64_t key, int64_t T_top, double a, double b)
 static int32_t fx_exponent(const double *x, int64_t R, int64_t stride)
 {
     double M = 0.0;
+#pragma omp parallel for schedule(static) reduction(max : M)
     for (int64_t i = 0; i < R; ++i) {
         double a = fabs(x[i * stride]);
         if (a > M) M = a;
@@ -695,6 +783,7 @@ static int32_t fx_exponent(const double *x, int64_t R, int64_t stride)
 void orc_fixed_point(const double *gw, int64_t R, int64_t *q, int32_t *e_g, int32_t *e_h)
 {
     int32_t eg = fx_exponent(gw, R, 2), eh = fx_exponent(gw + 1, R, 2);
+#pragma omp parallel for schedule(static)
     for (int64_t i = 0; i < R; ++i) {
         q[2 * i] = (int64_t)rint(ldexp(gw[2 * i], eg));
         q[2 * i + 1] = (int64_t)rint(ldexp(gw[2 * i + 1], eh));
@@ -726,23 +815,38 @@ void orc_build_hist(const orc_data *d, const int64_t *rows, int64_t n_rows, cons
     int64_t *off = (int64_t *)malloc(sizeof(int64_t) * (size_t)(d->m + 1));
     int64_t tb = total_bins(d, off);
     memset(hist, 0, sizeof(int64_t) * (size_t)(2 * tb));
-    for (int64_t k = 0; k < n_rows; ++k) {
-        int64_t r = rows[k];
-        int64_t qg = q[2 * r], qh = q[2 * r + 1];
-        if (d->dense) {
-            for (int32_t j = 0; j < d->m; ++j) {
-                uint16_t b = d->dense[r * d->m + j];
-                if (b == ORC_MISSING) continue;
-                hist[2 * (off[j] + b)] += qg;
-                hist[2 * (off[j] + b) + 1] += qh;
-            }
-        } else {
-            for (int64_t e = d->indptr[r]; e < d->indptr[r + 1]; ++e) {
-                int64_t gb = off[d->feat[e]] + d->bin[e];
-                hist[2 * gb] += qg;
-                hist[2 * gb + 1] += qh;
+    /* omp: each thread sums its rows into a histogram of its own, then the
+     * integer histograms are added (exact, so the order does not matter) */
+#pragma omp parallel if (n_rows >= 4096)
+    {
+        int64_t *h = hist;
+#ifdef _OPENMP
+        h = (int64_t *)calloc((size_t)(2 * tb + 2), sizeof(int64_t));
+#endif
+#pragma omp for schedule(static) nowait
+        for (int64_t k = 0; k < n_rows; ++k) {
+            int64_t r = rows[k];
+            int64_t qg = q[2 * r], qh = q[2 * r + 1];
+            if (d->dense) {
+                for (int32_t j = 0; j < d->m; ++j) {
+                    uint16_t b = d->dense[r * d->m + j];
+                    if (b == ORC_MISSING) continue;
+                    h[2 * (off[j] + b)] += qg;
+                    h[2 * (off[j] + b) + 1] += qh;
+                }
+            } else {
+                for (int64_t e = d->indptr[r]; e < d->indptr[r + 1]; ++e) {
+                    int64_t gb = off[d->feat[e]] + d->bin[e];
+                    h[2 * gb] += qg;
+                    h[2 * gb + 1] += qh;
+                }
             }
         }
+#ifdef _OPENMP
+#pragma omp critical
+        for (int64_t t = 0; t < 2 * tb; ++t) hist[t] += h[t];
+        free(h);
+#endif
     }
     free(off);
 }
@@ -773,52 +877,72 @@ static double split_gain(double GL, double HL, double GR, double HR, double G, d
     return 0.5 * ((a + b) - c) - gamma;
 }
 
-void orc_eval_node(const int64_t *hist, const int64_t node_sum[2], const int32_t *nbins, int32_t m,
-                   const orc_params *p, int32_t e_g, int32_t e_h, orc_split *out)
+/* The best candidate of one feature (the first of the highest gain in
+ * (s, direction) order); valid = 0 when it has none. */
+static orc_split eval_feature(const int64_t *hj, int32_t j, int32_t B, const int64_t node_sum[2], double G,
+                              double H, const orc_params *p, int32_t e_g, int32_t e_h)
 {
     orc_split best;
     memset(&best, 0, sizeof(best));
     best.feature = -1;
     best.split_bin = -1;
-    double G = to_double(node_sum[0], e_g), H = to_double(node_sum[1], e_h);
-    int64_t off = 0;
-    for (int32_t j = 0; j < m; ++j) {
-        const int64_t *hj = hist + 2 * off;
-        int32_t B = nbins[j];
-        off += B;
-        if (B < 2) continue;
-        int64_t tg = 0, th = 0;
-        for (int32_t b = 0; b < B; ++b) {
-            tg += hj[2 * b];
-            th += hj[2 * b + 1];
-        }
-        int64_t miss_g = node_sum[0] - tg, miss_h = node_sum[1] - th;
-        int64_t lg = 0, lh = 0;
-        for (int32_t s = 1; s < B; ++s) {
-            lg += hj[2 * (s - 1)];
-            lh += hj[2 * (s - 1) + 1];
-            for (int32_t dir = 0; dir < 2; ++dir) {
-                int64_t QLg = lg + (dir ? miss_g : 0), QLh = lh + (dir ? miss_h : 0);
-                int64_t QRg = node_sum[0] - QLg, QRh = node_sum[1] - QLh;
-                double GL = to_double(QLg, e_g), HL = to_double(QLh, e_h);
-                double GR = to_double(QRg, e_g), HR = to_double(QRh, e_h);
-                if (!(HL >= p->min_child_weight && HR >= p->min_child_weight)) continue;
-                double gain = split_gain(GL, HL, GR, HR, G, H, p->lambda, p->gamma);
-                if (isnan(gain)) continue;
-                if (!best.valid || gain > best.gain) {
-                    best.valid = 1;
-                    best.gain = gain;
-                    best.feature = j;
-                    best.split_bin = s;
-                    best.default_left = dir;
-                    best.left_g = QLg;
-                    best.left_h = QLh;
-                    best.right_g = QRg;
-                    best.right_h = QRh;
-                }
+    if (B < 2) return best;
+    int64_t tg = 0, th = 0;
+    for (int32_t b = 0; b < B; ++b) {
+        tg += hj[2 * b];
+        th += hj[2 * b + 1];
+    }
+    int64_t miss_g = node_sum[0] - tg, miss_h = node_sum[1] - th;
+    int64_t lg = 0, lh = 0;
+    for (int32_t s = 1; s < B; ++s) {
+        lg += hj[2 * (s - 1)];
+        lh += hj[2 * (s - 1) + 1];
+        for (int32_t dir = 0; dir < 2; ++dir) {
+            int64_t QLg = lg + (dir ? miss_g : 0), QLh = lh + (dir ? miss_h : 0);
+            int64_t QRg = node_sum[0] - QLg, QRh = node_sum[1] - QLh;
+            double GL = to_double(QLg, e_g), HL = to_double(QLh, e_h);
+            double GR = to_double(QRg, e_g), HR = to_double(QRh, e_h);
+            if (!(HL >= p->min_child_weight && HR >= p->min_child_weight)) continue;
+            double gain = split_gain(GL, HL, GR, HR, G, H, p->lambda, p->gamma);
+            if (isnan(gain)) continue;
+            if (!best.valid || gain > best.gain) {
+                best.valid = 1;
+                best.gain = gain;
+                best.feature = j;
+                best.split_bin = s;
+                best.default_left = dir;
+                best.left_g = QLg;
+                best.left_h = QLh;
+                best.right_g = QRg;
+                best.right_h = QRh;
             }
         }
     }
+    return best;
+}
+
+void orc_eval_node(const int64_t *hist, const int64_t node_sum[2], const int32_t *nbins, int32_t m,
+                   const orc_params *p, int32_t e_g, int32_t e_h, orc_split *out)
+{
+    double G = to_double(node_sum[0], e_g), H = to_double(node_sum[1], e_h);
+    int64_t *off = (int64_t *)malloc(sizeof(int64_t) * (size_t)(m + 1));
+    orc_split *per = (orc_split *)malloc(sizeof(orc_split) * (size_t)(m + 1));
+    off[0] = 0;
+    for (int32_t j = 0; j < m; ++j) off[j + 1] = off[j] + nbins[j];
+    /* omp: features are independent */
+#pragma omp parallel for schedule(dynamic, 4) if (off[m] >= 4096)
+    for (int32_t j = 0; j < m; ++j)
+        per[j] = eval_feature(hist + 2 * off[j], j, nbins[j], node_sum, G, H, p, e_g, e_h);
+    /* the first candidate of the highest gain in (feature, s, direction)
+     * order: features in order, strictly higher gains only */
+    orc_split best;
+    memset(&best, 0, sizeof(best));
+    best.feature = -1;
+    best.split_bin = -1;
+    for (int32_t j = 0; j < m; ++j)
+        if (per[j].valid && (!best.valid || per[j].gain > best.gain)) best = per[j];
+    free(off);
+    free(per);
     *out = best;
 }
 
@@ -1007,6 +1131,7 @@ int orc_train_tree(const orc_data *d, const float *label, float *margin, const o
     /* InitRoot: the root holds every training row; its sums are a direct
      * reduction */
     int64_t sg = 0, sh = 0;
+#pragma omp parallel for schedule(static) reduction(+ : sg, sh)
     for (int64_t k = 0; k < R; ++k) {
         sg += qt[2 * k];
         sh += qt[2 * k + 1];
@@ -1060,6 +1185,7 @@ int orc_train_tree(const orc_data *d, const float *label, float *margin, const o
     }
 
     /* Eq. 1: every one of the n rows adds its leaf to its margin */
+#pragma omp parallel for schedule(static)
     for (int64_t i = 0; i < n; ++i) {
         int64_t id = leaf_of_binned(d, i, tree);
         margin[i] = margin[i] + tree[id].leaf_value;

@@ -4,10 +4,14 @@ TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the benchmark's
 CPU-baseline leg are the only callers.  The product library never imports
 this module and this module never imports the product library.
 
-A thin ctypes layer over ``gbt_oracle.c`` (plain C, double precision,
-single-threaded, built with -O2 -ffp-contract=off).  Every function cites the
-passage of the paper it follows; the readings of passages the paper leaves
-open are written out in ``gbt_oracle.c``.
+A thin ctypes layer over ``gbt_oracle.c`` (plain C, double precision, built
+with -O2 -ffp-contract=off).  Every function cites the passage of the paper
+it follows; the readings of passages the paper leaves open are written out
+in ``gbt_oracle.c``.  Two builds of the same source: ``plain`` (single
+threaded) and ``omp`` (-fopenmp: loops over independent rows or features,
+and integer or maximum reductions, spread over threads; the same bits, which
+a CPU test checks).  ``select()`` chooses the build the functions below call;
+the default is ``omp`` unless GBT_ORACLE=plain is set.
 """
 from __future__ import annotations
 
@@ -20,7 +24,7 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "gbt_oracle.c")
-_LIB = os.path.join(_HERE, "liboracle.so")
+_LIBS = {"plain": os.path.join(_HERE, "liboracle.so"), "omp": os.path.join(_HERE, "liboracle_omp.so")}
 
 LOSS_LOGISTIC = 0
 LOSS_SQUARED = 1
@@ -31,14 +35,17 @@ MISSING = 0xFFFF
 
 
 def build(force: bool = True) -> str:
-    """Compile gbt_oracle.c into liboracle.so (plain gcc, no fast-math)."""
-    if force or not os.path.exists(_LIB):
-        tmp = _LIB + ".tmp"
-        subprocess.check_call(
-            ["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math", "-std=gnu11", "-fPIC",
-             "-shared", "-o", tmp, _SRC, "-lm"])
-        os.replace(tmp, _LIB)
-    return _LIB
+    """Compile gbt_oracle.c into liboracle.so (plain gcc, no fast-math) and
+    liboracle_omp.so (the same with -fopenmp)."""
+    for kind, path in _LIBS.items():
+        if force or not os.path.exists(path) or os.path.getmtime(path) < os.path.getmtime(_SRC):
+            tmp = path + ".tmp"
+            extra = ["-fopenmp"] if kind == "omp" else []
+            subprocess.check_call(
+                ["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math", "-std=gnu11", "-fPIC",
+                 "-shared", *extra, "-o", tmp, _SRC, "-lm"])
+            os.replace(tmp, path)
+    return _LIBS["plain"]
 
 
 class OrcData(C.Structure):
@@ -74,15 +81,34 @@ NODE_DTYPE = np.dtype([("feature", "<i4"), ("split_bin", "<i4"), ("threshold", "
                        ("pad", "u1", (3,))])
 assert NODE_DTYPE.itemsize == 48
 
-_lib = None
+_loaded = {}
+_kind = os.environ.get("GBT_ORACLE", "omp")
+if _kind not in _LIBS:
+    raise ValueError(f"GBT_ORACLE={_kind!r}: expected 'plain' or 'omp'")
+
+
+def select(kind: str) -> str:
+    """Make the functions of this module call build `kind` ('plain' or
+    'omp'); returns the previous choice."""
+    global _kind
+    if kind not in _LIBS:
+        raise ValueError(kind)
+    prev, _kind = _kind, kind
+    return prev
+
+
+def threads(n: int = 0) -> int:
+    """Threads of the omp build (n > 0 sets them); 1 for the plain build."""
+    L = lib()
+    return int(L.orc_threads(int(n)))
 
 
 def lib():
-    global _lib
-    if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-            build()
-        L = C.CDLL(_LIB)
+    if _kind not in _loaded:
+        path = _LIBS[_kind]
+        if not os.path.exists(path) or os.path.getmtime(path) < os.path.getmtime(_SRC):
+            build(force=False)
+        L = C.CDLL(path)
         vp, i64, i32, f64, u64 = C.c_void_p, C.c_int64, C.c_int32, C.c_double, C.c_uint64
         sig = {
             "orc_exp": (f64, [f64]),
@@ -116,13 +142,14 @@ def lib():
             "orc_predict_binned": (None, [vp, vp, vp, i32, C.c_float, vp]),
             "orc_predict_raw_dense": (None, [vp, i64, i64, vp, vp, i32, C.c_float, vp]),
             "orc_predict_raw_csr": (None, [vp, vp, vp, i64, vp, vp, i32, C.c_float, vp]),
+            "orc_threads": (i32, [i32]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
             fn.restype = res
             fn.argtypes = args
-        _lib = L
-    return _lib
+        _loaded[_kind] = L
+    return _loaded[_kind]
 
 
 def _p(a):

@@ -70,6 +70,7 @@ struct gbt_ctx {
     int timing = 0;  // 0 off, 1 histogram kernel only, 2 every phase
     int hist_kernel = GBT_HIST_AUTO;
     int compaction = GBT_COMPACT_AUTO;
+    int64_t stream_chunk_rows = (int64_t)1 << 22;  // rows per streamed chunk of a host or disk page
     struct Mark {
         int a, b;    // indices into events
         int phase;

@@ -268,4 +268,14 @@ gbt_status gbt_ctx_set_compaction(gbt_ctx *c, int32_t mode)
     return GBT_OK;
 }
 
+gbt_status gbt_ctx_set_stream_chunk_rows(gbt_ctx *c, int64_t rows)
+{
+    if (!c) return set_error(GBT_E_INVALID, "gbt_ctx_set_stream_chunk_rows: ctx is NULL");
+    if (rows < 0 || rows > ((int64_t)1 << 30))
+        return set_error(GBT_E_INVALID, "gbt_ctx_set_stream_chunk_rows: %lld rows outside [0, 2^30]",
+                         (long long)rows);
+    c->stream_chunk_rows = rows ? rows : ((int64_t)1 << 22);
+    return GBT_OK;
+}
+
 }  // extern "C"

@@ -722,6 +722,63 @@ __global__ void __launch_bounds__(256) k_fx_convert(const double2 *__restrict__ 
     }
 }
 
+// The MVS lambda estimate's two passes over every row, with the pair
+// recomputed from margin and label each time and rounded to float as
+// gbt_gradients stores it (nothing per row is kept): pass 0 folds the
+// maxima of |g| and |h|, pass 1 converts to the fixed point of those
+// maxima and folds the exact integer sums.
+template <int kPass>
+__global__ void __launch_bounds__(256) k_lambda_pass(int32_t loss, const float *__restrict__ margin,
+                                                     const float *__restrict__ label, int64_t n, int32_t log2n,
+                                                     SampleState *__restrict__ st)
+{
+    __shared__ unsigned long long lds4[4], m2[2];
+    int32_t eg = 0, eh = 0;
+    if (kPass == 1) {
+        int Eg, Eh;
+        frexp(__longlong_as_double(block_fold_max(st->gmax, &m2[0])), &Eg);
+        frexp(__longlong_as_double(block_fold_max(st->hmax, &m2[1])), &Eh);
+        eg = 62 - Eg - log2n;
+        eh = 62 - Eh - log2n;
+    }
+    unsigned long long a = 0, b = 0;
+    bool bad = false;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        double g, h;
+        gradient_pair(loss, margin[i], label[i], &g, &h);
+        const double gf = (double)(float)g, hf = (double)(float)h;
+        if (kPass == 0) {
+            bad |= !(fabs(gf) <= 1.7976931348623157e308) || !(fabs(hf) <= 1.7976931348623157e308);
+            const unsigned long long x = __double_as_longlong(fabs(gf)), y = __double_as_longlong(fabs(hf));
+            a = x > a ? x : a;
+            b = y > b ? y : b;
+        } else {
+            a += (unsigned long long)(long long)rint(ldexp(gf, eg));
+            b += (unsigned long long)(long long)rint(ldexp(hf, eh));
+        }
+    }
+    if (kPass == 0) {
+        if (bad) atomicOr(&st->bad, 1u);
+        a = block_max_u64(a, lds4);
+        b = block_max_u64(b, lds4);
+        if (threadIdx.x == 0) {
+            if (a) atomicMax(spread_at(st->gmax, blockIdx.x), a);
+            if (b) atomicMax(spread_at(st->hmax, blockIdx.x), b);
+        }
+    } else {
+        a = block_sum_u64(a, lds4);
+        b = block_sum_u64(b, lds4);
+        if (threadIdx.x == 0) {
+            if (a) atomicAdd(spread_at(st->root_g, blockIdx.x), a);
+            if (b) atomicAdd(spread_at(st->root_h, blockIdx.x), b);
+            if (blockIdx.x == 0) {
+                st->e_g = eg;
+                st->e_h = eh;
+            }
+        }
+    }
+}
+
 __global__ void k_state_init(SampleState *st)
 {
     static_assert(sizeof(SampleState) % 8 == 0, "SampleState is zeroed in 64-bit words");
@@ -879,6 +936,17 @@ gbt_status fixed_point(gbt_ctx *c, const double *gw, int64_t R, SampleState *st,
     }
     k_fx_convert<<<rblocks(R), 256, 0, c->stream>>>((const double2 *)gw, R, log2_ceil(R), st,
                                                    (longlong2 *)q);
+    GBT_LAUNCHED();
+    return GBT_OK;
+}
+
+gbt_status lambda_sums(gbt_ctx *c, int32_t loss, const float *margin, const float *label, int64_t n,
+                       SampleState *st)
+{
+    if (n == 0) return GBT_OK;
+    k_lambda_pass<0><<<rblocks(n), 256, 0, c->stream>>>(loss, margin, label, n, 0, st);
+    GBT_LAUNCHED();
+    k_lambda_pass<1><<<rblocks(n), 256, 0, c->stream>>>(loss, margin, label, n, log2_ceil(n), st);
     GBT_LAUNCHED();
     return GBT_OK;
 }

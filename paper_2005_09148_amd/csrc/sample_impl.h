@@ -99,6 +99,11 @@ gbt_status mvs_select(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t 
                       double lambda, const SampleState *st, uint64_t seed, uint64_t iteration,
                       int64_t row_offset, uint8_t *keep, int32_t *tile_cnt, const SampleRule &rule);
 gbt_status gw_all(gbt_ctx *c, const float *gpair, int64_t n, double *gw);
+// The exact fixed-point sums of all n rows' pairs (recomputed from margins
+// and labels, rounded to float) into st->root_g/root_h with st->e_g/e_h,
+// in two passes that keep nothing per row.
+gbt_status lambda_sums(gbt_ctx *c, int32_t loss, const float *margin, const float *label, int64_t n,
+                       SampleState *st);
 // fx_max_done: the maxima of |g'| and |h'| are already in st (fused upstream)
 gbt_status fixed_point(gbt_ctx *c, const double *gw, int64_t R, SampleState *st, int64_t *q,
                        bool fx_max_done = false);

@@ -36,8 +36,6 @@ struct StreamEvents {
     }
 };
 
-static int64_t g_stream_chunk_rows = (int64_t)1 << 22;
-
 gbt_status for_each_chunk(gbt_ctx *c, const gbt_matrix *mx, const ChunkFn &fn, double *h2d_bytes)
 {
     struct Chunk {
@@ -45,13 +43,14 @@ gbt_status for_each_chunk(gbt_ctx *c, const gbt_matrix *mx, const ChunkFn &fn, d
         int64_t off, rows;
     };
     std::vector<Chunk> host_chunks;
+    const int64_t chunk_rows = c->stream_chunk_rows;
     for (const auto &pg : mx->pages) {
         if (!pg.streamed()) {
             if (pg.rows) GBT_TRY(fn(pg.words, pg.row0, pg.rows));
             continue;
         }
-        for (int64_t o = 0; o < pg.rows; o += g_stream_chunk_rows)
-            host_chunks.push_back({&pg, o, std::min(g_stream_chunk_rows, pg.rows - o)});
+        for (int64_t o = 0; o < pg.rows; o += chunk_rows)
+            host_chunks.push_back({&pg, o, std::min(chunk_rows, pg.rows - o)});
     }
     if (host_chunks.empty()) return GBT_OK;
     const size_t row_bytes = (size_t)mx->row_words * 4;
@@ -155,7 +154,7 @@ static gbt_status reserve_stage(gbt_ctx *c, const gbt_matrix *mx)
 {
     int64_t maxrows = 0;
     for (const auto &pg : mx->pages)
-        if (pg.streamed()) maxrows = std::max(maxrows, std::min(pg.rows, g_stream_chunk_rows));
+        if (pg.streamed()) maxrows = std::max(maxrows, std::min(pg.rows, c->stream_chunk_rows));
     if (maxrows == 0) return GBT_OK;
     void *p;
     GBT_TRY(scratch(c, kScrStage0, (size_t)maxrows * mx->row_words * 4, &p));
@@ -1320,19 +1319,13 @@ gbt_status gbt_mvs_lambda_estimate(gbt_ctx *c, int32_t loss, const float *margin
     *lambda_out = 0.0;
     if (n == 0) return GBT_OK;
     GBT_TRY(set_device(c));
-    // every row's pair in its exact fixed point; the state folds the sums
-    float *gpair;
-    double *gw;
-    int64_t *q;
+    // every row's pair in its exact fixed point over the n rows; two passes
+    // fold the maxima, then the integer sums, into the state (no per-row
+    // buffer, so the call fits any budget that holds the state)
     SampleState *st;
-    GBT_TRY(scratch_t(c, kScrGpair, (size_t)n * 2, &gpair));
-    GBT_TRY(scratch_t(c, kScrGw, (size_t)n * 2, &gw));
-    GBT_TRY(scratch_t(c, kScrQ, (size_t)n * 2, &q));
     GBT_TRY(scratch_t(c, kScrState, 1, &st));
     GBT_TRY(state_init(c, st));
-    GBT_TRY(launch_gradients(c, loss, margin_d, label_d, nullptr, n, gpair));
-    GBT_TRY(gw_all(c, gpair, n, gw));
-    GBT_TRY(fixed_point(c, gw, n, st, q, false));
+    GBT_TRY(lambda_sums(c, loss, margin_d, label_d, n, st));
     SampleState hst;
     GBT_HIP(hipMemcpyAsync(&hst, st, sizeof(SampleState), hipMemcpyDeviceToHost, c->stream));
     GBT_HIP(hipStreamSynchronize(c->stream));
@@ -1546,7 +1539,7 @@ static gbt_status train_tree_naive_impl(gbt_ctx *c, const gbt_matrix *mx, const 
     const int32_t max_level = 1 << D;
     int64_t chunk_rows = 1;  // the largest chunk for_each_chunk passes
     for (const auto &pg : mx->pages)
-        chunk_rows = std::max(chunk_rows, pg.streamed() ? std::min(pg.rows, g_stream_chunk_rows) : pg.rows);
+        chunk_rows = std::max(chunk_rows, pg.streamed() ? std::min(pg.rows, c->stream_chunk_rows) : pg.rows);
     GBT_TRY(scratch_t(c, kScrNodes, (size_t)NN, &nodes));
     GBT_TRY(scratch_t(c, kScrPosition, (size_t)std::max<int64_t>(n, 1), &position));
     GBT_TRY(scratch_t(c, kScrSlotNode, (size_t)NN, &slot_of));

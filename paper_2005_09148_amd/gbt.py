@@ -146,6 +146,7 @@ SIGNATURES = {
     "gbt_ctx_set_timing": (_i32, [_vp, _i32]),
     "gbt_ctx_set_hist_kernel": (_i32, [_vp, _i32]),
     "gbt_ctx_set_compaction": (_i32, [_vp, _i32]),
+    "gbt_ctx_set_stream_chunk_rows": (_i32, [_vp, _i64]),
     "gbt_mvs_lambda_estimate": (_i32, [_vp, _i32, _vp, _vp, _i64, _vp]),
     "gbt_quantize": (_i32, [_vp, _vp, _vp, _vp]),
     "gbt_quantize_begin": (_i32, [_vp, _vp, _i32, _i64, _i32, _vp]),
@@ -220,6 +221,32 @@ def _ptr(t):
     return t.data_ptr()
 
 
+def _dev_args(ctx, *specs):
+    """Device pointers of the tensors in specs, each (tensor, name, dtype,
+    numel or None, optional), after checking that every one is a contiguous
+    torch tensor of its dtype and size on the context's device: a host or
+    short buffer handed to a kernel would be an out-of-bounds device access.
+    The layout of every argument is checked before any device placement."""
+    torch = _torch()
+    for t, name, dtype, numel, optional in specs:
+        if t is None:
+            if optional:
+                continue
+            raise ValueError(f"{name}: a device tensor is required")
+        if not isinstance(t, torch.Tensor):
+            raise ValueError(f"{name}: expected a torch tensor, got {type(t).__name__}")
+        if t.dtype != dtype:
+            raise ValueError(f"{name}: dtype {t.dtype}, expected {dtype}")
+        if not t.is_contiguous():
+            raise ValueError(f"{name}: must be contiguous")
+        if numel is not None and t.numel() != numel:
+            raise ValueError(f"{name}: {t.numel()} elements, expected {numel}")
+    for t, name, _, _, _ in specs:
+        if t is not None and (not t.is_cuda or t.device.index != ctx.device):
+            raise ValueError(f"{name}: must be on cuda:{ctx.device}, is on {t.device}")
+    return [None if t is None else t.data_ptr() for t, *_ in specs]
+
+
 def _dev_tensor(a, dtype, device):
     """A contiguous device tensor of `a` (numpy array or tensor)."""
     torch = _torch()
@@ -283,6 +310,11 @@ class Context:
         through the pages' device mapping) or COMPACT_AUTO; results are
         identical."""
         _check(_lib.gbt_ctx_set_compaction(self.h, int(mode)))
+
+    def set_stream_chunk_rows(self, rows: int):
+        """Rows per chunk when host or disk pages stream through the device
+        (0 = the default 2^22); results are identical."""
+        _check(_lib.gbt_ctx_set_stream_chunk_rows(self.h, int(rows)))
 
     @property
     def torch_device(self):
@@ -449,19 +481,25 @@ class Quantizer:
 # ---------------------------------------------------------------- iteration steps
 def gbt_gradients(ctx, loss, margin, label, weight=None, out=None):
     torch = _torch()
-    n = margin.numel()
-    if out is None:
-        out = torch.empty((n, 2), dtype=torch.float32, device=margin.device)
-    _check(_lib.gbt_gradients(ctx.h, loss, _ptr(margin), _ptr(label), _ptr(weight), n, _ptr(out)))
+    f32 = torch.float32
+    n = margin.numel() if isinstance(margin, torch.Tensor) else 0
+    if out is None and isinstance(margin, torch.Tensor):
+        out = torch.empty((n, 2), dtype=f32, device=margin.device)
+    m_p, y_p, w_p, o_p = _dev_args(ctx, (margin, "margin", f32, None, False), (label, "label", f32, n, False),
+                                   (weight, "weight", f32, n, True), (out, "out", f32, 2 * n, False))
+    _check(_lib.gbt_gradients(ctx.h, loss, m_p, y_p, w_p, n, o_p))
     return out
 
 
 def gbt_mvs_lambda_estimate(ctx, loss, margin, label):
     """MVS lambda as the squared initial leaf value -G/H of every row at
     `margin` (device tensors of equal length)."""
+    torch = _torch()
+    n = margin.numel() if isinstance(margin, torch.Tensor) else 0
+    m_p, y_p = _dev_args(ctx, (margin, "margin", torch.float32, None, False),
+                         (label, "label", torch.float32, n, False))
     out = C.c_double()
-    _check(_lib.gbt_mvs_lambda_estimate(ctx.h, int(loss), _ptr(margin), _ptr(label), margin.numel(),
-                                        C.byref(out)))
+    _check(_lib.gbt_mvs_lambda_estimate(ctx.h, int(loss), m_p, y_p, margin.numel(), C.byref(out)))
     return out.value
 
 
@@ -500,10 +538,13 @@ def gbt_sample(ctx, matrix: Matrix, gpair=None, margin=None, label=None, f=1.0, 
                seed=0, iteration=0, loss=LOSS_LOGISTIC, keep_handle=False, sampler=SAMPLE_MVS, goss_a=0.0):
     """Alg. 7 sampling + compaction; returns copies of the sampled arrays."""
     torch = _torch()
+    n = matrix.info().n_rows
+    f32 = torch.float32
+    g_p, m_p, y_p = _dev_args(ctx, (gpair, "gpair", f32, 2 * n, True), (margin, "margin", f32, n, True),
+                              (label, "label", f32, n, True))
     sp = SampleParams(f, mvs_lambda, seed, iteration, loss, sampler, goss_a)
     h = C.c_void_p()
-    _check(_lib.gbt_sample(ctx.h, matrix.h, _ptr(gpair), _ptr(margin), _ptr(label),
-                           C.byref(sp), C.byref(h)))
+    _check(_lib.gbt_sample(ctx.h, matrix.h, g_p, m_p, y_p, C.byref(sp), C.byref(h)))
     try:
         inf = SampledInfo()
         _check(_lib.gbt_sampled_info_get(h, C.byref(inf)))
@@ -522,10 +563,31 @@ def gbt_sample(ctx, matrix: Matrix, gpair=None, margin=None, label=None, f=1.0, 
 
 def gbt_build_hist(ctx, matrix: Matrix, page, q, rows, build, sub=(), parent_hist=None, hist=None):
     """build: [(slot, begin, end)], sub: [(parent_slot, built_slot, target_slot)]."""
+    torch = _torch()
+    inf = matrix.info()
+    if page is None or page.dim() != 2 or page.shape[1] != inf.row_words:
+        raise ValueError(f"page: expected [rows, {inf.row_words}] words")
+    n_page = page.shape[0]
+    if q is not None and q.numel() < 2 * n_page:
+        raise ValueError(f"q: {q.numel()} elements for {n_page} page rows")
+    n_idx = rows.numel() if rows is not None else n_page
+    slots = [s for s, _, _ in build] + [t for _, _, t in sub]
+    for s, b, e in build:
+        if not (0 <= b <= e <= n_idx):
+            raise ValueError(f"build segment ({s}, {b}, {e}) outside the {n_idx} rows")
+    tb = inf.total_bins
+    if hist is not None and slots and hist.numel() < (max(slots) + 1) * tb * 2:
+        raise ValueError(f"hist: {hist.numel()} elements, slot {max(slots)} needs {(max(slots) + 1) * tb * 2}")
+    if sub and parent_hist is not None and parent_hist.numel() < (max(p for p, _, _ in sub) + 1) * tb * 2:
+        raise ValueError("parent_hist: too short for the parent slots")
+    i32, i64 = torch.int32, torch.int64
+    pg_p, q_p, r_p, h_p, ph_p = _dev_args(ctx, (page, "page", i32, None, False), (q, "q", i64, None, False),
+                                          (rows, "rows", i32, None, True), (hist, "hist", i64, None, False),
+                                          (parent_hist, "parent_hist", i64, None, not sub))
     bl = (Seg * max(len(build), 1))(*[Seg(s, 0, b, e) for s, b, e in build])
     sl = (Sub * max(len(sub), 1))(*[Sub(p, b, t, 0) for p, b, t in sub])
-    _check(_lib.gbt_build_hist(ctx.h, matrix.h, _ptr(page), _ptr(q), _ptr(rows), bl, len(build),
-                               sl, len(sub), _ptr(parent_hist), _ptr(hist)))
+    _check(_lib.gbt_build_hist(ctx.h, matrix.h, pg_p, q_p, r_p, bl, len(build),
+                               sl, len(sub), ph_p, h_p))
     return hist
 
 
@@ -576,30 +638,39 @@ class TreeOut:
         return t
 
 
+def _label_margin(ctx, matrix, label, margin):
+    torch = _torch()
+    n = matrix.info().n_rows
+    return _dev_args(ctx, (label, "label", torch.float32, n, False), (margin, "margin", torch.float32, n, False))
+
+
 def gbt_train_tree(ctx, matrix: Matrix, label, margin, params: TrainParams, stats=True) -> TreeOut:
+    y_p, m_p = _label_margin(ctx, matrix, label, margin)
     nn = (1 << (params.max_depth + 1)) - 1
     nodes = np.zeros(nn, NODE_DTYPE)
     t = Tree(params.max_depth, nn, 0, 0, nodes.ctypes.data)
     st = TreeStats() if stats else None
-    _check(_lib.gbt_train_tree(ctx.h, matrix.h, _ptr(label), _ptr(margin), C.byref(params),
+    _check(_lib.gbt_train_tree(ctx.h, matrix.h, y_p, m_p, C.byref(params),
                                C.byref(t), C.byref(st) if st is not None else None))
     return TreeOut(nodes, t.exp_g, t.exp_h, params.max_depth, st)
 
 
 def gbt_train_tree_naive(ctx, matrix: Matrix, label, margin, params: TrainParams, stats=True) -> TreeOut:
     """Alg. 6, the naive out-of-core construction (a negative baseline)."""
+    y_p, m_p = _label_margin(ctx, matrix, label, margin)
     nn = (1 << (params.max_depth + 1)) - 1
     nodes = np.zeros(nn, NODE_DTYPE)
     t = Tree(params.max_depth, nn, 0, 0, nodes.ctypes.data)
     st = TreeStats() if stats else None
-    _check(_lib.gbt_train_tree_naive(ctx.h, matrix.h, _ptr(label), _ptr(margin), C.byref(params),
+    _check(_lib.gbt_train_tree_naive(ctx.h, matrix.h, y_p, m_p, C.byref(params),
                                      C.byref(t), C.byref(st) if st is not None else None))
     return TreeOut(nodes, t.exp_g, t.exp_h, params.max_depth, st)
 
 
 def gbt_update_leaves(ctx, tree: TreeOut, params: TrainParams, matrix: Matrix, margin):
+    m_p, = _dev_args(ctx, (margin, "margin", _torch().float32, matrix.info().n_rows, False))
     t = tree.as_struct()
-    _check(_lib.gbt_update_leaves(ctx.h, C.byref(t), C.byref(params), matrix.h, _ptr(margin)))
+    _check(_lib.gbt_update_leaves(ctx.h, C.byref(t), C.byref(params), matrix.h, m_p))
     return tree
 
 
@@ -611,7 +682,8 @@ def gbt_predict(ctx, trees, base_margin, binned: Matrix | None = None, raw=None,
         n = binned.info().n_rows
         if out is None:
             out = torch.empty(n, dtype=torch.float32, device=ctx.torch_device)
-        _check(_lib.gbt_predict(ctx.h, arr, len(trees), None, binned.h, base_margin, _ptr(out)))
+        o_p, = _dev_args(ctx, (out, "out", torch.float32, n, False))
+        _check(_lib.gbt_predict(ctx.h, arr, len(trees), None, binned.h, base_margin, o_p))
         return out
     if isinstance(raw, dict):
         inp, keep = csr_input(raw["indptr"], raw["indices"], raw["values"], raw["m"], LOC_DEVICE)
@@ -619,7 +691,8 @@ def gbt_predict(ctx, trees, base_margin, binned: Matrix | None = None, raw=None,
         inp, keep = dense_input(raw, LOC_DEVICE)
     if out is None:
         out = torch.empty(inp.n_rows, dtype=torch.float32, device=ctx.torch_device)
-    _check(_lib.gbt_predict(ctx.h, arr, len(trees), C.byref(inp), None, base_margin, _ptr(out)))
+    o_p, = _dev_args(ctx, (out, "out", torch.float32, inp.n_rows, False))
+    _check(_lib.gbt_predict(ctx.h, arr, len(trees), C.byref(inp), None, base_margin, o_p))
     return out
 
 

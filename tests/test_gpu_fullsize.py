@@ -1,10 +1,11 @@
 """Trees of the workloads at their full row counts against the oracle.
 
-Each test trains the first trees of one workload at full size on the GPU and
-with the oracle, on the same seeded data, and requires identical node tables
-and margins.  The oracle takes seconds per tree at these sizes, so a few
-trees are trained by default; GBT_FULL_TREES=1 trains each workload's whole
-tree count (minutes).  The 200M-row out-of-core workload is checked here at
+Each test trains one workload at full size, with its whole tree count, on
+the GPU and with the oracle (its OpenMP build), on the same seeded data, and
+requires identical node tables and margins after every tree: margins drift
+tree by tree, so late trees are where a difference in the fp32 margins or in
+the fixed-point exponents would show.  GBT_FULL_TREES=0 trains only the
+first trees (a quick run).  The 200M-row out-of-core workload is checked here at
 a reduced row count with the same page shape, feature count, sampling and
 device budget; its full size runs in bench.py's out-of-core mode.
 """
@@ -21,7 +22,7 @@ pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
 
-FULL = os.environ.get("GBT_FULL_TREES") == "1"
+FULL = os.environ.get("GBT_FULL_TREES", "1") == "1"
 
 
 @pytest.fixture(scope="module")
@@ -67,8 +68,10 @@ def run_workload(gbt, ctx, cfg_id, n_trees):
     mx = gbt.gbt_quantize(ctx, data, max_bin=cfg.max_bin)
     P, OP = params(gbt, cfg)
     trees, margin = gbt.train(ctx, mx, torch.from_numpy(y).cuda(), P, n_trees, cfg.base_margin)
+    print(f"[fullsize] workload {cfg_id}: {n_trees} GPU trees done", flush=True)
     b = oracle_bins(data, cfg.max_bin)
     otrees, omargin = orc.train(b, y, OP, n_trees, cfg.base_margin)
+    print(f"[fullsize] workload {cfg_id}: {n_trees} oracle trees done", flush=True)
     check_trees(trees, margin.cpu().numpy(), otrees, omargin)
     return trees
 

@@ -211,6 +211,7 @@ def test_sample(gbt, ctx, f, kind):
                        iteration=it)
     assert r.info.n_sampled == len(sel)
     if f < 1.0:
+        assert r.info.target == orc.mvs_target(f, n)
         assert r.info.threshold == T and r.info.exp_key == e
         assert same_bits(r.rows.cpu().numpy(), sel.astype(np.int32))
     else:

@@ -199,6 +199,25 @@ def test_goss_top_threshold_is_the_a_th_largest_key(orc, seed):
         assert (keys >= t).sum() >= A > (keys > t).sum()
 
 
+@pytest.mark.parametrize("f,n,K", [
+    (0.25, 10, 2),    # 2.5 rounds to even (half-up would give 3)
+    (0.75, 10, 8),    # 7.5 rounds to even (floor would give 7)
+    (0.1, 35, 4),     # f n is 3.5 in double: to even, up
+    (0.1, 25, 2),     # 2.5: to even, down
+    (0.29, 10, 3),    # 2.9 to nearest (floor would give 2)
+    (0.5, 3, 2),      # 1.5 to even, up
+    (0.05, 10, 1),    # 0.5 rounds to 0, clamped to one row
+    (1e-9, 10, 1),    # far below one row: clamped
+    (1.0, 7, 7),      # every row
+    (0.1, 200_000_000, 20_000_000),  # the out-of-core workload's target
+])
+def test_mvs_target_is_clamped_round_half_even(orc, f, n, K):
+    """K = max(1, rint(f n)) with IEEE round-half-to-even (the sample-size
+    reading of Eq. 9); hand-computed values that a floor, a round-half-up or
+    an unclamped rule would each get wrong."""
+    assert orc.mvs_target(f, n) == K
+
+
 def test_goss_top_count_rounds(orc):
     assert orc.goss_top_count(0.1, 1000) == 100
     assert orc.goss_top_count(0.0, 1000) == 0
