@@ -362,6 +362,26 @@ gbt_status gbt_build_hist(gbt_ctx *ctx, const gbt_matrix *layout, const uint32_t
                           int32_t n_build, const gbt_sub *sub_h, int32_t n_sub,
                           const int64_t *parent_hist_d, int64_t *hist_d);
 
+/* ---- gbt_build_hist without allocation ------------------------------------
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * arguments and results as gbt_build_hist, with its partial histograms and
+ * work plan in a static device array of 64 MiB that every GPU the library
+ * runs on holds until the process ends (its address on each device is
+ * resolved by gbt_ctx_create).  The call allocates no device memory and
+ * records no timing events; it may cut a node's rows into fewer, longer
+ * chunks than gbt_build_hist so that they fit (the histograms are the
+ * same), and returns GBT_E_INVALID when even one chunk per non-empty node
+ * does not fit (about 64 MiB / (total_bins * 16) nodes).  All calls on one
+ * GPU share its array: calls that overlap on a GPU (from several threads,
+ * contexts or streams) race and give wrong histograms; the call
+ * synchronizes its stream before returning, so calls made one after the
+ * other are safe. */
+gbt_status gbt_build_hist_noalloc(gbt_ctx *ctx, const gbt_matrix *layout, const uint32_t *page_d,
+                                  const int64_t *gpair_fx_d, const int32_t *rows_d,
+                                  const gbt_seg *build_h, int32_t n_build, const gbt_sub *sub_h,
+                                  int32_t n_sub, const int64_t *parent_hist_d, int64_t *hist_d);
+
 /* ---- Alg. 1 EvaluateSplit with Eq. 8 ---------------------------------------
  * For node k: histogram hist_d[node_slot_h[k]], node sum node_sum_d[2k..2k+1].
  * Every feature with >= 2 bins, every s in 1..B_j-1, missing right then

@@ -352,10 +352,14 @@ gbt_status scan_tile_counts(gbt_ctx *c, int32_t *tile_cnt, int64_t tiles, int32_
 // ---------------------------------------------------------------- shared launches
 gbt_status launch_gradients(gbt_ctx *c, int32_t loss, const float *margin, const float *label,
                             const float *weight, int64_t n, float *gpair);
+struct HistWorkspace;
+// ws: device memory for the partial histograms and the plan (NULL: the
+// context's workspaces)
 gbt_status build_hist_impl(gbt_ctx *c, const gbt_matrix *layout, const uint32_t *page,
                            const int64_t *q, const int32_t *rows, const gbt_seg *build,
                            int32_t n_build, const gbt_sub *sub, int32_t n_sub,
-                           const int64_t *parent_hist, int64_t *hist, gbt_tree_stats *stats);
+                           const int64_t *parent_hist, int64_t *hist, gbt_tree_stats *stats,
+                           const HistWorkspace *ws = nullptr);
 
 // Row-major ELLPACK page geometry helpers (host).
 int32_t ceil_log2_u64(uint64_t v);

@@ -1,5 +1,6 @@
 // ctx.hip -- context, error model and the budgeted device allocator.
 #include "common.h"
+#include "hist_impl.h"
 
 #include <mutex>
 
@@ -214,6 +215,14 @@ gbt_status gbt_ctx_create(int32_t device, uint64_t budget_bytes, void *hip_strea
     if (e != hipSuccess) {
         delete c;
         return hip_error(e, "hipStreamCreateWithFlags", __FILE__, __LINE__);
+    }
+    // the device address of gbt_build_hist_noalloc's static scratch on this
+    // device (resolved once per device, with the device current)
+    const gbt_status ss = static_scratch_init(device);
+    if (ss != GBT_OK) {
+        (void)hipStreamDestroy(c->side);
+        delete c;
+        return ss;
     }
     *out = c;
     return GBT_OK;

@@ -15,6 +15,14 @@
 
 #include <algorithm>
 #include <cstring>
+#include <mutex>
+
+// Device memory of gbt_build_hist_noalloc: its partial histograms and plan.
+// Every GPU the library runs on holds its own copy until the process ends;
+// host code reaches it only through the address hipGetSymbolAddress gives
+// on each device (the array's name is a host-side stand-in).
+constexpr size_t kStaticScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
 
 namespace gbt {
 
@@ -658,7 +666,7 @@ gbt_status hist_plan(const gbt_matrix *mx, int64_t rows_hint, int choice, HistPl
 gbt_status build_hist_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int64_t *q,
                            const int32_t *rows, const gbt_seg *build, int32_t n_build,
                            const gbt_sub *sub, int32_t n_sub, const int64_t *parent_hist,
-                           int64_t *hist, gbt_tree_stats *stats)
+                           int64_t *hist, gbt_tree_stats *stats, const HistWorkspace *ws)
 {
     const int64_t tb = mx->total_bins;
     if (tb == 0 || n_build == 0) {
@@ -676,6 +684,30 @@ gbt_status build_hist_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *pag
     const int64_t items = std::max<int64_t>(1, hp.target_wgs / G - n_build);
     int64_t chunk = (total_rows + items - 1) / items;
     chunk = std::max<int64_t>(chunk, 2048);
+    auto al = [](size_t b) { return (b + 255) / 256 * 256; };
+    if (ws) {
+        // the partials and the plan must fit the given workspace: fewer,
+        // longer chunks when the usual ones would not (each non-empty node
+        // needs at least one)
+        int64_t nonempty = 0, longest = 0;
+        for (int32_t k = 0; k < n_build; ++k) {
+            const int64_t len = std::max<int64_t>(0, build[k].end - build[k].begin);
+            nonempty += len > 0;
+            longest = std::max(longest, len);
+        }
+        const size_t fixed = al((size_t)G * sizeof(HistGroup)) + al((size_t)n_build * sizeof(HistReduce)) + 4 * 256;
+        const size_t per_part = (size_t)tb * 16 + sizeof(HistWork);
+        const int64_t pmax = ws->bytes > fixed ? (int64_t)((ws->bytes - fixed) / per_part) : 0;
+        if (pmax < nonempty)
+            return set_error(GBT_E_INVALID,
+                             "%lld non-empty nodes of %lld bins need %zu bytes of scratch; the static scratch "
+                             "holds %zu",
+                             (long long)nonempty, (long long)tb, fixed + (size_t)nonempty * per_part, ws->bytes);
+        if (nonempty > 0) {
+            const int64_t room = pmax - nonempty;
+            chunk = std::max(chunk, room > 0 ? (total_rows + room - 1) / room : longest);
+        }
+    }
     std::vector<HistWork> work;
     std::vector<HistReduce> red;
     int32_t nparts = 0;
@@ -698,11 +730,23 @@ gbt_status build_hist_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *pag
     }
 
     // upload the plan: groups | work | reduce items
-    size_t o_w = ((size_t)G * sizeof(HistGroup) + 255) / 256 * 256;
-    size_t o_r = o_w + (std::max<size_t>(work.size(), 1) * sizeof(HistWork) + 255) / 256 * 256;
+    size_t o_w = al((size_t)G * sizeof(HistGroup));
+    size_t o_r = o_w + al(std::max<size_t>(work.size(), 1) * sizeof(HistWork));
     size_t bytes = o_r + red.size() * sizeof(HistReduce) + 256;
+    const size_t part_bytes = (size_t)std::max(nparts, 1) * tb * 16;
     char *plan;
-    GBT_TRY(scratch_t(c, kScrWork, bytes, &plan));
+    longlong2 *partials = nullptr;
+    if (ws) {
+        // partials first, then the plan, in the caller's workspace
+        if (al(part_bytes) + bytes > ws->bytes)
+            return set_error(GBT_E_INVALID, "the histogram plan needs %zu bytes of scratch; the static scratch holds %zu",
+                             al(part_bytes) + bytes, ws->bytes);
+        partials = (longlong2 *)ws->base;
+        plan = ws->base + al(part_bytes);
+    } else {
+        GBT_TRY(scratch_t(c, kScrWork, bytes, &plan));
+        GBT_TRY(scratch(c, kScrPartials, part_bytes, (void **)&partials));
+    }
     std::vector<char> h(bytes);
     memcpy(h.data(), groups.data(), G * sizeof(HistGroup));
     if (!work.empty()) memcpy(h.data() + o_w, work.data(), work.size() * sizeof(HistWork));
@@ -712,8 +756,6 @@ gbt_status build_hist_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *pag
     const HistWork *work_d = (const HistWork *)(plan + o_w);
     const HistReduce *red_d = (const HistReduce *)(plan + o_r);
 
-    longlong2 *partials = nullptr;
-    GBT_TRY(scratch(c, kScrPartials, (size_t)std::max(nparts, 1) * tb * 16, (void **)&partials));
 
     // the tree driver zeroes these counters per tree and reads them once
     unsigned long long *upd = nullptr;
@@ -721,6 +763,7 @@ gbt_status build_hist_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *pag
 
     HistLaunch hl{hp.kind, groups_d, G, hp.max_groups_bins, work_d, nullptr, (int32_t)work.size(), red_d,
                   nullptr, (int32_t)red.size(), (int64_t *)partials};
+    hl.timed = ws == nullptr;
     GBT_CHECK(n_sub == 0 || parent_hist, "subtraction needs the parent histograms");
     GBT_TRY(hist_launch_device(c, mx, page, q, rows, hl, parent_hist, hist, upd));
     if (stats && !work.empty()) {
@@ -732,6 +775,34 @@ gbt_status build_hist_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *pag
         stats->hist_rows += total_rows;
         stats->hist_bytes += total_rows * (wbytes + 16 + (rows ? 4 : 0)) + (int64_t)n_build * tb * 16;
     }
+    return GBT_OK;
+}
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_static_mu;
+static void *g_static_at[kMaxDevices];  // the static scratch's address on each device
+
+gbt_status static_scratch_init(int device)
+{
+    if (device < 0 || device >= kMaxDevices)
+        return set_error(GBT_E_UNSUPPORTED, "device %d: the static scratch table holds %d devices", device,
+                         kMaxDevices);
+    std::lock_guard<std::mutex> lk(g_static_mu);
+    if (g_static_at[device]) return GBT_OK;
+    void *p = nullptr;
+    GBT_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(::scratch)));
+    if (!p) return set_error(GBT_E_DEVICE, "no device address for the static scratch on device %d", device);
+    g_static_at[device] = p;
+    return GBT_OK;
+}
+
+static gbt_status static_scratch(int device, HistWorkspace *ws)
+{
+    std::lock_guard<std::mutex> lk(g_static_mu);
+    if (device < 0 || device >= kMaxDevices || !g_static_at[device])
+        return set_error(GBT_E_INVALID, "no static scratch on device %d (the context did not resolve it)", device);
+    ws->base = (char *)g_static_at[device];
+    ws->bytes = kStaticScratchBytes;
     return GBT_OK;
 }
 
@@ -749,7 +820,7 @@ gbt_status hist_launch_device(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
         const unsigned grid = (unsigned)((size_t)hl.max_work * (size_t)G);
         const size_t lds = (size_t)kRotBins * kRotCols * 16;
         const longlong2 *qq = (const longlong2 *)q;
-        const int mark = timer_begin(c, kPhHist);
+        const int mark = hl.timed ? timer_begin(c, kPhHist) : -1;
 #define GBT_HIST_ROT(WB)                                                                                 \
     case WB:                                                                                             \
         if (rows)                                                                                        \
@@ -783,7 +854,7 @@ gbt_status hist_launch_device(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
         uint32_t null_sym = (mx->sparse || mx->has_missing) ? mx->null_sym : 0xffffffffu;
         uint32_t mask = mx->w >= 32 ? 0xffffffffu : ((1u << mx->w) - 1u);
         unsigned grid = (unsigned)((size_t)hl.max_work * (size_t)G);
-        const int mark = timer_begin(c, kPhHist);
+        const int mark = hl.timed ? timer_begin(c, kPhHist) : -1;
         if (mx->sparse) {
             size_t lds = (size_t)hl.max_groups_bins * 16;
             if (rows)
@@ -830,7 +901,7 @@ gbt_status hist_launch_device(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
         timer_end(c, mark);
     }
     if (hl.max_red > 0) {
-        const int aux = timer_begin(c, kPhHistAux);
+        const int aux = hl.timed ? timer_begin(c, kPhHistAux) : -1;
         dim3 rg((unsigned)((tb + kRedBins - 1) / kRedBins), (unsigned)hl.max_red);
         k_hist_reduce<<<rg, kRedBins * kRedSplit, 0, c->stream>>>(partials, hl.red, hl.n_red_d,
                                                                   (const longlong2 *)parent_hist,
@@ -861,6 +932,28 @@ extern "C" gbt_status gbt_build_hist(gbt_ctx *c, const gbt_matrix *layout, const
     GBT_TRY(set_device(c));
     GBT_TRY(build_hist_impl(c, layout, page_d, gpair_fx_d, rows_d, build_h, n_build, sub_h, n_sub,
                             parent_hist_d, hist_d, nullptr));
+    GBT_HIP(hipStreamSynchronize(c->stream));
+    return GBT_OK;
+}
+
+extern "C" gbt_status gbt_build_hist_noalloc(gbt_ctx *c, const gbt_matrix *layout, const uint32_t *page_d,
+                                             const int64_t *gpair_fx_d, const int32_t *rows_d,
+                                             const gbt_seg *build_h, int32_t n_build, const gbt_sub *sub_h,
+                                             int32_t n_sub, const int64_t *parent_hist_d, int64_t *hist_d)
+{
+    GBT_CHECK(c && layout && hist_d, "gbt_build_hist_noalloc: NULL argument");
+    GBT_CHECK(n_build >= 0 && n_sub >= 0, "negative counts");
+    GBT_CHECK(n_build == 0 || (page_d && gpair_fx_d && build_h), "gbt_build_hist_noalloc: NULL rows input");
+    GBT_CHECK(n_sub == 0 || (sub_h && parent_hist_d), "gbt_build_hist_noalloc: NULL subtraction input");
+    GBT_CHECK(((uintptr_t)page_d & 15) == 0, "gbt_build_hist_noalloc: the page must be 16-byte aligned");
+    for (int32_t k = 0; k < n_build; ++k)
+        GBT_CHECK(build_h[k].begin >= 0 && build_h[k].begin <= build_h[k].end && build_h[k].node_slot >= 0,
+                  "bad build segment %d", k);
+    GBT_TRY(set_device(c));
+    HistWorkspace ws;
+    GBT_TRY(static_scratch(c->device, &ws));
+    GBT_TRY(build_hist_impl(c, layout, page_d, gpair_fx_d, rows_d, build_h, n_build, sub_h, n_sub,
+                            parent_hist_d, hist_d, nullptr, &ws));
     GBT_HIP(hipStreamSynchronize(c->stream));
     return GBT_OK;
 }

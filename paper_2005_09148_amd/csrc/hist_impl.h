@@ -71,7 +71,20 @@ struct HistLaunch {
     int64_t *partials;
     const uint8_t *slot_tbl = nullptr;  // sparse: the page's slot table by row (SlotTable::row), or NULL
     int32_t tbl_stride = 0;
+    bool timed = true;  // record phase events (when the context's timing is on)
 };
+
+// Device memory a histogram call carves its partials and plan from, in
+// place of the context's workspaces (base is 256-byte aligned).
+struct HistWorkspace {
+    char *base;
+    size_t bytes;
+};
+
+// The static scratch of the allocation-free histogram entry point: its
+// device address on `device` is resolved once (hipGetSymbolAddress) with
+// that device current.
+gbt_status static_scratch_init(int device);
 
 // Whether a sparse page of mx's geometry takes a slot table for G groups
 // (rows of at most 255 slots and 64 words, at most 63 groups).

@@ -165,6 +165,7 @@ SIGNATURES = {
     "gbt_sampled_info_get": (_i32, [_vp, _vp]),
     "gbt_sampled_free": (_i32, [_vp]),
     "gbt_build_hist": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp]),
+    "gbt_build_hist_noalloc": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp]),
     "gbt_eval_splits": (_i32, [_vp, _vp, _vp, _vp, _vp, _i32, _vp, _i32, _i32, _vp]),
     "gbt_partition": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _i64, _vp, _vp]),
     "gbt_update_leaves": (_i32, [_vp, _vp, _vp, _vp, _vp]),
@@ -561,8 +562,11 @@ def gbt_sample(ctx, matrix: Matrix, gpair=None, margin=None, label=None, f=1.0, 
     return SampleResult(info, page, rows, gw, q)
 
 
-def gbt_build_hist(ctx, matrix: Matrix, page, q, rows, build, sub=(), parent_hist=None, hist=None):
-    """build: [(slot, begin, end)], sub: [(parent_slot, built_slot, target_slot)]."""
+def gbt_build_hist(ctx, matrix: Matrix, page, q, rows, build, sub=(), parent_hist=None, hist=None,
+                   noalloc=False):
+    """build: [(slot, begin, end)], sub: [(parent_slot, built_slot, target_slot)].
+    noalloc: call gbt_build_hist_noalloc (no device allocation; the
+    library's static scratch) instead of gbt_build_hist."""
     torch = _torch()
     inf = matrix.info()
     if page is None or page.dim() != 2 or page.shape[1] != inf.row_words:
@@ -586,8 +590,8 @@ def gbt_build_hist(ctx, matrix: Matrix, page, q, rows, build, sub=(), parent_his
                                           (parent_hist, "parent_hist", i64, None, not sub))
     bl = (Seg * max(len(build), 1))(*[Seg(s, 0, b, e) for s, b, e in build])
     sl = (Sub * max(len(sub), 1))(*[Sub(p, b, t, 0) for p, b, t in sub])
-    _check(_lib.gbt_build_hist(ctx.h, matrix.h, pg_p, q_p, r_p, bl, len(build),
-                               sl, len(sub), ph_p, h_p))
+    fn = _lib.gbt_build_hist_noalloc if noalloc else _lib.gbt_build_hist
+    _check(fn(ctx.h, matrix.h, pg_p, q_p, r_p, bl, len(build), sl, len(sub), ph_p, h_p))
     return hist
 
 
