@@ -20,7 +20,8 @@
  * Contents, in the order the paper presents them:
  *   orc_exp / orc_philox4x64_10 ...... helpers (Cody-Waite exp; Philox of
  *                                       Salmon et al., SC'11)
- *   orc_sketch_cuts_* ................ Sec. 3.1 (Alg. 2/3): quantile cuts
+ *   orc_sketch_cuts_* ................ Sec. 3.1 (Alg. 2/3): quantile cuts,
+ *                                       exact and batch-merged (Alg. 3)
  *   orc_bin_* / orc_ellpack_* ........ Sec. 2.2 + Sec. 3.2 (Alg. 4/5): bins
  *                                       and bit-packed ELLPACK rows
  *   orc_gradients .................... Sec. 2.1, Eq. 4-5: g and h
@@ -368,6 +369,302 @@ int orc_sketch_cuts_csr(const int64_t *indptr, const int32_t *indices, const flo
     free(fill);
     free(cnt);
     return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Sec. 3.1, Alg. 3: the out-of-core sketch.  The sketch sample (the rows    */
+/* above) arrives in batches, and each batch's column cuts are folded into   */
+/* one running summary per feature.  The paper leaves the folding open;      */
+/* reading: a summary is a list of distinct values v_1 < ... < v_k, each     */
+/* with an estimate c_i of the number of sample values <= v_i (c_k = N, the  */
+/* values summarised).                                                       */
+/*   batch summary: the batch's sorted values; all its distinct values with  */
+/*     their exact counts, pruned to S entries.                              */
+/*   merge(A, B): every value of A or B, with c(v) = c_A(v) + c_B(v), where  */
+/*     c_X(v) is the count of X's last entry <= v (0 if none); pruned to S.  */
+/*   prune to S (when k > S): for t = 1..S the entry i_t = min{ i : c_i >=   */
+/*     ceil(t N / S) }, each entry kept once (i_S = k: the maximum stays).   */
+/*   running summary: R_b = merge(R_{b-1}, summary of batch b), batch order. */
+/*   cuts: candidate j (1..B-1) is the value of min{ i : c_i >= ceil(jN/B) }; */
+/*     duplicates and values >= v_k dropped, as for the exact rule.          */
+/* When no summary ever exceeds S entries every count is exact and the cuts  */
+/* equal the exact rule's over the whole sample.  Otherwise each prune and   */
+/* merge can only lower a count: c(v) <= the true count of values <= v.      */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+    float v;
+    int64_t c;
+} orc_entry;
+
+/* Prune k entries (in) over N values to at most S (out, separate). */
+static int64_t summary_prune(const orc_entry *in, int64_t k, int64_t N, int32_t S, orc_entry *out)
+{
+    if (k <= S) {
+        memcpy(out, in, sizeof(orc_entry) * (size_t)k);
+        return k;
+    }
+    int64_t o = 0, i = 0, last = -1;
+    for (int64_t t = 1; t <= S; ++t) {
+        int64_t target = (t * N + S - 1) / S;
+        while (in[i].c < target) ++i;
+        if (i != last) out[o++] = in[i];
+        last = i;
+    }
+    return o;
+}
+
+/* The exact summary of n sorted values (distinct values, counts <= each). */
+static int64_t summary_of_sorted(const float *vals, int64_t n, orc_entry *out)
+{
+    int64_t k = 0;
+    for (int64_t i = 0; i < n; ++i)
+        if (i == n - 1 || vals[i] != vals[i + 1]) {
+            out[k].v = vals[i];
+            out[k].c = i + 1;
+            ++k;
+        }
+    return k;
+}
+
+static int64_t summary_merge(const orc_entry *A, int64_t ka, const orc_entry *B, int64_t kb, orc_entry *U)
+{
+    int64_t i = 0, j = 0, k = 0, ca = 0, cb = 0;
+    while (i < ka || j < kb) {
+        float v;
+        if (j >= kb || (i < ka && A[i].v < B[j].v)) {
+            v = A[i].v;
+            ca = A[i].c;
+            ++i;
+        } else if (i >= ka || B[j].v < A[i].v) {
+            v = B[j].v;
+            cb = B[j].c;
+            ++j;
+        } else {
+            v = A[i].v;
+            ca = A[i].c;
+            cb = B[j].c;
+            ++i;
+            ++j;
+        }
+        U[k].v = v;
+        U[k].c = ca + cb;
+        ++k;
+    }
+    return k;
+}
+
+/* The running summary of one feature after one more batch of n values
+ * (NaN removed, -0 made +0; vals is sorted in place). */
+static int summary_add_batch(orc_entry **R, int64_t *kR, float *vals, int64_t n, int32_t S)
+{
+    if (n <= 0) return ORC_OK;
+    qsort(vals, (size_t)n, sizeof(float), cmp_float);
+    orc_entry *e = (orc_entry *)malloc(sizeof(orc_entry) * (size_t)n);
+    orc_entry *b = (orc_entry *)malloc(sizeof(orc_entry) * (size_t)(S + 1));
+    orc_entry *u = (orc_entry *)malloc(sizeof(orc_entry) * (size_t)(*kR + S + 1));
+    orc_entry *r = (orc_entry *)malloc(sizeof(orc_entry) * (size_t)(S + 1));
+    if (!e || !b || !u || !r) {
+        free(e);
+        free(b);
+        free(u);
+        free(r);
+        return ORC_ENOMEM;
+    }
+    int64_t ke = summary_of_sorted(vals, n, e);
+    int64_t kb = summary_prune(e, ke, n, S, b);
+    int64_t NR = *kR ? (*R)[*kR - 1].c : 0;
+    int64_t ku = summary_merge(*R, *kR, b, kb, u);
+    int64_t kr = summary_prune(u, ku, NR + n, S, r);
+    free(e);
+    free(b);
+    free(u);
+    free(*R);
+    *R = r;
+    *kR = kr;
+    return ORC_OK;
+}
+
+/* Cuts of one feature from its summary (at most B-1; returns their count). */
+static int32_t cuts_from_summary(const orc_entry *R, int64_t k, int32_t B, float *out)
+{
+    if (k <= 0) return 0;
+    int64_t N = R[k - 1].c;
+    float top = R[k - 1].v;
+    int32_t c = 0;
+    int64_t i = 0;
+    for (int64_t j = 1; j < B; ++j) {
+        int64_t target = (j * N + B - 1) / B;
+        while (R[i].c < target) ++i;
+        float t = R[i].v;
+        if (t >= top) continue;
+        if (c > 0 && t == out[c - 1]) continue;
+        out[c++] = t;
+    }
+    return c;
+}
+
+/* Dense input in batches of batch_rows rows (the last one shorter).  The
+ * sketch sample is the rows of the exact rule (stride from n and
+ * sketch_max_rows); summary_size = S >= 2.  Same outputs as
+ * orc_sketch_cuts_dense; entries_out (optional) receives each feature's
+ * final summary size. */
+int orc_sketch_cuts_merge_dense(const float *X, int64_t n, int32_t m, int64_t ld, int32_t max_bin,
+                                int64_t sketch_max_rows, int32_t S, int64_t batch_rows, int32_t *cut_ptr,
+                                float *cut_values, int64_t *entries_out)
+{
+    if (n < 0 || m <= 0 || max_bin < 2 || ld < m || S < 2 || batch_rows <= 0) return ORC_EINVAL;
+    int64_t stride = sketch_stride(n, sketch_max_rows);
+    float *tmp = (float *)malloc(sizeof(float) * (size_t)m * (size_t)(max_bin - 1));
+    int32_t *cnt = (int32_t *)malloc(sizeof(int32_t) * (size_t)m);
+    if (!tmp || !cnt) {
+        free(tmp);
+        free(cnt);
+        return ORC_ENOMEM;
+    }
+    int bad = 0, oom = 0;
+    /* omp: features are independent */
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : bad, oom)
+    for (int32_t j = 0; j < m; ++j) {
+        orc_entry *R = NULL;
+        int64_t kR = 0;
+        float *vals = (float *)malloc(sizeof(float) * (size_t)(batch_rows / stride + 2));
+        cnt[j] = 0;
+        if (!vals) {
+            oom = 1;
+            continue;
+        }
+        for (int64_t b0 = 0; b0 < n && !bad && !oom; b0 += batch_rows) {
+            int64_t b1 = b0 + batch_rows < n ? b0 + batch_rows : n, N = 0;
+            for (int64_t i = (b0 + stride - 1) / stride * stride; i < b1; i += stride) {
+                float x = X[i * ld + j];
+                if (isnan(x)) continue;
+                if (isinf(x)) {
+                    bad = 1;
+                    break;
+                }
+                if (x == 0.0f) x = 0.0f;
+                vals[N++] = x;
+            }
+            if (!bad && summary_add_batch(&R, &kR, vals, N, S) != ORC_OK) oom = 1;
+        }
+        if (!bad && !oom) cnt[j] = cuts_from_summary(R, kR, max_bin, tmp + (size_t)j * (size_t)(max_bin - 1));
+        if (entries_out) entries_out[j] = kR;
+        free(R);
+        free(vals);
+    }
+    if (!bad && !oom) {
+        cut_ptr[0] = 0;
+        for (int32_t j = 0; j < m; ++j) {
+            memcpy(cut_values + cut_ptr[j], tmp + (size_t)j * (size_t)(max_bin - 1), sizeof(float) * (size_t)cnt[j]);
+            cut_ptr[j + 1] = cut_ptr[j] + cnt[j];
+        }
+    }
+    free(tmp);
+    free(cnt);
+    return oom ? ORC_ENOMEM : (bad ? ORC_EINVAL : ORC_OK);
+}
+
+/* The final running summary of feature j of dense input (as in
+ * orc_sketch_cuts_merge_dense): its k entries (returned) into v[], c[]
+ * (room for S entries), or -1 on error. */
+int64_t orc_sketch_summary_dense(const float *X, int64_t n, int32_t m, int64_t ld, int64_t sketch_max_rows,
+                                 int32_t S, int64_t batch_rows, int32_t j, float *v, int64_t *c)
+{
+    if (n < 0 || j < 0 || j >= m || ld < m || S < 2 || batch_rows <= 0) return -1;
+    int64_t stride = sketch_stride(n, sketch_max_rows);
+    orc_entry *R = NULL;
+    int64_t kR = 0;
+    float *vals = (float *)malloc(sizeof(float) * (size_t)(batch_rows / stride + 2));
+    if (!vals) return -1;
+    for (int64_t b0 = 0; b0 < n; b0 += batch_rows) {
+        int64_t b1 = b0 + batch_rows < n ? b0 + batch_rows : n, N = 0;
+        for (int64_t i = (b0 + stride - 1) / stride * stride; i < b1; i += stride) {
+            float x = X[i * ld + j];
+            if (isnan(x)) continue;
+            if (isinf(x)) {
+                free(vals);
+                free(R);
+                return -1;
+            }
+            if (x == 0.0f) x = 0.0f;
+            vals[N++] = x;
+        }
+        if (summary_add_batch(&R, &kR, vals, N, S) != ORC_OK) {
+            free(vals);
+            free(R);
+            return -1;
+        }
+    }
+    for (int64_t i = 0; i < kR; ++i) {
+        v[i] = R[i].v;
+        c[i] = R[i].c;
+    }
+    free(vals);
+    free(R);
+    return kR;
+}
+
+/* CSR input in batches of batch_rows rows: as orc_sketch_cuts_merge_dense,
+ * absent entries and NaN values missing. */
+int orc_sketch_cuts_merge_csr(const int64_t *indptr, const int32_t *indices, const float *values, int64_t n,
+                              int32_t m, int32_t max_bin, int64_t sketch_max_rows, int32_t S, int64_t batch_rows,
+                              int32_t *cut_ptr, float *cut_values, int64_t *entries_out)
+{
+    if (n < 0 || m <= 0 || max_bin < 2 || S < 2 || batch_rows <= 0) return ORC_EINVAL;
+    int64_t stride = sketch_stride(n, sketch_max_rows);
+    for (int64_t i = 0; i < n; ++i)
+        for (int64_t e = indptr[i]; e < indptr[i + 1]; ++e)
+            if (indices[e] < 0 || indices[e] >= m || isinf(values[e])) return ORC_EINVAL;
+    orc_entry **R = (orc_entry **)calloc((size_t)m, sizeof(orc_entry *));
+    int64_t *kR = (int64_t *)calloc((size_t)m, sizeof(int64_t));
+    int64_t *cnt = (int64_t *)malloc(sizeof(int64_t) * (size_t)(m + 1));
+    int64_t *fill = (int64_t *)malloc(sizeof(int64_t) * (size_t)m);
+    float *vals = NULL;
+    int rc = (R && kR && cnt && fill) ? ORC_OK : ORC_ENOMEM;
+    for (int64_t b0 = 0; b0 < n && rc == ORC_OK; b0 += batch_rows) {
+        int64_t b1 = b0 + batch_rows < n ? b0 + batch_rows : n;
+        /* the batch's sample values, grouped by feature */
+        memset(cnt, 0, sizeof(int64_t) * (size_t)(m + 1));
+        for (int64_t i = (b0 + stride - 1) / stride * stride; i < b1; i += stride)
+            for (int64_t e = indptr[i]; e < indptr[i + 1]; ++e)
+                if (!isnan(values[e])) cnt[indices[e] + 1]++;
+        for (int32_t j = 0; j < m; ++j) cnt[j + 1] += cnt[j];
+        free(vals);
+        vals = (float *)malloc(sizeof(float) * (size_t)(cnt[m] + 1));
+        if (!vals) {
+            rc = ORC_ENOMEM;
+            break;
+        }
+        for (int32_t j = 0; j < m; ++j) fill[j] = cnt[j];
+        for (int64_t i = (b0 + stride - 1) / stride * stride; i < b1; i += stride)
+            for (int64_t e = indptr[i]; e < indptr[i + 1]; ++e) {
+                float x = values[e];
+                if (isnan(x)) continue;
+                if (x == 0.0f) x = 0.0f;
+                vals[fill[indices[e]]++] = x;
+            }
+        int oom = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : oom)
+        for (int32_t j = 0; j < m; ++j)
+            if (summary_add_batch(&R[j], &kR[j], vals + cnt[j], cnt[j + 1] - cnt[j], S) != ORC_OK) oom = 1;
+        if (oom) rc = ORC_ENOMEM;
+    }
+    if (rc == ORC_OK) {
+        cut_ptr[0] = 0;
+        for (int32_t j = 0; j < m; ++j) {
+            int32_t c = cuts_from_summary(R[j], kR[j], max_bin, cut_values + cut_ptr[j]);
+            cut_ptr[j + 1] = cut_ptr[j] + c;
+            if (entries_out) entries_out[j] = kR[j];
+        }
+    }
+    if (R)
+        for (int32_t j = 0; j < m; ++j) free(R[j]);
+    free(R);
+    free(kR);
+    free(cnt);
+    free(fill);
+    free(vals);
+    return rc;
 }
 
 /* bin(x) = #{cuts < x}: the cuts ascend, so this is the first index whose

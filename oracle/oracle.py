@@ -115,6 +115,9 @@ def lib():
             "orc_philox4x64_10": (None, [vp, vp, vp]),
             "orc_sketch_cuts_dense": (C.c_int, [vp, i64, i32, i64, i32, i64, vp, vp]),
             "orc_sketch_cuts_csr": (C.c_int, [vp, vp, vp, i64, i32, i32, i64, vp, vp]),
+            "orc_sketch_cuts_merge_dense": (C.c_int, [vp, i64, i32, i64, i32, i64, i32, i64, vp, vp, vp]),
+            "orc_sketch_cuts_merge_csr": (C.c_int, [vp, vp, vp, i64, i32, i32, i64, i32, i64, vp, vp, vp]),
+            "orc_sketch_summary_dense": (i64, [vp, i64, i32, i64, i64, i32, i64, i32, vp, vp]),
             "orc_bin_dense": (C.c_int, [vp, i64, i32, i64, vp, vp, vp]),
             "orc_bin_csr": (C.c_int, [vp, vp, vp, i64, i32, vp, vp, vp, vp, vp]),
             "orc_ellpack_geometry": (None, [i32, i32, vp, i32, i32, vp]),
@@ -215,6 +218,48 @@ def sketch_cuts_csr(indptr, indices, values, m, max_bin, sketch_max_rows=1 << 24
     if rc:
         raise ValueError(f"orc_sketch_cuts_csr failed ({rc})")
     return Cuts(cp, cv[:cp[m]].copy())
+
+
+def sketch_cuts_merge_dense(X, max_bin, summary_size, batch_rows, sketch_max_rows=1 << 24):
+    """Sec. 3.1 Alg. 3: cuts from per-batch summaries (batches of batch_rows
+    rows) merged into one running summary of at most summary_size entries
+    per feature; returns (Cuts, entries per feature)."""
+    X = _c(X, np.float32)
+    n, m = X.shape
+    cp = np.zeros(m + 1, np.int32)
+    cv = np.zeros(m * (max_bin - 1) + 1, np.float32)
+    ent = np.zeros(m, np.int64)
+    rc = lib().orc_sketch_cuts_merge_dense(_p(X), n, m, m, max_bin, sketch_max_rows, summary_size, batch_rows,
+                                           _p(cp), _p(cv), _p(ent))
+    if rc:
+        raise ValueError(f"orc_sketch_cuts_merge_dense failed ({rc})")
+    return Cuts(cp, cv[:cp[m]].copy()), ent
+
+
+def sketch_cuts_merge_csr(indptr, indices, values, m, max_bin, summary_size, batch_rows,
+                          sketch_max_rows=1 << 24):
+    indptr, indices, values = _c(indptr, np.int64), _c(indices, np.int32), _c(values, np.float32)
+    n = len(indptr) - 1
+    cp = np.zeros(m + 1, np.int32)
+    cv = np.zeros(m * (max_bin - 1) + 1, np.float32)
+    ent = np.zeros(m, np.int64)
+    rc = lib().orc_sketch_cuts_merge_csr(_p(indptr), _p(indices), _p(values), n, m, max_bin, sketch_max_rows,
+                                         summary_size, batch_rows, _p(cp), _p(cv), _p(ent))
+    if rc:
+        raise ValueError(f"orc_sketch_cuts_merge_csr failed ({rc})")
+    return Cuts(cp, cv[:cp[m]].copy()), ent
+
+
+def sketch_summary_dense(X, j, summary_size, batch_rows, sketch_max_rows=1 << 24):
+    """The final running summary of feature j: (values, counts)."""
+    X = _c(X, np.float32)
+    n, m = X.shape
+    v = np.zeros(summary_size + 1, np.float32)
+    c = np.zeros(summary_size + 1, np.int64)
+    k = lib().orc_sketch_summary_dense(_p(X), n, m, m, sketch_max_rows, summary_size, batch_rows, j, _p(v), _p(c))
+    if k < 0:
+        raise ValueError("orc_sketch_summary_dense failed")
+    return v[:k].copy(), c[:k].copy()
 
 
 @dataclass
