@@ -53,7 +53,7 @@ typedef int32_t gbt_status;
 #define GBT_SAMPLE_SGB 1  /* stochastic gradient boosting: uniform rows */
 #define GBT_SAMPLE_GOSS 2 /* gradient-based one-side sampling */
 
-#define GBT_ABI_VERSION 3
+#define GBT_ABI_VERSION 4
 
 enum { GBT_INPUT_DENSE_F32 = 0, GBT_INPUT_CSR_F32 = 1 };
 enum { GBT_LOC_HOST = 0, GBT_LOC_DEVICE = 1 };
@@ -88,6 +88,10 @@ typedef struct {
     int64_t sketch_max_rows;  /* 0 = 2^24: above it, every ceil(n/this)-th row is sketched */
     int64_t page_rows;        /* rows per ELLPACK page; 0 = one page */
     const char *page_dir;     /* GBT_HOME_DISK: an existing directory for the page files */
+    int32_t sketch_summary;   /* 0: exact cuts of the sketch sample held whole on the device;
+                                 S in [2, 2^20]: Alg. 3's merged sketch, at most S entries per
+                                 feature (see gbt_quantize) */
+    int32_t pad0;
 } gbt_quant_params;
 
 /* Geometry of a quantized matrix.  Symbols: dense pages hold feature j's
@@ -280,7 +284,21 @@ gbt_status gbt_ctx_set_stream_chunk_rows(gbt_ctx *ctx, int64_t rows);
  * form takes batches (Alg. 3 sketch, then Alg. 5 pages):
  *   begin -> sketch_batch* (every batch, in row order) -> finalize_cuts ->
  *   encode_batch* (every batch again, same order) -> end.
- * n_rows_total fixes the sketch stride.  page_home DISK writes each page to
+ * n_rows_total fixes the sketch stride.
+ * sketch_summary = S > 0 selects Alg. 3's merged sketch instead: each
+ * sketch_batch call is one batch (gbt_quantize makes one batch of its
+ * input); the batch's sample values of every feature, sorted on the device,
+ * become a summary -- a list of distinct values v_1 < ... < v_k, each with a
+ * count c_i of the values <= v_i: the batch's distinct values with their
+ * exact counts when there are at most S, else the values at ranks
+ * ceil(tN/S), t = 1..S -- which is merged into the running summary (every
+ * value of either, counted c_A(v) + c_B(v) with c_X(v) the count of X's last
+ * entry <= v) and pruned back to S entries (entry min{i : c_i >= ceil(tN/S)}
+ * for t = 1..S).  The cuts are the exact rule applied to the final summary
+ * (candidate k: the value of min{i : c_i >= ceil(kN/max_bin)}), so they equal
+ * the exact cuts whenever no summary exceeds S entries.  The device holds one
+ * batch's sample keys and 5 * n_cols * S summary entries of 12 bytes, not
+ * the whole sample.  page_home DISK writes each page to
  * a file of its own under page_dir (Sec. 3.2: pages on disk), created
  * exclusively and unlinked at once, so the files vanish with the matrix or
  * the process; each tree then reads the pages back through pinned staging

@@ -25,7 +25,7 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-ffp-contract=o
          "-fno-fast-math", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wno-unused-command-line-argument", "-I", INCLUDE, "-I", CSRC]
 
-SOURCES = ["ctx.hip", "scan.hip", "quantize.hip", "sample.hip", "hist.hip", "split.hip", "tree.hip"]
+SOURCES = ["ctx.hip", "scan.hip", "quantize.hip", "sketch.hip", "sample.hip", "hist.hip", "split.hip", "tree.hip"]
 
 
 def _compile(src: str) -> str:

@@ -13,6 +13,7 @@
 // Pages: row-major rows of row_words 32-bit words; a row is the LSB-first
 // bit stream of its stride symbols (w bits each), zero padded.
 #include "common.h"
+#include "sketch_impl.h"
 
 #include <algorithm>
 #include <cerrno>
@@ -48,9 +49,10 @@ inline float key_float(uint32_t k)
 enum { kStNan = 0, kStInf, kStMaxNnz, kStKeys, kStBadIndex, kStWords };
 
 // Dense batch: validate every value, record the sketch keys of the sampled
-// rows (global row g with g % stride == 0) feature-major.
+// rows (global row g with g % stride == 0) feature-major: sample g / stride
+// at column g / stride - s_base of a key matrix of n_sketch columns.
 __global__ void k_dense_sketch(const float *__restrict__ X, int64_t rows, int32_t m, int64_t ld,
-                               int64_t row0, int64_t stride, int64_t n_sketch,
+                               int64_t row0, int64_t stride, int64_t n_sketch, int64_t s_base,
                                uint32_t *__restrict__ keys, unsigned long long *__restrict__ st)
 {
     int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -58,14 +60,14 @@ __global__ void k_dense_sketch(const float *__restrict__ X, int64_t rows, int32_
     if (i < rows) {
         int64_t g = row0 + i;
         bool take = (g % stride) == 0;
-        int64_t s = g / stride;
+        int64_t s = g / stride - s_base;
         const float *x = X + i * ld;
         for (int32_t j = 0; j < m; ++j) {
             float v = x[j];
             bool isn = v != v;
             nan |= isn;
             inf |= (!isn && (v - v) != 0.0f);
-            if (take && s < n_sketch) keys[(int64_t)j * n_sketch + s] = isn ? kNanKey : float_key(v);
+            if (take && s >= 0 && s < n_sketch) keys[(int64_t)j * n_sketch + s] = isn ? kNanKey : float_key(v);
         }
     }
     if (__any(nan) && (threadIdx.x & 63) == 0) atomicOr(&st[kStNan], 1ull);
@@ -300,6 +302,11 @@ struct gbt_quantizer {
     std::string dir;
     void *bounce = nullptr;
     size_t bounce_bytes = 0;
+    // merged sketch (sketch_summary > 0): the running summaries, and the
+    // keys of one batch
+    MergeSketch *ms = nullptr;
+    uint32_t *bkeys = nullptr;
+    size_t bkeys_bytes = 0;
 };
 
 namespace {
@@ -393,9 +400,55 @@ void free_quantizer(gbt_quantizer *q)
     dev_free(c, q->st, kStWords * sizeof(unsigned long long));
     dev_free(c, q->stage, q->stage_bytes);
     dev_free(c, q->enc, q->enc_bytes);
+    dev_free(c, q->bkeys, q->bkeys_bytes);
+    if (q->ms) {
+        merge_sketch_free(c, q->ms);
+        delete q->ms;
+    }
     if (q->bounce) (void)hipHostFree(q->bounce);
     if (q->mat) gbt_matrix_free(q->mat);
     delete q;
+}
+
+// A merged sketch's CSR batch: the batch's (feature, key) pairs grouped by
+// feature (counts, then a scatter), summarised and merged.
+gbt_status csr_merge_batch(gbt_quantizer *q)
+{
+    gbt_ctx *c = q->ctx;
+    const int32_t m = q->m;
+    unsigned long long stv[kStWords];
+    GBT_TRY(read_status(q, stv));
+    GBT_CHECK(!stv[kStBadIndex], "CSR column indices must be in [0, n_cols) and strictly ascending");
+    const int64_t nk = (int64_t)stv[kStKeys];
+    if (nk == 0) return GBT_OK;
+    unsigned long long *cnt = nullptr;
+    GBT_TRY(dev_alloc(c, (size_t)(m + 1) * 8, (void **)&cnt));
+    std::vector<unsigned long long> h(m + 1, 0ull), cur(m);
+    gbt_status s = GBT_OK;
+    auto run = [&]() -> gbt_status {
+        GBT_HIP(hipMemcpyAsync(cnt, h.data(), (m + 1) * 8, hipMemcpyHostToDevice, c->stream));
+        k_feat_count<<<grid_for(nk, 256), 256, 0, c->stream>>>(q->feats, nk, cnt);
+        GBT_LAUNCHED();
+        GBT_HIP(hipMemcpyAsync(h.data(), cnt, m * 8, hipMemcpyDeviceToHost, c->stream));
+        GBT_HIP(hipStreamSynchronize(c->stream));
+        std::vector<int64_t> sb(m), sl(m);
+        int64_t o = 0;
+        for (int32_t j = 0; j < m; ++j) {
+            sb[j] = o;
+            sl[j] = (int64_t)h[j];
+            cur[j] = (unsigned long long)o;
+            o += (int64_t)h[j];
+        }
+        GBT_TRY(ensure_buf(c, (void **)&q->bkeys, &q->bkeys_bytes, (size_t)nk * 4));
+        GBT_HIP(hipMemcpyAsync(cnt, cur.data(), m * 8, hipMemcpyHostToDevice, c->stream));
+        k_feat_scatter<<<grid_for(nk, 256), 256, 0, c->stream>>>(q->feats, q->keys, nk, cnt, q->bkeys);
+        GBT_LAUNCHED();
+        return merge_sketch_add(c, q->ms, q->bkeys, sb.data(), sl.data());
+    };
+    s = run();
+    (void)hipStreamSynchronize(c->stream);
+    dev_free(c, cnt, (size_t)(m + 1) * 8);
+    return s;
 }
 
 }  // namespace
@@ -417,6 +470,8 @@ gbt_status gbt_quantize_begin(gbt_ctx *c, const gbt_quant_params *p, int32_t n_c
               "unknown page_home %d", p->page_home);
     GBT_CHECK(p->page_home != GBT_HOME_DISK || (p->page_dir && p->page_dir[0]), "disk pages need page_dir");
     GBT_CHECK(p->page_rows >= 0 && p->sketch_max_rows >= 0, "negative page/sketch rows");
+    GBT_CHECK(p->sketch_summary == 0 || (p->sketch_summary >= 2 && p->sketch_summary <= (1 << 20)),
+              "sketch_summary %d outside {0} and [2, 2^20]", p->sketch_summary);
     GBT_TRY(set_device(c));
     auto *q = new gbt_quantizer();
     q->ctx = c;
@@ -437,7 +492,10 @@ gbt_status gbt_quantize_begin(gbt_ctx *c, const gbt_quant_params *p, int32_t n_c
         if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
         if (e != hipSuccess) s = hip_error(e, "status init", __FILE__, __LINE__);
     }
-    if (s == GBT_OK && input_kind == GBT_INPUT_DENSE_F32) {
+    if (s == GBT_OK && p->sketch_summary > 0) {
+        q->ms = new MergeSketch();
+        s = merge_sketch_init(c, q->ms, n_cols, p->sketch_summary);
+    } else if (s == GBT_OK && input_kind == GBT_INPUT_DENSE_F32) {
         q->n_sketch = (n_rows_total + q->stride - 1) / q->stride;
         q->keys_bytes = (size_t)q->n_sketch * (size_t)n_cols * 4;
         s = dev_alloc(c, q->keys_bytes, (void **)&q->keys);
@@ -462,14 +520,34 @@ gbt_status gbt_quantize_sketch_batch(gbt_quantizer *q, const gbt_input *batch)
     GBT_CHECK(q->sketched_rows + b.rows <= q->n_total, "more rows than announced (%lld)",
               (long long)q->n_total);
     if (b.rows > 0) {
-        if (q->kind == GBT_INPUT_DENSE_F32) {
+        if (q->kind == GBT_INPUT_DENSE_F32 && q->ms) {
+            // Alg. 3: this batch's sample keys, sorted per feature, summarised
+            // and merged into the running summaries
+            const int64_t g0 = q->sketched_rows, g1 = g0 + b.rows;
+            const int64_t s_lo = (g0 + q->stride - 1) / q->stride, s_hi = (g1 + q->stride - 1) / q->stride;
+            const int64_t ns = s_hi - s_lo;
+            GBT_TRY(ensure_buf(c, (void **)&q->bkeys, &q->bkeys_bytes, std::max<size_t>((size_t)ns * q->m * 4, 16)));
             k_dense_sketch<<<grid_for(b.rows, 256), 256, 0, c->stream>>>(
-                b.values, b.rows, q->m, b.ld, q->sketched_rows, q->stride, q->n_sketch, q->keys, q->st);
+                b.values, b.rows, q->m, b.ld, g0, q->stride, ns, s_lo, q->bkeys, q->st);
+            GBT_LAUNCHED();
+            std::vector<int64_t> sb(q->m), sl(q->m, ns);
+            for (int32_t j = 0; j < q->m; ++j) sb[j] = (int64_t)j * ns;
+            if (ns > 0) GBT_TRY(merge_sketch_add(c, q->ms, q->bkeys, sb.data(), sl.data()));
+        } else if (q->kind == GBT_INPUT_DENSE_F32) {
+            k_dense_sketch<<<grid_for(b.rows, 256), 256, 0, c->stream>>>(
+                b.values, b.rows, q->m, b.ld, q->sketched_rows, q->stride, q->n_sketch, 0, q->keys, q->st);
             GBT_LAUNCHED();
         } else {
-            // grow the pair buffers to hold every entry of this batch
+            // grow the pair buffers to hold every entry of this batch (a
+            // merged sketch keeps one batch's pairs at a time)
             unsigned long long stv[kStWords];
             GBT_TRY(read_status(q, stv));
+            if (q->ms && stv[kStKeys]) {
+                const unsigned long long zero = 0;
+                GBT_HIP(hipMemcpyAsync(q->st + kStKeys, &zero, 8, hipMemcpyHostToDevice, c->stream));
+                GBT_HIP(hipStreamSynchronize(c->stream));
+                stv[kStKeys] = 0;
+            }
             int64_t need = (int64_t)stv[kStKeys] + b.nnz;
             if (need > q->keys_cap) {
                 int64_t cap = std::max<int64_t>(need, q->keys_cap * 2);
@@ -497,6 +575,7 @@ gbt_status gbt_quantize_sketch_batch(gbt_quantizer *q, const gbt_input *batch)
                 b.indptr, b.indices, b.values, b.rows, q->m, q->sketched_rows, q->stride, q->keys,
                 q->feats, q->st);
             GBT_LAUNCHED();
+            if (q->ms) GBT_TRY(csr_merge_batch(q));
         }
     }
     q->sketched_rows += b.rows;
@@ -505,6 +584,46 @@ gbt_status gbt_quantize_sketch_batch(gbt_quantizer *q, const gbt_input *batch)
     GBT_CHECK(!stv[kStInf], "input holds an infinite value");
     GBT_CHECK(!stv[kStBadIndex], "CSR column indices must be in [0, n_cols) and strictly ascending");
     return GBT_OK;
+}
+
+static gbt_status finish_cuts(gbt_quantizer *q, std::vector<int32_t> cut_ptr_h, std::vector<float> cut_values_h,
+                              std::vector<int64_t> feat_count, const unsigned long long *stv);
+
+// Cuts of a merged sketch from its running summaries: candidate k is the
+// value of the first entry whose count reaches ceil(kN/B), duplicates and
+// values >= the maximum dropped.
+static gbt_status finalize_merged(gbt_quantizer *q, const unsigned long long *stv)
+{
+    const int32_t m = q->m, B = q->p.max_bin, S = q->ms->S;
+    std::vector<uint32_t> v;
+    std::vector<long long> cnt;
+    std::vector<int64_t> k;
+    GBT_TRY(merge_sketch_download(q->ctx, q->ms, &v, &cnt, &k));
+    std::vector<int32_t> cut_ptr_h(m + 1, 0);
+    std::vector<float> cut_values_h;
+    std::vector<int64_t> feat_count;
+    for (int32_t j = 0; j < m; ++j) {
+        const uint32_t *vj = v.data() + (size_t)j * S;
+        const long long *cj = cnt.data() + (size_t)j * S;
+        const int64_t kj = k[j];
+        const long long N = kj ? cj[kj - 1] : 0;
+        feat_count.push_back((int64_t)N);
+        if (kj > 0) {
+            const uint32_t top = vj[kj - 1];
+            int64_t i = 0;
+            for (int64_t b = 1; b < B; ++b) {
+                const long long target = (b * N + B - 1) / B;
+                while (cj[i] < target) ++i;
+                if (vj[i] >= top) continue;
+                const float x = key_float(vj[i]);
+                if (cut_values_h.size() > (size_t)cut_ptr_h[j] && x == cut_values_h.back()) continue;
+                cut_values_h.push_back(x);
+            }
+        }
+        cut_ptr_h[j + 1] = (int32_t)cut_values_h.size();
+    }
+    if (q->kind != GBT_INPUT_CSR_F32) feat_count.clear();
+    return finish_cuts(q, std::move(cut_ptr_h), std::move(cut_values_h), std::move(feat_count), stv);
 }
 
 gbt_status gbt_quantize_finalize_cuts(gbt_quantizer *q)
@@ -518,6 +637,10 @@ gbt_status gbt_quantize_finalize_cuts(gbt_quantizer *q)
     const int32_t m = q->m, B = q->p.max_bin;
     unsigned long long stv[kStWords];
     GBT_TRY(read_status(q, stv));
+    if (q->ms) {
+        GBT_CHECK(!stv[kStInf], "input holds an infinite value");
+        return finalize_merged(q, stv);
+    }
 
     // per-feature key segments
     std::vector<int64_t> seg(m + 1, 0);
@@ -717,6 +840,31 @@ gbt_status gbt_quantize_finalize_cuts(gbt_quantizer *q)
     cleanup();
 
     // cuts: distinct candidates strictly below the maximum
+    std::vector<int32_t> cut_ptr_h(m + 1, 0);
+    std::vector<float> cut_values_h;
+    for (int32_t j = 0; j < m; ++j) {
+        if (N[j] > 0) {
+            GBT_CHECK(lo[j].back() == hi[j].back(), "cut search did not converge");
+            float top = key_float(lo[j].back());
+            for (size_t t = 0; t + 1 < rank[j].size(); ++t) {
+                float v = key_float(lo[j][t]);
+                if (v >= top) continue;
+                if (cut_values_h.size() > (size_t)cut_ptr_h[j] && v == cut_values_h.back()) continue;
+                cut_values_h.push_back(v);
+            }
+        }
+        cut_ptr_h[j + 1] = (int32_t)cut_values_h.size();
+    }
+    return finish_cuts(q, std::move(cut_ptr_h), std::move(cut_values_h), std::move(feat_count), stv);
+}
+
+// The matrix geometry from the cuts (the tail of finalize_cuts for both
+// sketches), the cuts on the device, and the sketch state released.
+static gbt_status finish_cuts(gbt_quantizer *q, std::vector<int32_t> cut_ptr_h, std::vector<float> cut_values_h,
+                              std::vector<int64_t> feat_count, const unsigned long long *stv)
+{
+    gbt_ctx *c = q->ctx;
+    const int32_t m = q->m;
     gbt_matrix *mx = new gbt_matrix();
     q->mat = mx;
     mx->ctx = c;
@@ -726,21 +874,8 @@ gbt_status gbt_quantize_finalize_cuts(gbt_quantizer *q)
     mx->sparse = q->kind == GBT_INPUT_CSR_F32;
     mx->page_home = q->p.page_home;
     mx->page_rows = q->p.page_rows > 0 ? q->p.page_rows : std::max<int64_t>(q->n_total, 1);
-    mx->cut_ptr_h.assign(m + 1, 0);
-    for (int32_t j = 0; j < m; ++j) {
-        if (N[j] > 0) {
-            GBT_CHECK(lo[j].back() == hi[j].back(), "cut search did not converge");
-            float top = key_float(lo[j].back());
-            for (size_t t = 0; t + 1 < rank[j].size(); ++t) {
-                float v = key_float(lo[j][t]);
-                if (v >= top) continue;
-                if (mx->cut_values_h.size() > (size_t)mx->cut_ptr_h[j] && v == mx->cut_values_h.back())
-                    continue;
-                mx->cut_values_h.push_back(v);
-            }
-        }
-        mx->cut_ptr_h[j + 1] = (int32_t)mx->cut_values_h.size();
-    }
+    mx->cut_ptr_h = std::move(cut_ptr_h);
+    mx->cut_values_h = std::move(cut_values_h);
     mx->bin_ptr_h.assign(m + 1, 0);
     int32_t maxb = 1;
     for (int32_t j = 0; j < m; ++j) {
@@ -778,6 +913,14 @@ gbt_status gbt_quantize_finalize_cuts(gbt_quantizer *q)
     q->keys = nullptr;
     q->feats = nullptr;
     q->keys_bytes = q->feats_bytes = 0;
+    dev_free(c, q->bkeys, q->bkeys_bytes);
+    q->bkeys = nullptr;
+    q->bkeys_bytes = 0;
+    if (q->ms) {
+        merge_sketch_free(c, q->ms);
+        delete q->ms;
+        q->ms = nullptr;
+    }
     q->cuts_done = true;
     return GBT_OK;
 }

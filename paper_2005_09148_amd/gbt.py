@@ -57,12 +57,13 @@ class Input(C.Structure):
 
 class QuantParams(C.Structure):
     _fields_ = [("max_bin", C.c_int32), ("page_home", C.c_int32),
-                ("sketch_max_rows", C.c_int64), ("page_rows", C.c_int64), ("page_dir", C.c_char_p)]
+                ("sketch_max_rows", C.c_int64), ("page_rows", C.c_int64), ("page_dir", C.c_char_p),
+                ("sketch_summary", C.c_int32), ("pad0", C.c_int32)]
 
 
-def _quant_params(max_bin, page_home, sketch_max_rows, page_rows, page_dir):
+def _quant_params(max_bin, page_home, sketch_max_rows, page_rows, page_dir, sketch_summary=0):
     return QuantParams(max_bin, page_home, sketch_max_rows, page_rows,
-                       None if page_dir is None else os.fsencode(page_dir))
+                       None if page_dir is None else os.fsencode(page_dir), int(sketch_summary), 0)
 
 
 class MatrixInfo(C.Structure):
@@ -421,16 +422,17 @@ class Matrix:
 
 
 def gbt_quantize(ctx: Context, data, max_bin=256, page_rows=0, page_home=HOME_DEVICE,
-                 sketch_max_rows=0, page_dir=None) -> Matrix:
+                 sketch_max_rows=0, page_dir=None, sketch_summary=0) -> Matrix:
     """Sec. 3.1-3.2: quantile cuts and ELLPACK pages of dense X (numpy host
     array or device tensor) or CSR (a dict kind='csr'); HOME_DISK pages live
-    in files under page_dir."""
+    in files under page_dir; sketch_summary > 0: Alg. 3's merged sketch
+    with summaries of at most that many entries (one batch)."""
     if isinstance(data, dict):
         loc = LOC_HOST if isinstance(data["indptr"], np.ndarray) else LOC_DEVICE
         inp, keep = csr_input(data["indptr"], data["indices"], data["values"], data["m"], loc)
     else:
         inp, keep = dense_input(data)
-    qp = _quant_params(max_bin, page_home, sketch_max_rows, page_rows, page_dir)
+    qp = _quant_params(max_bin, page_home, sketch_max_rows, page_rows, page_dir, sketch_summary)
     h = C.c_void_p()
     _check(_lib.gbt_quantize(ctx.h, C.byref(inp), C.byref(qp), C.byref(h)))
     del keep
@@ -441,9 +443,9 @@ class Quantizer:
     """Incremental quantization (Alg. 3 sketch batches, then Alg. 5 pages)."""
 
     def __init__(self, ctx, n_cols, n_rows_total, max_bin=256, page_rows=0,
-                 page_home=HOME_DEVICE, sketch_max_rows=0, kind=INPUT_DENSE, page_dir=None):
+                 page_home=HOME_DEVICE, sketch_max_rows=0, kind=INPUT_DENSE, page_dir=None, sketch_summary=0):
         self.ctx = ctx
-        qp = _quant_params(max_bin, page_home, sketch_max_rows, page_rows, page_dir)
+        qp = _quant_params(max_bin, page_home, sketch_max_rows, page_rows, page_dir, sketch_summary)
         h = C.c_void_p()
         _check(_lib.gbt_quantize_begin(ctx.h, C.byref(qp), n_cols, n_rows_total, kind,
                                        C.byref(h)))
@@ -451,14 +453,23 @@ class Quantizer:
         ctx._own(self)
 
     def sketch(self, X):
-        inp, keep = dense_input(X)
+        """One batch (Alg. 3): dense X, or CSR as a dict kind='csr'."""
+        if isinstance(X, dict):
+            loc = LOC_HOST if isinstance(X["indptr"], np.ndarray) else LOC_DEVICE
+            inp, keep = csr_input(X["indptr"], X["indices"], X["values"], X["m"], loc)
+        else:
+            inp, keep = dense_input(X)
         _check(_lib.gbt_quantize_sketch_batch(self.h, C.byref(inp)))
 
     def finalize(self):
         _check(_lib.gbt_quantize_finalize_cuts(self.h))
 
     def encode(self, X):
-        inp, keep = dense_input(X)
+        if isinstance(X, dict):
+            loc = LOC_HOST if isinstance(X["indptr"], np.ndarray) else LOC_DEVICE
+            inp, keep = csr_input(X["indptr"], X["indices"], X["values"], X["m"], loc)
+        else:
+            inp, keep = dense_input(X)
         _check(_lib.gbt_quantize_encode_batch(self.h, C.byref(inp)))
 
     def end(self) -> Matrix:
