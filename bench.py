@@ -15,8 +15,9 @@ second of step time (G/s); ms_per_step is seconds per tree x 1000 (the timed
 trees carry no events); roofline is that of the histogram kernel
 (algorithmic bytes / its HIP-event time, the events around every histogram
 launch of as many further timed trees);
-cpu_baseline times the CPU oracle on the first two trees of the same
-workload on the host (single-threaded) and reports the same unit.
+cpu_baseline times the CPU oracle (its OpenMP build, on the threads the
+process is given, and the first tree again in one thread) on the first trees
+of the same workload on the host and reports the same unit.
 """
 from __future__ import annotations
 
@@ -132,7 +133,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--hist-kernel", default="auto", choices=["auto", "plain", "rotated"],
                     help="dense histogram kernel (auto: the library's choice by pass size)")
-    ap.add_argument("--cpu-trees", type=int, default=2)
+    ap.add_argument("--cpu-trees", type=int, default=4)
     ap.add_argument("--sampler", default="mvs", choices=["mvs", "sgb", "goss"],
                     help="the sampler used when f < 1 (Sec. 2.3-2.4)")
     ap.add_argument("--compaction", choices=["auto", "stream", "gather"], default="auto",
@@ -143,6 +144,9 @@ def parse():
                          "pinned host memory")
     ap.add_argument("--naive", action="store_true",
                     help="outofcore: Alg. 6, the naive construction (f = 1, every level streams every page)")
+    ap.add_argument("--sketch-summary", type=int, default=65536,
+                    help="outofcore: entries per feature of the merged quantile sketch (Alg. 3); 0 keeps the "
+                         "whole strided sample on the device for the exact rule")
     ap.add_argument("--goss-a", type=float, default=0.05,
                     help="GOSS top fraction a (the rest fraction is f - a)")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -184,12 +188,27 @@ def oracle_updates(b, res, depth):
     return int((nonnull * levels).sum())
 
 
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(X, y, cfg, n_trees, gpu_trees, gpu_updates, sampler=(0, 0.0)):
-    """Times the oracle on the first n_trees iterations of the same workload.
+    """Times the oracle on the first n_trees iterations of the same workload,
+    in its OpenMP build on every thread OpenMP is given (OMP_NUM_THREADS, else
+    the process's CPUs), and once more the first tree in one thread.
     Updates per tree: counted from the oracle's tree for dense data; for CSR
     data the GPU's count of the same (identical) tree."""
     from oracle import oracle as orc
-    print("[bench] cpu baseline: oracle cuts and bins", file=sys.stderr, flush=True)
+    orc.select("omp")
+    threads = orc.threads()
+    print(f"[bench] cpu baseline: oracle cuts and bins ({threads} threads)", file=sys.stderr, flush=True)
     t0 = time.perf_counter()
     if isinstance(X, dict):
         cuts = orc.sketch_cuts_csr(X["indptr"], X["indices"], X["values"], X["m"], cfg.max_bin)
@@ -201,27 +220,43 @@ def cpu_baseline(X, y, cfg, n_trees, gpu_trees, gpu_updates, sampler=(0, 0.0)):
     P = orc.Params(loss=cfg.loss, max_depth=cfg.max_depth, eta=cfg.eta, lambda_=cfg.lambda_,
                    gamma=cfg.gamma, min_child_weight=cfg.min_child_weight, f=cfg.f,
                    mvs_lambda=cfg.mvs_lambda, seed=cfg.seed, sampler=sampler[0], goss_a=sampler[1])
-    margin = np.full(len(y), cfg.base_margin, np.float32)
-    secs, updates, same = 0.0, 0, True
     if b.sparse:  # the update count comes from the GPU's identical trees
         n_trees = min(n_trees, len(gpu_updates))
-    for t in range(n_trees):
-        t1 = time.perf_counter()
-        res = orc.train_tree(b, y, margin, P, iteration=t, want_detail=True)
-        secs += time.perf_counter() - t1
-        print(f"[bench] oracle tree {t}: {time.perf_counter() - t1:.1f} s", file=sys.stderr, flush=True)
-        if t < len(gpu_trees):
-            same &= res.nodes.tobytes() == gpu_trees[t].tobytes()
-        updates += oracle_updates(b, res, cfg.max_depth) if not b.sparse else gpu_updates[t]
+
+    def run(trees):
+        margin = np.full(len(y), cfg.base_margin, np.float32)
+        secs, updates, out = 0.0, 0, []
+        for t in range(trees):
+            t1 = time.perf_counter()
+            res = orc.train_tree(b, y, margin, P, iteration=t, want_detail=True)
+            secs += time.perf_counter() - t1
+            print(f"[bench] oracle tree {t} ({orc.threads()} threads): {time.perf_counter() - t1:.2f} s",
+                  file=sys.stderr, flush=True)
+            out.append(res.nodes.tobytes())
+            updates += oracle_updates(b, res, cfg.max_depth) if not b.sparse else gpu_updates[t]
+        return secs, updates, out
+
+    secs, updates, trees = run(n_trees)
+    same = all(t == g.tobytes() for t, g in zip(trees, gpu_trees)) if len(gpu_trees) else None
+    orc.threads(1)
+    secs1, updates1, trees1 = run(1)
+    orc.threads(threads)
     return {
         "value": round(updates / secs / 1e9, 4),
         "unit": "G updates/s",
-        "cores": 1,
+        "cores": threads,
         "kind": "oracle",
-        "sample": f"first {n_trees} trees of the same {len(y):,}-row workload (oracle cuts and "
-                  f"bins prepared untimed in {prep:.0f} s); {secs / n_trees:.2f} s/tree",
-        "sec_per_tree": round(secs / n_trees, 3),
-        "trees_identical_to_gpu": bool(same),
+        "sample": f"first {n_trees} trees of the same {len(y):,}-row workload on {threads} OpenMP threads "
+                  f"(oracle cuts and bins prepared untimed in {prep:.0f} s); {secs / n_trees:.3f} s/tree",
+        "sec_per_tree": round(secs / n_trees, 4),
+        "trees_identical_to_gpu": same,
+        "omp_num_threads": os.environ.get("OMP_NUM_THREADS"),
+        "affinity_cpus": len(os.sched_getaffinity(0)),
+        "cpu_model": cpu_model(),
+        "single_thread": {"value": round(updates1 / secs1 / 1e9, 4), "unit": "G updates/s", "cores": 1,
+                          "sample": "first tree of the same workload in one OpenMP thread",
+                          "sec_per_tree": round(secs1, 4),
+                          "tree_identical_to_threaded": trees1[0] == trees[0]},
     }
 
 
@@ -260,8 +295,11 @@ def run_outofcore(args):
     sub = 1 << 21  # rows per host batch handed to the quantizer
     t = time.perf_counter()
     home = gbt.HOME_DISK if args.page_dir else gbt.HOME_PINNED_HOST
+    # Alg. 3: each batch's sample is summarised and merged into running
+    # summaries of sketch_summary entries per feature (0: the whole sample
+    # is kept on the device for the exact rule)
     q = gbt.Quantizer(ctx, 100, n, max_bin=cfg.max_bin, page_rows=page_rows, page_home=home,
-                      page_dir=args.page_dir)
+                      page_dir=args.page_dir, sketch_summary=args.sketch_summary)
     raw, labels = [], []
     for p, rows in enumerate(sizes):
         d = datagen.config4_page(p, rows=rows)
@@ -279,6 +317,8 @@ def run_outofcore(args):
         raw[p] = None
         print(f"[bench] page {p}: encoded ({time.perf_counter() - t:.0f} s)", file=sys.stderr, flush=True)
     mx = q.end()
+    quant_secs = time.perf_counter() - t
+    quant_peak = ctx.memory()[1]
     info = mx.info()
     y = np.concatenate(labels)
     del labels
@@ -340,7 +380,10 @@ def run_outofcore(args):
         "host_link": {"h2d_bytes_per_tree": round(h2d / args.steps), "achieved_gbs": round(h2d / dt / 1e9, 2),
                       "pinned_copy_peak_gbs": round(link_peak, 2),
                       "frac": round(h2d / dt / 1e9 / link_peak, 4)},
-        "device_memory": {"budget_bytes": budget, "peak_bytes": peak},
+        "device_memory": {"budget_bytes": budget, "peak_bytes": peak, "quantize_peak_bytes": quant_peak},
+        "quantize": {"secs": round(quant_secs, 1), "sketch": (f"merged summaries of {args.sketch_summary} "
+                                                              "entries per feature, batches of 2^21 rows")
+                     if args.sketch_summary else "exact rule on the whole strided sample"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
                      "kernel": "+".join(sorted(kernels)), "launches": launches,

@@ -69,6 +69,7 @@ def quantize_batches(gbt, ctx, X, max_bin, S, batch_rows, sketch_max_rows=0, dev
     (30_000, 5, "normal", 0.05, 2, 16, 1_000, 0),      # tiny summaries, many batches
     (25_000, 4, "normal", 0.0, 256, 8192, 25_000, 0),  # one batch, pruned once
     (60_001, 7, "mixed", 0.1, 128, 512, 9_999, 20_000),  # strided sample (every 4th row)
+    (600_000, 3, "normal", 0.0, 256, 65_536, 150_000, 0),  # large summaries, pruned at every merge
 ])
 def test_dense_merged_cuts_match_oracle(gbt, ctx, n, m, kind, missing, max_bin, S, batch_rows, smr):
     X = make_dense(n + m, n, m, kind, missing)
