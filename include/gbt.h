@@ -26,7 +26,8 @@
  *  GBT_E_BUDGET       the context's device byte budget would be exceeded
  *                     (the out-of-memory limit of the paper's Table 1)
  *  GBT_E_DEVICE       a HIP runtime error (message saved)
- *  GBT_E_UNSUPPORTED  a valid request this build does not implement
+ *  GBT_E_UNSUPPORTED  a valid request this build does not implement (for
+ *                     example max_bin above the bins of one histogram group)
  *  GBT_E_IO           a page file could not be created, written or read
  */
 #ifndef GBT_H
@@ -53,7 +54,7 @@ typedef int32_t gbt_status;
 #define GBT_SAMPLE_SGB 1  /* stochastic gradient boosting: uniform rows */
 #define GBT_SAMPLE_GOSS 2 /* gradient-based one-side sampling */
 
-#define GBT_ABI_VERSION 4
+#define GBT_ABI_VERSION 5
 
 enum { GBT_INPUT_DENSE_F32 = 0, GBT_INPUT_CSR_F32 = 1 };
 enum { GBT_LOC_HOST = 0, GBT_LOC_DEVICE = 1 };
@@ -83,7 +84,9 @@ typedef struct {
 } gbt_input;
 
 typedef struct {
-    int32_t max_bin;          /* Sec. 2.2: bins per feature, default 256 */
+    int32_t max_bin;          /* Sec. 2.2: bins per feature, default 256; at most 2560
+                                 for dense input and 10176 for CSR input (the bins one
+                                 histogram group holds), else GBT_E_UNSUPPORTED */
     int32_t page_home;        /* GBT_HOME_DEVICE | GBT_HOME_PINNED_HOST | GBT_HOME_DISK */
     int64_t sketch_max_rows;  /* 0 = 2^24: above it, every ceil(n/this)-th row is sketched */
     int64_t page_rows;        /* rows per ELLPACK page; 0 = one page */
@@ -154,6 +157,9 @@ typedef struct {
     int32_t split_bin;     /* left iff bin < split_bin */
     int32_t default_left;  /* missing values go left */
     int32_t valid;
+    float threshold;       /* raw-value form: left iff x <= threshold, the cut
+                              value below bin split_bin (0 when not valid) */
+    int32_t pad0;
 } gbt_split;
 
 /* One node of a heap-ordered tree: the children of node i are 2i+1, 2i+2. */
@@ -401,35 +407,59 @@ gbt_status gbt_build_hist_noalloc(gbt_ctx *ctx, const gbt_matrix *layout, const 
                                   int32_t n_sub, const int64_t *parent_hist_d, int64_t *hist_d);
 
 /* ---- Alg. 1 EvaluateSplit with Eq. 8 ---------------------------------------
- * For node k: histogram hist_d[node_slot_h[k]], node sum node_sum_d[2k..2k+1].
+ * For node k: histogram hist_d[node_slot_d[k]], node sum node_sum_d[2k..2k+1]
+ * (every array on the device; node_slot_d[k] must name a slot of hist_d).
  * Every feature with >= 2 bins, every s in 1..B_j-1, missing right then
  * left: Q_L = sum_{b<s} H (+ missing sums), Q_R = node - Q_L; valid when
  * H_L, H_R >= min_child_weight; gain = 0.5((G_L^2/(H_L+l) + G_R^2/(H_R+l))
  * - G^2/(H+l)) - gamma in double; the best is the highest gain, ties to the
- * lower feature, lower s, missing right.  out_d[k] receives it. */
+ * lower feature, lower s, missing right.  out_d[k] receives it, with the
+ * split's threshold from the cuts of `layout`.  Enqueued on the context
+ * stream without waiting for it (no host round trip): out_d is ready in
+ * stream order. */
 gbt_status gbt_eval_splits(gbt_ctx *ctx, const gbt_matrix *layout, const int64_t *hist_d,
-                           const int64_t *node_sum_d, const int32_t *node_slot_h, int32_t n_nodes,
+                           const int64_t *node_sum_d, const int32_t *node_slot_d, int32_t n_nodes,
                            const gbt_train_params *tp, int32_t exp_g, int32_t exp_h,
                            gbt_split *out_d);
 
 /* ---- Alg. 1 RepartitionInstances -------------------------------------------
- * For node k with segment seg_h[k] of rows_d and split split_h[k] (valid):
- * stable partition into [left | right] where a row goes left iff its bin
- * for the split feature is < split_bin, or it is missing and default_left.
- * position_d[row] receives child_h[2k] or child_h[2k+1].  seg_out_h[2k],
- * seg_out_h[2k+1] receive the child segments (host, after a sync).
- * rows_tmp_d is scratch of the same length as rows_d (n_rows). */
+ * For node k with segment seg_d[k] of rows_d (segments disjoint) and split
+ * split_d[k]: when valid, a stable partition of the segment into
+ * [left | right] where a row goes left iff its bin for the split feature is
+ * < split_bin, or it is missing and default_left, and position_d[row]
+ * receives child_d[2k] or child_d[2k+1]; a node that does not split keeps
+ * its rows in place.  seg_out_d[2k], seg_out_d[2k+1] receive the child
+ * segments {child_d[2k], begin, begin + n_left}, {child_d[2k+1],
+ * begin + n_left, end} (the whole segment left when the node does not
+ * split).  Every array is on the device (rows_d, rows_tmp_d n_rows entries,
+ * 16-byte aligned; rows_d values are rows of page_d; position_d indexed by
+ * those rows); rows_tmp_d is scratch.  Enqueued on the context stream
+ * without waiting for it: results are ready in stream order.  Malformed
+ * entries cannot be reported before the work runs: a segment outside
+ * [0, n_rows] is clamped into it, a split feature outside [0, m) does not
+ * split, and when status_d (device, may be NULL) is given *status_d
+ * receives the number of such nodes plus the number of rows that two
+ * segments claim (then the order of those segments' rows is unspecified). */
 gbt_status gbt_partition(gbt_ctx *ctx, const gbt_matrix *layout, const uint32_t *page_d,
-                         const gbt_split *split_h, const gbt_seg *seg_h, const int32_t *child_h,
+                         const gbt_split *split_d, const gbt_seg *seg_d, const int32_t *child_d,
                          int32_t n_nodes, int32_t *rows_d, int32_t *rows_tmp_d, int64_t n_rows,
-                         int32_t *position_d, gbt_seg *seg_out_h);
+                         int32_t *position_d, gbt_seg *seg_out_d, int32_t *status_d);
 
 /* ---- Eq. 6 leaves and the Eq. 1 margin update -------------------------------
  * Leaves of `tree` (flags LEAF) get leaf_value = (float)((-G/(H+lambda))*eta)
  * from their fixed-point sums; then margin_d[i] += leaf(tree, row i) for the
- * n rows of `data`, by traversal of each row's binned symbols. */
+ * n rows of `data`.  The training rows whose leaf is known take it from
+ * their positions: entry i < n_pos names row rows_d[i] of `data` (i when
+ * rows_d is NULL; distinct rows, as gbt_sampled_info's rows_d) and its node
+ * position_d[i] (as gbt_partition leaves it after the last level); the
+ * other rows are traversed by their binned symbols.  Entries whose position
+ * is not a leaf of the tree, or whose row is out of range or repeated, are
+ * counted and their rows traversed instead: the margins are right, and the
+ * call returns GBT_E_INVALID with the count.  Synchronizes the context
+ * stream (the tree's leaf values are written back to `tree`). */
 gbt_status gbt_update_leaves(gbt_ctx *ctx, gbt_tree *tree, const gbt_train_params *tp,
-                             const gbt_matrix *data, float *margin_d);
+                             const gbt_matrix *data, const int32_t *rows_d, const int32_t *position_d,
+                             int64_t n_pos, float *margin_d);
 
 /* ---- one boosting iteration: Alg. 7 then Alg. 1 -----------------------------
  * Gradients, sampling (f < 1) with compaction into one device page, the

@@ -38,6 +38,20 @@ constexpr int kSparseMinGroups = 16;
 // four workgroups fit a CU's LDS.
 constexpr int kDenseBins = 2560;
 
+int32_t hist_feature_bin_limit(bool sparse) { return sparse ? kLdsBins : kDenseBins; }
+
+gbt_status hist_check_feature_bins(const gbt_matrix *mx)
+{
+    const int32_t lim = hist_feature_bin_limit(mx->sparse != 0);
+    for (int32_t f = 0; f < mx->m; ++f) {
+        const int32_t b = mx->bin_ptr_h[f + 1] - mx->bin_ptr_h[f];
+        if (b > lim)
+            return set_error(GBT_E_UNSUPPORTED, "feature %d has %d bins (at most %d in a %s page)", f, b, lim,
+                             mx->sparse ? "sparse" : "dense");
+    }
+    return GBT_OK;
+}
+
 // A dense group's bits lie within this many words from its first word (one
 // 16-byte load), and it holds at most this many features.
 constexpr int kGroupWords = 4;

@@ -99,6 +99,12 @@ inline int32_t slot_table_row_stride(int32_t G) { return (G + 1 + 3) / 4 * 4; }
 gbt_status sparse_slot_table(gbt_ctx *c, const gbt_matrix *mx, const HistGroup *groups_d, int32_t G,
                              const uint32_t *page, int64_t n, uint8_t *row_tbl, uint16_t *col_tbl);
 
+// Most bins one feature may have for the histogram kernels of a dense or a
+// sparse page (one histogram group in LDS).
+int32_t hist_feature_bin_limit(bool sparse);
+// GBT_E_UNSUPPORTED unless every feature of mx fits that limit.
+gbt_status hist_check_feature_bins(const gbt_matrix *mx);
+
 gbt_status hist_launch_device(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int64_t *q,
                               const int32_t *rows, const HistLaunch &hl, const int64_t *parent_hist,
                               int64_t *hist, unsigned long long *n_updates);

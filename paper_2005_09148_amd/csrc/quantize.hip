@@ -13,6 +13,7 @@
 // Pages: row-major rows of row_words 32-bit words; a row is the LSB-first
 // bit stream of its stride symbols (w bits each), zero padded.
 #include "common.h"
+#include "hist_impl.h"
 #include "sketch_impl.h"
 
 #include <algorithm>
@@ -465,6 +466,13 @@ gbt_status gbt_quantize_begin(gbt_ctx *c, const gbt_quant_params *p, int32_t n_c
     GBT_CHECK(n_rows_total >= 0, "n_rows must be >= 0");
     GBT_CHECK(input_kind == GBT_INPUT_DENSE_F32 || input_kind == GBT_INPUT_CSR_F32,
               "unknown input kind %d", input_kind);
+    {
+        // a feature takes up to max_bin bins: they must fit a histogram group
+        const int32_t lim = hist_feature_bin_limit(input_kind == GBT_INPUT_CSR_F32);
+        if (p->max_bin > lim)
+            return set_error(GBT_E_UNSUPPORTED, "max_bin %d: the histograms of a %s page hold at most %d bins "
+                             "per feature", p->max_bin, input_kind == GBT_INPUT_CSR_F32 ? "sparse" : "dense", lim);
+    }
     GBT_CHECK(p->page_home == GBT_HOME_DEVICE || p->page_home == GBT_HOME_PINNED_HOST ||
                   p->page_home == GBT_HOME_DISK,
               "unknown page_home %d", p->page_home);

@@ -40,6 +40,13 @@ __device__ inline bool better(const Cand &a, const Cand &b)
 
 __device__ inline double fx(long long Q, int32_t e) { return ldexp((double)Q, -e); }
 
+// The split's raw-value form: bins < split_bin hold the values <= the cut
+// below bin split_bin.
+__device__ inline float split_threshold(const SplitCuts &c, int32_t feature, int32_t split_bin)
+{
+    return c.values[c.ptr[feature] + split_bin - 1];
+}
+
 __device__ inline double eq8_gain(double GL, double HL, double GR, double HR, double G, double H,
                                   double lambda, double gamma)
 {
@@ -194,7 +201,7 @@ __device__ Cand eval_feature(const longlong2 *__restrict__ hj, int32_t B, long l
 // `decide` given, a node whose best valid gain is > 0 is also marked as
 // split in the tree driver's node table (depth < max_depth is the caller's).
 __device__ inline void reduce_node(const EvalCand *cand, int32_t n_fblocks, const EvalNode &node, int32_t k,
-                                   gbt_split *__restrict__ out, DevNode *__restrict__ decide)
+                                   gbt_split *__restrict__ out, DevNode *__restrict__ decide, SplitCuts cuts)
 {
     EvalCand b;
     b.valid = 0;
@@ -213,6 +220,8 @@ __device__ inline void reduce_node(const EvalCand *cand, int32_t n_fblocks, cons
     s.left_h = b.valid ? b.lh : 0;
     s.right_g = b.valid ? node.sum_g - b.lg : 0;
     s.right_h = b.valid ? node.sum_h - b.lh : 0;
+    s.threshold = b.valid ? split_threshold(cuts, b.feature, b.split_bin) : 0.0f;
+    s.pad0 = 0;
     out[k] = s;
     if (decide && s.valid && s.gain > 0.0) {
         DevNode &d = decide[node.heap];
@@ -231,11 +240,11 @@ __device__ inline void reduce_node(const EvalCand *cand, int32_t n_fblocks, cons
 __global__ void k_eval_reduce(const EvalCand *__restrict__ cand, int32_t n_fblocks,
                               const EvalNode *__restrict__ nodes, int32_t n_nodes,
                               const int32_t *__restrict__ n_nodes_d, gbt_split *__restrict__ out,
-                              DevNode *__restrict__ decide)
+                              DevNode *__restrict__ decide, SplitCuts cuts)
 {
     int32_t k = blockIdx.x * blockDim.x + threadIdx.x;
     if (k >= n_nodes || (n_nodes_d && k >= *n_nodes_d)) return;
-    reduce_node(cand, n_fblocks, nodes[k], k, out, decide);
+    reduce_node(cand, n_fblocks, nodes[k], k, out, decide, cuts);
 }
 
 __global__ void __launch_bounds__(kEvalThreads)
@@ -555,7 +564,7 @@ __global__ void __launch_bounds__(256)
 __global__ void __launch_bounds__(256)
     k_eval_reduce_wave(const EvalCand *__restrict__ cand, int32_t n_fblocks, const EvalNode *__restrict__ nodes,
                        int32_t n_nodes, const int32_t *__restrict__ n_nodes_d, gbt_split *__restrict__ out,
-                       DevNode *__restrict__ decide)
+                       DevNode *__restrict__ decide, SplitCuts cuts)
 {
     const int lane = threadIdx.x & 63;
     const int32_t k = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -588,6 +597,8 @@ __global__ void __launch_bounds__(256)
     sp.left_h = b.valid ? b.lh : 0;
     sp.right_g = b.valid ? node.sum_g - b.lg : 0;
     sp.right_h = b.valid ? node.sum_h - b.lh : 0;
+    sp.threshold = b.valid ? split_threshold(cuts, b.feature, b.split_bin) : 0.0f;
+    sp.pad0 = 0;
     out[k] = sp;
     if (decide && sp.valid && sp.gain > 0.0) {
         DevNode &d = decide[node.heap];
@@ -645,12 +656,13 @@ gbt_status reduce_eval_impl(gbt_ctx *c, const gbt_matrix *mx, const int64_t *par
     return GBT_OK;
 }
 
-gbt_status eval_reduce_impl(gbt_ctx *c, const EvalCand *cand, int32_t n_fblocks, const EvalNode *nodes_d,
-                            int32_t n_nodes, const int32_t *n_nodes_d, gbt_split *out_d, DevNode *decide)
+gbt_status eval_reduce_impl(gbt_ctx *c, const gbt_matrix *mx, const EvalCand *cand, int32_t n_fblocks,
+                            const EvalNode *nodes_d, int32_t n_nodes, const int32_t *n_nodes_d, gbt_split *out_d,
+                            DevNode *decide)
 {
     if (n_nodes <= 0) return GBT_OK;
     k_eval_reduce_wave<<<(n_nodes + 3) / 4, 256, 0, c->stream>>>(cand, n_fblocks, nodes_d, n_nodes, n_nodes_d,
-                                                                 out_d, decide);
+                                                                 out_d, decide, cuts_of(mx));
     GBT_LAUNCHED();
     return GBT_OK;
 }
@@ -668,7 +680,7 @@ gbt_status eval_impl(gbt_ctx *c, const gbt_matrix *mx, const int64_t *hist, cons
                                                  mx->bin_ptr_d, mx->m, ep, cand);
     GBT_LAUNCHED();
     k_eval_reduce<<<(n_nodes + 127) / 128, 128, 0, c->stream>>>(cand, nfb, nodes_d, n_nodes, n_nodes_d, out_d,
-                                                                decide);
+                                                                decide, cuts_of(mx));
     GBT_LAUNCHED();
     return GBT_OK;
 }
@@ -1269,6 +1281,113 @@ gbt_status partition_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page
     return GBT_OK;
 }
 
+// ------------------------------------------------------------ public calls
+// Work tables of gbt_eval_splits and gbt_partition built on the device from
+// the caller's device arrays.
+
+constexpr unsigned kSegBlocks = 64;  // blocks per node segment in k_slot_of_segments
+
+__global__ void k_zero_i32(int32_t *__restrict__ p, int32_t n)
+{
+    if ((int32_t)threadIdx.x < n) p[threadIdx.x] = 0;
+}
+
+__global__ void k_copy_i32(const int32_t *__restrict__ src, int32_t *__restrict__ dst, int32_t n)
+{
+    if ((int32_t)threadIdx.x < n) dst[threadIdx.x] = src[threadIdx.x];
+}
+
+__global__ void k_fill_i32(int32_t *__restrict__ p, int64_t n, int32_t v)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+__global__ void k_eval_nodes(const int64_t *__restrict__ sums, const int32_t *__restrict__ slots, int32_t n,
+                             EvalNode *__restrict__ out)
+{
+    const int32_t k = (int32_t)(blockIdx.x * blockDim.x + threadIdx.x);
+    if (k >= n) return;
+    EvalNode e;
+    e.sum_g = sums[2 * (int64_t)k];
+    e.sum_h = sums[2 * (int64_t)k + 1];
+    e.slot = slots[k];
+    e.heap = k;
+    out[k] = e;
+}
+
+// Node k of the partition from split[k], seg[k] and child[2k], child[2k+1].
+// A segment outside [0, n_rows] is clamped into it and a split feature
+// outside [0, m) does not split: either adds one to *bad.
+__global__ void k_part_nodes(const gbt_split *__restrict__ split, const gbt_seg *__restrict__ seg,
+                             const int32_t *__restrict__ child, int32_t n_nodes, int64_t n_rows, int32_t m,
+                             DevNode *__restrict__ nodes, int32_t *__restrict__ bad)
+{
+    const int32_t k = (int32_t)(blockIdx.x * blockDim.x + threadIdx.x);
+    if (k >= n_nodes) return;
+    const gbt_seg sg = seg[k];
+    const gbt_split sp = split[k];
+    bool ok = true;
+    int64_t b = sg.begin, e = sg.end;
+    if (b < 0 || b > e || e > n_rows) {
+        ok = false;
+        b = b < 0 ? 0 : (b > n_rows ? n_rows : b);
+        e = e < b ? b : (e > n_rows ? n_rows : e);
+    }
+    bool splits = sp.valid != 0;
+    if (splits && (sp.feature < 0 || sp.feature >= m)) {
+        ok = false;
+        splits = false;
+    }
+    DevNode d = {};
+    d.begin = b;
+    d.end = e;
+    d.present = 1;
+    d.split = splits ? 1 : 0;
+    d.feature = splits ? sp.feature : 0;
+    d.split_bin = splits ? sp.split_bin : 0;
+    d.default_left = splits ? sp.default_left : 0;
+    d.left_child = child[2 * (int64_t)k];
+    d.right_child = child[2 * (int64_t)k + 1];
+    nodes[k] = d;
+    if (!ok) atomicAdd(bad, 1);
+}
+
+// slot_node[i] = k for every slot i of node k's segment (blockIdx.x = k,
+// gridDim.y blocks stride over it); a slot that two segments claim adds one
+// to *bad.
+__global__ void k_slot_of_segments(const DevNode *__restrict__ nodes, int32_t *__restrict__ slot_node,
+                                   int32_t *__restrict__ bad)
+{
+    const int32_t k = (int32_t)blockIdx.x;
+    const int64_t b = nodes[k].begin, e = nodes[k].end;
+    const int64_t step = (int64_t)gridDim.y * blockDim.x;
+    for (int64_t i = b + (int64_t)blockIdx.y * blockDim.x + threadIdx.x; i < e; i += step)
+        if (atomicExch(&slot_node[i], k) != -1) atomicAdd(bad, 1);
+}
+
+// The child segments of node k: [begin, begin + nleft) and [begin + nleft,
+// end) of a splitting node; the whole segment left of one that does not split.
+__global__ void k_child_segments(const DevNode *__restrict__ nodes, int32_t n_nodes, int64_t n_rows,
+                                 gbt_seg *__restrict__ out)
+{
+    const int32_t k = (int32_t)(blockIdx.x * blockDim.x + threadIdx.x);
+    if (k >= n_nodes) return;
+    const DevNode &d = nodes[k];
+    const int64_t nl = (d.split && n_rows) ? d.nleft : d.end - d.begin;
+    gbt_seg l, r;
+    l.node_slot = d.left_child;
+    l.pad0 = 0;
+    l.begin = d.begin;
+    l.end = d.begin + nl;
+    r.node_slot = d.right_child;
+    r.pad0 = 0;
+    r.begin = d.begin + nl;
+    r.end = d.end;
+    out[2 * (int64_t)k] = l;
+    out[2 * (int64_t)k + 1] = r;
+}
+
 }  // namespace gbt
 
 using namespace gbt;
@@ -1276,104 +1395,69 @@ using namespace gbt;
 extern "C" {
 
 gbt_status gbt_eval_splits(gbt_ctx *c, const gbt_matrix *layout, const int64_t *hist_d,
-                           const int64_t *node_sum_d, const int32_t *node_slot_h, int32_t n_nodes,
+                           const int64_t *node_sum_d, const int32_t *node_slot_d, int32_t n_nodes,
                            const gbt_train_params *tp, int32_t exp_g, int32_t exp_h, gbt_split *out_d)
 {
     GBT_CHECK(c && layout && tp && out_d, "gbt_eval_splits: NULL argument");
     GBT_CHECK(n_nodes >= 0, "negative node count");
     if (n_nodes == 0) return GBT_OK;
-    GBT_CHECK(hist_d && node_sum_d && node_slot_h, "gbt_eval_splits: NULL input");
+    GBT_CHECK(hist_d && node_sum_d && node_slot_d, "gbt_eval_splits: NULL input");
     GBT_TRY(set_device(c));
-    std::vector<int64_t> sums(2 * (size_t)n_nodes);
-    GBT_HIP(hipMemcpyAsync(sums.data(), node_sum_d, sums.size() * 8, hipMemcpyDeviceToHost, c->stream));
-    GBT_HIP(hipStreamSynchronize(c->stream));
-    std::vector<EvalNode> nodes(n_nodes);
-    for (int32_t k = 0; k < n_nodes; ++k) {
-        nodes[k].sum_g = sums[2 * k];
-        nodes[k].sum_h = sums[2 * k + 1];
-        nodes[k].slot = node_slot_h[k];
-        nodes[k].heap = k;
-    }
     EvalNode *nodes_d;
     GBT_TRY(scratch_t(c, kScrEvalNodes, (size_t)n_nodes, &nodes_d));
-    GBT_HIP(hipMemcpyAsync(nodes_d, nodes.data(), nodes.size() * sizeof(EvalNode), hipMemcpyHostToDevice,
-                           c->stream));
+    k_eval_nodes<<<(unsigned)((n_nodes + 255) / 256), 256, 0, c->stream>>>(node_sum_d, node_slot_d, n_nodes,
+                                                                          nodes_d);
+    GBT_LAUNCHED();
     EvalParams ep{tp->lambda, tp->gamma, tp->min_child_weight, exp_g, exp_h, nullptr};
-    GBT_TRY(eval_impl(c, layout, hist_d, nodes_d, n_nodes, ep, out_d));
-    GBT_HIP(hipStreamSynchronize(c->stream));
-    return GBT_OK;
-}
-
-__global__ void k_fill_slot_node(const gbt_seg *__restrict__ segs, int32_t n_nodes,
-                                 int32_t *__restrict__ slot_node, int64_t n)
-{
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n) return;
-    int32_t k = -1;
-    for (int32_t t = 0; t < n_nodes; ++t)
-        if (i >= segs[t].begin && i < segs[t].end) k = t;
-    slot_node[i] = k;
+    return eval_impl(c, layout, hist_d, nodes_d, n_nodes, ep, out_d);
 }
 
 gbt_status gbt_partition(gbt_ctx *c, const gbt_matrix *layout, const uint32_t *page_d,
-                         const gbt_split *split_h, const gbt_seg *seg_h, const int32_t *child_h,
+                         const gbt_split *split_d, const gbt_seg *seg_d, const int32_t *child_d,
                          int32_t n_nodes, int32_t *rows_d, int32_t *rows_tmp_d, int64_t n_rows,
-                         int32_t *position_d, gbt_seg *seg_out_h)
+                         int32_t *position_d, gbt_seg *seg_out_d, int32_t *status_d)
 {
-    GBT_CHECK(c && layout && page_d && split_h && seg_h && child_h && rows_d && rows_tmp_d && position_d,
-              "gbt_partition: NULL argument");
+    GBT_CHECK(c && layout && page_d && rows_d && rows_tmp_d && position_d, "gbt_partition: NULL argument");
     GBT_CHECK(n_nodes >= 0 && n_rows >= 0, "negative sizes");
+    GBT_CHECK(n_nodes == 0 || (split_d && seg_d && child_d && seg_out_d), "gbt_partition: NULL node arrays");
+    GBT_CHECK(n_rows < ((int64_t)1 << 31) - 1, "partition of %lld rows (limit 2^31-2)", (long long)n_rows);
     GBT_CHECK(((uintptr_t)rows_d & 15) == 0 && ((uintptr_t)rows_tmp_d & 15) == 0,
               "gbt_partition: rows_d and rows_tmp_d must be 16-byte aligned");
-    for (int32_t k = 0; k < n_nodes; ++k) {
-        GBT_CHECK(seg_h[k].begin >= 0 && seg_h[k].begin <= seg_h[k].end && seg_h[k].end <= n_rows,
-                  "segment %d outside [0, n_rows]", k);
-        if (split_h[k].valid)
-            GBT_CHECK(split_h[k].feature >= 0 && split_h[k].feature < layout->m, "split feature %d", k);
-    }
     GBT_TRY(set_device(c));
-    std::vector<DevNode> nodes(std::max(n_nodes, 1));
-    for (int32_t k = 0; k < n_nodes; ++k) {
-        DevNode &d = nodes[k];
-        memset(&d, 0, sizeof(d));
-        d.begin = seg_h[k].begin;
-        d.end = seg_h[k].end;
-        d.present = 1;
-        d.split = split_h[k].valid ? 1 : 0;
-        d.feature = split_h[k].feature;
-        d.split_bin = split_h[k].split_bin;
-        d.default_left = split_h[k].default_left;
-        d.left_child = child_h[2 * k];
-        d.right_child = child_h[2 * k + 1];
-    }
     DevNode *nodes_d;
-    gbt_seg *segs_d;
-    int32_t *slot_node;
-    GBT_TRY(scratch_t(c, kScrNodes, nodes.size(), &nodes_d));
-    GBT_TRY(scratch_t(c, kScrEvalNodes, (size_t)std::max(n_nodes, 1), &segs_d));
+    int32_t *slot_node, *bad;
+    GBT_TRY(scratch_t(c, kScrNodes, (size_t)std::max(n_nodes, 1), &nodes_d));
     GBT_TRY(scratch_t(c, kScrSlotNode, (size_t)std::max<int64_t>(n_rows, 1), &slot_node));
-    GBT_HIP(hipMemcpyAsync(nodes_d, nodes.data(), nodes.size() * sizeof(DevNode), hipMemcpyHostToDevice, c->stream));
-    if (n_nodes)
-        GBT_HIP(hipMemcpyAsync(segs_d, seg_h, n_nodes * sizeof(gbt_seg), hipMemcpyHostToDevice, c->stream));
-    if (n_rows) {
-        k_fill_slot_node<<<(unsigned)((n_rows + 255) / 256), 256, 0, c->stream>>>(segs_d, n_nodes, slot_node, n_rows);
+    GBT_TRY(scratch_t(c, kScrEvalNodes, 4, &bad));
+    k_zero_i32<<<1, 64, 0, c->stream>>>(bad, 1);
+    GBT_LAUNCHED();
+    if (n_nodes) {
+        k_part_nodes<<<(unsigned)((n_nodes + 255) / 256), 256, 0, c->stream>>>(split_d, seg_d, child_d, n_nodes,
+                                                                               n_rows, layout->m, nodes_d, bad);
         GBT_LAUNCHED();
+    }
+    if (n_rows) {
+        k_fill_i32<<<(unsigned)((n_rows + 255) / 256), 256, 0, c->stream>>>(slot_node, n_rows, -1);
+        GBT_LAUNCHED();
+        if (n_nodes) {
+            // each node's (clamped) segment, strided over by up to kSegBlocks blocks
+            const unsigned per = (unsigned)std::max<int64_t>(1, std::min<int64_t>(kSegBlocks, 65536 / n_nodes));
+            k_slot_of_segments<<<dim3((unsigned)n_nodes, per), 256, 0, c->stream>>>(nodes_d, slot_node, bad);
+            GBT_LAUNCHED();
+        }
     }
     GBT_TRY(partition_impl(c, layout, page_d, rows_d, n_rows, position_d, slot_node, nullptr, nodes_d, nullptr,
                            nullptr, n_nodes, rows_tmp_d));
     if (n_rows)
         GBT_HIP(hipMemcpyAsync(rows_d, rows_tmp_d, (size_t)n_rows * 4, hipMemcpyDeviceToDevice, c->stream));
-    if (n_rows && n_nodes)
-        GBT_HIP(hipMemcpyAsync(nodes.data(), nodes_d, (size_t)n_nodes * sizeof(DevNode), hipMemcpyDeviceToHost,
-                               c->stream));
-    GBT_HIP(hipStreamSynchronize(c->stream));
-    if (seg_out_h) {
-        for (int32_t k = 0; k < n_nodes; ++k) {
-            int64_t b = seg_h[k].begin, e = seg_h[k].end;
-            int64_t nl = (split_h[k].valid && n_rows) ? nodes[k].nleft : e - b;
-            seg_out_h[2 * k] = {child_h[2 * k], 0, b, b + nl};
-            seg_out_h[2 * k + 1] = {child_h[2 * k + 1], 0, b + nl, e};
-        }
+    if (n_nodes) {
+        k_child_segments<<<(unsigned)((n_nodes + 255) / 256), 256, 0, c->stream>>>(nodes_d, n_nodes, n_rows,
+                                                                                   seg_out_d);
+        GBT_LAUNCHED();
+    }
+    if (status_d) {
+        k_copy_i32<<<1, 64, 0, c->stream>>>(bad, status_d, 1);
+        GBT_LAUNCHED();
     }
     return GBT_OK;
 }

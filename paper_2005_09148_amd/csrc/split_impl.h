@@ -16,6 +16,13 @@ struct EvalParams {
     const int32_t *e_dev;  // when set, {e_g, e_h} are read from device memory
 };
 
+// The matrix's cuts on the device, for the raw-value thresholds of splits.
+struct SplitCuts {
+    const float *values;
+    const int32_t *ptr;
+};
+inline SplitCuts cuts_of(const gbt_matrix *mx) { return SplitCuts{mx->cut_values_d, mx->cut_ptr_d}; }
+
 struct EvalNode {
     long long sum_g, sum_h;
     int32_t slot;   // histogram slot
@@ -48,8 +55,9 @@ gbt_status reduce_eval_impl(gbt_ctx *c, const gbt_matrix *mx, const int64_t *par
                             const EvalNode *ev, const EvalParams &ep, EvalCand *cand);
 // Each listed node's best split from cand (n_fblocks entries per node);
 // count *n_nodes_d (at most n_nodes); decide as in eval_impl.
-gbt_status eval_reduce_impl(gbt_ctx *c, const EvalCand *cand, int32_t n_fblocks, const EvalNode *nodes_d,
-                            int32_t n_nodes, const int32_t *n_nodes_d, gbt_split *out_d, DevNode *decide);
+gbt_status eval_reduce_impl(gbt_ctx *c, const gbt_matrix *mx, const EvalCand *cand, int32_t n_fblocks,
+                            const EvalNode *nodes_d, int32_t n_nodes, const int32_t *n_nodes_d, gbt_split *out_d,
+                            DevNode *decide);
 
 // Stable partition of rows[0, n) by each slot's node (slot_node[i], or
 // position[rows[i]] when slot_node is NULL): the rows of every splitting

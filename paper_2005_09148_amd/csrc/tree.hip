@@ -943,16 +943,55 @@ __global__ void k_leaf_values(gbt_node *__restrict__ t, int32_t n, int32_t eg, i
         t[i].leaf_value = leaf_of(t[i].sum_g, t[i].sum_h, eg, eh, lambda, eta);
 }
 
+// Rows whose leaf is known (bit r of done, global row row0 + i): skipped.
 template <bool kStage>
 __global__ void __launch_bounds__(kWalkThreads)
     k_margin_add_tree(const uint32_t *__restrict__ words, int64_t rows, Geo geo,
-                      const gbt_node *__restrict__ t, int64_t nn, float *__restrict__ margin)
+                      const gbt_node *__restrict__ t, int64_t nn, float *__restrict__ margin,
+                      const uint32_t *__restrict__ done, int64_t row0)
 {
     extern __shared__ uint32_t walk_lds[];
     const uint32_t *row = stage_row<kStage>(words, rows, geo.row_words, walk_lds);
     int64_t i = (int64_t)blockIdx.x * kWalkThreads + threadIdx.x;
     if (i >= rows) return;
+    if (done) {
+        const int64_t g = row0 + i;
+        if ((done[g >> 5] >> (g & 31)) & 1u) return;
+    }
     margin[i] = margin[i] + t[walk_binned(t, nn, row, geo)].leaf_value;
+}
+
+__global__ void k_fill_u32(uint32_t *__restrict__ p, int64_t n, uint32_t v)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+// Training rows whose node is known: entry i is row r = rows[i] (i when rows
+// is NULL) in node pos[i].  When r is a row of the data, pos[i] a leaf of
+// the tree and no earlier claim holds r, margin[r] receives the leaf and r
+// is marked done; otherwise *bad counts the entry and r (if it is a row)
+// is left to the traversal.
+__global__ void k_margin_add_positions(const int32_t *__restrict__ rows, const int32_t *__restrict__ pos,
+                                       int64_t n_pos, int64_t n_rows, const gbt_node *__restrict__ t, int32_t nn,
+                                       float *__restrict__ margin, uint32_t *__restrict__ done,
+                                       unsigned long long *__restrict__ bad)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n_pos) return;
+    const int64_t r = rows ? rows[i] : i;
+    const int32_t k = pos[i];
+    const bool leaf = k >= 0 && k < nn && (t[k].flags & GBT_NODE_PRESENT) && (t[k].flags & GBT_NODE_LEAF);
+    if (r < 0 || r >= n_rows || !leaf) {
+        atomicAdd(bad, 1ull);
+        return;
+    }
+    const uint32_t bit = 1u << (r & 31);
+    if (atomicOr(&done[r >> 5], bit) & bit) {
+        atomicAdd(bad, 1ull);  // the row appears twice
+        return;
+    }
+    margin[r] = margin[r] + t[k].leaf_value;
 }
 
 static size_t walk_lds_bytes(const Geo &g) { return (size_t)kWalkThreads * (g.row_words + 1) * 4; }
@@ -1135,7 +1174,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         if (fused) {
             mark = timer_begin(c, kPhHistAux);
             GBT_TRY(reduce_eval_impl(c, mx, partials, red_d, nullptr, 1, nullptr, histA, evA, ep, cand));
-            if (!choose) GBT_TRY(eval_reduce_impl(c, cand, mx->m, evA, 1, cntA, splits_d, nodes));
+            if (!choose) GBT_TRY(eval_reduce_impl(c, mx, cand, mx->m, evA, 1, cntA, splits_d, nodes));
             timer_end(c, mark);
         }
     }
@@ -1167,7 +1206,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
                 // the deepest evaluated level's histograms are nobody's parents
                 GBT_TRY(reduce_eval_impl(c, mx, partials, red_d, cnt + 3, maxn, histA, d + 2 < D ? histB : nullptr,
                                          evB, ep, cand));
-                if (!choose) GBT_TRY(eval_reduce_impl(c, cand, mx->m, evB, nxt, cntB, splits_d, nodes));
+                if (!choose) GBT_TRY(eval_reduce_impl(c, mx, cand, mx->m, evB, nxt, cntB, splits_d, nodes));
                 timer_end(c, mark);
             }
             std::swap(histA, histB);
@@ -1718,6 +1757,7 @@ gbt_status gbt_train_tree_naive(gbt_ctx *c, const gbt_matrix *data, const float 
 {
     GBT_CHECK(c && data && p && tree && tree->nodes, "gbt_train_tree_naive: NULL argument");
     GBT_CHECK(data->n_rows == 0 || (label_d && margin_d), "gbt_train_tree_naive: NULL labels/margins");
+    GBT_TRY(hist_check_feature_bins(data));
     GBT_CHECK(p->max_depth >= 0 && p->max_depth <= kNaiveMaxDepth, "max_depth %d outside [0, %d]", p->max_depth,
               kNaiveMaxDepth);
     GBT_CHECK(p->f == 1.0, "the naive construction trains every row (f = 1, got %g)", p->f);
@@ -1736,6 +1776,7 @@ gbt_status gbt_train_tree(gbt_ctx *c, const gbt_matrix *data, const float *label
 {
     GBT_CHECK(c && data && p && tree && tree->nodes, "gbt_train_tree: NULL argument");
     GBT_CHECK(data->n_rows == 0 || (label_d && margin_d), "gbt_train_tree: NULL labels/margins");
+    GBT_TRY(hist_check_feature_bins(data));
     GBT_CHECK(p->max_depth >= 0 && p->max_depth <= 20, "max_depth %d outside [0, 20]", p->max_depth);
     GBT_CHECK(p->f > 0.0 && p->f <= 1.0, "f %g outside (0, 1]", p->f);
     GBT_CHECK(p->loss == GBT_LOSS_LOGISTIC || p->loss == GBT_LOSS_SQUARED, "unknown loss %d", p->loss);
@@ -1749,10 +1790,13 @@ gbt_status gbt_train_tree(gbt_ctx *c, const gbt_matrix *data, const float *label
 }
 
 gbt_status gbt_update_leaves(gbt_ctx *c, gbt_tree *tree, const gbt_train_params *tp, const gbt_matrix *data,
-                             float *margin_d)
+                             const int32_t *rows_d, const int32_t *position_d, int64_t n_pos, float *margin_d)
 {
     GBT_CHECK(c && tree && tree->nodes && tp && data, "gbt_update_leaves: NULL argument");
     GBT_CHECK(data->n_rows == 0 || margin_d, "margins are NULL");
+    GBT_CHECK(n_pos >= 0 && n_pos <= data->n_rows, "n_pos %lld outside [0, %lld]", (long long)n_pos,
+              (long long)data->n_rows);
+    GBT_CHECK(n_pos == 0 || position_d, "positions are NULL");
     GBT_TRY(set_device(c));
     gbt_node *nodes_d;
     int64_t *offs_d;
@@ -1760,23 +1804,43 @@ gbt_status gbt_update_leaves(gbt_ctx *c, gbt_tree *tree, const gbt_train_params 
     k_leaf_values<<<blocks(tree->n_nodes), 256, 0, c->stream>>>(nodes_d, tree->n_nodes, tree->exp_g,
                                                                tree->exp_h, tp->lambda, tp->eta);
     GBT_LAUNCHED();
+    // rows with known leaves first (marked done), then the traversal of the rest
+    uint32_t *done = nullptr;
+    unsigned long long *bad = nullptr;
+    if (n_pos > 0) {
+        const int64_t words = (data->n_rows + 31) / 32;
+        GBT_TRY(scratch_t(c, kScrPartFlags, (size_t)words + 2 * sizeof(unsigned long long) / 4, &done));
+        const int64_t at = (words + 1) & ~(int64_t)1;  // 8-byte aligned, after the bits
+        bad = (unsigned long long *)(done + at);
+        k_fill_u32<<<blocks(at + 2), 256, 0, c->stream>>>(done, at + 2, 0u);
+        GBT_LAUNCHED();
+        k_margin_add_positions<<<blocks(n_pos), 256, 0, c->stream>>>(rows_d, position_d, n_pos, data->n_rows,
+                                                                     nodes_d, tree->n_nodes, margin_d, done, bad);
+        GBT_LAUNCHED();
+    }
     Geo geo = geo_of(data);
     GBT_TRY(for_each_chunk(
         c, data,
         [&](const uint32_t *words, int64_t row0, int64_t rows) -> gbt_status {
             if (geo.row_words <= kWalkMaxWords)
                 k_margin_add_tree<true><<<blocks(rows), kWalkThreads, walk_lds_bytes(geo), c->stream>>>(
-                    words, rows, geo, nodes_d, tree->n_nodes, margin_d + row0);
+                    words, rows, geo, nodes_d, tree->n_nodes, margin_d + row0, done, row0);
             else
                 k_margin_add_tree<false><<<blocks(rows), kWalkThreads, 0, c->stream>>>(
-                    words, rows, geo, nodes_d, tree->n_nodes, margin_d + row0);
+                    words, rows, geo, nodes_d, tree->n_nodes, margin_d + row0, done, row0);
             GBT_LAUNCHED();
             return GBT_OK;
         },
         nullptr));
     GBT_HIP(hipMemcpyAsync(tree->nodes, nodes_d, tree->n_nodes * sizeof(gbt_node), hipMemcpyDeviceToHost,
                            c->stream));
+    unsigned long long n_bad = 0;
+    if (bad) GBT_HIP(hipMemcpyAsync(&n_bad, bad, sizeof(n_bad), hipMemcpyDeviceToHost, c->stream));
     GBT_HIP(hipStreamSynchronize(c->stream));
+    GBT_CHECK(n_bad == 0,
+              "%llu of %lld positions name no leaf of the tree or no new row of the data (those rows were "
+              "updated by traversal)",
+              n_bad, (long long)n_pos);
     return GBT_OK;
 }
 

@@ -94,18 +94,21 @@ class Sub(C.Structure):
 
 SPLIT_DTYPE = np.dtype([("gain", "<f8"), ("left_g", "<i8"), ("left_h", "<i8"),
                         ("right_g", "<i8"), ("right_h", "<i8"), ("feature", "<i4"),
-                        ("split_bin", "<i4"), ("default_left", "<i4"), ("valid", "<i4")])
+                        ("split_bin", "<i4"), ("default_left", "<i4"), ("valid", "<i4"),
+                        ("threshold", "<f4"), ("pad0", "<i4")])
+SEG_DTYPE = np.dtype([("node_slot", "<i4"), ("pad0", "<i4"), ("begin", "<i8"), ("end", "<i8")])
 NODE_DTYPE = np.dtype([("feature", "<i4"), ("split_bin", "<i4"), ("threshold", "<f4"),
                        ("leaf_value", "<f4"), ("gain", "<f8"), ("sum_g", "<i8"),
                        ("sum_h", "<i8"), ("n_rows", "<i4"), ("flags", "u1"),
                        ("pad", "u1", (3,))])
-assert SPLIT_DTYPE.itemsize == 56 and NODE_DTYPE.itemsize == 48
+assert SPLIT_DTYPE.itemsize == 64 and NODE_DTYPE.itemsize == 48 and SEG_DTYPE.itemsize == 24
 
 
 class Split(C.Structure):
     _fields_ = [("gain", C.c_double), ("left_g", C.c_int64), ("left_h", C.c_int64),
                 ("right_g", C.c_int64), ("right_h", C.c_int64), ("feature", C.c_int32),
-                ("split_bin", C.c_int32), ("default_left", C.c_int32), ("valid", C.c_int32)]
+                ("split_bin", C.c_int32), ("default_left", C.c_int32), ("valid", C.c_int32),
+                ("threshold", C.c_float), ("pad0", C.c_int32)]
 
 
 class Tree(C.Structure):
@@ -168,8 +171,8 @@ SIGNATURES = {
     "gbt_build_hist": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp]),
     "gbt_build_hist_noalloc": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _i32, _vp, _vp]),
     "gbt_eval_splits": (_i32, [_vp, _vp, _vp, _vp, _vp, _i32, _vp, _i32, _i32, _vp]),
-    "gbt_partition": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _i64, _vp, _vp]),
-    "gbt_update_leaves": (_i32, [_vp, _vp, _vp, _vp, _vp]),
+    "gbt_partition": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _i64, _vp, _vp, _vp]),
+    "gbt_update_leaves": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _i64, _vp]),
     "gbt_train_tree": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     "gbt_train_tree_naive": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     "gbt_predict": (_i32, [_vp, _vp, _i32, _vp, _vp, _f32, _vp]),
@@ -613,31 +616,95 @@ def make_train_params(loss=LOSS_LOGISTIC, max_depth=6, eta=0.3, lambda_=1.0, gam
                        seed, iteration, sampler, 0, goss_a)
 
 
-def gbt_eval_splits(ctx, matrix: Matrix, hist, node_sums, slots, params: TrainParams, e_g, e_h):
+def _int_range(t, name, lo, hi):
+    """Checks lo <= every value < hi of an int tensor or sequence (a device
+    tensor is read back: its values index device memory)."""
     torch = _torch()
-    n = len(slots)
-    out = torch.zeros((max(n, 1), SPLIT_DTYPE.itemsize // 8), dtype=torch.int64,
-                      device=ctx.torch_device)
-    sl = np.ascontiguousarray(slots, np.int32)
-    _check(_lib.gbt_eval_splits(ctx.h, matrix.h, _ptr(hist), _ptr(node_sums), _ptr(sl), n,
-                                C.byref(params), e_g, e_h, _ptr(out)))
-    return out.cpu().numpy().view(SPLIT_DTYPE).reshape(-1)[:n]
+    if isinstance(t, torch.Tensor):
+        if t.numel() == 0:
+            return
+        a, b = int(t.min()), int(t.max())
+    else:
+        v = np.asarray(t)
+        if v.size == 0:
+            return
+        a, b = int(v.min()), int(v.max())
+    if a < lo or b >= hi:
+        raise ValueError(f"{name}: values in [{a}, {b}], expected [{lo}, {hi})")
+
+
+def gbt_eval_splits(ctx, matrix: Matrix, hist, node_sums, slots, params: TrainParams, e_g, e_h,
+                    out=None):
+    """hist: int64 device [slots, total_bins, 2]; node_sums: int64 device
+    [n, 2]; slots: n histogram slots (sequence or int32 device tensor).
+    Returns the n splits (SPLIT_DTYPE) on the host, or, when out (an int64
+    device tensor of n * 8 words) is given, fills it and returns it."""
+    torch = _torch()
+    dev = ctx.torch_device
+    sl = slots if isinstance(slots, torch.Tensor) else _dev_tensor(np.asarray(slots, np.int32), torch.int32, dev)
+    n = sl.numel()
+    tb = matrix.info().total_bins
+    if hist is None or hist.numel() % (2 * tb):
+        raise ValueError(f"hist: expected [slots, {tb}, 2]")
+    _int_range(sl, "slots", 0, hist.numel() // (2 * tb))
+    res = out if out is not None else torch.zeros((max(n, 1), SPLIT_DTYPE.itemsize // 8), dtype=torch.int64,
+                                                  device=dev)
+    if res.numel() < n * SPLIT_DTYPE.itemsize // 8:
+        raise ValueError(f"out: {res.numel()} words for {n} splits")
+    h_p, s_p, sl_p, o_p = _dev_args(ctx, (hist, "hist", torch.int64, None, False),
+                                    (node_sums, "node_sums", torch.int64, 2 * n, False),
+                                    (sl, "slots", torch.int32, n, False), (res, "out", torch.int64, None, False))
+    _check(_lib.gbt_eval_splits(ctx.h, matrix.h, h_p, s_p, sl_p, n, C.byref(params), e_g, e_h, o_p))
+    if out is not None:
+        return out
+    return res.cpu().numpy().view(SPLIT_DTYPE).reshape(-1)[:n]
 
 
 def gbt_partition(ctx, matrix: Matrix, page, splits, segs, children, rows, position):
-    """splits: SPLIT_DTYPE array; segs: [(slot, begin, end)]; children: [l0, r0, l1, r1, ...].
-    rows/position are int32 device tensors (partitioned/updated in place).  Returns the
-    child segments as a list of (child, begin, end)."""
+    """splits: n splits (SPLIT_DTYPE array, or an int64 device tensor of
+    n * 8 words as gbt_eval_splits fills); segs: [(slot, begin, end)];
+    children: [l0, r0, l1, r1, ...].  rows/position are int32 device tensors
+    (partitioned/updated in place).  Every node array goes to the device and
+    the library works from there.  Returns the child segments as a list of
+    (child, begin, end); raises GbtError when the library counted malformed
+    entries."""
     torch = _torch()
+    dev = ctx.torch_device
     n = len(segs)
-    sp = np.ascontiguousarray(splits, SPLIT_DTYPE)
-    sg = (Seg * max(n, 1))(*[Seg(s, 0, b, e) for s, b, e in segs])
-    ch = np.ascontiguousarray(children, np.int32)
-    out = (Seg * max(2 * n, 1))()
+    inf = matrix.info()
+    if page is None or page.dim() != 2 or page.shape[1] != inf.row_words:
+        raise ValueError(f"page: expected [rows, {inf.row_words}] words")
+    if isinstance(splits, torch.Tensor):
+        sp = splits
+    else:
+        sp = _dev_tensor(np.ascontiguousarray(splits, SPLIT_DTYPE).view(np.int64), torch.int64, dev)
+    sg = np.zeros(max(n, 1), SEG_DTYPE)
+    for k, (slot, b, e) in enumerate(segs):
+        sg[k] = (slot, 0, b, e)
+    sg_d = _dev_tensor(sg.view(np.int64), torch.int64, dev)
+    ch = _dev_tensor(np.ascontiguousarray(children, np.int32).reshape(-1), torch.int32, dev)
+    if ch.numel() != 2 * n:
+        raise ValueError(f"children: {ch.numel()} ids for {n} nodes")
+    seg_out = torch.zeros(max(2 * n, 1) * SEG_DTYPE.itemsize // 8, dtype=torch.int64, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
     tmp = torch.empty_like(rows)
-    _check(_lib.gbt_partition(ctx.h, matrix.h, _ptr(page), sp.ctypes.data, sg, _ptr(ch), n,
-                              _ptr(rows), _ptr(tmp), rows.numel(), _ptr(position), out))
-    return [(out[i].node_slot, out[i].begin, out[i].end) for i in range(2 * n)]
+    _int_range(rows, "rows", 0, page.shape[0])
+    pg_p, sp_p, r_p, t_p, ps_p = _dev_args(ctx, (page, "page", torch.int32, None, False),
+                                           (sp, "splits", torch.int64, None, False),
+                                           (rows, "rows", torch.int32, None, False),
+                                           (tmp, "rows_tmp", torch.int32, rows.numel(), False),
+                                           (position, "position", torch.int32, None, False))
+    if sp.numel() < n * SPLIT_DTYPE.itemsize // 8:
+        raise ValueError(f"splits: {sp.numel()} words for {n} splits")
+    if position.numel() < page.shape[0]:
+        raise ValueError(f"position: {position.numel()} entries for {page.shape[0]} page rows")
+    _check(_lib.gbt_partition(ctx.h, matrix.h, pg_p, sp_p, _ptr(sg_d), _ptr(ch), n, r_p, t_p, rows.numel(),
+                              ps_p, _ptr(seg_out), _ptr(status)))
+    bad = int(status.item())
+    if bad:
+        raise GbtError(GBT_E_INVALID, f"gbt_partition: {bad} malformed segment/split entries")
+    so = seg_out.cpu().numpy().view(SEG_DTYPE)[:2 * n]
+    return [(int(x["node_slot"]), int(x["begin"]), int(x["end"])) for x in so]
 
 
 @dataclass
@@ -682,10 +749,21 @@ def gbt_train_tree_naive(ctx, matrix: Matrix, label, margin, params: TrainParams
     return TreeOut(nodes, t.exp_g, t.exp_h, params.max_depth, st)
 
 
-def gbt_update_leaves(ctx, tree: TreeOut, params: TrainParams, matrix: Matrix, margin):
-    m_p, = _dev_args(ctx, (margin, "margin", _torch().float32, matrix.info().n_rows, False))
+def gbt_update_leaves(ctx, tree: TreeOut, params: TrainParams, matrix: Matrix, margin, rows=None,
+                      position=None):
+    """Leaf values of `tree` and the margin update of every row of `matrix`.
+    position (int32 device, optional): the leaf of each training row
+    (entry i: row rows[i], or row i without rows), as gbt_partition leaves
+    it; those rows take their leaf without traversal."""
+    torch = _torch()
+    n_pos = position.numel() if position is not None else 0
+    if rows is not None and position is None:
+        raise ValueError("rows without position")
+    m_p, r_p, p_p = _dev_args(ctx, (margin, "margin", torch.float32, matrix.info().n_rows, False),
+                              (rows, "rows", torch.int32, n_pos, True),
+                              (position, "position", torch.int32, None, True))
     t = tree.as_struct()
-    _check(_lib.gbt_update_leaves(ctx.h, C.byref(t), C.byref(params), matrix.h, m_p))
+    _check(_lib.gbt_update_leaves(ctx.h, C.byref(t), C.byref(params), matrix.h, r_p, p_p, n_pos, m_p))
     return tree
 
 

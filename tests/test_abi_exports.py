@@ -31,7 +31,7 @@ def test_library_exports_every_declared_symbol():
     missing = [n for n in declared_functions() if not hasattr(lib, n)]
     assert not missing, missing
     lib.gbt_abi_version.restype = ctypes.c_int32
-    assert lib.gbt_abi_version() == 4
+    assert lib.gbt_abi_version() == 5
 
 
 @pytest.mark.skipif(not os.path.exists(LIB), reason="libgbt.so not built")
@@ -84,6 +84,7 @@ def test_binding_layouts_and_constants_match_the_header():
     for name, cls in pairs:
         assert c[name] == ctypes.sizeof(cls), name
     assert c["gbt_node"] == gbt.NODE_DTYPE.itemsize and c["gbt_split"] == gbt.SPLIT_DTYPE.itemsize
+    assert c["gbt_seg"] == gbt.SEG_DTYPE.itemsize
     py = {"GBT_E_INVALID": gbt.GBT_E_INVALID, "GBT_E_OOM": gbt.GBT_E_OOM, "GBT_E_BUDGET": gbt.GBT_E_BUDGET,
           "GBT_E_DEVICE": gbt.GBT_E_DEVICE, "GBT_E_UNSUPPORTED": gbt.GBT_E_UNSUPPORTED, "GBT_E_IO": gbt.GBT_E_IO,
           "GBT_HOME_DEVICE": gbt.HOME_DEVICE, "GBT_HOME_PINNED_HOST": gbt.HOME_PINNED_HOST,

@@ -366,18 +366,29 @@ def test_build_hist_symbol_widths(gbt, ctx, hist_kernel, n, m, missing, max_bin,
     assert same_bits(h[1], orc.build_hist(b, sel, q))
 
 
-def test_build_hist_rejects_oversized_feature(gbt, ctx):
-    """A dense feature of more bins than a histogram group holds (2560) is an
-    error, not a wrong histogram."""
+def test_quantize_rejects_oversized_feature(gbt, ctx):
+    """A dense feature may take more bins than a histogram group holds (2560)
+    only if max_bin allows it: such a max_bin is refused when quantization
+    starts, not in the middle of training; CSR input (sparse groups of up to
+    10176 bins) takes it."""
     n = 12000
     X = dense_case(35, n, 3, 0.0, "normal")
-    mx = gbt.gbt_quantize(ctx, X, max_bin=8000)
-    assert mx.info().total_bins > 3 * 2560
+    with pytest.raises(gbt.GbtError, match="max_bin") as e:
+        gbt.gbt_quantize(ctx, X, max_bin=2561)
+    assert e.value.code == gbt.GBT_E_UNSUPPORTED
+    mx = gbt.gbt_quantize(ctx, X, max_bin=2560)
+    assert mx.info().total_bins == 3 * 2560
     q = torch.zeros((n, 2), dtype=torch.int64, device="cuda")
     page = torch.from_numpy(mx.page(0).view(np.int32)).cuda()
     hist = torch.zeros((1, mx.info().total_bins, 2), dtype=torch.int64, device="cuda")
-    with pytest.raises(RuntimeError, match="bins"):
-        gbt.gbt_build_hist(ctx, mx, page, q, None, [(0, 0, n)], hist=hist)
+    gbt.gbt_build_hist(ctx, mx, page, q, None, [(0, 0, n)], hist=hist)
+    mx.free()
+    ds, _ = small_csr(3000, 4, 0.9, 36)
+    ms = gbt.gbt_quantize(ctx, ds, max_bin=8000)
+    assert ms.info().total_bins > 2560
+    with pytest.raises(gbt.GbtError, match="max_bin"):
+        gbt.gbt_quantize(ctx, ds, max_bin=10177)
+    ms.free()
 
 
 # ------------------------------------------------------------ split evaluation
@@ -397,16 +408,23 @@ def test_eval_splits(gbt, ctx, lam, gamma, mcw):
     hists = np.stack([orc.build_hist(b, r, q) for r in node_rows])
     sums = np.stack([q[r].sum(0) for r in node_rows]).astype(np.int64)
     P = gbt.make_train_params(lambda_=lam, gamma=gamma, min_child_weight=mcw)
-    out = gbt.gbt_eval_splits(ctx, mx, torch.from_numpy(hists).cuda(), torch.from_numpy(sums).cuda(),
-                              list(range(len(node_rows))), P, eg, eh)
+    # the node list on the device, in a shuffled slot order
+    order = np.array([2, 0, 3, 1], np.int32)
+    hd = torch.from_numpy(hists).cuda()
+    out = gbt.gbt_eval_splits(ctx, mx, hd, torch.from_numpy(sums[order]).cuda(),
+                              torch.from_numpy(order).cuda(), P, eg, eh)
     OP = orc.Params(lambda_=lam, gamma=gamma, min_child_weight=mcw)
-    for k in range(len(node_rows)):
+    cut_ptr, cut_values = mx.cuts()
+    for i, k in enumerate(order):
         s = orc.eval_node(hists[k], sums[k], b.cuts.nbins, OP, eg, eh)
-        got = out[k]
+        got = out[i]
         assert got["valid"] == s.valid
         if s.valid:
             assert (got["feature"], got["split_bin"], got["default_left"]) == \
                 (s.feature, s.split_bin, s.default_left)
+            thr = b.cuts.cut_values[b.cuts.cut_ptr[s.feature] + s.split_bin - 1]
+            assert np.float32(got["threshold"]).tobytes() == np.float32(thr).tobytes()
+            assert cut_values[cut_ptr[s.feature] + s.split_bin - 1] == thr
             assert np.float64(got["gain"]).tobytes() == np.float64(s.gain).tobytes()
             assert (got["left_g"], got["left_h"], got["right_g"], got["right_h"]) == \
                 (s.left_g, s.left_h, s.right_g, s.right_h)
@@ -433,13 +451,18 @@ def test_partition(gbt, ctx):
         rows = torch.from_numpy(perm.copy()).cuda()
         position = torch.full((n,), -1, dtype=torch.int32, device="cuda")
         page = torch.from_numpy(mx.page(0).view(np.int32)).cuda()
-        out = gbt.gbt_partition(ctx, mx, page, splits, segs, children, rows, position)
+        # splits on the device, as gbt_eval_splits leaves them, for the
+        # dense case; a host array for the sparse one
+        sp = torch.from_numpy(splits.view(np.int64).copy()).cuda() if mb == 256 else splits
+        out = gbt.gbt_partition(ctx, mx, page, sp, segs, children, rows, position)
         got = rows.cpu().numpy()
         pos = position.cpu().numpy()
         for k in range(4):
             seg = perm[bounds[k]:bounds[k + 1]].astype(np.int64)
             if not splits[k]["valid"]:
                 assert same_bits(got[bounds[k]:bounds[k + 1]], seg.astype(np.int32))
+                assert out[2 * k] == (children[2 * k], bounds[k], bounds[k + 1])
+                assert out[2 * k + 1] == (children[2 * k + 1], bounds[k + 1], bounds[k + 1])
                 continue
             left, right = orc.partition(b, seg, int(splits[k]["feature"]), int(splits[k]["split_bin"]),
                                         bool(splits[k]["default_left"]))
@@ -448,6 +471,31 @@ def test_partition(gbt, ctx):
             assert same_bits(got[bounds[k]:bounds[k] + nl], left.astype(np.int32))
             assert same_bits(got[bounds[k] + nl:bounds[k + 1]], right.astype(np.int32))
             assert (pos[left] == children[2 * k]).all() and (pos[right] == children[2 * k + 1]).all()
+
+
+def test_partition_reports_malformed_entries(gbt, ctx):
+    """A segment past the rows, a split feature out of range and two
+    segments that claim the same rows are counted on the device (no host
+    check before the work) and raise; every access stays in bounds."""
+    X = dense_case(53, 3000, 6, 0.1)
+    mx = gbt.gbt_quantize(ctx, X, max_bin=64)
+    page = torch.from_numpy(mx.page(0).view(np.int32)).cuda()
+    n = 3000
+    ok = np.zeros(1, gbt.SPLIT_DTYPE)
+    ok[0]["valid"], ok[0]["feature"], ok[0]["split_bin"] = 1, 2, 5
+    bad_feat = ok.copy()
+    bad_feat[0]["feature"] = 6
+    cases = [(ok, [(0, 0, n + 5)]), (bad_feat, [(0, 0, n)]), (np.concatenate([ok, ok]), [(0, 0, 2000), (1, 1500, n)])]
+    for splits, segs in cases:
+        rows = torch.arange(n, dtype=torch.int32, device="cuda")
+        position = torch.full((n,), -1, dtype=torch.int32, device="cuda")
+        with pytest.raises(gbt.GbtError, match="malformed"):
+            gbt.gbt_partition(ctx, mx, page, splits, segs, list(range(1, 2 * len(segs) + 1)), rows, position)
+    # and a well-formed call on the same context still works
+    rows = torch.arange(n, dtype=torch.int32, device="cuda")
+    position = torch.full((n,), -1, dtype=torch.int32, device="cuda")
+    out = gbt.gbt_partition(ctx, mx, page, ok, [(0, 0, n)], [1, 2], rows, position)
+    assert out[0][1] == 0 and out[1][2] == n and out[0][2] == out[1][1]
 
 
 # ------------------------------------------------------------ whole trees
@@ -750,7 +798,58 @@ def test_predict_and_update_leaves(gbt, ctx):
     P = gbt.make_train_params(max_depth=5, eta=0.3)
     gbt.gbt_update_leaves(ctx, blank, P, mx, mg)
     assert same_bits(blank.nodes, t0.nodes)
-    assert same_bits(mg.cpu().numpy(), orc.predict_binned(b, [otrees[0]], 0.0))
+    want = orc.predict_binned(b, [otrees[0]], 0.0)
+    assert same_bits(mg.cpu().numpy(), want)
+    # the training rows' leaves from their positions (a third of the rows,
+    # ascending ids), the rest traversed: the same margins
+    n = mx.info().n_rows
+    leaf = leaf_ids(b, t0.nodes)
+    rng = np.random.default_rng(61)
+    sel = np.sort(rng.choice(n, n // 3, replace=False)).astype(np.int32)
+    mg2 = torch.zeros(n, dtype=torch.float32, device="cuda")
+    gbt.gbt_update_leaves(ctx, blank, P, mx, mg2, rows=torch.from_numpy(sel).cuda(),
+                          position=torch.from_numpy(leaf[sel].astype(np.int32)).cuda())
+    assert same_bits(mg2.cpu().numpy(), want)
+    # the positions are what those rows take: name one other leaf for all of them
+    leaves = np.nonzero(t0.nodes["flags"] & orc.NODE_LEAF)[0]
+    other = int(leaves[-1])
+    mg3 = torch.zeros(n, dtype=torch.float32, device="cuda")
+    gbt.gbt_update_leaves(ctx, blank, P, mx, mg3, rows=torch.from_numpy(sel).cuda(),
+                          position=torch.full((len(sel),), other, dtype=torch.int32, device="cuda"))
+    g3 = mg3.cpu().numpy()
+    rest = np.setdiff1d(np.arange(n), sel)
+    assert (g3[sel] == t0.nodes["leaf_value"][other]).all() and same_bits(g3[rest], want[rest])
+    # no rows given: entry i is row i
+    k = 500
+    mg4 = torch.zeros(n, dtype=torch.float32, device="cuda")
+    gbt.gbt_update_leaves(ctx, blank, P, mx, mg4, position=torch.from_numpy(leaf[:k].astype(np.int32)).cuda())
+    assert same_bits(mg4.cpu().numpy(), want)
+    # a split node, a row past the data and a repeated row: counted, raised,
+    # and those rows traversed
+    split_node = int(np.nonzero((t0.nodes["flags"] & orc.NODE_LEAF) == 0)[0][0])
+    bad_rows = np.array([3, 7, n + 2, 9, 9], np.int32)
+    bad_pos = np.array([leaf[3], split_node, leaf[0], leaf[9], leaf[9]], np.int32)
+    mg5 = torch.zeros(n, dtype=torch.float32, device="cuda")
+    with pytest.raises(gbt.GbtError, match="3 of 5 positions"):
+        gbt.gbt_update_leaves(ctx, blank, P, mx, mg5, rows=torch.from_numpy(bad_rows).cuda(),
+                              position=torch.from_numpy(bad_pos).cuda())
+    assert same_bits(mg5.cpu().numpy(), want)
+
+
+def leaf_ids(b, nodes):
+    """Each row's leaf in a heap-ordered tree, by its oracle bins."""
+    node = np.zeros(b.n, np.int64)
+    while True:
+        nd = nodes[node]
+        inner = (nd["flags"] & orc.NODE_LEAF) == 0
+        if not inner.any():
+            return node
+        idx = np.nonzero(inner)[0]
+        f = nd["feature"][inner]
+        binv = b.dense[idx, f]
+        dl = (nd["flags"][inner] & orc.NODE_DEFAULT_LEFT) != 0
+        left = np.where(binv == orc.MISSING, dl, binv < nd["split_bin"][inner])
+        node[idx] = np.where(left, 2 * node[idx] + 1, 2 * node[idx] + 2)
 
 
 def test_budget_is_enforced(gbt):
