@@ -333,6 +333,9 @@ struct __align__(16) DevNode {
     int64_t nleft;          // partition: rows of the segment that go left
     double gain;
     int64_t left_g, left_h, right_g, right_h;
+    // tree driver's partition: the tiles of the first and last slot and the
+    // left flags of those tiles before the first slot and up to the last
+    int32_t tile_b, left_b, tile_e, left_e;
 };
 static_assert(sizeof(DevNode) % 16 == 0, "DevNode is read with 16-byte loads");
 

@@ -13,6 +13,7 @@
 // split feature, a device-wide exclusive scan of the flags, and a scatter
 // that writes [left | right] of every splitting segment in input order.
 #include "split_impl.h"
+#include "plan_impl.h"
 
 #include <cstring>
 
@@ -790,7 +791,7 @@ __device__ inline int4 wave_decide(const EvalCand *__restrict__ cand, int32_t m,
 // wave chooses the splits of the level's nodes among its slots from their
 // candidates, and the wave holding a node's first slot records the choice
 // (a node without slots cannot split).
-template <bool kChoose>
+template <bool kChoose, bool kCount>
 __global__ void __launch_bounds__(kPartThreads)
     k_part_flags_tiles(const int32_t *__restrict__ rows, int64_t n, const uint32_t *__restrict__ page, Geo geo,
                        const int32_t *__restrict__ position, const int32_t *__restrict__ slot_node,
@@ -864,6 +865,35 @@ __global__ void __launch_bounds__(kPartThreads)
 #pragma unroll
         for (int k = 0; k < kPartItems; ++k)
             if (i0 + k < n) flags[i0 + k] = (uint8_t)((f4 >> (8 * k)) & 1u);
+    }
+    if (kCount) {
+        // the left flags of this tile before each node's first slot and up
+        // to its last slot, written by the tile holding that slot (the plan
+        // adds the counts of the tiles before); a node's slots are one run
+        // of equal slot nodes
+        const int32_t prev = i0 > 0 && i0 <= n ? slot_node[i0 - 1] : -2;
+        const int32_t next = i0 + kPartItems < n ? slot_node[i0 + kPartItems] : -2;
+        int32_t tot;
+        int32_t pre = part_block_scan(cnt, red, &tot);
+#pragma unroll
+        for (int k = 0; k < kPartItems; ++k) {
+            const int32_t f = (int32_t)((f4 >> (8 * k)) & 1u);
+            if (i0 + k < n && nid[k] >= 0) {
+                const int32_t lo = k == 0 ? prev : nid[k - 1];
+                const int32_t hi = k == kPartItems - 1 ? next : nid[k + 1];
+                if (lo != nid[k]) {
+                    nodes[nid[k]].tile_b = (int32_t)blockIdx.x;
+                    nodes[nid[k]].left_b = pre;
+                }
+                if (hi != nid[k]) {
+                    nodes[nid[k]].tile_e = (int32_t)blockIdx.x;
+                    nodes[nid[k]].left_e = pre + f;
+                }
+            }
+            pre += f;
+        }
+        if (threadIdx.x == 0) tile_cnt[blockIdx.x] = tot;
+        return;
     }
     for (int d = 32; d > 0; d >>= 1) cnt += __shfl_xor(cnt, d, 64);
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = cnt;
@@ -997,19 +1027,31 @@ __global__ void __launch_bounds__(kPartThreads)
 // from this tile's scan when the node starts in the tile; the one node that
 // starts in an earlier tile (the node of the tile's first slot) gets them
 // from the tile counts before its first tile and that tile's flags.  The
-// block holding a node's last slot writes the node's left count.  The order
-// of rows within a node enters no result.
+// nodes' left counts come from the flags pass.  The order of rows within a
+// node enters no result.  With `has_plan`, block 0 is the level's plan
+// (plan_impl.h), which reads only the node records and left counts of the
+// flags pass and writes the children's records, which no other block reads;
+// the tiles are blocks 1.. then.
 __global__ void __launch_bounds__(kPartThreads)
     k_part_scatter_rev(const int32_t *__restrict__ rows, int64_t n, const uint8_t *__restrict__ flags,
                        const int32_t *__restrict__ tile_cnt, const long long *__restrict__ tile_off,
                        const int32_t *__restrict__ slot_node, int32_t *__restrict__ slot_node_out,
-                       DevNode *__restrict__ nodes, int32_t *__restrict__ rows_out)
+                       DevNode *__restrict__ nodes, int32_t *__restrict__ rows_out, int32_t has_plan,
+                       PlanArgs pa)
 {
+    if (has_plan && blockIdx.x == 0) {
+        pa.tile_cnt = tile_cnt;
+        pa.tile_off = tile_off;
+        pa.tiles = (n + kPartTile - 1) / kPartTile;
+        plan_level_block<kPartThreads>(nodes, pa);
+        return;
+    }
+    const int64_t tile = (int64_t)blockIdx.x - (has_plan ? 1 : 0);
     __shared__ int32_t lds16[kPartThreads / 64];
     __shared__ long long s_red[2][kPartThreads / 64];
     __shared__ int32_t s_pref[kPartThreads];  // left flags of the tile before each thread's slots
     __shared__ uint32_t s_f4[kPartThreads];   // each thread's four flags, one per byte
-    const int64_t ts = (int64_t)blockIdx.x * kPartTile;
+    const int64_t ts = tile * kPartTile;
     const int64_t i0 = ts + (int64_t)threadIdx.x * kPartItems;
     int32_t r[kPartItems], nid[kPartItems];
     part_load(rows, nullptr, slot_node, i0, n, r, nid);
@@ -1033,11 +1075,11 @@ __global__ void __launch_bounds__(kPartThreads)
     if (tile_off) {
         // exclusive tile offsets: the first wave's first lane takes both
         if (threadIdx.x == 0) {
-            before = tile_off[blockIdx.x];
+            before = tile_off[tile];
             before_b = tile_off[tb];
         }
     } else {
-        for (int64_t k = threadIdx.x; k < (int64_t)blockIdx.x; k += kPartThreads) {
+        for (int64_t k = threadIdx.x; k < tile; k += kPartThreads) {
             const int32_t v = tile_cnt[k];
             before += v;
             before_b += k < tb ? v : 0;
@@ -1097,7 +1139,6 @@ __global__ void __launch_bounds__(kPartThreads)
                         dest = end - 1 - ((i - begin) - lb);
                         child = nd.right_child;
                     }
-                    if (i == end - 1) nd.nleft = P + f - pl;
                 }
             }
             rows_out[dest] = r[k];
@@ -1112,6 +1153,7 @@ __global__ void __launch_bounds__(kPartThreads)
 // and each thread writes its run's offsets.
 constexpr int kTileScanThreads = 1024;
 constexpr int64_t kScanTilesAbove = 2048;
+static_assert(kScanTilesAbove <= kPlanScanTiles, "the plan block scans the tile counts that have no offsets");
 
 __global__ void __launch_bounds__(kTileScanThreads)
     k_tile_offsets(const int32_t *__restrict__ cnt, int64_t tiles, long long *__restrict__ off)
@@ -1216,7 +1258,7 @@ gbt_status split_columns(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page,
 gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int32_t *rows,
                               int64_t n, const int32_t *slot_node, int32_t *slot_node_out, DevNode *nodes,
                               int32_t *rows_out, const LevelChoice *choice, const SlotTable *stbl,
-                              const uint16_t *cols)
+                              const uint16_t *cols, const PlanArgs *plan)
 {
     if (n == 0) return GBT_OK;
     const SlotTable st = stbl ? *stbl : SlotTable{nullptr, nullptr, nullptr, 0, 0, 0};
@@ -1227,10 +1269,10 @@ gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
     int32_t *tile_cnt;
     GBT_TRY(scratch_t(c, kScrScan, (size_t)tiles + 1, &tile_cnt));
     if (choice)
-        k_part_flags_tiles<true><<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(
+        k_part_flags_tiles<true, true><<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(
             rows, n, page, geo_of(mx), nullptr, slot_node, nodes, flags, tile_cnt, *choice, st, cols);
     else
-        k_part_flags_tiles<false><<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(
+        k_part_flags_tiles<false, true><<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(
             rows, n, page, geo_of(mx), nullptr, slot_node, nodes, flags, tile_cnt, LevelChoice{}, st, cols);
     GBT_LAUNCHED();
     // many tiles: one block scans the tile counts first, instead of every
@@ -1241,8 +1283,10 @@ gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
         k_tile_offsets<<<1, kTileScanThreads, 0, c->stream>>>(tile_cnt, tiles, tile_off);
         GBT_LAUNCHED();
     }
-    k_part_scatter_rev<<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(rows, n, flags, tile_cnt, tile_off,
-                                                                       slot_node, slot_node_out, nodes, rows_out);
+    const int32_t has_plan = plan ? 1 : 0;
+    k_part_scatter_rev<<<(unsigned)(tiles + has_plan), kPartThreads, 0, c->stream>>>(
+        rows, n, flags, tile_cnt, tile_off, slot_node, slot_node_out, nodes, rows_out, has_plan,
+        plan ? *plan : PlanArgs{});
     GBT_LAUNCHED();
     return GBT_OK;
 }
@@ -1262,7 +1306,7 @@ gbt_status partition_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page
     GBT_TRY(scratch_t(c, kScrScan, (size_t)tiles + 1, &tile_off));
     // tile_off receives each tile's left count; the bounds and the scatter
     // sum the counts before their tiles themselves
-    k_part_flags_tiles<false><<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(rows, n, page, geo, position, slot_node,
+    k_part_flags_tiles<false, false><<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(rows, n, page, geo, position, slot_node,
                                                                        nodes, flags, tile_off, LevelChoice{},
                                                                        SlotTable{nullptr, nullptr, nullptr, 0, 0, 0},
                                                                        nullptr);

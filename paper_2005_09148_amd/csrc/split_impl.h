@@ -82,10 +82,14 @@ struct LevelChoice {
     int32_t lo, hi;
 };
 
+struct PlanArgs;
+
 // The tree driver's partition: rows[0, n) by slot_node as partition_impl,
 // except that a splitting node's right rows land at the back of its segment
-// in reverse slot order; nodes[id].nleft receives each splitting node's left
-// count (pleft is not written).  Two kernels.  With `choice`, the split
+// in reverse slot order; nodes[id].nleft (zero before the call) receives
+// each splitting node's left count (pleft is not written).  Two kernels;
+// with `plan`, the second also runs the level's plan (plan_impl.h) in one
+// of its blocks.  With `choice`, the split
 // records of the level's nodes are chosen from the candidates and written
 // by the first kernel (instead of by eval_reduce_impl).  With `stbl` (a
 // sparse page's slot table), the search for a row's split feature looks
@@ -96,7 +100,8 @@ struct LevelChoice {
 gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int32_t *rows,
                               int64_t n, const int32_t *slot_node, int32_t *slot_node_out, DevNode *nodes,
                               int32_t *rows_out, const LevelChoice *choice = nullptr,
-                              const SlotTable *stbl = nullptr, const uint16_t *cols = nullptr);
+                              const SlotTable *stbl = nullptr, const uint16_t *cols = nullptr,
+                              const PlanArgs *plan = nullptr);
 
 // Whether a page of mx's geometry takes a column copy (dense, symbols of at
 // most 16 bits).

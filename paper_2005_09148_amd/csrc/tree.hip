@@ -12,6 +12,7 @@
 #include "sample_impl.h"
 #include "hist_impl.h"
 #include "split_impl.h"
+#include "plan_impl.h"
 
 namespace gbt {
 
@@ -370,185 +371,6 @@ __global__ void k_tree_init(DevNode *__restrict__ nodes, int32_t n_nodes, const 
     if (i < n_root) {
         const int64_t b = i * chunk;
         work[i] = {b, b + chunk < R ? b + chunk : R, (int32_t)i, 0};
-    }
-}
-
-// Exclusive scan across a 1024-thread block; *total receives the sum.
-__device__ inline int32_t scan1024(int32_t v, int32_t *lds16, int32_t *total)
-{
-    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-    int32_t x = v;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        int32_t y = __shfl_up(x, d, 64);
-        if (lane >= d) x += y;
-    }
-    __syncthreads();
-    if (lane == 63) lds16[wid] = x;
-    __syncthreads();
-    int32_t off = 0, tot = 0;
-    for (int w = 0; w < 16; ++w) {
-        if (w < wid) off += lds16[w];
-        tot += lds16[w];
-    }
-    *total = tot;
-    return x - v + off;
-}
-
-// After a level's partition (one block of 1024 threads): the child segments
-// of every split node from the partition's left count (nleft), then, when `plan`
-// is set, the plan of the next level: the list of present children in heap
-// order with their histogram slots, and for each split parent the smaller
-// child to build (chunked into work items) with the larger one as parent
-// minus it.  The chunk size is chosen so that the level has at most
-// `items` work items per feature group (one per workgroup slot), unless it
-// builds more nodes than that.
-constexpr int64_t kMinChunk = 1024;
-
-// What the plan needs of one split parent, all from the parent's record.
-struct PlanNode {
-    int64_t begin, nl, nr;  // segment start, left and right row counts
-    long long lg, lh, rg, rh;
-    int32_t p, slot, split, pad0;
-};
-
-__device__ inline PlanNode plan_node(const EvalNode *__restrict__ cur, const DevNode *__restrict__ nodes, int32_t t)
-{
-    PlanNode x;
-    x.p = cur[t].heap;
-    x.slot = cur[t].slot;
-    const DevNode &d = nodes[x.p];
-    x.split = d.split;
-    x.begin = d.begin;
-    x.nl = d.nleft;
-    x.nr = d.end - d.begin - d.nleft;
-    x.lg = d.left_g;
-    x.lh = d.left_h;
-    x.rg = d.right_g;
-    x.rh = d.right_h;
-    x.pad0 = 0;
-    return x;
-}
-
-__global__ void __launch_bounds__(1024)
-    k_plan_level(const EvalNode *__restrict__ cur, const int32_t *__restrict__ n_cur_d,
-                 DevNode *__restrict__ nodes, int32_t plan, int32_t items,
-                 EvalNode *__restrict__ next, int32_t *__restrict__ n_next_d, HistWork *__restrict__ work,
-                 int32_t *__restrict__ n_work_d, HistReduce *__restrict__ red, int32_t *__restrict__ n_red_d,
-                 unsigned long long *__restrict__ stat)
-{
-    __shared__ int32_t lds16[16];
-    __shared__ unsigned long long red_rows[16];
-    __shared__ int32_t red_nodes[16];
-    // one pass's nodes: first work item (and the pass's end), row segment
-    __shared__ int32_t s_kp[1025];
-    __shared__ long long s_sb[1024], s_se[1024];
-    const int32_t n_cur = *n_cur_d;
-    // the children's segments and sums; the rows and nodes to build, for the
-    // chunk size (a level of at most 1024 nodes keeps each thread's node in
-    // registers for the second pass)
-    PlanNode mine{};
-    unsigned long long rb = 0;
-    int32_t nbuild = 0;
-    for (int32_t t = threadIdx.x; t < n_cur; t += 1024) {
-        const PlanNode x = plan_node(cur, nodes, t);
-        if (t < 1024) mine = x;
-        if (!x.split) continue;
-        DevNode &L = nodes[2 * x.p + 1];
-        DevNode &Rn = nodes[2 * x.p + 2];
-        L.present = 1;
-        L.sum_g = x.lg;
-        L.sum_h = x.lh;
-        L.begin = x.begin;
-        L.end = x.begin + x.nl;
-        Rn.present = 1;
-        Rn.sum_g = x.rg;
-        Rn.sum_h = x.rh;
-        Rn.begin = x.begin + x.nl;
-        Rn.end = x.begin + x.nl + x.nr;
-        rb += (unsigned long long)(x.nl <= x.nr ? x.nl : x.nr);
-        ++nbuild;
-    }
-    if (!plan) return;
-    for (int d = 32; d > 0; d >>= 1) {
-        rb += __shfl_xor(rb, d, 64);
-        nbuild += __shfl_xor(nbuild, d, 64);
-    }
-    if ((threadIdx.x & 63) == 0) {
-        red_rows[threadIdx.x >> 6] = rb;
-        red_nodes[threadIdx.x >> 6] = nbuild;
-    }
-    __syncthreads();
-    unsigned long long rows_total = 0;
-    int32_t nodes_total = 0;
-    for (int w = 0; w < 16; ++w) {
-        rows_total += red_rows[w];
-        nodes_total += red_nodes[w];
-    }
-    // room for the chunks of large nodes: what the node count leaves of the
-    // target, but at least half of it (a level of many nodes may then take
-    // up to 1.5 times the target)
-    const int64_t room = items - nodes_total > items / 2 ? items - nodes_total : (items / 2 > 1 ? items / 2 : 1);
-    int64_t chunk = ((int64_t)rows_total + room - 1) / room;
-    chunk = chunk > kMinChunk ? chunk : kMinChunk;
-    int32_t c_build = 0, c_part = 0;
-    unsigned long long rows_built = 0;
-    for (int32_t base = 0; base < n_cur; base += 1024) {
-        const int32_t t = base + (int32_t)threadIdx.x;
-        PlanNode x{};
-        if (t < n_cur) x = n_cur <= 1024 ? mine : plan_node(cur, nodes, t);
-        const bool split = t < n_cur && x.split;
-        int32_t nchunks = 0;
-        if (split) {
-            const int64_t ns = x.nl <= x.nr ? x.nl : x.nr;
-            nchunks = (int32_t)(ns > 0 ? (ns + chunk - 1) / chunk : 1);
-            rows_built += (unsigned long long)ns;
-        }
-        int32_t tot_b, tot_p;
-        const int32_t kb = scan1024(split ? 1 : 0, lds16, &tot_b) + c_build;
-        const int32_t kp = scan1024(nchunks, lds16, &tot_p) + c_part;
-        if (split) {
-            const int32_t sl = 2 * kb, sr = sl + 1;  // the children of split parents, in heap order
-            next[sl] = {x.lg, x.lh, sl, 2 * x.p + 1};
-            next[sr] = {x.rg, x.rh, sr, 2 * x.p + 2};
-            nodes[2 * x.p + 1].slot = sl;
-            nodes[2 * x.p + 2].slot = sr;
-            const bool left_small = x.nl <= x.nr;
-            const int64_t sb = left_small ? x.begin : x.begin + x.nl;
-            const int64_t se = left_small ? x.begin + x.nl : x.begin + x.nl + x.nr;
-            red[kb] = {left_small ? sl : sr, kp, nchunks, x.slot, left_small ? sr : sl, 0};
-            s_sb[threadIdx.x] = sb;
-            s_se[threadIdx.x] = se;
-        }
-        s_kp[threadIdx.x] = kp;
-        if (threadIdx.x == 1023) s_kp[1024] = c_part + tot_p;
-        __syncthreads();
-        // the pass's work items, written by all threads: item e belongs to
-        // the last node whose first item is <= e (nodes without items have
-        // the next node's first item)
-        for (int32_t e = c_part + (int32_t)threadIdx.x; e < c_part + tot_p; e += 1024) {
-            int32_t lo = 0, hi = 1024;  // s_kp[lo] <= e < s_kp[hi]
-            while (hi - lo > 1) {
-                const int32_t mid = (lo + hi) >> 1;
-                if (s_kp[mid] <= e)
-                    lo = mid;
-                else
-                    hi = mid;
-            }
-            const int64_t b = s_sb[lo] + (int64_t)(e - s_kp[lo]) * chunk;
-            work[e] = {b, b + chunk < s_se[lo] ? b + chunk : s_se[lo], e, 0};
-        }
-        __syncthreads();
-        c_build += tot_b;
-        c_part += tot_p;
-    }
-    for (int d = 32; d > 0; d >>= 1) rows_built += __shfl_xor(rows_built, d, 64);
-    if ((threadIdx.x & 63) == 0 && rows_built) atomicAdd(&stat[0], rows_built);
-    if (threadIdx.x == 0) {
-        *n_next_d = 2 * c_build;
-        *n_red_d = c_build;
-        *n_work_d = c_part;
-        atomicAdd(&stat[1], (unsigned long long)c_build);
     }
 }
 
@@ -1183,16 +1005,13 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         mark = timer_begin(c, kPhSplit);
         if (!fused && R > 0) GBT_TRY(eval_impl(c, mx, histA, evA, maxn, ep, splits_d, cntA, nodes));
         const LevelChoice lc{cand, mx->m, (int32_t)((1u << d) - 1), (int32_t)((2u << d) - 1)};
+        const bool plan_next = d + 1 < D && R > 0;
+        // the partition's second kernel also plans the next level
+        const PlanArgs pa{evA, cntA, plan_next ? 1 : 0, items, evB, cntB, work_d, cnt + 2, red_d, cnt + 3, stat};
         GBT_TRY(partition_rev_impl(c, mx, so.page, rows, R, slot_node, slot_tmp, nodes, rows_tmp,
-                                   choose ? &lc : nullptr, stbl.row ? &stbl : nullptr, cols));
+                                   choose ? &lc : nullptr, stbl.row ? &stbl : nullptr, cols, &pa));
         std::swap(rows, rows_tmp);
         std::swap(slot_node, slot_tmp);
-        const bool plan_next = d + 1 < D && R > 0;
-        if (R > 0) {
-            k_plan_level<<<1, 1024, 0, c->stream>>>(evA, cntA, nodes, plan_next ? 1 : 0, items, evB, cntB,
-                                                    work_d, cnt + 2, red_d, cnt + 3, stat);
-            GBT_LAUNCHED();
-        }
         timer_end(c, mark);
         if (plan_next) {
             HistLaunch hl{hp.kind, groups_d, G, hp.max_groups_bins, work_d, cnt + 2, max_work, red_d, cnt + 3,
