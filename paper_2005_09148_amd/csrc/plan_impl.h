@@ -65,6 +65,37 @@ __device__ inline int32_t plan_block_scan(int32_t v, int32_t *lds, int32_t *tota
     return x - v + off;
 }
 
+// Eq. 6 scaled by the learning rate, for every present node that does not
+// split: leaf = (float)((-G/(H+lambda)) * eta).
+__device__ inline float leaf_of(long long Qg, long long Qh, int32_t eg, int32_t eh, double lambda, double eta)
+{
+    double G = ldexp((double)Qg, -eg), H = ldexp((double)Qh, -eh);
+    double w = -G / (H + lambda);
+    return (float)(w * eta);
+}
+
+// Node i's leaf value, and its entry in the compact form of the tree used by
+// the row walk: {feature, split_bin << 2 | default_left << 1 | splits}.
+__device__ inline void leaf_entry(const DevNode *__restrict__ nodes, int32_t i, int32_t eg, int32_t eh,
+                                  double lambda, double eta, float *__restrict__ leaf, uint2 *__restrict__ compact)
+{
+    const DevNode d = nodes[i];
+    leaf[i] = (d.present && !d.split) ? leaf_of(d.sum_g, d.sum_h, eg, eh, lambda, eta) : 0.0f;
+    compact[i] = d.split ? make_uint2((uint32_t)d.feature, ((uint32_t)d.split_bin << 2) |
+                                                               ((d.default_left ? 1u : 0u) << 1) | 1u)
+                         : make_uint2(0u, 0u);
+}
+
+// The tree's leaves, made by the last level's plan (leaf == NULL: none).
+struct LeafArgs {
+    float *leaf;
+    uint2 *compact;
+    const int32_t *e_dev;  // {e_g, e_h}
+    double lambda, eta;
+    int32_t n_nodes;
+    int32_t pad0;
+};
+
 struct PlanArgs {
     const EvalNode *cur;     // the level's nodes (count *n_cur_d)
     const int32_t *n_cur_d;
@@ -84,6 +115,7 @@ struct PlanArgs {
     const int32_t *tile_cnt;
     const long long *tile_off;
     int64_t tiles;
+    LeafArgs lv;
 };
 
 // nleft of each of the level's nodes: the left flags before its last slot's
@@ -161,6 +193,12 @@ __device__ void plan_level_block(DevNode *__restrict__ nodes, const PlanArgs &a)
         Rn.end = x.begin + x.nl + x.nr;
         rb += (unsigned long long)(x.nl <= x.nr ? x.nl : x.nr);
         ++nbuild;
+    }
+    if (a.lv.leaf) {
+        __syncthreads();  // every child's record is written
+        const int32_t eg = a.lv.e_dev[0], eh = a.lv.e_dev[1];
+        for (int32_t i = threadIdx.x; i < a.lv.n_nodes; i += T)
+            leaf_entry(nodes, i, eg, eh, a.lv.lambda, a.lv.eta, a.lv.leaf, a.lv.compact);
     }
     if (!a.plan) return;
     for (int d = 32; d > 0; d >>= 1) {

@@ -1258,9 +1258,10 @@ gbt_status split_columns(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page,
 gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int32_t *rows,
                               int64_t n, const int32_t *slot_node, int32_t *slot_node_out, DevNode *nodes,
                               int32_t *rows_out, const LevelChoice *choice, const SlotTable *stbl,
-                              const uint16_t *cols, const PlanArgs *plan)
+                              const uint16_t *cols, const PlanArgs *plan, bool order)
 {
     if (n == 0) return GBT_OK;
+    GBT_CHECK(order || plan, "a partition without the row order needs the plan");
     const SlotTable st = stbl ? *stbl : SlotTable{nullptr, nullptr, nullptr, 0, 0, 0};
     GBT_CHECK(n < ((int64_t)1 << 31) - 1, "partition of %lld rows (limit 2^31-2)", (long long)n);
     uint8_t *flags;
@@ -1284,7 +1285,9 @@ gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
         GBT_LAUNCHED();
     }
     const int32_t has_plan = plan ? 1 : 0;
-    k_part_scatter_rev<<<(unsigned)(tiles + has_plan), kPartThreads, 0, c->stream>>>(
+    // without the row order only the plan block runs (the left counts come
+    // from the flags pass)
+    k_part_scatter_rev<<<(unsigned)((order ? tiles : 0) + has_plan), kPartThreads, 0, c->stream>>>(
         rows, n, flags, tile_cnt, tile_off, slot_node, slot_node_out, nodes, rows_out, has_plan,
         plan ? *plan : PlanArgs{});
     GBT_LAUNCHED();

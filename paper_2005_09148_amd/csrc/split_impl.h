@@ -89,7 +89,8 @@ struct PlanArgs;
 // in reverse slot order; nodes[id].nleft (zero before the call) receives
 // each splitting node's left count (pleft is not written).  Two kernels;
 // with `plan`, the second also runs the level's plan (plan_impl.h) in one
-// of its blocks.  With `choice`, the split
+// of its blocks; `order` false (only with a plan) skips the rows' new order
+// (rows_out and slot_node_out are not written) and runs the plan alone.  With `choice`, the split
 // records of the level's nodes are chosen from the candidates and written
 // by the first kernel (instead of by eval_reduce_impl).  With `stbl` (a
 // sparse page's slot table), the search for a row's split feature looks
@@ -101,7 +102,7 @@ gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
                               int64_t n, const int32_t *slot_node, int32_t *slot_node_out, DevNode *nodes,
                               int32_t *rows_out, const LevelChoice *choice = nullptr,
                               const SlotTable *stbl = nullptr, const uint16_t *cols = nullptr,
-                              const PlanArgs *plan = nullptr);
+                              const PlanArgs *plan = nullptr, bool order = true);
 
 // Whether a page of mx's geometry takes a column copy (dense, symbols of at
 // most 16 bits).

@@ -374,29 +374,14 @@ __global__ void k_tree_init(DevNode *__restrict__ nodes, int32_t n_nodes, const 
     }
 }
 
-// Eq. 6 scaled by the learning rate, for every present node that does not
-// split: leaf = (float)((-G/(H+lambda)) * eta).
-__device__ inline float leaf_of(long long Qg, long long Qh, int32_t eg, int32_t eh, double lambda,
-                                double eta)
-{
-    double G = ldexp((double)Qg, -eg), H = ldexp((double)Qh, -eh);
-    double w = -G / (H + lambda);
-    return (float)(w * eta);
-}
-
-// Leaf values, and the compact form of the tree used by the row walk:
-// {feature, split_bin << 2 | default_left << 1 | splits} per node.
+// Leaf values and the compact tree, when the last level's plan did not make
+// them (no level, or no rows).
 __global__ void k_leaves(const DevNode *__restrict__ nodes, int32_t n_nodes, const int32_t *__restrict__ e_dev,
                          double lambda, double eta, float *__restrict__ leaf, uint2 *__restrict__ compact)
 {
     int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n_nodes) return;
-    const int32_t eg = e_dev[0], eh = e_dev[1];
-    const DevNode d = nodes[i];
-    leaf[i] = (d.present && !d.split) ? leaf_of(d.sum_g, d.sum_h, eg, eh, lambda, eta) : 0.0f;
-    compact[i] = d.split ? make_uint2((uint32_t)d.feature, ((uint32_t)d.split_bin << 2) |
-                                                               ((d.default_left ? 1u : 0u) << 1) | 1u)
-                         : make_uint2(0u, 0u);
+    leaf_entry(nodes, i, e_dev[0], e_dev[1], lambda, eta, leaf, compact);
 }
 
 // What the host reads after a tree, written by the device into pinned memory.
@@ -411,28 +396,37 @@ struct TreeResult {
 };
 
 // The tree in its public form (threshold = the split's cut value) and the
-// call's counters.
-__global__ void k_finalize(const DevNode *__restrict__ nodes, int32_t n_nodes, const float *__restrict__ leaf,
-                           const int32_t *__restrict__ cut_ptr, const float *__restrict__ cut_values,
-                           const SampleState *__restrict__ st, const unsigned long long *__restrict__ upd,
-                           const unsigned long long *__restrict__ stat, TreeResult *__restrict__ out)
+// call's counters, written into the host's pinned result.
+struct FinalizeArgs {
+    const DevNode *nodes;
+    int32_t n_nodes;
+    int32_t pad0;
+    const float *leaf;
+    const int32_t *cut_ptr;
+    const float *cut_values;
+    const SampleState *st;
+    const unsigned long long *upd;
+    const unsigned long long *stat;
+    TreeResult *out;
+};
+
+__device__ inline void finalize_entry(const FinalizeArgs &a, int32_t i)
 {
-    const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i == 0) {
         unsigned long long u = 0;
-        if (upd)
-            for (int k = 0; k < kUpdCounters; ++k) u += upd[k * kUpdStride];
-        out->updates = u;
-        out->rows_built = stat[0];
-        out->built = stat[1];
-        out->T = st->T;
-        out->e_key = st->e_key;
-        out->e_g = st->e_g;
-        out->e_h = st->e_h;
-        out->bad = st->bad;
+        if (a.upd)
+            for (int k = 0; k < kUpdCounters; ++k) u += a.upd[k * kUpdStride];
+        a.out->updates = u;
+        a.out->rows_built = a.stat[0];
+        a.out->built = a.stat[1];
+        a.out->T = a.st->T;
+        a.out->e_key = a.st->e_key;
+        a.out->e_g = a.st->e_g;
+        a.out->e_h = a.st->e_h;
+        a.out->bad = a.st->bad;
     }
-    if (i >= n_nodes) return;
-    const DevNode d = nodes[i];
+    if (i >= a.n_nodes) return;
+    const DevNode d = a.nodes[i];
     gbt_node o;
     memset(&o, 0, sizeof(o));
     if (d.present) {
@@ -443,17 +437,22 @@ __global__ void k_finalize(const DevNode *__restrict__ nodes, int32_t n_nodes, c
         if (d.split) {
             o.feature = d.feature;
             o.split_bin = d.split_bin;
-            o.threshold = cut_values[cut_ptr[d.feature] + d.split_bin - 1];
+            o.threshold = a.cut_values[a.cut_ptr[d.feature] + d.split_bin - 1];
             o.gain = d.gain;
             if (d.default_left) o.flags |= GBT_NODE_DEFAULT_LEFT;
         } else {
             o.feature = -1;
             o.split_bin = -1;
             o.flags |= GBT_NODE_LEAF;
-            o.leaf_value = leaf[i];
+            o.leaf_value = a.leaf[i];
         }
     }
-    out->nodes[i] = o;  // absent nodes stay all zero
+    a.out->nodes[i] = o;  // absent nodes stay all zero
+}
+
+__global__ void k_finalize(FinalizeArgs a)
+{
+    finalize_entry(a, (int32_t)(blockIdx.x * blockDim.x + threadIdx.x));
 }
 
 // Margin update from the final node of each training slot (no sampling:
@@ -576,8 +575,14 @@ template <int kQ>
 __global__ void __launch_bounds__(kWalkTileRows)
     k_margin_walk_pf(const uint32_t *__restrict__ words, int64_t rows, Geo geo,
                      const uint2 *__restrict__ compact, const float *__restrict__ leaf, int32_t nn,
-                     float *__restrict__ margin)
+                     float *__restrict__ margin, int32_t fin_blocks, FinalizeArgs fa)
 {
+    // the last fin_blocks blocks write the tree's host result instead
+    const uint32_t walk_blocks = gridDim.x - (uint32_t)fin_blocks;
+    if (blockIdx.x >= walk_blocks) {
+        finalize_entry(fa, (int32_t)((blockIdx.x - walk_blocks) * blockDim.x + threadIdx.x));
+        return;
+    }
     extern __shared__ uint32_t walk_lds[];
     uint2 *tn = (uint2 *)walk_lds;
     float *tl = (float *)(tn + nn);
@@ -606,7 +611,7 @@ __global__ void __launch_bounds__(kWalkTileRows)
     };
     int64_t tile = blockIdx.x;
     if (tile < n_tiles) load(tile);
-    for (; tile < n_tiles; tile += gridDim.x) {
+    for (; tile < n_tiles; tile += walk_blocks) {
         const int64_t r0 = tile * kWalkTileRows;
         const int32_t nr = (int32_t)min((int64_t)kWalkTileRows, rows - r0);
         __syncthreads();  // the previous tile's rows are consumed (and the tree is loaded)
@@ -621,7 +626,7 @@ __global__ void __launch_bounds__(kWalkTileRows)
         }
         const float m = mnext;
         __syncthreads();
-        if (tile + gridDim.x < n_tiles) load(tile + gridDim.x);
+        if (tile + walk_blocks < n_tiles) load(tile + walk_blocks);
         if ((int32_t)threadIdx.x < nr) {
             const uint32_t *row = rb + threadIdx.x * ps;
             int32_t id = 0;
@@ -647,14 +652,15 @@ __global__ void __launch_bounds__(kWalkTileRows)
     }
 }
 
+// grid walk blocks, then fin_blocks blocks of the tree's host result (fa)
 static void launch_walk_pf(gbt_ctx *c, int q4, unsigned grid, size_t lds_bytes, const uint32_t *words,
                            int64_t rows, const Geo &geo, const uint2 *compact, const float *leaf, int32_t nn,
-                           float *margin)
+                           float *margin, int32_t fin_blocks, const FinalizeArgs &fa)
 {
 #define GBT_WALK_PF(Q)                                                                                         \
     case Q:                                                                                                    \
-        k_margin_walk_pf<Q><<<grid, kWalkTileRows, lds_bytes, c->stream>>>(words, rows, geo, compact, leaf, nn, \
-                                                                            margin);                           \
+        k_margin_walk_pf<Q><<<grid + (unsigned)fin_blocks, kWalkTileRows, lds_bytes, c->stream>>>(              \
+            words, rows, geo, compact, leaf, nn, margin, fin_blocks, fa);                                      \
         break;
     switch (q4) {
         GBT_WALK_PF(1)
@@ -1000,16 +1006,29 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
             timer_end(c, mark);
         }
     }
+    // the walk's compact tree and the leaf values: made by the last level's
+    // plan (by k_leaves when there is no level or no row)
+    uint2 *compact;
+    GBT_TRY(scratch_t(c, kScrCompact, (size_t)NN, &compact));
+    const bool leaves_in_plan = D > 0 && R > 0;
+    // the rows' final slots give their leaves (below) only on sparse pages
+    // that are the data's own page; otherwise nothing reads the last
+    // level's row order and its partition only counts
+    const bool final_order = so.alias && mx->sparse;
     for (int32_t d = 0; d < D; ++d) {
         const int32_t maxn = (int32_t)std::min<int64_t>((int64_t)1 << d, max_level_nodes);
         mark = timer_begin(c, kPhSplit);
         if (!fused && R > 0) GBT_TRY(eval_impl(c, mx, histA, evA, maxn, ep, splits_d, cntA, nodes));
         const LevelChoice lc{cand, mx->m, (int32_t)((1u << d) - 1), (int32_t)((2u << d) - 1)};
         const bool plan_next = d + 1 < D && R > 0;
-        // the partition's second kernel also plans the next level
-        const PlanArgs pa{evA, cntA, plan_next ? 1 : 0, items, evB, cntB, work_d, cnt + 2, red_d, cnt + 3, stat};
+        // the partition's second kernel also plans the next level (and
+        // after the last level makes the leaves)
+        const bool last = d + 1 == D;
+        PlanArgs pa{evA, cntA, plan_next ? 1 : 0, items, evB, cntB, work_d, cnt + 2, red_d, cnt + 3, stat};
+        if (last) pa.lv = LeafArgs{leaf, compact, e_dev, p->lambda, p->eta, NN, 0};
         GBT_TRY(partition_rev_impl(c, mx, so.page, rows, R, slot_node, slot_tmp, nodes, rows_tmp,
-                                   choose ? &lc : nullptr, stbl.row ? &stbl : nullptr, cols, &pa));
+                                   choose ? &lc : nullptr, stbl.row ? &stbl : nullptr, cols, &pa,
+                                   !last || final_order));
         std::swap(rows, rows_tmp);
         std::swap(slot_node, slot_tmp);
         timer_end(c, mark);
@@ -1035,14 +1054,23 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     }
     // ---- leaves and the margin update of all n rows (Eq. 1)
     mark = timer_begin(c, kPhMargin);
-    uint2 *compact;
-    GBT_TRY(scratch_t(c, kScrCompact, (size_t)NN, &compact));
-    k_leaves<<<blocks(NN), 256, 0, c->stream>>>(nodes, NN, e_dev, p->lambda, p->eta, leaf, compact);
-    GBT_LAUNCHED();
+    if (!leaves_in_plan) {
+        k_leaves<<<blocks(NN), 256, 0, c->stream>>>(nodes, NN, e_dev, p->lambda, p->eta, leaf, compact);
+        GBT_LAUNCHED();
+    }
+    // the tree and the counters: written by the device into pinned memory,
+    // read after the one synchronization of the call; with the dense walk,
+    // by two more blocks of its first launch
+    void *hio, *hio_d;
+    const size_t res_bytes = sizeof(TreeResult) + (size_t)NN * sizeof(gbt_node);
+    GBT_TRY(host_io(c, res_bytes, &hio, &hio_d));
+    const FinalizeArgs fa{nodes, NN, 0, leaf, mx->cut_ptr_d, mx->cut_values_d, so.st, upd, stat,
+                          (TreeResult *)hio_d};
+    bool finalized = false;
     // the rows' final slots give their leaves when every row trained; on
     // dense pages the walk of the page in row order is cheaper than adding
     // into the margins at the slots' (scattered) rows
-    if (so.alias && mx->sparse) {
+    if (final_order) {
         if (n) {
             k_margin_slots<<<blocks(n), 256, 0, c->stream>>>(margin, rows, slot_node, leaf, n);
             GBT_LAUNCHED();
@@ -1059,7 +1087,10 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
                 if (q4 <= 8 && NN <= kWalkLdsNodes && lds_bytes <= 64 * 1024) {
                     int64_t tiles = (rows_n + kWalkTileRows - 1) / kWalkTileRows;
                     unsigned grid = (unsigned)tiles;
-                    launch_walk_pf(c, q4, grid, lds_bytes, words, rows_n, geo, compact, leaf, NN, margin + row0);
+                    const int32_t fin = finalized ? 0 : (int32_t)blocks(NN);
+                    launch_walk_pf(c, q4, grid, lds_bytes, words, rows_n, geo, compact, leaf, NN, margin + row0,
+                                   fin, fa);
+                    finalized = true;
                 } else if (geo.row_words <= kWalkMaxWords && NN <= kWalkLdsNodes && lds_bytes <= 64 * 1024) {
                     int64_t tiles = (rows_n + kWalkTileRows - 1) / kWalkTileRows;
                     unsigned grid = (unsigned)std::min<int64_t>(tiles, 4 * kCUs);
@@ -1077,14 +1108,10 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
             &h2d));
     }
     timer_end(c, mark);
-    // ---- the tree and the counters: written by the device into pinned
-    // memory, read after the one synchronization of the call
-    void *hio, *hio_d;
-    const size_t res_bytes = sizeof(TreeResult) + (size_t)NN * sizeof(gbt_node);
-    GBT_TRY(host_io(c, res_bytes, &hio, &hio_d));
-    k_finalize<<<blocks(NN), 256, 0, c->stream>>>(nodes, NN, leaf, mx->cut_ptr_d, mx->cut_values_d, so.st, upd,
-                                                  stat, (TreeResult *)hio_d);
-    GBT_LAUNCHED();
+    if (!finalized) {
+        k_finalize<<<blocks(NN), 256, 0, c->stream>>>(fa);
+        GBT_LAUNCHED();
+    }
     GBT_HIP(hipStreamSynchronize(c->stream));
     const TreeResult *res = (const TreeResult *)hio;
     if (res->bad) return set_error(GBT_E_INVALID, "sampling failed (state flags %u)", res->bad);
@@ -1541,8 +1568,8 @@ static gbt_status train_tree_naive_impl(gbt_ctx *c, const gbt_matrix *mx, const 
     GBT_LAUNCHED();
     void *hio, *hio_d;
     GBT_TRY(host_io(c, sizeof(TreeResult) + (size_t)NN * sizeof(gbt_node), &hio, &hio_d));
-    k_finalize<<<blocks(NN), 256, 0, c->stream>>>(nodes, NN, leaf, mx->cut_ptr_d, mx->cut_values_d, st, upd,
-                                                  stat, (TreeResult *)hio_d);
+    k_finalize<<<blocks(NN), 256, 0, c->stream>>>(
+        FinalizeArgs{nodes, NN, 0, leaf, mx->cut_ptr_d, mx->cut_values_d, st, upd, stat, (TreeResult *)hio_d});
     GBT_LAUNCHED();
     GBT_HIP(hipStreamSynchronize(c->stream));
     const TreeResult *res = (const TreeResult *)hio;
