@@ -96,6 +96,11 @@ struct gbt_ctx {
     // pinned buffers that disk pages are read into before their copy
     void *disk_stage[2] = {nullptr, nullptr};
     size_t disk_stage_bytes = 0;
+    // the MVS key exponent of the last tree with sampling, for its row
+    // count and lambda (the next tree's gradient pass guesses it)
+    int32_t key_e_last = 0;
+    int64_t key_n_last = -1;
+    double key_lambda_last = 0.0;
 };
 
 namespace gbt {

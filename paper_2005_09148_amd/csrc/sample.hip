@@ -253,11 +253,22 @@ __global__ void __launch_bounds__(256) k_mvs_keys(SampleSrc src, int64_t n, doub
 
 // Closed form when T* exceeds every key; otherwise the radix descent
 // starts on [0, 2^S) with 2^S > amax + 1.  done_host (pinned host memory,
-// may be NULL) receives 1 for the closed form, else 0.
+// may be NULL) receives 1 for the closed form, else 0.  check_log2n >= 0:
+// the key sums were formed with the exponent in st->e_key, which is first
+// checked against the one max r gives (e = 62 - E - check_log2n); when they
+// differ nothing else is done and done_host receives 2.
 __global__ void k_mvs_thresh_init(SampleState *__restrict__ st, int64_t K, int32_t *__restrict__ done_host,
-                                  int32_t count_mode)
+                                  int32_t count_mode, int32_t check_log2n)
 {
     if (threadIdx.x != 0) return;
+    if (check_log2n >= 0) {
+        int E;
+        frexp(sqrt(__longlong_as_double(fold_max(st->rmax))), &E);
+        if (62 - E - check_log2n != st->e_key) {
+            if (done_host) __hip_atomic_store(done_host, 2, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+            return;
+        }
+    }
     unsigned long long amax = fold_max(st->amax), asum = fold_sum(st->asum);
     st->C_above = 0;
     st->F_below = 0;
@@ -631,13 +642,16 @@ __global__ void __launch_bounds__(256)
     }
 }
 
+// kSpec: also the keys' maximum and sum with the key exponent e_spec (the
+// keys pass's, when e_spec turns out to be the exponent it would take).
+template <bool kSpec>
 __global__ void __launch_bounds__(256) k_gradients_rmax(int32_t loss, const float *__restrict__ margin,
                                                         const float *__restrict__ label, int64_t n,
                                                         float2 *__restrict__ gpair, double lambda,
-                                                        SampleState *__restrict__ st)
+                                                        SampleState *__restrict__ st, int32_t e_spec)
 {
     __shared__ unsigned long long lds4[4];
-    unsigned long long b = 0;
+    unsigned long long b = 0, amx = 0, asm_ = 0;
     bool bad = false;
     auto one = [&](float m, float y, float2 *out) {
         double g, h;
@@ -648,6 +662,11 @@ __global__ void __launch_bounds__(256) k_gradients_rmax(int32_t loss, const floa
         bad |= !(x <= 1.7976931348623157e308);  // NaN or infinite
         const unsigned long long xb = __double_as_longlong(x);
         b = xb > b ? xb : b;
+        if (kSpec) {
+            const unsigned long long a = (unsigned long long)(long long)rint(ldexp(mvs_r((double)p.x, (double)p.y, lambda), e_spec));
+            amx = a > amx ? a : amx;
+            asm_ += a;
+        }
     };
     const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x, step = (int64_t)gridDim.x * blockDim.x;
     if (((uintptr_t)margin & 7u) == 0 && ((uintptr_t)label & 7u) == 0 && ((uintptr_t)gpair & 15u) == 0) {
@@ -667,6 +686,24 @@ __global__ void __launch_bounds__(256) k_gradients_rmax(int32_t loss, const floa
     if (bad) atomicOr(&st->bad, 1u);
     b = block_max_u64(b, lds4);
     if (threadIdx.x == 0 && b) atomicMax(spread_at(st->rmax, blockIdx.x), b);
+    if (kSpec) {
+        amx = block_max_u64(amx, lds4);
+        asm_ = block_sum_u64(asm_, lds4);
+        if (threadIdx.x == 0) {
+            if (amx) atomicMax(spread_at(st->amax, blockIdx.x), amx);
+            if (asm_) atomicAdd(spread_at(st->asum, blockIdx.x), asm_);
+            if (blockIdx.x == 0) st->e_key = e_spec;
+        }
+    }
+}
+
+// The keys' maximum and sum cleared (a speculated exponent was wrong).
+__global__ void k_keys_reset(SampleState *__restrict__ st)
+{
+    for (int t = threadIdx.x; t < kSpread * kLineWords; t += blockDim.x) {
+        (&st->amax[0][0])[t] = 0ull;
+        (&st->asum[0][0])[t] = 0ull;
+    }
 }
 
 // ------------------------------------------------------------ fixed point
@@ -801,8 +838,10 @@ static int32_t log2_ceil(int64_t v) { return v <= 1 ? 0 : ceil_log2_u64((uint64_
 // ------------------------------------------------------------ drivers
 gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
                          double lambda, int64_t K, SampleState *st, bool skip_closed, bool rmax_done,
-                         bool count_mode)
+                         bool count_mode, bool keys_spec)
 {
+    GBT_CHECK(!keys_spec || (skip_closed && rmax_done && !keys && !count_mode),
+              "speculated key sums need the host's closed-form test");
     int32_t l2 = log2_ceil(n);
     unsigned long long *hist = nullptr;
     GBT_TRY(scratch_t(c, kScrMisc, 2 * kDigitBuckets, &hist));
@@ -814,12 +853,17 @@ gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64
         else
             k_mvs_rmax<kSrcMargin><<<rblocks(n), 256, 0, c->stream>>>(src, n, lambda, st);
         GBT_LAUNCHED();
+    }
+    auto keys_pass = [&]() -> gbt_status {
         if (kind == kSrcGpair)
             k_mvs_keys<kSrcGpair><<<rblocks(n), 256, 0, c->stream>>>(src, n, lambda, l2, st, (int64_t *)keys);
         else
             k_mvs_keys<kSrcMargin><<<rblocks(n), 256, 0, c->stream>>>(src, n, lambda, l2, st, (int64_t *)keys);
         GBT_LAUNCHED();
-    }
+        return GBT_OK;
+    };
+    // speculated: the gradient pass summed the keys with a guessed exponent
+    if (n > 0 && !keys_spec) GBT_TRY(keys_pass());
     // skip_closed: the host learns from pinned memory whether the closed form
     // holds (it waits for the passes above, nothing else is queued) and then
     // launches no descent levels, which would all return at once
@@ -832,15 +876,29 @@ gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64
         done_dev = (int32_t *)hio_d;
         *done_poll = -1;
     }
-    k_mvs_thresh_init<<<1, 64, 0, c->stream>>>(st, K, done_dev, count_mode ? 1 : 0);
-    GBT_LAUNCHED();
-    if (done_poll) {
+    auto wait_flag = [&]() -> gbt_status {
         const auto t0 = std::chrono::steady_clock::now();
         for (uint32_t spin = 0; *done_poll < 0; ++spin) {
             if ((spin & 1023u) == 0 && std::chrono::steady_clock::now() - t0 > std::chrono::seconds(2)) {
                 GBT_HIP(hipStreamSynchronize(c->stream));  // the flag is written by then
                 break;
             }
+        }
+        return GBT_OK;
+    };
+    k_mvs_thresh_init<<<1, 64, 0, c->stream>>>(st, K, done_dev, count_mode ? 1 : 0, keys_spec && n > 0 ? l2 : -1);
+    GBT_LAUNCHED();
+    if (done_poll) {
+        GBT_TRY(wait_flag());
+        if (*done_poll == 2) {
+            // the guessed exponent was not the keys': the keys pass after all
+            k_keys_reset<<<1, 256, 0, c->stream>>>(st);
+            GBT_LAUNCHED();
+            GBT_TRY(keys_pass());
+            *done_poll = -1;
+            k_mvs_thresh_init<<<1, 64, 0, c->stream>>>(st, K, done_dev, count_mode ? 1 : 0, -1);
+            GBT_LAUNCHED();
+            GBT_TRY(wait_flag());
         }
         if (*done_poll == 1) return GBT_OK;
     }
@@ -890,10 +948,15 @@ gbt_status gw_all(gbt_ctx *c, const float *gpair, int64_t n, double *gw)
 }
 
 gbt_status gradients_rmax(gbt_ctx *c, int32_t loss, const float *margin, const float *label, int64_t n,
-                          float *gpair, double lambda, SampleState *st)
+                          float *gpair, double lambda, SampleState *st, int32_t e_spec)
 {
     if (n == 0) return GBT_OK;
-    k_gradients_rmax<<<rblocks(n), 256, 0, c->stream>>>(loss, margin, label, n, (float2 *)gpair, lambda, st);
+    if (e_spec == kNoKeySpec)
+        k_gradients_rmax<false><<<rblocks(n), 256, 0, c->stream>>>(loss, margin, label, n, (float2 *)gpair, lambda,
+                                                                   st, 0);
+    else
+        k_gradients_rmax<true><<<rblocks(n), 256, 0, c->stream>>>(loss, margin, label, n, (float2 *)gpair, lambda,
+                                                                  st, e_spec);
     GBT_LAUNCHED();
     return GBT_OK;
 }

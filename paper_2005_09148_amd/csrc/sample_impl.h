@@ -90,9 +90,12 @@ gbt_status state_init(gbt_ctx *c, SampleState *st);
 // used).
 // count_mode (GOSS): K is the top count A, and T in st becomes the A-th
 // largest key (INT64_MAX when A = 0) instead of the MVS threshold.
+// keys_spec (with skip_closed and rmax_done): the key maximum and sum are
+// already in st, formed by gradients_rmax with a guessed exponent; the
+// threshold pass checks it and runs the keys pass only when it was wrong.
 gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
                          double lambda, int64_t K, SampleState *st, bool skip_closed,
-                         bool rmax_done = false, bool count_mode = false);
+                         bool rmax_done = false, bool count_mode = false, bool keys_spec = false);
 // Keep flags of rows [0, n) and, when tile_cnt is given, the kept count of
 // each tile of kCompactTile rows.
 gbt_status mvs_select(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
@@ -107,9 +110,12 @@ gbt_status lambda_sums(gbt_ctx *c, int32_t loss, const float *margin, const floa
 // fx_max_done: the maxima of |g'| and |h'| are already in st (fused upstream)
 gbt_status fixed_point(gbt_ctx *c, const double *gw, int64_t R, SampleState *st, int64_t *q,
                        bool fx_max_done = false);
-// Gradients of all rows and, fused, the maximum of r^2 = g^2 + lambda h^2.
+// Gradients of all rows and, fused, the maximum of r^2 = g^2 + lambda h^2;
+// with e_spec (not kNoKeySpec) also the MVS keys' maximum and sum with that
+// key exponent, st->e_key = e_spec (to be checked by mvs_threshold).
+constexpr int32_t kNoKeySpec = -0x7fffffff;
 gbt_status gradients_rmax(gbt_ctx *c, int32_t loss, const float *margin, const float *label, int64_t n,
-                          float *gpair, double lambda, SampleState *st);
+                          float *gpair, double lambda, SampleState *st, int32_t e_spec = kNoKeySpec);
 // Exclusive per-tile offsets from the per-tile counts mvs_select wrote into
 // tile_off (tiles of kCompactTile rows), and the total at tile_off[tiles]
 // (and at *total_host, pinned host memory, when given).

@@ -219,7 +219,8 @@ static double sample_lambda(const gbt_sample_params &sp)
 // stay in o->st on the device.
 gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, const float *margin,
                       const float *label, const gbt_sample_params &sp, Buffers &bufs, SampleOut *o,
-                      double *h2d_bytes, SampleState *st_ready = nullptr, bool read_state = true)
+                      double *h2d_bytes, SampleState *st_ready = nullptr, bool read_state = true,
+                      bool keys_spec = false)
 {
     const int64_t n = mx->n_rows;
     GBT_CHECK(sp.f > 0.0 && sp.f <= 1.0, "sampling fraction %g outside (0, 1]", sp.f);
@@ -265,7 +266,8 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
             rule = SampleRule{GBT_SAMPLE_GOSS, p >= 1.0 ? 1 : 0, p >= 1.0 ? 0 : draw_limit(p), (1.0 - a) / b};
         } else if (sp.f < 1.0) {
             o->K = std::max<int64_t>(1, (int64_t)std::nearbyint(sp.f * (double)n));
-            GBT_TRY(mvs_threshold(c, src, kind, nullptr, n, lam, o->K, st, true, st_ready != nullptr));
+            GBT_TRY(mvs_threshold(c, src, kind, nullptr, n, lam, o->K, st, true, st_ready != nullptr, false,
+                                  keys_spec && st_ready != nullptr));
         }
         // with f = 1 the state keeps T = 0: every row is kept with weight 1
         GBT_TRY(mvs_select(c, src, kind, nullptr, n, lam, st, sp.seed, sp.iteration, 0, keep, tile_off, rule));
@@ -844,20 +846,28 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     float *gpair = nullptr;
     SampleState *st_ready = nullptr;
     const gbt_sample_params sp{p->f, p->mvs_lambda, p->seed, p->iteration, p->loss, p->sampler, p->goss_a};
+    // MVS: the gradient pass sums the keys with the last tree's exponent, a
+    // guess checked before the threshold is taken (the keys pass runs only
+    // when it was wrong)
+    const bool mvs = p->f < 1.0 && p->sampler == GBT_SAMPLE_MVS;
+    int32_t e_spec = kNoKeySpec;
+    if (mvs && c->key_n_last == n && c->key_lambda_last == sample_lambda(sp)) e_spec = c->key_e_last;
+    c->key_n_last = -1;  // set again when this tree has finished
     if (!host_pages) {
         GBT_TRY(scratch_t(c, kScrGpair, (size_t)std::max<int64_t>(n, 1) * 2, &gpair));
         if (p->f < 1.0) {
             // the gradient pass also folds the maximum of r for the sampling keys
             GBT_TRY(scratch_t(c, kScrState, 1, &st_ready));
             GBT_TRY(state_init(c, st_ready));
-            GBT_TRY(gradients_rmax(c, p->loss, margin, label, n, gpair, sample_lambda(sp), st_ready));
+            GBT_TRY(gradients_rmax(c, p->loss, margin, label, n, gpair, sample_lambda(sp), st_ready, e_spec));
         } else {
             GBT_TRY(launch_gradients(c, p->loss, margin, label, nullptr, n, gpair));
         }
     }
     Buffers bufs{c, false, {}};
     SampleOut so;
-    GBT_TRY(sample_run(c, mx, gpair, margin, label, sp, bufs, &so, &h2d, st_ready, false));
+    GBT_TRY(sample_run(c, mx, gpair, margin, label, sp, bufs, &so, &h2d, st_ready, false,
+                       st_ready != nullptr && e_spec != kNoKeySpec));
     timer_end(c, mark);
     const int64_t R = so.R;
     const int32_t *e_dev = &so.st->e_g;  // {e_g, e_h} on the device
@@ -1115,6 +1125,11 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     GBT_HIP(hipStreamSynchronize(c->stream));
     const TreeResult *res = (const TreeResult *)hio;
     if (res->bad) return set_error(GBT_E_INVALID, "sampling failed (state flags %u)", res->bad);
+    if (mvs) {
+        c->key_e_last = res->e_key;
+        c->key_n_last = n;
+        c->key_lambda_last = sample_lambda(sp);
+    }
     tree->exp_g = res->e_g;
     tree->exp_h = res->e_h;
     memcpy(tree->nodes, res->nodes, (size_t)NN * sizeof(gbt_node));

@@ -859,3 +859,31 @@ def test_budget_is_enforced(gbt):
         gbt.gbt_quantize(small, d["X"])
     assert e.value.code == gbt.GBT_E_BUDGET
     small.close()
+
+
+def test_mvs_key_exponent_guess_both_ways(gbt, ctx):
+    """The gradient pass sums the MVS keys with the last tree's key exponent
+    (same row count and lambda), a guess checked before the threshold is
+    taken.  Labels scaled by 1000 between two trees move the largest r by
+    about 2^10, so the second tree's guess is wrong and the keys pass runs
+    after all; the third guesses right.  Every tree equals the oracle's."""
+    cfg = datagen.CONFIGS[3]
+    d = datagen.config3(n=40_000)
+    X, y = d["X"], d["y"]
+    _, b, _, _ = oracle_quantize(X, cfg.max_bin)
+    mx = gbt.gbt_quantize(ctx, X, max_bin=cfg.max_bin)
+    kw = dict(loss=cfg.loss, max_depth=6, eta=0.3, f=0.2, mvs_lambda=0.5, seed=11)
+    P = gbt.make_train_params(**kw)
+    OP = orc.Params(**kw)
+    for it, scale in enumerate([1.0, 1000.0, 1000.0]):
+        ys = (y * np.float32(scale)).astype(np.float32)
+        margin = np.zeros(len(ys), np.float32)
+        mg = torch.from_numpy(margin.copy()).cuda()
+        P.iteration = it
+        t = gbt.gbt_train_tree(ctx, mx, torch.from_numpy(ys).cuda(), mg, P)
+        o = orc.train_tree(b, ys, margin, OP, iteration=it)
+        dd = node_diff(t.nodes, o.nodes)
+        assert dd is None, f"tree {it} node {dd[0]}"
+        assert t.stats.threshold == o.info.T
+        assert same_bits(mg.cpu().numpy(), margin)
+    mx.free()
