@@ -13,8 +13,8 @@ partitions), the leaves and the margin update of all 10M rows.
 Prints one JSON line: value = histogram row-feature updates performed per
 second of step time (G/s); ms_per_step is seconds per tree x 1000 (the timed
 trees carry no events); roofline is that of the histogram kernel
-(algorithmic bytes / its HIP-event time, the events around every histogram
-launch of as many further timed trees);
+(algorithmic bytes / its HIP-event time: every histogram launch of as many
+further timed trees fills two events with its own start and end);
 cpu_baseline times the CPU oracle (its OpenMP build, on the threads the
 process is given, and the first tree again in one thread) on the first trees
 of the same workload on the host and reports the same unit.
@@ -468,9 +468,9 @@ def main():
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     print(f"[bench] {args.steps} trees in {dt:.3f} s", file=sys.stderr, flush=True)
-    # the histogram kernel's launch time: HIP events on the compute stream
-    # around every histogram launch, over as many further timed trees of the
-    # same workload
+    # the histogram kernel's launch time: every histogram launch fills a pair
+    # of HIP events on the compute stream with its own start and end, over as
+    # many further timed trees of the same workload
     ctx.set_timing(1)
     estats = []
     t1 = time.perf_counter()
@@ -541,8 +541,9 @@ def main():
                      "kernel": kernel, "launches": launches,
                      "avg_launch_us": round(hms * 1e3 / max(launches, 1), 2),
                      "algorithmic_bytes_per_launch": hbytes // max(launches, 1),
-                     "timing": f"HIP events around each histogram launch over {args.steps} further timed "
-                               f"trees ({round(dt_ev * 1e3 / args.steps, 4)} ms per tree with the events)"},
+                     "timing": f"start and end events of every histogram launch, filled by the launch itself "
+                               f"(hipExtLaunchKernel), over {args.steps} further timed trees "
+                               f"({round(dt_ev * 1e3 / args.steps, 4)} ms per tree with the events)"},
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(X, y, cfg, args.cpu_trees, first_trees, first_updates, sampler)

@@ -110,6 +110,10 @@ namespace gbt {
 enum Phase { kPhSample = 0, kPhHist, kPhHistAux, kPhSplit, kPhMargin, kPhCount };
 int timer_begin(gbt_ctx *c, int phase);   // -1 when timing is off
 void timer_end(gbt_ctx *c, int mark);
+// A mark whose two events one kernel launch fills itself (its start and end
+// timestamps, hipExtLaunchKernel): no timer_end.
+int timer_begin_launch(gbt_ctx *c, int phase);
+void timer_events(gbt_ctx *c, int mark, hipEvent_t *a, hipEvent_t *b);
 void timer_collect(gbt_ctx *c, double *ms_per_phase);  // adds, then resets
 
 gbt_status dev_alloc(gbt_ctx *c, size_t bytes, void **p);

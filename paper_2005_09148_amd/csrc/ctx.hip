@@ -156,6 +156,21 @@ int timer_begin(gbt_ctx *c, int phase)
     return (int)c->marks.size() - 1;
 }
 
+int timer_begin_launch(gbt_ctx *c, int phase)
+{
+    if (c->timing == 0 || (c->timing == 1 && phase != kPhHist)) return -1;
+    int a = next_event(c), b = next_event(c);
+    if (a < 0 || b < 0) return -1;
+    c->marks.push_back({a, b, phase});
+    return (int)c->marks.size() - 1;
+}
+
+void timer_events(gbt_ctx *c, int mark, hipEvent_t *a, hipEvent_t *b)
+{
+    *a = c->events[c->marks[mark].a];
+    *b = c->events[c->marks[mark].b];
+}
+
 void timer_end(gbt_ctx *c, int mark)
 {
     if (mark < 0) return;

@@ -13,6 +13,8 @@
 // share its L2 for the gradient pairs and row ids.
 #include "hist_impl.h"
 
+#include <hip/hip_ext.h>
+
 #include <algorithm>
 #include <cstring>
 #include <mutex>
@@ -820,6 +822,21 @@ static gbt_status static_scratch(int device, HistWorkspace *ws)
     return GBT_OK;
 }
 
+// A histogram kernel launch on the context stream; with a timer mark the
+// launch fills the mark's events with its own start and end (the kernel's
+// time, without the dispatch around it).
+#define GBT_HIST_LAUNCH(KFN, GRID, BLOCK, LDS, ...)                                                       \
+    do {                                                                                                 \
+        if (mark >= 0) {                                                                                 \
+            hipEvent_t ev_a, ev_b;                                                                       \
+            timer_events(c, mark, &ev_a, &ev_b);                                                         \
+            hipExtLaunchKernelGGL(KFN, dim3(GRID), dim3(BLOCK), (uint32_t)(LDS), c->stream, ev_a, ev_b, 0u, \
+                                  __VA_ARGS__);                                                          \
+        } else {                                                                                         \
+            KFN<<<GRID, BLOCK, LDS, c->stream>>>(__VA_ARGS__);                                           \
+        }                                                                                                \
+    } while (0)
+
 gbt_status hist_launch_device(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int64_t *q,
                               const int32_t *rows, const HistLaunch &hl, const int64_t *parent_hist,
                               int64_t *hist, unsigned long long *upd)
@@ -834,20 +851,14 @@ gbt_status hist_launch_device(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
         const unsigned grid = (unsigned)((size_t)hl.max_work * (size_t)G);
         const size_t lds = (size_t)kRotBins * kRotCols * 16;
         const longlong2 *qq = (const longlong2 *)q;
-        const int mark = hl.timed ? timer_begin(c, kPhHist) : -1;
+        const int mark = hl.timed ? timer_begin_launch(c, kPhHist) : -1;
 #define GBT_HIST_ROT(WB)                                                                                 \
-    case WB:                                                                                             \
-        if (rows)                                                                                        \
-            k_hist_rot<WB, true><<<grid, kRotThreads, lds, c->stream>>>(page, mx->row_words, null_sym, qq, \
-                                                                       rows, hl.work, hl.groups, G,      \
-                                                                       hl.n_work_d, mx->bin_ptr_d, tb,   \
-                                                                       partials, upd);                   \
-        else                                                                                             \
-            k_hist_rot<WB, false><<<grid, kRotThreads, lds, c->stream>>>(page, mx->row_words, null_sym, qq, \
-                                                                        rows, hl.work, hl.groups, G,     \
-                                                                        hl.n_work_d, mx->bin_ptr_d, tb,  \
-                                                                        partials, upd);                  \
-        break;
+    case WB: {                                                                                           \
+        auto kfn = rows ? k_hist_rot<WB, true> : k_hist_rot<WB, false>;                                   \
+        GBT_HIST_LAUNCH(kfn, grid, kRotThreads, lds, page, mx->row_words, null_sym, qq, rows, hl.work,     \
+                        hl.groups, G, hl.n_work_d, mx->bin_ptr_d, tb, partials, upd);                    \
+        break;                                                                                           \
+    }
         switch (mx->w) {
             GBT_HIST_ROT(1)
             GBT_HIST_ROT(2)
@@ -863,38 +874,27 @@ gbt_status hist_launch_device(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
         }
 #undef GBT_HIST_ROT
         GBT_LAUNCHED();
-        timer_end(c, mark);
     } else if (hl.max_work > 0) {
         uint32_t null_sym = (mx->sparse || mx->has_missing) ? mx->null_sym : 0xffffffffu;
         uint32_t mask = mx->w >= 32 ? 0xffffffffu : ((1u << mx->w) - 1u);
         unsigned grid = (unsigned)((size_t)hl.max_work * (size_t)G);
-        const int mark = hl.timed ? timer_begin(c, kPhHist) : -1;
+        const int mark = hl.timed ? timer_begin_launch(c, kPhHist) : -1;
         if (mx->sparse) {
             size_t lds = (size_t)hl.max_groups_bins * 16;
-            if (rows)
-                k_hist_sparse<true><<<grid, kSparseThreads, lds, c->stream>>>(
-                    page, mx->row_words, mx->w, mask, mx->stride, (const longlong2 *)q, rows, hl.work, hl.groups,
-                    G, hl.n_work_d, tb, partials, upd, hl.slot_tbl, hl.tbl_stride);
-            else
-                k_hist_sparse<false><<<grid, kSparseThreads, lds, c->stream>>>(
-                    page, mx->row_words, mx->w, mask, mx->stride, (const longlong2 *)q, rows, hl.work, hl.groups,
-                    G, hl.n_work_d, tb, partials, upd, hl.slot_tbl, hl.tbl_stride);
+            auto kfn = rows ? k_hist_sparse<true> : k_hist_sparse<false>;
+            GBT_HIST_LAUNCH(kfn, grid, kSparseThreads, lds, page, mx->row_words, mx->w, mask, mx->stride,
+                            (const longlong2 *)q, rows, hl.work, hl.groups, G, hl.n_work_d, tb, partials, upd,
+                            hl.slot_tbl, hl.tbl_stride);
         } else {
             const size_t lds = (size_t)(kDenseBins + hl.max_groups_bins) * 8;
             const longlong2 *qq = (const longlong2 *)q;
 #define GBT_HIST_DENSE(WB)                                                                                  \
-    case WB:                                                                                                \
-        if (rows)                                                                                           \
-            k_hist_dense<WB, true><<<grid, kHistThreads, lds, c->stream>>>(page, mx->row_words, null_sym, qq, \
-                                                                          rows, hl.work, hl.groups, G,      \
-                                                                          hl.n_work_d, mx->bin_ptr_d, tb,   \
-                                                                          partials, upd);                   \
-        else                                                                                                \
-            k_hist_dense<WB, false><<<grid, kHistThreads, lds, c->stream>>>(page, mx->row_words, null_sym, qq, \
-                                                                           rows, hl.work, hl.groups, G,     \
-                                                                           hl.n_work_d, mx->bin_ptr_d, tb,  \
-                                                                           partials, upd);                  \
-        break;
+    case WB: {                                                                                              \
+        auto kfn = rows ? k_hist_dense<WB, true> : k_hist_dense<WB, false>;                                  \
+        GBT_HIST_LAUNCH(kfn, grid, kHistThreads, lds, page, mx->row_words, null_sym, qq, rows, hl.work,       \
+                        hl.groups, G, hl.n_work_d, mx->bin_ptr_d, tb, partials, upd);                       \
+        break;                                                                                              \
+    }
             switch (mx->w) {
                 GBT_HIST_DENSE(1)
                 GBT_HIST_DENSE(2)
@@ -912,7 +912,6 @@ gbt_status hist_launch_device(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
 #undef GBT_HIST_DENSE
         }
         GBT_LAUNCHED();
-        timer_end(c, mark);
     }
     if (hl.max_red > 0) {
         const int aux = hl.timed ? timer_begin(c, kPhHistAux) : -1;
