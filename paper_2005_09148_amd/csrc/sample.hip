@@ -836,72 +836,55 @@ static unsigned rblocks(int64_t n) { return std::max(1u, std::min(blocks(n), (un
 static int32_t log2_ceil(int64_t v) { return v <= 1 ? 0 : ceil_log2_u64((uint64_t)v); }
 
 // ------------------------------------------------------------ drivers
-gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
-                         double lambda, int64_t K, SampleState *st, bool skip_closed, bool rmax_done,
-                         bool count_mode, bool keys_spec)
+namespace {
+
+void keys_pass(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n, double lambda,
+               int32_t l2, SampleState *st)
 {
-    GBT_CHECK(!keys_spec || (skip_closed && rmax_done && !keys && !count_mode),
-              "speculated key sums need the host's closed-form test");
-    int32_t l2 = log2_ceil(n);
-    unsigned long long *hist = nullptr;
-    GBT_TRY(scratch_t(c, kScrMisc, 2 * kDigitBuckets, &hist));
-    if (n > 0) {
-        if (rmax_done)
-            ;
-        else if (kind == kSrcGpair)
-            k_mvs_rmax<kSrcGpair><<<rblocks(n), 256, 0, c->stream>>>(src, n, lambda, st);
-        else
-            k_mvs_rmax<kSrcMargin><<<rblocks(n), 256, 0, c->stream>>>(src, n, lambda, st);
-        GBT_LAUNCHED();
-    }
-    auto keys_pass = [&]() -> gbt_status {
-        if (kind == kSrcGpair)
-            k_mvs_keys<kSrcGpair><<<rblocks(n), 256, 0, c->stream>>>(src, n, lambda, l2, st, (int64_t *)keys);
-        else
-            k_mvs_keys<kSrcMargin><<<rblocks(n), 256, 0, c->stream>>>(src, n, lambda, l2, st, (int64_t *)keys);
-        GBT_LAUNCHED();
-        return GBT_OK;
-    };
-    // speculated: the gradient pass summed the keys with a guessed exponent
-    if (n > 0 && !keys_spec) GBT_TRY(keys_pass());
-    // skip_closed: the host learns from pinned memory whether the closed form
-    // holds (it waits for the passes above, nothing else is queued) and then
-    // launches no descent levels, which would all return at once
-    volatile int32_t *done_poll = nullptr;
-    int32_t *done_dev = nullptr;
-    if (skip_closed) {
-        void *hio, *hio_d;
-        GBT_TRY(host_io(c, 64, &hio, &hio_d));
-        done_poll = (volatile int32_t *)hio;
-        done_dev = (int32_t *)hio_d;
-        *done_poll = -1;
-    }
-    auto wait_flag = [&]() -> gbt_status {
-        const auto t0 = std::chrono::steady_clock::now();
-        for (uint32_t spin = 0; *done_poll < 0; ++spin) {
-            if ((spin & 1023u) == 0 && std::chrono::steady_clock::now() - t0 > std::chrono::seconds(2)) {
-                GBT_HIP(hipStreamSynchronize(c->stream));  // the flag is written by then
-                break;
-            }
+    if (kind == kSrcGpair)
+        k_mvs_keys<kSrcGpair><<<rblocks(n), 256, 0, c->stream>>>(src, n, lambda, l2, st, (int64_t *)keys);
+    else
+        k_mvs_keys<kSrcMargin><<<rblocks(n), 256, 0, c->stream>>>(src, n, lambda, l2, st, (int64_t *)keys);
+}
+
+gbt_status wait_flag(gbt_ctx *c, volatile int32_t *done_poll)
+{
+    const auto t0 = std::chrono::steady_clock::now();
+    for (uint32_t spin = 0; *done_poll < 0; ++spin) {
+        if ((spin & 1023u) == 0 && std::chrono::steady_clock::now() - t0 > std::chrono::seconds(2)) {
+            GBT_HIP(hipStreamSynchronize(c->stream));  // the flag is written by then
+            break;
         }
-        return GBT_OK;
-    };
-    k_mvs_thresh_init<<<1, 64, 0, c->stream>>>(st, K, done_dev, count_mode ? 1 : 0, keys_spec && n > 0 ? l2 : -1);
-    GBT_LAUNCHED();
+    }
+    return GBT_OK;
+}
+
+// After the threshold's first kernel: with a host flag, its outcome (1 the
+// closed form holds, 0 a descent is needed, 2 the guessed key exponent was
+// wrong: the keys pass and the first kernel again); then the radix descent
+// unless the closed form held.
+gbt_status threshold_rest(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
+                          double lambda, int64_t K, SampleState *st, bool count_mode, volatile int32_t *done_poll,
+                          int32_t *done_dev)
+{
+    const int32_t l2 = log2_ceil(n);
     if (done_poll) {
-        GBT_TRY(wait_flag());
+        GBT_TRY(wait_flag(c, done_poll));
         if (*done_poll == 2) {
             // the guessed exponent was not the keys': the keys pass after all
             k_keys_reset<<<1, 256, 0, c->stream>>>(st);
             GBT_LAUNCHED();
-            GBT_TRY(keys_pass());
+            keys_pass(c, src, kind, keys, n, lambda, l2, st);
+            GBT_LAUNCHED();
             *done_poll = -1;
             k_mvs_thresh_init<<<1, 64, 0, c->stream>>>(st, K, done_dev, count_mode ? 1 : 0, -1);
             GBT_LAUNCHED();
-            GBT_TRY(wait_flag());
+            GBT_TRY(wait_flag(c, done_poll));
         }
         if (*done_poll == 1) return GBT_OK;
     }
+    unsigned long long *hist = nullptr;
+    GBT_TRY(scratch_t(c, kScrMisc, 2 * kDigitBuckets, &hist));
     k_zero_u64<<<blocks(2 * kDigitBuckets), 256, 0, c->stream>>>(hist, 2 * kDigitBuckets);
     GBT_LAUNCHED();
     // Every key is at most 2^(62 - ceil(log2 n)), so the descent needs at
@@ -921,6 +904,60 @@ gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64
         GBT_LAUNCHED();
     }
     return GBT_OK;
+}
+
+}  // namespace
+
+gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
+                         double lambda, int64_t K, SampleState *st, bool skip_closed, bool rmax_done,
+                         bool count_mode, bool keys_spec, bool defer)
+{
+    GBT_CHECK(!keys_spec || (skip_closed && rmax_done && !keys && !count_mode),
+              "speculated key sums need the host's closed-form test");
+    GBT_CHECK(!defer || skip_closed, "a deferred threshold needs the host's closed-form test");
+    const int32_t l2 = log2_ceil(n);
+    if (n > 0) {
+        if (rmax_done)
+            ;
+        else if (kind == kSrcGpair)
+            k_mvs_rmax<kSrcGpair><<<rblocks(n), 256, 0, c->stream>>>(src, n, lambda, st);
+        else
+            k_mvs_rmax<kSrcMargin><<<rblocks(n), 256, 0, c->stream>>>(src, n, lambda, st);
+        GBT_LAUNCHED();
+    }
+    // speculated: the gradient pass summed the keys with a guessed exponent
+    if (n > 0 && !keys_spec) {
+        keys_pass(c, src, kind, keys, n, lambda, l2, st);
+        GBT_LAUNCHED();
+    }
+    // skip_closed: the host learns from pinned memory whether the closed form
+    // holds (it waits for the passes above, nothing else is queued) and then
+    // launches no descent levels, which would all return at once
+    volatile int32_t *done_poll = nullptr;
+    int32_t *done_dev = nullptr;
+    if (skip_closed) {
+        void *hio, *hio_d;
+        GBT_TRY(host_io(c, 64, &hio, &hio_d));
+        done_poll = (volatile int32_t *)hio;
+        done_dev = (int32_t *)hio_d;
+        *done_poll = -1;
+    }
+    k_mvs_thresh_init<<<1, 64, 0, c->stream>>>(st, K, done_dev, count_mode ? 1 : 0, keys_spec && n > 0 ? l2 : -1);
+    GBT_LAUNCHED();
+    if (defer) return GBT_OK;
+    return threshold_rest(c, src, kind, keys, n, lambda, K, st, count_mode, done_poll, done_dev);
+}
+
+gbt_status mvs_threshold_resume(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
+                                double lambda, int64_t K, SampleState *st, bool *redo)
+{
+    void *hio, *hio_d;
+    GBT_TRY(host_io(c, 64, &hio, &hio_d));
+    volatile int32_t *done_poll = (volatile int32_t *)hio;
+    GBT_TRY(wait_flag(c, done_poll));
+    *redo = *done_poll != 1;
+    if (!*redo) return GBT_OK;
+    return threshold_rest(c, src, kind, keys, n, lambda, K, st, false, done_poll, (int32_t *)hio_d);
 }
 
 gbt_status mvs_select(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,

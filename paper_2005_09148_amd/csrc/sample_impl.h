@@ -93,9 +93,20 @@ gbt_status state_init(gbt_ctx *c, SampleState *st);
 // keys_spec (with skip_closed and rmax_done): the key maximum and sum are
 // already in st, formed by gradients_rmax with a guessed exponent; the
 // threshold pass checks it and runs the keys pass only when it was wrong.
+// defer (with skip_closed): return after the threshold's first kernel; the
+// caller may queue work that reads T (it is 0, keeping every row, unless the
+// closed form held) and then calls mvs_threshold_resume, after a
+// synchronization of its own.
 gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
                          double lambda, int64_t K, SampleState *st, bool skip_closed,
-                         bool rmax_done = false, bool count_mode = false, bool keys_spec = false);
+                         bool rmax_done = false, bool count_mode = false, bool keys_spec = false,
+                         bool defer = false);
+// The rest of a deferred MVS threshold: *redo is false when the closed form
+// held (T was final for the queued work), else the threshold is completed
+// (the keys pass if the key exponent was guessed wrong, the radix descent)
+// and the work that read T must be queued again.
+gbt_status mvs_threshold_resume(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
+                                double lambda, int64_t K, SampleState *st, bool *redo);
 // Keep flags of rows [0, n) and, when tile_cnt is given, the kept count of
 // each tile of kCompactTile rows.
 gbt_status mvs_select(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,

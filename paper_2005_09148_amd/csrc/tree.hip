@@ -264,19 +264,35 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
             o->K = std::min<int64_t>(n, std::max<int64_t>(0, (int64_t)std::nearbyint(a * (double)n)));
             GBT_TRY(mvs_threshold(c, src, kind, nullptr, n, lam, o->K, st, true, st_ready != nullptr, true));
             rule = SampleRule{GBT_SAMPLE_GOSS, p >= 1.0 ? 1 : 0, p >= 1.0 ? 0 : draw_limit(p), (1.0 - a) / b};
-        } else if (sp.f < 1.0) {
+        }
+        // MVS: the selection is queued right behind the threshold's first
+        // kernel, before the host learns whether the closed form held (it
+        // almost always does); otherwise the threshold is completed and the
+        // selection queued again
+        const bool mvs = sp.f < 1.0 && sp.sampler == GBT_SAMPLE_MVS;
+        if (mvs) {
             o->K = std::max<int64_t>(1, (int64_t)std::nearbyint(sp.f * (double)n));
             GBT_TRY(mvs_threshold(c, src, kind, nullptr, n, lam, o->K, st, true, st_ready != nullptr, false,
-                                  keys_spec && st_ready != nullptr));
+                                  keys_spec && st_ready != nullptr, true));
         }
-        // with f = 1 the state keeps T = 0: every row is kept with weight 1
-        GBT_TRY(mvs_select(c, src, kind, nullptr, n, lam, st, sp.seed, sp.iteration, 0, keep, tile_off, rule));
-        // the sample size sizes the buffers below: one round trip
+        // the sample size sizes the buffers below: one round trip (its word
+        // sits apart from the threshold's flag in the pinned buffer)
         void *hio, *hio_d;
         GBT_TRY(host_io(c, 64, &hio, &hio_d));
-        GBT_TRY(keep_tile_offsets(c, n, tile_off, (int32_t *)hio_d));
-        GBT_HIP(hipStreamSynchronize(c->stream));
-        o->R = *(volatile int32_t *)hio;
+        auto select = [&]() -> gbt_status {
+            // with f = 1 the state keeps T = 0: every row is kept with weight 1
+            GBT_TRY(mvs_select(c, src, kind, nullptr, n, lam, st, sp.seed, sp.iteration, 0, keep, tile_off, rule));
+            GBT_TRY(keep_tile_offsets(c, n, tile_off, (int32_t *)hio_d + 4));
+            GBT_HIP(hipStreamSynchronize(c->stream));
+            return GBT_OK;
+        };
+        GBT_TRY(select());
+        if (mvs) {
+            bool redo = false;
+            GBT_TRY(mvs_threshold_resume(c, src, kind, nullptr, n, lam, o->K, st, &redo));
+            if (redo) GBT_TRY(select());
+        }
+        o->R = *((volatile int32_t *)hio + 4);
         size_t rb = (size_t)mx->row_words * 4;
         uint32_t *spage;
         GBT_TRY(bufs.get(kScrSampled, (size_t)std::max<int64_t>(o->R, 1) * rb, (void **)&spage));
