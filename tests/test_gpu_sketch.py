@@ -177,3 +177,67 @@ def test_rejects_bad_summary_size(gbt, ctx):
     for S in (1, -3, (1 << 20) + 1):
         with pytest.raises(gbt.GbtError):
             gbt.Quantizer(ctx, 3, 100, sketch_summary=S)
+
+
+@pytest.mark.parametrize("S,batch_rows,n", [(2, 5_000, 30_000), (4, 1, 300), (3, 777, 9_001)])
+def test_merged_sketch_small_summaries_and_tiny_batches(gbt, ctx, S, batch_rows, n):
+    """The smallest summaries (S = 2: the minimum and the maximum survive each
+    prune), one-row batches, and features missing in some batches only."""
+    rng = np.random.default_rng(S * 1000 + batch_rows)
+    m = 5
+    X = rng.normal(size=(n, m)).astype(np.float32)
+    X[: n // 2, 1] = np.nan          # missing in the first batches only
+    X[n // 3:, 2] = np.nan           # present in the first batches only
+    X[:, 3] = np.round(X[:, 3] * 2)  # ties
+    X[rng.random((n, m)) < 0.1] = np.nan
+    mx = quantize_batches(gbt, ctx, X, 64, S, batch_rows)
+    cuts, _ = orc.sketch_cuts_merge_dense(X, 64, S, batch_rows)
+    cp, cv = mx.cuts()
+    assert same_bits(cp, cuts.cut_ptr) and same_bits(cv, cuts.cut_values)
+    mx.free()
+
+
+def test_empty_batches_change_nothing(gbt, ctx):
+    X = make_dense(11, 20_000, 4, "normal", 0.1)
+    q = gbt.Quantizer(ctx, 4, len(X), max_bin=128, sketch_summary=200)
+    empty = X[:0]
+    parts = [X[b:b + 3_000] for b in range(0, len(X), 3_000)]
+    for p in parts:
+        q.sketch(empty)
+        q.sketch(p)
+    q.sketch(empty)
+    q.finalize()
+    for p in parts:
+        q.encode(p)
+    mx = q.end()
+    cuts, _ = orc.sketch_cuts_merge_dense(X, 128, 200, 3_000)
+    cp, cv = mx.cuts()
+    assert same_bits(cp, cuts.cut_ptr) and same_bits(cv, cuts.cut_values)
+    mx.free()
+
+
+def test_wide_csr_tiny_summaries(gbt, ctx):
+    """3000 features, most of them empty in most batches, S = 4."""
+    rng = np.random.default_rng(12)
+    n, m = 6_000, 3_000
+    X = np.full((n, m), np.nan, np.float32)
+    nnz = 40_000
+    r, cidx = rng.integers(0, n, nnz), (rng.zipf(1.3, nnz) - 1) % m
+    X[r, cidx] = rng.lognormal(size=nnz).astype(np.float32)
+    indptr, idx, val = to_csr(X)
+    q = gbt.Quantizer(ctx, m, n, max_bin=16, sketch_summary=4, kind=gbt.INPUT_CSR)
+    bounds = list(range(0, n, 1_000)) + [n]
+    for b0, b1 in zip(bounds, bounds[1:]):
+        lo, hi = indptr[b0], indptr[b1]
+        q.sketch({"kind": "csr", "indptr": indptr[b0:b1 + 1] - lo, "indices": idx[lo:hi], "values": val[lo:hi],
+                  "m": m})
+    q.finalize()
+    for b0, b1 in zip(bounds, bounds[1:]):
+        lo, hi = indptr[b0], indptr[b1]
+        q.encode({"kind": "csr", "indptr": indptr[b0:b1 + 1] - lo, "indices": idx[lo:hi], "values": val[lo:hi],
+                  "m": m})
+    mx = q.end()
+    cuts, _ = orc.sketch_cuts_merge_csr(indptr, idx, val, m, 16, 4, 1_000)
+    cp, cv = mx.cuts()
+    assert same_bits(cp, cuts.cut_ptr) and same_bits(cv, cuts.cut_values)
+    mx.free()
