@@ -1027,26 +1027,24 @@ __global__ void __launch_bounds__(kPartThreads)
 // from this tile's scan when the node starts in the tile; the one node that
 // starts in an earlier tile (the node of the tile's first slot) gets them
 // from the tile counts before its first tile and that tile's flags.  The
-// nodes' left counts come from the flags pass.  The order of rows within a
-// node enters no result.  With `has_plan`, block 0 is the level's plan
-// (plan_impl.h), which reads only the node records and left counts of the
-// flags pass and writes the children's records, which no other block reads;
-// the tiles are blocks 1.. then.
+// order of rows within a node enters no result.  Block 0 is the level's plan (plan_impl.h), which
+// reads only the node records and the boundary counts of the flags pass and
+// writes the nodes' left counts and the children's records, which no other
+// block reads; the tiles are blocks 1.. .
 __global__ void __launch_bounds__(kPartThreads)
     k_part_scatter_rev(const int32_t *__restrict__ rows, int64_t n, const uint8_t *__restrict__ flags,
                        const int32_t *__restrict__ tile_cnt, const long long *__restrict__ tile_off,
                        const int32_t *__restrict__ slot_node, int32_t *__restrict__ slot_node_out,
-                       DevNode *__restrict__ nodes, int32_t *__restrict__ rows_out, int32_t has_plan,
-                       PlanArgs pa)
+                       DevNode *__restrict__ nodes, int32_t *__restrict__ rows_out, PlanArgs pa)
 {
-    if (has_plan && blockIdx.x == 0) {
+    if (blockIdx.x == 0) {
         pa.tile_cnt = tile_cnt;
         pa.tile_off = tile_off;
         pa.tiles = (n + kPartTile - 1) / kPartTile;
         plan_level_block<kPartThreads>(nodes, pa);
         return;
     }
-    const int64_t tile = (int64_t)blockIdx.x - (has_plan ? 1 : 0);
+    const int64_t tile = (int64_t)blockIdx.x - 1;
     __shared__ int32_t lds16[kPartThreads / 64];
     __shared__ long long s_red[2][kPartThreads / 64];
     __shared__ int32_t s_pref[kPartThreads];  // left flags of the tile before each thread's slots
@@ -1258,10 +1256,9 @@ gbt_status split_columns(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page,
 gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int32_t *rows,
                               int64_t n, const int32_t *slot_node, int32_t *slot_node_out, DevNode *nodes,
                               int32_t *rows_out, const LevelChoice *choice, const SlotTable *stbl,
-                              const uint16_t *cols, const PlanArgs *plan, bool order)
+                              const uint16_t *cols, const PlanArgs &plan, bool order)
 {
     if (n == 0) return GBT_OK;
-    GBT_CHECK(order || plan, "a partition without the row order needs the plan");
     const SlotTable st = stbl ? *stbl : SlotTable{nullptr, nullptr, nullptr, 0, 0, 0};
     GBT_CHECK(n < ((int64_t)1 << 31) - 1, "partition of %lld rows (limit 2^31-2)", (long long)n);
     uint8_t *flags;
@@ -1284,12 +1281,9 @@ gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
         k_tile_offsets<<<1, kTileScanThreads, 0, c->stream>>>(tile_cnt, tiles, tile_off);
         GBT_LAUNCHED();
     }
-    const int32_t has_plan = plan ? 1 : 0;
-    // without the row order only the plan block runs (the left counts come
-    // from the flags pass)
-    k_part_scatter_rev<<<(unsigned)((order ? tiles : 0) + has_plan), kPartThreads, 0, c->stream>>>(
-        rows, n, flags, tile_cnt, tile_off, slot_node, slot_node_out, nodes, rows_out, has_plan,
-        plan ? *plan : PlanArgs{});
+    // without the row order only the plan block runs
+    k_part_scatter_rev<<<(unsigned)((order ? tiles : 0) + 1), kPartThreads, 0, c->stream>>>(
+        rows, n, flags, tile_cnt, tile_off, slot_node, slot_node_out, nodes, rows_out, plan);
     GBT_LAUNCHED();
     return GBT_OK;
 }

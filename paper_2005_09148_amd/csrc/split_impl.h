@@ -86,11 +86,13 @@ struct PlanArgs;
 
 // The tree driver's partition: rows[0, n) by slot_node as partition_impl,
 // except that a splitting node's right rows land at the back of its segment
-// in reverse slot order; nodes[id].nleft (zero before the call) receives
-// each splitting node's left count (pleft is not written).  Two kernels;
-// with `plan`, the second also runs the level's plan (plan_impl.h) in one
-// of its blocks; `order` false (only with a plan) skips the rows' new order
-// (rows_out and slot_node_out are not written) and runs the plan alone.  With `choice`, the split
+// in reverse slot order.  Two kernels: the first writes the left flags and,
+// for each node, the tile and in-tile left count at its first and last slot
+// (DevNode tile_b/left_b/tile_e/left_e); the second scatters the rows and,
+// in one of its blocks, runs the level's `plan` (plan_impl.h), which turns
+// those into the nodes' left counts (nleft; pleft is not written) and the
+// children's records.  `order` false skips the rows' new order (rows_out and
+// slot_node_out are not written) and runs the plan alone.  With `choice`, the split
 // records of the level's nodes are chosen from the candidates and written
 // by the first kernel (instead of by eval_reduce_impl).  With `stbl` (a
 // sparse page's slot table), the search for a row's split feature looks
@@ -100,9 +102,9 @@ struct PlanArgs;
 // segment, so a column's lines serve many of them.
 gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int32_t *rows,
                               int64_t n, const int32_t *slot_node, int32_t *slot_node_out, DevNode *nodes,
-                              int32_t *rows_out, const LevelChoice *choice = nullptr,
-                              const SlotTable *stbl = nullptr, const uint16_t *cols = nullptr,
-                              const PlanArgs *plan = nullptr, bool order = true);
+                              int32_t *rows_out, const LevelChoice *choice,
+                              const SlotTable *stbl, const uint16_t *cols, const PlanArgs &plan,
+                              bool order);
 
 // Whether a page of mx's geometry takes a column copy (dense, symbols of at
 // most 16 bits).

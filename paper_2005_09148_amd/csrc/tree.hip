@@ -1053,7 +1053,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         PlanArgs pa{evA, cntA, plan_next ? 1 : 0, items, evB, cntB, work_d, cnt + 2, red_d, cnt + 3, stat};
         if (last) pa.lv = LeafArgs{leaf, compact, e_dev, p->lambda, p->eta, NN, 0};
         GBT_TRY(partition_rev_impl(c, mx, so.page, rows, R, slot_node, slot_tmp, nodes, rows_tmp,
-                                   choose ? &lc : nullptr, stbl.row ? &stbl : nullptr, cols, &pa,
+                                   choose ? &lc : nullptr, stbl.row ? &stbl : nullptr, cols, pa,
                                    !last || final_order));
         std::swap(rows, rows_tmp);
         std::swap(slot_node, slot_tmp);

@@ -241,3 +241,27 @@ def test_wide_csr_tiny_summaries(gbt, ctx):
     cp, cv = mx.cuts()
     assert same_bits(cp, cuts.cut_ptr) and same_bits(cv, cuts.cut_values)
     mx.free()
+
+
+def test_outofcore_batch_shape(gbt, ctx):
+    # the out-of-core workload's sketch at its own per-batch shape: N(0,1)
+    # features, batches of 2^21 rows, every 12th row sampled (200M rows
+    # under a 2^24-row sample take stride 12; here sketch_max_rows sets it),
+    # so each batch adds about 174763 keys per feature to summaries of
+    # 65536 entries, and every merge prunes
+    n, m, br, S = 8 << 21, 4, 1 << 21, 65_536
+    smr = -(-n // 12)
+    assert -(-n // smr) == 12 and -(-200_000_000 // (1 << 24)) == 12
+    X = np.random.default_rng(2005).standard_normal((n, m), dtype=np.float32)
+    q = gbt.Quantizer(ctx, m, n, max_bin=256, sketch_max_rows=smr, sketch_summary=S)
+    for b0 in range(0, n, br):
+        q.sketch(X[b0:b0 + br])
+    q.finalize()
+    for b0 in range(0, n, br):
+        q.encode(X[b0:b0 + br])
+    mx = q.end()
+    cuts, ent = orc.sketch_cuts_merge_dense(X, 256, S, br, smr)
+    assert (ent <= S).all() and n // 12 > 16 * S  # pruned: the sample is far larger than a summary
+    cp, cv = mx.cuts()
+    assert same_bits(cp, cuts.cut_ptr) and same_bits(cv, cuts.cut_values)
+    mx.free()
