@@ -10,6 +10,7 @@
 #pragma once
 
 #include "split_impl.h"
+#include "wave_impl.h"
 
 namespace gbt {
 
@@ -47,12 +48,7 @@ template <int T>
 __device__ inline int32_t plan_block_scan(int32_t v, int32_t *lds, int32_t *total)
 {
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-    int32_t x = v;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        int32_t y = __shfl_up(x, d, 64);
-        if (lane >= d) x += y;
-    }
+    const int32_t x = wave_incl_sum(v);
     __syncthreads();
     if (lane == 63) lds[wid] = x;
     __syncthreads();
@@ -201,10 +197,8 @@ __device__ void plan_level_block(DevNode *__restrict__ nodes, const PlanArgs &a)
             leaf_entry(nodes, i, eg, eh, a.lv.lambda, a.lv.eta, a.lv.leaf, a.lv.compact);
     }
     if (!a.plan) return;
-    for (int d = 32; d > 0; d >>= 1) {
-        rb += __shfl_xor(rb, d, 64);
-        nbuild += __shfl_xor(nbuild, d, 64);
-    }
+    rb = wave_total(rb);
+    nbuild = wave_total(nbuild);
     if ((threadIdx.x & 63) == 0) {
         red_rows[threadIdx.x >> 6] = rb;
         red_nodes[threadIdx.x >> 6] = nbuild;
@@ -274,7 +268,7 @@ __device__ void plan_level_block(DevNode *__restrict__ nodes, const PlanArgs &a)
         c_build += tot_b;
         c_part += tot_p;
     }
-    for (int d = 32; d > 0; d >>= 1) rows_built += __shfl_xor(rows_built, d, 64);
+    rows_built = wave_total(rows_built);
     if ((threadIdx.x & 63) == 0 && rows_built) atomicAdd(&a.stat[0], rows_built);
     if (threadIdx.x == 0) {
         *a.n_next_d = 2 * c_build;

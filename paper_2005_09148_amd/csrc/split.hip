@@ -14,6 +14,7 @@
 // that writes [left | right] of every splitting segment in input order.
 #include "split_impl.h"
 #include "plan_impl.h"
+#include "wave_impl.h"
 
 #include <cstring>
 
@@ -48,13 +49,48 @@ __device__ inline float split_threshold(const SplitCuts &c, int32_t feature, int
     return c.values[c.ptr[feature] + split_bin - 1];
 }
 
-__device__ inline double eq8_gain(double GL, double HL, double GR, double HR, double G, double H,
-                                  double lambda, double gamma)
+// Eq. 8: 0.5*((G_L^2/(H_L+lambda) + G_R^2/(H_R+lambda)) - c) - gamma, with
+// the parent's term c = G^2/(H+lambda) computed once per node.
+__device__ inline double eq8_gain_c(double GL, double HL, double GR, double HR, double c, double lambda,
+                                    double gamma)
 {
     double a = (GL * GL) / (HL + lambda);
     double b = (GR * GR) / (HR + lambda);
-    double c = (G * G) / (H + lambda);
     return 0.5 * ((a + b) - c) - gamma;
+}
+
+// A lane's kN candidates of one feature: every gain is computed before any
+// is compared (the divisions of different candidates overlap instead of
+// waiting on each other's branches), then the candidates are taken in
+// (s, dir) order exactly as a loop that skips the inadmissible ones would.
+// lg/lh: left sums; s: the cut (left = bins < s) of candidate k / 2.
+template <int kN>
+__device__ inline void pick_candidates(const long long *lg, const long long *lh, const int32_t *s, int32_t B,
+                                       long long Qg, long long Qh, double c, const EvalParams &ep, Cand &best)
+{
+    double gain[kN];
+    bool ok[kN];
+#pragma unroll
+    for (int k = 0; k < kN; ++k) {
+        const double GL = fx(lg[k], ep.e_g), HL = fx(lh[k], ep.e_h);
+        const double GR = fx(Qg - lg[k], ep.e_g), HR = fx(Qh - lh[k], ep.e_h);
+        gain[k] = eq8_gain_c(GL, HL, GR, HR, c, ep.lambda, ep.gamma);
+        // no short circuit: the gain is needed whatever the other tests say,
+        // so its division is not moved under a branch of its own
+        ok[k] = (s[k / 2] <= B - 1) & (HL >= ep.mcw) & (HR >= ep.mcw) & (gain[k] == gain[k]);
+    }
+    // better() as selects, without branches
+#pragma unroll
+    for (int k = 0; k < kN; ++k) {
+        const int32_t order = s[k / 2] * 2 + (k & 1);
+        const bool take = ok[k] & (!best.valid | (gain[k] > best.gain) |
+                                   ((gain[k] == best.gain) & (order < best.order)));
+        best.gain = take ? gain[k] : best.gain;
+        best.order = take ? order : best.order;
+        best.valid = take ? 1 : best.valid;
+        best.lg = take ? lg[k] : best.lg;
+        best.lh = take ? lh[k] : best.lh;
+    }
 }
 
 // The best candidate of the wavefront (every lane receives it): the highest
@@ -69,74 +105,51 @@ __device__ inline Cand wave_best(Cand x)
     r.order = 0;
     r.lg = r.lh = 0;
     if (!any) return r;
-    double m = x.valid ? x.gain : -__builtin_inf();
-    for (int d = 32; d > 0; d >>= 1) m = fmax(m, __shfl_xor(m, d, 64));
+    const double m = wave_max_f64(x.valid ? x.gain : -__builtin_inf());
     const bool cand = x.valid && x.gain == m;
-    int32_t o = cand ? x.order : 0x7fffffff;
-    for (int d = 32; d > 0; d >>= 1) o = min(o, __shfl_xor(o, d, 64));
+    const int32_t o = wave_min<int32_t>(cand ? x.order : 0x7fffffff);
     const unsigned long long win = __ballot(cand && x.order == o);
     const int wl = __ffsll((long long)win) - 1;
     r.valid = 1;
-    r.gain = __shfl(x.gain, wl, 64);  // the winner's own bits (+0 and -0 compare equal)
+    r.gain = wave_read(x.gain, wl);  // the winner's own bits (+0 and -0 compare equal)
     r.order = o;
-    r.lg = __shfl(x.lg, wl, 64);
-    r.lh = __shfl(x.lh, wl, 64);
+    r.lg = wave_read(x.lg, wl);
+    r.lh = wave_read(x.lh, wl);
     return r;
 }
 
-__device__ inline long long wave_sum(long long v)
-{
-    for (int d = 32; d > 0; d >>= 1) v += __shfl_xor(v, d, 64);
-    return v;
-}
+__device__ inline long long wave_sum(long long v) { return wave_total(v); }
 
 // Best split of one feature for one node, evaluated by one wavefront.  The
 // result (valid in every lane) carries order = s*2 + dir.
 // The gains of the four cuts after this lane's bins of one 256-bin chunk:
 // pg, ph enter as the sums of all bins before the lane's first bin.
 __device__ inline void eval_chunk(const longlong2 v[4], int32_t base, int32_t B, long long pg, long long ph,
-                                  long long Qg, long long Qh, long long mg, long long mh, double G, double H,
+                                  long long Qg, long long Qh, long long mg, long long mh, double c,
                                   const EvalParams &ep, Cand &best)
 {
     const int lane = threadIdx.x & 63;
+    long long lg[8], lh[8];
+    int32_t s[4];
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-        const int32_t b = base + lane * 4 + t;
         pg += v[t].x;
         ph += v[t].y;
-        const int32_t s = b + 1;  // left = bins < s
-        if (s > B - 1) continue;
+        s[t] = base + lane * 4 + t + 1;  // left = bins < s
 #pragma unroll
         for (int dir = 0; dir < 2; ++dir) {
-            const long long lg = pg + (dir ? mg : 0), lh = ph + (dir ? mh : 0);
-            const double GL = fx(lg, ep.e_g), HL = fx(lh, ep.e_h);
-            const double GR = fx(Qg - lg, ep.e_g), HR = fx(Qh - lh, ep.e_h);
-            if (!(HL >= ep.mcw && HR >= ep.mcw)) continue;
-            const double gain = eq8_gain(GL, HL, GR, HR, G, H, ep.lambda, ep.gamma);
-            if (gain != gain) continue;
-            Cand c;
-            c.gain = gain;
-            c.order = s * 2 + dir;
-            c.valid = 1;
-            c.lg = lg;
-            c.lh = lh;
-            if (better(c, best)) best = c;
+            lg[2 * t + dir] = pg + (dir ? mg : 0);
+            lh[2 * t + dir] = ph + (dir ? mh : 0);
         }
     }
+    pick_candidates<8>(lg, lh, s, B, Qg, Qh, c, ep, best);
 }
 
 // Inclusive wavefront scan of a pair of int64 values.
 __device__ inline void wave_scan2(long long &xg, long long &xh)
 {
-    const int lane = threadIdx.x & 63;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const long long yg = __shfl_up(xg, d, 64), yh = __shfl_up(xh, d, 64);
-        if (lane >= d) {
-            xg += yg;
-            xh += yh;
-        }
-    }
+    xg = wave_incl_sum(xg);
+    xh = wave_incl_sum(xh);
 }
 
 // Best split of one feature for one node, evaluated by one wavefront.  The
@@ -151,6 +164,7 @@ __device__ Cand eval_feature(const longlong2 *__restrict__ hj, int32_t B, long l
     best.order = 0;
     best.lg = best.lh = 0;
     const double G = fx(Qg, ep.e_g), H = fx(Qh, ep.e_h);
+    const double c = (G * G) / (H + ep.lambda);
     if (B <= 256) {
         // one chunk: the scan's last lane holds the feature's bin totals
         longlong2 v[4];
@@ -164,8 +178,8 @@ __device__ Cand eval_feature(const longlong2 *__restrict__ hj, int32_t B, long l
         }
         long long xg = sg, xh = sh;
         wave_scan2(xg, xh);
-        const long long tg = __shfl(xg, 63, 64), th = __shfl(xh, 63, 64);
-        eval_chunk(v, 0, B, xg - sg, xh - sh, Qg, Qh, Qg - tg, Qh - th, G, H, ep, best);
+        const long long tg = wave_read(xg, 63), th = wave_read(xh, 63);
+        eval_chunk(v, 0, B, xg - sg, xh - sh, Qg, Qh, Qg - tg, Qh - th, c, ep, best);
         return wave_best(best);
     }
     // totals over the feature's bins -> missing sums
@@ -191,9 +205,9 @@ __device__ Cand eval_feature(const longlong2 *__restrict__ hj, int32_t B, long l
         }
         long long xg = sg, xh = sh;
         wave_scan2(xg, xh);
-        eval_chunk(v, base, B, carry_g + xg - sg, carry_h + xh - sh, Qg, Qh, mg, mh, G, H, ep, best);
-        carry_g += __shfl(xg, 63, 64);
-        carry_h += __shfl(xh, 63, 64);
+        eval_chunk(v, base, B, carry_g + xg - sg, carry_h + xh - sh, Qg, Qh, mg, mh, c, ep, best);
+        carry_g += wave_read(xg, 63);
+        carry_h += wave_read(xh, 63);
     }
     return wave_best(best);
 }
@@ -416,32 +430,22 @@ __device__ Cand eval_feature_regs(const long long *g, const long long *h, int32_
         wave_scan2(xg, xh);
         pgs[t] = cg + xg;
         phs[t] = ch + xh;
-        cg += __shfl(xg, 63, 64);
-        ch += __shfl(xh, 63, 64);
+        cg += wave_read(xg, 63);
+        ch += wave_read(xh, 63);
     }
     const long long mg = Qg - cg, mh = Qh - ch;
+    long long lg[2 * kBL], lh[2 * kBL];
+    int32_t s[kBL];
 #pragma unroll
     for (int t = 0; t < kBL; ++t) {
-        const long long pg = pgs[t], ph = phs[t];
-        const int32_t s = t * 64 + lane + 1;  // left = bins < s
-        if (s > B - 1) continue;
+        s[t] = t * 64 + lane + 1;  // left = bins < s
 #pragma unroll
         for (int dir = 0; dir < 2; ++dir) {
-            const long long lg = pg + (dir ? mg : 0), lh = ph + (dir ? mh : 0);
-            const double GL = fx(lg, ep.e_g), HL = fx(lh, ep.e_h);
-            const double GR = fx(Qg - lg, ep.e_g), HR = fx(Qh - lh, ep.e_h);
-            if (!(HL >= ep.mcw && HR >= ep.mcw)) continue;
-            const double gain = eq8_gain(GL, HL, GR, HR, G, H, ep.lambda, ep.gamma);
-            if (gain != gain) continue;
-            Cand c;
-            c.gain = gain;
-            c.order = s * 2 + dir;
-            c.valid = 1;
-            c.lg = lg;
-            c.lh = lh;
-            if (better(c, best)) best = c;
+            lg[2 * t + dir] = pgs[t] + (dir ? mg : 0);
+            lh[2 * t + dir] = phs[t] + (dir ? mh : 0);
         }
     }
+    pick_candidates<2 * kBL>(lg, lh, s, B, Qg, Qh, (G * G) / (H + ep.lambda), ep, best);
     return wave_best(best);
 }
 
@@ -581,10 +585,8 @@ __global__ void __launch_bounds__(256)
             bg = o.gain;
         }
     }
-    double m = bi >= 0 ? bg : -__builtin_inf();
-    for (int d = 32; d > 0; d >>= 1) m = fmax(m, __shfl_xor(m, d, 64));
-    int32_t best = (bi >= 0 && bg == m) ? bi : 0x7fffffff;
-    for (int d = 32; d > 0; d >>= 1) best = min(best, __shfl_xor(best, d, 64));
+    const double m = wave_max_f64(bi >= 0 ? bg : -__builtin_inf());
+    const int32_t best = wave_min<int32_t>((bi >= 0 && bg == m) ? bi : 0x7fffffff);
     if (lane != 0) return;
     const EvalCand b = best != 0x7fffffff ? cand[(int64_t)k * n_fblocks + best] : EvalCand{0.0, 0, 0, -1, -1, 0, 0};
     const EvalNode node = nodes[k];
@@ -699,12 +701,7 @@ constexpr int kPartTile = kPartThreads * kPartItems;  // the scan's tile
 __device__ inline int32_t part_block_scan(int32_t v, int32_t *lds16, int32_t *total)
 {
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-    int32_t x = v;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const int32_t y = __shfl_up(x, d, 64);
-        if (lane >= d) x += y;
-    }
+    const int32_t x = wave_incl_sum(v);
     if (lane == 63) lds16[wid] = x;
     __syncthreads();
     int32_t off = 0, tot = 0;
@@ -764,10 +761,8 @@ __device__ inline int4 wave_decide(const EvalCand *__restrict__ cand, int32_t m,
             bg = o.gain;
         }
     }
-    double mx = bi >= 0 ? bg : -__builtin_inf();
-    for (int d = 32; d > 0; d >>= 1) mx = fmax(mx, __shfl_xor(mx, d, 64));
-    int32_t best = (bi >= 0 && bg == mx) ? bi : 0x7fffffff;
-    for (int d = 32; d > 0; d >>= 1) best = min(best, __shfl_xor(best, d, 64));
+    const double mx = wave_max_f64(bi >= 0 ? bg : -__builtin_inf());
+    const int32_t best = wave_min<int32_t>((bi >= 0 && bg == mx) ? bi : 0x7fffffff);
     if (best == 0x7fffffff) return make_int4(0, 0, 0, 0);
     const EvalCand b = c[best];
     if (!(b.gain > 0.0)) return make_int4(0, 0, 0, 0);
@@ -819,7 +814,7 @@ __global__ void __launch_bounds__(kPartThreads)
 #pragma unroll
             for (int k = 0; k < kPartItems; ++k)
                 if ((need >> k) & 1u) t = min(t, nid[k]);
-            for (int d = 32; d > 0; d >>= 1) t = min(t, __shfl_xor(t, d, 64));
+            t = wave_min(t);
             if (t == 0x7fffffff) break;
             const int64_t b0 = nodes[t].begin;
             const int4 ch = wave_decide(lc.cand, lc.m, nodes, t, b0 >= w_lo && b0 < w_lo + 64 * kPartItems);
@@ -895,7 +890,7 @@ __global__ void __launch_bounds__(kPartThreads)
         if (threadIdx.x == 0) tile_cnt[blockIdx.x] = tot;
         return;
     }
-    for (int d = 32; d > 0; d >>= 1) cnt += __shfl_xor(cnt, d, 64);
+    cnt = wave_total(cnt);
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = cnt;
     __syncthreads();
     if (threadIdx.x == 0) {
@@ -928,7 +923,7 @@ __device__ inline int64_t part_prefix(const uint8_t *__restrict__ flags, const i
         for (int64_t k = j; k < x; ++k) c += flags[k];
     }
     for (int64_t k = threadIdx.x; k < t; k += kBoundThreads) c += tile_cnt[k];
-    for (int d = 32; d > 0; d >>= 1) c += __shfl_xor(c, d, 64);
+    c = wave_total(c);
     __syncthreads();
     if ((threadIdx.x & 63) == 0) lds4[threadIdx.x >> 6] = c;
     __syncthreads();
@@ -983,7 +978,7 @@ __global__ void __launch_bounds__(kPartThreads)
     __shared__ long long tl16[kPartThreads / 64];
     long long before = 0;
     for (int64_t k = threadIdx.x; k < (int64_t)blockIdx.x; k += kPartThreads) before += tile_cnt[k];
-    for (int d = 32; d > 0; d >>= 1) before += __shfl_xor(before, d, 64);
+    before = wave_total(before);
     if ((threadIdx.x & 63) == 0) tl16[threadIdx.x >> 6] = before;
     int32_t total;
     const int32_t in_tile = part_block_scan(mine, lds16, &total);  // synchronizes the block
@@ -1088,10 +1083,8 @@ __global__ void __launch_bounds__(kPartThreads)
 #pragma unroll
         for (int k = 0; k < kPartItems; ++k) before_b += j + k < b0 ? flags[j + k] : 0;
     }
-    for (int d = 32; d > 0; d >>= 1) {
-        before += __shfl_xor(before, d, 64);
-        before_b += __shfl_xor(before_b, d, 64);
-    }
+    before = wave_total(before);
+    before_b = wave_total(before_b);
     if ((threadIdx.x & 63) == 0) {
         s_red[0][threadIdx.x >> 6] = before;
         s_red[1][threadIdx.x >> 6] = before_b;
@@ -1172,12 +1165,7 @@ __global__ void __launch_bounds__(kTileScanThreads)
     }
     // inclusive scan of the run totals: within the wave, then over waves
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-    long long x = run;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const long long y = __shfl_up(x, d, 64);
-        if (lane >= d) x += y;
-    }
+    const long long x = wave_incl_sum(run);
     if (lane == 63) s_w[wid] = x;
     __syncthreads();
     long long base = x - run;
