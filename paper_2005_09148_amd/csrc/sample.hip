@@ -9,6 +9,7 @@
 // exactly in ceil(bits/11) passes over the keys.  When T* exceeds every key
 // it has the closed form ceil(sum a / K).
 #include "sample_impl.h"
+#include "wave_impl.h"
 
 #include <chrono>
 
@@ -131,10 +132,7 @@ __device__ inline void philox_block(uint64_t c0, uint64_t c1, uint64_t k0, uint6
 // 256-thread blocks: wavefront butterfly, then the four wave results in LDS.
 __device__ inline unsigned long long block_max_u64(unsigned long long v, unsigned long long *lds4)
 {
-    for (int d = 32; d > 0; d >>= 1) {
-        unsigned long long o = __shfl_xor(v, d, 64);
-        v = o > v ? o : v;
-    }
+    v = wave_max(v);
     __syncthreads();
     if ((threadIdx.x & 63) == 0) lds4[threadIdx.x >> 6] = v;
     __syncthreads();
@@ -145,7 +143,7 @@ __device__ inline unsigned long long block_max_u64(unsigned long long v, unsigne
 
 __device__ inline unsigned long long block_sum_u64(unsigned long long v, unsigned long long *lds4)
 {
-    for (int d = 32; d > 0; d >>= 1) v += __shfl_xor(v, d, 64);
+    v = wave_total(v);
     __syncthreads();
     if ((threadIdx.x & 63) == 0) lds4[threadIdx.x >> 6] = v;
     __syncthreads();
@@ -189,11 +187,7 @@ __device__ inline double mvs_r(double g, double h, double lambda)
 __device__ inline unsigned long long block_fold_max(const Spread &a, unsigned long long *lds1)
 {
     if (threadIdx.x < 64) {
-        unsigned long long v = threadIdx.x < kSpread ? a[threadIdx.x][0] : 0ull;
-        for (int d = 32; d > 0; d >>= 1) {
-            const unsigned long long o = __shfl_xor(v, d, 64);
-            v = o > v ? o : v;
-        }
+        const unsigned long long v = wave_max(threadIdx.x < kSpread ? a[threadIdx.x][0] : 0ull);
         if (threadIdx.x == 0) *lds1 = v;
     }
     __syncthreads();
@@ -378,15 +372,7 @@ __global__ void __launch_bounds__(256) k_mvs_radix_decide(SampleState *__restric
         rc += cnt[j];
     }
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-    unsigned long long xf = rf, xc = rc;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const unsigned long long yf = __shfl_up(xf, d, 64), yc = __shfl_up(xc, d, 64);
-        if (lane >= d) {
-            xf += yf;
-            xc += yc;
-        }
-    }
+    const unsigned long long xf = wave_incl_sum(rf), xc = wave_incl_sum(rc);
     if (lane == 63) {
         s_wf[wid] = xf;
         s_wc[wid] = xc;
@@ -540,7 +526,7 @@ __global__ void __launch_bounds__(256) k_mvs_select(SampleSrc src, const int64_t
                 if (i0 + j < n) keep[i0 + j] = (uint8_t)((kb >> (8 * j)) & 1u);
         }
     }
-    for (int d = 32; d > 0; d >>= 1) cnt += __shfl_xor(cnt, d, 64);
+    cnt = wave_total(cnt);
     if ((threadIdx.x & 63) == 0) red4[threadIdx.x >> 6] = cnt;
     __syncthreads();
     if (threadIdx.x == 0 && tile_cnt) tile_cnt[blockIdx.x] = red4[0] + red4[1] + red4[2] + red4[3];
@@ -587,12 +573,7 @@ __global__ void __launch_bounds__(256)
     // exclusive scan of the per-thread counts across the block
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
     const int32_t cnt = __popc(bits);
-    int32_t x = cnt;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        int32_t y = __shfl_up(x, d, 64);
-        if (lane >= d) x += y;
-    }
+    const int32_t x = wave_incl_sum(cnt);
     if (lane == 63) lds4[wid] = x;
     __syncthreads();
     int32_t run = x - cnt;

@@ -1,6 +1,7 @@
 // scan.hip -- device-wide exclusive prefix sums (reduce, spine, downsweep).
 // Used by the compaction behind sampling and by the stable partition.
 #include "common.h"
+#include "wave_impl.h"
 
 namespace gbt {
 
@@ -13,12 +14,7 @@ constexpr int kScanTile = kScanThreads * kScanItems;
 __device__ inline int32_t block_exclusive_scan(int32_t v, int32_t *lds4, int32_t *total)
 {
     int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-    int32_t x = v;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        int32_t y = __shfl_up(x, d, 64);
-        if (lane >= d) x += y;
-    }
+    const int32_t x = wave_incl_sum(v);
     if (lane == 63) lds4[wid] = x;
     __syncthreads();
     int32_t off = 0, tot = 0;
@@ -62,12 +58,7 @@ __global__ void __launch_bounds__(1024) k_scan_spine(int32_t *__restrict__ bsum,
     for (int64_t base = 0; base < nb; base += 1024) {
         int64_t i = base + threadIdx.x;
         int32_t v = i < nb ? bsum[i] : 0;
-        int32_t x = v;
-#pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-            int32_t y = __shfl_up(x, d, 64);
-            if (lane >= d) x += y;
-        }
+        const int32_t x = wave_incl_sum(v);
         if (lane == 63) lds16[wid] = x;
         __syncthreads();
         int32_t off = carry, tot = 0;

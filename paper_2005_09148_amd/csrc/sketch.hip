@@ -3,6 +3,7 @@
 // summaries that are merged into the running summary (sketch_impl.h gives
 // the rules).  Every feature is independent: one segment, one block.
 #include "sketch_impl.h"
+#include "wave_impl.h"
 
 #include <algorithm>
 #include <cstring>
@@ -58,12 +59,7 @@ __global__ void __launch_bounds__(256)
     const int d = threadIdx.x, lane = d & 63, wid = d >> 6;
     uint32_t total = 0;
     for (int32_t t = t0; t < t1; ++t) total += hist[(int64_t)t * 256 + d];
-    uint32_t x = total;
-#pragma unroll
-    for (int s = 1; s < 64; s <<= 1) {
-        const uint32_t y = __shfl_up(x, s, 64);
-        if (lane >= s) x += y;
-    }
+    const uint32_t x = wave_incl_sum(total);
     if (lane == 63) wsum[wid] = x;
     __syncthreads();
     uint32_t base = x - total;
@@ -80,12 +76,7 @@ __global__ void __launch_bounds__(256)
 __device__ inline int32_t sort_block_scan(int32_t v, int32_t *wsum, int32_t *total)
 {
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-    int32_t x = v;
-#pragma unroll
-    for (int s = 1; s < 64; s <<= 1) {
-        const int32_t y = __shfl_up(x, s, 64);
-        if (lane >= s) x += y;
-    }
+    const int32_t x = wave_incl_sum(v);
     __syncthreads();
     if (lane == 63) wsum[wid] = x;
     __syncthreads();
@@ -162,12 +153,7 @@ constexpr int kSumThreads = 1024;
 __device__ inline int32_t sum_block_scan(int32_t v, int32_t *wsum, int32_t *total)
 {
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-    int32_t x = v;
-#pragma unroll
-    for (int s = 1; s < 64; s <<= 1) {
-        const int32_t y = __shfl_up(x, s, 64);
-        if (lane >= s) x += y;
-    }
+    const int32_t x = wave_incl_sum(v);
     __syncthreads();
     if (lane == 63) wsum[wid] = x;
     __syncthreads();
@@ -182,7 +168,7 @@ __device__ inline int32_t sum_block_scan(int32_t v, int32_t *wsum, int32_t *tota
 
 __device__ inline int64_t block_sum64(int64_t v, long long *wsum)
 {
-    for (int s = 32; s > 0; s >>= 1) v += __shfl_xor(v, s, 64);
+    v = wave_total(v);
     __syncthreads();
     if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = v;
     __syncthreads();
