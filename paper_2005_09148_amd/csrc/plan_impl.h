@@ -5,8 +5,9 @@
 // present children in heap order with their histogram slots, and for each
 // split parent the smaller child to build (chunked into work items) with the
 // larger one as parent minus it.  The chunk size is chosen so that the level
-// has at most `items` work items per feature group (one per workgroup slot),
-// unless it builds more nodes than that.
+// has at most `items` work items per feature group (one per workgroup slot)
+// while it builds at most items / 2 nodes, and at most items plus its node
+// count beyond that.
 #pragma once
 
 #include "split_impl.h"
@@ -211,10 +212,12 @@ __device__ void plan_level_block(DevNode *__restrict__ nodes, const PlanArgs &a)
         nodes_total += red_nodes[w];
     }
     // room for the chunks of large nodes: what the node count leaves of the
-    // target, but at least half of it (a level of many nodes may then take
-    // up to 1.5 times the target)
+    // target; a level of more than items / 2 nodes takes chunks of
+    // rows_total / items rows (nodes smaller than the target's share would
+    // otherwise take one chunk each and leave workgroup slots idle; up to
+    // items + nodes_total work items)
     const int64_t items = a.items;
-    const int64_t room = items - nodes_total > items / 2 ? items - nodes_total : (items / 2 > 1 ? items / 2 : 1);
+    const int64_t room = items - nodes_total > items / 2 ? items - nodes_total : items;
     int64_t chunk = ((int64_t)rows_total + room - 1) / room;
     chunk = chunk > kMinChunk ? chunk : kMinChunk;
     int32_t c_build = 0, c_part = 0;

@@ -606,12 +606,6 @@ __global__ void __launch_bounds__(kWalkTileRows)
     float *tl = (float *)(tn + nn);
     uint32_t *rb = (uint32_t *)(tl + nn);
     const bool dense = !geo.sparse;
-    for (int32_t t = threadIdx.x; t < nn; t += kWalkTileRows) {
-        uint2 c = compact[t];
-        if (dense && (c.y & 1u)) c.x *= (uint32_t)geo.w;
-        tn[t] = c;
-        tl[t] = leaf[t];
-    }
     constexpr int32_t ps = 4 * kQ + 1;  // odd row pitch in LDS
     const int64_t n_tiles = (rows + kWalkTileRows - 1) / kWalkTileRows;
     uint4 nxt[kQ];
@@ -627,8 +621,16 @@ __global__ void __launch_bounds__(kWalkTileRows)
         }
         mnext = (int32_t)threadIdx.x < nr ? margin[r0 + threadIdx.x] : 0.0f;
     };
+    // the first tile's rows are requested before the tree, so that their
+    // trip to memory overlaps the tree's (cached) loads
     int64_t tile = blockIdx.x;
     if (tile < n_tiles) load(tile);
+    for (int32_t t = threadIdx.x; t < nn; t += kWalkTileRows) {
+        uint2 c = compact[t];
+        if (dense && (c.y & 1u)) c.x *= (uint32_t)geo.w;
+        tn[t] = c;
+        tl[t] = leaf[t];
+    }
     for (; tile < n_tiles; tile += walk_blocks) {
         const int64_t r0 = tile * kWalkTileRows;
         const int32_t nr = (int32_t)min((int64_t)kWalkTileRows, rows - r0);
@@ -918,9 +920,10 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     const int32_t G = (int32_t)groups.size();
     const int64_t twg = hp.target_wgs;
     // work items per group and level: one per workgroup slot (more only when
-    // a level builds more nodes)
+    // a level builds more than items / 2 nodes: then up to items plus the
+    // node count)
     const int32_t items = (int32_t)std::max<int64_t>(1, twg / G);
-    const int32_t max_work = std::max(items, items / 2 + max_level_nodes) + 1;
+    const int32_t max_work = items + max_level_nodes + 1;
     auto al = [](size_t b) { return (b + 255) / 256 * 256; };
     const size_t o_ev1 = al((size_t)max_level_nodes * sizeof(EvalNode));
     const size_t o_cnt = o_ev1 + o_ev1;
