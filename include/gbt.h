@@ -54,7 +54,7 @@ typedef int32_t gbt_status;
 #define GBT_SAMPLE_SGB 1  /* stochastic gradient boosting: uniform rows */
 #define GBT_SAMPLE_GOSS 2 /* gradient-based one-side sampling */
 
-#define GBT_ABI_VERSION 5
+#define GBT_ABI_VERSION 6
 
 enum { GBT_INPUT_DENSE_F32 = 0, GBT_INPUT_CSR_F32 = 1 };
 enum { GBT_LOC_HOST = 0, GBT_LOC_DEVICE = 1 };
@@ -202,7 +202,9 @@ typedef struct {
     double ms_total;        /* wall time of the call */
     double h2d_bytes;       /* bytes streamed from pinned-host or disk pages */
     int32_t hist_kernel;    /* GBT_HIST_PLAIN or GBT_HIST_ROTATED (dense), 0 sparse */
-    int32_t pad0;
+    int32_t hist_cols;      /* 1: the root histogram pass also wrote the partition's column
+                               copy of the training page (2 bytes per symbol, counted in
+                               hist_bytes), 0: a kernel of its own did or none was made */
 } gbt_tree_stats;
 
 typedef struct {

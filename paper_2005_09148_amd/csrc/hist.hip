@@ -105,7 +105,8 @@ __global__ void __launch_bounds__(kHistThreads)
                  const longlong2 *__restrict__ q, const int32_t *__restrict__ rows,
                  const HistWork *__restrict__ work, const HistGroup *__restrict__ groups, int32_t n_groups,
                  const int32_t *__restrict__ n_work_d, const int32_t *__restrict__ bin_ptr, int64_t total_bins,
-                 longlong2 *__restrict__ partials, unsigned long long *__restrict__ n_updates)
+                 longlong2 *__restrict__ partials, unsigned long long *__restrict__ n_updates,
+                 uint16_t *__restrict__ cols, int64_t cols_n)
 {
     extern __shared__ unsigned long long lds[];
     const uint32_t active = n_work_d ? (uint32_t)(*n_work_d * n_groups) : gridDim.x;
@@ -165,6 +166,9 @@ __global__ void __launch_bounds__(kHistThreads)
                     sym = __builtin_amdgcn_alignbit(a[k + 1], a[k], (uint32_t)sft) & kMask;
                 const bool ok = sym != null_sym;
                 cnt += (unsigned int)__popcll(__ballot(ok));
+                // a pass over the page in row order also writes the column
+                // copy: cols[f * cols_n + row] = the row's symbol of feature f
+                if (!kRows && cols) cols[(int64_t)(gr.f0 + u) * cols_n + i] = (uint16_t)sym;
                 if (ok) {
                     unsigned long long *pg = (unsigned long long *)(base[u] + sym * 8u);
                     atomicAdd(pg, qg);
@@ -846,6 +850,9 @@ gbt_status hist_launch_device(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
     longlong2 *partials = (longlong2 *)hl.partials;
     if (!mx->sparse && (mx->w < 1 || mx->w > 12))
         return set_error(GBT_E_UNSUPPORTED, "dense symbols of %d bits", mx->w);
+    if (hl.cols)
+        GBT_CHECK(!rows && !mx->sparse && hl.kind == kHistDense,
+                  "a column copy from a histogram pass needs the plain dense kernel over the page in row order");
     if (hl.max_work > 0 && hl.kind == kHistRot) {
         const uint32_t null_sym = mx->has_missing ? mx->null_sym : 0xffffffffu;
         const unsigned grid = (unsigned)((size_t)hl.max_work * (size_t)G);
@@ -892,7 +899,7 @@ gbt_status hist_launch_device(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
     case WB: {                                                                                              \
         auto kfn = rows ? k_hist_dense<WB, true> : k_hist_dense<WB, false>;                                  \
         GBT_HIST_LAUNCH(kfn, grid, kHistThreads, lds, page, mx->row_words, null_sym, qq, rows, hl.work,       \
-                        hl.groups, G, hl.n_work_d, mx->bin_ptr_d, tb, partials, upd);                       \
+                        hl.groups, G, hl.n_work_d, mx->bin_ptr_d, tb, partials, upd, hl.cols, hl.cols_n);   \
         break;                                                                                              \
     }
             switch (mx->w) {

@@ -72,6 +72,11 @@ struct HistLaunch {
     const uint8_t *slot_tbl = nullptr;  // sparse: the page's slot table by row (SlotTable::row), or NULL
     int32_t tbl_stride = 0;
     bool timed = true;  // record phase events (when the context's timing is on)
+    // plain dense kernel, rows NULL (work items that cover the page's rows
+    // [0, cols_n) once): also write the page's column copy, cols[f * cols_n
+    // + r] = the symbol of feature f in row r (the layout split_columns makes)
+    uint16_t *cols = nullptr;
+    int64_t cols_n = 0;
 };
 
 // Device memory a histogram call carves its partials and plan from, in

@@ -984,13 +984,19 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     // copy of the training page, made once per tree (once per matrix when
     // the training page is the matrix's own device page)
     const uint16_t *cols = nullptr;
+    uint16_t *cols_root = nullptr;  // the copy the root histogram pass writes
     if (D >= 2 && R > 0 && split_columns_fit(mx) &&
         scratch_fits(c, kScrCols, (size_t)mx->m * (size_t)R * sizeof(uint16_t))) {
         uint16_t *cd;
         GBT_TRY(scratch_t(c, kScrCols, (size_t)mx->m * (size_t)R, &cd));
         const bool kept = so.alias && c->cols_uid == mx->uid && c->cols_page == so.page && c->cols_at == cd &&
                           c->cols_rows == R;
-        if (!kept) {
+        if (!kept && !so.alias && hp.kind == kHistDense) {
+            // a sampled page: the root pass of the plain kernel decodes every
+            // symbol of every row anyway and writes the copy as it goes
+            c->cols_uid = 0;
+            cols_root = cd;
+        } else if (!kept) {
             c->cols_uid = 0;
             GBT_TRY(split_columns(c, mx, so.page, R, cd));
             if (so.alias) {
@@ -1026,6 +1032,8 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     if (D > 0 && R > 0) {
         HistLaunch hl{hp.kind, groups_d, G, hp.max_groups_bins, work_d, nullptr, n_root, red_d, nullptr,
                       fused ? 0 : 1, partials, stbl.row, stbl.row_stride};
+        hl.cols = cols_root;  // the root's work items cover rows [0, R) once per group
+        hl.cols_n = R;
         GBT_TRY(hist_launch_device(c, mx, so.page, so.q, nullptr, hl, nullptr, histA, upd));
         ++hist_launches;
         if (fused) {
@@ -1160,14 +1168,17 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         stats->exp_key = res->e_key;
         stats->hist_updates = (int64_t)res->updates;
         // algorithmic bytes: the packed symbols of each row, its 16-byte
-        // fixed-point pair, its 4-byte row id below the root, and one write of
-        // every built node's histogram (the chunk partials are not counted)
+        // fixed-point pair, its 4-byte row id below the root, one write of
+        // every built node's histogram (the chunk partials are not counted),
+        // and the column copy when the root pass writes it (2 bytes per
+        // symbol)
         const int64_t wbytes = 4 * (((int64_t)mx->stride * mx->w + 31) / 32);
         const int64_t root_built = (D > 0 && R > 0) ? 1 : 0;
         stats->hist_launches = hist_launches;
         stats->hist_rows = (D > 0 ? R : 0) + (int64_t)res->rows_built;
         stats->hist_bytes = (D > 0 ? R : 0) * (wbytes + 16) + (int64_t)res->rows_built * (wbytes + 20) +
-                            (root_built + (int64_t)res->built) * mx->total_bins * 16;
+                            (root_built + (int64_t)res->built) * mx->total_bins * 16 +
+                            (cols_root ? 2 * (int64_t)mx->m * R : 0);
         stats->ms_sample = ms[kPhSample];
         stats->ms_hist = ms[kPhHist];
         stats->ms_hist_aux = ms[kPhHistAux];
@@ -1175,6 +1186,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         stats->ms_margin = ms[kPhMargin];
         stats->h2d_bytes = h2d;
         stats->hist_kernel = hp.kind == kHistRot ? GBT_HIST_ROTATED : (hp.kind == kHistDense ? GBT_HIST_PLAIN : 0);
+        stats->hist_cols = cols_root ? 1 : 0;
         stats->ms_total =
             std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t_start).count();
     }

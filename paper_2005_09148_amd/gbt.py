@@ -122,7 +122,7 @@ class TreeStats(C.Structure):
                 ("hist_updates", C.c_int64), ("hist_bytes", C.c_int64), ("ms_hist", C.c_double),
                 ("ms_hist_aux", C.c_double), ("ms_sample", C.c_double), ("ms_split", C.c_double),
                 ("ms_margin", C.c_double), ("ms_total", C.c_double), ("h2d_bytes", C.c_double),
-                ("hist_kernel", C.c_int32), ("pad0", C.c_int32)]
+                ("hist_kernel", C.c_int32), ("hist_cols", C.c_int32)]
 
 
 class SampleParams(C.Structure):
