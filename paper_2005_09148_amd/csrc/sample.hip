@@ -250,7 +250,9 @@ __global__ void __launch_bounds__(256) k_mvs_keys(SampleSrc src, int64_t n, doub
 // may be NULL) receives 1 for the closed form, else 0.  check_log2n >= 0:
 // the key sums were formed with the exponent in st->e_key, which is first
 // checked against the one max r gives (e = 62 - E - check_log2n); when they
-// differ nothing else is done and done_host receives 2.
+// differ nothing else is done and done_host receives 2.  The flag is a
+// relaxed store: the host reads nothing else this kernel writes (the
+// kernels it queues after reading the flag see the rest in stream order).
 __global__ void k_mvs_thresh_init(SampleState *__restrict__ st, int64_t K, int32_t *__restrict__ done_host,
                                   int32_t count_mode, int32_t check_log2n)
 {
@@ -259,7 +261,7 @@ __global__ void k_mvs_thresh_init(SampleState *__restrict__ st, int64_t K, int32
         int E;
         frexp(sqrt(__longlong_as_double(fold_max(st->rmax))), &E);
         if (62 - E - check_log2n != st->e_key) {
-            if (done_host) __hip_atomic_store(done_host, 2, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+            if (done_host) __hip_atomic_store(done_host, 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
             return;
         }
     }
@@ -274,10 +276,10 @@ __global__ void k_mvs_thresh_init(SampleState *__restrict__ st, int64_t K, int32
                            : (long long)((asum + (unsigned long long)K - 1) / (unsigned long long)K);
         st->done = 1;
         st->levels = 0;
-        if (done_host) __hip_atomic_store(done_host, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+        if (done_host) __hip_atomic_store(done_host, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
         return;
     }
-    if (done_host) __hip_atomic_store(done_host, 0, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+    if (done_host) __hip_atomic_store(done_host, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     int S = 64 - __clzll((long long)(amax + 1));  // 2^S > amax + 1
     int levels = (S + kDigitBits - 1) / kDigitBits;
     st->shift = (levels - 1) * kDigitBits;

@@ -741,6 +741,16 @@ __device__ inline void part_load(const int32_t *__restrict__ rows, const int32_t
     }
 }
 
+// The root level's slots: slot i holds row i, all in node 0 (no arrays read).
+__device__ inline void part_root(int64_t i0, int64_t n, int32_t r[kPartItems], int32_t nid[kPartItems])
+{
+#pragma unroll
+    for (int k = 0; k < kPartItems; ++k) {
+        r[k] = i0 + k < n ? (int32_t)(i0 + k) : 0;
+        nid[k] = i0 + k < n ? 0 : -1;
+    }
+}
+
 // The split choice of one node, made by one wave from the node's candidates
 // (one per feature): the highest gain, equal gains to the lowest feature; the
 // node splits when that gain is positive.  Returns {split, feature,
@@ -792,12 +802,15 @@ __global__ void __launch_bounds__(kPartThreads)
                        const int32_t *__restrict__ position, const int32_t *__restrict__ slot_node,
                        DevNode *__restrict__ nodes, uint8_t *__restrict__ flags,
                        int32_t *__restrict__ tile_cnt, LevelChoice lc, SlotTable stbl,
-                       const uint16_t *__restrict__ cols)
+                       const uint16_t *__restrict__ cols, int32_t root)
 {
     __shared__ int32_t red[kPartThreads / 64];
     const int64_t i0 = (int64_t)blockIdx.x * kPartTile + (int64_t)threadIdx.x * kPartItems;
     int32_t r[kPartItems], nid[kPartItems];
-    part_load(rows, position, slot_node, i0, n, r, nid);
+    if (root)
+        part_root(i0, n, r, nid);
+    else
+        part_load(rows, position, slot_node, i0, n, r, nid);
     int4 rec[kPartItems];  // {split, feature, split_bin, default_left}
     if (kChoose) {
         const int lane = threadIdx.x & 63;
@@ -866,8 +879,8 @@ __global__ void __launch_bounds__(kPartThreads)
         // to its last slot, written by the tile holding that slot (the plan
         // adds the counts of the tiles before); a node's slots are one run
         // of equal slot nodes
-        const int32_t prev = i0 > 0 && i0 <= n ? slot_node[i0 - 1] : -2;
-        const int32_t next = i0 + kPartItems < n ? slot_node[i0 + kPartItems] : -2;
+        const int32_t prev = i0 > 0 && i0 <= n ? (root ? 0 : slot_node[i0 - 1]) : -2;
+        const int32_t next = i0 + kPartItems < n ? (root ? 0 : slot_node[i0 + kPartItems]) : -2;
         int32_t tot;
         int32_t pre = part_block_scan(cnt, red, &tot);
 #pragma unroll
@@ -1030,7 +1043,7 @@ __global__ void __launch_bounds__(kPartThreads)
     k_part_scatter_rev(const int32_t *__restrict__ rows, int64_t n, const uint8_t *__restrict__ flags,
                        const int32_t *__restrict__ tile_cnt, const long long *__restrict__ tile_off,
                        const int32_t *__restrict__ slot_node, int32_t *__restrict__ slot_node_out,
-                       DevNode *__restrict__ nodes, int32_t *__restrict__ rows_out, PlanArgs pa)
+                       DevNode *__restrict__ nodes, int32_t *__restrict__ rows_out, int32_t root, PlanArgs pa)
 {
     if (blockIdx.x == 0) {
         pa.tile_cnt = tile_cnt;
@@ -1047,7 +1060,10 @@ __global__ void __launch_bounds__(kPartThreads)
     const int64_t ts = tile * kPartTile;
     const int64_t i0 = ts + (int64_t)threadIdx.x * kPartItems;
     int32_t r[kPartItems], nid[kPartItems];
-    part_load(rows, nullptr, slot_node, i0, n, r, nid);
+    if (root)
+        part_root(i0, n, r, nid);
+    else
+        part_load(rows, nullptr, slot_node, i0, n, r, nid);
     uint32_t f4 = 0;
     if (i0 + kPartItems <= n) {
         f4 = *(const uint32_t *)(flags + i0);
@@ -1058,7 +1074,7 @@ __global__ void __launch_bounds__(kPartThreads)
     }
     const int32_t mine = (int32_t)((f4 & 1u) + ((f4 >> 8) & 1u) + ((f4 >> 16) & 1u) + ((f4 >> 24) & 1u));
     // the node of the tile's first slot, when it starts in an earlier tile
-    const int32_t n0 = slot_node[ts];
+    const int32_t n0 = root ? 0 : slot_node[ts];
     const int64_t b0 = n0 >= 0 ? nodes[n0].begin : ts;
     const bool ext = b0 < ts;
     const int64_t tb = b0 / kPartTile;  // its first tile
@@ -1244,7 +1260,7 @@ gbt_status split_columns(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page,
 gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int32_t *rows,
                               int64_t n, const int32_t *slot_node, int32_t *slot_node_out, DevNode *nodes,
                               int32_t *rows_out, const LevelChoice *choice, const SlotTable *stbl,
-                              const uint16_t *cols, const PlanArgs &plan, bool order)
+                              const uint16_t *cols, const PlanArgs &plan, bool order, bool root)
 {
     if (n == 0) return GBT_OK;
     const SlotTable st = stbl ? *stbl : SlotTable{nullptr, nullptr, nullptr, 0, 0, 0};
@@ -1256,10 +1272,11 @@ gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
     GBT_TRY(scratch_t(c, kScrScan, (size_t)tiles + 1, &tile_cnt));
     if (choice)
         k_part_flags_tiles<true, true><<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(
-            rows, n, page, geo_of(mx), nullptr, slot_node, nodes, flags, tile_cnt, *choice, st, cols);
+            rows, n, page, geo_of(mx), nullptr, slot_node, nodes, flags, tile_cnt, *choice, st, cols, root ? 1 : 0);
     else
         k_part_flags_tiles<false, true><<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(
-            rows, n, page, geo_of(mx), nullptr, slot_node, nodes, flags, tile_cnt, LevelChoice{}, st, cols);
+            rows, n, page, geo_of(mx), nullptr, slot_node, nodes, flags, tile_cnt, LevelChoice{}, st, cols,
+            root ? 1 : 0);
     GBT_LAUNCHED();
     // many tiles: one block scans the tile counts first, instead of every
     // block summing the counts before it
@@ -1271,7 +1288,7 @@ gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
     }
     // without the row order only the plan block runs
     k_part_scatter_rev<<<(unsigned)((order ? tiles : 0) + 1), kPartThreads, 0, c->stream>>>(
-        rows, n, flags, tile_cnt, tile_off, slot_node, slot_node_out, nodes, rows_out, plan);
+        rows, n, flags, tile_cnt, tile_off, slot_node, slot_node_out, nodes, rows_out, root ? 1 : 0, plan);
     GBT_LAUNCHED();
     return GBT_OK;
 }
@@ -1294,7 +1311,7 @@ gbt_status partition_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page
     k_part_flags_tiles<false, false><<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(rows, n, page, geo, position, slot_node,
                                                                        nodes, flags, tile_off, LevelChoice{},
                                                                        SlotTable{nullptr, nullptr, nullptr, 0, 0, 0},
-                                                                       nullptr);
+                                                                       nullptr, 0);
     GBT_LAUNCHED();
     if (n_list > 0) {
         k_part_bounds<<<(unsigned)n_list, kBoundThreads, 0, c->stream>>>(list, n_list_d, n_list, nodes, flags,

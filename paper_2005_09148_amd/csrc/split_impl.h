@@ -92,7 +92,9 @@ struct PlanArgs;
 // in one of its blocks, runs the level's `plan` (plan_impl.h), which turns
 // those into the nodes' left counts (nleft; pleft is not written) and the
 // children's records.  `order` false skips the rows' new order (rows_out and
-// slot_node_out are not written) and runs the plan alone.  With `choice`, the split
+// slot_node_out are not written) and runs the plan alone.  `root`: the root
+// level, whose slots are rows 0..n-1 of node 0 (rows and slot_node are not
+// read).  With `choice`, the split
 // records of the level's nodes are chosen from the candidates and written
 // by the first kernel (instead of by eval_reduce_impl).  With `stbl` (a
 // sparse page's slot table), the search for a row's split feature looks
@@ -104,7 +106,7 @@ gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
                               int64_t n, const int32_t *slot_node, int32_t *slot_node_out, DevNode *nodes,
                               int32_t *rows_out, const LevelChoice *choice,
                               const SlotTable *stbl, const uint16_t *cols, const PlanArgs &plan,
-                              bool order);
+                              bool order, bool root);
 
 // Whether a page of mx's geometry takes a column copy (dense, symbols of at
 // most 16 bits).

@@ -358,10 +358,11 @@ __global__ void k_tree_init(DevNode *__restrict__ nodes, int32_t n_nodes, const 
                             int64_t R, EvalNode *__restrict__ level, int32_t *__restrict__ cnt,
                             HistWork *__restrict__ work, HistReduce *__restrict__ red, int64_t chunk,
                             int32_t n_root, int32_t *__restrict__ rows, int32_t *__restrict__ slot_node,
-                            unsigned long long *__restrict__ upd, unsigned long long *__restrict__ stat)
+                            int64_t n_slots, unsigned long long *__restrict__ upd,
+                            unsigned long long *__restrict__ stat)
 {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < R) {
+    if (i < n_slots) {  // the root's slots (the root level's partition does not read them)
         rows[i] = (int32_t)i;
         slot_node[i] = 0;
     }
@@ -1010,9 +1011,13 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     }
     int64_t *partials = nullptr;
     GBT_TRY(scratch(c, kScrPartialsDev, (size_t)std::max(max_items, 1) * mx->total_bins * 16, (void **)&partials));
-    const int64_t n_init = std::max<int64_t>({(int64_t)NN, (int64_t)n_root, R, (int64_t)kUpdCounters});
+    // the root's slot arrays only for a tree without levels (whose leaves
+    // may be added at the slots' rows); the root level's partition takes
+    // slot i as row i of node 0 without reading them
+    const int64_t n_slots = D == 0 ? R : 0;
+    const int64_t n_init = std::max<int64_t>({(int64_t)NN, (int64_t)n_root, n_slots, (int64_t)kUpdCounters});
     k_tree_init<<<blocks(n_init), 256, 0, c->stream>>>(nodes, NN, so.st, R, evA, cnt, work_d, red_d, root_chunk,
-                                                       n_root, rows, slot_node, upd, stat);
+                                                       n_root, rows, slot_node, n_slots, upd, stat);
     GBT_LAUNCHED();
     EvalParams ep{p->lambda, p->gamma, p->min_child_weight, 0, 0, e_dev};
     // features of at most 256 bins: each histogram pass ends with the fused
@@ -1065,7 +1070,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         if (last) pa.lv = LeafArgs{leaf, compact, e_dev, p->lambda, p->eta, NN, 0};
         GBT_TRY(partition_rev_impl(c, mx, so.page, rows, R, slot_node, slot_tmp, nodes, rows_tmp,
                                    choose ? &lc : nullptr, stbl.row ? &stbl : nullptr, cols, pa,
-                                   !last || final_order));
+                                   !last || final_order, d == 0));
         std::swap(rows, rows_tmp);
         std::swap(slot_node, slot_tmp);
         timer_end(c, mark);
