@@ -762,7 +762,8 @@ def test_trees_many_partition_tiles(gbt, ctx):
     assert_same_trees(*r[:4])
 
 
-@pytest.mark.parametrize("depth,n", [(0, 1000), (1, 65), (3, 1), (4, 63)])
+@pytest.mark.parametrize("depth,n", [(0, 1000), (1, 65), (3, 1), (4, 63),
+                                     (3, 1025), (5, 2049), (2, 4097)])  # sampled pages near partition-tile edges
 def test_degenerate_trees(gbt, ctx, hist_kernel, depth, n):
     cfg = datagen.TrainConfig("t", 1, 32, depth, 2, eta=0.5, f=0.5 if n > 10 else 1.0)
     d = datagen.config3(n=n, m=6)
