@@ -982,8 +982,9 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         stbl = SlotTable{tb, tc, (const uint8_t *)mx->groups_d + fg_off, R, rs, 0};
     }
     // dense pages: the partition reads each row's split symbol from a column
-    // copy of the training page, made once per tree (once per matrix when
-    // the training page is the matrix's own device page)
+    // copy of the training page, made once per tree (by the root histogram
+    // pass for a sampled page of the plain kernel, else by split_columns;
+    // once per matrix when the training page is the matrix's own device page)
     const uint16_t *cols = nullptr;
     uint16_t *cols_root = nullptr;  // the copy the root histogram pass writes
     if (D >= 2 && R > 0 && split_columns_fit(mx) &&
