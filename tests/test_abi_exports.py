@@ -40,6 +40,21 @@ def test_binding_signatures_cover_the_header():
     assert set(gbt.SIGNATURES) == set(declared_functions())
 
 
+def test_binding_fails_loudly_without_the_library(tmp_path):
+    # a copy of the binding whose package holds no libgbt.so must refuse to
+    # import (there is no fallback path that would run without the kernels)
+    import shutil
+    import subprocess
+    import sys
+    pkg = tmp_path / "gbtcopy"
+    pkg.mkdir()
+    (pkg / "__init__.py").write_text("")
+    shutil.copy(os.path.join(ROOT, "paper_2005_09148_amd", "gbt.py"), pkg / "gbt.py")
+    r = subprocess.run([sys.executable, "-c", "import gbtcopy.gbt"], cwd=tmp_path, capture_output=True, text=True)
+    assert r.returncode != 0
+    assert "ImportError" in r.stderr and "is not built" in r.stderr
+
+
 def test_oracle_is_not_imported_by_the_product():
     pkg = os.path.join(ROOT, "paper_2005_09148_amd")
     for dirpath, _, files in os.walk(pkg):
