@@ -893,3 +893,52 @@ def test_mvs_key_exponent_guess_both_ways(gbt, ctx):
         assert t.stats.threshold == o.info.T
         assert same_bits(mg.cpu().numpy(), margin)
     mx.free()
+
+
+# ------------------------------------------------------------ seeded configuration sweep
+def random_case(seed):
+    """A seeded random workload and its hyperparameters: dense or CSR,
+    1 to 20,000 rows, 1 to 60 features, 2 to 256 bins, depth 0 to 8, either
+    loss, MVS fractions from 0.05 to 1, and the regularisation terms varied."""
+    r = np.random.default_rng(1000 + seed)
+    u = r.random()
+    n = int(r.choice([1, 7, 300, 1025])) if u < 0.3 else int(r.integers(2000, 20_001 if u < 0.85 else 60_001))
+    m = int(r.integers(1, 61))
+    loss = int(r.integers(0, 2))
+    sparse = bool(r.random() < 0.25) and m >= 4
+    if sparse:
+        data, X = small_csr(n, m, float(r.uniform(0.05, 0.6)), 2000 + seed)
+        max_bin = int(r.choice([2, 16, 64]))
+    else:
+        X = dense_case(2000 + seed, n, m, float(r.choice([0.0, 0.0, 0.1, 0.4])),
+                       str(r.choice(["normal", "uniform", "ties"])))
+        data = X
+        max_bin = int(r.choice([2, 3, 17, 64, 200, 256]))
+    signal = np.nan_to_num(X[:, 0]) + 0.5 * np.nan_to_num(X[:, -1])
+    if loss == datagen.LOSS_LOGISTIC:
+        y = (signal + r.normal(size=n) > np.median(signal)).astype(np.float32)
+    else:
+        y = (signal + r.normal(size=n)).astype(np.float32)
+    cfg = datagen.TrainConfig("sweep", loss, max_bin, int(r.integers(0, 9)), 2,
+                              eta=float(r.choice([0.05, 0.3, 1.0])), lambda_=float(r.choice([0.0, 1.0, 5.0])),
+                              gamma=float(r.choice([0.0, 0.0, 0.2])),
+                              min_child_weight=float(r.choice([0.0, 1.0, 3.0])),
+                              f=float(r.choice([1.0, 0.5, 0.2, 0.05])),
+                              mvs_lambda=float(r.choice([0.1, 1.0, 4.0])), seed=int(r.integers(0, 1 << 30)))
+    if cfg.lambda_ == 0.0 and cfg.min_child_weight == 0.0:
+        cfg.min_child_weight = 1.0  # keep H_L + lambda > 0 in every admissible split
+    if cfg.lambda_ == 0.0 and cfg.f < 1.0:
+        cfg.lambda_ = 1.0  # an empty sample's root leaf is -0 / (0 + lambda)
+    # a fifth of the cases keep their pages in pinned host memory
+    page_rows = int(r.integers(300, max(n, 301) + 1)) if r.random() < 0.2 else 0
+    return data, y, cfg, page_rows
+
+
+@pytest.mark.parametrize("seed", range(64))
+def test_random_configs_match_oracle(gbt, ctx, seed):
+    data, y, cfg, page_rows = random_case(seed)
+    print(f"[sweep] seed {seed}: n {len(y)}, page_rows {page_rows}, {cfg}", flush=True)
+    trees, margin, otrees, omargin, _, _ = train_both(
+        gbt, ctx, data, y, cfg, cfg.n_trees, page_rows=page_rows,
+        home=gbt.HOME_PINNED_HOST if page_rows else 0)
+    assert_same_trees(trees, margin, otrees, omargin)
