@@ -499,18 +499,19 @@ def test_partition_reports_malformed_entries(gbt, ctx):
 
 
 # ------------------------------------------------------------ whole trees
-def train_both(gbt, ctx, data, y, cfg, n_trees, page_rows=0, home=0, budget_ctx=None, page_dir=None):
+def train_both(gbt, ctx, data, y, cfg, n_trees, page_rows=0, home=0, budget_ctx=None, page_dir=None,
+               sampler=0, goss_a=0.0):
     c = budget_ctx or ctx
     mb = cfg.max_bin
     _, b, _, _ = oracle_quantize(data, mb)
     mx = gbt.gbt_quantize(c, data, max_bin=mb, page_rows=page_rows, page_home=home, page_dir=page_dir)
     P = gbt.make_train_params(loss=cfg.loss, max_depth=cfg.max_depth, eta=cfg.eta, lambda_=cfg.lambda_,
                               gamma=cfg.gamma, min_child_weight=cfg.min_child_weight, f=cfg.f,
-                              mvs_lambda=cfg.mvs_lambda, seed=cfg.seed)
+                              mvs_lambda=cfg.mvs_lambda, seed=cfg.seed, sampler=sampler, goss_a=goss_a)
     trees, margin = gbt.train(c, mx, torch.from_numpy(y).cuda(), P, n_trees, cfg.base_margin)
     OP = orc.Params(loss=cfg.loss, max_depth=cfg.max_depth, eta=cfg.eta, lambda_=cfg.lambda_,
                     gamma=cfg.gamma, min_child_weight=cfg.min_child_weight, f=cfg.f,
-                    mvs_lambda=cfg.mvs_lambda, seed=cfg.seed)
+                    mvs_lambda=cfg.mvs_lambda, seed=cfg.seed, sampler=sampler, goss_a=goss_a)
     otrees, omargin = orc.train(b, y, OP, n_trees, cfg.base_margin)
     return trees, margin.cpu().numpy(), otrees, omargin, mx, b
 
@@ -941,4 +942,25 @@ def test_random_configs_match_oracle(gbt, ctx, seed):
     trees, margin, otrees, omargin, _, _ = train_both(
         gbt, ctx, data, y, cfg, cfg.n_trees, page_rows=page_rows,
         home=gbt.HOME_PINNED_HOST if page_rows else 0)
+    assert_same_trees(trees, margin, otrees, omargin)
+
+
+@pytest.mark.parametrize("seed", range(64, 96))
+def test_random_samplers_and_kernels_match_oracle(gbt, ctx, seed):
+    # the same sweep with SGB and GOSS as well, and the dense histogram
+    # kernel chosen at random (automatic, plain or rotated)
+    data, y, cfg, page_rows = random_case(seed)
+    r = np.random.default_rng(5000 + seed)
+    sampler = int(r.choice([gbt.SAMPLE_MVS, gbt.SAMPLE_SGB, gbt.SAMPLE_GOSS])) if cfg.f < 1.0 else gbt.SAMPLE_MVS
+    goss_a = float(cfg.f * r.choice([0.1, 0.5, 0.9])) if sampler == gbt.SAMPLE_GOSS else 0.0
+    kernel = [ctx.HIST_AUTO, ctx.HIST_PLAIN, ctx.HIST_ROTATED][int(r.integers(0, 3))]
+    print(f"[sweep] seed {seed}: n {len(y)}, sampler {sampler}, goss_a {goss_a}, kernel {kernel}, "
+          f"page_rows {page_rows}, {cfg}", flush=True)
+    ctx.set_hist_kernel(kernel)
+    try:
+        trees, margin, otrees, omargin, _, _ = train_both(
+            gbt, ctx, data, y, cfg, cfg.n_trees, page_rows=page_rows,
+            home=gbt.HOME_PINNED_HOST if page_rows else 0, sampler=sampler, goss_a=goss_a)
+    finally:
+        ctx.set_hist_kernel(ctx.HIST_AUTO)
     assert_same_trees(trees, margin, otrees, omargin)
