@@ -542,8 +542,8 @@ def main():
                      "avg_launch_us": round(hms * 1e3 / max(launches, 1), 2),
                      "algorithmic_bytes_per_launch": hbytes // max(launches, 1),
                      # of which the partition's column copy of the sampled page,
-                     # written by the root pass (2 bytes per symbol)
-                     "column_copy_bytes_per_launch": sum(2 * m * s.n_sampled for s in estats if s.hist_cols)
+                     # written by the root pass (1 or 2 bytes per symbol)
+                     "column_copy_bytes_per_launch": sum(s.hist_cols * m * s.n_sampled for s in estats)
                                                      // max(launches, 1),
                      "timing": f"start and end events of every histogram launch, filled by the launch itself "
                                f"(hipExtLaunchKernel), over {args.steps} further timed trees "

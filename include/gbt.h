@@ -202,9 +202,10 @@ typedef struct {
     double ms_total;        /* wall time of the call */
     double h2d_bytes;       /* bytes streamed from pinned-host or disk pages */
     int32_t hist_kernel;    /* GBT_HIST_PLAIN or GBT_HIST_ROTATED (dense), 0 sparse */
-    int32_t hist_cols;      /* 1: the root histogram pass also wrote the partition's column
-                               copy of the training page (2 bytes per symbol, counted in
-                               hist_bytes), 0: a kernel of its own did or none was made */
+    int32_t hist_cols;      /* bytes per symbol (1 or 2) of the partition's column copy of
+                               the training page when the root histogram pass also wrote it
+                               (counted in hist_bytes); 0: a kernel of its own did or none
+                               was made */
 } gbt_tree_stats;
 
 typedef struct {

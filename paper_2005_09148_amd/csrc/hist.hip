@@ -105,8 +105,7 @@ __global__ void __launch_bounds__(kHistThreads)
                  const longlong2 *__restrict__ q, const int32_t *__restrict__ rows,
                  const HistWork *__restrict__ work, const HistGroup *__restrict__ groups, int32_t n_groups,
                  const int32_t *__restrict__ n_work_d, const int32_t *__restrict__ bin_ptr, int64_t total_bins,
-                 longlong2 *__restrict__ partials, unsigned long long *__restrict__ n_updates,
-                 uint16_t *__restrict__ cols, int64_t cols_n)
+                 longlong2 *__restrict__ partials, unsigned long long *__restrict__ n_updates, ColCopy cols)
 {
     extern __shared__ unsigned long long lds[];
     const uint32_t active = n_work_d ? (uint32_t)(*n_work_d * n_groups) : gridDim.x;
@@ -167,8 +166,14 @@ __global__ void __launch_bounds__(kHistThreads)
                 const bool ok = sym != null_sym;
                 cnt += (unsigned int)__popcll(__ballot(ok));
                 // a pass over the page in row order also writes the column
-                // copy: cols[f * cols_n + row] = the row's symbol of feature f
-                if (!kRows && cols) cols[(int64_t)(gr.f0 + u) * cols_n + i] = (uint16_t)sym;
+                // copy: entry (f, row) for each feature f of the group
+                if (!kRows && cols.p) {
+                    const int64_t e = (int64_t)(gr.f0 + u) * cols.stride + i;
+                    if (cols.bytes == 1)
+                        ((uint8_t *)cols.p)[e] = col_byte(sym, null_sym);
+                    else
+                        ((uint16_t *)cols.p)[e] = (uint16_t)sym;
+                }
                 if (ok) {
                     unsigned long long *pg = (unsigned long long *)(base[u] + sym * 8u);
                     atomicAdd(pg, qg);
@@ -850,8 +855,8 @@ gbt_status hist_launch_device(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
     longlong2 *partials = (longlong2 *)hl.partials;
     if (!mx->sparse && (mx->w < 1 || mx->w > 12))
         return set_error(GBT_E_UNSUPPORTED, "dense symbols of %d bits", mx->w);
-    if (hl.cols)
-        GBT_CHECK(!rows && !mx->sparse && hl.kind == kHistDense,
+    if (hl.cols.p)
+        GBT_CHECK(!rows && !mx->sparse && hl.kind == kHistDense && (hl.cols.bytes == 1 || hl.cols.bytes == 2),
                   "a column copy from a histogram pass needs the plain dense kernel over the page in row order");
     if (hl.max_work > 0 && hl.kind == kHistRot) {
         const uint32_t null_sym = mx->has_missing ? mx->null_sym : 0xffffffffu;
@@ -899,7 +904,7 @@ gbt_status hist_launch_device(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *
     case WB: {                                                                                              \
         auto kfn = rows ? k_hist_dense<WB, true> : k_hist_dense<WB, false>;                                  \
         GBT_HIST_LAUNCH(kfn, grid, kHistThreads, lds, page, mx->row_words, null_sym, qq, rows, hl.work,       \
-                        hl.groups, G, hl.n_work_d, mx->bin_ptr_d, tb, partials, upd, hl.cols, hl.cols_n);   \
+                        hl.groups, G, hl.n_work_d, mx->bin_ptr_d, tb, partials, upd, hl.cols);             \
         break;                                                                                              \
     }
             switch (mx->w) {

@@ -55,6 +55,22 @@ struct HistPlan {
 // feature does not fit any kernel.
 gbt_status hist_plan(const gbt_matrix *mx, int64_t rows_hint, int choice, HistPlan *out);
 
+// The partition's column copy of a dense training page: m columns of
+// `stride` entries, entry (f, r) the symbol of feature f in row r.  One
+// byte per entry when every feature has at most 256 bins: 255 for a missing
+// value, min(symbol, 254) otherwise (a reader whose split bin exceeds 254
+// takes an entry of 254 from the row itself); else two bytes, the symbol.
+struct ColCopy {
+    void *p = nullptr;
+    int64_t stride = 0;
+    int32_t bytes = 0;
+};
+
+__device__ __host__ inline uint8_t col_byte(uint32_t sym, uint32_t null_sym)
+{
+    return (uint8_t)(sym == null_sym ? 255u : (sym < 254u ? sym : 254u));
+}
+
 // A histogram pass whose work lists live on the device.  Counts are read
 // from device memory (n_work_d, n_red_d); the grids are sized by the maxima.
 struct HistLaunch {
@@ -73,10 +89,9 @@ struct HistLaunch {
     int32_t tbl_stride = 0;
     bool timed = true;  // record phase events (when the context's timing is on)
     // plain dense kernel, rows NULL (work items that cover the page's rows
-    // [0, cols_n) once): also write the page's column copy, cols[f * cols_n
-    // + r] = the symbol of feature f in row r (the layout split_columns makes)
-    uint16_t *cols = nullptr;
-    int64_t cols_n = 0;
+    // [0, cols.stride) once): also write the page's column copy (the layout
+    // split_columns makes)
+    ColCopy cols;
 };
 
 // Device memory a histogram call carves its partials and plan from, in

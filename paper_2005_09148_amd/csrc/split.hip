@@ -801,8 +801,8 @@ __global__ void __launch_bounds__(kPartThreads)
     k_part_flags_tiles(const int32_t *__restrict__ rows, int64_t n, const uint32_t *__restrict__ page, Geo geo,
                        const int32_t *__restrict__ position, const int32_t *__restrict__ slot_node,
                        DevNode *__restrict__ nodes, uint8_t *__restrict__ flags,
-                       int32_t *__restrict__ tile_cnt, LevelChoice lc, SlotTable stbl,
-                       const uint16_t *__restrict__ cols, int32_t root)
+                       int32_t *__restrict__ tile_cnt, LevelChoice lc, SlotTable stbl, ColCopy cols,
+                       int32_t root)
 {
     __shared__ int32_t red[kPartThreads / 64];
     const int64_t i0 = (int64_t)blockIdx.x * kPartTile + (int64_t)threadIdx.x * kPartItems;
@@ -851,9 +851,17 @@ __global__ void __launch_bounds__(kPartThreads)
         if (rec[k].x) {
             const uint32_t *row = page + (int64_t)r[k] * geo.row_words;
             int32_t b;
-            if (cols) {
-                const uint32_t s = cols[(int64_t)rec[k].y * n + r[k]];
-                b = s == geo.null_sym ? -1 : (int32_t)s;
+            if (cols.p) {
+                const int64_t e = (int64_t)rec[k].y * cols.stride + r[k];
+                if (cols.bytes == 1) {
+                    // 255: missing; 254: bin 254 or above, read from the row
+                    // when the split bin is above 254
+                    const uint32_t s = ((const uint8_t *)cols.p)[e];
+                    b = s == 255u ? -1 : (s == 254u && rec[k].z > 254 ? row_feature_bin(row, geo, rec[k].y) : (int32_t)s);
+                } else {
+                    const uint32_t s = ((const uint16_t *)cols.p)[e];
+                    b = s == geo.null_sym ? -1 : (int32_t)s;
+                }
             } else {
                 if (stbl.col) {
                     const uint32_t se = stbl.col[(int64_t)stbl.feat_grp[rec[k].y] * stbl.rows + r[k]];
@@ -1201,15 +1209,16 @@ __global__ void __launch_bounds__(kTileScanThreads)
     }
 }
 
-// Column copy of a dense page: cols[f * n + r] = symbol of feature f in row
-// r.  A block stages 256 consecutive rows in LDS (an odd pitch keeps the
-// threads' reads on distinct banks) and writes each feature's 256 symbols
-// with consecutive 2-byte stores.
+// Column copy of a dense page (ColCopy: entry (f, r) at f * stride + r).  A
+// block stages 256 consecutive rows in LDS (an odd pitch keeps the threads'
+// reads on distinct banks) and writes each feature's 256 entries with
+// consecutive stores.
 constexpr int kColRows = 256;
 
+template <typename T>
 __global__ void __launch_bounds__(kColRows)
     k_page_columns(const uint32_t *__restrict__ page, int64_t n, int32_t row_words, int32_t m, int32_t w,
-                   uint32_t mask, uint16_t *__restrict__ cols)
+                   uint32_t mask, uint32_t null_sym, T *__restrict__ cols, int64_t stride)
 {
     extern __shared__ uint32_t rows_l[];  // kColRows x (row_words | 1)
     const int64_t r0 = (int64_t)blockIdx.x * kColRows;
@@ -1235,24 +1244,42 @@ __global__ void __launch_bounds__(kColRows)
     __syncthreads();
     if ((int32_t)threadIdx.x >= nr) return;
     const uint32_t *row = rows_l + threadIdx.x * lw;
-    uint16_t *dst = cols + r0 + threadIdx.x;
+    T *dst = cols + r0 + threadIdx.x;
     for (int32_t f = 0; f < m; ++f) {
         const uint32_t bit = (uint32_t)f * (uint32_t)w, k = bit >> 5;
         const uint32_t hi = k + 1 < (uint32_t)row_words ? row[k + 1] : 0u;
-        dst[(int64_t)f * n] = (uint16_t)(__builtin_amdgcn_alignbit(hi, row[k], bit & 31u) & mask);
+        const uint32_t sym = __builtin_amdgcn_alignbit(hi, row[k], bit & 31u) & mask;
+        if constexpr (sizeof(T) == 1)
+            dst[(int64_t)f * stride] = col_byte(sym, null_sym);
+        else
+            dst[(int64_t)f * stride] = (T)sym;
     }
 }
 
 bool split_columns_fit(const gbt_matrix *mx) { return !mx->sparse && mx->w <= 16 && mx->row_words <= 64; }
 
-gbt_status split_columns(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, int64_t n, uint16_t *cols)
+int32_t split_columns_bytes(const gbt_matrix *mx)
+{
+    int32_t max_bins = 0;
+    for (int32_t f = 0; f < mx->m; ++f) max_bins = std::max(max_bins, mx->bin_ptr_h[f + 1] - mx->bin_ptr_h[f]);
+    return max_bins <= 256 ? 1 : 2;
+}
+
+gbt_status split_columns(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, int64_t n, const ColCopy &cols)
 {
     GBT_CHECK(split_columns_fit(mx), "column copy of a page with %d-bit symbols", mx->w);
+    GBT_CHECK((cols.bytes == 1 || cols.bytes == 2) && cols.stride >= n, "column copy layout");
     if (n <= 0) return GBT_OK;
     const uint32_t mask = mx->w >= 32 ? 0xffffffffu : ((1u << mx->w) - 1u);
+    const uint32_t null_sym = mx->has_missing ? mx->null_sym : 0xffffffffu;
     const size_t lds = (size_t)kColRows * (mx->row_words | 1) * 4;
-    k_page_columns<<<(unsigned)((n + kColRows - 1) / kColRows), kColRows, lds, c->stream>>>(
-        page, n, mx->row_words, mx->m, mx->w, mask, cols);
+    const unsigned grid = (unsigned)((n + kColRows - 1) / kColRows);
+    if (cols.bytes == 1)
+        k_page_columns<uint8_t><<<grid, kColRows, lds, c->stream>>>(page, n, mx->row_words, mx->m, mx->w, mask,
+                                                                   null_sym, (uint8_t *)cols.p, cols.stride);
+    else
+        k_page_columns<uint16_t><<<grid, kColRows, lds, c->stream>>>(page, n, mx->row_words, mx->m, mx->w, mask,
+                                                                    null_sym, (uint16_t *)cols.p, cols.stride);
     GBT_LAUNCHED();
     return GBT_OK;
 }
@@ -1260,7 +1287,7 @@ gbt_status split_columns(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page,
 gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int32_t *rows,
                               int64_t n, const int32_t *slot_node, int32_t *slot_node_out, DevNode *nodes,
                               int32_t *rows_out, const LevelChoice *choice, const SlotTable *stbl,
-                              const uint16_t *cols, const PlanArgs &plan, bool order, bool root)
+                              const ColCopy &cols, const PlanArgs &plan, bool order, bool root)
 {
     if (n == 0) return GBT_OK;
     const SlotTable st = stbl ? *stbl : SlotTable{nullptr, nullptr, nullptr, 0, 0, 0};
@@ -1311,7 +1338,7 @@ gbt_status partition_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page
     k_part_flags_tiles<false, false><<<(unsigned)tiles, kPartThreads, 0, c->stream>>>(rows, n, page, geo, position, slot_node,
                                                                        nodes, flags, tile_off, LevelChoice{},
                                                                        SlotTable{nullptr, nullptr, nullptr, 0, 0, 0},
-                                                                       nullptr, 0);
+                                                                       ColCopy{}, 0);
     GBT_LAUNCHED();
     if (n_list > 0) {
         k_part_bounds<<<(unsigned)n_list, kBoundThreads, 0, c->stream>>>(list, n_list_d, n_list, nodes, flags,

@@ -105,14 +105,17 @@ struct PlanArgs;
 gbt_status partition_rev_impl(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, const int32_t *rows,
                               int64_t n, const int32_t *slot_node, int32_t *slot_node_out, DevNode *nodes,
                               int32_t *rows_out, const LevelChoice *choice,
-                              const SlotTable *stbl, const uint16_t *cols, const PlanArgs &plan,
+                              const SlotTable *stbl, const ColCopy &cols, const PlanArgs &plan,
                               bool order, bool root);
 
 // Whether a page of mx's geometry takes a column copy (dense, symbols of at
 // most 16 bits).
 bool split_columns_fit(const gbt_matrix *mx);
-// cols[f * n + r] = symbol of feature f in row r of `page` (n rows of mx's
-// geometry); cols holds m * n entries.
-gbt_status split_columns(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, int64_t n, uint16_t *cols);
+// The column copy (ColCopy, cols.stride >= n) of rows [0, n) of `page`
+// (mx's geometry).
+gbt_status split_columns(gbt_ctx *c, const gbt_matrix *mx, const uint32_t *page, int64_t n, const ColCopy &cols);
+// The entry width of mx's column copy: 1 byte when every feature has at most
+// 256 bins, else 2.
+int32_t split_columns_bytes(const gbt_matrix *mx);
 
 }  // namespace gbt

@@ -985,22 +985,24 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     // copy of the training page, made once per tree (by the root histogram
     // pass for a sampled page of the plain kernel, else by split_columns;
     // once per matrix when the training page is the matrix's own device page)
-    const uint16_t *cols = nullptr;
-    uint16_t *cols_root = nullptr;  // the copy the root histogram pass writes
-    if (D >= 2 && R > 0 && split_columns_fit(mx) &&
-        scratch_fits(c, kScrCols, (size_t)mx->m * (size_t)R * sizeof(uint16_t))) {
-        uint16_t *cd;
-        GBT_TRY(scratch_t(c, kScrCols, (size_t)mx->m * (size_t)R, &cd));
+    ColCopy cols;       // the copy the partition reads (cols.p NULL: none)
+    ColCopy cols_root;  // the copy the root histogram pass writes
+    const int32_t col_bytes = split_columns_fit(mx) ? split_columns_bytes(mx) : 0;
+    if (D >= 2 && R > 0 && col_bytes &&
+        scratch_fits(c, kScrCols, (size_t)mx->m * (size_t)R * (size_t)col_bytes)) {
+        void *cd;
+        GBT_TRY(scratch(c, kScrCols, (size_t)mx->m * (size_t)R * (size_t)col_bytes, &cd));
+        const ColCopy cc{cd, R, col_bytes};
         const bool kept = so.alias && c->cols_uid == mx->uid && c->cols_page == so.page && c->cols_at == cd &&
                           c->cols_rows == R;
         if (!kept && !so.alias && hp.kind == kHistDense) {
             // a sampled page: the root pass of the plain kernel decodes every
             // symbol of every row anyway and writes the copy as it goes
             c->cols_uid = 0;
-            cols_root = cd;
+            cols_root = cc;
         } else if (!kept) {
             c->cols_uid = 0;
-            GBT_TRY(split_columns(c, mx, so.page, R, cd));
+            GBT_TRY(split_columns(c, mx, so.page, R, cc));
             if (so.alias) {
                 c->cols_uid = mx->uid;
                 c->cols_page = so.page;
@@ -1008,7 +1010,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
                 c->cols_rows = R;
             }
         }
-        cols = cd;
+        cols = cc;
     }
     int64_t *partials = nullptr;
     GBT_TRY(scratch(c, kScrPartialsDev, (size_t)std::max(max_items, 1) * mx->total_bins * 16, (void **)&partials));
@@ -1039,7 +1041,6 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         HistLaunch hl{hp.kind, groups_d, G, hp.max_groups_bins, work_d, nullptr, n_root, red_d, nullptr,
                       fused ? 0 : 1, partials, stbl.row, stbl.row_stride};
         hl.cols = cols_root;  // the root's work items cover rows [0, R) once per group
-        hl.cols_n = R;
         GBT_TRY(hist_launch_device(c, mx, so.page, so.q, nullptr, hl, nullptr, histA, upd));
         ++hist_launches;
         if (fused) {
@@ -1176,7 +1177,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         // algorithmic bytes: the packed symbols of each row, its 16-byte
         // fixed-point pair, its 4-byte row id below the root, one write of
         // every built node's histogram (the chunk partials are not counted),
-        // and the column copy when the root pass writes it (2 bytes per
+        // and the column copy when the root pass writes it (1 or 2 bytes per
         // symbol)
         const int64_t wbytes = 4 * (((int64_t)mx->stride * mx->w + 31) / 32);
         const int64_t root_built = (D > 0 && R > 0) ? 1 : 0;
@@ -1184,7 +1185,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         stats->hist_rows = (D > 0 ? R : 0) + (int64_t)res->rows_built;
         stats->hist_bytes = (D > 0 ? R : 0) * (wbytes + 16) + (int64_t)res->rows_built * (wbytes + 20) +
                             (root_built + (int64_t)res->built) * mx->total_bins * 16 +
-                            (cols_root ? 2 * (int64_t)mx->m * R : 0);
+                            (int64_t)cols_root.bytes * mx->m * R;
         stats->ms_sample = ms[kPhSample];
         stats->ms_hist = ms[kPhHist];
         stats->ms_hist_aux = ms[kPhHistAux];
@@ -1192,7 +1193,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         stats->ms_margin = ms[kPhMargin];
         stats->h2d_bytes = h2d;
         stats->hist_kernel = hp.kind == kHistRot ? GBT_HIST_ROTATED : (hp.kind == kHistDense ? GBT_HIST_PLAIN : 0);
-        stats->hist_cols = cols_root ? 1 : 0;
+        stats->hist_cols = cols_root.bytes;
         stats->ms_total =
             std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t_start).count();
     }

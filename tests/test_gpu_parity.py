@@ -964,3 +964,24 @@ def test_random_samplers_and_kernels_match_oracle(gbt, ctx, seed):
     finally:
         ctx.set_hist_kernel(ctx.HIST_AUTO)
     assert_same_trees(trees, margin, otrees, omargin)
+
+
+@pytest.mark.parametrize("f,missing", [(0.5, 0.0), (0.5, 0.1), (1.0, 0.1)])
+def test_split_at_the_last_bin_of_256(gbt, ctx, hist_kernel, f, missing):
+    # features of 256 bins: the partition's column copy holds a byte per
+    # symbol, with the top two bins sharing one code; a split between them
+    # (split bin 255) takes those rows' symbols from the rows themselves
+    r = np.random.default_rng(77)
+    n = 20_000
+    X = r.random((n, 3), dtype=np.float32)
+    top = X[:, 0] > np.quantile(X[:, 0], 1 - 1 / 256)
+    y = np.where(top, 10.0, 0.0).astype(np.float32) + 0.01 * r.normal(size=n).astype(np.float32)
+    if missing:
+        X[r.random((n, 3)) < missing] = np.nan
+    cfg = datagen.TrainConfig("t", datagen.LOSS_SQUARED, 256, 3, 2, eta=0.5, f=f)
+    trees, margin, otrees, omargin, mx, _ = train_both(gbt, ctx, X, y, cfg, 2)
+    assert_same_trees(trees, margin, otrees, omargin)
+    info = mx.info()
+    assert info.total_bins >= 256
+    root = otrees[0].nodes[0]
+    assert root["feature"] == 0 and root["split_bin"] == 255, (root["feature"], root["split_bin"])
