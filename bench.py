@@ -450,21 +450,18 @@ def main():
                               min_child_weight=cfg.min_child_weight, f=cfg.f,
                               mvs_lambda=cfg.mvs_lambda, seed=cfg.seed, sampler=sampler[0], goss_a=sampler[1])
     ctx.set_timing(0)
-    first_trees, first_updates = [], []
-    for w in range(args.warmup):
-        P.iteration = w
-        tr = gbt.gbt_train_tree(ctx, mx, label, margin, P)
-        first_trees.append(tr.nodes.copy())
-        first_updates.append(tr.stats.hist_updates)
+    # the boosting loop: one call trains a run of trees, each queued before
+    # the host reads the one before it
+    P.iteration = 0
+    warm = gbt.gbt_train_trees(ctx, mx, label, margin, P, args.warmup)
+    first_trees = [tr.nodes.copy() for tr in warm]
+    first_updates = [tr.stats.hist_updates for tr in warm]
     torch.cuda.synchronize()
     # the timed steps carry no events: a HIP event pair around each histogram
     # launch leaves the GPU idle for a few microseconds per event
-    stats = []
     t0 = time.perf_counter()
-    for k in range(args.steps):
-        P.iteration = args.warmup + k
-        tr = gbt.gbt_train_tree(ctx, mx, label, margin, P)
-        stats.append(tr.stats)
+    P.iteration = args.warmup
+    stats = [tr.stats for tr in gbt.gbt_train_trees(ctx, mx, label, margin, P, args.steps)]
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     print(f"[bench] {args.steps} trees in {dt:.3f} s", file=sys.stderr, flush=True)

@@ -54,7 +54,7 @@ typedef int32_t gbt_status;
 #define GBT_SAMPLE_SGB 1  /* stochastic gradient boosting: uniform rows */
 #define GBT_SAMPLE_GOSS 2 /* gradient-based one-side sampling */
 
-#define GBT_ABI_VERSION 6
+#define GBT_ABI_VERSION 7
 
 enum { GBT_INPUT_DENSE_F32 = 0, GBT_INPUT_CSR_F32 = 1 };
 enum { GBT_LOC_HOST = 0, GBT_LOC_DEVICE = 1 };
@@ -473,6 +473,22 @@ gbt_status gbt_update_leaves(gbt_ctx *ctx, gbt_tree *tree, const gbt_train_param
 gbt_status gbt_train_tree(gbt_ctx *ctx, const gbt_matrix *data, const float *label_d,
                           float *margin_d, const gbt_train_params *p, gbt_tree *tree,
                           gbt_tree_stats *stats);
+
+/* ---- n_trees boosting iterations: Alg. 1's loop over trees ------------------
+ * The same as n_trees calls of gbt_train_tree with p->iteration,
+ * p->iteration + 1, ... (the same trees, margins and stats, bit for bit):
+ * trees[t] (each holding 2^(max_depth+1)-1 nodes) and stats[t] (stats may
+ * be NULL) receive tree t, and margin_d holds the margins after the last
+ * tree.  Each tree is queued on the context stream without waiting for the
+ * tree before it (no host round trip separates them); the trees' results
+ * are read from a ring of pinned host memory the context keeps (64 trees'
+ * results, at most 64 MiB, or two when one exceeds 32 MiB) as it fills,
+ * and the rest when the stream has drained.  The call returns with the
+ * stream synchronized.  n_trees = 0 does nothing.  On an error the trees
+ * from the failing one on, and the margins, are undefined. */
+gbt_status gbt_train_trees(gbt_ctx *ctx, const gbt_matrix *data, const float *label_d,
+                           float *margin_d, const gbt_train_params *p, int32_t n_trees,
+                           gbt_tree *trees, gbt_tree_stats *stats);
 
 /* ---- Alg. 6: the naive out-of-core tree construction (Sec. 3.3) ------------
  * A measured negative baseline, not the path to use: every row trains

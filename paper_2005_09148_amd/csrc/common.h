@@ -87,6 +87,13 @@ struct gbt_ctx {
     void *hio = nullptr;
     void *hio_d = nullptr;
     size_t hio_bytes = 0;
+    // pinned memory a tree's last kernels write the tree into (one slot per
+    // tree of a run of trees whose results are read together), and events
+    // recorded after trees whose slot is reused within a run
+    void *tres = nullptr;
+    void *tres_d = nullptr;
+    size_t tres_bytes = 0;
+    std::vector<hipEvent_t> tres_ev;
     // what the column-copy workspace holds: a matrix's own device page
     // (kept across trees, since such a page does not change)
     uint64_t cols_uid = 0;
@@ -127,10 +134,16 @@ gbt_status scratch(gbt_ctx *c, int slot, size_t bytes, void **p);
 gbt_status file_read(int fd, void *dst, size_t bytes, int64_t off);
 gbt_status file_write(int fd, const void *src, size_t bytes, int64_t off);
 bool scratch_fits(const gbt_ctx *c, int slot, size_t bytes);
+// The bytes workspace `slot` holds now (0 before its first use).
+size_t scratch_bytes(const gbt_ctx *c, int slot);
 // Grow-only pinned host buffer that kernels write into: *host for the host,
 // *dev for kernels.  The stream must not be using it (the call syncs
 // before growing).
 gbt_status host_io(gbt_ctx *c, size_t bytes, void **host, void **dev);
+// The tree driver's pinned result memory, grown like host_io's.
+gbt_status tree_io(gbt_ctx *c, size_t bytes, void **host, void **dev);
+// Event i of the tree driver (created on first use).
+gbt_status tree_event(gbt_ctx *c, int i, hipEvent_t *ev);
 gbt_status set_device(gbt_ctx *c);
 
 enum ScratchSlot {

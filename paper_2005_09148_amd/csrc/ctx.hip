@@ -82,6 +82,39 @@ gbt_status host_io(gbt_ctx *c, size_t bytes, void **host, void **dev)
     return GBT_OK;
 }
 
+gbt_status tree_io(gbt_ctx *c, size_t bytes, void **host, void **dev)
+{
+    if (c->tres_bytes < bytes) {
+        GBT_HIP(hipStreamSynchronize(c->stream));
+        if (c->tres) GBT_HIP(hipHostFree(c->tres));
+        c->tres = c->tres_d = nullptr;
+        c->tres_bytes = 0;
+        const size_t sz = std::max<size_t>(bytes, 1 << 16);
+        GBT_HIP(hipHostMalloc(&c->tres, sz, hipHostMallocMapped | hipHostMallocCoherent));
+        GBT_HIP(hipHostGetDevicePointer(&c->tres_d, c->tres, 0));
+        c->tres_bytes = sz;
+    }
+    *host = c->tres;
+    *dev = c->tres_d;
+    return GBT_OK;
+}
+
+gbt_status tree_event(gbt_ctx *c, int i, hipEvent_t *ev)
+{
+    while ((int)c->tres_ev.size() <= i) {
+        hipEvent_t e;
+        GBT_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+        c->tres_ev.push_back(e);
+    }
+    *ev = c->tres_ev[i];
+    return GBT_OK;
+}
+
+size_t scratch_bytes(const gbt_ctx *c, int slot)
+{
+    return slot < (int)c->scratch.size() ? c->scratch[slot].bytes : 0;
+}
+
 gbt_status scratch(gbt_ctx *c, int slot, size_t bytes, void **p)
 {
     if ((int)c->scratch.size() <= slot) c->scratch.resize(slot + 1);
@@ -251,6 +284,8 @@ gbt_status gbt_ctx_destroy(gbt_ctx *c)
     (void)hipStreamSynchronize(c->side);
     for (auto &s : c->scratch) dev_free(c, s.p, s.bytes);
     if (c->hio) (void)hipHostFree(c->hio);
+    if (c->tres) (void)hipHostFree(c->tres);
+    for (auto e : c->tres_ev) (void)hipEventDestroy(e);
     for (void *p : c->disk_stage)
         if (p) (void)hipHostFree(p);
     for (auto e : c->events) (void)hipEventDestroy(e);

@@ -554,7 +554,7 @@ __global__ void __launch_bounds__(256)
                     const uint8_t *__restrict__ keep, const int32_t *__restrict__ tile_off,
                     int64_t tile0, int64_t row_lo, int64_t row_hi, const uint4 *__restrict__ words,
                     int32_t row_q4, uint4 *__restrict__ out_page, int32_t *__restrict__ sel,
-                    double2 *__restrict__ gw, SampleRule rule)
+                    double2 *__restrict__ gw, SampleRule rule, int64_t cap)
 {
     __shared__ int32_t lds4[4];
     __shared__ unsigned long long red4[4];
@@ -588,6 +588,7 @@ __global__ void __launch_bounds__(256)
     }
     __syncthreads();
     const int64_t pos0 = tile_off[tile];
+    if (pos0 + nk > cap) return;  // the whole block: the buffers are too small
     // the rows, 16 bytes per thread and step
     for (int32_t e = threadIdx.x; e < nk * row_q4; e += 256) {
         const int32_t j = e / row_q4, t = e - j * row_q4;
@@ -631,9 +632,11 @@ template <bool kSpec>
 __global__ void __launch_bounds__(256) k_gradients_rmax(int32_t loss, const float *__restrict__ margin,
                                                         const float *__restrict__ label, int64_t n,
                                                         float2 *__restrict__ gpair, double lambda,
-                                                        SampleState *__restrict__ st, int32_t e_spec)
+                                                        SampleState *__restrict__ st, int32_t e_spec,
+                                                        const int32_t *__restrict__ e_spec_at)
 {
     __shared__ unsigned long long lds4[4];
+    if (kSpec && e_spec_at) e_spec = *e_spec_at;
     unsigned long long b = 0, amx = 0, asm_ = 0;
     bool bad = false;
     auto one = [&](float m, float y, float2 *out) {
@@ -686,6 +689,15 @@ __global__ void k_keys_reset(SampleState *__restrict__ st)
     for (int t = threadIdx.x; t < kSpread * kLineWords; t += blockDim.x) {
         (&st->amax[0][0])[t] = 0ull;
         (&st->asum[0][0])[t] = 0ull;
+    }
+}
+
+// The maxima of |g'| and |h'| cleared (a compaction is redone).
+__global__ void k_fx_max_reset(SampleState *__restrict__ st)
+{
+    for (int t = threadIdx.x; t < kSpread * kLineWords; t += blockDim.x) {
+        (&st->gmax[0][0])[t] = 0ull;
+        (&st->hmax[0][0])[t] = 0ull;
     }
 }
 
@@ -802,8 +814,13 @@ __global__ void __launch_bounds__(256) k_lambda_pass(int32_t loss, const float *
 __global__ void k_state_init(SampleState *st)
 {
     static_assert(sizeof(SampleState) % 8 == 0, "SampleState is zeroed in 64-bit words");
+    __shared__ int32_t e_prev;
+    if (threadIdx.x == 0) e_prev = st->e_key;
+    __syncthreads();
     unsigned long long *w = (unsigned long long *)st;
     for (int i = threadIdx.x; i < (int)(sizeof(SampleState) / 8); i += blockDim.x) w[i] = 0ull;
+    __syncthreads();
+    if (threadIdx.x == 0) st->e_key_prev = e_prev;
 }
 
 __global__ void k_zero_u64(unsigned long long *p, int64_t n)
@@ -819,17 +836,6 @@ static unsigned rblocks(int64_t n) { return std::max(1u, std::min(blocks(n), (un
 static int32_t log2_ceil(int64_t v) { return v <= 1 ? 0 : ceil_log2_u64((uint64_t)v); }
 
 // ------------------------------------------------------------ drivers
-namespace {
-
-void keys_pass(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n, double lambda,
-               int32_t l2, SampleState *st)
-{
-    if (kind == kSrcGpair)
-        k_mvs_keys<kSrcGpair><<<rblocks(n), 256, 0, c->stream>>>(src, n, lambda, l2, st, (int64_t *)keys);
-    else
-        k_mvs_keys<kSrcMargin><<<rblocks(n), 256, 0, c->stream>>>(src, n, lambda, l2, st, (int64_t *)keys);
-}
-
 gbt_status wait_flag(gbt_ctx *c, volatile int32_t *done_poll)
 {
     const auto t0 = std::chrono::steady_clock::now();
@@ -841,6 +847,18 @@ gbt_status wait_flag(gbt_ctx *c, volatile int32_t *done_poll)
     }
     return GBT_OK;
 }
+
+namespace {
+
+void keys_pass(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n, double lambda,
+               int32_t l2, SampleState *st)
+{
+    if (kind == kSrcGpair)
+        k_mvs_keys<kSrcGpair><<<rblocks(n), 256, 0, c->stream>>>(src, n, lambda, l2, st, (int64_t *)keys);
+    else
+        k_mvs_keys<kSrcMargin><<<rblocks(n), 256, 0, c->stream>>>(src, n, lambda, l2, st, (int64_t *)keys);
+}
+
 
 // After the threshold's first kernel: with a host flag, its outcome (1 the
 // closed form holds, 0 a descent is needed, 2 the guessed key exponent was
@@ -968,15 +986,16 @@ gbt_status gw_all(gbt_ctx *c, const float *gpair, int64_t n, double *gw)
 }
 
 gbt_status gradients_rmax(gbt_ctx *c, int32_t loss, const float *margin, const float *label, int64_t n,
-                          float *gpair, double lambda, SampleState *st, int32_t e_spec)
+                          float *gpair, double lambda, SampleState *st, int32_t e_spec,
+                          const int32_t *e_spec_at)
 {
     if (n == 0) return GBT_OK;
-    if (e_spec == kNoKeySpec)
+    if (e_spec == kNoKeySpec && !e_spec_at)
         k_gradients_rmax<false><<<rblocks(n), 256, 0, c->stream>>>(loss, margin, label, n, (float2 *)gpair, lambda,
-                                                                   st, 0);
+                                                                   st, 0, nullptr);
     else
         k_gradients_rmax<true><<<rblocks(n), 256, 0, c->stream>>>(loss, margin, label, n, (float2 *)gpair, lambda,
-                                                                  st, e_spec);
+                                                                  st, e_spec, e_spec_at);
     GBT_LAUNCHED();
     return GBT_OK;
 }
@@ -989,7 +1008,7 @@ gbt_status keep_tile_offsets(gbt_ctx *c, int64_t n, int32_t *tile_off, int32_t *
 gbt_status mvs_compact_tiles(gbt_ctx *c, const SampleSrc &src, int kind, int64_t n, double lambda,
                              SampleState *st, const uint8_t *keep, const int32_t *tile_off,
                              int64_t row_lo, int64_t row_hi, const uint32_t *words, int32_t row_words,
-                             uint32_t *out_page, int32_t *sel, double *gw, const SampleRule &rule)
+                             uint32_t *out_page, int32_t *sel, double *gw, const SampleRule &rule, int64_t cap)
 {
     if (row_hi <= row_lo) return GBT_OK;
     const int64_t t0 = row_lo / kCompactTile, t1 = (row_hi - 1) / kCompactTile + 1;
@@ -997,11 +1016,18 @@ gbt_status mvs_compact_tiles(gbt_ctx *c, const SampleSrc &src, int kind, int64_t
     if (kind == kSrcGpair)
         k_compact_tiles<kSrcGpair><<<grid, 256, 0, c->stream>>>(
             src, n, lambda, st, keep, tile_off, t0, row_lo, row_hi, (const uint4 *)words, row_words / 4,
-            (uint4 *)out_page, sel, (double2 *)gw, rule);
+            (uint4 *)out_page, sel, (double2 *)gw, rule, cap);
     else
         k_compact_tiles<kSrcMargin><<<grid, 256, 0, c->stream>>>(
             src, n, lambda, st, keep, tile_off, t0, row_lo, row_hi, (const uint4 *)words, row_words / 4,
-            (uint4 *)out_page, sel, (double2 *)gw, rule);
+            (uint4 *)out_page, sel, (double2 *)gw, rule, cap);
+    GBT_LAUNCHED();
+    return GBT_OK;
+}
+
+gbt_status fx_max_reset(gbt_ctx *c, SampleState *st)
+{
+    k_fx_max_reset<<<1, 256, 0, c->stream>>>(st);
     GBT_LAUNCHED();
     return GBT_OK;
 }

@@ -64,6 +64,8 @@ struct SampleState {
     int32_t levels;
     int32_t done;
     unsigned int bad;
+    int32_t e_key_prev;  // e_key as the state's last use left it (kept by state_init)
+    int32_t pad0;
 };
 
 // Block b's copy of a spread reduction.
@@ -83,6 +85,8 @@ __host__ __device__ inline unsigned long long fold_sum(const Spread &a)
     return m;
 }
 
+// Zeroes the state except e_key_prev, which takes the e_key the state held
+// (the last tree's key exponent, the next tree's guess).
 gbt_status state_init(gbt_ctx *c, SampleState *st);
 // keys may be NULL (recomputed on every pass).  Leaves T* in st (device).
 // skip_closed: wait on the host for the closed-form test and launch the
@@ -123,20 +127,31 @@ gbt_status fixed_point(gbt_ctx *c, const double *gw, int64_t R, SampleState *st,
                        bool fx_max_done = false);
 // Gradients of all rows and, fused, the maximum of r^2 = g^2 + lambda h^2;
 // with e_spec (not kNoKeySpec) also the MVS keys' maximum and sum with that
-// key exponent, st->e_key = e_spec (to be checked by mvs_threshold).
+// key exponent, st->e_key = e_spec (to be checked by mvs_threshold); with
+// e_spec_at (device) the exponent is read there instead.
 constexpr int32_t kNoKeySpec = -0x7fffffff;
 gbt_status gradients_rmax(gbt_ctx *c, int32_t loss, const float *margin, const float *label, int64_t n,
-                          float *gpair, double lambda, SampleState *st, int32_t e_spec = kNoKeySpec);
+                          float *gpair, double lambda, SampleState *st, int32_t e_spec = kNoKeySpec,
+                          const int32_t *e_spec_at = nullptr);
 // Exclusive per-tile offsets from the per-tile counts mvs_select wrote into
 // tile_off (tiles of kCompactTile rows), and the total at tile_off[tiles]
 // (and at *total_host, pinned host memory, when given).
 gbt_status keep_tile_offsets(gbt_ctx *c, int64_t n, int32_t *tile_off, int32_t *total_host = nullptr);
 // Compaction of the kept rows among global rows [row_lo, row_hi) whose page
 // words start at `words`; positions come from the tile offsets; also folds
-// the maxima of |g'| and |h'| into st.
+// the maxima of |g'| and |h'| into st.  cap: the output buffers' rows; a
+// tile whose kept rows would reach past it writes nothing (a compaction
+// queued before the host knows the sample size, into buffers that are then
+// large enough unless the sample is; the host redoes it when it was not).
 gbt_status mvs_compact_tiles(gbt_ctx *c, const SampleSrc &src, int kind, int64_t n, double lambda,
                              SampleState *st, const uint8_t *keep, const int32_t *tile_off,
                              int64_t row_lo, int64_t row_hi, const uint32_t *words, int32_t row_words,
-                             uint32_t *out_page, int32_t *sel, double *gw, const SampleRule &rule);
+                             uint32_t *out_page, int32_t *sel, double *gw, const SampleRule &rule,
+                             int64_t cap = INT64_MAX);
+// Spins until a kernel has written a value >= 0 at *flag (pinned host
+// memory); after 2 s, synchronizes the stream instead.
+gbt_status wait_flag(gbt_ctx *c, volatile int32_t *flag);
+// Clears the maxima of |g'| and |h'| (before a compaction is redone).
+gbt_status fx_max_reset(gbt_ctx *c, SampleState *st);
 
 }  // namespace gbt

@@ -73,7 +73,8 @@ __global__ void __launch_bounds__(1024) k_scan_spine(int32_t *__restrict__ bsum,
     }
     if (threadIdx.x == 0) {
         *total_out = carry;
-        if (total_host) *total_host = carry;
+        // the host may poll it while later kernels run
+        if (total_host) __hip_atomic_store(total_host, carry, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     }
 }
 

@@ -279,22 +279,49 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
         // sits apart from the threshold's flag in the pinned buffer)
         void *hio, *hio_d;
         GBT_TRY(host_io(c, 64, &hio, &hio_d));
-        auto select = [&]() -> gbt_status {
+        volatile int32_t *r_host = (volatile int32_t *)hio + 4;
+        auto select = [&](bool wait) -> gbt_status {
             // with f = 1 the state keeps T = 0: every row is kept with weight 1
+            *r_host = -1;
             GBT_TRY(mvs_select(c, src, kind, nullptr, n, lam, st, sp.seed, sp.iteration, 0, keep, tile_off, rule));
             GBT_TRY(keep_tile_offsets(c, n, tile_off, (int32_t *)hio_d + 4));
-            GBT_HIP(hipStreamSynchronize(c->stream));
+            if (wait) GBT_HIP(hipStreamSynchronize(c->stream));
             return GBT_OK;
         };
-        GBT_TRY(select());
-        if (mvs) {
-            bool redo = false;
-            GBT_TRY(mvs_threshold_resume(c, src, kind, nullptr, n, lam, o->K, st, &redo));
-            if (redo) GBT_TRY(select());
+        const size_t rb = (size_t)mx->row_words * 4;
+        // A page on the device with the context's own workspaces: the
+        // compaction is queued behind the selection before the host reads
+        // the sample size, into buffers sized for about f n rows (held from
+        // the trees before), so the host's round trip overlaps it.  It is
+        // redone when the threshold had to be completed or the sample is
+        // larger than the buffers.
+        const bool early = all_device_single(mx) && !bufs.owned && n > 0;
+        int64_t cap = 0;
+        uint32_t *spage = nullptr;
+        if (early) {
+            const int64_t guess = std::min<int64_t>(n, (int64_t)std::ceil(sp.f * (double)n)) + 1;
+            GBT_TRY(bufs.get(kScrSampled, (size_t)guess * rb, (void **)&spage));
+            GBT_TRY(bufs.get(kScrSel, (size_t)guess * 4, (void **)&o->sel));
+            GBT_TRY(bufs.get(kScrGw, (size_t)guess * 16, (void **)&o->gw));
+            cap = (int64_t)std::min({scratch_bytes(c, kScrSampled) / rb, scratch_bytes(c, kScrSel) / 4,
+                                     scratch_bytes(c, kScrGw) / 16});
+            GBT_TRY(select(false));
+            GBT_TRY(mvs_compact_tiles(c, src, kind, n, lam, st, keep, tile_off, 0, n, mx->pages[0].words,
+                                      mx->row_words, spage, o->sel, o->gw, rule, cap));
+            GBT_TRY(wait_flag(c, r_host));
+        } else {
+            GBT_TRY(select(true));
         }
-        o->R = *((volatile int32_t *)hio + 4);
-        size_t rb = (size_t)mx->row_words * 4;
-        uint32_t *spage;
+        bool redo = false;
+        if (mvs) {
+            GBT_TRY(mvs_threshold_resume(c, src, kind, nullptr, n, lam, o->K, st, &redo));
+            if (redo) GBT_TRY(select(true));
+        }
+        o->R = *r_host;
+        GBT_CHECK(o->R >= 0 && o->R <= n, "sample size %lld of %lld rows", (long long)o->R, (long long)n);
+        const bool compacted = early && !redo && o->R <= cap;
+        // the early compaction's maxima of the reweighted pairs are void
+        if (early && !compacted) GBT_TRY(fx_max_reset(c, st));
         GBT_TRY(bufs.get(kScrSampled, (size_t)std::max<int64_t>(o->R, 1) * rb, (void **)&spage));
         GBT_TRY(bufs.get(kScrSel, (size_t)std::max<int64_t>(o->R, 1) * 4, (void **)&o->sel));
         GBT_TRY(bufs.get(kScrGw, (size_t)std::max<int64_t>(o->R, 1) * 16, (void **)&o->gw));
@@ -303,7 +330,8 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
         const bool host = any_host_pages(mx) && mx->page_home == GBT_HOME_PINNED_HOST;
         const bool gather = host && (c->compaction == GBT_COMPACT_GATHER ||
                                      (c->compaction == GBT_COMPACT_AUTO && 2 * (int64_t)o->R <= n));
-        if (gather) {
+        if (compacted) {
+        } else if (gather) {
             // the kernel reads the kept rows of each pinned page through its
             // device mapping: only those rows cross the host link
             for (const auto &pg : mx->pages) {
@@ -847,8 +875,29 @@ static size_t walk_lds_bytes(const Geo &g) { return (size_t)kWalkThreads * (g.ro
 
 // ------------------------------------------------------------ the iteration
 
-static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float *label, float *margin,
-                                  const gbt_train_params *p, gbt_tree *tree, gbt_tree_stats *stats)
+// A tree whose kernels are queued: what the host needs to read its result.
+struct TreePending {
+    const void *res = nullptr;  // its pinned result (TreeResult)
+    hipEvent_t done = nullptr;  // recorded after its last kernel, or NULL
+    int64_t n = 0, R = 0;
+    int32_t NN = 0, D = 0;
+    bool mvs = false, stats = false;
+    double key_lambda = 0.0;
+    int32_t hist_launches = 0, hist_kind = 0, cols_bytes = 0;
+    int64_t hist_bytes_fixed = 0;  // the root's part of the algorithmic bytes
+    int64_t row_bytes_below = 0;   // per row built below the root
+    int64_t node_hist_bytes = 0;   // per histogram built below the root
+    double h2d = 0.0;
+    std::chrono::steady_clock::time_point t_start;
+};
+
+// Queues one tree: gradients to the margin update, and the tree's copy into
+// the pinned result res_h (res_d on the device), then `done` when not NULL.
+// spec_prev: the MVS key exponent is guessed from the sampling state's last
+// tree on the device (that tree is queued, and the host has not read it).
+static gbt_status train_tree_enqueue(gbt_ctx *c, const gbt_matrix *mx, const float *label, float *margin,
+                                     const gbt_train_params *p, bool want_stats, void *res_h, void *res_d,
+                                     hipEvent_t done, bool spec_prev, TreePending *pt)
 {
     auto t_start = std::chrono::steady_clock::now();
     const int64_t n = mx->n_rows;
@@ -858,7 +907,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     double h2d = 0.0;
 
     unsigned long long *upd = nullptr;  // zeroed with the tree's other counters
-    if (stats) GBT_TRY(scratch_t(c, kScrUpd, kUpdWords, &upd));
+    if (want_stats) GBT_TRY(scratch_t(c, kScrUpd, kUpdWords, &upd));
     c->marks.clear();
     c->events_used = 0;
     int mark = timer_begin(c, kPhSample);
@@ -870,15 +919,18 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     // when it was wrong)
     const bool mvs = p->f < 1.0 && p->sampler == GBT_SAMPLE_MVS;
     int32_t e_spec = kNoKeySpec;
-    if (mvs && c->key_n_last == n && c->key_lambda_last == sample_lambda(sp)) e_spec = c->key_e_last;
+    if (mvs && !spec_prev && c->key_n_last == n && c->key_lambda_last == sample_lambda(sp)) e_spec = c->key_e_last;
     c->key_n_last = -1;  // set again when this tree has finished
+    const int32_t *e_spec_at = nullptr;
     if (!host_pages) {
         GBT_TRY(scratch_t(c, kScrGpair, (size_t)std::max<int64_t>(n, 1) * 2, &gpair));
         if (p->f < 1.0) {
             // the gradient pass also folds the maximum of r for the sampling keys
             GBT_TRY(scratch_t(c, kScrState, 1, &st_ready));
             GBT_TRY(state_init(c, st_ready));
-            GBT_TRY(gradients_rmax(c, p->loss, margin, label, n, gpair, sample_lambda(sp), st_ready, e_spec));
+            if (mvs && spec_prev) e_spec_at = &st_ready->e_key_prev;
+            GBT_TRY(gradients_rmax(c, p->loss, margin, label, n, gpair, sample_lambda(sp), st_ready, e_spec,
+                                   e_spec_at));
         } else {
             GBT_TRY(launch_gradients(c, p->loss, margin, label, nullptr, n, gpair));
         }
@@ -886,7 +938,7 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     Buffers bufs{c, false, {}};
     SampleOut so;
     GBT_TRY(sample_run(c, mx, gpair, margin, label, sp, bufs, &so, &h2d, st_ready, false,
-                       st_ready != nullptr && e_spec != kNoKeySpec));
+                       st_ready != nullptr && (e_spec != kNoKeySpec || e_spec_at != nullptr)));
     timer_end(c, mark);
     const int64_t R = so.R;
     const int32_t *e_dev = &so.st->e_g;  // {e_g, e_h} on the device
@@ -1105,11 +1157,8 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     // the tree and the counters: written by the device into pinned memory,
     // read after the one synchronization of the call; with the dense walk,
     // by two more blocks of its first launch
-    void *hio, *hio_d;
-    const size_t res_bytes = sizeof(TreeResult) + (size_t)NN * sizeof(gbt_node);
-    GBT_TRY(host_io(c, res_bytes, &hio, &hio_d));
     const FinalizeArgs fa{nodes, NN, 0, leaf, mx->cut_ptr_d, mx->cut_values_d, so.st, upd, stat,
-                          (TreeResult *)hio_d};
+                          (TreeResult *)res_d};
     bool finalized = false;
     // the rows' final slots give their leaves when every row trained; on
     // dense pages the walk of the page in row order is cheaper than adding
@@ -1156,48 +1205,91 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
         k_finalize<<<blocks(NN), 256, 0, c->stream>>>(fa);
         GBT_LAUNCHED();
     }
-    GBT_HIP(hipStreamSynchronize(c->stream));
-    const TreeResult *res = (const TreeResult *)hio;
+    if (done) GBT_HIP(hipEventRecord(done, c->stream));
+    // algorithmic bytes of the histogram passes: the packed symbols of each
+    // row, its 16-byte fixed-point pair, its 4-byte row id below the root,
+    // one write of every built node's histogram (the chunk partials are not
+    // counted), and the column copy when the root pass writes it (1 or 2
+    // bytes per symbol)
+    const int64_t wbytes = 4 * (((int64_t)mx->stride * mx->w + 31) / 32);
+    const int64_t root_built = (D > 0 && R > 0) ? 1 : 0;
+    pt->res = res_h;
+    pt->done = done;
+    pt->n = n;
+    pt->R = R;
+    pt->NN = NN;
+    pt->D = D;
+    pt->mvs = mvs;
+    pt->stats = want_stats;
+    pt->key_lambda = sample_lambda(sp);
+    pt->hist_launches = hist_launches;
+    pt->hist_kind = hp.kind == kHistRot ? GBT_HIST_ROTATED : (hp.kind == kHistDense ? GBT_HIST_PLAIN : 0);
+    pt->cols_bytes = cols_root.bytes;
+    pt->hist_bytes_fixed = (D > 0 ? R : 0) * (wbytes + 16) + root_built * mx->total_bins * 16 +
+                           (int64_t)cols_root.bytes * mx->m * R;
+    pt->row_bytes_below = wbytes + 20;
+    pt->node_hist_bytes = mx->total_bins * 16;
+    pt->h2d = h2d;
+    pt->t_start = t_start;
+    return GBT_OK;
+}
+
+// Reads a queued tree's result into `tree` (and `stats`, when the tree was
+// queued with them); the caller has waited for its last kernels.
+static gbt_status train_tree_finish(gbt_ctx *c, const TreePending &pt, gbt_tree *tree, gbt_tree_stats *stats)
+{
+    const TreeResult *res = (const TreeResult *)pt.res;
     if (res->bad) return set_error(GBT_E_INVALID, "sampling failed (state flags %u)", res->bad);
-    if (mvs) {
+    if (pt.mvs) {
         c->key_e_last = res->e_key;
-        c->key_n_last = n;
-        c->key_lambda_last = sample_lambda(sp);
+        c->key_n_last = pt.n;
+        c->key_lambda_last = pt.key_lambda;
     }
+    tree->max_depth = pt.D;
     tree->exp_g = res->e_g;
     tree->exp_h = res->e_h;
-    memcpy(tree->nodes, res->nodes, (size_t)NN * sizeof(gbt_node));
+    memcpy(tree->nodes, res->nodes, (size_t)pt.NN * sizeof(gbt_node));
     double ms[kPhCount] = {0.0};
     timer_collect(c, ms);
-    if (stats) {
-        stats->n_sampled = R;
+    if (stats && pt.stats) {
+        memset(stats, 0, sizeof(*stats));
+        stats->n_sampled = pt.R;
         stats->threshold = res->T;
         stats->exp_key = res->e_key;
         stats->hist_updates = (int64_t)res->updates;
-        // algorithmic bytes: the packed symbols of each row, its 16-byte
-        // fixed-point pair, its 4-byte row id below the root, one write of
-        // every built node's histogram (the chunk partials are not counted),
-        // and the column copy when the root pass writes it (1 or 2 bytes per
-        // symbol)
-        const int64_t wbytes = 4 * (((int64_t)mx->stride * mx->w + 31) / 32);
-        const int64_t root_built = (D > 0 && R > 0) ? 1 : 0;
-        stats->hist_launches = hist_launches;
-        stats->hist_rows = (D > 0 ? R : 0) + (int64_t)res->rows_built;
-        stats->hist_bytes = (D > 0 ? R : 0) * (wbytes + 16) + (int64_t)res->rows_built * (wbytes + 20) +
-                            (root_built + (int64_t)res->built) * mx->total_bins * 16 +
-                            (int64_t)cols_root.bytes * mx->m * R;
+        stats->hist_launches = pt.hist_launches;
+        stats->hist_rows = (pt.D > 0 ? pt.R : 0) + (int64_t)res->rows_built;
+        stats->hist_bytes = pt.hist_bytes_fixed + (int64_t)res->rows_built * pt.row_bytes_below +
+                            (int64_t)res->built * pt.node_hist_bytes;
         stats->ms_sample = ms[kPhSample];
         stats->ms_hist = ms[kPhHist];
         stats->ms_hist_aux = ms[kPhHistAux];
         stats->ms_split = ms[kPhSplit];
         stats->ms_margin = ms[kPhMargin];
-        stats->h2d_bytes = h2d;
-        stats->hist_kernel = hp.kind == kHistRot ? GBT_HIST_ROTATED : (hp.kind == kHistDense ? GBT_HIST_PLAIN : 0);
-        stats->hist_cols = cols_root.bytes;
+        stats->h2d_bytes = pt.h2d;
+        stats->hist_kernel = pt.hist_kind;
+        stats->hist_cols = pt.cols_bytes;
         stats->ms_total =
-            std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t_start).count();
+            std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - pt.t_start).count();
     }
     return GBT_OK;
+}
+
+// Bytes of one tree's pinned result (a multiple of 256).
+static size_t tree_result_bytes(int32_t NN)
+{
+    return (sizeof(TreeResult) + (size_t)NN * sizeof(gbt_node) + 255) / 256 * 256;
+}
+
+static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float *label, float *margin,
+                                  const gbt_train_params *p, gbt_tree *tree, gbt_tree_stats *stats)
+{
+    void *rh, *rd;
+    GBT_TRY(tree_io(c, tree_result_bytes((1 << (p->max_depth + 1)) - 1), &rh, &rd));
+    TreePending pt;
+    GBT_TRY(train_tree_enqueue(c, mx, label, margin, p, stats != nullptr, rh, rd, nullptr, false, &pt));
+    GBT_HIP(hipStreamSynchronize(c->stream));
+    return train_tree_finish(c, pt, tree, stats);
 }
 
 static gbt_status upload_trees(gbt_ctx *c, const gbt_tree *trees, int32_t n_trees, gbt_node **nodes_d,
@@ -1686,6 +1778,74 @@ gbt_status gbt_train_tree(gbt_ctx *c, const gbt_matrix *data, const float *label
     if (stats) memset(stats, 0, sizeof(*stats));
     GBT_TRY(set_device(c));
     return train_tree_impl(c, data, label_d, margin_d, p, tree, stats);
+}
+
+gbt_status gbt_train_trees(gbt_ctx *c, const gbt_matrix *data, const float *label_d, float *margin_d,
+                           const gbt_train_params *p, int32_t n_trees, gbt_tree *trees, gbt_tree_stats *stats)
+{
+    GBT_CHECK(c && data && p, "gbt_train_trees: NULL argument");
+    GBT_CHECK(n_trees >= 0, "n_trees %d < 0", n_trees);
+    if (n_trees == 0) return GBT_OK;
+    GBT_CHECK(trees, "gbt_train_trees: NULL trees");
+    GBT_CHECK(data->n_rows == 0 || (label_d && margin_d), "gbt_train_trees: NULL labels/margins");
+    GBT_TRY(hist_check_feature_bins(data));
+    GBT_CHECK(p->max_depth >= 0 && p->max_depth <= 20, "max_depth %d outside [0, 20]", p->max_depth);
+    GBT_CHECK(p->f > 0.0 && p->f <= 1.0, "f %g outside (0, 1]", p->f);
+    GBT_CHECK(p->loss == GBT_LOSS_LOGISTIC || p->loss == GBT_LOSS_SQUARED, "unknown loss %d", p->loss);
+    GBT_CHECK(data->n_rows < ((int64_t)1 << 31) - 1, "more than 2^31-2 rows");
+    const int32_t NN = (1 << (p->max_depth + 1)) - 1;
+    for (int32_t t = 0; t < n_trees; ++t) {
+        GBT_CHECK(trees[t].nodes, "trees[%d].nodes is NULL", t);
+        GBT_CHECK(trees[t].n_nodes >= NN, "trees[%d] holds %d nodes, needs %d", t, trees[t].n_nodes, NN);
+    }
+    if (stats) memset(stats, 0, sizeof(*stats) * (size_t)n_trees);
+    GBT_TRY(set_device(c));
+    gbt_train_params q = *p;
+    // With timing on, each tree is read before the next is queued (the
+    // timing marks are per tree).
+    if (c->timing) {
+        for (int32_t t = 0; t < n_trees; ++t) {
+            q.iteration = p->iteration + (uint64_t)t;
+            GBT_TRY(train_tree_impl(c, data, label_d, margin_d, &q, &trees[t], stats ? &stats[t] : nullptr));
+        }
+        return GBT_OK;
+    }
+    // Every tree is queued without waiting for the one before: its first
+    // kernels follow the last tree's margin update on the stream, and its
+    // sampling keys' exponent is guessed from that tree's on the device.
+    // Each tree writes its result into a slot of a ring (S slots, at most 64
+    // MiB; sized by the tree depth alone, so a context allocates it once);
+    // the ring's halves are read in turn: before tree t reuses the slots of
+    // trees t - S .. t - S + H - 1, those are read after the event recorded
+    // behind the last of them.  The rest are read once the stream drains.
+    const size_t rb = tree_result_bytes(NN);
+    const int32_t S = 2 * (int32_t)std::max<int64_t>(1, std::min<int64_t>(32, ((int64_t)32 << 20) / (int64_t)rb));
+    const int32_t H = S / 2;
+    void *rh, *rd;
+    GBT_TRY(tree_io(c, (size_t)S * rb, &rh, &rd));
+    std::vector<TreePending> pend((size_t)S);
+    int32_t n_read = 0;
+    auto read_to = [&](int32_t end) -> gbt_status {
+        for (; n_read < end; ++n_read)
+            GBT_TRY(train_tree_finish(c, pend[n_read % S], &trees[n_read], stats ? &stats[n_read] : nullptr));
+        return GBT_OK;
+    };
+    for (int32_t t = 0; t < n_trees; ++t) {
+        if (t >= S && t % H == 0) {
+            GBT_HIP(hipEventSynchronize(pend[(t - S + H - 1) % S].done));
+            GBT_TRY(read_to(t - S + H));
+        }
+        // the event behind the last tree of a half whose slots are reused
+        const int32_t g = t / H;
+        hipEvent_t ev = nullptr;
+        if ((t + 1) % H == 0 && (int64_t)n_trees > (int64_t)(g + 2) * H) GBT_TRY(tree_event(c, g & 1, &ev));
+        q.iteration = p->iteration + (uint64_t)t;
+        GBT_TRY(train_tree_enqueue(c, data, label_d, margin_d, &q, stats != nullptr, (char *)rh + (size_t)(t % S) * rb,
+                                   (char *)rd + (size_t)(t % S) * rb, ev, t > 0, &pend[t % S]));
+    }
+    GBT_HIP(hipStreamSynchronize(c->stream));
+    GBT_TRY(read_to(n_trees));
+    return GBT_OK;
 }
 
 gbt_status gbt_update_leaves(gbt_ctx *c, gbt_tree *tree, const gbt_train_params *tp, const gbt_matrix *data,

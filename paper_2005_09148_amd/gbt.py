@@ -116,6 +116,12 @@ class Tree(C.Structure):
                 ("exp_h", C.c_int32), ("nodes", C.c_void_p)]
 
 
+# gbt_tree's layout, for arrays of trees built with numpy
+_TREE_DTYPE = np.dtype([("max_depth", "<i4"), ("n_nodes", "<i4"), ("exp_g", "<i4"), ("exp_h", "<i4"),
+                        ("nodes", "<u8")], align=True)
+assert _TREE_DTYPE.itemsize == C.sizeof(Tree)
+
+
 class TreeStats(C.Structure):
     _fields_ = [("n_sampled", C.c_int64), ("threshold", C.c_int64), ("exp_key", C.c_int32),
                 ("hist_launches", C.c_int32), ("hist_rows", C.c_int64),
@@ -174,6 +180,7 @@ SIGNATURES = {
     "gbt_partition": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _i64, _vp, _vp, _vp]),
     "gbt_update_leaves": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _i64, _vp]),
     "gbt_train_tree": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "gbt_train_trees": (_i32, [_vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp]),
     "gbt_train_tree_naive": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     "gbt_predict": (_i32, [_vp, _vp, _i32, _vp, _vp, _f32, _vp]),
 }
@@ -737,6 +744,27 @@ def gbt_train_tree(ctx, matrix: Matrix, label, margin, params: TrainParams, stat
     return TreeOut(nodes, t.exp_g, t.exp_h, params.max_depth, st)
 
 
+def gbt_train_trees(ctx, matrix: Matrix, label, margin, params: TrainParams, n_trees: int,
+                    stats=True) -> list[TreeOut]:
+    """n_trees boosting iterations from params.iteration on, in one call."""
+    y_p, m_p = _label_margin(ctx, matrix, label, margin)
+    if n_trees < 0:
+        raise ValueError(f"n_trees {n_trees} < 0")
+    nn = (1 << (params.max_depth + 1)) - 1
+    # the gbt_tree array as a structured array (one numpy call per field, not
+    # one ctypes object per tree); tree t's nodes are row t of one array
+    nodes = np.zeros((max(n_trees, 1), nn), NODE_DTYPE)
+    ts = np.zeros(max(n_trees, 1), _TREE_DTYPE)
+    ts["max_depth"] = params.max_depth
+    ts["n_nodes"] = nn
+    ts["nodes"] = nodes.ctypes.data + np.arange(len(ts), dtype=np.uint64) * np.uint64(nn * NODE_DTYPE.itemsize)
+    st = (TreeStats * max(n_trees, 1))() if stats else None
+    _check(_lib.gbt_train_trees(ctx.h, matrix.h, y_p, m_p, C.byref(params), n_trees, ts.ctypes.data, st))
+    eg, eh = ts["exp_g"].tolist(), ts["exp_h"].tolist()
+    return [TreeOut(nodes[t], eg[t], eh[t], params.max_depth, st[t] if st is not None else None)
+            for t in range(n_trees)]
+
+
 def gbt_train_tree_naive(ctx, matrix: Matrix, label, margin, params: TrainParams, stats=True) -> TreeOut:
     """Alg. 6, the naive out-of-core construction (a negative baseline)."""
     y_p, m_p = _label_margin(ctx, matrix, label, margin)
@@ -795,9 +823,6 @@ def train(ctx, matrix: Matrix, label, params: TrainParams, n_trees, base_margin,
     n = matrix.info().n_rows
     if margin is None:
         margin = torch.full((n,), base_margin, dtype=torch.float32, device=ctx.torch_device)
-    trees = []
-    for t in range(n_trees):
-        p = TrainParams.from_buffer_copy(params)
-        p.iteration = t
-        trees.append(gbt_train_tree(ctx, matrix, label, margin, p))
-    return trees, margin
+    p = TrainParams.from_buffer_copy(params)
+    p.iteration = 0
+    return gbt_train_trees(ctx, matrix, label, margin, p, n_trees), margin

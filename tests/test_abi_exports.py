@@ -31,7 +31,7 @@ def test_library_exports_every_declared_symbol():
     missing = [n for n in declared_functions() if not hasattr(lib, n)]
     assert not missing, missing
     lib.gbt_abi_version.restype = ctypes.c_int32
-    assert lib.gbt_abi_version() == 6
+    assert lib.gbt_abi_version() == 7
 
 
 @pytest.mark.skipif(not os.path.exists(LIB), reason="libgbt.so not built")

@@ -544,6 +544,132 @@ def test_train_trees_match_oracle(gbt, ctx, hist_kernel, cfg_id, n, n_trees):
     assert [t.stats.hist_cols for t in trees] == [want] * n_trees
 
 
+STAT_FIELDS = ("n_sampled", "threshold", "exp_key", "hist_updates", "hist_launches", "hist_rows", "hist_bytes",
+               "hist_kernel", "hist_cols")
+
+
+@pytest.mark.parametrize("case", ["mvs", "mvs_eta1", "sgb", "goss", "all_rows", "csr", "pinned", "depth0",
+                                  "timed"])
+def test_train_trees_equals_tree_by_tree(gbt, ctx, case):
+    """gbt_train_trees queues each tree before the host reads the one before
+    (the sampling keys' exponent guessed on the device): the same trees,
+    margins and counters as one gbt_train_tree call per tree, and as the
+    oracle's."""
+    cfg = datagen.CONFIGS[3]
+    n, n_trees, kw, home, page_rows = 40_000, 5, {}, 0, 0
+    sampler, goss_a = gbt.SAMPLE_MVS, 0.0
+    if case == "csr":
+        cfg = datagen.CONFIGS[5]
+        d = datagen.config5(n=6_000, m=300)
+        data, y = d, d["y"]
+    else:
+        d = datagen.make(3, n)
+        data, y = d["X"], d["y"]
+    if case == "mvs_eta1":
+        kw["eta"] = 1.0  # the residuals shrink fast: the key exponent moves between trees
+    if case == "sgb":
+        sampler = gbt.SAMPLE_SGB
+    if case == "goss":
+        sampler, goss_a = gbt.SAMPLE_GOSS, 0.05
+    if case == "all_rows":
+        kw["f"] = 1.0
+    if case == "pinned":
+        home, page_rows = gbt.HOME_PINNED_HOST, 16_384
+    if case == "depth0":
+        kw["max_depth"] = 0
+    args = dict(loss=cfg.loss, max_depth=cfg.max_depth, eta=cfg.eta, lambda_=cfg.lambda_, gamma=cfg.gamma,
+                min_child_weight=cfg.min_child_weight, f=cfg.f, mvs_lambda=cfg.mvs_lambda, seed=cfg.seed)
+    args.update(kw)
+    mx = gbt.gbt_quantize(ctx, data, max_bin=cfg.max_bin, page_rows=page_rows, page_home=home)
+    label = torch.from_numpy(y).cuda()
+    P = gbt.make_train_params(sampler=sampler, goss_a=goss_a, **args)
+    P.iteration = 3
+    m1 = torch.full((len(y),), cfg.base_margin, dtype=torch.float32, device="cuda")
+    ctx.set_timing(1 if case == "timed" else 0)
+    try:
+        many = gbt.gbt_train_trees(ctx, mx, label, m1, P, n_trees)
+        assert gbt.gbt_train_trees(ctx, mx, label, m1, P, 0) == []
+    finally:
+        ctx.set_timing(0)
+    m2 = torch.full((len(y),), cfg.base_margin, dtype=torch.float32, device="cuda")
+    one = []
+    for t in range(n_trees):
+        Q = gbt.TrainParams.from_buffer_copy(P)
+        Q.iteration = 3 + t
+        one.append(gbt.gbt_train_tree(ctx, mx, label, m2, Q))
+    for t, (a, b) in enumerate(zip(many, one)):
+        dd = node_diff(a.nodes, b.nodes)
+        assert dd is None, f"tree {t} node {dd[0]}: one call {dd[1]}, per tree {dd[2]}"
+        assert (a.exp_g, a.exp_h) == (b.exp_g, b.exp_h)
+        for f in STAT_FIELDS:
+            assert getattr(a.stats, f) == getattr(b.stats, f), (t, f)
+    assert same_bits(m1.cpu().numpy(), m2.cpu().numpy())
+    # the oracle, from iteration 3 on
+    _, bo, _, _ = oracle_quantize(data, cfg.max_bin)
+    OP = orc.Params(loss=cfg.loss, max_depth=args["max_depth"], eta=args["eta"], lambda_=cfg.lambda_,
+                    gamma=cfg.gamma, min_child_weight=cfg.min_child_weight, f=args["f"],
+                    mvs_lambda=cfg.mvs_lambda, seed=cfg.seed, sampler=sampler, goss_a=goss_a)
+    om = np.full(len(y), cfg.base_margin, np.float32)
+    for t in range(n_trees):
+        ot = orc.train_tree(bo, y, om, OP, iteration=3 + t)
+        dd = node_diff(many[t].nodes, ot.nodes)
+        assert dd is None, f"tree {t} node {dd[0]}: gpu {dd[1]} oracle {dd[2]}"
+    assert same_bits(m1.cpu().numpy(), om)
+
+
+@pytest.mark.parametrize("depth,n_trees", [(18, 3), (6, 70)])
+def test_train_trees_reuses_result_slots(gbt, ctx, depth, n_trees):
+    """More trees than result slots: trees of depth 18 (25 MB of nodes each)
+    get two slots, so the first is read before the third is queued; trees
+    of depth 6 get 64, read 32 at a time before their slots are reused."""
+    cfg = datagen.CONFIGS[3]
+    d = datagen.make(3, 3000)
+    mx = gbt.gbt_quantize(ctx, d["X"], max_bin=cfg.max_bin)
+    label = torch.from_numpy(d["y"]).cuda()
+    P = gbt.make_train_params(loss=cfg.loss, max_depth=depth, eta=cfg.eta, lambda_=cfg.lambda_, gamma=0.0,
+                              min_child_weight=0.0, f=0.5, mvs_lambda=cfg.mvs_lambda, seed=cfg.seed)
+    m1 = torch.zeros(3000, dtype=torch.float32, device="cuda")
+    many = gbt.gbt_train_trees(ctx, mx, label, m1, P, n_trees)
+    m2 = torch.zeros(3000, dtype=torch.float32, device="cuda")
+    for t in range(n_trees):
+        Q = gbt.TrainParams.from_buffer_copy(P)
+        Q.iteration = t
+        b = gbt.gbt_train_tree(ctx, mx, label, m2, Q)
+        assert node_diff(many[t].nodes, b.nodes) is None, t
+        assert many[t].stats.hist_updates == b.stats.hist_updates
+    assert same_bits(m1.cpu().numpy(), m2.cpu().numpy())
+    # deeper than the data allows: the last levels split no node
+    assert (many[0].nodes["flags"] != 0).sum() < 2 * 3000
+
+
+def test_train_trees_then_train_tree(gbt, ctx):
+    """A tree trained after a gbt_train_trees call guesses its key exponent
+    from the call's last tree, read on the host: the same as five single
+    calls."""
+    cfg = datagen.CONFIGS[3]
+    d = datagen.make(3, 30_000)
+    mx = gbt.gbt_quantize(ctx, d["X"], max_bin=cfg.max_bin)
+    label = torch.from_numpy(d["y"]).cuda()
+    P = gbt.make_train_params(loss=cfg.loss, max_depth=cfg.max_depth, eta=cfg.eta, lambda_=cfg.lambda_,
+                              gamma=cfg.gamma, min_child_weight=cfg.min_child_weight, f=cfg.f,
+                              mvs_lambda=cfg.mvs_lambda, seed=cfg.seed)
+    m1 = torch.full((30_000,), cfg.base_margin, dtype=torch.float32, device="cuda")
+    trees = gbt.gbt_train_trees(ctx, mx, label, m1, P, 3)
+    for t in (3, 4):
+        Q = gbt.TrainParams.from_buffer_copy(P)
+        Q.iteration = t
+        trees.append(gbt.gbt_train_tree(ctx, mx, label, m1, Q))
+    m2 = torch.full((30_000,), cfg.base_margin, dtype=torch.float32, device="cuda")
+    for t in range(5):
+        Q = gbt.TrainParams.from_buffer_copy(P)
+        Q.iteration = t
+        b = gbt.gbt_train_tree(ctx, mx, label, m2, Q)
+        assert node_diff(trees[t].nodes, b.nodes) is None, t
+    assert same_bits(m1.cpu().numpy(), m2.cpu().numpy())
+    with pytest.raises(ValueError):
+        gbt.gbt_train_trees(ctx, mx, label, m1, P, -1)
+
+
 def test_out_of_core_equals_in_core(gbt, ctx):
     # no sampling: streamed pinned-host pages give the in-core trees (Sec. 4.2)
     cfg = datagen.TrainConfig("t", 0, 64, 5, 3, eta=0.3)
