@@ -253,10 +253,9 @@ __global__ void __launch_bounds__(256) k_mvs_keys(SampleSrc src, int64_t n, doub
 // differ nothing else is done and done_host receives 2.  The flag is a
 // relaxed store: the host reads nothing else this kernel writes (the
 // kernels it queues after reading the flag see the rest in stream order).
-__global__ void k_mvs_thresh_init(SampleState *__restrict__ st, int64_t K, int32_t *__restrict__ done_host,
-                                  int32_t count_mode, int32_t check_log2n)
+__device__ inline void thresh_first(SampleState *__restrict__ st, int64_t K, int32_t *__restrict__ done_host,
+                                    int32_t count_mode, int32_t check_log2n)
 {
-    if (threadIdx.x != 0) return;
     if (check_log2n >= 0) {
         int E;
         frexp(sqrt(__longlong_as_double(fold_max(st->rmax))), &E);
@@ -287,6 +286,38 @@ __global__ void k_mvs_thresh_init(SampleState *__restrict__ st, int64_t K, int32
     st->levels = levels;
     st->done = 0;
     st->T = 0;
+}
+
+__global__ void k_mvs_thresh_init(SampleState *__restrict__ st, int64_t K, int32_t *__restrict__ done_host,
+                                  int32_t count_mode, int32_t check_log2n)
+{
+    if (threadIdx.x == 0) thresh_first(st, K, done_host, count_mode, check_log2n);
+}
+
+// The T that thresh_first (count_mode 0) leaves in a state whose T was 0:
+// the closed form's when the exponent checks and the form holds, else 0.
+// Called by a whole wave: lane l folds entry l of the spread sums.
+__device__ inline unsigned long long thresh_first_T_wave(const SampleState *__restrict__ st, int64_t K,
+                                                         int32_t check_log2n)
+{
+    static_assert(kSpread <= 64, "one spread entry per lane");
+    const int lane = threadIdx.x & 63;
+    unsigned long long rm = 0, am = 0, as = 0;
+    if (lane < kSpread) {
+        rm = st->rmax[lane][0];
+        am = st->amax[lane][0];
+        as = st->asum[lane][0];
+    }
+    rm = wave_max(rm);  // r^2 >= 0: the double bits order as integers
+    am = wave_max(am);
+    as = wave_total(as);
+    if (check_log2n >= 0) {
+        int E;
+        frexp(sqrt(__longlong_as_double(rm)), &E);
+        if (62 - E - check_log2n != st->e_key) return 0;
+    }
+    const unsigned long long Tc = (as + (unsigned long long)K - 1) / (unsigned long long)K;
+    return Tc > am + 1 ? Tc : 0;
 }
 
 template <int kSrc>
@@ -443,16 +474,33 @@ __global__ void __launch_bounds__(256) k_mvs_radix_decide(SampleState *__restric
 // rows (16 per thread, a block stride apart) and writes its kept count.
 template <int kSrc>
 __global__ void __launch_bounds__(256) k_mvs_select(SampleSrc src, const int64_t *__restrict__ keys,
-                                                    int64_t n, double lambda,
-                                                    const SampleState *__restrict__ st,
+                                                    int64_t n, double lambda, SampleState *__restrict__ st,
                                                     uint64_t seed, uint64_t iteration,
                                                     int64_t row_offset, uint8_t *__restrict__ keep,
-                                                    int32_t *__restrict__ tile_cnt, SampleRule rule)
+                                                    int32_t *__restrict__ tile_cnt, SampleRule rule,
+                                                    ThreshFuse fuse)
 {
     __shared__ int32_t red4[4];
+    __shared__ unsigned long long s_T;
     const bool sgb = rule.mode == GBT_SAMPLE_SGB, goss = rule.mode == GBT_SAMPLE_GOSS;
-    // SGB reads no key: every row's key stands at 0 below T = 1
-    const unsigned long long T = sgb ? 1ull : (unsigned long long)st->T;
+    // SGB reads no key: every row's key stands at 0 below T = 1.  With the
+    // threshold's first step fused, every block derives T from the key sums
+    // and block 0 writes the state and the host flag (the other blocks read
+    // none of the fields it writes).
+    unsigned long long T;
+    if (fuse.on) {
+        if (threadIdx.x < 64) {
+            const unsigned long long t = thresh_first_T_wave(st, fuse.K, fuse.check_log2n);
+            if (threadIdx.x == 0) {
+                s_T = t;
+                if (blockIdx.x == 0) thresh_first(st, fuse.K, fuse.done_host, 0, fuse.check_log2n);
+            }
+        }
+        __syncthreads();
+        T = s_T;
+    } else {
+        T = sgb ? 1ull : (unsigned long long)st->T;
+    }
     const int32_t e = st->e_key;
     const int64_t tbase = (int64_t)blockIdx.x * kCompactTile;
     // global row r draws word r mod 4 of the Philox block r div 4; when the
@@ -811,17 +859,7 @@ __global__ void __launch_bounds__(256) k_lambda_pass(int32_t loss, const float *
     }
 }
 
-__global__ void k_state_init(SampleState *st)
-{
-    static_assert(sizeof(SampleState) % 8 == 0, "SampleState is zeroed in 64-bit words");
-    __shared__ int32_t e_prev;
-    if (threadIdx.x == 0) e_prev = st->e_key;
-    __syncthreads();
-    unsigned long long *w = (unsigned long long *)st;
-    for (int i = threadIdx.x; i < (int)(sizeof(SampleState) / 8); i += blockDim.x) w[i] = 0ull;
-    __syncthreads();
-    if (threadIdx.x == 0) st->e_key_prev = e_prev;
-}
+__global__ void k_state_init(SampleState *st) { state_reset_block(st); }
 
 __global__ void k_zero_u64(unsigned long long *p, int64_t n)
 {
@@ -911,8 +949,9 @@ gbt_status threshold_rest(gbt_ctx *c, const SampleSrc &src, int kind, const int6
 
 gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
                          double lambda, int64_t K, SampleState *st, bool skip_closed, bool rmax_done,
-                         bool count_mode, bool keys_spec, bool defer)
+                         bool count_mode, bool keys_spec, bool defer, ThreshFuse *fuse)
 {
+    GBT_CHECK(!fuse || (defer && !count_mode), "a threshold fused into the selection is deferred MVS");
     GBT_CHECK(!keys_spec || (skip_closed && rmax_done && !keys && !count_mode),
               "speculated key sums need the host's closed-form test");
     GBT_CHECK(!defer || skip_closed, "a deferred threshold needs the host's closed-form test");
@@ -943,6 +982,10 @@ gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64
         done_dev = (int32_t *)hio_d;
         *done_poll = -1;
     }
+    if (fuse) {
+        *fuse = ThreshFuse{K, done_dev, keys_spec && n > 0 ? l2 : -1, 1};
+        return GBT_OK;
+    }
     k_mvs_thresh_init<<<1, 64, 0, c->stream>>>(st, K, done_dev, count_mode ? 1 : 0, keys_spec && n > 0 ? l2 : -1);
     GBT_LAUNCHED();
     if (defer) return GBT_OK;
@@ -962,17 +1005,19 @@ gbt_status mvs_threshold_resume(gbt_ctx *c, const SampleSrc &src, int kind, cons
 }
 
 gbt_status mvs_select(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
-                      double lambda, const SampleState *st, uint64_t seed, uint64_t iteration,
-                      int64_t row_offset, uint8_t *keep, int32_t *tile_cnt, const SampleRule &rule)
+                      double lambda, SampleState *st, uint64_t seed, uint64_t iteration,
+                      int64_t row_offset, uint8_t *keep, int32_t *tile_cnt, const SampleRule &rule,
+                      const ThreshFuse &fuse)
 {
+    GBT_CHECK(!fuse.on || rule.mode == GBT_SAMPLE_MVS, "a fused threshold needs the MVS rule");
     if (n == 0) return GBT_OK;
     const unsigned grid = (unsigned)((n + kCompactTile - 1) / kCompactTile);
     if (kind == kSrcGpair)
         k_mvs_select<kSrcGpair><<<grid, 256, 0, c->stream>>>(src, keys, n, lambda, st, seed, iteration,
-                                                             row_offset, keep, tile_cnt, rule);
+                                                             row_offset, keep, tile_cnt, rule, fuse);
     else
         k_mvs_select<kSrcMargin><<<grid, 256, 0, c->stream>>>(src, keys, n, lambda, st, seed, iteration,
-                                                              row_offset, keep, tile_cnt, rule);
+                                                              row_offset, keep, tile_cnt, rule, fuse);
     GBT_LAUNCHED();
     return GBT_OK;
 }

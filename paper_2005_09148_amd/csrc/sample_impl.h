@@ -88,6 +88,20 @@ __host__ __device__ inline unsigned long long fold_sum(const Spread &a)
 // Zeroes the state except e_key_prev, which takes the e_key the state held
 // (the last tree's key exponent, the next tree's guess).
 gbt_status state_init(gbt_ctx *c, SampleState *st);
+// state_init's work by the threads of one block (all of them call it; no
+// LDS, so that a kernel's dynamic LDS keeps its alignment).  The last word
+// holds e_key_prev and the pad: thread 0 writes it from e_key first (the
+// store waits for the load), then the block clears every other word.
+__device__ inline void state_reset_block(SampleState *st)
+{
+    static_assert(sizeof(SampleState) % 8 == 0, "SampleState is zeroed in 64-bit words");
+    static_assert(offsetof(SampleState, e_key_prev) == sizeof(SampleState) - 8, "e_key_prev, pad0 end the state");
+    constexpr int kWords = (int)(sizeof(SampleState) / 8);
+    unsigned long long *w = (unsigned long long *)st;
+    if (threadIdx.x == 0) w[kWords - 1] = (unsigned long long)(uint32_t)st->e_key;
+    __syncthreads();
+    for (int i = threadIdx.x; i < kWords - 1; i += blockDim.x) w[i] = 0ull;
+}
 // keys may be NULL (recomputed on every pass).  Leaves T* in st (device).
 // skip_closed: wait on the host for the closed-form test and launch the
 // radix descent only when it fails (the context's pinned host buffer is
@@ -101,10 +115,20 @@ gbt_status state_init(gbt_ctx *c, SampleState *st);
 // caller may queue work that reads T (it is 0, keeping every row, unless the
 // closed form held) and then calls mvs_threshold_resume, after a
 // synchronization of its own.
+// The threshold's first step (the exponent check and the closed-form test)
+// made by the selection's blocks instead of a kernel of its own.
+struct ThreshFuse {
+    int64_t K = 0;
+    int32_t *done_host = nullptr;  // the host's flag (device address)
+    int32_t check_log2n = -1;
+    int32_t on = 0;
+};
+// fuse (deferred MVS only): the first step is left to mvs_select, with these
+// arguments.
 gbt_status mvs_threshold(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
                          double lambda, int64_t K, SampleState *st, bool skip_closed,
                          bool rmax_done = false, bool count_mode = false, bool keys_spec = false,
-                         bool defer = false);
+                         bool defer = false, ThreshFuse *fuse = nullptr);
 // The rest of a deferred MVS threshold: *redo is false when the closed form
 // held (T was final for the queued work), else the threshold is completed
 // (the keys pass if the key exponent was guessed wrong, the radix descent)
@@ -114,8 +138,9 @@ gbt_status mvs_threshold_resume(gbt_ctx *c, const SampleSrc &src, int kind, cons
 // Keep flags of rows [0, n) and, when tile_cnt is given, the kept count of
 // each tile of kCompactTile rows.
 gbt_status mvs_select(gbt_ctx *c, const SampleSrc &src, int kind, const int64_t *keys, int64_t n,
-                      double lambda, const SampleState *st, uint64_t seed, uint64_t iteration,
-                      int64_t row_offset, uint8_t *keep, int32_t *tile_cnt, const SampleRule &rule);
+                      double lambda, SampleState *st, uint64_t seed, uint64_t iteration,
+                      int64_t row_offset, uint8_t *keep, int32_t *tile_cnt, const SampleRule &rule,
+                      const ThreshFuse &fuse = ThreshFuse{});
 gbt_status gw_all(gbt_ctx *c, const float *gpair, int64_t n, double *gw);
 // The exact fixed-point sums of all n rows' pairs (recomputed from margins
 // and labels, rounded to float) into st->root_g/root_h with st->e_g/e_h,

@@ -270,10 +270,12 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
         // almost always does); otherwise the threshold is completed and the
         // selection queued again
         const bool mvs = sp.f < 1.0 && sp.sampler == GBT_SAMPLE_MVS;
+        // the threshold's first step is made by the selection's blocks
+        ThreshFuse fuse;
         if (mvs) {
             o->K = std::max<int64_t>(1, (int64_t)std::nearbyint(sp.f * (double)n));
             GBT_TRY(mvs_threshold(c, src, kind, nullptr, n, lam, o->K, st, true, st_ready != nullptr, false,
-                                  keys_spec && st_ready != nullptr, true));
+                                  keys_spec && st_ready != nullptr, true, n > 0 ? &fuse : nullptr));
         }
         // the sample size sizes the buffers below: one round trip (its word
         // sits apart from the threshold's flag in the pinned buffer)
@@ -283,7 +285,9 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
         auto select = [&](bool wait) -> gbt_status {
             // with f = 1 the state keeps T = 0: every row is kept with weight 1
             *r_host = -1;
-            GBT_TRY(mvs_select(c, src, kind, nullptr, n, lam, st, sp.seed, sp.iteration, 0, keep, tile_off, rule));
+            GBT_TRY(mvs_select(c, src, kind, nullptr, n, lam, st, sp.seed, sp.iteration, 0, keep, tile_off, rule,
+                               fuse));
+            fuse = ThreshFuse{};  // a selection queued again reads the completed threshold
             GBT_TRY(keep_tile_offsets(c, n, tile_off, (int32_t *)hio_d + 4));
             if (wait) GBT_HIP(hipStreamSynchronize(c->stream));
             return GBT_OK;
@@ -455,6 +459,7 @@ struct FinalizeArgs {
     const unsigned long long *upd;
     const unsigned long long *stat;
     TreeResult *out;
+    SampleState *reset;  // when not NULL: st, reset for the next tree once read
 };
 
 __device__ inline void finalize_entry(const FinalizeArgs &a, int32_t i)
@@ -497,10 +502,18 @@ __device__ inline void finalize_entry(const FinalizeArgs &a, int32_t i)
     a.out->nodes[i] = o;  // absent nodes stay all zero
 }
 
-__global__ void k_finalize(FinalizeArgs a)
+// The block of entry 0 (the only reader of the sampling state) resets the
+// state afterwards when asked.
+__device__ inline void finalize_block(const FinalizeArgs &a, uint32_t b)
 {
-    finalize_entry(a, (int32_t)(blockIdx.x * blockDim.x + threadIdx.x));
+    finalize_entry(a, (int32_t)(b * blockDim.x + threadIdx.x));
+    if (a.reset && b == 0) {
+        __syncthreads();  // entry 0 has read the state
+        state_reset_block(a.reset);
+    }
 }
+
+__global__ void k_finalize(FinalizeArgs a) { finalize_block(a, blockIdx.x); }
 
 // Margin update from the final node of each training slot (no sampling:
 // the slots hold every row once).
@@ -548,7 +561,7 @@ __global__ void __launch_bounds__(kWalkThreads)
                   const DevNode *__restrict__ nodes, const float *__restrict__ leaf,
                   float *__restrict__ margin)
 {
-    extern __shared__ uint32_t walk_lds[];
+    extern __shared__ __align__(16) uint32_t walk_lds[];
     const uint32_t *row = stage_row<kStage>(words, rows, geo.row_words, walk_lds);
     int64_t i = (int64_t)blockIdx.x * kWalkThreads + threadIdx.x;
     if (i >= rows) return;
@@ -573,7 +586,7 @@ __global__ void __launch_bounds__(kWalkTileRows)
                       const uint2 *__restrict__ compact, const float *__restrict__ leaf, int32_t nn,
                       float *__restrict__ margin)
 {
-    extern __shared__ uint32_t walk_lds[];
+    extern __shared__ __align__(16) uint32_t walk_lds[];
     uint2 *tn = (uint2 *)walk_lds;
     float *tl = (float *)(tn + nn);
     uint32_t *rb = (uint32_t *)(tl + nn);
@@ -627,10 +640,10 @@ __global__ void __launch_bounds__(kWalkTileRows)
     // the last fin_blocks blocks write the tree's host result instead
     const uint32_t walk_blocks = gridDim.x - (uint32_t)fin_blocks;
     if (blockIdx.x >= walk_blocks) {
-        finalize_entry(fa, (int32_t)((blockIdx.x - walk_blocks) * blockDim.x + threadIdx.x));
+        finalize_block(fa, blockIdx.x - walk_blocks);
         return;
     }
-    extern __shared__ uint32_t walk_lds[];
+    extern __shared__ __align__(16) uint32_t walk_lds[];
     uint2 *tn = (uint2 *)walk_lds;
     float *tl = (float *)(tn + nn);
     uint32_t *rb = (uint32_t *)(tl + nn);
@@ -743,7 +756,7 @@ __global__ void __launch_bounds__(kWalkThreads)
                      const gbt_node *__restrict__ trees, const int64_t *__restrict__ offs,
                      int32_t n_trees, float base, float *__restrict__ out)
 {
-    extern __shared__ uint32_t walk_lds[];
+    extern __shared__ __align__(16) uint32_t walk_lds[];
     const uint32_t *row = stage_row<kStage>(words, rows, geo.row_words, walk_lds);
     int64_t i = (int64_t)blockIdx.x * kWalkThreads + threadIdx.x;
     if (i >= rows) return;
@@ -827,7 +840,7 @@ __global__ void __launch_bounds__(kWalkThreads)
                       const gbt_node *__restrict__ t, int64_t nn, float *__restrict__ margin,
                       const uint32_t *__restrict__ done, int64_t row0)
 {
-    extern __shared__ uint32_t walk_lds[];
+    extern __shared__ __align__(16) uint32_t walk_lds[];
     const uint32_t *row = stage_row<kStage>(words, rows, geo.row_words, walk_lds);
     int64_t i = (int64_t)blockIdx.x * kWalkThreads + threadIdx.x;
     if (i >= rows) return;
@@ -895,9 +908,13 @@ struct TreePending {
 // the pinned result res_h (res_d on the device), then `done` when not NULL.
 // spec_prev: the MVS key exponent is guessed from the sampling state's last
 // tree on the device (that tree is queued, and the host has not read it).
+// reset_state: the tree's last kernel resets the sampling state for a next
+// tree, which is then queued with state_ready (it skips state_init; both
+// only for sampled trees on device pages).
 static gbt_status train_tree_enqueue(gbt_ctx *c, const gbt_matrix *mx, const float *label, float *margin,
                                      const gbt_train_params *p, bool want_stats, void *res_h, void *res_d,
-                                     hipEvent_t done, bool spec_prev, TreePending *pt)
+                                     hipEvent_t done, bool spec_prev, bool state_ready, bool reset_state,
+                                     TreePending *pt)
 {
     auto t_start = std::chrono::steady_clock::now();
     const int64_t n = mx->n_rows;
@@ -927,7 +944,7 @@ static gbt_status train_tree_enqueue(gbt_ctx *c, const gbt_matrix *mx, const flo
         if (p->f < 1.0) {
             // the gradient pass also folds the maximum of r for the sampling keys
             GBT_TRY(scratch_t(c, kScrState, 1, &st_ready));
-            GBT_TRY(state_init(c, st_ready));
+            if (!state_ready) GBT_TRY(state_init(c, st_ready));
             if (mvs && spec_prev) e_spec_at = &st_ready->e_key_prev;
             GBT_TRY(gradients_rmax(c, p->loss, margin, label, n, gpair, sample_lambda(sp), st_ready, e_spec,
                                    e_spec_at));
@@ -1158,7 +1175,7 @@ static gbt_status train_tree_enqueue(gbt_ctx *c, const gbt_matrix *mx, const flo
     // read after the one synchronization of the call; with the dense walk,
     // by two more blocks of its first launch
     const FinalizeArgs fa{nodes, NN, 0, leaf, mx->cut_ptr_d, mx->cut_values_d, so.st, upd, stat,
-                          (TreeResult *)res_d};
+                          (TreeResult *)res_d, reset_state ? so.st : nullptr};
     bool finalized = false;
     // the rows' final slots give their leaves when every row trained; on
     // dense pages the walk of the page in row order is cheaper than adding
@@ -1287,7 +1304,8 @@ static gbt_status train_tree_impl(gbt_ctx *c, const gbt_matrix *mx, const float 
     void *rh, *rd;
     GBT_TRY(tree_io(c, tree_result_bytes((1 << (p->max_depth + 1)) - 1), &rh, &rd));
     TreePending pt;
-    GBT_TRY(train_tree_enqueue(c, mx, label, margin, p, stats != nullptr, rh, rd, nullptr, false, &pt));
+    GBT_TRY(train_tree_enqueue(c, mx, label, margin, p, stats != nullptr, rh, rd, nullptr, false, false, false,
+                               &pt));
     GBT_HIP(hipStreamSynchronize(c->stream));
     return train_tree_finish(c, pt, tree, stats);
 }
@@ -1714,7 +1732,8 @@ static gbt_status train_tree_naive_impl(gbt_ctx *c, const gbt_matrix *mx, const 
     void *hio, *hio_d;
     GBT_TRY(host_io(c, sizeof(TreeResult) + (size_t)NN * sizeof(gbt_node), &hio, &hio_d));
     k_finalize<<<blocks(NN), 256, 0, c->stream>>>(
-        FinalizeArgs{nodes, NN, 0, leaf, mx->cut_ptr_d, mx->cut_values_d, st, upd, stat, (TreeResult *)hio_d});
+        FinalizeArgs{nodes, NN, 0, leaf, mx->cut_ptr_d, mx->cut_values_d, st, upd, stat, (TreeResult *)hio_d,
+                     nullptr});
     GBT_LAUNCHED();
     GBT_HIP(hipStreamSynchronize(c->stream));
     const TreeResult *res = (const TreeResult *)hio;
@@ -1824,6 +1843,9 @@ gbt_status gbt_train_trees(gbt_ctx *c, const gbt_matrix *data, const float *labe
     void *rh, *rd;
     GBT_TRY(tree_io(c, (size_t)S * rb, &rh, &rd));
     std::vector<TreePending> pend((size_t)S);
+    // sampled trees on device pages: each tree's last kernel resets the
+    // sampling state for the next
+    const bool carry = p->f < 1.0 && !any_host_pages(data);
     int32_t n_read = 0;
     auto read_to = [&](int32_t end) -> gbt_status {
         for (; n_read < end; ++n_read)
@@ -1841,7 +1863,8 @@ gbt_status gbt_train_trees(gbt_ctx *c, const gbt_matrix *data, const float *labe
         if ((t + 1) % H == 0 && (int64_t)n_trees > (int64_t)(g + 2) * H) GBT_TRY(tree_event(c, g & 1, &ev));
         q.iteration = p->iteration + (uint64_t)t;
         GBT_TRY(train_tree_enqueue(c, data, label_d, margin_d, &q, stats != nullptr, (char *)rh + (size_t)(t % S) * rb,
-                                   (char *)rd + (size_t)(t % S) * rb, ev, t > 0, &pend[t % S]));
+                                   (char *)rd + (size_t)(t % S) * rb, ev, t > 0, carry && t > 0,
+                                   carry && t + 1 < n_trees, &pend[t % S]));
     }
     GBT_HIP(hipStreamSynchronize(c->stream));
     GBT_TRY(read_to(n_trees));
