@@ -452,7 +452,10 @@ __device__ Cand eval_feature_regs(const long long *g, const long long *h, int32_
 // k_reduce_eval with the histograms in registers: a wave takes 4 / kBL
 // features of one node (features of at most 64 kBL bins), lane l bins
 // l, l + 64, ...; the parent's and the partials' loads of all of them are
-// in flight together.  No LDS and no block barrier.
+// in flight together.  No LDS and no block barrier.  blockIdx.z = 0 sums the
+// built node's partials, writes its histogram and evaluates it; z = 1 does
+// the same for its sibling (parent minus the sums), so the two evaluations
+// run side by side.
 template <int kBL>
 __global__ void __launch_bounds__(256)
     k_reduce_eval_regs(const longlong2 *__restrict__ partials, const HistReduce *__restrict__ red,
@@ -468,6 +471,8 @@ __global__ void __launch_bounds__(256)
     if (f0 >= m) return;  // the whole wave
     const HistReduce rd = red[blockIdx.y];
     const bool sib = rd.sub_target >= 0;
+    const int which = (int)blockIdx.z;
+    if (which == 1 && !sib) return;
     int32_t off[kV];  // bin offset of each value, -1 past its feature's bins
 #pragma unroll
     for (int j = 0; j < kFW; ++j) {
@@ -483,7 +488,8 @@ __global__ void __launch_bounds__(256)
     longlong2 pv[kV];
 #pragma unroll
     for (int i = 0; i < kV; ++i)
-        pv[i] = (sib && off[i] >= 0) ? parent[(int64_t)rd.sub_parent * total_bins + off[i]] : make_longlong2(0, 0);
+        pv[i] = (which == 1 && off[i] >= 0) ? parent[(int64_t)rd.sub_parent * total_bins + off[i]]
+                                            : make_longlong2(0, 0);
     long long g[kV], h[kV];
 #pragma unroll
     for (int i = 0; i < kV; ++i) g[i] = h[i] = 0;
@@ -512,28 +518,25 @@ __global__ void __launch_bounds__(256)
             h[i] += v.y;
         }
     }
-    // the sibling in place of the parent
+    // z = 1: the sibling in place of the built node
+    if (which == 1) {
 #pragma unroll
-    for (int i = 0; i < kV; ++i) {
-        pv[i].x -= g[i];
-        pv[i].y -= h[i];
-        if (hist && off[i] >= 0) {
-            hist[(int64_t)rd.slot * total_bins + off[i]] = make_longlong2(g[i], h[i]);
-            if (sib) hist[(int64_t)rd.sub_target * total_bins + off[i]] = pv[i];
+        for (int i = 0; i < kV; ++i) {
+            g[i] = pv[i].x - g[i];
+            h[i] = pv[i].y - h[i];
         }
     }
-    long long sgv[kV], shv[kV];
+    const int32_t slot = which == 0 ? rd.slot : rd.sub_target;
+    if (hist) {
 #pragma unroll
-    for (int i = 0; i < kV; ++i) {
-        sgv[i] = pv[i].x;
-        shv[i] = pv[i].y;
+        for (int i = 0; i < kV; ++i)
+            if (off[i] >= 0) hist[(int64_t)slot * total_bins + off[i]] = make_longlong2(g[i], h[i]);
     }
     if (ep.e_dev) {
         ep.e_g = ep.e_dev[0];
         ep.e_h = ep.e_dev[1];
     }
-    for (int which = 0; which < (sib ? 2 : 1); ++which) {
-        const int32_t slot = which == 0 ? rd.slot : rd.sub_target;
+    {
         const EvalNode nd = ev[slot];
 #pragma unroll
         for (int j = 0; j < kFW; ++j) {
@@ -548,8 +551,7 @@ __global__ void __launch_bounds__(256)
             o.default_left = 0;
             o.lg = o.lh = 0;
             if (B >= 2) {
-                const Cand cb = which == 0 ? eval_feature_regs<kBL>(g + j * kBL, h + j * kBL, B, nd.sum_g, nd.sum_h, ep)
-                                           : eval_feature_regs<kBL>(sgv + j * kBL, shv + j * kBL, B, nd.sum_g, nd.sum_h, ep);
+                const Cand cb = eval_feature_regs<kBL>(g + j * kBL, h + j * kBL, B, nd.sum_g, nd.sum_h, ep);
                 if (cb.valid) {
                     o.valid = 1;
                     o.gain = cb.gain;
@@ -630,7 +632,8 @@ gbt_status reduce_eval_impl(gbt_ctx *c, const gbt_matrix *mx, const int64_t *par
     const int kbl = max_feature_bins <= 64 ? 1 : max_feature_bins <= 128 ? 2 : max_feature_bins <= 256 ? 4 : 0;
     if (kbl == 1 || (kbl > 0 && (int64_t)max_red * mx->m >= 2 * kCUs)) {
         const int fpb = 4 * (4 / kbl);  // features per block
-        dim3 gr((unsigned)((mx->m + fpb - 1) / fpb), (unsigned)max_red);
+        // z: the built node and, below the root, its sibling
+        dim3 gr((unsigned)((mx->m + fpb - 1) / fpb), (unsigned)max_red, parent ? 2u : 1u);
 #define GBT_REG_EVAL(BL)                                                                                       \
     k_reduce_eval_regs<BL><<<gr, 256, 0, c->stream>>>((const longlong2 *)partials, red, n_red_d,           \
                                                       (const longlong2 *)parent, (longlong2 *)hist,         \
