@@ -115,44 +115,63 @@ struct PlanArgs {
     LeafArgs lv;
 };
 
-// nleft of each of the level's nodes: the left flags before its last slot's
-// tile and within it, less those before its first slot.
+// Exclusive offsets of the partition's tile left counts (at most
+// kPlanScanTiles of them; more come with their offsets in a.tile_off) into
+// s_off: per thread a run of consecutive tiles.
 template <int T>
-__device__ void plan_left_counts(DevNode *__restrict__ nodes, const PlanArgs &a, int32_t n_cur)
+__device__ void plan_tile_offsets(const PlanArgs &a, int32_t *s_off)
 {
-    __shared__ int32_t s_off[kPlanScanTiles + 1];
     __shared__ int32_t s_w[T / 64];
-    if (!a.tile_off) {
-        // exclusive offsets of at most kPlanScanTiles counts: per thread a
-        // run of consecutive tiles
-        constexpr int kPer = (kPlanScanTiles + T - 1) / T;
-        const int64_t t0 = (int64_t)threadIdx.x * kPer;
-        int32_t v[kPer], run = 0;
+    constexpr int kPer = (kPlanScanTiles + T - 1) / T;
+    const int64_t t0 = (int64_t)threadIdx.x * kPer;
+    int32_t v[kPer], run = 0;
 #pragma unroll
-        for (int j = 0; j < kPer; ++j) {
-            v[j] = t0 + j < a.tiles ? a.tile_cnt[t0 + j] : 0;
-            run += v[j];
-        }
-        int32_t tot;
-        int32_t o = plan_block_scan<T>(run, s_w, &tot);
-#pragma unroll
-        for (int j = 0; j < kPer; ++j) {
-            if (t0 + j <= kPlanScanTiles) s_off[t0 + j] = o;
-            o += v[j];
-        }
-        __syncthreads();
+    for (int j = 0; j < kPer; ++j) {
+        v[j] = t0 + j < a.tiles ? a.tile_cnt[t0 + j] : 0;
+        run += v[j];
     }
-    for (int32_t t = threadIdx.x; t < n_cur; t += T) {
-        DevNode &d = nodes[a.cur[t].heap];
+    int32_t tot;
+    int32_t o = plan_block_scan<T>(run, s_w, &tot);
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+        if (t0 + j <= kPlanScanTiles) s_off[t0 + j] = o;
+        o += v[j];
+    }
+    __syncthreads();
+}
+
+// plan_node of level node t with its left count: from the partition's tile
+// prefixes when a.tile_cnt is set (the left flags before its last slot's
+// tile and within it, less those before its first slot; recorded in the
+// node for later readers), else the node's own.  One read of the node.
+__device__ inline PlanNode plan_node_counted(const PlanArgs &a, DevNode *__restrict__ nodes, int32_t t,
+                                             const int32_t *s_off)
+{
+    const EvalNode e = a.cur[t];
+    DevNode &d = nodes[e.heap];
+    PlanNode x;
+    x.p = e.heap;
+    x.slot = e.slot;
+    x.split = d.split;
+    x.begin = d.begin;
+    int64_t nl = d.nleft;
+    if (a.tile_cnt) {
+        nl = 0;
         if (d.end > d.begin) {
             const long long ob = a.tile_off ? a.tile_off[d.tile_b] : s_off[d.tile_b];
             const long long oe = a.tile_off ? a.tile_off[d.tile_e] : s_off[d.tile_e];
-            d.nleft = (oe + d.left_e) - (ob + d.left_b);
-        } else {
-            d.nleft = 0;
+            nl = (oe + d.left_e) - (ob + d.left_b);
         }
+        d.nleft = nl;
     }
-    __syncthreads();  // the counts are read by other threads of the block
+    x.nl = nl;
+    x.nr = d.end - d.begin - nl;
+    x.lg = d.left_g;
+    x.lh = d.left_h;
+    x.rg = d.right_g;
+    x.rh = d.right_h;
+    x.pad0 = 0;
+    return x;
 }
 
 template <int T>
@@ -164,16 +183,19 @@ __device__ void plan_level_block(DevNode *__restrict__ nodes, const PlanArgs &a)
     // one pass's nodes: first work item (and the pass's end), row segment
     __shared__ int32_t s_kp[T + 1];
     __shared__ long long s_sb[T], s_se[T];
+    __shared__ int32_t s_off[kPlanScanTiles + 1];
     const int32_t n_cur = *a.n_cur_d;
-    if (a.tile_cnt) plan_left_counts<T>(nodes, a, n_cur);
+    if (a.tile_cnt && !a.tile_off) plan_tile_offsets<T>(a, s_off);
     // the children's segments and sums; the rows and nodes to build, for the
     // chunk size (a level of at most T nodes keeps each thread's node in
-    // registers for the second pass)
+    // registers for the second pass; a thread handles the same nodes in
+    // both, so a larger level's second pass reads the left counts its
+    // thread recorded)
     PlanNode mine{};
     unsigned long long rb = 0;
     int32_t nbuild = 0;
     for (int32_t t = threadIdx.x; t < n_cur; t += T) {
-        const PlanNode x = plan_node(a.cur, nodes, t);
+        const PlanNode x = plan_node_counted(a, nodes, t, s_off);
         if (t < T) mine = x;
         if (!x.split) continue;
         DevNode &L = nodes[2 * x.p + 1];
@@ -233,9 +255,13 @@ __device__ void plan_level_block(DevNode *__restrict__ nodes, const PlanArgs &a)
             nchunks = (int32_t)(ns > 0 ? (ns + chunk - 1) / chunk : 1);
             rows_built += (unsigned long long)ns;
         }
-        int32_t tot_b, tot_p;
-        const int32_t kb = plan_block_scan<T>(split ? 1 : 0, lds16, &tot_b) + c_build;
-        const int32_t kp = plan_block_scan<T>(nchunks, lds16, &tot_p) + c_part;
+        // one scan of both counts: the split flags in the low 16 bits (at
+        // most T of them), the chunks above (at most items + T per pass)
+        int32_t tot;
+        const int32_t pre = plan_block_scan<T>((split ? 1 : 0) | (nchunks << 16), lds16, &tot);
+        const int32_t tot_b = tot & 0xffff, tot_p = tot >> 16;
+        const int32_t kb = (pre & 0xffff) + c_build;
+        const int32_t kp = (pre >> 16) + c_part;
         if (split) {
             const int32_t sl = 2 * kb, sr = sl + 1;  // the children of split parents, in heap order
             a.next[sl] = {x.lg, x.lh, sl, 2 * x.p + 1};

@@ -993,6 +993,9 @@ static gbt_status train_tree_enqueue(gbt_ctx *c, const gbt_matrix *mx, const flo
     // a level builds more than items / 2 nodes: then up to items plus the
     // node count)
     const int32_t items = (int32_t)std::max<int64_t>(1, twg / G);
+    // the level plan scans its pass's chunk counts (at most items plus a
+    // block of nodes) in 16 bits
+    GBT_CHECK(items < (1 << 14), "%d work items per group", items);
     const int32_t max_work = items + max_level_nodes + 1;
     auto al = [](size_t b) { return (b + 255) / 256 * 256; };
     const size_t o_ev1 = al((size_t)max_level_nodes * sizeof(EvalNode));
