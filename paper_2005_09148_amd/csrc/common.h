@@ -108,6 +108,9 @@ struct gbt_ctx {
     int32_t key_e_last = 0;
     int64_t key_n_last = -1;
     double key_lambda_last = 0.0;
+    // whether the last MVS threshold needed the radix descent (the next
+    // tree then compacts only after the threshold is complete)
+    bool mvs_descent_last = false;
 };
 
 namespace gbt {

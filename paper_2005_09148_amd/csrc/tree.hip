@@ -299,7 +299,7 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
         // the trees before), so the host's round trip overlaps it.  It is
         // redone when the threshold had to be completed or the sample is
         // larger than the buffers.
-        const bool early = all_device_single(mx) && !bufs.owned && n > 0;
+        const bool early = all_device_single(mx) && !bufs.owned && n > 0 && !(mvs && c->mvs_descent_last);
         int64_t cap = 0;
         uint32_t *spage = nullptr;
         if (early) {
@@ -319,6 +319,8 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
         bool redo = false;
         if (mvs) {
             GBT_TRY(mvs_threshold_resume(c, src, kind, nullptr, n, lam, o->K, st, &redo));
+            // the threshold's flag: 1 closed form, 0 the descent ran
+            c->mvs_descent_last = redo && *(volatile int32_t *)hio == 0;
             if (redo) GBT_TRY(select(true));
         }
         o->R = *r_host;
