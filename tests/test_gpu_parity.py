@@ -548,9 +548,9 @@ STAT_FIELDS = ("n_sampled", "threshold", "exp_key", "hist_updates", "hist_launch
                "hist_kernel", "hist_cols")
 
 
-@pytest.mark.parametrize("case", ["mvs", "mvs_eta1", "sgb", "goss", "all_rows", "csr", "pinned", "depth0",
+@pytest.mark.parametrize("case", ["mvs", "mvs_eta1", "sgb", "goss", "all_rows", "csr", "pinned", "disk", "depth0",
                                   "timed"])
-def test_train_trees_equals_tree_by_tree(gbt, ctx, case):
+def test_train_trees_equals_tree_by_tree(gbt, ctx, case, tmp_path):
     """gbt_train_trees queues each tree before the host reads the one before
     (the sampling keys' exponent guessed on the device): the same trees,
     margins and counters as one gbt_train_tree call per tree, and as the
@@ -575,12 +575,15 @@ def test_train_trees_equals_tree_by_tree(gbt, ctx, case):
         kw["f"] = 1.0
     if case == "pinned":
         home, page_rows = gbt.HOME_PINNED_HOST, 16_384
+    page_dir = None
+    if case == "disk":
+        home, page_rows, page_dir = gbt.HOME_DISK, 16_384, str(tmp_path)
     if case == "depth0":
         kw["max_depth"] = 0
     args = dict(loss=cfg.loss, max_depth=cfg.max_depth, eta=cfg.eta, lambda_=cfg.lambda_, gamma=cfg.gamma,
                 min_child_weight=cfg.min_child_weight, f=cfg.f, mvs_lambda=cfg.mvs_lambda, seed=cfg.seed)
     args.update(kw)
-    mx = gbt.gbt_quantize(ctx, data, max_bin=cfg.max_bin, page_rows=page_rows, page_home=home)
+    mx = gbt.gbt_quantize(ctx, data, max_bin=cfg.max_bin, page_rows=page_rows, page_home=home, page_dir=page_dir)
     label = torch.from_numpy(y).cuda()
     P = gbt.make_train_params(sampler=sampler, goss_a=goss_a, **args)
     P.iteration = 3
