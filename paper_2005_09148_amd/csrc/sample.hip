@@ -602,13 +602,23 @@ __global__ void __launch_bounds__(256)
                     const uint8_t *__restrict__ keep, const int32_t *__restrict__ tile_off,
                     int64_t tile0, int64_t row_lo, int64_t row_hi, const uint4 *__restrict__ words,
                     int32_t row_q4, uint4 *__restrict__ out_page, int32_t *__restrict__ sel,
-                    double2 *__restrict__ gw, SampleRule rule, int64_t cap)
+                    double2 *__restrict__ gw, SampleRule rule, int64_t cap, int64_t self_tiles,
+                    int32_t *__restrict__ total_host)
 {
     __shared__ int32_t lds4[4];
     __shared__ unsigned long long red4[4];
     __shared__ uint16_t klist[kCompactTile];
     const int64_t tile = tile0 + blockIdx.x;
     const int64_t tbase = tile * kCompactTile;
+    // self_tiles > 0: tile_off holds the selection's per-tile counts (no
+    // scan ran); the block sums those before its tile, and block 0 all of
+    // them for the host (the sample size)
+    unsigned long long pre = 0, all = 0;
+    if (self_tiles > 0) {
+        for (int64_t k = threadIdx.x; k < tile; k += blockDim.x) pre += (unsigned long long)tile_off[k];
+        if (blockIdx.x == 0)
+            for (int64_t k = threadIdx.x; k < self_tiles; k += blockDim.x) all += (unsigned long long)tile_off[k];
+    }
     const int64_t base = tbase + (int64_t)threadIdx.x * 16;
     uint32_t bits = 0;
     if (base + 16 <= n) {
@@ -635,7 +645,17 @@ __global__ void __launch_bounds__(256)
         klist[run++] = (uint16_t)(threadIdx.x * 16 + k);
     }
     __syncthreads();
-    const int64_t pos0 = tile_off[tile];
+    int64_t pos0;
+    if (self_tiles > 0) {
+        pos0 = (int64_t)block_sum_u64(pre, red4);
+        if (blockIdx.x == 0) {
+            all = block_sum_u64(all, red4);
+            if (threadIdx.x == 0)
+                __hip_atomic_store(total_host, (int32_t)all, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        }
+    } else {
+        pos0 = tile_off[tile];
+    }
     if (pos0 + nk > cap) return;  // the whole block: the buffers are too small
     // the rows, 16 bytes per thread and step
     for (int32_t e = threadIdx.x; e < nk * row_q4; e += 256) {
@@ -1053,19 +1073,23 @@ gbt_status keep_tile_offsets(gbt_ctx *c, int64_t n, int32_t *tile_off, int32_t *
 gbt_status mvs_compact_tiles(gbt_ctx *c, const SampleSrc &src, int kind, int64_t n, double lambda,
                              SampleState *st, const uint8_t *keep, const int32_t *tile_off,
                              int64_t row_lo, int64_t row_hi, const uint32_t *words, int32_t row_words,
-                             uint32_t *out_page, int32_t *sel, double *gw, const SampleRule &rule, int64_t cap)
+                             uint32_t *out_page, int32_t *sel, double *gw, const SampleRule &rule, int64_t cap,
+                             int32_t *total_host)
 {
     if (row_hi <= row_lo) return GBT_OK;
     const int64_t t0 = row_lo / kCompactTile, t1 = (row_hi - 1) / kCompactTile + 1;
     const unsigned grid = (unsigned)(t1 - t0);
+    // total_host: the offsets come from the counts (all of rows [0, n))
+    GBT_CHECK(!total_host || (row_lo == 0 && row_hi == n), "a compaction that sums its own tile offsets covers every row");
+    const int64_t self_tiles = total_host ? (int64_t)grid : 0;
     if (kind == kSrcGpair)
         k_compact_tiles<kSrcGpair><<<grid, 256, 0, c->stream>>>(
             src, n, lambda, st, keep, tile_off, t0, row_lo, row_hi, (const uint4 *)words, row_words / 4,
-            (uint4 *)out_page, sel, (double2 *)gw, rule, cap);
+            (uint4 *)out_page, sel, (double2 *)gw, rule, cap, self_tiles, total_host);
     else
         k_compact_tiles<kSrcMargin><<<grid, 256, 0, c->stream>>>(
             src, n, lambda, st, keep, tile_off, t0, row_lo, row_hi, (const uint4 *)words, row_words / 4,
-            (uint4 *)out_page, sel, (double2 *)gw, rule, cap);
+            (uint4 *)out_page, sel, (double2 *)gw, rule, cap, self_tiles, total_host);
     GBT_LAUNCHED();
     return GBT_OK;
 }

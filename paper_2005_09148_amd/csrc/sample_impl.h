@@ -168,11 +168,14 @@ gbt_status keep_tile_offsets(gbt_ctx *c, int64_t n, int32_t *tile_off, int32_t *
 // tile whose kept rows would reach past it writes nothing (a compaction
 // queued before the host knows the sample size, into buffers that are then
 // large enough unless the sample is; the host redoes it when it was not).
+// total_host (pinned, device address; rows [0, n) only): tile_off holds the
+// selection's per-tile counts, not their offsets; each block sums the
+// counts before its tile, and the total goes to *total_host.
 gbt_status mvs_compact_tiles(gbt_ctx *c, const SampleSrc &src, int kind, int64_t n, double lambda,
                              SampleState *st, const uint8_t *keep, const int32_t *tile_off,
                              int64_t row_lo, int64_t row_hi, const uint32_t *words, int32_t row_words,
                              uint32_t *out_page, int32_t *sel, double *gw, const SampleRule &rule,
-                             int64_t cap = INT64_MAX);
+                             int64_t cap = INT64_MAX, int32_t *total_host = nullptr);
 // Spins until a kernel has written a value >= 0 at *flag (pinned host
 // memory); after 2 s, synchronizes the stream instead.
 gbt_status wait_flag(gbt_ctx *c, volatile int32_t *flag);

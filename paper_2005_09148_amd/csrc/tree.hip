@@ -282,13 +282,15 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
         void *hio, *hio_d;
         GBT_TRY(host_io(c, 64, &hio, &hio_d));
         volatile int32_t *r_host = (volatile int32_t *)hio + 4;
-        auto select = [&](bool wait) -> gbt_status {
+        // scan: the tile offsets by a scan of their own (else the early
+        // compaction sums the counts itself)
+        auto select = [&](bool wait, bool scan) -> gbt_status {
             // with f = 1 the state keeps T = 0: every row is kept with weight 1
             *r_host = -1;
             GBT_TRY(mvs_select(c, src, kind, nullptr, n, lam, st, sp.seed, sp.iteration, 0, keep, tile_off, rule,
                                fuse));
             fuse = ThreshFuse{};  // a selection queued again reads the completed threshold
-            GBT_TRY(keep_tile_offsets(c, n, tile_off, (int32_t *)hio_d + 4));
+            if (scan) GBT_TRY(keep_tile_offsets(c, n, tile_off, (int32_t *)hio_d + 4));
             if (wait) GBT_HIP(hipStreamSynchronize(c->stream));
             return GBT_OK;
         };
@@ -309,25 +311,27 @@ gbt_status sample_run(gbt_ctx *c, const gbt_matrix *mx, const float *gpair, cons
             GBT_TRY(bufs.get(kScrGw, (size_t)guess * 16, (void **)&o->gw));
             cap = (int64_t)std::min({scratch_bytes(c, kScrSampled) / rb, scratch_bytes(c, kScrSel) / 4,
                                      scratch_bytes(c, kScrGw) / 16});
-            GBT_TRY(select(false));
+            GBT_TRY(select(false, false));
             GBT_TRY(mvs_compact_tiles(c, src, kind, n, lam, st, keep, tile_off, 0, n, mx->pages[0].words,
-                                      mx->row_words, spage, o->sel, o->gw, rule, cap));
+                                      mx->row_words, spage, o->sel, o->gw, rule, cap, (int32_t *)hio_d + 4));
             GBT_TRY(wait_flag(c, r_host));
         } else {
-            GBT_TRY(select(true));
+            GBT_TRY(select(true, true));
         }
         bool redo = false;
         if (mvs) {
             GBT_TRY(mvs_threshold_resume(c, src, kind, nullptr, n, lam, o->K, st, &redo));
             // the threshold's flag: 1 closed form, 0 the descent ran
             c->mvs_descent_last = redo && *(volatile int32_t *)hio == 0;
-            if (redo) GBT_TRY(select(true));
+            if (redo) GBT_TRY(select(true, true));
         }
         o->R = *r_host;
         GBT_CHECK(o->R >= 0 && o->R <= n, "sample size %lld of %lld rows", (long long)o->R, (long long)n);
         const bool compacted = early && !redo && o->R <= cap;
-        // the early compaction's maxima of the reweighted pairs are void
+        // the early compaction's maxima of the reweighted pairs are void;
+        // its tile counts (when no selection was queued again) become offsets
         if (early && !compacted) GBT_TRY(fx_max_reset(c, st));
+        if (early && !compacted && !redo) GBT_TRY(keep_tile_offsets(c, n, tile_off, nullptr));
         GBT_TRY(bufs.get(kScrSampled, (size_t)std::max<int64_t>(o->R, 1) * rb, (void **)&spage));
         GBT_TRY(bufs.get(kScrSel, (size_t)std::max<int64_t>(o->R, 1) * 4, (void **)&o->sel));
         GBT_TRY(bufs.get(kScrGw, (size_t)std::max<int64_t>(o->R, 1) * 16, (void **)&o->gw));
