@@ -100,6 +100,10 @@ def test_binding_layouts_and_constants_match_the_header():
         assert c[name] == ctypes.sizeof(cls), name
     assert c["gbt_node"] == gbt.NODE_DTYPE.itemsize and c["gbt_split"] == gbt.SPLIT_DTYPE.itemsize
     assert c["gbt_seg"] == gbt.SEG_DTYPE.itemsize
+    # the numpy form of gbt_tree that gbt_train_trees passes as an array
+    assert c["gbt_tree"] == gbt._TREE_DTYPE.itemsize
+    for f, _ in gbt.Tree._fields_:
+        assert gbt._TREE_DTYPE.fields[f][1] == getattr(gbt.Tree, f).offset, f
     py = {"GBT_E_INVALID": gbt.GBT_E_INVALID, "GBT_E_OOM": gbt.GBT_E_OOM, "GBT_E_BUDGET": gbt.GBT_E_BUDGET,
           "GBT_E_DEVICE": gbt.GBT_E_DEVICE, "GBT_E_UNSUPPORTED": gbt.GBT_E_UNSUPPORTED, "GBT_E_IO": gbt.GBT_E_IO,
           "GBT_HOME_DEVICE": gbt.HOME_DEVICE, "GBT_HOME_PINNED_HOST": gbt.HOME_PINNED_HOST,
